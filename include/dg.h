@@ -1,0 +1,264 @@
+/*
+ * dg.h — C ABI of libdg: the group-sampling -> batched-packing -> batch-assembly
+ * path of offline-sampling GNN training (DiskGNN, arXiv 2405.05231), on one
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The method (paper §3 "Offline Sampling", §4, §5.2): sample many mini-batches
+ * before any model computation, collect the node features each of them will
+ * read, and lay those features out in advance.  Three calls cover the path:
+ *
+ *   dg_sample_group    node-wise fan-out neighbour sampling (§2, Fig. 1) for a
+ *                      group of B mini-batches at once.
+ *   dg_pack_group      batched feature packing (§5.2, Fig. 6b): deduplicate the
+ *                      group's node IDs, drop the nodes held in the feature cache
+ *                      (§3 "cache configuration", §4 four-level store), and copy
+ *                      each remaining feature row once from the feature table into
+ *                      the packed chunk of every mini-batch that needs it; also
+ *                      build the per-batch address tables (§6 "interpreted address
+ *                      tables").
+ *   dg_assemble_batch  feature assembling (§4, Fig. 3): merge cache rows and packed
+ *                      rows into one mini-batch's input tensor, in sampled order.
+ *
+ * Everything lives in device memory (HBM): the disk tiers of the paper are not
+ * part of this library.
+ *
+ * ------------------------------------------------------------------------------
+ * Conventions shared by every entry point
+ * ------------------------------------------------------------------------------
+ *  - Pointers are DEVICE pointers unless the comment says [host].
+ *  - Node IDs are int32 in [0, N) (N < 2^31); CSR edge offsets are int64.
+ *  - The caller owns every buffer.  The library never allocates device memory:
+ *    scratch space is the caller's workspace `ws`, sized by the matching
+ *    *_workspace_bytes() query and aligned to 256 bytes.  Workspace contents on
+ *    entry are irrelevant; on return they are unspecified.
+ *  - Work is enqueued on the caller's stream `stream` (NULL = the default
+ *    stream).  dg_sample_group and dg_pack_group return only when their work has
+ *    completed (their output sizes are data-dependent and are reported in
+ *    `*sizes`); dg_assemble_batch is asynchronous.
+ *  - Return value: a dg_status.  On a non-OK return dg_last_error() gives a
+ *    message (per calling thread).  No exception or abort crosses the ABI.
+ *    On DG_ECAPACITY the call stops before writing past any output buffer;
+ *    outputs are then unspecified and `*sizes` holds the sizes needed.
+ *  - Calls that share a workspace must not overlap in time; calls with distinct
+ *    workspaces may run concurrently on different streams.
+ *
+ * ------------------------------------------------------------------------------
+ * Sampling rule (§2 "Graph sampling for GNN training", Fig. 1)
+ * ------------------------------------------------------------------------------
+ * For each mini-batch b independently, with seeds s_0..s_{S-1} (distinct) and
+ * fan-outs f_1..f_K (fanouts[k-1] is hop k):
+ *   hop 0 frontier = the seeds, in the given order;
+ *   at hop k every node of the hop-(k-1) frontier, in frontier order, draws
+ *   min(deg, f_k) distinct neighbour positions of its CSR row (all of them when
+ *   f_k < 0 or deg <= f_k), ordered by ascending position; each draw is a
+ *   sampled edge (frontier node -> neighbour);
+ *   the hop-k frontier = the sampled neighbours not yet in the mini-batch,
+ *   deduplicated and sorted by ascending node ID.  Only these newly reached
+ *   nodes sample at hop k+1 (in Fig. 1 the seed does not sample again at the
+ *   second step).
+ * Node list of b:   nodes_b = seeds || hop-1 frontier || ... || hop-K frontier.
+ * Edge list of b:   hop by hop; within a hop by frontier position, then by
+ *                   ascending CSR position.  Endpoints are local indices into
+ *                   nodes_b.
+ *
+ * Subset drawn when deg d > f (the paper leaves the sampler's randomness to
+ * the external framework; this library fixes one, uniform without replacement):
+ *   mix64(z): z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9;
+ *             z = (z ^ (z >> 27)) * 0x94D049BB133111EB;  return z ^ (z >> 31)
+ *             (the SplitMix64 output function; all arithmetic mod 2^64)
+ *   gamma   = 0x9E3779B97F4A7C15
+ *   key     = mix64( mix64(rng_seed + gamma * (g + 1)) ^ ((uint64)k << 32 | v) )
+ *             with g = batch_base + b (the global mini-batch number, as uint64),
+ *             k = hop number 1..K, v = the frontier node's ID
+ *   h_i     = mix64(key + gamma * (i + 1))      (i-th SplitMix64 output from key)
+ *   below(h, m) = floor(h * m / 2^64)           (high word of the 128-bit product)
+ *   Floyd's subset (Bentley & Floyd, CACM 30(9), 1987): for i = 0..f-1, with
+ *   j = d - f + i, t = below(h_i, j + 1); add t to the subset unless it is
+ *   already there, in which case add j.  Positions are then sorted ascending.
+ *
+ * ------------------------------------------------------------------------------
+ * Packing layout (§5.2 "Batched packing", Fig. 6b; §4 "Packed feature chunk")
+ * ------------------------------------------------------------------------------
+ *   U      = ascending set of all node IDs of the group (its union).
+ *   P_b    = ascending IDs of nodes_b whose cache_slot is -1 (not cached): the
+ *            packed chunk of b holds exactly the features of P_b, in this order
+ *            (batched packing appends features partition by partition in
+ *            consecutive-ID order, so each chunk comes out ascending).
+ *   packed_ptr[b] = sum_{c<b} |P_c|;  packed row packed_ptr[b]+r = X[P_b[r]].
+ *   loc_b[j] = -(cache_slot[u]+1) if u = nodes_b[j] is cached,
+ *              else the rank r of u in P_b.
+ *   Assembly:  Y_b[j] = cache[-loc_b[j]-1] if loc_b[j] < 0, else packed_b[loc_b[j]],
+ *              which equals X[nodes_b[j]] whenever cache row s holds X of the
+ *              node whose cache_slot is s.
+ * Feature rows are opaque bytes (fp32, fp16, anything): they are copied, never
+ * converted.  Rows move as 16-byte vectors when row_bytes and the row base
+ * pointers are multiples of 16, and by narrower words otherwise.
+ */
+#ifndef DG_H
+#define DG_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DG_MAX_BATCHES 64 /* a group holds at most 64 mini-batches (one bit each) */
+
+typedef enum dg_status {
+  DG_OK = 0,
+  DG_EINVAL = -1,     /* bad argument, or bad input data found by a device check */
+  DG_ECAPACITY = -2,  /* an output buffer is too small; see *sizes */
+  DG_EHIP = -3,       /* the HIP runtime returned an error */
+  DG_EWORKSPACE = -4  /* workspace missing, misaligned or smaller than required */
+} dg_status;
+
+/* CSR graph: the neighbours of node v are indices[offsets[v] .. offsets[v+1]).
+ * offsets: [N+1] int64, offsets[0] = 0, non-decreasing, offsets[N] = num_edges.
+ * indices: [num_edges] int32 node IDs.  Both device pointers. */
+typedef struct dg_csr {
+  int64_t num_nodes;
+  int64_t num_edges;
+  const int64_t *offsets;
+  const int32_t *indices;
+} dg_csr;
+
+/* [host] Sizes reported by dg_sample_group / dg_pack_group.  Fields a call does
+ * not compute are set to -1.  exact = 0 means a capacity stop ended the call
+ * early and the sampling figures are lower bounds (use dg_sample_bounds()). */
+typedef struct dg_sizes {
+  int64_t max_batch_nodes; /* max_b n_b: the node_cap needed                */
+  int64_t max_batch_edges; /* max_b e_b: the edge_cap needed                */
+  int64_t total_nodes;     /* sum_b n_b (= number of (node, batch) pairs)    */
+  int64_t total_edges;     /* sum_b e_b                                     */
+  int64_t packed_rows;     /* sum_b |P_b|: the packed_cap needed            */
+  int64_t unique_nodes;    /* |U|: the unique_cap needed                    */
+  int64_t unique_packed;   /* |U minus cached|: feature rows read by packing */
+  int32_t exact;
+} dg_sizes;
+
+/* [host] Optional per-phase device times in milliseconds, measured with HIP
+ * events on the call's stream when a non-NULL pointer is passed.  Phases a call
+ * does not run are set to 0. */
+typedef struct dg_timing {
+  float sample_ms;  /* dg_sample_group: frontier degree pass + draw + mark      */
+  float dedup_ms;   /* dg_sample_group: per-hop new-node compaction            */
+  float relabel_ms; /* dg_sample_group: global -> local neighbour IDs          */
+  float mark_ms;    /* dg_pack_group:   group membership bitmask               */
+  float order_ms;   /* dg_pack_group:   unique set, P_b order, packed_ptr      */
+  float loc_ms;     /* dg_pack_group:   address tables                         */
+  float gather_ms;  /* dg_pack_group:   fan-out row gather (the copy itself)   */
+  float total_ms;   /* whole call, first to last enqueued kernel               */
+} dg_timing;
+
+/* Library version string (static storage). */
+const char *dg_version(void);
+
+/* Message for the last non-OK status returned on the calling thread
+ * (thread-local storage; valid until the thread's next dg_* call). */
+const char *dg_last_error(void);
+
+/* [host only, no device work] Upper bounds on n_b and e_b for any graph with
+ * `num_nodes` nodes and `num_edges` edges: n_b <= min(N, S*(1 + f1 + f1*f2 + ...)),
+ * e_b <= min(E, S*f1 + S*f1*f2 + ...), where a negative fan-out counts as
+ * "all neighbours" (bounded by N for nodes and E for edges).  Capacities this
+ * large never trigger DG_ECAPACITY.  Returns DG_EINVAL on a null pointer,
+ * S < 1, K < 0 or num_nodes < 1. */
+int dg_sample_bounds(int64_t num_nodes, int64_t num_edges, int32_t S,
+                     const int32_t *fanouts /*[host] K*/, int32_t K,
+                     int64_t *node_cap /*[host] out*/, int64_t *edge_cap /*[host] out*/);
+
+/* Workspace bytes dg_sample_group needs for N nodes, B batches and the given
+ * per-batch capacities. */
+size_t dg_sample_workspace_bytes(int64_t num_nodes, int32_t B, int64_t node_cap,
+                                 int64_t edge_cap);
+
+/* Group sampling (§2 Fig. 1; §3: many mini-batches are sampled before any
+ * computation).  Rule and randomness: see the top of this file.
+ *   g          CSR graph [host struct, device arrays].
+ *   seeds      [B*S] int32; batch b's seeds are seeds[b*S .. b*S+S), distinct
+ *              within a batch, each in [0, N).  Batches may share seeds.
+ *   B          1..64 mini-batches;  S >= 1 seeds per batch.
+ *   batch_base global number of batch 0 (the RNG key uses batch_base + b, so a
+ *              group split into several calls gives the same result).
+ *   fanouts    [host] K fan-outs, hop 1 first; f < 0 means "all neighbours",
+ *              f = 0 samples nothing at that hop.  K >= 0.
+ *   rng_seed   sampler seed.
+ * Outputs (row b of each starts at b*cap):
+ *   nodes      [B*node_cap] int32: nodes_b in the order above.
+ *   hop_ptr    [host] [B*(K+2)] int64: hop_ptr[b*(K+2)+h] = start of hop h in
+ *              nodes_b (h = 0 is the seeds), hop_ptr[b*(K+2)+K+1] = n_b.
+ *   edge_src, edge_dst  [B*edge_cap] int32: sampled edge (frontier node ->
+ *              sampled neighbour), both as local indices into nodes_b.
+ *   edge_ptr   [host] [B*(K+1)] int64: edge_ptr[b*(K+1)+k] = start of hop-(k+1)
+ *              edges, edge_ptr[b*(K+1)+K] = e_b.
+ *   sizes      [host] filled on DG_OK and DG_ECAPACITY.
+ *   timing     [host] optional (NULL = not measured).
+ * Errors: DG_EINVAL for null pointers, B outside 1..64, S < 1, K < 0, caps < S,
+ * and for bad data found on the device: a seed outside [0,N), a seed repeated in
+ * a batch, a CSR row with offsets outside [0,E] or decreasing, a neighbour ID
+ * outside [0,N).  Bad data never causes an access outside the given arrays. */
+int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S,
+                    int64_t batch_base, const int32_t *fanouts, int32_t K,
+                    uint64_t rng_seed, int64_t node_cap, int32_t *nodes,
+                    int64_t *hop_ptr, int64_t edge_cap, int32_t *edge_src,
+                    int32_t *edge_dst, int64_t *edge_ptr, void *ws, size_t ws_bytes,
+                    hipStream_t stream, dg_sizes *sizes, dg_timing *timing);
+
+/* Workspace bytes dg_pack_group needs for N nodes, B batches whose node lists
+ * hold `total_nodes` entries in all. */
+size_t dg_pack_workspace_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes);
+
+/* Batched packing (§5.2 Fig. 6b) + address tables (§6).  Layout: see the top of
+ * this file.
+ *   feats       [N*row_bytes] feature table X, row v at feats + v*row_bytes.
+ *   N, row_bytes  row_bytes >= 1.
+ *   cache_slot  [N] int32: row of node v in the cache table, or -1 if not cached.
+ *   B           1..64;  nodes [B*node_stride] int32, batch b's list at
+ *               nodes + b*node_stride, distinct within a batch (any order: the
+ *               lists may come from any sampler, §3 "Generality").
+ *   node_count  [host] [B] int64: n_b (0 <= n_b <= node_stride).
+ * Outputs:
+ *   packed      [packed_cap*row_bytes] bytes: the packed chunks, batch-major.
+ *   packed_ids  [packed_cap] int32: node ID of each packed row (P_0 || P_1 ...).
+ *   packed_ptr  [B+1] int64 (device) and packed_ptr_host [host] [B+1] int64:
+ *               chunk b is rows packed_ptr[b] .. packed_ptr[b+1).
+ *   loc         [B*node_stride] int32: address table, loc_b at loc + b*node_stride.
+ *   group_unique  [unique_cap] int32 or NULL: U ascending.
+ *   sizes, timing as for dg_sample_group.
+ * Errors: DG_EINVAL for null pointers, B outside 1..64, row_bytes < 1, n_b out of
+ * range, and on the device a node ID outside [0,N), a node repeated within a
+ * batch, or cache_slot[v] < -1.  DG_ECAPACITY when packed_cap < sum|P_b| or
+ * (group_unique != NULL and) unique_cap < |U|. */
+int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
+                  const int32_t *cache_slot, int32_t B, const int32_t *nodes,
+                  int64_t node_stride, const int64_t *node_count, int64_t packed_cap,
+                  void *packed, int32_t *packed_ids, int64_t *packed_ptr,
+                  int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique,
+                  int64_t unique_cap, void *ws, size_t ws_bytes, hipStream_t stream,
+                  dg_sizes *sizes, dg_timing *timing);
+
+/* Feature assembling for one mini-batch (§4 Fig. 3, second step; addresses come
+ * from the precomputed table of §6, so no lookup structure is consulted):
+ *   out[j] = cache[-loc_b[j]-1] if loc_b[j] < 0, else packed_b[loc_b[j]],
+ *   for j in [0, n_b); each row is row_bytes bytes.
+ *   cache      [cache_rows*row_bytes] the cache table (may be NULL if cache_rows=0).
+ *   packed_b   [packed_rows_b*row_bytes] = packed + packed_ptr[b]*row_bytes.
+ *   loc_b      [n_b] int32;  out [n_b*row_bytes].
+ *   status     optional device int32: on an entry of loc_b outside
+ *              [-cache_rows, packed_rows_b) the kernel writes a zero row and ORs
+ *              bit 1 into *status (no access outside the given buffers).
+ * Asynchronous on `stream`.  Returns DG_EINVAL for null pointers (other than
+ * cache with cache_rows = 0 and status), n_b < 0, row_bytes < 1, or buffers that
+ * overlap; n_b = 0 is a no-op. */
+int dg_assemble_batch(const void *cache, int64_t cache_rows, const void *packed_b,
+                      int64_t packed_rows_b, const int32_t *loc_b, int64_t n_b,
+                      int64_t row_bytes, void *out, int32_t *status,
+                      hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DG_H */

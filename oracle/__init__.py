@@ -1,0 +1,208 @@
+"""CPU oracle for the offline-sampling path — TEST INFRASTRUCTURE ONLY.
+
+Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product library
+(``paper_2405_05231_amd``) never imports it and shares no code with it.
+
+The arithmetic lives in ``oracle.c`` (plain C, single thread, qsort/bsearch,
+written from the paper: node-wise sampling §2 Fig. 1, batched packing §5.2
+Fig. 6b, address tables §6, feature assembling §4 Fig. 3).  This module only
+compiles it with gcc and marshals numpy arrays in and out.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+I64P = ctypes.POINTER(ctypes.c_int64)
+I32P = ctypes.POINTER(ctypes.c_int32)
+VP = ctypes.c_void_p
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.c into liboracle.so with gcc (no GPU code involved)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp"
+        subprocess.run(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-Wall", "-Werror",
+                        _SRC, "-o", tmp], check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build()
+        L = ctypes.CDLL(_LIB_PATH)
+        L.or_mix64.restype = ctypes.c_uint64
+        L.or_mix64.argtypes = [ctypes.c_uint64]
+        L.or_splitmix_nth.restype = ctypes.c_uint64
+        L.or_splitmix_nth.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
+        L.or_draw_key.restype = ctypes.c_uint64
+        L.or_draw_key.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int32, ctypes.c_int32]
+        L.or_below.restype = ctypes.c_uint64
+        L.or_below.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
+        L.or_floyd.restype = ctypes.c_int
+        L.or_floyd.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64, I64P]
+        L.or_sample_group.restype = ctypes.c_int
+        L.or_sample_group.argtypes = [
+            ctypes.c_int64, ctypes.c_int64, I64P, I32P, I32P, ctypes.c_int32, ctypes.c_int32,
+            ctypes.c_int64, I32P, ctypes.c_int32, ctypes.c_uint64, ctypes.c_int64, I32P, I64P,
+            ctypes.c_int64, I32P, I32P, I64P, I64P]
+        L.or_pack_group.restype = ctypes.c_int
+        L.or_pack_group.argtypes = [
+            ctypes.c_int64, ctypes.c_int64, VP, I32P, ctypes.c_int32, I32P, ctypes.c_int64, I64P,
+            ctypes.c_int64, VP, I32P, I64P, I32P, I32P, ctypes.c_int64, I64P]
+        L.or_assemble_batch.restype = ctypes.c_int
+        L.or_assemble_batch.argtypes = [VP, ctypes.c_int64, VP, ctypes.c_int64, I32P,
+                                        ctypes.c_int64, ctypes.c_int64, VP]
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray, t):
+    return a.ctypes.data_as(t)
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+# ---------------------------------------------------------------- randomness
+def mix64(z: int) -> int:
+    return lib().or_mix64(z & (2**64 - 1))
+
+
+def splitmix_nth(state: int, i: int) -> int:
+    return lib().or_splitmix_nth(state & (2**64 - 1), i)
+
+
+def draw_key(rng_seed: int, g: int, k: int, v: int) -> int:
+    return lib().or_draw_key(rng_seed & (2**64 - 1), g & (2**64 - 1), k, v)
+
+
+def below(h: int, m: int) -> int:
+    return lib().or_below(h & (2**64 - 1), m)
+
+
+def floyd(d: int, f: int, key: int) -> list[int]:
+    out = np.zeros(max(f, 1), dtype=np.int64)
+    rc = lib().or_floyd(d, f, key & (2**64 - 1), _p(out, I64P))
+    if rc:
+        raise OracleError(f"or_floyd rc={rc}")
+    return out[:f].tolist()
+
+
+# ---------------------------------------------------------------- sampling
+def sample_bounds(N: int, E: int, S: int, fanouts) -> tuple[int, int]:
+    """Per-batch upper bounds on node and edge counts (negative fan-out = all)."""
+    n, e, layer = S, 0, S
+    for f in fanouts:
+        if f < 0:
+            return N, E
+        layer = layer * f
+        e += layer
+        n += layer
+        if n >= N and e >= E:
+            break
+    return min(n, N), min(e, E)
+
+
+def sample_group(offsets, indices, seeds, fanouts, rng_seed, batch_base=0):
+    """Group sampling.  seeds: int32 [B, S].  Returns a dict with per-batch
+    numpy arrays: nodes[b], hop_ptr[b], edge_src[b], edge_dst[b], edge_ptr[b]."""
+    off = np.ascontiguousarray(offsets, dtype=np.int64)
+    idx = np.ascontiguousarray(indices, dtype=np.int32)
+    sd = np.ascontiguousarray(seeds, dtype=np.int32)
+    B, S = sd.shape
+    fo = np.ascontiguousarray(fanouts, dtype=np.int32)
+    K = len(fo)
+    N = len(off) - 1
+    E = int(off[-1])
+    ncap, ecap = sample_bounds(N, E, S, [int(x) for x in fo])
+    ncap, ecap = max(ncap, 1), max(ecap, 1)
+    nodes = np.zeros(B * ncap, dtype=np.int32)
+    hop = np.zeros(B * (K + 2), dtype=np.int64)
+    es = np.zeros(B * ecap, dtype=np.int32)
+    ed = np.zeros(B * ecap, dtype=np.int32)
+    ep = np.zeros(B * (K + 1), dtype=np.int64)
+    need = np.zeros(2, dtype=np.int64)
+    rc = lib().or_sample_group(N, E, _p(off, I64P), _p(idx, I32P), _p(sd, I32P), B, S, batch_base,
+                               _p(fo, I32P), K, rng_seed & (2**64 - 1), ncap, _p(nodes, I32P),
+                               _p(hop, I64P), ecap, _p(es, I32P), _p(ed, I32P), _p(ep, I64P),
+                               _p(need, I64P))
+    if rc:
+        raise OracleError(f"or_sample_group rc={rc}")
+    hop = hop.reshape(B, K + 2)
+    ep = ep.reshape(B, K + 1)
+    out = {"nodes": [], "hop_ptr": [], "edge_src": [], "edge_dst": [], "edge_ptr": []}
+    for b in range(B):
+        n, e = int(hop[b, K + 1]), int(ep[b, K])
+        out["nodes"].append(nodes[b * ncap:b * ncap + n].copy())
+        out["hop_ptr"].append(hop[b].copy())
+        out["edge_src"].append(es[b * ecap:b * ecap + e].copy())
+        out["edge_dst"].append(ed[b * ecap:b * ecap + e].copy())
+        out["edge_ptr"].append(ep[b].copy())
+    out["max_nodes"], out["max_edges"] = int(need[0]), int(need[1])
+    return out
+
+
+# ---------------------------------------------------------------- packing
+def pack_group(feats, cache_slot, node_lists, with_unique=True):
+    """Batched packing.  feats: numpy [N, ...] (rows are copied as bytes);
+    cache_slot: int32 [N]; node_lists: list of int32 arrays (one per batch)."""
+    X = np.ascontiguousarray(feats)
+    N = X.shape[0]
+    R = X.nbytes // N
+    cs = np.ascontiguousarray(cache_slot, dtype=np.int32)
+    B = len(node_lists)
+    counts = np.array([len(x) for x in node_lists], dtype=np.int64)
+    stride = max(int(counts.max()) if B else 0, 1)
+    nodes = np.zeros(B * stride, dtype=np.int32)
+    for b, x in enumerate(node_lists):
+        nodes[b * stride:b * stride + len(x)] = x
+    total = int(counts.sum())
+    packed = np.zeros((max(total, 1), R), dtype=np.uint8)
+    pids = np.zeros(max(total, 1), dtype=np.int32)
+    pptr = np.zeros(B + 1, dtype=np.int64)
+    loc = np.zeros(B * stride, dtype=np.int32)
+    uniq = np.zeros(max(total, 1), dtype=np.int32)
+    need = np.zeros(3, dtype=np.int64)
+    rc = lib().or_pack_group(N, R, X.ctypes.data_as(VP), _p(cs, I32P), B, _p(nodes, I32P), stride,
+                             _p(counts, I64P), total, packed.ctypes.data_as(VP), _p(pids, I32P),
+                             _p(pptr, I64P), _p(loc, I32P),
+                             _p(uniq, I32P) if with_unique else None, total, _p(need, I64P))
+    if rc:
+        raise OracleError(f"or_pack_group rc={rc}")
+    rows = int(need[0])
+    return {
+        "packed": packed[:rows], "packed_ids": pids[:rows], "packed_ptr": pptr,
+        "loc": [loc[b * stride:b * stride + int(counts[b])].copy() for b in range(B)],
+        "unique": uniq[:int(need[1])].copy() if with_unique else None,
+        "packed_rows": rows, "unique_nodes": int(need[1]), "unique_packed": int(need[2]),
+    }
+
+
+def assemble_batch(cache, packed_b, loc_b, row_bytes):
+    """Feature assembling for one batch: rows from the cache (loc < 0) or the
+    batch's packed chunk, in the order of loc_b.  Returns uint8 [n_b, row_bytes]."""
+    c = np.ascontiguousarray(cache).view(np.uint8).reshape(-1)
+    p = np.ascontiguousarray(packed_b).view(np.uint8).reshape(-1)
+    lb = np.ascontiguousarray(loc_b, dtype=np.int32)
+    n = len(lb)
+    out = np.zeros((n, row_bytes), dtype=np.uint8)
+    rc = lib().or_assemble_batch(c.ctypes.data_as(VP), len(c) // row_bytes, p.ctypes.data_as(VP),
+                                 len(p) // row_bytes, _p(lb, I32P), n, row_bytes,
+                                 out.ctypes.data_as(VP))
+    if rc:
+        raise OracleError(f"or_assemble_batch rc={rc}")
+    return out
