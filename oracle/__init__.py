@@ -157,12 +157,19 @@ def sample_group(offsets, indices, seeds, fanouts, rng_seed, batch_base=0):
 
 
 # ---------------------------------------------------------------- packing
-def pack_group(feats, cache_slot, node_lists, with_unique=True):
+def pack_group(feats, cache_slot, node_lists, with_unique=True, rows=True, row_bytes=None):
     """Batched packing.  feats: numpy [N, ...] (rows are copied as bytes);
-    cache_slot: int32 [N]; node_lists: list of int32 arrays (one per batch)."""
-    X = np.ascontiguousarray(feats)
-    N = X.shape[0]
-    R = X.nbytes // N
+    cache_slot: int32 [N]; node_lists: list of int32 arrays (one per batch).
+    rows=False computes the tables only (feats may then be None, with
+    row_bytes given)."""
+    if rows:
+        X = np.ascontiguousarray(feats)
+        N = X.shape[0]
+        R = X.nbytes // N
+    else:
+        X = None
+        N = len(cache_slot)
+        R = row_bytes or 1
     cs = np.ascontiguousarray(cache_slot, dtype=np.int32)
     B = len(node_lists)
     counts = np.array([len(x) for x in node_lists], dtype=np.int64)
@@ -171,24 +178,25 @@ def pack_group(feats, cache_slot, node_lists, with_unique=True):
     for b, x in enumerate(node_lists):
         nodes[b * stride:b * stride + len(x)] = x
     total = int(counts.sum())
-    packed = np.zeros((max(total, 1), R), dtype=np.uint8)
+    packed = np.zeros((max(total, 1), R), dtype=np.uint8) if rows else None
     pids = np.zeros(max(total, 1), dtype=np.int32)
     pptr = np.zeros(B + 1, dtype=np.int64)
     loc = np.zeros(B * stride, dtype=np.int32)
     uniq = np.zeros(max(total, 1), dtype=np.int32)
     need = np.zeros(3, dtype=np.int64)
-    rc = lib().or_pack_group(N, R, X.ctypes.data_as(VP), _p(cs, I32P), B, _p(nodes, I32P), stride,
-                             _p(counts, I64P), total, packed.ctypes.data_as(VP), _p(pids, I32P),
+    rc = lib().or_pack_group(N, R, X.ctypes.data_as(VP) if rows else None, _p(cs, I32P), B,
+                             _p(nodes, I32P), stride, _p(counts, I64P), total,
+                             packed.ctypes.data_as(VP) if rows else None, _p(pids, I32P),
                              _p(pptr, I64P), _p(loc, I32P),
                              _p(uniq, I32P) if with_unique else None, total, _p(need, I64P))
     if rc:
         raise OracleError(f"or_pack_group rc={rc}")
-    rows = int(need[0])
+    nrows = int(need[0])
     return {
-        "packed": packed[:rows], "packed_ids": pids[:rows], "packed_ptr": pptr,
+        "packed": packed[:nrows] if rows else None, "packed_ids": pids[:nrows], "packed_ptr": pptr,
         "loc": [loc[b * stride:b * stride + int(counts[b])].copy() for b in range(B)],
         "unique": uniq[:int(need[1])].copy() if with_unique else None,
-        "packed_rows": rows, "unique_nodes": int(need[1]), "unique_packed": int(need[2]),
+        "packed_rows": nrows, "unique_nodes": int(need[1]), "unique_packed": int(need[2]),
     }
 
 

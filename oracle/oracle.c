@@ -298,8 +298,9 @@ int or_pack_group(int64_t N, int64_t row_bytes, const void *feats, const int32_t
           cache_slot[u] >= 0 ? -(cache_slot[u] + 1) : (int32_t)find_i32(pb, cnt, u);
     }
   }
-  /* packed row i holds the feature row of node packed_ids[i] */
-  for (int64_t i = 0; i < rows; ++i)
+  /* packed row i holds the feature row of node packed_ids[i]
+     (packed == NULL: tables only, no row copies) */
+  for (int64_t i = 0; packed && i < rows; ++i)
     memcpy((char *)packed + i * row_bytes, (const char *)feats + (int64_t)packed_ids[i] * row_bytes,
            (size_t)row_bytes);
   return 0;

@@ -1,0 +1,235 @@
+"""MI355X (gfx950) offline-sampling hot path after DiskGNN (arXiv 2405.05231):
+group sampling, batched packing and batch assembly, run by the HIP kernels of
+libdg.so.
+
+This module only marshals torch tensors (device memory + the current HIP
+stream) into the C ABI declared in include/dg.h; every step of the path runs
+in the library's kernels.  Importing it fails if libdg.so is missing.
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+from . import _lib
+from ._lib import (DG_ECAPACITY, DG_MAX_BATCHES, DG_OK, DGError, Csr, Sizes, Timing, check,
+                   load)
+
+__all__ = ["sample_bounds", "sample_group", "pack_group", "assemble_batch", "DGError",
+           "SampleResult", "PackResult", "version"]
+
+_L = load()
+
+
+def version() -> str:
+    return _L.dg_version().decode()
+
+
+def _ptr(t: torch.Tensor | None):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _need(t: torch.Tensor, name: str, dtype=None, device=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name}: expected device {device}, got {t.device}")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name}: must live in GPU memory")
+
+
+def _workspace(nbytes: int, device, ws: torch.Tensor | None):
+    if ws is not None and ws.numel() * ws.element_size() >= nbytes:
+        return ws
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+def sample_bounds(num_nodes: int, num_edges: int, S: int, fanouts) -> tuple[int, int]:
+    fo = (ctypes.c_int32 * max(len(fanouts), 1))(*fanouts)
+    nc, ec = ctypes.c_int64(), ctypes.c_int64()
+    check(_L.dg_sample_bounds(num_nodes, num_edges, S, fo, len(fanouts), ctypes.byref(nc),
+                              ctypes.byref(ec)))
+    return nc.value, ec.value
+
+
+@dataclass
+class SampleResult:
+    nodes: torch.Tensor      # int32 [B, node_cap]
+    hop_ptr: np.ndarray      # int64 [B, K+2]
+    edge_src: torch.Tensor   # int32 [B, edge_cap] local
+    edge_dst: torch.Tensor   # int32 [B, edge_cap] local
+    edge_ptr: np.ndarray     # int64 [B, K+1]
+    sizes: dict
+    timing: dict | None
+
+    @property
+    def node_count(self) -> np.ndarray:
+        return np.ascontiguousarray(self.hop_ptr[:, -1])
+
+    def batch_nodes(self, b: int) -> torch.Tensor:
+        return self.nodes[b, :int(self.hop_ptr[b, -1])]
+
+    def batch_edges(self, b: int):
+        e = int(self.edge_ptr[b, -1])
+        return self.edge_src[b, :e], self.edge_dst[b, :e]
+
+
+def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tensor, fanouts,
+                 rng_seed: int, batch_base: int = 0, node_cap: int | None = None,
+                 edge_cap: int | None = None, out: SampleResult | None = None,
+                 workspace: torch.Tensor | None = None, stream=None, timing: bool = False
+                 ) -> SampleResult:
+    """Group sampling (dg_sample_group).  seeds: int32 [B, S] on the GPU."""
+    dev = offsets.device
+    _need(offsets, "offsets", torch.int64)
+    _need(indices, "indices", torch.int32, dev)
+    _need(seeds, "seeds", torch.int32, dev)
+    if seeds.dim() != 2:
+        raise ValueError("seeds must be [B, S]")
+    B, S = seeds.shape
+    N = offsets.numel() - 1
+    E = indices.numel()
+    fanouts = [int(f) for f in fanouts]
+    K = len(fanouts)
+    if out is not None:
+        node_cap, edge_cap = out.nodes.shape[1], out.edge_src.shape[1]
+    else:
+        bn, be = sample_bounds(N, E, S, fanouts)
+        node_cap = bn if node_cap is None else node_cap
+        edge_cap = be if edge_cap is None else edge_cap
+        out = SampleResult(
+            nodes=torch.empty((B, node_cap), dtype=torch.int32, device=dev),
+            hop_ptr=np.zeros((B, K + 2), dtype=np.int64),
+            edge_src=torch.empty((B, max(edge_cap, 1)), dtype=torch.int32, device=dev),
+            edge_dst=torch.empty((B, max(edge_cap, 1)), dtype=torch.int32, device=dev),
+            edge_ptr=np.zeros((B, K + 1), dtype=np.int64), sizes={}, timing=None)
+    ws_bytes = _L.dg_sample_workspace_bytes(N, B, node_cap, edge_cap)
+    ws = _workspace(ws_bytes, dev, workspace)
+    g = Csr(N, E, offsets.data_ptr(), indices.data_ptr())
+    fo = (ctypes.c_int32 * max(K, 1))(*fanouts)
+    sz, tm = Sizes(), Timing()
+    st = _L.dg_sample_group(
+        ctypes.byref(g), _ptr(seeds), B, S, batch_base, fo, K, rng_seed & (2**64 - 1),
+        node_cap, _ptr(out.nodes), out.hop_ptr.ctypes.data_as(_lib.I64P), edge_cap,
+        _ptr(out.edge_src), _ptr(out.edge_dst), out.edge_ptr.ctypes.data_as(_lib.I64P),
+        _ptr(ws), ws.numel(), _stream(stream), ctypes.byref(sz),
+        ctypes.byref(tm) if timing else None)
+    out.sizes = sz.as_dict()
+    check(st)
+    out.timing = tm.as_dict() if timing else None
+    return out
+
+
+@dataclass
+class PackResult:
+    packed: torch.Tensor          # uint8 [packed_rows, row_bytes] (or the caller's buffer)
+    packed_ids: torch.Tensor      # int32 [packed_rows]
+    packed_ptr: torch.Tensor      # int64 [B+1] on the GPU
+    packed_ptr_host: np.ndarray   # int64 [B+1]
+    loc: torch.Tensor             # int32 [B, node_stride]
+    unique: torch.Tensor | None   # int32 [|U|]
+    sizes: dict
+    timing: dict | None
+    row_bytes: int
+
+    def chunk(self, b: int) -> torch.Tensor:
+        """Packed rows of batch b (a view)."""
+        return self.packed[int(self.packed_ptr_host[b]):int(self.packed_ptr_host[b + 1])]
+
+
+def _row_bytes(feats: torch.Tensor) -> int:
+    return feats[0].numel() * feats.element_size() if feats.shape[0] else 0
+
+
+def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tensor, node_count,
+               with_unique: bool = False, out: PackResult | None = None,
+               workspace: torch.Tensor | None = None, stream=None, timing: bool = False
+               ) -> PackResult:
+    """Batched packing (dg_pack_group).  nodes: int32 [B, node_stride];
+    node_count: the B list lengths (host)."""
+    dev = feats.device
+    _need(feats, "feats", None)
+    _need(cache_slot, "cache_slot", torch.int32, dev)
+    _need(nodes, "nodes", torch.int32, dev)
+    N = feats.shape[0]
+    R = _row_bytes(feats)
+    B, stride = nodes.shape
+    counts = np.ascontiguousarray(np.asarray(node_count, dtype=np.int64).reshape(-1))
+    if counts.shape[0] != B:
+        raise ValueError("node_count must have one entry per batch")
+    total = int(counts.sum())
+    ws_bytes = _L.dg_pack_workspace_bytes(N, B, total)
+    ws = _workspace(ws_bytes, dev, workspace)
+    ptr_host = np.zeros(B + 1, dtype=np.int64)
+    sz, tm = Sizes(), Timing()
+    if out is None:
+        loc = torch.empty((B, stride), dtype=torch.int32, device=dev)
+        ptr = torch.empty(B + 1, dtype=torch.int64, device=dev)
+        # size query: a zero packed capacity returns the exact sizes needed
+        st = _L.dg_pack_group(_ptr(feats), N, R, _ptr(cache_slot), B, _ptr(nodes), stride,
+                              counts.ctypes.data_as(_lib.I64P), 0, None, None, _ptr(ptr),
+                              ptr_host.ctypes.data_as(_lib.I64P), _ptr(loc), None, 0, _ptr(ws),
+                              ws.numel(), _stream(stream), ctypes.byref(sz), None)
+        if st not in (DG_OK, DG_ECAPACITY):
+            check(st)
+        rows, nu = sz.packed_rows, sz.unique_nodes
+        out = PackResult(
+            packed=torch.empty((max(rows, 1), R), dtype=torch.uint8, device=dev),
+            packed_ids=torch.empty(max(rows, 1), dtype=torch.int32, device=dev),
+            packed_ptr=ptr, packed_ptr_host=ptr_host, loc=loc,
+            unique=torch.empty(max(nu, 1), dtype=torch.int32, device=dev) if with_unique else None,
+            sizes={}, timing=None, row_bytes=R)
+    cap = out.packed_ids.numel()
+    if out.packed.numel() < cap * R:
+        raise ValueError("packed buffer smaller than packed_ids")
+    st = _L.dg_pack_group(_ptr(feats), N, R, _ptr(cache_slot), B, _ptr(nodes), stride,
+                          counts.ctypes.data_as(_lib.I64P), cap, _ptr(out.packed),
+                          _ptr(out.packed_ids), _ptr(out.packed_ptr),
+                          out.packed_ptr_host.ctypes.data_as(_lib.I64P), _ptr(out.loc),
+                          _ptr(out.unique), out.unique.numel() if out.unique is not None else 0,
+                          _ptr(ws), ws.numel(), _stream(stream), ctypes.byref(sz),
+                          ctypes.byref(tm) if timing else None)
+    out.sizes = sz.as_dict()
+    check(st)
+    out.timing = tm.as_dict() if timing else None
+    return out
+
+
+def assemble_batch(cache: torch.Tensor | None, packed_b: torch.Tensor, loc_b: torch.Tensor,
+                   row_bytes: int, out: torch.Tensor | None = None,
+                   status: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Feature assembling for one batch (dg_assemble_batch), asynchronous on the
+    stream.  Returns `out` viewed as uint8 [n_b, row_bytes]."""
+    _need(loc_b, "loc_b", torch.int32)
+    dev = loc_b.device
+    n = loc_b.numel()
+    if out is None:
+        out = torch.empty((n, row_bytes), dtype=torch.uint8, device=dev)
+    _need(out, "out", None, dev)
+    cache_rows = 0
+    if cache is not None and cache.numel():
+        _need(cache, "cache", None, dev)
+        cache_rows = cache.numel() * cache.element_size() // row_bytes
+    pr = 0
+    if packed_b is not None and packed_b.numel():
+        _need(packed_b, "packed_b", None, dev)
+        pr = packed_b.numel() * packed_b.element_size() // row_bytes
+    if out.numel() * out.element_size() < n * row_bytes:
+        raise ValueError("out is too small")
+    check(_L.dg_assemble_batch(_ptr(cache) if cache_rows else None, cache_rows,
+                               _ptr(packed_b) if pr else None, pr, _ptr(loc_b), n, row_bytes,
+                               _ptr(out), _ptr(status), _stream(stream)))
+    return out

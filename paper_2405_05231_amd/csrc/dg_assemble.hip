@@ -1,0 +1,165 @@
+// Feature assembling (DiskGNN §4, Fig. 3, second step): each required feature
+// row of a mini-batch comes from the cache table or from the batch's packed
+// chunk, at the address the precomputed table gives (§6), written in sampled
+// order.  Pure HBM row gather; no lookup structure is consulted.
+#include <initializer_list>
+
+#include "dg_rows.h"
+
+namespace dg {
+namespace {
+
+constexpr int THREADS = 256;
+constexpr int UNROLL = 4;
+
+__device__ __forceinline__ const char *row_source(int32_t l, const char *cache, int64_t cache_rows,
+                                                  const char *packed, int64_t packed_rows,
+                                                  int64_t row_bytes, int32_t *status) {
+  if (l < 0) {
+    int64_t r = -(int64_t)l - 1;
+    if (r < cache_rows) return cache + r * row_bytes;
+  } else if ((int64_t)l < packed_rows) {
+    return packed + (int64_t)l * row_bytes;
+  }
+  if (status) atomicOr(status, 1);
+  return nullptr;
+}
+
+template <int LPR, int CPL>
+__global__ __launch_bounds__(THREADS) void k_assemble16(const uint4 *cache, int64_t cache_rows,
+                                                        const uint4 *packed, int64_t packed_rows,
+                                                        const int32_t *loc, int64_t n, int C,
+                                                        uint4 *out, int32_t *status) {
+  constexpr int GPB = THREADS / LPR;  // row groups per block
+  const int sub = threadIdx.x % LPR;
+  const int64_t grp = (int64_t)blockIdx.x * GPB + threadIdx.x / LPR;
+  const int64_t ngrp = (int64_t)gridDim.x * GPB;
+  for (int64_t j0 = grp * UNROLL; j0 < n; j0 += ngrp * UNROLL) {
+    const uint4 *src[UNROLL];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      int64_t j = j0 + u;
+      src[u] = nullptr;
+      if (j < n) {
+        int32_t l = loc[j];
+        src[u] = reinterpret_cast<const uint4 *>(
+            row_source(l, reinterpret_cast<const char *>(cache), cache_rows,
+                       reinterpret_cast<const char *>(packed), packed_rows, (int64_t)C * 16,
+                       sub == 0 ? status : nullptr));
+      }
+    }
+    uint4 v[UNROLL][CPL];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u)
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        int ch = sub + c * LPR;
+        v[u][c] = (src[u] && ch < C) ? src[u][ch] : make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      int64_t j = j0 + u;
+      if (j < n) {
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+          int ch = sub + c * LPR;
+          if (ch < C) out[j * C + ch] = v[u][c];
+        }
+      }
+    }
+  }
+}
+
+// Any row size / alignment: one wave per row, words of sizeof(T).
+template <typename T>
+__global__ __launch_bounds__(THREADS) void k_assemble_any(const T *cache, int64_t cache_rows,
+                                                          const T *packed, int64_t packed_rows,
+                                                          const int32_t *loc, int64_t n,
+                                                          int64_t W, T *out, int32_t *status) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = ((int64_t)blockIdx.x * THREADS + threadIdx.x) >> 6;
+  const int64_t nwave = ((int64_t)gridDim.x * THREADS) >> 6;
+  for (int64_t j = wave; j < n; j += nwave) {
+    const T *src = reinterpret_cast<const T *>(
+        row_source(loc[j], reinterpret_cast<const char *>(cache), cache_rows,
+                   reinterpret_cast<const char *>(packed), packed_rows, W * (int64_t)sizeof(T),
+                   lane == 0 ? status : nullptr));
+    for (int64_t c = lane; c < W; c += 64) out[j * W + c] = src ? src[c] : zero_word<T>();
+  }
+}
+
+template <typename T>
+int launch_any(const void *cache, int64_t cache_rows, const void *packed, int64_t packed_rows,
+               const int32_t *loc, int64_t n, int64_t row_bytes, void *out, int32_t *status,
+               hipStream_t s) {
+  int64_t W = row_bytes / (int64_t)sizeof(T);
+  int64_t blocks = (n + 3) / 4;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(k_assemble_any<T>, dim3((unsigned)blocks), dim3(THREADS), 0, s,
+                     (const T *)cache, cache_rows, (const T *)packed, packed_rows, loc, n, W,
+                     (T *)out, status);
+  DG_HIP(hipGetLastError());
+  return DG_OK;
+}
+
+template <int LPR, int CPL>
+int launch16(const void *cache, int64_t cache_rows, const void *packed, int64_t packed_rows,
+             const int32_t *loc, int64_t n, int C, void *out, int32_t *status, hipStream_t s) {
+  constexpr int GPB = THREADS / LPR;
+  int64_t groups = (n + UNROLL - 1) / UNROLL;
+  int64_t blocks = (groups + GPB - 1) / GPB;
+  if (blocks > (1ll << 20)) blocks = 1ll << 20;
+  hipLaunchKernelGGL((k_assemble16<LPR, CPL>), dim3((unsigned)blocks), dim3(THREADS), 0, s,
+                     (const uint4 *)cache, cache_rows, (const uint4 *)packed, packed_rows, loc, n,
+                     C, (uint4 *)out, status);
+  DG_HIP(hipGetLastError());
+  return DG_OK;
+}
+
+bool overlaps(const void *a, int64_t an, const void *b, int64_t bn) {
+  if (!a || !b || an <= 0 || bn <= 0) return false;
+  uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + (uintptr_t)bn && y < x + (uintptr_t)an;
+}
+
+}  // namespace
+}  // namespace dg
+
+using namespace dg;
+
+extern "C" int dg_assemble_batch(const void *cache, int64_t cache_rows, const void *packed_b,
+                                 int64_t packed_rows_b, const int32_t *loc_b, int64_t n_b,
+                                 int64_t row_bytes, void *out, int32_t *status,
+                                 hipStream_t stream) {
+  if (n_b < 0 || row_bytes < 1 || cache_rows < 0 || packed_rows_b < 0)
+    return set_error(DG_EINVAL, "dg_assemble_batch: bad sizes");
+  if (n_b == 0) return DG_OK;
+  if (!loc_b || !out || (cache_rows > 0 && !cache) || (packed_rows_b > 0 && !packed_b))
+    return set_error(DG_EINVAL, "dg_assemble_batch: null pointer argument");
+  const int64_t out_bytes = n_b * row_bytes;
+  if (overlaps(out, out_bytes, cache, cache_rows * row_bytes) ||
+      overlaps(out, out_bytes, packed_b, packed_rows_b * row_bytes) ||
+      overlaps(out, out_bytes, loc_b, n_b * 4))
+    return set_error(DG_EINVAL, "dg_assemble_batch: output overlaps an input");
+  const int w = word_bytes(row_bytes, {cache, packed_b, out});
+  if (w == 16) {
+    const int64_t C = row_bytes / 16;
+    RowShape sh;
+    if (row_shape16(C, &sh)) {
+      const int c = (int)C;
+      if (sh.lpr == 4) return launch16<4, 1>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, c, out, status, stream);
+      if (sh.lpr == 8) return launch16<8, 1>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, c, out, status, stream);
+      if (sh.lpr == 16) return launch16<16, 1>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, c, out, status, stream);
+      if (sh.lpr == 32 && sh.cpl == 1) return launch16<32, 1>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, c, out, status, stream);
+      if (sh.lpr == 64 && sh.cpl == 1) return launch16<64, 1>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, c, out, status, stream);
+      if (sh.lpr == 32 && sh.cpl == 3) return launch16<32, 3>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, c, out, status, stream);
+      if (sh.lpr == 64 && sh.cpl == 2) return launch16<64, 2>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, c, out, status, stream);
+      if (sh.lpr == 64 && sh.cpl == 4) return launch16<64, 4>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, c, out, status, stream);
+    }
+    return launch_any<uint4>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, row_bytes, out, status, stream);
+  }
+  if (w == 8) return launch_any<uint2>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, row_bytes, out, status, stream);
+  if (w == 4) return launch_any<uint32_t>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, row_bytes, out, status, stream);
+  if (w == 2) return launch_any<uint16_t>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, row_bytes, out, status, stream);
+  return launch_any<uint8_t>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, row_bytes, out, status, stream);
+}

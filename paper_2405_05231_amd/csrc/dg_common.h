@@ -1,0 +1,156 @@
+// Internal declarations shared by the libdg translation units (not installed).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stdio.h>
+
+#include "dg.h"
+
+namespace dg {
+
+// ---------------------------------------------------------------- errors
+// Bits ORed into the device-side error word by data checks.
+enum : uint32_t {
+  ERR_NODE_RANGE = 1u << 0,  // a seed / node ID outside [0, N)
+  ERR_DUP_NODE = 1u << 1,    // a node repeated within one mini-batch
+  ERR_CSR = 1u << 2,         // a CSR row with offsets outside [0,E] or decreasing
+  ERR_NBR_RANGE = 1u << 3,   // a neighbour ID outside [0, N)
+  ERR_CACHE_SLOT = 1u << 4,  // cache_slot[v] < -1
+  ERR_ROW_RANGE = 1u << 5,   // an address-table entry outside its table
+};
+
+int set_error(int status, const char *fmt, ...);
+const char *describe_device_error(uint32_t bits);
+
+#define DG_HIP(call)                                                              \
+  do {                                                                            \
+    hipError_t e_ = (call);                                                       \
+    if (e_ != hipSuccess)                                                         \
+      return ::dg::set_error(DG_EHIP, "%s failed: %s", #call, hipGetErrorString(e_)); \
+  } while (0)
+
+// ---------------------------------------------------------------- workspace
+// Bump allocator over the caller's workspace (256-byte aligned pieces).
+struct Carve {
+  char *base;
+  size_t used = 0;
+  explicit Carve(void *p) : base(static_cast<char *>(p)) {}
+  template <typename T>
+  T *take(size_t count) {
+    T *p = reinterpret_cast<T *>(base ? base + used : nullptr);
+    used += (count * sizeof(T) + 255) & ~size_t(255);
+    return p;
+  }
+};
+
+// ---------------------------------------------------------------- wave64 helpers
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+__device__ __forceinline__ uint64_t lanes_below() { return (1ull << lane_id()) - 1ull; }
+
+template <typename T>
+__device__ __forceinline__ T wave_incl_sum(T x) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    T y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
+__device__ __forceinline__ uint64_t wave_or(uint64_t x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x |= __shfl_xor(x, o, 64);
+  return x;
+}
+
+// Binary search over a non-decreasing prefix array p[0..n] (p[0] = 0): the
+// batch b with p[b] <= i < p[b+1].
+__device__ __forceinline__ int find_batch(const int64_t *p, int n, int64_t i) {
+  int lo = 0, hi = n;  // invariant p[lo] <= i < p[hi]
+  while (hi - lo > 1) {
+    int mid = (lo + hi) >> 1;
+    if (p[mid] <= i) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+// ---------------------------------------------------------------- fill / scan
+int fill_u64(uint64_t *p, size_t n, uint64_t value, hipStream_t s);
+
+// Exclusive scan of n int64 values: out[0..n] (out[n] = total).  tile_sums needs
+// scan_tile_count(n) entries.
+size_t scan_tile_count(int64_t n);
+int scan_exclusive(const int64_t *in, int64_t *out, int64_t n, int64_t *tile_sums,
+                   hipStream_t s);
+
+// ---------------------------------------------------------------- mask compaction
+// A node-major membership mask: bit b of mask[u] says that node u belongs to
+// mini-batch b.  One tile of MC_TILE consecutive nodes per thread block.
+constexpr int MC_THREADS = 256;
+constexpr int MC_ROUNDS = 16;
+constexpr int MC_TILE = MC_THREADS * MC_ROUNDS;
+
+inline int64_t mc_blocks(int64_t N) { return (N + MC_TILE - 1) / MC_TILE; }
+
+// Count-matrix rows: [0,B) per batch (non-cached members), then:
+__host__ __device__ inline int row_all(int B) { return B; }        // nodes with any bit set (U)
+__host__ __device__ inline int row_packed(int B) { return B + 1; } // ... and not cached (U_nc)
+__host__ __device__ inline int row_pairs(int B) { return B + 2; }  // (node, batch) pairs of U_nc nodes
+__host__ __device__ inline int mc_rows(int B) { return B + 3; }
+
+struct MaskScan {
+  uint64_t *mask;
+  const int32_t *cache_slot;  // nullable: no node is cached
+  int64_t N;
+  int B;
+  int64_t nblk;
+  uint32_t *cnt;    // [rows * nblk]
+  int64_t *base;    // [rows * nblk]  exclusive scans along each row
+  int64_t *totals;  // [rows]
+  uint32_t *err;
+  // write pass (each output nullable)
+  int64_t seg_base[DG_MAX_BATCHES];  // start index of batch b's list in seg_out
+  int32_t *seg_out;                  // per-batch ascending lists of non-cached members
+  int32_t *uniq_out;                 // U ascending
+  int32_t *unc_ids;                  // U_nc ascending
+  int64_t *unc_off;                  // first pair of each U_nc node
+  int64_t *nodeoff;                  // [N] first pair of node u (U_nc nodes only)
+  int64_t *pairdest;                 // per pair: seg_base[b] + rank of u in b's list
+  int clear;                         // zero mask[u] once read
+};
+
+size_t mask_scan_ws_bytes(int64_t N, int B);
+void mask_scan_carve(MaskScan &m, Carve &c);
+// Count pass + per-row scans; totals are copied to host_totals (B+3 values)
+// after a stream synchronisation.
+int mask_scan_count(MaskScan &m, int64_t *host_totals, hipStream_t s);
+// Write pass (uses the scans of the preceding count pass).
+int mask_scan_write(const MaskScan &m, hipStream_t s);
+
+// ---------------------------------------------------------------- timing
+struct PhaseTimer {
+  bool on;
+  hipStream_t s;
+  hipEvent_t ev[24];
+  int used = 0;
+  explicit PhaseTimer(bool enable, hipStream_t st) : on(enable), s(st) {}
+  ~PhaseTimer() {
+    for (int i = 0; i < used; ++i) (void)hipEventDestroy(ev[i]);
+  }
+  int mark() {  // returns the index of a new recorded event, or -1
+    if (!on || used >= 24) return -1;
+    if (hipEventCreate(&ev[used]) != hipSuccess) return -1;
+    (void)hipEventRecord(ev[used], s);
+    return used++;
+  }
+  float ms(int a, int b) const {
+    if (a < 0 || b < 0) return 0.f;
+    float t = 0.f;
+    (void)hipEventElapsedTime(&t, ev[a], ev[b]);
+    return t;
+  }
+};
+
+}  // namespace dg

@@ -1,0 +1,345 @@
+// Batched feature packing (DiskGNN §5.2, Fig. 6b) and the interpreted address
+// tables (§6), for up to 64 mini-batches at once.
+//
+// The paper's packer scans the feature table partition by partition in
+// consecutive-ID order and appends each needed feature to every mini-batch
+// that needs it, so each feature is read once.  Here the table is in HBM and
+// the "partition scan" becomes one pass over a node-major membership mask
+// (bit b of mask[u] = batch b needs u): that pass yields, in ascending ID
+// order, the group's unique set U, the non-cached unique set U_nc, each
+// batch's packed order P_b, and for every (u, b) pair of U_nc the packed row
+// it goes to.  The gather then reads each row of U_nc once and writes it to
+// all its destination rows.
+#include <initializer_list>
+#include <string.h>
+
+#include "dg_rows.h"
+
+namespace dg {
+namespace {
+
+constexpr int THREADS = 256;
+constexpr int UNROLL = 4;
+
+struct Lists {
+  int B;
+  int64_t stride;
+  int64_t start[DG_MAX_BATCHES + 1];  // prefix of node counts
+};
+
+inline unsigned blocks_for(int64_t n) { return (unsigned)((n + THREADS - 1) / THREADS); }
+
+__global__ __launch_bounds__(THREADS) void k_pack_mark(Lists L, const int32_t *nodes, int64_t N,
+                                                       uint64_t *mask, uint32_t *err) {
+  int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
+  if (i >= L.start[L.B]) return;
+  int b = find_batch(L.start, L.B, i);
+  int32_t u = nodes[(int64_t)b * L.stride + (i - L.start[b])];
+  if (u < 0 || (int64_t)u >= N) {
+    atomicOr(err, ERR_NODE_RANGE);
+    return;
+  }
+  unsigned long long bit = 1ull << b;
+  unsigned long long old = atomicOr((unsigned long long *)&mask[u], bit);
+  if (old & bit) atomicOr(err, ERR_DUP_NODE);
+}
+
+// packed_ptr from the per-batch totals of the count pass.
+__global__ void k_packed_ptr(const int64_t *totals, int B, int64_t *packed_ptr) {
+  if (threadIdx.x == 0) {
+    int64_t run = 0;
+    packed_ptr[0] = 0;
+    for (int b = 0; b < B; ++b) {
+      run += totals[b];
+      packed_ptr[b + 1] = run;
+    }
+  }
+}
+
+// loc_b[j] = -(slot+1) for a cached node, else its rank in P_b.
+__global__ __launch_bounds__(THREADS) void k_build_loc(Lists L, const int32_t *nodes,
+                                                       const int32_t *cache_slot,
+                                                       const uint64_t *mask,
+                                                       const int64_t *nodeoff,
+                                                       const int64_t *pairdest,
+                                                       const int64_t *packed_ptr, int32_t *loc) {
+  int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
+  if (i >= L.start[L.B]) return;
+  int b = find_batch(L.start, L.B, i);
+  int64_t at = (int64_t)b * L.stride + (i - L.start[b]);
+  int32_t u = nodes[at];
+  int32_t sl = cache_slot[u];
+  int32_t out;
+  if (sl >= 0) {
+    out = -(sl + 1);
+  } else {
+    uint64_t below = mask[u] & ((1ull << b) - 1ull);
+    out = (int32_t)(pairdest[nodeoff[u] + __popcll(below)] - packed_ptr[b]);
+  }
+  loc[at] = out;
+}
+
+// Fan-out gather, 16-byte path: a group of LPR lanes reads the row of one U_nc
+// node once and stores it into each of its destination rows.
+template <int LPR, int CPL>
+__global__ __launch_bounds__(THREADS) void k_fanout16(const uint4 *X, const int32_t *unc_ids,
+                                                      const int64_t *unc_off, int64_t n_unc,
+                                                      int64_t n_pairs, const int64_t *pairdest,
+                                                      int C, uint4 *packed) {
+  constexpr int GPB = THREADS / LPR;
+  const int sub = threadIdx.x % LPR;
+  const int64_t grp = (int64_t)blockIdx.x * GPB + threadIdx.x / LPR;
+  const int64_t ngrp = (int64_t)gridDim.x * GPB;
+  for (int64_t i0 = grp * UNROLL; i0 < n_unc; i0 += ngrp * UNROLL) {
+    int64_t p0[UNROLL], p1[UNROLL];
+    uint4 v[UNROLL][CPL];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      int64_t i = i0 + u;
+      p0[u] = p1[u] = 0;
+      const uint4 *src = nullptr;
+      if (i < n_unc) {
+        src = X + (int64_t)unc_ids[i] * C;
+        p0[u] = unc_off[i];
+        p1[u] = i + 1 < n_unc ? unc_off[i + 1] : n_pairs;
+      }
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        int ch = sub + c * LPR;
+        v[u][c] = (src && ch < C) ? src[ch] : make_uint4(0, 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      for (int64_t p = p0[u]; p < p1[u]; ++p) {
+        uint4 *dst = packed + pairdest[p] * C;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+          int ch = sub + c * LPR;
+          if (ch < C) dst[ch] = v[u][c];
+        }
+      }
+    }
+  }
+}
+
+// Any row size / alignment: one wave per U_nc node, words of sizeof(T).
+template <typename T>
+__global__ __launch_bounds__(THREADS) void k_fanout_any(const T *X, const int32_t *unc_ids,
+                                                        const int64_t *unc_off, int64_t n_unc,
+                                                        int64_t n_pairs, const int64_t *pairdest,
+                                                        int64_t W, T *packed) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = ((int64_t)blockIdx.x * THREADS + threadIdx.x) >> 6;
+  const int64_t nwave = ((int64_t)gridDim.x * THREADS) >> 6;
+  for (int64_t i = wave; i < n_unc; i += nwave) {
+    const T *src = X + (int64_t)unc_ids[i] * W;
+    int64_t p0 = unc_off[i], p1 = i + 1 < n_unc ? unc_off[i + 1] : n_pairs;
+    for (int64_t c = lane; c < W; c += 64) {
+      T x = src[c];
+      for (int64_t p = p0; p < p1; ++p) packed[pairdest[p] * W + c] = x;
+    }
+  }
+}
+
+template <int LPR, int CPL>
+void launch16(const void *X, const int32_t *ids, const int64_t *off, int64_t n, int64_t pairs,
+              const int64_t *dest, int C, void *packed, hipStream_t s) {
+  constexpr int GPB = THREADS / LPR;
+  int64_t groups = (n + UNROLL - 1) / UNROLL;
+  int64_t blocks = (groups + GPB - 1) / GPB;
+  if (blocks > (1ll << 20)) blocks = 1ll << 20;
+  hipLaunchKernelGGL((k_fanout16<LPR, CPL>), dim3((unsigned)blocks), dim3(THREADS), 0, s,
+                     (const uint4 *)X, ids, off, n, pairs, dest, C, (uint4 *)packed);
+}
+
+template <typename T>
+void launch_any(const void *X, const int32_t *ids, const int64_t *off, int64_t n, int64_t pairs,
+                const int64_t *dest, int64_t row_bytes, void *packed, hipStream_t s) {
+  int64_t blocks = (n + 3) / 4;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(k_fanout_any<T>, dim3((unsigned)blocks), dim3(THREADS), 0, s, (const T *)X,
+                     ids, off, n, pairs, dest, row_bytes / (int64_t)sizeof(T), (T *)packed);
+}
+
+int launch_fanout(const void *X, const int32_t *ids, const int64_t *off, int64_t n, int64_t pairs,
+                  const int64_t *dest, int64_t row_bytes, void *packed, hipStream_t s) {
+  if (n == 0) return DG_OK;
+  const int w = word_bytes(row_bytes, {X, packed});
+  RowShape sh;
+  if (w == 16 && row_shape16(row_bytes / 16, &sh)) {
+    const int C = (int)(row_bytes / 16);
+    if (sh.lpr == 4) launch16<4, 1>(X, ids, off, n, pairs, dest, C, packed, s);
+    else if (sh.lpr == 8) launch16<8, 1>(X, ids, off, n, pairs, dest, C, packed, s);
+    else if (sh.lpr == 16) launch16<16, 1>(X, ids, off, n, pairs, dest, C, packed, s);
+    else if (sh.lpr == 32 && sh.cpl == 1) launch16<32, 1>(X, ids, off, n, pairs, dest, C, packed, s);
+    else if (sh.lpr == 64 && sh.cpl == 1) launch16<64, 1>(X, ids, off, n, pairs, dest, C, packed, s);
+    else if (sh.lpr == 32 && sh.cpl == 3) launch16<32, 3>(X, ids, off, n, pairs, dest, C, packed, s);
+    else if (sh.lpr == 64 && sh.cpl == 2) launch16<64, 2>(X, ids, off, n, pairs, dest, C, packed, s);
+    else launch16<64, 4>(X, ids, off, n, pairs, dest, C, packed, s);
+  } else if (w == 16) {
+    launch_any<uint4>(X, ids, off, n, pairs, dest, row_bytes, packed, s);
+  } else if (w == 8) {
+    launch_any<uint2>(X, ids, off, n, pairs, dest, row_bytes, packed, s);
+  } else if (w == 4) {
+    launch_any<uint32_t>(X, ids, off, n, pairs, dest, row_bytes, packed, s);
+  } else if (w == 2) {
+    launch_any<uint16_t>(X, ids, off, n, pairs, dest, row_bytes, packed, s);
+  } else {
+    launch_any<uint8_t>(X, ids, off, n, pairs, dest, row_bytes, packed, s);
+  }
+  DG_HIP(hipGetLastError());
+  return DG_OK;
+}
+
+struct PackWs {
+  uint32_t *err;
+  uint64_t *mask;
+  int64_t *nodeoff;
+  int32_t *unc_ids;
+  int64_t *unc_off;
+  int64_t *pairdest;
+  MaskScan ms;
+};
+
+void carve_pack(PackWs &w, Carve &c, int64_t N, int B, int64_t total_nodes) {
+  int64_t ucap = total_nodes < N ? total_nodes : N;
+  w.err = c.take<uint32_t>(64);
+  w.mask = c.take<uint64_t>((size_t)N);
+  w.nodeoff = c.take<int64_t>((size_t)N);
+  w.unc_ids = c.take<int32_t>((size_t)ucap + 1);
+  w.unc_off = c.take<int64_t>((size_t)ucap + 1);
+  w.pairdest = c.take<int64_t>((size_t)total_nodes + 1);
+  w.ms = MaskScan{};
+  w.ms.N = N;
+  w.ms.B = B;
+  mask_scan_carve(w.ms, c);
+}
+
+int read_err(uint32_t *err, hipStream_t s) {
+  uint32_t bits = 0;
+  DG_HIP(hipMemcpyAsync(&bits, err, sizeof(bits), hipMemcpyDeviceToHost, s));
+  DG_HIP(hipStreamSynchronize(s));
+  if (bits) return set_error(DG_EINVAL, "invalid input data: %s", describe_device_error(bits));
+  return DG_OK;
+}
+
+}  // namespace
+}  // namespace dg
+
+using namespace dg;
+
+extern "C" size_t dg_pack_workspace_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes) {
+  if (num_nodes < 1 || B < 1 || B > DG_MAX_BATCHES || total_nodes < 0) return 0;
+  Carve c(nullptr);
+  PackWs w;
+  carve_pack(w, c, num_nodes, B, total_nodes);
+  return c.used;
+}
+
+extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
+                             const int32_t *cache_slot, int32_t B, const int32_t *nodes,
+                             int64_t node_stride, const int64_t *node_count, int64_t packed_cap,
+                             void *packed, int32_t *packed_ids, int64_t *packed_ptr,
+                             int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique,
+                             int64_t unique_cap, void *ws, size_t ws_bytes, hipStream_t stream,
+                             dg_sizes *sizes, dg_timing *timing) {
+  if (!feats || !cache_slot || !nodes || !node_count || !packed_ptr || !packed_ptr_host ||
+      !loc || !sizes)
+    return set_error(DG_EINVAL, "dg_pack_group: null pointer argument");
+  if (N < 1 || N > 0x7fffffffll || row_bytes < 1 || B < 1 || B > DG_MAX_BATCHES ||
+      node_stride < 0 || packed_cap < 0 || unique_cap < 0)
+    return set_error(DG_EINVAL, "dg_pack_group: bad sizes (N=%lld row_bytes=%lld B=%d)",
+                     (long long)N, (long long)row_bytes, B);
+  Lists L;
+  L.B = B;
+  L.stride = node_stride;
+  L.start[0] = 0;
+  for (int b = 0; b < B; ++b) {
+    if (node_count[b] < 0 || node_count[b] > node_stride)
+      return set_error(DG_EINVAL, "dg_pack_group: node_count[%d] = %lld outside [0, %lld]", b,
+                       (long long)node_count[b], (long long)node_stride);
+    L.start[b + 1] = L.start[b] + node_count[b];
+  }
+  const int64_t total = L.start[B];
+  if (total > 0 && (!packed || !packed_ids) && packed_cap > 0)
+    return set_error(DG_EINVAL, "dg_pack_group: null output buffer");
+  const size_t need_ws = dg_pack_workspace_bytes(N, B, total);
+  if (!ws || ws_bytes < need_ws || ((uintptr_t)ws & 255))
+    return set_error(DG_EWORKSPACE, "dg_pack_group: workspace needs %zu bytes, 256-aligned",
+                     need_ws);
+
+  hipStream_t s = stream;
+  PackWs w;
+  Carve c(ws);
+  carve_pack(w, c, N, B, total);
+  w.ms.err = w.err;
+  memset(sizes, 0, sizeof(*sizes));
+  sizes->max_batch_nodes = sizes->max_batch_edges = sizes->total_edges = -1;
+  sizes->total_nodes = total;
+  sizes->exact = 1;
+  if (timing) memset(timing, 0, sizeof(*timing));
+  PhaseTimer tm(timing != nullptr, s);
+
+  int rc;
+  const int e0 = tm.mark();
+  if ((rc = fill_u64(reinterpret_cast<uint64_t *>(w.err), 32, 0, s))) return rc;
+  if ((rc = fill_u64(w.mask, (size_t)N, 0, s))) return rc;
+  if (total > 0) {
+    hipLaunchKernelGGL(k_pack_mark, dim3(blocks_for(total)), dim3(THREADS), 0, s, L, nodes, N,
+                       w.mask, w.err);
+    DG_HIP(hipGetLastError());
+  }
+  const int e1 = tm.mark();
+  // unique set, packed order, packed_ptr
+  int64_t totals[DG_MAX_BATCHES + 3];
+  w.ms.mask = w.mask;
+  w.ms.cache_slot = cache_slot;
+  if ((rc = mask_scan_count(w.ms, totals, s))) return rc;
+  if ((rc = read_err(w.err, s))) return rc;
+  int64_t rows = 0;
+  packed_ptr_host[0] = 0;
+  for (int b = 0; b < B; ++b) {
+    rows += totals[b];
+    packed_ptr_host[b + 1] = rows;
+  }
+  sizes->packed_rows = rows;
+  sizes->unique_nodes = totals[row_all(B)];
+  sizes->unique_packed = totals[row_packed(B)];
+  if (rows != totals[row_pairs(B)])
+    return set_error(DG_EINVAL, "dg_pack_group: internal pair count mismatch");
+  if (rows > packed_cap || (group_unique && sizes->unique_nodes > unique_cap))
+    return set_error(DG_ECAPACITY,
+                     "dg_pack_group: need packed_cap >= %lld and unique_cap >= %lld",
+                     (long long)rows, (long long)sizes->unique_nodes);
+  hipLaunchKernelGGL(k_packed_ptr, dim3(1), dim3(64), 0, s, w.ms.totals, B, packed_ptr);
+  for (int b = 0; b < B; ++b) w.ms.seg_base[b] = packed_ptr_host[b];
+  w.ms.seg_out = packed_ids;
+  w.ms.uniq_out = group_unique;
+  w.ms.unc_ids = w.unc_ids;
+  w.ms.unc_off = w.unc_off;
+  w.ms.nodeoff = w.nodeoff;
+  w.ms.pairdest = w.pairdest;
+  w.ms.clear = 0;
+  if ((rc = mask_scan_write(w.ms, s))) return rc;
+  const int e2 = tm.mark();
+  if (total > 0) {
+    hipLaunchKernelGGL(k_build_loc, dim3(blocks_for(total)), dim3(THREADS), 0, s, L, nodes,
+                       cache_slot, w.mask, w.nodeoff, w.pairdest, packed_ptr, loc);
+    DG_HIP(hipGetLastError());
+  }
+  const int e3 = tm.mark();
+  if ((rc = launch_fanout(feats, w.unc_ids, w.unc_off, sizes->unique_packed, rows, w.pairdest,
+                          row_bytes, packed, s)))
+    return rc;
+  const int e4 = tm.mark();
+  if ((rc = read_err(w.err, s))) return rc;
+  if (timing) {
+    timing->mark_ms = tm.ms(e0, e1);
+    timing->order_ms = tm.ms(e1, e2);
+    timing->loc_ms = tm.ms(e2, e3);
+    timing->gather_ms = tm.ms(e3, e4);
+    timing->total_ms = tm.ms(e0, e4);
+  }
+  return DG_OK;
+}

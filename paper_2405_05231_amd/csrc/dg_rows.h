@@ -1,0 +1,54 @@
+// Feature-row movement shared by the packing gather and the assembly kernel.
+//
+// A feature row is row_bytes opaque bytes.  When row_bytes and every base
+// pointer are multiples of 16 the row moves as C = row_bytes/16 uint4 vectors;
+// a group of LPR lanes owns one row and each lane moves CPL vectors of it
+// (vector c of the row goes to lane c % LPR), so each load instruction of a
+// group covers LPR*16 contiguous bytes.  Each group handles UNROLL rows per
+// iteration and issues all their loads before any store, to keep enough bytes
+// in flight to cover HBM latency.  Other sizes take a narrower word and one
+// wave per row.
+#pragma once
+
+#include "dg_common.h"
+
+namespace dg {
+
+struct RowShape {
+  int lpr;  // lanes per row
+  int cpl;  // vectors per lane
+};
+
+// Launch shapes of the 16-byte path, by vectors per row (C).
+inline bool row_shape16(int64_t C, RowShape *s) {
+  if (C <= 4) { *s = {4, 1}; return true; }
+  if (C <= 8) { *s = {8, 1}; return true; }
+  if (C <= 16) { *s = {16, 1}; return true; }
+  if (C <= 32) { *s = {32, 1}; return true; }
+  if (C <= 64) { *s = {64, 1}; return true; }
+  if (C <= 96) { *s = {32, 3}; return true; }
+  if (C <= 128) { *s = {64, 2}; return true; }
+  if (C <= 256) { *s = {64, 4}; return true; }
+  return false;  // longer rows: generic path
+}
+
+inline int word_bytes(int64_t row_bytes, std::initializer_list<const void *> ptrs) {
+  int w = 16;
+  auto fits = [&](int a) {
+    if (row_bytes % a) return false;
+    for (const void *p : ptrs)
+      if (p && ((uintptr_t)p % a)) return false;
+    return true;
+  };
+  while (w > 1 && !fits(w)) w >>= 1;
+  return w;
+}
+
+template <typename T>
+__device__ __forceinline__ T zero_word() {
+  T z;
+  memset(&z, 0, sizeof(T));
+  return z;
+}
+
+}  // namespace dg

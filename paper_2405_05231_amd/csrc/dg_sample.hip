@@ -1,0 +1,494 @@
+// Group sampling: node-wise fan-out neighbour sampling (DiskGNN §2, Fig. 1) for
+// up to 64 mini-batches in one pass (offline sampling, §3).
+//
+// Device state: a node-major membership mask visited[u] (bit b = u is already
+// in mini-batch b) and fresh[u] (bit b = u joined b at the current hop).  A hop
+// is: degree pass over the frontier -> exclusive scan (edge slots) -> draw +
+// mark (atomicOr on visited/fresh) -> mask compaction of fresh into each
+// batch's new segment, ascending, with no sort.  Local IDs are assigned at the
+// end through a (node, batch) pair table built from the final mask.
+#include <string.h>
+
+#include "dg_common.h"
+
+namespace dg {
+namespace {
+
+constexpr int THREADS = 256;
+constexpr int FMAX = 32;  // fan-outs up to this take the register path
+
+__host__ __device__ __forceinline__ uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+constexpr uint64_t GAMMA = 0x9E3779B97F4A7C15ull;
+
+// Per-hop description of the frontier, passed by value.
+struct Hop {
+  int B;
+  int32_t f;        // fan-out of this hop (< 0: all)
+  int32_t k;        // hop number, 1-based (RNG key)
+  int64_t ftot;     // frontier entries over all batches
+  int64_t fstart[DG_MAX_BATCHES + 1];  // prefix of frontier sizes
+  int64_t fpos[DG_MAX_BATCHES];        // local position of b's first frontier node
+  int64_t estart[DG_MAX_BATCHES + 1];  // prefix of this hop's edge counts
+  int64_t ebase[DG_MAX_BATCHES];       // edges of b before this hop
+  uint64_t bstate[DG_MAX_BATCHES];     // mix64(rng_seed + gamma*(g+1)) per batch
+};
+
+// Flattened (batch, position) ranges, for passes over all node or edge lists.
+struct Lists {
+  int B;
+  int64_t start[DG_MAX_BATCHES + 1];
+};
+
+__global__ __launch_bounds__(THREADS) void k_seed_init(const int32_t *seeds, int B, int S,
+                                                       int64_t N, int64_t node_cap,
+                                                       int32_t *nodes, uint64_t *visited,
+                                                       uint32_t *err) {
+  int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
+  if (i >= (int64_t)B * S) return;
+  int b = (int)(i / S);
+  int64_t j = i - (int64_t)b * S;
+  int32_t v = seeds[i];
+  nodes[(int64_t)b * node_cap + j] = v;
+  if (v < 0 || (int64_t)v >= N) {
+    atomicOr(err, ERR_NODE_RANGE);
+    return;
+  }
+  unsigned long long bit = 1ull << b;
+  unsigned long long old = atomicOr((unsigned long long *)&visited[v], bit);
+  if (old & bit) atomicOr(err, ERR_DUP_NODE);
+}
+
+__global__ __launch_bounds__(THREADS) void k_frontier_degree(
+    Hop h, const int32_t *nodes, int64_t node_cap, const int64_t *off, int64_t N, int64_t E,
+    int64_t *f_off, int64_t *f_deg, int64_t *f_cnt, uint32_t *err) {
+  int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
+  if (i >= h.ftot) return;
+  int b = find_batch(h.fstart, h.B, i);
+  int32_t v = nodes[(int64_t)b * node_cap + h.fpos[b] + (i - h.fstart[b])];
+  int64_t o0 = 0, d = 0;
+  if (v >= 0 && (int64_t)v < N) {
+    o0 = off[v];
+    int64_t o1 = off[v + 1];
+    if (o0 < 0 || o1 < o0 || o1 > E) {
+      atomicOr(err, ERR_CSR);
+    } else {
+      d = o1 - o0;
+    }
+  }
+  f_off[i] = o0;
+  f_deg[i] = d;
+  f_cnt[i] = (h.f < 0 || d <= (int64_t)h.f) ? d : (int64_t)h.f;
+}
+
+__device__ __forceinline__ void emit(int32_t u, int b, int64_t slot, int32_t parent,
+                                     int32_t *edge_src, int32_t *edge_dst, uint64_t *visited,
+                                     uint64_t *fresh, int64_t N, uint32_t *err) {
+  edge_src[slot] = parent;
+  edge_dst[slot] = u;
+  if (u < 0 || (int64_t)u >= N) {
+    atomicOr(err, ERR_NBR_RANGE);
+    return;
+  }
+  unsigned long long bit = 1ull << b;
+  unsigned long long old = atomicOr((unsigned long long *)&visited[u], bit);
+  if (!(old & bit)) atomicOr((unsigned long long *)&fresh[u], bit);
+}
+
+// One lane per frontier node.  Floyd's subset is built in registers (fully
+// unrolled, so the arrays stay in VGPRs); each drawn position's rank among the
+// f positions gives its slot, so no sort is needed.
+__global__ __launch_bounds__(THREADS) void k_hop_sample(
+    Hop h, const int32_t *nodes, int64_t node_cap, const int32_t *idx, const int64_t *f_off,
+    const int64_t *f_deg, const int64_t *f_eoff, int64_t edge_cap, int32_t *edge_src,
+    int32_t *edge_dst, uint64_t *visited, uint64_t *fresh, int64_t N, uint32_t *err) {
+  int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
+  if (i >= h.ftot) return;
+  int b = find_batch(h.fstart, h.B, i);
+  int64_t p = h.fpos[b] + (i - h.fstart[b]);
+  int64_t o0 = f_off[i], d = f_deg[i];
+  int64_t base = (int64_t)b * edge_cap + h.ebase[b] + (f_eoff[i] - h.estart[b]);
+  int32_t parent = (int32_t)p;
+  if (h.f < 0 || d <= (int64_t)h.f) {
+    for (int64_t q = 0; q < d; ++q)
+      emit(idx[o0 + q], b, base + q, parent, edge_src, edge_dst, visited, fresh, N, err);
+    return;
+  }
+  const int32_t f = h.f;
+  int32_t v = nodes[(int64_t)b * node_cap + p];
+  uint64_t key = mix64(h.bstate[b] ^ (((uint64_t)(uint32_t)h.k << 32) | (uint64_t)(uint32_t)v));
+  if (d > 0x7fffffffll) {  // positions are kept as 32-bit values
+    atomicOr(err, ERR_CSR);
+    return;
+  }
+  if (f <= FMAX) {
+    uint32_t r[FMAX];
+#pragma unroll
+    for (int s = 0; s < FMAX; ++s) {
+      r[s] = 0xffffffffu;
+      if (s < f) {
+        uint32_t j = (uint32_t)(d - f + s);
+        uint64_t hs = mix64(key + GAMMA * (uint64_t)(s + 1));
+        uint32_t t = (uint32_t)__umul64hi(hs, (uint64_t)j + 1ull);
+        bool seen = false;
+#pragma unroll
+        for (int m = 0; m < s; ++m) seen |= (r[m] == t);
+        r[s] = seen ? j : t;
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < FMAX; ++s) {
+      if (s < f) {
+        int rank = 0;
+#pragma unroll
+        for (int m = 0; m < FMAX; ++m) rank += (m < f && r[m] < r[s]) ? 1 : 0;
+        emit(idx[o0 + r[s]], b, base + rank, parent, edge_src, edge_dst, visited, fresh, N, err);
+      }
+    }
+    return;
+  }
+  // Larger fan-outs: the subset is built in this node's edge slots, then sorted.
+  int32_t *r = edge_dst + base;
+  for (int s = 0; s < f; ++s) {
+    int64_t j = d - f + s;
+    uint64_t hs = mix64(key + GAMMA * (uint64_t)(s + 1));
+    int32_t t = (int32_t)__umul64hi(hs, (uint64_t)(j + 1));
+    bool seen = false;
+    for (int m = 0; m < s; ++m) seen |= (r[m] == t);
+    r[s] = seen ? (int32_t)j : t;
+  }
+  for (int s = 1; s < f; ++s) {  // insertion sort
+    int32_t x = r[s];
+    int m = s - 1;
+    while (m >= 0 && r[m] > x) {
+      r[m + 1] = r[m];
+      --m;
+    }
+    r[m + 1] = x;
+  }
+  for (int s = 0; s < f; ++s)
+    emit(idx[o0 + r[s]], b, base + s, parent, edge_src, edge_dst, visited, fresh, N, err);
+}
+
+// pairloc[first pair of u + (# batches below b that hold u)] = local index of u in b.
+__global__ __launch_bounds__(THREADS) void k_pairloc(Lists L, const int32_t *nodes,
+                                                     int64_t node_cap, const uint64_t *visited,
+                                                     const int64_t *nodeoff, int32_t *pairloc) {
+  int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
+  if (i >= L.start[L.B]) return;
+  int b = find_batch(L.start, L.B, i);
+  int64_t j = i - L.start[b];
+  int32_t u = nodes[(int64_t)b * node_cap + j];
+  uint64_t below = visited[u] & ((1ull << b) - 1ull);
+  pairloc[nodeoff[u] + __popcll(below)] = (int32_t)j;
+}
+
+__global__ __launch_bounds__(THREADS) void k_relabel(Lists L, int64_t edge_cap, int32_t *edge_dst,
+                                                     const uint64_t *visited,
+                                                     const int64_t *nodeoff,
+                                                     const int32_t *pairloc, int64_t N) {
+  int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
+  if (i >= L.start[L.B]) return;
+  int b = find_batch(L.start, L.B, i);
+  int64_t e = (int64_t)b * edge_cap + (i - L.start[b]);
+  int32_t u = edge_dst[e];
+  if (u < 0 || (int64_t)u >= N) return;  // already reported
+  uint64_t below = visited[u] & ((1ull << b) - 1ull);
+  edge_dst[e] = pairloc[nodeoff[u] + __popcll(below)];
+}
+
+// eoff at each batch's first frontier entry (and at the end).
+__global__ void k_batch_bounds(Hop h, const int64_t *f_eoff, int64_t *out) {
+  int b = threadIdx.x;
+  if (b <= h.B) out[b] = f_eoff[h.fstart[b]];
+}
+
+inline unsigned blocks_for(int64_t n) { return (unsigned)((n + THREADS - 1) / THREADS); }
+
+struct SampleWs {
+  uint32_t *err;
+  uint64_t *visited, *fresh;
+  int64_t *nodeoff;
+  int64_t *f_off, *f_deg, *f_cnt, *f_eoff, *tiles;
+  int32_t *pairloc;
+  int64_t *small;  // host-visible staging for a few counts
+  MaskScan ms;
+};
+
+void carve_sample(SampleWs &w, Carve &c, int64_t N, int B, int64_t node_cap) {
+  int64_t fmax = (int64_t)B * node_cap;  // frontier entries never exceed the node lists
+  w.err = c.take<uint32_t>(64);
+  w.visited = c.take<uint64_t>((size_t)N);
+  w.fresh = c.take<uint64_t>((size_t)N);
+  w.nodeoff = c.take<int64_t>((size_t)N);
+  w.f_off = c.take<int64_t>((size_t)fmax);
+  w.f_deg = c.take<int64_t>((size_t)fmax);
+  w.f_cnt = c.take<int64_t>((size_t)fmax);
+  w.f_eoff = c.take<int64_t>((size_t)fmax + 1);
+  w.tiles = c.take<int64_t>(scan_tile_count(fmax));
+  w.pairloc = c.take<int32_t>((size_t)fmax);
+  w.small = c.take<int64_t>(2 * (DG_MAX_BATCHES + 1));
+  w.ms = MaskScan{};
+  w.ms.N = N;
+  w.ms.B = B;
+  mask_scan_carve(w.ms, c);
+}
+
+int check_err(uint32_t *err_dev, hipStream_t s) {
+  uint32_t bits = 0;
+  DG_HIP(hipMemcpyAsync(&bits, err_dev, sizeof(bits), hipMemcpyDeviceToHost, s));
+  DG_HIP(hipStreamSynchronize(s));
+  if (bits) return set_error(DG_EINVAL, "invalid input data: %s", describe_device_error(bits));
+  return DG_OK;
+}
+
+}  // namespace
+}  // namespace dg
+
+using namespace dg;
+
+extern "C" int dg_sample_bounds(int64_t num_nodes, int64_t num_edges, int32_t S,
+                                const int32_t *fanouts, int32_t K, int64_t *node_cap,
+                                int64_t *edge_cap) {
+  if (!node_cap || !edge_cap || (K > 0 && !fanouts) || S < 1 || K < 0 || num_nodes < 1 ||
+      num_edges < 0)
+    return set_error(DG_EINVAL, "dg_sample_bounds: bad argument");
+  // Saturating arithmetic: once a layer reaches N nodes, nothing grows further.
+  int64_t n = S, e = 0, layer = S;
+  bool all = false;
+  for (int k = 0; k < K && !all; ++k) {
+    int32_t f = fanouts[k];
+    if (f < 0) { all = true; break; }
+    if (layer > 0 && f > 0 && layer > INT64_MAX / 4 / f) { all = true; break; }
+    layer *= f;
+    e += layer;
+    n += layer;
+    if (n > num_nodes && e > num_edges) { all = true; break; }
+  }
+  *node_cap = all ? num_nodes : (n < num_nodes ? n : num_nodes);
+  *edge_cap = all ? num_edges : (e < num_edges ? e : num_edges);
+  if (*edge_cap < 1) *edge_cap = 1;
+  return DG_OK;
+}
+
+extern "C" size_t dg_sample_workspace_bytes(int64_t num_nodes, int32_t B, int64_t node_cap,
+                                            int64_t edge_cap) {
+  (void)edge_cap;
+  if (num_nodes < 1 || B < 1 || B > DG_MAX_BATCHES || node_cap < 1) return 0;
+  Carve c(nullptr);
+  SampleWs w;
+  carve_sample(w, c, num_nodes, B, node_cap);
+  return c.used;
+}
+
+extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S,
+                               int64_t batch_base, const int32_t *fanouts, int32_t K,
+                               uint64_t rng_seed, int64_t node_cap, int32_t *nodes,
+                               int64_t *hop_ptr, int64_t edge_cap, int32_t *edge_src,
+                               int32_t *edge_dst, int64_t *edge_ptr, void *ws, size_t ws_bytes,
+                               hipStream_t stream, dg_sizes *sizes, dg_timing *timing) {
+  if (!g || !seeds || !nodes || !hop_ptr || !edge_src || !edge_dst || !edge_ptr || !sizes ||
+      (K > 0 && !fanouts))
+    return set_error(DG_EINVAL, "dg_sample_group: null pointer argument");
+  if (!g->offsets || (g->num_edges > 0 && !g->indices) || g->num_nodes < 1 ||
+      g->num_nodes > 0x7fffffffll || g->num_edges < 0)
+    return set_error(DG_EINVAL, "dg_sample_group: bad CSR description");
+  if (B < 1 || B > DG_MAX_BATCHES || S < 1 || K < 0 || node_cap < S || edge_cap < 0 ||
+      (int64_t)S > g->num_nodes)
+    return set_error(DG_EINVAL, "dg_sample_group: bad sizes (B=%d S=%d K=%d node_cap=%lld)", B,
+                     S, K, (long long)node_cap);
+  if (node_cap > 0x7fffffffll)
+    return set_error(DG_EINVAL, "dg_sample_group: node_cap too large for int32 local IDs");
+  const size_t need_ws = dg_sample_workspace_bytes(g->num_nodes, B, node_cap, edge_cap);
+  if (!ws || ws_bytes < need_ws || ((uintptr_t)ws & 255))
+    return set_error(DG_EWORKSPACE, "dg_sample_group: workspace needs %zu bytes, 256-aligned",
+                     need_ws);
+
+  const int64_t N = g->num_nodes, E = g->num_edges;
+  hipStream_t s = stream;
+  SampleWs w;
+  Carve c(ws);
+  carve_sample(w, c, N, B, node_cap);
+  w.ms.err = w.err;
+
+  memset(sizes, 0, sizeof(*sizes));
+  sizes->packed_rows = sizes->unique_nodes = sizes->unique_packed = -1;
+  sizes->exact = 1;
+  if (timing) memset(timing, 0, sizeof(*timing));
+  PhaseTimer tm(timing != nullptr, s);
+  float t_sample = 0.f, t_dedup = 0.f;
+  const int ev_start = tm.mark();
+
+  int rc;
+  if ((rc = fill_u64(reinterpret_cast<uint64_t *>(w.err), 32, 0, s))) return rc;
+  if ((rc = fill_u64(w.visited, (size_t)N, 0, s))) return rc;
+  if ((rc = fill_u64(w.fresh, (size_t)N, 0, s))) return rc;
+  hipLaunchKernelGGL(k_seed_init, dim3(blocks_for((int64_t)B * S)), dim3(THREADS), 0, s, seeds,
+                     B, S, N, node_cap, nodes, w.visited, w.err);
+  DG_HIP(hipGetLastError());
+  if ((rc = check_err(w.err, s))) return rc;
+
+  int64_t n_b[DG_MAX_BATCHES], e_b[DG_MAX_BATCHES];
+  for (int b = 0; b < B; ++b) {
+    n_b[b] = S;
+    e_b[b] = 0;
+    hop_ptr[(int64_t)b * (K + 2) + 0] = 0;
+    hop_ptr[(int64_t)b * (K + 2) + 1] = S;
+  }
+
+  Hop h;
+  memset(&h, 0, sizeof(h));
+  h.B = B;
+  for (int b = 0; b < B; ++b)
+    h.bstate[b] = mix64(rng_seed + GAMMA * ((uint64_t)(batch_base + b) + 1ull));
+  int64_t fbeg[DG_MAX_BATCHES], fend[DG_MAX_BATCHES];
+  for (int b = 0; b < B; ++b) {
+    fbeg[b] = 0;
+    fend[b] = S;
+  }
+  int64_t totals[DG_MAX_BATCHES + 3];
+
+  for (int k = 1; k <= K; ++k) {
+    for (int b = 0; b < B; ++b) edge_ptr[(int64_t)b * (K + 1) + (k - 1)] = e_b[b];
+    const int32_t f = fanouts[k - 1];
+    h.f = f;
+    h.k = k;
+    h.fstart[0] = 0;
+    for (int b = 0; b < B; ++b) {
+      h.fpos[b] = fbeg[b];
+      h.fstart[b + 1] = h.fstart[b] + (fend[b] - fbeg[b]);
+      h.ebase[b] = e_b[b];
+    }
+    h.ftot = h.fstart[B];
+    int64_t new_b[DG_MAX_BATCHES];
+    if (h.ftot == 0 || f == 0) {
+      for (int b = 0; b < B; ++b) new_b[b] = 0;
+    } else {
+      const int ev0 = tm.mark();
+      hipLaunchKernelGGL(k_frontier_degree, dim3(blocks_for(h.ftot)), dim3(THREADS), 0, s, h,
+                         nodes, node_cap, g->offsets, N, E, w.f_off, w.f_deg, w.f_cnt, w.err);
+      DG_HIP(hipGetLastError());
+      if ((rc = scan_exclusive(w.f_cnt, w.f_eoff, h.ftot, w.tiles, s))) return rc;
+      // edge counts per batch: f_eoff at the batch boundaries
+      int64_t bound[DG_MAX_BATCHES + 1];
+      hipLaunchKernelGGL(k_batch_bounds, dim3(1), dim3(DG_MAX_BATCHES + 1), 0, s, h, w.f_eoff,
+                         w.small);
+      DG_HIP(hipGetLastError());
+      DG_HIP(hipMemcpyAsync(bound, w.small, sizeof(int64_t) * (B + 1), hipMemcpyDeviceToHost, s));
+      DG_HIP(hipStreamSynchronize(s));
+      h.estart[0] = 0;
+      bool over = false;
+      for (int b = 0; b < B; ++b) {
+        h.estart[b + 1] = bound[b + 1];
+        int64_t cnt = bound[b + 1] - bound[b];
+        if (e_b[b] + cnt > edge_cap) over = true;
+        if (e_b[b] + cnt > sizes->max_batch_edges) sizes->max_batch_edges = e_b[b] + cnt;
+      }
+      if (over) {
+        sizes->exact = 0;
+        for (int b = 0; b < B; ++b)
+          if (n_b[b] > sizes->max_batch_nodes) sizes->max_batch_nodes = n_b[b];
+        return set_error(DG_ECAPACITY, "dg_sample_group: edge_cap %lld too small at hop %d",
+                         (long long)edge_cap, k);
+      }
+      hipLaunchKernelGGL(k_hop_sample, dim3(blocks_for(h.ftot)), dim3(THREADS), 0, s, h, nodes,
+                         node_cap, g->indices, w.f_off, w.f_deg, w.f_eoff, edge_cap, edge_src,
+                         edge_dst, w.visited, w.fresh, N, w.err);
+      DG_HIP(hipGetLastError());
+      const int ev1 = tm.mark();
+      // new nodes of this hop, per batch, ascending
+      w.ms.mask = w.fresh;
+      w.ms.cache_slot = nullptr;
+      if ((rc = mask_scan_count(w.ms, totals, s))) return rc;
+      bool nover = false;
+      for (int b = 0; b < B; ++b) {
+        new_b[b] = totals[b];
+        if (n_b[b] + new_b[b] > node_cap) nover = true;
+      }
+      for (int b = 0; b < B; ++b) {
+        e_b[b] += bound[b + 1] - bound[b];
+        if (n_b[b] + new_b[b] > sizes->max_batch_nodes) sizes->max_batch_nodes = n_b[b] + new_b[b];
+      }
+      if (nover) {
+        sizes->exact = 0;
+        return set_error(DG_ECAPACITY, "dg_sample_group: node_cap %lld too small at hop %d",
+                         (long long)node_cap, k);
+      }
+      for (int b = 0; b < B; ++b) w.ms.seg_base[b] = (int64_t)b * node_cap + n_b[b];
+      w.ms.seg_out = nodes;
+      w.ms.uniq_out = nullptr;
+      w.ms.unc_ids = nullptr;
+      w.ms.unc_off = nullptr;
+      w.ms.nodeoff = nullptr;
+      w.ms.pairdest = nullptr;
+      w.ms.clear = 1;
+      if ((rc = mask_scan_write(w.ms, s))) return rc;
+      const int ev2 = tm.mark();
+      DG_HIP(hipStreamSynchronize(s));
+      t_sample += tm.ms(ev0, ev1);
+      t_dedup += tm.ms(ev1, ev2);
+    }
+    for (int b = 0; b < B; ++b) {
+      fbeg[b] = n_b[b];
+      n_b[b] += new_b[b];
+      fend[b] = n_b[b];
+      hop_ptr[(int64_t)b * (K + 2) + k + 1] = n_b[b];
+    }
+  }
+  for (int b = 0; b < B; ++b) edge_ptr[(int64_t)b * (K + 1) + K] = e_b[b];
+  if ((rc = check_err(w.err, s))) return rc;
+
+  // Local IDs: pair table over the final membership mask.
+  const int ev_r0 = tm.mark();
+  Lists LN, LE;
+  LN.B = LE.B = B;
+  LN.start[0] = LE.start[0] = 0;
+  for (int b = 0; b < B; ++b) {
+    LN.start[b + 1] = LN.start[b] + n_b[b];
+    LE.start[b + 1] = LE.start[b] + e_b[b];
+  }
+  if (LE.start[B] > 0) {
+    w.ms.mask = w.visited;
+    w.ms.cache_slot = nullptr;
+    if ((rc = mask_scan_count(w.ms, totals, s))) return rc;
+    if (totals[row_pairs(B)] != LN.start[B])
+      return set_error(DG_EINVAL, "dg_sample_group: internal pair count mismatch");
+    w.ms.seg_out = nullptr;
+    w.ms.uniq_out = nullptr;
+    w.ms.unc_ids = nullptr;
+    w.ms.unc_off = nullptr;
+    w.ms.nodeoff = w.nodeoff;
+    w.ms.pairdest = nullptr;
+    w.ms.clear = 0;
+    if ((rc = mask_scan_write(w.ms, s))) return rc;
+    hipLaunchKernelGGL(k_pairloc, dim3(blocks_for(LN.start[B])), dim3(THREADS), 0, s, LN, nodes,
+                       node_cap, w.visited, w.nodeoff, w.pairloc);
+    hipLaunchKernelGGL(k_relabel, dim3(blocks_for(LE.start[B])), dim3(THREADS), 0, s, LE,
+                       edge_cap, edge_dst, w.visited, w.nodeoff, w.pairloc, N);
+    DG_HIP(hipGetLastError());
+  }
+  const int ev_r1 = tm.mark();
+  if ((rc = check_err(w.err, s))) return rc;
+
+  int64_t tn = 0, te = 0, mn = 0, me = 0;
+  for (int b = 0; b < B; ++b) {
+    tn += n_b[b];
+    te += e_b[b];
+    if (n_b[b] > mn) mn = n_b[b];
+    if (e_b[b] > me) me = e_b[b];
+  }
+  sizes->max_batch_nodes = mn;
+  sizes->max_batch_edges = me;
+  sizes->total_nodes = tn;
+  sizes->total_edges = te;
+  if (timing) {
+    timing->sample_ms = t_sample;
+    timing->dedup_ms = t_dedup;
+    timing->relabel_ms = tm.ms(ev_r0, ev_r1);
+    timing->total_ms = tm.ms(ev_start, ev_r1);
+  }
+  return DG_OK;
+}

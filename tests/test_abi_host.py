@@ -1,0 +1,106 @@
+"""The C ABI on the host side (no GPU needed): the library loads, exports every
+entry point the header declares, and rejects bad arguments before any device
+work."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from conftest import ROOT
+
+HEADER = os.path.join(ROOT, "include", "dg.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dg_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2405_05231_amd import _lib
+    return _lib.load()
+
+
+def test_header_declares_the_three_path_calls():
+    names = declared_functions()
+    for want in ("dg_sample_group", "dg_pack_group", "dg_assemble_batch"):
+        assert want in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    from paper_2405_05231_amd import _lib
+    names = declared_functions()
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(_lib.SIGNATURES), "binding signatures out of sync with dg.h"
+    assert L.dg_version().decode().startswith("libdg")
+
+
+def test_no_fallback_when_library_missing(tmp_path, monkeypatch):
+    from paper_2405_05231_amd import _lib
+    monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(_lib, "_lib", None)
+    with pytest.raises(ImportError):
+        _lib.load()
+
+
+def test_sample_bounds(L):
+    import paper_2405_05231_amd as dg
+    assert dg.sample_bounds(10_000, 105_000, 64, [5, 5]) == (64 * 31, 64 * 30)
+    assert dg.sample_bounds(100_000_000, 1_600_000_000, 1024, [15, 10, 5]) == (937_984, 936_960)
+    assert dg.sample_bounds(1000, 5000, 4, [-1, 2]) == (1000, 5000)
+    assert dg.sample_bounds(50, 10**9, 8, [10, 10]) == (50, 880)
+    with pytest.raises(dg.DGError):
+        dg.sample_bounds(0, 10, 1, [1])
+
+
+def test_workspace_queries(L):
+    a = L.dg_sample_workspace_bytes(10_000, 4, 2000, 2000)
+    b = L.dg_sample_workspace_bytes(20_000, 4, 2000, 2000)
+    assert 0 < a < b and a % 256 == 0
+    assert L.dg_sample_workspace_bytes(10_000, 65, 2000, 2000) == 0
+    p = L.dg_pack_workspace_bytes(10_000, 4, 8000)
+    assert p > 8 * 10_000 and p % 256 == 0
+    assert L.dg_pack_workspace_bytes(10_000, 0, 10) == 0
+
+
+def test_host_side_argument_errors(L):
+    from paper_2405_05231_amd import _lib
+    sizes = _lib.Sizes()
+    # null CSR / outputs: rejected before any device call
+    rc = L.dg_sample_group(None, None, 1, 1, 0, None, 0, 0, 1, None, None, 1, None, None, None,
+                           None, 0, None, ctypes.byref(sizes), None)
+    assert rc == _lib.DG_EINVAL
+    assert b"null" in L.dg_last_error()
+    g = _lib.Csr(10, 0, 0x1000, 0)
+    hop = (ctypes.c_int64 * 4)()
+    ep = (ctypes.c_int64 * 3)()
+    fo = (ctypes.c_int32 * 1)(2)
+    fake = ctypes.c_void_p(0x1000)
+    # B out of range
+    rc = L.dg_sample_group(ctypes.byref(g), fake, 65, 1, 0, fo, 1, 0, 4, fake, hop, 4, fake, fake,
+                           ep, fake, 1 << 20, None, ctypes.byref(sizes), None)
+    assert rc == _lib.DG_EINVAL
+    # workspace missing
+    rc = L.dg_sample_group(ctypes.byref(g), fake, 1, 1, 0, fo, 1, 0, 4, fake, hop, 4, fake, fake,
+                           ep, None, 0, None, ctypes.byref(sizes), None)
+    assert rc == _lib.DG_EWORKSPACE
+    # pack: B = 0, row_bytes = 0, counts beyond the stride
+    cnt = (ctypes.c_int64 * 2)(3, 9)
+    ph = (ctypes.c_int64 * 3)()
+    rc = L.dg_pack_group(fake, 10, 0, fake, 2, fake, 8, cnt, 0, None, None, fake, ph, fake, None,
+                         0, fake, 1 << 20, None, ctypes.byref(sizes), None)
+    assert rc == _lib.DG_EINVAL
+    rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, cnt, 0, None, None, fake, ph, fake, None,
+                         0, fake, 1 << 20, None, ctypes.byref(sizes), None)
+    assert rc == _lib.DG_EINVAL and b"node_count" in L.dg_last_error()
+    # assemble: n_b = 0 is a no-op; negative sizes and overlap are rejected
+    assert L.dg_assemble_batch(None, 0, None, 0, None, 0, 16, None, None, None) == _lib.DG_OK
+    assert L.dg_assemble_batch(None, 0, None, 0, fake, -1, 16, fake, None, None) == _lib.DG_EINVAL
+    buf = ctypes.c_void_p(0x100000)
+    rc = L.dg_assemble_batch(buf, 100, ctypes.c_void_p(0x900000), 10, ctypes.c_void_p(0xF00000), 4,
+                             16, ctypes.c_void_p(0x100010), None, None)
+    assert rc == _lib.DG_EINVAL and b"overlap" in L.dg_last_error()

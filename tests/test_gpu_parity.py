@@ -1,0 +1,209 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle, bit-exact:
+every output is an integer or a row copy, so the tolerance is zero.  Small
+workloads compare every output element; edge cases cover empty and ragged
+inputs, fan-outs below / at / above the degree, all-neighbour hops, fan-outs
+beyond the register path, every cache share, odd row sizes and the group
+split."""
+import random
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module")
+def dg():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2405_05231_amd as m
+    return m
+
+
+def to_np(t):
+    return t.detach().cpu().numpy()
+
+
+def run_path(dg, off, idx, seeds, fanouts, rng_seed, feats, cache_slot, cache_nodes,
+             batch_base=0, sample_kw=None):
+    """The device path: sample -> pack -> assemble every batch."""
+    off_d, idx_d = off.to(DEV), idx.to(DEV)
+    seeds_d = seeds.to(DEV)
+    sr = dg.sample_group(off_d, idx_d, seeds_d, fanouts, rng_seed, batch_base=batch_base,
+                         **(sample_kw or {}))
+    X = feats.to(DEV)
+    slot = cache_slot.to(DEV)
+    cache = X.index_select(0, cache_nodes.to(DEV)) if cache_nodes.numel() else None
+    R = X[0].numel() * X.element_size()
+    pr = dg.pack_group(X, slot, sr.nodes, sr.node_count, with_unique=True)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    Y = []
+    for b in range(seeds.shape[0]):
+        n = int(sr.hop_ptr[b, -1])
+        Y.append(dg.assemble_batch(cache, pr.chunk(b), pr.loc[b, :n], R, status=status))
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    return sr, pr, Y, cache
+
+
+def compare_sampling(sr, ref, B):
+    for b in range(B):
+        n = int(sr.hop_ptr[b, -1])
+        e = int(sr.edge_ptr[b, -1])
+        assert np.array_equal(sr.hop_ptr[b], ref["hop_ptr"][b]), b
+        assert np.array_equal(sr.edge_ptr[b], ref["edge_ptr"][b]), b
+        assert np.array_equal(to_np(sr.nodes[b, :n]), ref["nodes"][b]), b
+        assert np.array_equal(to_np(sr.edge_src[b, :e]), ref["edge_src"][b]), b
+        assert np.array_equal(to_np(sr.edge_dst[b, :e]), ref["edge_dst"][b]), b
+
+
+def compare_packing(pr, ref, B, full_rows=True):
+    rows = ref["packed_rows"]
+    assert pr.sizes["packed_rows"] == rows
+    assert pr.sizes["unique_nodes"] == ref["unique_nodes"]
+    assert pr.sizes["unique_packed"] == ref["unique_packed"]
+    assert np.array_equal(pr.packed_ptr_host, ref["packed_ptr"])
+    assert np.array_equal(to_np(pr.packed_ptr), ref["packed_ptr"])
+    assert np.array_equal(to_np(pr.packed_ids[:rows]), ref["packed_ids"])
+    assert np.array_equal(to_np(pr.unique[:ref["unique_nodes"]]), ref["unique"])
+    for b in range(B):
+        n = len(ref["loc"][b])
+        assert np.array_equal(to_np(pr.loc[b, :n]), ref["loc"][b]), b
+    if full_rows:
+        assert np.array_equal(to_np(pr.packed[:rows]), ref["packed"])
+
+
+def oracle_full(orc, off, idx, seeds, fanouts, rng_seed, feats, cache_slot, cache_nodes,
+                batch_base=0):
+    X = to_np(feats)
+    ref_s = orc.sample_group(to_np(off), to_np(idx), to_np(seeds), fanouts, rng_seed,
+                             batch_base=batch_base)
+    ref_p = orc.pack_group(X, to_np(cache_slot), ref_s["nodes"])
+    R = X[0].nbytes
+    cache = X[to_np(cache_nodes)] if cache_nodes.numel() else np.zeros((0,) + X.shape[1:], X.dtype)
+    ref_y = []
+    for b in range(len(ref_s["nodes"])):
+        lo, hi = ref_p["packed_ptr"][b], ref_p["packed_ptr"][b + 1]
+        ref_y.append(orc.assemble_batch(cache, ref_p["packed"][lo:hi], ref_p["loc"][b], R))
+    return ref_s, ref_p, ref_y
+
+
+def check_all(dg, orc, off, idx, seeds, fanouts, rng_seed, feats, cache_slot, cache_nodes,
+              batch_base=0, sample_kw=None):
+    sr, pr, Y, _ = run_path(dg, off, idx, seeds, fanouts, rng_seed, feats, cache_slot,
+                            cache_nodes, batch_base, sample_kw)
+    ref_s, ref_p, ref_y = oracle_full(orc, off, idx, seeds, fanouts, rng_seed, feats, cache_slot,
+                                      cache_nodes, batch_base)
+    B = seeds.shape[0]
+    compare_sampling(sr, ref_s, B)
+    compare_packing(pr, ref_p, B)
+    X = to_np(feats).view(np.uint8).reshape(feats.shape[0], -1)
+    for b in range(B):
+        y = to_np(Y[b])
+        assert np.array_equal(y, ref_y[b]), b
+        assert np.array_equal(y, X[ref_s["nodes"][b]]), b        # closed form Y_b = X[nodes_b]
+    return sr, pr
+
+
+# ------------------------------------------------------------------ workloads
+def test_tiny_workload_T(dg, orc):
+    w = synth.make_workload("T")
+    check_all(dg, orc, w.offsets, w.indices, w.seeds, list(w.cfg.fanouts), w.rng_seed, w.feats,
+              w.cache_slot, w.cache_nodes)
+
+
+def test_tiny_workload_T_is_deterministic(dg):
+    w = synth.make_workload("T")
+    a, pa, ya, _ = run_path(dg, w.offsets, w.indices, w.seeds, list(w.cfg.fanouts), w.rng_seed,
+                            w.feats, w.cache_slot, w.cache_nodes)
+    b, pb, yb, _ = run_path(dg, w.offsets, w.indices, w.seeds, list(w.cfg.fanouts), w.rng_seed,
+                            w.feats, w.cache_slot, w.cache_nodes)
+    for B in range(w.cfg.B):
+        assert torch.equal(a.batch_nodes(B), b.batch_nodes(B))
+        assert torch.equal(ya[B], yb[B])
+    assert torch.equal(pa.packed, pb.packed)
+
+
+def test_group_split_equals_whole(dg):
+    w = synth.make_workload("T")
+    fan = list(w.cfg.fanouts)
+    whole = dg.sample_group(w.offsets.to(DEV), w.indices.to(DEV), w.seeds.to(DEV), fan,
+                            w.rng_seed, batch_base=7)
+    part0 = dg.sample_group(w.offsets.to(DEV), w.indices.to(DEV), w.seeds[:1].to(DEV), fan,
+                            w.rng_seed, batch_base=7)
+    part1 = dg.sample_group(w.offsets.to(DEV), w.indices.to(DEV), w.seeds[1:].contiguous().to(DEV),
+                            fan, w.rng_seed, batch_base=8)
+    parts = [(part0, 0)] + [(part1, i) for i in range(w.cfg.B - 1)]
+    for b, (p, i) in enumerate(parts):
+        assert torch.equal(whole.batch_nodes(b), p.batch_nodes(i))
+        assert torch.equal(whole.batch_edges(b)[1], p.batch_edges(i)[1])
+
+
+# ------------------------------------------------------------------ edge cases
+def random_case(rnd, n, maxdeg):
+    deg = [rnd.randint(0, min(maxdeg, n - 1)) for _ in range(n)]
+    rows = [sorted(rnd.sample([u for u in range(n) if u != v], d)) for v, d in enumerate(deg)]
+    off = np.zeros(n + 1, dtype=np.int64)
+    off[1:] = np.cumsum(deg)
+    idx = np.array([u for r in rows for u in r], dtype=np.int32)
+    return torch.from_numpy(off), torch.from_numpy(idx)
+
+
+CASES = [
+    # (n, maxdeg, B, S, fanouts, row elems, dtype, cache share)
+    (50, 8, 1, 1, [2, 2], 4, torch.float32, 0.0),
+    (300, 30, 3, 7, [5, -1], 16, torch.float32, 0.2),
+    (300, 60, 2, 5, [40, 3], 16, torch.float32, 0.5),          # f > register path
+    (200, 12, 4, 9, [0, 3], 8, torch.float32, 0.1),            # f = 0 hop
+    (500, 25, 64, 3, [4, 4, 4], 32, torch.float32, 0.05),      # B = 64
+    (1000, 20, 5, 20, [10, 10, 10], 24, torch.float16, 0.3),   # 48-byte rows
+    (400, 15, 3, 11, [15, 15], 3, torch.uint8, 0.0),           # 3-byte rows
+    (400, 15, 3, 11, [7, 1], 5, torch.int16, 1.0),             # every node cached
+    (777, 40, 7, 13, [-1, 2], 385, torch.float32, 0.02),       # 1540-byte rows
+    (100, 99, 2, 4, [99, 99], 4, torch.float32, 0.0),          # f = d on full rows
+    (2, 1, 2, 1, [1, 1, 1], 4, torch.float32, 0.0),            # tiny graph, cycles
+    (64, 0, 3, 5, [3, 3], 4, torch.float32, 0.0),              # no edges at all
+]
+
+
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_edge_cases(dg, orc, case):
+    n, maxdeg, B, S, fan, dim, dtype, share = CASES[case]
+    rnd = random.Random(900 + case)
+    off, idx = random_case(rnd, n, maxdeg) if maxdeg else (
+        torch.zeros(n + 1, dtype=torch.int64), torch.zeros(0, dtype=torch.int32))
+    seeds = torch.tensor([rnd.sample(range(n), S) for _ in range(B)], dtype=torch.int32)
+    gen = torch.Generator().manual_seed(case)
+    if dtype.is_floating_point:
+        feats = torch.randn((n, dim), generator=gen).to(dtype)
+    else:
+        feats = torch.randint(0, 100, (n, dim), generator=gen).to(dtype)
+    ncache = int(n * share)
+    cache_nodes = torch.tensor(rnd.sample(range(n), ncache), dtype=torch.int64)
+    slot = torch.full((n,), -1, dtype=torch.int32)
+    slot[cache_nodes] = torch.arange(ncache, dtype=torch.int32)
+    check_all(dg, orc, off, idx, seeds, fan, 12345 + case, feats, slot, cache_nodes,
+              batch_base=case)
+
+
+def test_fig1_example_on_device(dg, orc):
+    import json, os
+    from conftest import GOLDEN
+    fx = json.load(open(os.path.join(GOLDEN, "fig1_sampling.json")))
+    n = fx["num_nodes"]
+    off = np.zeros(n + 1, dtype=np.int64)
+    idx = []
+    for v in range(n):
+        r = fx["rows"].get(str(v), [])
+        idx += r
+        off[v + 1] = off[v] + len(r)
+    sr = dg.sample_group(torch.from_numpy(off).to(DEV), torch.tensor(idx, dtype=torch.int32,
+                         device=DEV), torch.tensor(fx["seeds"], dtype=torch.int32, device=DEV),
+                         fx["fanouts"], 0)
+    assert to_np(sr.batch_nodes(0)).tolist() == fx["expect"]["nodes"]
+    assert sr.hop_ptr[0].tolist() == fx["expect"]["hop_ptr"]
