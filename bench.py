@@ -1,0 +1,252 @@
+"""Benchmark of the offline-sampling hot path on one MI355X.
+
+One step = one pass of the whole path over a group of mini-batches whose
+inputs are resident in HBM: group sampling (dg_sample_group) -> batched
+packing (dg_pack_group) -> assembly of every mini-batch (dg_assemble_batch).
+
+Reported value: feature bytes the method must move per step (packing: each
+non-cached unique row read once + one row write per packed row; assembly: one
+row read + one row write per required row) divided by the wall time of the
+whole step, in GB/s.  Sampled edges/s, per-phase rates and the roofline
+fraction of the fan-out gather kernel are reported beside it, with the CPU
+oracle timed on a bounded sample of the same workload.
+
+Usage: python bench.py [--steps K] [--warmup W] [--workload L100] [--gpus 1]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def kernel_source_digest() -> str:
+    """Digest of the sources the timed kernels are built from (ties committed
+    counter readings to the code they were taken on)."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2405_05231_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload: str, kernel: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("source_digest") != kernel_source_digest():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="L100")
+    ap.add_argument("--cache-pct", type=int, default=None)
+    ap.add_argument("--cpu-batches", type=int, default=4,
+                    help="mini-batches in the CPU-oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calib", action="store_true",
+                    help="also run a plain copy of known size (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on exactly one GPU: the hot path is measured on one GPU's "
+              "share; see DESIGN.md for how it would shard.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2405_05231_amd as dg
+    import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = synth.CONFIGS[args.workload]
+    t0 = time.perf_counter()
+    log(f"generating {cfg.name}: N={cfg.n:,} draws={cfg.draws:,} dim={cfg.dim} {cfg.dtype}")
+    w = synth.make_workload(cfg, device=dev, cache_pct=args.cache_pct)
+    torch.cuda.synchronize()
+    log(f"workload ready in {time.perf_counter() - t0:.1f}s: E={w.num_edges:,} "
+        f"cache={w.cache_nodes.numel():,} rows")
+    torch.cuda.empty_cache()
+
+    fan = list(cfg.fanouts)
+    R = cfg.row_bytes
+    B = cfg.B
+    stream = torch.cuda.current_stream()
+
+    # first pass: sizes and buffers (outside the timed region)
+    sr = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed)
+    ws_s = torch.empty(dg._L.dg_sample_workspace_bytes(cfg.n, B, sr.nodes.shape[1],
+                                                       sr.edge_src.shape[1]),
+                       dtype=torch.uint8, device=dev)
+    counts = sr.node_count.copy()
+    pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts)
+    ws_p = torch.empty(dg._L.dg_pack_workspace_bytes(cfg.n, B, int(counts.sum())),
+                       dtype=torch.uint8, device=dev)
+    nmax = int(counts.max())
+    ybuf = [torch.empty((nmax, R), dtype=torch.uint8, device=dev) for _ in range(2)]
+    sizes_s, sizes_p = dict(sr.sizes), dict(pr.sizes)
+    log(f"sizes: nodes/batch max {sizes_s['max_batch_nodes']:,} total {sizes_s['total_nodes']:,} "
+        f"edges {sizes_s['total_edges']:,} packed rows {sizes_p['packed_rows']:,} "
+        f"|U| {sizes_p['unique_nodes']:,} |U_nc| {sizes_p['unique_packed']:,}")
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(B)]
+
+    def step(record):
+        s_out = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, out=sr,
+                                workspace=ws_s, timing=record)
+        p_out = dg.pack_group(w.feats, w.cache_slot, s_out.nodes, counts, out=pr,
+                              workspace=ws_p, timing=record)
+        for b in range(B):
+            n = int(counts[b])
+            if record:
+                ev[b][0].record(stream)
+            dg.assemble_batch(w.cache, p_out.chunk(b), p_out.loc[b, :n], R, out=ybuf[b & 1],
+                              stream=stream)
+            if record:
+                ev[b][1].record(stream)
+        return s_out, p_out
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+
+    # timed region: K whole steps
+    samp_ms, gather_ms, pack_ms, asm_ms, sample_total_ms = [], [], [], [], []
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        s_out, p_out = step(True)
+        samp_ms.append(s_out.timing["total_ms"])
+        pack_ms.append(p_out.timing["total_ms"])
+        gather_ms.append(p_out.timing["gather_ms"])
+        torch.cuda.synchronize()
+        asm_ms.append(sum(a.elapsed_time(b) for a, b in ev))
+    torch.cuda.synchronize()
+    t_total = time.perf_counter() - t_start
+    if s_out.sizes != sizes_s or p_out.sizes != sizes_p:
+        raise RuntimeError("sizes changed between steps")
+
+    Uc = sizes_p["unique_packed"]
+    P = sizes_p["packed_rows"]
+    n_pairs = sizes_s["total_nodes"]
+    F_pack = R * (Uc + P)
+    F_asm = 2 * R * n_pairs
+    F = F_pack + F_asm
+    ms_step = 1e3 * t_total / args.steps
+    value = F * args.steps / t_total / 1e9
+    g_ms = float(np.mean(gather_ms))
+    achieved = F_pack / (g_ms * 1e-3) / 1e9
+    edges = sizes_s["total_edges"]
+    traffic = load_traffic(cfg.name, "fanout_gather")
+
+    out = {
+        "metric": "packed+assembled feature GB/s (and % HBM peak); sampled edges/s, 1 MI355X",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "nodes": cfg.n, "edges": w.num_edges,
+                   "rmat_draws": cfg.draws, "feature": f"{cfg.dim}x{str(cfg.dtype)[6:]}",
+                   "row_bytes": R, "batches": B, "seeds_per_batch": cfg.S, "fanouts": fan,
+                   "cache_rows": int(w.cache_nodes.numel()), "parallelism": "single-gpu"},
+        "frac_hbm_peak": round(value / HBM_PEAK_GBPS, 4),
+        "sampled_edges_per_s": round(edges / (np.mean(samp_ms) * 1e-3), 1),
+        "phases_ms": {"sample": round(float(np.mean(samp_ms)), 3),
+                      "pack": round(float(np.mean(pack_ms)), 3),
+                      "fanout_gather": round(g_ms, 3),
+                      "assemble_all_batches": round(float(np.mean(asm_ms)), 3)},
+        "phase_gbps": {"pack_call": round(F_pack / (np.mean(pack_ms) * 1e-3) / 1e9, 1),
+                       "assemble_kernels": round(F_asm / (np.mean(asm_ms) * 1e-3) / 1e9, 1)},
+        "sizes": {"total_nodes": n_pairs, "total_edges": edges, "packed_rows": P,
+                  "unique_nodes": sizes_p["unique_nodes"], "unique_packed": Uc},
+        "roofline": {"kernel": "k_fanout16 (fan-out gather)", "bound": "hbm",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                     "algorithmic_bytes": F_pack},
+    }
+
+    if args.copy_calib:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, cfg, args.cpu_batches)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(w, cfg, nb):
+    """The oracle (single-threaded C) timed on the host on a bounded sample of
+    the same workload: the first `nb` mini-batches of the group, on the full
+    graph and full feature table."""
+    import numpy as np
+
+    import oracle
+
+    t0 = time.perf_counter()
+    log("cpu baseline: copying graph and features to host")
+    off = w.offsets.cpu().numpy()
+    idx = w.indices.cpu().numpy()
+    seeds = w.seeds[:nb].cpu().numpy()
+    X = w.feats.cpu().numpy()
+    slot = w.cache_slot.cpu().numpy()
+    cache = w.cache.cpu().numpy()
+    log(f"host copies in {time.perf_counter() - t0:.1f}s; running the oracle on {nb} batches")
+    R = cfg.row_bytes
+    t1 = time.perf_counter()
+    rs = oracle.sample_group(off, idx, seeds, list(cfg.fanouts), w.rng_seed)
+    t2 = time.perf_counter()
+    rp = oracle.pack_group(X, slot, rs["nodes"], with_unique=False)
+    t3 = time.perf_counter()
+    for b in range(nb):
+        lo, hi = rp["packed_ptr"][b], rp["packed_ptr"][b + 1]
+        oracle.assemble_batch(cache, rp["packed"][lo:hi], rp["loc"][b], R)
+    t4 = time.perf_counter()
+    pairs = sum(len(x) for x in rs["nodes"])
+    edges = sum(len(x) for x in rs["edge_src"])
+    F = R * (rp["unique_packed"] + rp["packed_rows"]) + 2 * R * pairs
+    return {"value": round(F / (t4 - t1) / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {nb} of {cfg.B} mini-batches of {cfg.name} (full graph and feature "
+                      f"table), sample+pack+assemble, single-threaded C",
+            "seconds": {"sample": round(t2 - t1, 3), "pack": round(t3 - t2, 3),
+                        "assemble": round(t4 - t3, 3)},
+            "sampled_edges_per_s": round(edges / (t2 - t1), 1)}
+
+
+if __name__ == "__main__":
+    main()

@@ -93,7 +93,7 @@ def sampler_seed(seed: int) -> int:
 
 
 # --------------------------------------------------------------- permutations
-def feistel_permute(x: torch.Tensor, n: int, key: int, rounds: int = 6) -> torch.Tensor:
+def feistel_permute(x: torch.Tensor, n: int, key: int, rounds: int = 4) -> torch.Tensor:
     """Keyed bijection of [0, n) (balanced Feistel network over an even number
     of bits, with cycle walking back into [0, n)).  x: int64 values in [0, n)."""
     bits = max(2, math.ceil(math.log2(max(n, 2))))
@@ -110,10 +110,11 @@ def feistel_permute(x: torch.Tensor, n: int, key: int, rounds: int = 6) -> torch
         return (L << half) | R
 
     y = enc(x)
-    out_of_range = y >= n
-    while bool(out_of_range.any()):
-        y = torch.where(out_of_range, enc(y), y)
-        out_of_range = y >= n
+    walk = torch.nonzero(y >= n).squeeze(1)
+    while walk.numel():  # cycle walking: re-encrypt only the values still outside
+        z = enc(y[walk])
+        y[walk] = z
+        walk = walk[z >= n]
     return y
 
 
@@ -151,13 +152,15 @@ def uniform_graph(n: int, dmin: int, dmax: int, seed: int):
 def rmat_edges(n: int, draws: int, a: float, b: float, c: float, seed: int,
                device="cpu", chunk: int = 1 << 26) -> torch.Tensor:
     """R-MAT edge draws (Chakrabarti, Zhan & Faloutsos, SDM 2004) at scale
-    ceil(log2 n); a draw with an endpoint >= n is redrawn.  Endpoints are then
-    relabelled by a keyed permutation (hubs scattered over the ID range).
-    Returns int64 keys src*n + dst of the distinct non-loop edges, ascending."""
+    ceil(log2 n); each level's quadrant comes from a 16-bit slice of a 64-bit
+    counter hash (four levels per hash); a draw with an endpoint >= n is
+    redrawn.  Endpoints are then relabelled by a keyed permutation (hubs
+    scattered over the ID range).  Returns int64 keys src*n + dst of the
+    distinct non-loop edges, ascending."""
     scale = max(1, math.ceil(math.log2(n)))
     key = stream_key(seed, STREAM_GRAPH)
     rkey = stream_key(seed, STREAM_RELABEL)
-    ta, tb, tc = (int(round(p * 2**32)) for p in (a, a + b, a + b + c))
+    ta, tb, tc = (int(round(p * 2**16)) for p in (a, a + b, a + b + c))
     keys = []
     for start in range(0, draws, chunk):
         m = min(chunk, draws - start)
@@ -170,7 +173,9 @@ def rmat_edges(n: int, draws: int, a: float, b: float, c: float, seed: int,
             s = torch.zeros_like(ee)
             d = torch.zeros_like(ee)
             for lvl in range(scale):
-                r = hash_u32(key, (ee << 11) | (lvl << 6) | attempt)
+                if lvl % 4 == 0:
+                    h = fmix64(((ee << 9) | ((lvl // 4) << 6) | attempt) * _INC + _s64(key))
+                r = (h >> (16 * (lvl % 4))) & 0xFFFF
                 s = (s << 1) | (r >= tb).long()
                 d = (d << 1) | (((r >= ta) & (r < tb)) | (r >= tc)).long()
             src[todo] = s
@@ -210,13 +215,32 @@ def rmat_graph(n, draws, a, b, c, seed, device="cpu"):
 
 
 # --------------------------------------------------------------- other inputs
-def seed_batches(n: int, B: int, S: int, seed: int, device="cpu") -> torch.Tensor:
-    """B x S seed nodes drawn without replacement: the first B*S values of a
-    keyed permutation of [0, n), split consecutively into batches."""
-    if B * S > n:
-        raise ValueError("more seeds than nodes")
-    i = torch.arange(B * S, dtype=torch.int64, device=device)
-    return feistel_permute(i, n, stream_key(seed, STREAM_SEEDS)).to(torch.int32).reshape(B, S)
+def seed_batches(n: int, B: int, S: int, seed: int, device="cpu", offsets=None) -> torch.Tensor:
+    """B x S seed nodes drawn without replacement: a keyed permutation of
+    [0, n) is walked in order and the first B*S nodes with at least one
+    out-neighbour are kept (seeds are training nodes, which in the paper's
+    datasets sit in the graph's connected part); they are split consecutively
+    into batches.  Without `offsets` every node is eligible."""
+    key = stream_key(seed, STREAM_SEEDS)
+    need = B * S
+    if offsets is None:
+        if need > n:
+            raise ValueError("more seeds than nodes")
+        i = torch.arange(need, dtype=torch.int64, device=device)
+        return feistel_permute(i, n, key).to(torch.int32).reshape(B, S)
+    deg = offsets[1:] - offsets[:-1]
+    out, have, start = [], 0, 0
+    step = max(4 * need, 1 << 16)
+    while have < need:
+        if start >= n:
+            raise ValueError("fewer nodes with out-neighbours than seeds")
+        i = torch.arange(start, min(n, start + step), dtype=torch.int64, device=device)
+        v = feistel_permute(i, n, key)
+        v = v[deg[v] > 0]
+        out.append(v[:need - have])
+        have += out[-1].numel()
+        start += step
+    return torch.cat(out).to(torch.int32).reshape(B, S)
 
 
 def features(n: int, dim: int, dtype, seed: int, device="cpu", chunk_rows: int = 1 << 22):
@@ -328,7 +352,9 @@ def make_workload(name_or_cfg, device="cpu", feats=True, cache_pct=None, feats_d
     table on `feats_device` (default: `device`)."""
     cfg = CONFIGS[name_or_cfg] if isinstance(name_or_cfg, str) else name_or_cfg
     off, idx = make_graph(cfg, device)
-    seeds = seed_batches(cfg.n, cfg.B, cfg.S, cfg.seed, device)
+    if torch.device(device).type == "cuda":
+        torch.cuda.empty_cache()  # give generation temporaries back before the feature table
+    seeds = seed_batches(cfg.n, cfg.B, cfg.S, cfg.seed, device, offsets=off)
     w = Workload(cfg, off, idx, seeds, rng_seed=sampler_seed(cfg.seed))
     if feats:
         fd = feats_device or device

@@ -1,0 +1,136 @@
+"""Parity on the named workloads, in the launch configuration bench.py times.
+
+M1 (1M nodes) compares every integer output with the oracle and every row on
+the device.  The full-size workloads (L100, W120, H65 at three cache shares)
+compare, against the oracle: the sampled lists of the first and last
+mini-batch (an oracle run over those batches alone, with their global batch
+numbers) and every packing table of the whole group (U, P_b order,
+packed_ptr, address tables); feature rows are checked on the device against
+an independent library gather (torch.index_select) of the feature table, for
+every packed row and every assembled row."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module")
+def dg():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2405_05231_amd as m
+    return m
+
+
+def rows_equal(a: torch.Tensor, b: torch.Tensor) -> bool:
+    return torch.equal(a.view(torch.uint8).reshape(a.shape[0], -1),
+                       b.contiguous().view(torch.uint8).reshape(b.shape[0], -1))
+
+
+def check_rows_on_device(X, ids, got, chunk=1 << 20):
+    """got[i] == X[ids[i]] bitwise, in chunks."""
+    for lo in range(0, ids.numel(), chunk):
+        hi = min(ids.numel(), lo + chunk)
+        ref = X.index_select(0, ids[lo:hi].long())
+        assert rows_equal(got[lo:hi], ref), (lo, hi)
+
+
+def run_and_check(dg, orc, w, oracle_batches):
+    cfg = w.cfg
+    fan = list(cfg.fanouts)
+    R = cfg.row_bytes
+    sr = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed)
+    counts = sr.node_count.copy()
+    pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, with_unique=True)
+    torch.cuda.synchronize()
+    print(f"[{cfg.name}] nodes {sr.sizes['total_nodes']:,} edges {sr.sizes['total_edges']:,} "
+          f"packed {pr.sizes['packed_rows']:,} U {pr.sizes['unique_nodes']:,}", flush=True)
+
+    # sampling: oracle on selected batches (same global batch numbers)
+    off = w.offsets.cpu().numpy()
+    idx = w.indices.cpu().numpy()
+    for b in oracle_batches:
+        ref = orc.sample_group(off, idx, w.seeds[b:b + 1].cpu().numpy(), fan, w.rng_seed,
+                               batch_base=b)
+        n, e = int(sr.hop_ptr[b, -1]), int(sr.edge_ptr[b, -1])
+        assert np.array_equal(sr.hop_ptr[b], ref["hop_ptr"][0]), b
+        assert np.array_equal(sr.edge_ptr[b], ref["edge_ptr"][0]), b
+        assert np.array_equal(sr.nodes[b, :n].cpu().numpy(), ref["nodes"][0]), b
+        assert np.array_equal(sr.edge_src[b, :e].cpu().numpy(), ref["edge_src"][0]), b
+        assert np.array_equal(sr.edge_dst[b, :e].cpu().numpy(), ref["edge_dst"][0]), b
+    del off, idx
+
+    # packing tables of the whole group: oracle over the device's node lists
+    lists = [sr.nodes[b, :int(counts[b])].cpu().numpy() for b in range(cfg.B)]
+    refp = orc.pack_group(None, w.cache_slot.cpu().numpy(), lists, rows=False, row_bytes=R)
+    rows = refp["packed_rows"]
+    assert pr.sizes["packed_rows"] == rows
+    assert pr.sizes["unique_nodes"] == refp["unique_nodes"]
+    assert pr.sizes["unique_packed"] == refp["unique_packed"]
+    assert np.array_equal(pr.packed_ptr_host, refp["packed_ptr"])
+    assert np.array_equal(pr.packed_ids[:rows].cpu().numpy(), refp["packed_ids"])
+    assert np.array_equal(pr.unique[:refp["unique_nodes"]].cpu().numpy(), refp["unique"])
+    for b in range(cfg.B):
+        assert np.array_equal(pr.loc[b, :int(counts[b])].cpu().numpy(), refp["loc"][b]), b
+    # rows
+    check_rows_on_device(w.feats, pr.packed_ids[:rows], pr.packed[:rows].view(w.feats.dtype)
+                         .reshape(rows, -1))
+    out = torch.empty((int(counts.max()), R), dtype=torch.uint8, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    for b in range(cfg.B):
+        n = int(counts[b])
+        y = dg.assemble_batch(w.cache, pr.chunk(b), pr.loc[b, :n], R, out=out, status=status)
+        check_rows_on_device(w.feats, sr.nodes[b, :n], y[:n].view(w.feats.dtype).reshape(n, -1))
+    assert int(status.item()) == 0
+    return sr, pr
+
+
+def test_workload_M1_full(dg, orc):
+    w = synth.make_workload("M1", device=DEV)
+    sr, pr = run_and_check(dg, orc, w, oracle_batches=range(w.cfg.B))
+    # every row also against the oracle's own copies on a few batches
+    X = w.feats.cpu().numpy()
+    lists = [sr.nodes[b, :int(sr.hop_ptr[b, -1])].cpu().numpy() for b in (0, 1)]
+    refp = orc.pack_group(X, w.cache_slot.cpu().numpy(), lists)
+    cache = w.cache.cpu().numpy()
+    for b in (0, 1):
+        lo, hi = refp["packed_ptr"][b], refp["packed_ptr"][b + 1]
+        y_ref = orc.assemble_batch(cache, refp["packed"][lo:hi], refp["loc"][b], w.cfg.row_bytes)
+        n = len(lists[b])
+        y = dg.assemble_batch(w.cache, pr.chunk(b), pr.loc[b, :n], w.cfg.row_bytes)
+        assert np.array_equal(y.cpu().numpy(), y_ref)
+
+
+def big(name, cache_pct=None):
+    w = synth.make_workload(name, device=DEV, cache_pct=cache_pct)
+    torch.cuda.synchronize()
+    return w
+
+
+@pytest.mark.big
+@pytest.mark.timeout(900)
+def test_workload_L100(dg, orc):
+    w = big("L100")
+    run_and_check(dg, orc, w, oracle_batches=(0, w.cfg.B - 1))
+
+
+@pytest.mark.big
+@pytest.mark.timeout(900)
+def test_workload_W120(dg, orc):
+    w = big("W120")
+    run_and_check(dg, orc, w, oracle_batches=(0, w.cfg.B - 1))
+
+
+@pytest.mark.big
+@pytest.mark.timeout(1200)
+def test_workload_H65_cache_sweep(dg, orc):
+    w = big("H65", cache_pct=0)
+    for pct in synth.CONFIGS["H65"].cache_pct:
+        synth.set_cache(w, pct)
+        print(f"[H65] cache {pct}%", flush=True)
+        run_and_check(dg, orc, w, oracle_batches=(0, w.cfg.B - 1) if pct == 0 else ())
+        torch.cuda.empty_cache()

@@ -61,3 +61,17 @@ def test_tiny_workload_is_deterministic():
     assert torch.equal(a.seeds, b.seeds) and torch.equal(a.feats, b.feats)
     assert a.cache.shape == (1000, 16)
     assert torch.equal(a.cache, a.feats[a.cache_nodes])
+
+
+def test_seeds_skip_isolated_nodes():
+    n = 3000
+    off, idx = synth.rmat_graph(n, 20_000, 0.57, 0.19, 0.19, 0)
+    deg = off[1:] - off[:-1]
+    assert int((deg == 0).sum()) > 0
+    s = synth.seed_batches(n, 4, 100, 0, offsets=off)
+    assert s.unique().numel() == 400
+    assert bool((deg[s.long()] > 0).all())
+    # with every node eligible the walk is the plain keyed permutation
+    full = torch.ones(n + 1, dtype=torch.int64).cumsum(0) - 1
+    assert torch.equal(synth.seed_batches(n, 4, 100, 0, offsets=full),
+                       synth.seed_batches(n, 4, 100, 0))
