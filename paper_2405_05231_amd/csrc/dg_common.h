@@ -59,10 +59,21 @@ __device__ __forceinline__ T wave_incl_sum(T x) {
   return x;
 }
 
-__device__ __forceinline__ uint64_t wave_or(uint64_t x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x |= __shfl_xor(x, o, 64);
-  return x;
+// Wave-wide OR / inclusive sum through the device library's DPP reductions
+// (no LDS round trip).
+extern "C" __device__ uint64_t __ockl_wfred_or_u64(uint64_t);
+extern "C" __device__ int32_t __ockl_wfscan_add_i32(int32_t, bool inclusive);
+
+__device__ __forceinline__ uint64_t wave_or(uint64_t x) { return __ockl_wfred_or_u64(x); }
+__device__ __forceinline__ int32_t wave_incl_sum_i32(int32_t x) {
+  return __ockl_wfscan_add_i32(x, true);
+}
+
+// Value of x in lane `src`, where src is the same in every lane (v_readlane).
+__device__ __forceinline__ int64_t read_lane(int64_t x, int src) {
+  uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, src);
+  uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)x >> 32), src);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
 // Binary search over a non-decreasing prefix array p[0..n] (p[0] = 0): the
@@ -87,12 +98,18 @@ int scan_exclusive(const int64_t *in, int64_t *out, int64_t n, int64_t *tile_sum
 
 // ---------------------------------------------------------------- mask compaction
 // A node-major membership mask: bit b of mask[u] says that node u belongs to
-// mini-batch b.  One tile of MC_TILE consecutive nodes per thread block.
-constexpr int MC_THREADS = 256;
+// mini-batch b.  A block of MC_WAVES waves owns MC_BLOCK_NODES consecutive
+// nodes; wave w owns the w-th run of MC_TILE of them, and round r of a wave
+// covers nodes tile0 + r*64 + lane, so (wave, round, lane) order is node order.
+constexpr int MC_WAVES = 4;
+constexpr int MC_THREADS = 64 * MC_WAVES;
 constexpr int MC_ROUNDS = 16;
-constexpr int MC_TILE = MC_THREADS * MC_ROUNDS;
+constexpr int MC_TILE = 64 * MC_ROUNDS;
+constexpr int MC_BLOCK_NODES = MC_TILE * MC_WAVES;
+constexpr int MC_CHUNK = 64;  // blocks per chunk of the row scan
 
-inline int64_t mc_blocks(int64_t N) { return (N + MC_TILE - 1) / MC_TILE; }
+__host__ __device__ inline int64_t mc_blocks(int64_t N) { return (N + MC_BLOCK_NODES - 1) / MC_BLOCK_NODES; }
+__host__ __device__ inline int64_t mc_chunks(int64_t nblk) { return (nblk + MC_CHUNK - 1) / MC_CHUNK; }
 
 // Count-matrix rows: [0,B) per batch (non-cached members), then:
 __host__ __device__ inline int row_all(int B) { return B; }        // nodes with any bit set (U)
@@ -105,10 +122,11 @@ struct MaskScan {
   const int32_t *cache_slot;  // nullable: no node is cached
   int64_t N;
   int B;
-  int64_t nblk;
-  uint32_t *cnt;    // [rows * nblk]
-  int64_t *base;    // [rows * nblk]  exclusive scans along each row
-  int64_t *totals;  // [rows]
+  int64_t nblk;        // blocks of MC_BLOCK_NODES nodes
+  uint32_t *cnt;       // [nblk][rows] per-block counts
+  int64_t *base;       // [nblk][rows] exclusive scans down each row
+  int64_t *chunk_sum;  // [chunks][rows]
+  int64_t *totals;     // [rows]
   uint32_t *err;
   // write pass (each output nullable)
   int64_t seg_base[DG_MAX_BATCHES];  // start index of batch b's list in seg_out

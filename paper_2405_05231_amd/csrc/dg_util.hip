@@ -153,72 +153,146 @@ size_t mask_scan_ws_bytes(int64_t N, int B) {
 
 void mask_scan_carve(MaskScan &m, Carve &c) {
   m.nblk = mc_blocks(m.N);
-  size_t cells = (size_t)mc_rows(m.B) * (size_t)m.nblk;
-  m.cnt = c.take<uint32_t>(cells);
-  m.base = c.take<int64_t>(cells);
-  m.totals = c.take<int64_t>((size_t)mc_rows(m.B));
+  size_t rows = (size_t)mc_rows(m.B);
+  m.cnt = c.take<uint32_t>(rows * (size_t)m.nblk);
+  m.base = c.take<int64_t>(rows * (size_t)m.nblk);
+  m.chunk_sum = c.take<int64_t>(rows * (size_t)mc_chunks(m.nblk));
+  m.totals = c.take<int64_t>(rows);
 }
 
-// Count pass: for each tile, the number of members of every batch (non-cached
-// only), of U, of U_nc, and of U_nc's (node, batch) pairs.
-__global__ __launch_bounds__(MC_THREADS) void k_mask_count(MaskScan a) {
-  __shared__ uint32_t s_cnt[DG_MAX_BATCHES + 3];
-  const int B = a.B, rows = mc_rows(B);
-  for (int i = threadIdx.x; i < rows; i += MC_THREADS) s_cnt[i] = 0;
-  __syncthreads();
-  const int lane = lane_id();
-  const int64_t t0 = (int64_t)blockIdx.x * MC_TILE;
+// Tile loads: all MC_ROUNDS mask words (and the cached flags of non-empty
+// ones) are requested before any is used, so a wave keeps 16 loads in flight.
+struct TileBits {
+  uint64_t m[MC_ROUNDS];
+  uint32_t cached;  // bit r: node of round r is cached
+};
+
+__device__ __forceinline__ void load_tile(const MaskScan &a, int64_t t0, int lane, TileBits &t,
+                                          bool check_slots) {
+#pragma unroll
   for (int r = 0; r < MC_ROUNDS; ++r) {
-    int64_t u = t0 + (int64_t)r * MC_THREADS + threadIdx.x;
-    uint64_t m = u < a.N ? a.mask[u] : 0ull;
+    int64_t u = t0 + r * 64 + lane;
+    t.m[r] = u < a.N ? a.mask[u] : 0ull;
+  }
+  t.cached = 0;
+  if (a.cache_slot) {
+    int32_t sl[MC_ROUNDS];
+#pragma unroll
+    for (int r = 0; r < MC_ROUNDS; ++r)
+      sl[r] = t.m[r] ? a.cache_slot[t0 + r * 64 + lane] : -1;
+#pragma unroll
+    for (int r = 0; r < MC_ROUNDS; ++r) {
+      if (check_slots && sl[r] < -1) atomicOr(a.err, ERR_CACHE_SLOT);
+      t.cached |= (sl[r] >= 0 ? 1u : 0u) << r;
+    }
+  }
+}
+
+// Per-wave counts of one tile: lane b returns batch b's non-cached members;
+// *cu, *cnc, *cp (wave-uniform) get the members of U, of U_nc and U_nc's pairs.
+__device__ __forceinline__ uint32_t tile_counts(const TileBits &t, int lane, uint32_t *cu,
+                                                uint32_t *cnc, uint32_t *cp) {
+  uint32_t mine = 0, u = 0, nc = 0, p = 0;
+#pragma unroll
+  for (int r = 0; r < MC_ROUNDS; ++r) {
+    uint64_t m = t.m[r];
     uint64_t any = __ballot(m != 0ull);
     if (any == 0ull) continue;  // wave-uniform
-    bool cached = false;
-    if (m != 0ull && a.cache_slot) {
-      int32_t sl = a.cache_slot[u];
-      if (sl < -1) atomicOr(a.err, ERR_CACHE_SLOT);
-      cached = sl >= 0;
-    }
-    uint64_t mnc = cached ? 0ull : m;
-    uint64_t anync = __ballot(mnc != 0ull);
-    if (lane == 0) {
-      atomicAdd(&s_cnt[row_all(B)], (uint32_t)__popcll(any));
-      atomicAdd(&s_cnt[row_packed(B)], (uint32_t)__popcll(anync));
-    }
+    uint64_t mnc = ((t.cached >> r) & 1u) ? 0ull : m;
+    u += (uint32_t)__popcll(any);
+    nc += (uint32_t)__popcll(__ballot(mnc != 0ull));
     uint64_t uni = wave_or(mnc);
     while (uni) {
       int b = __ffsll((long long)uni) - 1;
       uni &= uni - 1;
-      uint64_t bal = __ballot((mnc >> b) & 1ull);
-      if (lane == 0) atomicAdd(&s_cnt[b], (uint32_t)__popcll(bal));
+      uint32_t c = (uint32_t)__popcll(__ballot((mnc >> b) & 1ull));
+      p += c;
+      if (lane == b) mine += c;
     }
   }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t pairs = 0;
-    for (int b = 0; b < B; ++b) pairs += s_cnt[b];
-    s_cnt[row_pairs(B)] = pairs;
-  }
-  __syncthreads();
-  for (int i = threadIdx.x; i < rows; i += MC_THREADS)
-    a.cnt[(size_t)i * a.nblk + blockIdx.x] = s_cnt[i];
+  *cu = u;
+  *cnc = nc;
+  *cp = p;
+  return mine;
 }
 
-// One block per row: exclusive scan of the row's per-tile counts.
-__global__ __launch_bounds__(1024) void k_mask_rows(MaskScan a) {
+// Stores one wave's counts into its LDS row (rows = B + 3).
+__device__ __forceinline__ void stash_counts(uint32_t *row, int B, int lane, uint32_t mine,
+                                             uint32_t cu, uint32_t cnc, uint32_t cp) {
+  if (lane < B) row[lane] = mine;
+  if (lane == 0) {
+    row[row_all(B)] = cu;
+    row[row_packed(B)] = cnc;
+    row[row_pairs(B)] = cp;
+  }
+}
+
+// Count pass: per block, the number of members of every batch (non-cached
+// only), of U, of U_nc, and of U_nc's (node, batch) pairs; stored as one
+// contiguous row per block.
+__global__ __launch_bounds__(MC_THREADS) void k_mask_count(MaskScan a) {
+  __shared__ uint32_t s_cnt[MC_WAVES][DG_MAX_BATCHES + 3];
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+  const int B = a.B, rows = mc_rows(B);
+  const int64_t t0 = (int64_t)blockIdx.x * MC_BLOCK_NODES + (int64_t)w * MC_TILE;
+  TileBits t;
+  load_tile(a, t0, lane, t, true);
+  uint32_t cu, cnc, cp;
+  uint32_t mine = tile_counts(t, lane, &cu, &cnc, &cp);
+  stash_counts(s_cnt[w], B, lane, mine, cu, cnc, cp);
+  __syncthreads();
+  for (int i = threadIdx.x; i < rows; i += MC_THREADS) {
+    uint32_t v = 0;
+#pragma unroll
+    for (int j = 0; j < MC_WAVES; ++j) v += s_cnt[j][i];
+    a.cnt[(size_t)blockIdx.x * rows + i] = v;
+  }
+}
+
+// Row scan, three phases over the [nblk][rows] count matrix: chunk sums,
+// scan of chunk sums down each row, then per-block bases.
+__global__ __launch_bounds__(128) void k_rows_chunk_sum(MaskScan a) {
+  const int rows = mc_rows(a.B);
+  const int t = threadIdx.x;
+  if (t >= rows) return;
+  const int64_t b0 = (int64_t)blockIdx.x * MC_CHUNK;
+  const int64_t n = a.nblk - b0 < MC_CHUNK ? a.nblk - b0 : MC_CHUNK;
+  int64_t acc = 0;
+#pragma unroll 16
+  for (int64_t i = 0; i < n; ++i) acc += a.cnt[(size_t)(b0 + i) * rows + t];
+  a.chunk_sum[(size_t)blockIdx.x * rows + t] = acc;
+}
+
+__global__ __launch_bounds__(1024) void k_rows_chunk_scan(MaskScan a) {
+  const int rows = mc_rows(a.B);
   const int row = blockIdx.x;
-  const uint32_t *c = a.cnt + (size_t)row * a.nblk;
-  int64_t *o = a.base + (size_t)row * a.nblk;
+  const int64_t nch = mc_chunks(a.nblk);
   int64_t carry = 0;
-  for (int64_t c0 = 0; c0 < a.nblk; c0 += 1024) {
-    int64_t i = c0 + threadIdx.x;
-    int64_t v = i < a.nblk ? (int64_t)c[i] : 0;
+  for (int64_t c0 = 0; c0 < nch; c0 += 1024) {
+    const int64_t i = c0 + threadIdx.x;
+    const int64_t v = i < nch ? a.chunk_sum[(size_t)i * rows + row] : 0;
     int64_t total;
-    int64_t ex = block_excl_scan<1024>(v, &total);
-    if (i < a.nblk) o[i] = carry + ex;
+    const int64_t ex = block_excl_scan<1024>(v, &total);
+    if (i < nch) a.chunk_sum[(size_t)i * rows + row] = carry + ex;
     carry += total;
   }
   if (threadIdx.x == 0) a.totals[row] = carry;
+}
+
+__global__ __launch_bounds__(128) void k_rows_apply(MaskScan a) {
+  const int rows = mc_rows(a.B);
+  const int t = threadIdx.x;
+  if (t >= rows) return;
+  const int64_t b0 = (int64_t)blockIdx.x * MC_CHUNK;
+  const int64_t n = a.nblk - b0 < MC_CHUNK ? a.nblk - b0 : MC_CHUNK;
+  int64_t run = a.chunk_sum[(size_t)blockIdx.x * rows + t];
+#pragma unroll 16
+  for (int64_t i = 0; i < n; ++i) {
+    const size_t at = (size_t)(b0 + i) * rows + t;
+    const int64_t v = a.cnt[at];
+    a.base[at] = run;
+    run += v;
+  }
 }
 
 int mask_scan_count(MaskScan &m, int64_t *host_totals, hipStream_t s) {
@@ -226,8 +300,11 @@ int mask_scan_count(MaskScan &m, int64_t *host_totals, hipStream_t s) {
     for (int i = 0; i < mc_rows(m.B); ++i) host_totals[i] = 0;
     return DG_OK;
   }
+  const unsigned nch = (unsigned)mc_chunks(m.nblk);
   hipLaunchKernelGGL(k_mask_count, dim3((unsigned)m.nblk), dim3(MC_THREADS), 0, s, m);
-  hipLaunchKernelGGL(k_mask_rows, dim3((unsigned)mc_rows(m.B)), dim3(1024), 0, s, m);
+  hipLaunchKernelGGL(k_rows_chunk_sum, dim3(nch), dim3(128), 0, s, m);
+  hipLaunchKernelGGL(k_rows_chunk_scan, dim3((unsigned)mc_rows(m.B)), dim3(1024), 0, s, m);
+  hipLaunchKernelGGL(k_rows_apply, dim3(nch), dim3(128), 0, s, m);
   DG_HIP(hipGetLastError());
   DG_HIP(hipMemcpyAsync(host_totals, m.totals, sizeof(int64_t) * mc_rows(m.B),
                         hipMemcpyDeviceToHost, s));
@@ -235,83 +312,71 @@ int mask_scan_count(MaskScan &m, int64_t *host_totals, hipStream_t s) {
   return DG_OK;
 }
 
-// Write pass.  Within a tile, round r covers nodes t0 + r*256 + [0,256), so
-// ascending (round, wave, lane) order is ascending node order; ranks come from
-// per-wave ballots plus the counts of earlier waves and rounds.
+// Write pass: every rank is the block's base from the row scan, plus the
+// counts of the block's earlier waves, plus the running counts of the wave's
+// earlier rounds (lane b holds batch b's), plus the ballot prefix within the
+// round.
 __global__ __launch_bounds__(MC_THREADS) void k_mask_write(MaskScan a) {
-  __shared__ int64_t s_run[DG_MAX_BATCHES + 3];
-  __shared__ int64_t s_w[MC_THREADS / 64][DG_MAX_BATCHES + 3];
-  const int B = a.B, rows = mc_rows(B);
+  __shared__ uint32_t s_cnt[MC_WAVES][DG_MAX_BATCHES + 3];
   const int lane = lane_id(), w = threadIdx.x >> 6;
-  for (int i = threadIdx.x; i < rows; i += MC_THREADS)
-    s_run[i] = a.base[(size_t)i * a.nblk + blockIdx.x];
-  const int64_t t0 = (int64_t)blockIdx.x * MC_TILE;
+  const int B = a.B, rows = mc_rows(B);
+  const int64_t t0 = (int64_t)blockIdx.x * MC_BLOCK_NODES + (int64_t)w * MC_TILE;
+  TileBits t;
+  load_tile(a, t0, lane, t, false);
+  {
+    uint32_t cu, cnc, cp;
+    uint32_t mine = tile_counts(t, lane, &cu, &cnc, &cp);
+    stash_counts(s_cnt[w], B, lane, mine, cu, cnc, cp);
+  }
+  __syncthreads();
+  const int64_t *bb = a.base + (size_t)blockIdx.x * rows;
+  auto before = [&](int row) {
+    int64_t v = 0;
+    for (int j = 0; j < w; ++j) v += s_cnt[j][row];
+    return v;
+  };
+  int64_t run_b = lane < B ? bb[lane] + before(lane) : 0;
+  const int64_t seg_b = lane < B ? a.seg_base[lane] : 0;
+  int64_t run_u = bb[row_all(B)] + before(row_all(B));
+  int64_t run_nc = bb[row_packed(B)] + before(row_packed(B));
+  int64_t run_p = bb[row_pairs(B)] + before(row_pairs(B));
+  const uint64_t lt = lanes_below();
+#pragma unroll
   for (int r = 0; r < MC_ROUNDS; ++r) {
-    for (int i = threadIdx.x; i < (MC_THREADS / 64) * rows; i += MC_THREADS)
-      s_w[i / rows][i % rows] = 0;
-    __syncthreads();
-    int64_t u = t0 + (int64_t)r * MC_THREADS + threadIdx.x;
-    uint64_t m = u < a.N ? a.mask[u] : 0ull;
-    uint64_t any = __ballot(m != 0ull);
-    uint64_t mnc = 0ull, anync = 0ull, uni = 0ull;
-    int64_t pc = 0, pincl = 0;
-    if (any != 0ull) {
-      bool cached = (m != 0ull && a.cache_slot) ? a.cache_slot[u] >= 0 : false;
-      mnc = cached ? 0ull : m;
-      anync = __ballot(mnc != 0ull);
-      pc = __popcll(mnc);
-      pincl = wave_incl_sum(pc);
-      uni = wave_or(mnc);
-      if (lane == 0) {
-        s_w[w][row_all(B)] = __popcll(any);
-        s_w[w][row_packed(B)] = __popcll(anync);
-      }
-      if (lane == 63) s_w[w][row_pairs(B)] = pincl;
-      uint64_t x = uni;
-      while (x) {
-        int b = __ffsll((long long)x) - 1;
-        x &= x - 1;
-        uint64_t bal = __ballot((mnc >> b) & 1ull);
-        if (lane == 0) s_w[w][b] = __popcll(bal);
-      }
+    const uint64_t m = t.m[r];
+    const uint64_t any = __ballot(m != 0ull);
+    if (any == 0ull) continue;  // wave-uniform
+    const int32_t u = (int32_t)(t0 + r * 64 + lane);
+    const uint64_t mnc = ((t.cached >> r) & 1u) ? 0ull : m;
+    if (m != 0ull && a.uniq_out) a.uniq_out[run_u + __popcll(any & lt)] = u;
+    run_u += __popcll(any);
+    const uint64_t anc = __ballot(mnc != 0ull);
+    const int32_t pc = __popcll(mnc);
+    const int32_t pincl = wave_incl_sum_i32(pc);
+    const int64_t pair0 = run_p + (pincl - pc);
+    if (mnc != 0ull) {
+      const int64_t rk = run_nc + __popcll(anc & lt);
+      if (a.unc_ids) a.unc_ids[rk] = u;
+      if (a.unc_off) a.unc_off[rk] = pair0;
+      if (a.nodeoff) a.nodeoff[u] = pair0;
     }
-    __syncthreads();
-    if (any != 0ull) {
-      const uint64_t lt = lanes_below();
-      auto wave_base = [&](int row) {
-        int64_t v = s_run[row];
-        for (int i = 0; i < w; ++i) v += s_w[i][row];
-        return v;
-      };
-      if (m != 0ull && a.uniq_out)
-        a.uniq_out[wave_base(row_all(B)) + __popcll(any & lt)] = (int32_t)u;
-      int64_t pair0 = wave_base(row_pairs(B)) + (pincl - pc);
-      if (mnc != 0ull) {
-        int64_t rk = wave_base(row_packed(B)) + __popcll(anync & lt);
-        if (a.unc_ids) a.unc_ids[rk] = (int32_t)u;
-        if (a.unc_off) a.unc_off[rk] = pair0;
-        if (a.nodeoff) a.nodeoff[u] = pair0;
+    run_nc += __popcll(anc);
+    run_p += __builtin_amdgcn_readlane(pincl, 63);
+    uint64_t uni = wave_or(mnc);
+    while (uni) {
+      const int b = __ffsll((long long)uni) - 1;
+      uni &= uni - 1;
+      const uint64_t bal = __ballot((mnc >> b) & 1ull);
+      const int64_t rb = read_lane(run_b, b);
+      const int64_t sb = read_lane(seg_b, b);
+      if ((mnc >> b) & 1ull) {
+        const int64_t dest = sb + rb + __popcll(bal & lt);
+        if (a.seg_out) a.seg_out[dest] = u;
+        if (a.pairdest) a.pairdest[pair0 + __popcll(mnc & ((1ull << b) - 1ull))] = dest;
       }
-      uint64_t x = uni;
-      while (x) {
-        int b = __ffsll((long long)x) - 1;
-        x &= x - 1;
-        uint64_t bal = __ballot((mnc >> b) & 1ull);
-        if ((mnc >> b) & 1ull) {
-          int64_t dest = a.seg_base[b] + wave_base(b) + __popcll(bal & lt);
-          if (a.seg_out) a.seg_out[dest] = (int32_t)u;
-          if (a.pairdest) a.pairdest[pair0 + __popcll(mnc & ((1ull << b) - 1ull))] = dest;
-        }
-      }
-      if (a.clear && m != 0ull) a.mask[u] = 0ull;
+      if (lane == b) run_b += __popcll(bal);
     }
-    __syncthreads();
-    for (int i = threadIdx.x; i < rows; i += MC_THREADS) {
-      int64_t add = 0;
-      for (int j = 0; j < MC_THREADS / 64; ++j) add += s_w[j][i];
-      s_run[i] += add;
-    }
-    __syncthreads();
+    if (a.clear && m != 0ull) a.mask[t0 + r * 64 + lane] = 0ull;
   }
 }
 
