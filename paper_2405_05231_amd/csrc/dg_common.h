@@ -18,6 +18,7 @@ enum : uint32_t {
   ERR_NBR_RANGE = 1u << 3,   // a neighbour ID outside [0, N)
   ERR_CACHE_SLOT = 1u << 4,  // cache_slot[v] < -1
   ERR_ROW_RANGE = 1u << 5,   // an address-table entry outside its table
+  ERR_INTERNAL = 1u << 6,    // an internal table overflowed (a library bug)
 };
 
 int set_error(int status, const char *fmt, ...);
@@ -85,6 +86,56 @@ __device__ __forceinline__ int find_batch(const int64_t *p, int n, int64_t i) {
     if (p[mid] <= i) lo = mid; else hi = mid;
   }
   return lo;
+}
+
+// ---------------------------------------------------------------- local-index table
+// (node u, batch b) -> local index j of u in batch b's node list.  Open
+// addressing with linear probing over 2^bits 64-bit slots; an entry is
+// key << LT_VALUE_BITS | j with key = u*64 + b + 1 (never 0, so 0 = empty).
+// Sized for a load factor of at most 1/2, so probes end quickly.
+constexpr int LT_VALUE_BITS = 27;
+constexpr int64_t LT_MAX_VALUE = (1ll << LT_VALUE_BITS) - 1;
+
+struct LocalTable {
+  uint64_t *slots;
+  int bits;
+};
+
+__host__ __device__ inline uint64_t lt_key(int32_t u, int b) {
+  return (((uint64_t)(uint32_t)u << 6) | (uint64_t)b) + 1ull;
+}
+__device__ __forceinline__ uint64_t lt_slot(const LocalTable &t, uint64_t key) {
+  return (key * 0x9E3779B97F4A7C15ull) >> (64 - t.bits);  // Fibonacci hashing
+}
+// Returns false only if the table is full (cannot happen at the sizes used).
+__device__ __forceinline__ bool lt_insert(const LocalTable &t, int32_t u, int b, int64_t j) {
+  const uint64_t key = lt_key(u, b);
+  const uint64_t e = (key << LT_VALUE_BITS) | (uint64_t)j;
+  const uint64_t m = (1ull << t.bits) - 1ull;
+  uint64_t s = lt_slot(t, key);
+  for (uint64_t probe = 0; probe <= m; ++probe, s = (s + 1) & m) {
+    unsigned long long old =
+        atomicCAS((unsigned long long *)&t.slots[s], 0ull, (unsigned long long)e);
+    if (old == 0ull) return true;
+  }
+  return false;
+}
+// Local index of (u, b), or -1 if absent.
+__device__ __forceinline__ int64_t lt_find(const LocalTable &t, int32_t u, int b) {
+  const uint64_t key = lt_key(u, b);
+  const uint64_t m = (1ull << t.bits) - 1ull;
+  uint64_t s = lt_slot(t, key);
+  for (uint64_t probe = 0; probe <= m; ++probe, s = (s + 1) & m) {
+    const uint64_t e = t.slots[s];
+    if (e == 0ull) return -1;
+    if ((e >> LT_VALUE_BITS) == key) return (int64_t)(e & (uint64_t)LT_MAX_VALUE);
+  }
+  return -1;
+}
+inline int lt_bits_for(int64_t entries) {
+  int bits = 10;
+  while ((1ll << bits) < 2 * entries) ++bits;
+  return bits;
 }
 
 // ---------------------------------------------------------------- fill / scan

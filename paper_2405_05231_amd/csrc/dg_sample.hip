@@ -5,8 +5,10 @@
 // in mini-batch b) and fresh[u] (bit b = u joined b at the current hop).  A hop
 // is: degree pass over the frontier -> exclusive scan (edge slots) -> draw +
 // mark (atomicOr on visited/fresh) -> mask compaction of fresh into each
-// batch's new segment, ascending, with no sort.  Local IDs are assigned at the
-// end through a (node, batch) pair table built from the final mask.
+// batch's new segment, ascending, with no sort.  Each node's local index is
+// recorded in a (node, batch) hash table when it joins a batch (seed
+// initialisation, each hop's compaction); sampled neighbours are relabelled
+// from global to local IDs through it at the end.
 #include <string.h>
 
 #include "dg_common.h"
@@ -46,7 +48,7 @@ struct Lists {
 __global__ __launch_bounds__(THREADS) void k_seed_init(const int32_t *seeds, int B, int S,
                                                        int64_t N, int64_t node_cap,
                                                        int32_t *nodes, uint64_t *visited,
-                                                       uint32_t *err) {
+                                                       LocalTable table, uint32_t *err) {
   int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (i >= (int64_t)B * S) return;
   int b = (int)(i / S);
@@ -59,7 +61,11 @@ __global__ __launch_bounds__(THREADS) void k_seed_init(const int32_t *seeds, int
   }
   unsigned long long bit = 1ull << b;
   unsigned long long old = atomicOr((unsigned long long *)&visited[v], bit);
-  if (old & bit) atomicOr(err, ERR_DUP_NODE);
+  if (old & bit) {
+    atomicOr(err, ERR_DUP_NODE);
+    return;
+  }
+  if (!lt_insert(table, v, b, j)) atomicOr(err, ERR_INTERNAL);
 }
 
 __global__ __launch_bounds__(THREADS) void k_frontier_degree(
@@ -173,31 +179,40 @@ __global__ __launch_bounds__(THREADS) void k_hop_sample(
     emit(idx[o0 + r[s]], b, base + s, parent, edge_src, edge_dst, visited, fresh, N, err);
 }
 
-// pairloc[first pair of u + (# batches below b that hold u)] = local index of u in b.
-__global__ __launch_bounds__(THREADS) void k_pairloc(Lists L, const int32_t *nodes,
-                                                     int64_t node_cap, const uint64_t *visited,
-                                                     const int64_t *nodeoff, int32_t *pairloc) {
+// New hop segments: batch b's segment starts at local index seg0[b].
+struct Segs {
+  int B;
+  int64_t start[DG_MAX_BATCHES + 1];  // prefix of segment lengths
+  int64_t seg0[DG_MAX_BATCHES];
+};
+
+// Records the local index of every node of the new hop segments.
+__global__ __launch_bounds__(THREADS) void k_table_insert(Segs L, const int32_t *nodes,
+                                                          int64_t node_cap, LocalTable table,
+                                                          uint32_t *err) {
   int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (i >= L.start[L.B]) return;
   int b = find_batch(L.start, L.B, i);
-  int64_t j = i - L.start[b];
-  int32_t u = nodes[(int64_t)b * node_cap + j];
-  uint64_t below = visited[u] & ((1ull << b) - 1ull);
-  pairloc[nodeoff[u] + __popcll(below)] = (int32_t)j;
+  int64_t j = L.seg0[b] + (i - L.start[b]);
+  if (!lt_insert(table, nodes[(int64_t)b * node_cap + j], b, j)) atomicOr(err, ERR_INTERNAL);
 }
 
+// Sampled neighbours' global IDs -> local indices through the (node, batch)
+// table filled at seed initialisation and at each hop's compaction.
 __global__ __launch_bounds__(THREADS) void k_relabel(Lists L, int64_t edge_cap, int32_t *edge_dst,
-                                                     const uint64_t *visited,
-                                                     const int64_t *nodeoff,
-                                                     const int32_t *pairloc, int64_t N) {
+                                                     LocalTable table, int64_t N, uint32_t *err) {
   int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (i >= L.start[L.B]) return;
   int b = find_batch(L.start, L.B, i);
   int64_t e = (int64_t)b * edge_cap + (i - L.start[b]);
   int32_t u = edge_dst[e];
   if (u < 0 || (int64_t)u >= N) return;  // already reported
-  uint64_t below = visited[u] & ((1ull << b) - 1ull);
-  edge_dst[e] = pairloc[nodeoff[u] + __popcll(below)];
+  int64_t j = lt_find(table, u, b);
+  if (j < 0) {
+    atomicOr(err, ERR_INTERNAL);
+    return;
+  }
+  edge_dst[e] = (int32_t)j;
 }
 
 // eoff at each batch's first frontier entry (and at the end).
@@ -211,10 +226,9 @@ inline unsigned blocks_for(int64_t n) { return (unsigned)((n + THREADS - 1) / TH
 struct SampleWs {
   uint32_t *err;
   uint64_t *visited, *fresh;
-  int64_t *nodeoff;
   int64_t *f_off, *f_deg, *f_cnt, *f_eoff, *tiles;
-  int32_t *pairloc;
-  int64_t *small;  // host-visible staging for a few counts
+  LocalTable table;
+  int64_t *small;  // staging for a few counts
   MaskScan ms;
 };
 
@@ -223,13 +237,13 @@ void carve_sample(SampleWs &w, Carve &c, int64_t N, int B, int64_t node_cap) {
   w.err = c.take<uint32_t>(64);
   w.visited = c.take<uint64_t>((size_t)N);
   w.fresh = c.take<uint64_t>((size_t)N);
-  w.nodeoff = c.take<int64_t>((size_t)N);
   w.f_off = c.take<int64_t>((size_t)fmax);
   w.f_deg = c.take<int64_t>((size_t)fmax);
   w.f_cnt = c.take<int64_t>((size_t)fmax);
   w.f_eoff = c.take<int64_t>((size_t)fmax + 1);
   w.tiles = c.take<int64_t>(scan_tile_count(fmax));
-  w.pairloc = c.take<int32_t>((size_t)fmax);
+  w.table.bits = lt_bits_for(fmax);
+  w.table.slots = c.take<uint64_t>((size_t)1 << w.table.bits);
   w.small = c.take<int64_t>(2 * (DG_MAX_BATCHES + 1));
   w.ms = MaskScan{};
   w.ms.N = N;
@@ -300,8 +314,8 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       (int64_t)S > g->num_nodes)
     return set_error(DG_EINVAL, "dg_sample_group: bad sizes (B=%d S=%d K=%d node_cap=%lld)", B,
                      S, K, (long long)node_cap);
-  if (node_cap > 0x7fffffffll)
-    return set_error(DG_EINVAL, "dg_sample_group: node_cap too large for int32 local IDs");
+  if (node_cap > LT_MAX_VALUE)
+    return set_error(DG_EINVAL, "dg_sample_group: node_cap above 2^27 - 1 is not supported");
   const size_t need_ws = dg_sample_workspace_bytes(g->num_nodes, B, node_cap, edge_cap);
   if (!ws || ws_bytes < need_ws || ((uintptr_t)ws & 255))
     return set_error(DG_EWORKSPACE, "dg_sample_group: workspace needs %zu bytes, 256-aligned",
@@ -320,14 +334,17 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
   if (timing) memset(timing, 0, sizeof(*timing));
   PhaseTimer tm(timing != nullptr, s);
   float t_sample = 0.f, t_dedup = 0.f;
+  int hop_ev[8][3];
+  int nhop_ev = 0;
   const int ev_start = tm.mark();
 
   int rc;
   if ((rc = fill_u64(reinterpret_cast<uint64_t *>(w.err), 32, 0, s))) return rc;
   if ((rc = fill_u64(w.visited, (size_t)N, 0, s))) return rc;
   if ((rc = fill_u64(w.fresh, (size_t)N, 0, s))) return rc;
+  if ((rc = fill_u64(w.table.slots, (size_t)1 << w.table.bits, 0, s))) return rc;
   hipLaunchKernelGGL(k_seed_init, dim3(blocks_for((int64_t)B * S)), dim3(THREADS), 0, s, seeds,
-                     B, S, N, node_cap, nodes, w.visited, w.err);
+                     B, S, N, node_cap, nodes, w.visited, w.table, w.err);
   DG_HIP(hipGetLastError());
   if ((rc = check_err(w.err, s))) return rc;
 
@@ -426,10 +443,27 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       w.ms.pairdest = nullptr;
       w.ms.clear = 1;
       if ((rc = mask_scan_write(w.ms, s))) return rc;
+      {
+        Segs LS;
+        LS.B = B;
+        LS.start[0] = 0;
+        for (int b = 0; b < B; ++b) {
+          LS.start[b + 1] = LS.start[b] + new_b[b];
+          LS.seg0[b] = n_b[b];
+        }
+        if (LS.start[B] > 0) {
+          hipLaunchKernelGGL(k_table_insert, dim3(blocks_for(LS.start[B])), dim3(THREADS), 0, s,
+                             LS, nodes, node_cap, w.table, w.err);
+          DG_HIP(hipGetLastError());
+        }
+      }
       const int ev2 = tm.mark();
-      DG_HIP(hipStreamSynchronize(s));
-      t_sample += tm.ms(ev0, ev1);
-      t_dedup += tm.ms(ev1, ev2);
+      if (nhop_ev < 8) {
+        hop_ev[nhop_ev][0] = ev0;
+        hop_ev[nhop_ev][1] = ev1;
+        hop_ev[nhop_ev][2] = ev2;
+        ++nhop_ev;
+      }
     }
     for (int b = 0; b < B; ++b) {
       fbeg[b] = n_b[b];
@@ -439,35 +473,16 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
     }
   }
   for (int b = 0; b < B; ++b) edge_ptr[(int64_t)b * (K + 1) + K] = e_b[b];
-  if ((rc = check_err(w.err, s))) return rc;
 
-  // Local IDs: pair table over the final membership mask.
+  // Local IDs through the (node, batch) table.
   const int ev_r0 = tm.mark();
-  Lists LN, LE;
-  LN.B = LE.B = B;
-  LN.start[0] = LE.start[0] = 0;
-  for (int b = 0; b < B; ++b) {
-    LN.start[b + 1] = LN.start[b] + n_b[b];
-    LE.start[b + 1] = LE.start[b] + e_b[b];
-  }
+  Lists LE;
+  LE.B = B;
+  LE.start[0] = 0;
+  for (int b = 0; b < B; ++b) LE.start[b + 1] = LE.start[b] + e_b[b];
   if (LE.start[B] > 0) {
-    w.ms.mask = w.visited;
-    w.ms.cache_slot = nullptr;
-    if ((rc = mask_scan_count(w.ms, totals, s))) return rc;
-    if (totals[row_pairs(B)] != LN.start[B])
-      return set_error(DG_EINVAL, "dg_sample_group: internal pair count mismatch");
-    w.ms.seg_out = nullptr;
-    w.ms.uniq_out = nullptr;
-    w.ms.unc_ids = nullptr;
-    w.ms.unc_off = nullptr;
-    w.ms.nodeoff = w.nodeoff;
-    w.ms.pairdest = nullptr;
-    w.ms.clear = 0;
-    if ((rc = mask_scan_write(w.ms, s))) return rc;
-    hipLaunchKernelGGL(k_pairloc, dim3(blocks_for(LN.start[B])), dim3(THREADS), 0, s, LN, nodes,
-                       node_cap, w.visited, w.nodeoff, w.pairloc);
     hipLaunchKernelGGL(k_relabel, dim3(blocks_for(LE.start[B])), dim3(THREADS), 0, s, LE,
-                       edge_cap, edge_dst, w.visited, w.nodeoff, w.pairloc, N);
+                       edge_cap, edge_dst, w.table, N, w.err);
     DG_HIP(hipGetLastError());
   }
   const int ev_r1 = tm.mark();
@@ -485,6 +500,10 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
   sizes->total_nodes = tn;
   sizes->total_edges = te;
   if (timing) {
+    for (int i = 0; i < nhop_ev && i < 8; ++i) {
+      t_sample += tm.ms(hop_ev[i][0], hop_ev[i][1]);
+      t_dedup += tm.ms(hop_ev[i][1], hop_ev[i][2]);
+    }
     timing->sample_ms = t_sample;
     timing->dedup_ms = t_dedup;
     timing->relabel_ms = tm.ms(ev_r0, ev_r1);

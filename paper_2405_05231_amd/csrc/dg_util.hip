@@ -25,6 +25,7 @@ const char *describe_device_error(uint32_t bits) {
   if (bits & ERR_NBR_RANGE) return "a CSR neighbour ID is outside [0, N)";
   if (bits & ERR_CACHE_SLOT) return "cache_slot holds a value below -1";
   if (bits & ERR_ROW_RANGE) return "an address-table entry is outside its table";
+  if (bits & ERR_INTERNAL) return "internal table overflow";
   return "unknown device error";
 }
 
