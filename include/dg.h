@@ -194,8 +194,12 @@ size_t dg_sample_workspace_bytes(int64_t num_nodes, int32_t B, int64_t node_cap,
  *              sampled neighbour), both as local indices into nodes_b.
  *   edge_ptr   [host] [B*(K+1)] int64: edge_ptr[b*(K+1)+k] = start of hop-(k+1)
  *              edges, edge_ptr[b*(K+1)+K] = e_b.
+ *   membership optional [N] uint64 output (NULL = kept in the workspace): on
+ *              return bit b of membership[u] is set iff u is in nodes_b.  It can
+ *              be handed to dg_pack_group, which then skips building it.
  *   sizes      [host] filled on DG_OK and DG_ECAPACITY.
  *   timing     [host] optional (NULL = not measured).
+ * node_cap must be below 2^27.
  * Errors: DG_EINVAL for null pointers, B outside 1..64, S < 1, K < 0, caps < S,
  * and for bad data found on the device: a seed outside [0,N), a seed repeated in
  * a batch, a CSR row with offsets outside [0,E] or decreasing, a neighbour ID
@@ -204,8 +208,8 @@ int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S,
                     int64_t batch_base, const int32_t *fanouts, int32_t K,
                     uint64_t rng_seed, int64_t node_cap, int32_t *nodes,
                     int64_t *hop_ptr, int64_t edge_cap, int32_t *edge_src,
-                    int32_t *edge_dst, int64_t *edge_ptr, void *ws, size_t ws_bytes,
-                    hipStream_t stream, dg_sizes *sizes, dg_timing *timing);
+                    int32_t *edge_dst, int64_t *edge_ptr, uint64_t *membership, void *ws,
+                    size_t ws_bytes, hipStream_t stream, dg_sizes *sizes, dg_timing *timing);
 
 /* Workspace bytes dg_pack_group needs for N nodes, B batches whose node lists
  * hold `total_nodes` entries in all. */
@@ -227,6 +231,14 @@ size_t dg_pack_workspace_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes
  *               chunk b is rows packed_ptr[b] .. packed_ptr[b+1).
  *   loc         [B*node_stride] int32: address table, loc_b at loc + b*node_stride.
  *   group_unique  [unique_cap] int32 or NULL: U ascending.
+ *   membership  optional [N] uint64 input (NULL = built here from the lists):
+ *               bit b of membership[u] set iff u is in batch b's list, as
+ *               dg_sample_group returns it; bits of batches >= B are ignored.
+ *               The call checks that the bit of every non-cached list entry is
+ *               set and that the mask holds as many (node, batch) pairs as the
+ *               lists have entries (DG_EINVAL otherwise); a mask that passes these
+ *               checks and still differs from the lists gives unspecified packing
+ *               outputs, never an access outside the given buffers.
  *   sizes, timing as for dg_sample_group.
  * Errors: DG_EINVAL for null pointers, B outside 1..64, row_bytes < 1, n_b out of
  * range, and on the device a node ID outside [0,N), a node repeated within a
@@ -237,8 +249,9 @@ int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
                   int64_t node_stride, const int64_t *node_count, int64_t packed_cap,
                   void *packed, int32_t *packed_ids, int64_t *packed_ptr,
                   int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique,
-                  int64_t unique_cap, void *ws, size_t ws_bytes, hipStream_t stream,
-                  dg_sizes *sizes, dg_timing *timing);
+                  int64_t unique_cap, const uint64_t *membership, void *ws,
+                  size_t ws_bytes, hipStream_t stream, dg_sizes *sizes,
+                  dg_timing *timing);
 
 /* Feature assembling for one mini-batch (§4 Fig. 3, second step; addresses come
  * from the precomputed table of §6, so no lookup structure is consulted):

@@ -90,13 +90,19 @@ class SampleResult:
 def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tensor, fanouts,
                  rng_seed: int, batch_base: int = 0, node_cap: int | None = None,
                  edge_cap: int | None = None, out: SampleResult | None = None,
-                 workspace: torch.Tensor | None = None, stream=None, timing: bool = False
-                 ) -> SampleResult:
-    """Group sampling (dg_sample_group).  seeds: int32 [B, S] on the GPU."""
+                 workspace: torch.Tensor | None = None, stream=None, timing: bool = False,
+                 membership: torch.Tensor | None = None) -> SampleResult:
+    """Group sampling (dg_sample_group).  seeds: int32 [B, S] on the GPU.
+    membership: optional int64 [N] tensor that receives the (node, batch)
+    membership mask (bit b of word u = u is in batch b)."""
     dev = offsets.device
     _need(offsets, "offsets", torch.int64)
     _need(indices, "indices", torch.int32, dev)
     _need(seeds, "seeds", torch.int32, dev)
+    if membership is not None:
+        _need(membership, "membership", torch.int64, dev)
+        if membership.numel() != offsets.numel() - 1:
+            raise ValueError("membership must hold one word per node")
     if seeds.dim() != 2:
         raise ValueError("seeds must be [B, S]")
     B, S = seeds.shape
@@ -125,7 +131,7 @@ def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tens
         ctypes.byref(g), _ptr(seeds), B, S, batch_base, fo, K, rng_seed & (2**64 - 1),
         node_cap, _ptr(out.nodes), out.hop_ptr.ctypes.data_as(_lib.I64P), edge_cap,
         _ptr(out.edge_src), _ptr(out.edge_dst), out.edge_ptr.ctypes.data_as(_lib.I64P),
-        _ptr(ws), ws.numel(), _stream(stream), ctypes.byref(sz),
+        _ptr(membership), _ptr(ws), ws.numel(), _stream(stream), ctypes.byref(sz),
         ctypes.byref(tm) if timing else None)
     out.sizes = sz.as_dict()
     check(st)
@@ -156,10 +162,11 @@ def _row_bytes(feats: torch.Tensor) -> int:
 
 def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tensor, node_count,
                with_unique: bool = False, out: PackResult | None = None,
-               workspace: torch.Tensor | None = None, stream=None, timing: bool = False
-               ) -> PackResult:
+               workspace: torch.Tensor | None = None, stream=None, timing: bool = False,
+               membership: torch.Tensor | None = None) -> PackResult:
     """Batched packing (dg_pack_group).  nodes: int32 [B, node_stride];
-    node_count: the B list lengths (host)."""
+    node_count: the B list lengths (host).  membership: optional int64 [N]
+    mask from sample_group (skips rebuilding it)."""
     dev = feats.device
     _need(feats, "feats", None)
     _need(cache_slot, "cache_slot", torch.int32, dev)
@@ -167,6 +174,10 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
     N = feats.shape[0]
     R = _row_bytes(feats)
     B, stride = nodes.shape
+    if membership is not None:
+        _need(membership, "membership", torch.int64, dev)
+        if membership.numel() != N:
+            raise ValueError("membership must hold one word per node")
     counts = np.ascontiguousarray(np.asarray(node_count, dtype=np.int64).reshape(-1))
     if counts.shape[0] != B:
         raise ValueError("node_count must have one entry per batch")
@@ -181,8 +192,9 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
         # size query: a zero packed capacity returns the exact sizes needed
         st = _L.dg_pack_group(_ptr(feats), N, R, _ptr(cache_slot), B, _ptr(nodes), stride,
                               counts.ctypes.data_as(_lib.I64P), 0, None, None, _ptr(ptr),
-                              ptr_host.ctypes.data_as(_lib.I64P), _ptr(loc), None, 0, _ptr(ws),
-                              ws.numel(), _stream(stream), ctypes.byref(sz), None)
+                              ptr_host.ctypes.data_as(_lib.I64P), _ptr(loc), None, 0,
+                              _ptr(membership), _ptr(ws), ws.numel(), _stream(stream),
+                              ctypes.byref(sz), None)
         if st not in (DG_OK, DG_ECAPACITY):
             check(st)
         rows, nu = sz.packed_rows, sz.unique_nodes
@@ -200,7 +212,8 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
                           _ptr(out.packed_ids), _ptr(out.packed_ptr),
                           out.packed_ptr_host.ctypes.data_as(_lib.I64P), _ptr(out.loc),
                           _ptr(out.unique), out.unique.numel() if out.unique is not None else 0,
-                          _ptr(ws), ws.numel(), _stream(stream), ctypes.byref(sz),
+                          _ptr(membership), _ptr(ws), ws.numel(), _stream(stream),
+                          ctypes.byref(sz),
                           ctypes.byref(tm) if timing else None)
     out.sizes = sz.as_dict()
     check(st)

@@ -26,35 +26,35 @@ __device__ __forceinline__ const char *row_source(int32_t l, const char *cache, 
 }
 
 template <int LPR, int CPL>
-__global__ __launch_bounds__(THREADS) void k_assemble16(const uint4 *cache, int64_t cache_rows,
-                                                        const uint4 *packed, int64_t packed_rows,
+__global__ __launch_bounds__(THREADS) void k_assemble16(const v4u *cache, int64_t cache_rows,
+                                                        const v4u *packed, int64_t packed_rows,
                                                         const int32_t *loc, int64_t n, int C,
-                                                        uint4 *out, int32_t *status) {
+                                                        v4u *out, int32_t *status) {
   constexpr int GPB = THREADS / LPR;  // row groups per block
   const int sub = threadIdx.x % LPR;
   const int64_t grp = (int64_t)blockIdx.x * GPB + threadIdx.x / LPR;
   const int64_t ngrp = (int64_t)gridDim.x * GPB;
   for (int64_t j0 = grp * UNROLL; j0 < n; j0 += ngrp * UNROLL) {
-    const uint4 *src[UNROLL];
+    const v4u *src[UNROLL];
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
       int64_t j = j0 + u;
       src[u] = nullptr;
       if (j < n) {
         int32_t l = loc[j];
-        src[u] = reinterpret_cast<const uint4 *>(
+        src[u] = reinterpret_cast<const v4u *>(
             row_source(l, reinterpret_cast<const char *>(cache), cache_rows,
                        reinterpret_cast<const char *>(packed), packed_rows, (int64_t)C * 16,
                        sub == 0 ? status : nullptr));
       }
     }
-    uint4 v[UNROLL][CPL];
+    v4u v[UNROLL][CPL];
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u)
 #pragma unroll
       for (int c = 0; c < CPL; ++c) {
         int ch = sub + c * LPR;
-        v[u][c] = (src[u] && ch < C) ? src[u][ch] : make_uint4(0, 0, 0, 0);
+        v[u][c] = (src[u] && ch < C) ? ld_stream(src[u] + ch) : v4u{0u, 0u, 0u, 0u};
       }
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
@@ -63,7 +63,7 @@ __global__ __launch_bounds__(THREADS) void k_assemble16(const uint4 *cache, int6
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
           int ch = sub + c * LPR;
-          if (ch < C) out[j * C + ch] = v[u][c];
+          if (ch < C) st_stream(v[u][c], out + j * C + ch);
         }
       }
     }
@@ -110,8 +110,8 @@ int launch16(const void *cache, int64_t cache_rows, const void *packed, int64_t 
   int64_t blocks = (groups + GPB - 1) / GPB;
   if (blocks > (1ll << 20)) blocks = 1ll << 20;
   hipLaunchKernelGGL((k_assemble16<LPR, CPL>), dim3((unsigned)blocks), dim3(THREADS), 0, s,
-                     (const uint4 *)cache, cache_rows, (const uint4 *)packed, packed_rows, loc, n,
-                     C, (uint4 *)out, status);
+                     (const v4u *)cache, cache_rows, (const v4u *)packed, packed_rows, loc, n, C,
+                     (v4u *)out, status);
   DG_HIP(hipGetLastError());
   return DG_OK;
 }

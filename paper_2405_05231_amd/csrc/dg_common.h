@@ -19,6 +19,7 @@ enum : uint32_t {
   ERR_CACHE_SLOT = 1u << 4,  // cache_slot[v] < -1
   ERR_ROW_RANGE = 1u << 5,   // an address-table entry outside its table
   ERR_INTERNAL = 1u << 6,    // an internal table overflowed (a library bug)
+  ERR_MEMBERSHIP = 1u << 7,  // a given membership mask misses a list entry
 };
 
 int set_error(int status, const char *fmt, ...);
@@ -64,6 +65,7 @@ __device__ __forceinline__ T wave_incl_sum(T x) {
 // (no LDS round trip).
 extern "C" __device__ uint64_t __ockl_wfred_or_u64(uint64_t);
 extern "C" __device__ int32_t __ockl_wfscan_add_i32(int32_t, bool inclusive);
+extern "C" __device__ int32_t __ockl_wfred_add_i32(int32_t);
 
 __device__ __forceinline__ uint64_t wave_or(uint64_t x) { return __ockl_wfred_or_u64(x); }
 __device__ __forceinline__ int32_t wave_incl_sum_i32(int32_t x) {
@@ -166,7 +168,8 @@ __host__ __device__ inline int64_t mc_chunks(int64_t nblk) { return (nblk + MC_C
 __host__ __device__ inline int row_all(int B) { return B; }        // nodes with any bit set (U)
 __host__ __device__ inline int row_packed(int B) { return B + 1; } // ... and not cached (U_nc)
 __host__ __device__ inline int row_pairs(int B) { return B + 2; }  // (node, batch) pairs of U_nc nodes
-__host__ __device__ inline int mc_rows(int B) { return B + 3; }
+__host__ __device__ inline int row_all_pairs(int B) { return B + 3; }  // all (node, batch) pairs
+__host__ __device__ inline int mc_rows(int B) { return B + 4; }
 
 struct MaskScan {
   uint64_t *mask;
@@ -187,8 +190,11 @@ struct MaskScan {
   int64_t *unc_off;                  // first pair of each U_nc node
   int64_t *nodeoff;                  // [N] first pair of node u (U_nc nodes only)
   int64_t *pairdest;                 // per pair: seg_base[b] + rank of u in b's list
-  int clear;                         // zero mask[u] once read
+  uint64_t *prev;                    // nullable: members already listed; the passes
+                                     // see mask & ~prev, and the write pass sets
+                                     // prev = mask where they differ
 };
+
 
 size_t mask_scan_ws_bytes(int64_t N, int B);
 void mask_scan_carve(MaskScan &m, Carve &c);

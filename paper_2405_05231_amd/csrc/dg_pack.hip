@@ -39,9 +39,9 @@ __global__ __launch_bounds__(THREADS) void k_pack_mark(Lists L, const int32_t *n
     atomicOr(err, ERR_NODE_RANGE);
     return;
   }
-  unsigned long long bit = 1ull << b;
-  unsigned long long old = atomicOr((unsigned long long *)&mask[u], bit);
-  if (old & bit) atomicOr(err, ERR_DUP_NODE);
+  // no-return atomic: a node repeated within a batch shows up later as fewer
+  // (node, batch) pairs in the mask than list entries
+  atomicOr((unsigned long long *)&mask[u], 1ull << b);
 }
 
 // packed_ptr from the per-batch totals of the count pass.
@@ -62,19 +62,27 @@ __global__ __launch_bounds__(THREADS) void k_build_loc(Lists L, const int32_t *n
                                                        const uint64_t *mask,
                                                        const int64_t *nodeoff,
                                                        const int64_t *pairdest,
-                                                       const int64_t *packed_ptr, int32_t *loc) {
-  int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
+                                                       const int64_t *packed_ptr, int32_t *loc,
+                                                       int64_t N, uint32_t *err) {
+  const int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (i >= L.start[L.B]) return;
-  int b = find_batch(L.start, L.B, i);
-  int64_t at = (int64_t)b * L.stride + (i - L.start[b]);
-  int32_t u = nodes[at];
-  int32_t sl = cache_slot[u];
-  int32_t out;
+  const int b = find_batch(L.start, L.B, i);
+  const int64_t at = (int64_t)b * L.stride + (i - L.start[b]);
+  const int32_t u = nodes[at];
+  if (u < 0 || (int64_t)u >= N) {
+    atomicOr(err, ERR_NODE_RANGE);
+    return;
+  }
+  const int32_t sl = cache_slot[u];
+  int32_t out = 0;
   if (sl >= 0) {
     out = -(sl + 1);
   } else {
-    uint64_t below = mask[u] & ((1ull << b) - 1ull);
-    out = (int32_t)(pairdest[nodeoff[u] + __popcll(below)] - packed_ptr[b]);
+    const uint64_t m = mask[u];
+    if (!((m >> b) & 1ull))  // only a given (external) mask can miss an entry
+      atomicOr(err, ERR_MEMBERSHIP);
+    else
+      out = (int32_t)(pairdest[nodeoff[u] + __popcll(m & ((1ull << b) - 1ull))] - packed_ptr[b]);
   }
   loc[at] = out;
 }
@@ -82,22 +90,22 @@ __global__ __launch_bounds__(THREADS) void k_build_loc(Lists L, const int32_t *n
 // Fan-out gather, 16-byte path: a group of LPR lanes reads the row of one U_nc
 // node once and stores it into each of its destination rows.
 template <int LPR, int CPL>
-__global__ __launch_bounds__(THREADS) void k_fanout16(const uint4 *X, const int32_t *unc_ids,
+__global__ __launch_bounds__(THREADS) void k_fanout16(const v4u *X, const int32_t *unc_ids,
                                                       const int64_t *unc_off, int64_t n_unc,
                                                       int64_t n_pairs, const int64_t *pairdest,
-                                                      int C, uint4 *packed) {
+                                                      int C, v4u *packed) {
   constexpr int GPB = THREADS / LPR;
   const int sub = threadIdx.x % LPR;
   const int64_t grp = (int64_t)blockIdx.x * GPB + threadIdx.x / LPR;
   const int64_t ngrp = (int64_t)gridDim.x * GPB;
   for (int64_t i0 = grp * UNROLL; i0 < n_unc; i0 += ngrp * UNROLL) {
     int64_t p0[UNROLL], p1[UNROLL];
-    uint4 v[UNROLL][CPL];
+    v4u v[UNROLL][CPL];
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
       int64_t i = i0 + u;
       p0[u] = p1[u] = 0;
-      const uint4 *src = nullptr;
+      const v4u *src = nullptr;
       if (i < n_unc) {
         src = X + (int64_t)unc_ids[i] * C;
         p0[u] = unc_off[i];
@@ -106,17 +114,17 @@ __global__ __launch_bounds__(THREADS) void k_fanout16(const uint4 *X, const int3
 #pragma unroll
       for (int c = 0; c < CPL; ++c) {
         int ch = sub + c * LPR;
-        v[u][c] = (src && ch < C) ? src[ch] : make_uint4(0, 0, 0, 0);
+        v[u][c] = (src && ch < C) ? ld_stream(src + ch) : v4u{0u, 0u, 0u, 0u};
       }
     }
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
       for (int64_t p = p0[u]; p < p1[u]; ++p) {
-        uint4 *dst = packed + pairdest[p] * C;
+        v4u *dst = packed + pairdest[p] * C;
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
           int ch = sub + c * LPR;
-          if (ch < C) dst[ch] = v[u][c];
+          if (ch < C) st_stream(v[u][c], dst + ch);
         }
       }
     }
@@ -150,7 +158,7 @@ void launch16(const void *X, const int32_t *ids, const int64_t *off, int64_t n, 
   int64_t blocks = (groups + GPB - 1) / GPB;
   if (blocks > (1ll << 20)) blocks = 1ll << 20;
   hipLaunchKernelGGL((k_fanout16<LPR, CPL>), dim3((unsigned)blocks), dim3(THREADS), 0, s,
-                     (const uint4 *)X, ids, off, n, pairs, dest, C, (uint4 *)packed);
+                     (const v4u *)X, ids, off, n, pairs, dest, C, (v4u *)packed);
 }
 
 template <typename T>
@@ -204,7 +212,7 @@ struct PackWs {
 
 void carve_pack(PackWs &w, Carve &c, int64_t N, int B, int64_t total_nodes) {
   int64_t ucap = total_nodes < N ? total_nodes : N;
-  w.err = c.take<uint32_t>(64);
+  w.err = c.take<uint32_t>(32);
   w.mask = c.take<uint64_t>((size_t)N);
   w.nodeoff = c.take<int64_t>((size_t)N);
   w.unc_ids = c.take<int32_t>((size_t)ucap + 1);
@@ -242,8 +250,9 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
                              int64_t node_stride, const int64_t *node_count, int64_t packed_cap,
                              void *packed, int32_t *packed_ids, int64_t *packed_ptr,
                              int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique,
-                             int64_t unique_cap, void *ws, size_t ws_bytes, hipStream_t stream,
-                             dg_sizes *sizes, dg_timing *timing) {
+                             int64_t unique_cap, const uint64_t *membership, void *ws,
+                             size_t ws_bytes, hipStream_t stream, dg_sizes *sizes,
+                             dg_timing *timing) {
   if (!feats || !cache_slot || !nodes || !node_count || !packed_ptr || !packed_ptr_host ||
       !loc || !sizes)
     return set_error(DG_EINVAL, "dg_pack_group: null pointer argument");
@@ -283,16 +292,20 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
 
   int rc;
   const int e0 = tm.mark();
-  if ((rc = fill_u64(reinterpret_cast<uint64_t *>(w.err), 32, 0, s))) return rc;
-  if ((rc = fill_u64(w.mask, (size_t)N, 0, s))) return rc;
-  if (total > 0) {
-    hipLaunchKernelGGL(k_pack_mark, dim3(blocks_for(total)), dim3(THREADS), 0, s, L, nodes, N,
-                       w.mask, w.err);
-    DG_HIP(hipGetLastError());
+  if ((rc = fill_u64(reinterpret_cast<uint64_t *>(w.err), 16, 0, s))) return rc;
+  if (membership) {
+    w.mask = const_cast<uint64_t *>(membership);  // read only below
+  } else {
+    if ((rc = fill_u64(w.mask, (size_t)N, 0, s))) return rc;
+    if (total > 0) {
+      hipLaunchKernelGGL(k_pack_mark, dim3(blocks_for(total)), dim3(THREADS), 0, s, L, nodes, N,
+                         w.mask, w.err);
+      DG_HIP(hipGetLastError());
+    }
   }
   const int e1 = tm.mark();
   // unique set, packed order, packed_ptr
-  int64_t totals[DG_MAX_BATCHES + 3];
+  int64_t totals[DG_MAX_BATCHES + 4];
   w.ms.mask = w.mask;
   w.ms.cache_slot = cache_slot;
   if ((rc = mask_scan_count(w.ms, totals, s))) return rc;
@@ -308,6 +321,11 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
   sizes->unique_packed = totals[row_packed(B)];
   if (rows != totals[row_pairs(B)])
     return set_error(DG_EINVAL, "dg_pack_group: internal pair count mismatch");
+  if (totals[row_all_pairs(B)] != total)
+    return set_error(DG_EINVAL, "invalid input data: %s",
+                     membership ? "the membership mask does not match the node lists (or a node "
+                                  "appears twice in one mini-batch)"
+                                : describe_device_error(ERR_DUP_NODE));
   if (rows > packed_cap || (group_unique && sizes->unique_nodes > unique_cap))
     return set_error(DG_ECAPACITY,
                      "dg_pack_group: need packed_cap >= %lld and unique_cap >= %lld",
@@ -320,12 +338,11 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
   w.ms.unc_off = w.unc_off;
   w.ms.nodeoff = w.nodeoff;
   w.ms.pairdest = w.pairdest;
-  w.ms.clear = 0;
   if ((rc = mask_scan_write(w.ms, s))) return rc;
   const int e2 = tm.mark();
   if (total > 0) {
     hipLaunchKernelGGL(k_build_loc, dim3(blocks_for(total)), dim3(THREADS), 0, s, L, nodes,
-                       cache_slot, w.mask, w.nodeoff, w.pairdest, packed_ptr, loc);
+                       cache_slot, w.mask, w.nodeoff, w.pairdest, packed_ptr, loc, N, w.err);
     DG_HIP(hipGetLastError());
   }
   const int e3 = tm.mark();

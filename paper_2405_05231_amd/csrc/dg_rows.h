@@ -44,6 +44,14 @@ inline int word_bytes(int64_t row_bytes, std::initializer_list<const void *> ptr
   return w;
 }
 
+// 16-byte row vector as a native vector type, so the nontemporal builtins
+// apply: every row is read once and written once, so neither side should
+// displace reusable lines from the caches.
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ v4u ld_stream(const v4u *p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ void st_stream(v4u x, v4u *p) { __builtin_nontemporal_store(x, p); }
+
 template <typename T>
 __device__ __forceinline__ T zero_word() {
   T z;

@@ -1,14 +1,14 @@
 // Group sampling: node-wise fan-out neighbour sampling (DiskGNN §2, Fig. 1) for
 // up to 64 mini-batches in one pass (offline sampling, §3).
 //
-// Device state: a node-major membership mask visited[u] (bit b = u is already
-// in mini-batch b) and fresh[u] (bit b = u joined b at the current hop).  A hop
-// is: degree pass over the frontier -> exclusive scan (edge slots) -> draw +
-// mark (atomicOr on visited/fresh) -> mask compaction of fresh into each
-// batch's new segment, ascending, with no sort.  Each node's local index is
-// recorded in a (node, batch) hash table when it joins a batch (seed
-// initialisation, each hop's compaction); sampled neighbours are relabelled
-// from global to local IDs through it at the end.
+// Device state: a node-major membership mask visited[u] (bit b = u is in
+// mini-batch b) and its copy prev[u] as of the start of the current hop.  A
+// hop is: degree pass over the frontier -> exclusive scan (edge slots) -> draw
+// + mark (fire-and-forget atomicOr on visited) -> compaction of visited & ~prev
+// (the nodes new at this hop) into each batch's new segment, ascending, with
+// no sort; the compaction also brings prev up to date.  At the end every node's
+// local index goes into a (node, batch) hash table sized for the group, and
+// sampled neighbours are relabelled from global to local IDs through it.
 #include <string.h>
 
 #include "dg_common.h"
@@ -48,7 +48,7 @@ struct Lists {
 __global__ __launch_bounds__(THREADS) void k_seed_init(const int32_t *seeds, int B, int S,
                                                        int64_t N, int64_t node_cap,
                                                        int32_t *nodes, uint64_t *visited,
-                                                       LocalTable table, uint32_t *err) {
+                                                       uint64_t *prev, uint32_t *err) {
   int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (i >= (int64_t)B * S) return;
   int b = (int)(i / S);
@@ -61,11 +61,8 @@ __global__ __launch_bounds__(THREADS) void k_seed_init(const int32_t *seeds, int
   }
   unsigned long long bit = 1ull << b;
   unsigned long long old = atomicOr((unsigned long long *)&visited[v], bit);
-  if (old & bit) {
-    atomicOr(err, ERR_DUP_NODE);
-    return;
-  }
-  if (!lt_insert(table, v, b, j)) atomicOr(err, ERR_INTERNAL);
+  if (old & bit) atomicOr(err, ERR_DUP_NODE);
+  atomicOr((unsigned long long *)&prev[v], bit);  // seeds are not new at hop 1
 }
 
 __global__ __launch_bounds__(THREADS) void k_frontier_degree(
@@ -90,27 +87,42 @@ __global__ __launch_bounds__(THREADS) void k_frontier_degree(
   f_cnt[i] = (h.f < 0 || d <= (int64_t)h.f) ? d : (int64_t)h.f;
 }
 
-__device__ __forceinline__ void emit(int32_t u, int b, int64_t slot, int32_t parent,
-                                     int32_t *edge_src, int32_t *edge_dst, uint64_t *visited,
-                                     uint64_t *fresh, int64_t N, uint32_t *err) {
-  edge_src[slot] = parent;
-  edge_dst[slot] = u;
-  if (u < 0 || (int64_t)u >= N) {
-    atomicOr(err, ERR_NBR_RANGE);
-    return;
+// Emits up to EMIT sampled edges whose neighbour IDs are already loaded:
+// edge stores, then plain loads of the membership words, then a
+// fire-and-forget atomicOr for each neighbour not yet in the batch.
+constexpr int EMIT = 8;
+
+__device__ __forceinline__ void emit_chunk(const int32_t (&u)[EMIT], const int64_t (&slot)[EMIT],
+                                           int cnt, int b, int32_t parent, int32_t *edge_src,
+                                           int32_t *edge_dst, uint64_t *visited, int64_t N,
+                                           uint32_t *err) {
+  const uint64_t bit = 1ull << b;
+  uint64_t seen[EMIT];
+#pragma unroll
+  for (int k = 0; k < EMIT; ++k) {
+    seen[k] = bit;
+    if (k < cnt) {
+      edge_src[slot[k]] = parent;
+      edge_dst[slot[k]] = u[k];
+      if (u[k] >= 0 && (int64_t)u[k] < N)
+        seen[k] = visited[u[k]];
+      else
+        atomicOr(err, ERR_NBR_RANGE);
+    }
   }
-  unsigned long long bit = 1ull << b;
-  unsigned long long old = atomicOr((unsigned long long *)&visited[u], bit);
-  if (!(old & bit)) atomicOr((unsigned long long *)&fresh[u], bit);
+#pragma unroll
+  for (int k = 0; k < EMIT; ++k)
+    if (k < cnt && !(seen[k] & bit)) atomicOr((unsigned long long *)&visited[u[k]], bit);
 }
 
 // One lane per frontier node.  Floyd's subset is built in registers (fully
 // unrolled, so the arrays stay in VGPRs); each drawn position's rank among the
-// f positions gives its slot, so no sort is needed.
+// f positions gives its slot, so no sort is needed.  Neighbour loads and
+// membership atomics are issued EMIT at a time so their latencies overlap.
 __global__ __launch_bounds__(THREADS) void k_hop_sample(
     Hop h, const int32_t *nodes, int64_t node_cap, const int32_t *idx, const int64_t *f_off,
     const int64_t *f_deg, const int64_t *f_eoff, int64_t edge_cap, int32_t *edge_src,
-    int32_t *edge_dst, uint64_t *visited, uint64_t *fresh, int64_t N, uint32_t *err) {
+    int32_t *edge_dst, uint64_t *visited, int64_t N, uint32_t *err) {
   int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (i >= h.ftot) return;
   int b = find_batch(h.fstart, h.B, i);
@@ -118,9 +130,18 @@ __global__ __launch_bounds__(THREADS) void k_hop_sample(
   int64_t o0 = f_off[i], d = f_deg[i];
   int64_t base = (int64_t)b * edge_cap + h.ebase[b] + (f_eoff[i] - h.estart[b]);
   int32_t parent = (int32_t)p;
-  if (h.f < 0 || d <= (int64_t)h.f) {
-    for (int64_t q = 0; q < d; ++q)
-      emit(idx[o0 + q], b, base + q, parent, edge_src, edge_dst, visited, fresh, N, err);
+  int32_t u[EMIT];
+  int64_t slot[EMIT];
+  if (h.f < 0 || d <= (int64_t)h.f) {  // every neighbour, in CSR order
+    for (int64_t q0 = 0; q0 < d; q0 += EMIT) {
+      const int cnt = d - q0 < EMIT ? (int)(d - q0) : EMIT;
+#pragma unroll
+      for (int k = 0; k < EMIT; ++k) {
+        slot[k] = base + q0 + k;
+        u[k] = k < cnt ? idx[o0 + q0 + k] : 0;
+      }
+      emit_chunk(u, slot, cnt, b, parent, edge_src, edge_dst, visited, N, err);
+    }
     return;
   }
   const int32_t f = h.f;
@@ -146,12 +167,19 @@ __global__ __launch_bounds__(THREADS) void k_hop_sample(
       }
     }
 #pragma unroll
-    for (int s = 0; s < FMAX; ++s) {
-      if (s < f) {
-        int rank = 0;
+    for (int s0 = 0; s0 < FMAX; s0 += EMIT) {
+      if (s0 < f) {
+        const int cnt = f - s0 < EMIT ? f - s0 : EMIT;
 #pragma unroll
-        for (int m = 0; m < FMAX; ++m) rank += (m < f && r[m] < r[s]) ? 1 : 0;
-        emit(idx[o0 + r[s]], b, base + rank, parent, edge_src, edge_dst, visited, fresh, N, err);
+        for (int k = 0; k < EMIT; ++k) {
+          const int s = s0 + k;
+          int rank = 0;
+#pragma unroll
+          for (int m = 0; m < FMAX; ++m) rank += (m < f && r[m] < r[s]) ? 1 : 0;
+          slot[k] = base + rank;
+          u[k] = k < cnt ? idx[o0 + r[s]] : 0;
+        }
+        emit_chunk(u, slot, cnt, b, parent, edge_src, edge_dst, visited, N, err);
       }
     }
     return;
@@ -175,18 +203,25 @@ __global__ __launch_bounds__(THREADS) void k_hop_sample(
     }
     r[m + 1] = x;
   }
-  for (int s = 0; s < f; ++s)
-    emit(idx[o0 + r[s]], b, base + s, parent, edge_src, edge_dst, visited, fresh, N, err);
+  for (int s0 = 0; s0 < f; s0 += EMIT) {
+    const int cnt = f - s0 < EMIT ? f - s0 : EMIT;
+#pragma unroll
+    for (int k = 0; k < EMIT; ++k) {
+      slot[k] = base + s0 + k;
+      u[k] = k < cnt ? idx[o0 + r[s0 + k]] : 0;
+    }
+    emit_chunk(u, slot, cnt, b, parent, edge_src, edge_dst, visited, N, err);
+  }
 }
 
-// New hop segments: batch b's segment starts at local index seg0[b].
+// List segments: batch b's segment starts at local index seg0[b].
 struct Segs {
   int B;
   int64_t start[DG_MAX_BATCHES + 1];  // prefix of segment lengths
   int64_t seg0[DG_MAX_BATCHES];
 };
 
-// Records the local index of every node of the new hop segments.
+// Records the local index of every node of the given list segments.
 __global__ __launch_bounds__(THREADS) void k_table_insert(Segs L, const int32_t *nodes,
                                                           int64_t node_cap, LocalTable table,
                                                           uint32_t *err) {
@@ -197,8 +232,8 @@ __global__ __launch_bounds__(THREADS) void k_table_insert(Segs L, const int32_t 
   if (!lt_insert(table, nodes[(int64_t)b * node_cap + j], b, j)) atomicOr(err, ERR_INTERNAL);
 }
 
-// Sampled neighbours' global IDs -> local indices through the (node, batch)
-// table filled at seed initialisation and at each hop's compaction.
+// Sampled neighbours' global IDs -> local indices through the group's
+// (node, batch) table.
 __global__ __launch_bounds__(THREADS) void k_relabel(Lists L, int64_t edge_cap, int32_t *edge_dst,
                                                      LocalTable table, int64_t N, uint32_t *err) {
   int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
@@ -225,7 +260,7 @@ inline unsigned blocks_for(int64_t n) { return (unsigned)((n + THREADS - 1) / TH
 
 struct SampleWs {
   uint32_t *err;
-  uint64_t *visited, *fresh;
+  uint64_t *visited, *prev;
   int64_t *f_off, *f_deg, *f_cnt, *f_eoff, *tiles;
   LocalTable table;
   int64_t *small;  // staging for a few counts
@@ -236,7 +271,7 @@ void carve_sample(SampleWs &w, Carve &c, int64_t N, int B, int64_t node_cap) {
   int64_t fmax = (int64_t)B * node_cap;  // frontier entries never exceed the node lists
   w.err = c.take<uint32_t>(64);
   w.visited = c.take<uint64_t>((size_t)N);
-  w.fresh = c.take<uint64_t>((size_t)N);
+  w.prev = c.take<uint64_t>((size_t)N);
   w.f_off = c.take<int64_t>((size_t)fmax);
   w.f_deg = c.take<int64_t>((size_t)fmax);
   w.f_cnt = c.take<int64_t>((size_t)fmax);
@@ -302,8 +337,9 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
                                int64_t batch_base, const int32_t *fanouts, int32_t K,
                                uint64_t rng_seed, int64_t node_cap, int32_t *nodes,
                                int64_t *hop_ptr, int64_t edge_cap, int32_t *edge_src,
-                               int32_t *edge_dst, int64_t *edge_ptr, void *ws, size_t ws_bytes,
-                               hipStream_t stream, dg_sizes *sizes, dg_timing *timing) {
+                               int32_t *edge_dst, int64_t *edge_ptr, uint64_t *membership,
+                               void *ws, size_t ws_bytes, hipStream_t stream, dg_sizes *sizes,
+                               dg_timing *timing) {
   if (!g || !seeds || !nodes || !hop_ptr || !edge_src || !edge_dst || !edge_ptr || !sizes ||
       (K > 0 && !fanouts))
     return set_error(DG_EINVAL, "dg_sample_group: null pointer argument");
@@ -340,11 +376,11 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
 
   int rc;
   if ((rc = fill_u64(reinterpret_cast<uint64_t *>(w.err), 32, 0, s))) return rc;
+  if (membership) w.visited = membership;
   if ((rc = fill_u64(w.visited, (size_t)N, 0, s))) return rc;
-  if ((rc = fill_u64(w.fresh, (size_t)N, 0, s))) return rc;
-  if ((rc = fill_u64(w.table.slots, (size_t)1 << w.table.bits, 0, s))) return rc;
+  if ((rc = fill_u64(w.prev, (size_t)N, 0, s))) return rc;
   hipLaunchKernelGGL(k_seed_init, dim3(blocks_for((int64_t)B * S)), dim3(THREADS), 0, s, seeds,
-                     B, S, N, node_cap, nodes, w.visited, w.table, w.err);
+                     B, S, N, node_cap, nodes, w.visited, w.prev, w.err);
   DG_HIP(hipGetLastError());
   if ((rc = check_err(w.err, s))) return rc;
 
@@ -366,7 +402,7 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
     fbeg[b] = 0;
     fend[b] = S;
   }
-  int64_t totals[DG_MAX_BATCHES + 3];
+  int64_t totals[DG_MAX_BATCHES + 4];
 
   for (int k = 1; k <= K; ++k) {
     for (int b = 0; b < B; ++b) edge_ptr[(int64_t)b * (K + 1) + (k - 1)] = e_b[b];
@@ -413,11 +449,12 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       }
       hipLaunchKernelGGL(k_hop_sample, dim3(blocks_for(h.ftot)), dim3(THREADS), 0, s, h, nodes,
                          node_cap, g->indices, w.f_off, w.f_deg, w.f_eoff, edge_cap, edge_src,
-                         edge_dst, w.visited, w.fresh, N, w.err);
+                         edge_dst, w.visited, N, w.err);
       DG_HIP(hipGetLastError());
       const int ev1 = tm.mark();
       // new nodes of this hop, per batch, ascending
-      w.ms.mask = w.fresh;
+      w.ms.mask = w.visited;
+      w.ms.prev = w.prev;
       w.ms.cache_slot = nullptr;
       if ((rc = mask_scan_count(w.ms, totals, s))) return rc;
       bool nover = false;
@@ -441,22 +478,8 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       w.ms.unc_off = nullptr;
       w.ms.nodeoff = nullptr;
       w.ms.pairdest = nullptr;
-      w.ms.clear = 1;
       if ((rc = mask_scan_write(w.ms, s))) return rc;
-      {
-        Segs LS;
-        LS.B = B;
-        LS.start[0] = 0;
-        for (int b = 0; b < B; ++b) {
-          LS.start[b + 1] = LS.start[b] + new_b[b];
-          LS.seg0[b] = n_b[b];
-        }
-        if (LS.start[B] > 0) {
-          hipLaunchKernelGGL(k_table_insert, dim3(blocks_for(LS.start[B])), dim3(THREADS), 0, s,
-                             LS, nodes, node_cap, w.table, w.err);
-          DG_HIP(hipGetLastError());
-        }
-      }
+
       const int ev2 = tm.mark();
       if (nhop_ev < 8) {
         hop_ev[nhop_ev][0] = ev0;
@@ -481,8 +504,21 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
   LE.start[0] = 0;
   for (int b = 0; b < B; ++b) LE.start[b + 1] = LE.start[b] + e_b[b];
   if (LE.start[B] > 0) {
+    // the table holds every (node, batch) pair of the group, at load <= 1/2
+    Segs LS;
+    LS.B = B;
+    LS.start[0] = 0;
+    for (int b = 0; b < B; ++b) {
+      LS.start[b + 1] = LS.start[b] + n_b[b];
+      LS.seg0[b] = 0;
+    }
+    LocalTable table = w.table;
+    table.bits = lt_bits_for(LS.start[B]);
+    if ((rc = fill_u64(table.slots, (size_t)1 << table.bits, 0, s))) return rc;
+    hipLaunchKernelGGL(k_table_insert, dim3(blocks_for(LS.start[B])), dim3(THREADS), 0, s, LS,
+                       nodes, node_cap, table, w.err);
     hipLaunchKernelGGL(k_relabel, dim3(blocks_for(LE.start[B])), dim3(THREADS), 0, s, LE,
-                       edge_cap, edge_dst, w.table, N, w.err);
+                       edge_cap, edge_dst, table, N, w.err);
     DG_HIP(hipGetLastError());
   }
   const int ev_r1 = tm.mark();

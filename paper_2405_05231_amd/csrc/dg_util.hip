@@ -26,6 +26,7 @@ const char *describe_device_error(uint32_t bits) {
   if (bits & ERR_CACHE_SLOT) return "cache_slot holds a value below -1";
   if (bits & ERR_ROW_RANGE) return "an address-table entry is outside its table";
   if (bits & ERR_INTERNAL) return "internal table overflow";
+  if (bits & ERR_MEMBERSHIP) return "the membership mask does not match the node lists";
   return "unknown device error";
 }
 
@@ -175,6 +176,18 @@ __device__ __forceinline__ void load_tile(const MaskScan &a, int64_t t0, int lan
     int64_t u = t0 + r * 64 + lane;
     t.m[r] = u < a.N ? a.mask[u] : 0ull;
   }
+  if (a.B < 64) {  // bits of batches outside the group are ignored
+    const uint64_t keep = (1ull << a.B) - 1ull;
+#pragma unroll
+    for (int r = 0; r < MC_ROUNDS; ++r) t.m[r] &= keep;
+  }
+  if (a.prev) {
+    uint64_t p[MC_ROUNDS];
+#pragma unroll
+    for (int r = 0; r < MC_ROUNDS; ++r) p[r] = t.m[r] ? a.prev[t0 + r * 64 + lane] : 0ull;
+#pragma unroll
+    for (int r = 0; r < MC_ROUNDS; ++r) t.m[r] &= ~p[r];
+  }
   t.cached = 0;
   if (a.cache_slot) {
     int32_t sl[MC_ROUNDS];
@@ -192,13 +205,15 @@ __device__ __forceinline__ void load_tile(const MaskScan &a, int64_t t0, int lan
 // Per-wave counts of one tile: lane b returns batch b's non-cached members;
 // *cu, *cnc, *cp (wave-uniform) get the members of U, of U_nc and U_nc's pairs.
 __device__ __forceinline__ uint32_t tile_counts(const TileBits &t, int lane, uint32_t *cu,
-                                                uint32_t *cnc, uint32_t *cp) {
+                                                uint32_t *cnc, uint32_t *cp, uint32_t *call) {
   uint32_t mine = 0, u = 0, nc = 0, p = 0;
+  int32_t all = 0;
 #pragma unroll
   for (int r = 0; r < MC_ROUNDS; ++r) {
     uint64_t m = t.m[r];
     uint64_t any = __ballot(m != 0ull);
     if (any == 0ull) continue;  // wave-uniform
+    all += __popcll(m);
     uint64_t mnc = ((t.cached >> r) & 1u) ? 0ull : m;
     u += (uint32_t)__popcll(any);
     nc += (uint32_t)__popcll(__ballot(mnc != 0ull));
@@ -214,17 +229,20 @@ __device__ __forceinline__ uint32_t tile_counts(const TileBits &t, int lane, uin
   *cu = u;
   *cnc = nc;
   *cp = p;
+  *call = (uint32_t)__ockl_wfred_add_i32(all);
   return mine;
 }
 
 // Stores one wave's counts into its LDS row (rows = B + 3).
 __device__ __forceinline__ void stash_counts(uint32_t *row, int B, int lane, uint32_t mine,
-                                             uint32_t cu, uint32_t cnc, uint32_t cp) {
+                                             uint32_t cu, uint32_t cnc, uint32_t cp,
+                                             uint32_t call) {
   if (lane < B) row[lane] = mine;
   if (lane == 0) {
     row[row_all(B)] = cu;
     row[row_packed(B)] = cnc;
     row[row_pairs(B)] = cp;
+    row[row_all_pairs(B)] = call;
   }
 }
 
@@ -232,15 +250,15 @@ __device__ __forceinline__ void stash_counts(uint32_t *row, int B, int lane, uin
 // only), of U, of U_nc, and of U_nc's (node, batch) pairs; stored as one
 // contiguous row per block.
 __global__ __launch_bounds__(MC_THREADS) void k_mask_count(MaskScan a) {
-  __shared__ uint32_t s_cnt[MC_WAVES][DG_MAX_BATCHES + 3];
+  __shared__ uint32_t s_cnt[MC_WAVES][DG_MAX_BATCHES + 4];
   const int lane = lane_id(), w = threadIdx.x >> 6;
   const int B = a.B, rows = mc_rows(B);
   const int64_t t0 = (int64_t)blockIdx.x * MC_BLOCK_NODES + (int64_t)w * MC_TILE;
   TileBits t;
   load_tile(a, t0, lane, t, true);
-  uint32_t cu, cnc, cp;
-  uint32_t mine = tile_counts(t, lane, &cu, &cnc, &cp);
-  stash_counts(s_cnt[w], B, lane, mine, cu, cnc, cp);
+  uint32_t cu, cnc, cp, call;
+  uint32_t mine = tile_counts(t, lane, &cu, &cnc, &cp, &call);
+  stash_counts(s_cnt[w], B, lane, mine, cu, cnc, cp, call);
   __syncthreads();
   for (int i = threadIdx.x; i < rows; i += MC_THREADS) {
     uint32_t v = 0;
@@ -318,16 +336,16 @@ int mask_scan_count(MaskScan &m, int64_t *host_totals, hipStream_t s) {
 // earlier rounds (lane b holds batch b's), plus the ballot prefix within the
 // round.
 __global__ __launch_bounds__(MC_THREADS) void k_mask_write(MaskScan a) {
-  __shared__ uint32_t s_cnt[MC_WAVES][DG_MAX_BATCHES + 3];
+  __shared__ uint32_t s_cnt[MC_WAVES][DG_MAX_BATCHES + 4];
   const int lane = lane_id(), w = threadIdx.x >> 6;
   const int B = a.B, rows = mc_rows(B);
   const int64_t t0 = (int64_t)blockIdx.x * MC_BLOCK_NODES + (int64_t)w * MC_TILE;
   TileBits t;
   load_tile(a, t0, lane, t, false);
   {
-    uint32_t cu, cnc, cp;
-    uint32_t mine = tile_counts(t, lane, &cu, &cnc, &cp);
-    stash_counts(s_cnt[w], B, lane, mine, cu, cnc, cp);
+    uint32_t cu, cnc, cp, call;
+    uint32_t mine = tile_counts(t, lane, &cu, &cnc, &cp, &call);
+    stash_counts(s_cnt[w], B, lane, mine, cu, cnc, cp, call);
   }
   __syncthreads();
   const int64_t *bb = a.base + (size_t)blockIdx.x * rows;
@@ -377,7 +395,7 @@ __global__ __launch_bounds__(MC_THREADS) void k_mask_write(MaskScan a) {
       }
       if (lane == b) run_b += __popcll(bal);
     }
-    if (a.clear && m != 0ull) a.mask[t0 + r * 64 + lane] = 0ull;
+    if (a.prev && m != 0ull) a.prev[t0 + r * 64 + lane] |= m;
   }
 }
 

@@ -72,7 +72,7 @@ def test_host_side_argument_errors(L):
     sizes = _lib.Sizes()
     # null CSR / outputs: rejected before any device call
     rc = L.dg_sample_group(None, None, 1, 1, 0, None, 0, 0, 1, None, None, 1, None, None, None,
-                           None, 0, None, ctypes.byref(sizes), None)
+                           None, None, 0, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL
     assert b"null" in L.dg_last_error()
     g = _lib.Csr(10, 0, 0x1000, 0)
@@ -82,20 +82,20 @@ def test_host_side_argument_errors(L):
     fake = ctypes.c_void_p(0x1000)
     # B out of range
     rc = L.dg_sample_group(ctypes.byref(g), fake, 65, 1, 0, fo, 1, 0, 4, fake, hop, 4, fake, fake,
-                           ep, fake, 1 << 20, None, ctypes.byref(sizes), None)
+                           ep, None, fake, 1 << 20, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL
     # workspace missing
     rc = L.dg_sample_group(ctypes.byref(g), fake, 1, 1, 0, fo, 1, 0, 4, fake, hop, 4, fake, fake,
-                           ep, None, 0, None, ctypes.byref(sizes), None)
+                           ep, None, None, 0, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EWORKSPACE
     # pack: B = 0, row_bytes = 0, counts beyond the stride
     cnt = (ctypes.c_int64 * 2)(3, 9)
     ph = (ctypes.c_int64 * 3)()
     rc = L.dg_pack_group(fake, 10, 0, fake, 2, fake, 8, cnt, 0, None, None, fake, ph, fake, None,
-                         0, fake, 1 << 20, None, ctypes.byref(sizes), None)
+                         0, None, fake, 1 << 20, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL
     rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, cnt, 0, None, None, fake, ph, fake, None,
-                         0, fake, 1 << 20, None, ctypes.byref(sizes), None)
+                         0, None, fake, 1 << 20, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL and b"node_count" in L.dg_last_error()
     # assemble: n_b = 0 is a no-op; negative sizes and overlap are rejected
     assert L.dg_assemble_batch(None, 0, None, 0, None, 0, 16, None, None, None) == _lib.DG_OK

@@ -1,0 +1,141 @@
+"""Error paths of the device library, forced from the host with bad inputs or
+small capacities: every kernel still runs to completion and stays inside its
+buffers; the call reports the problem."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module")
+def dg():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2405_05231_amd as m
+    return m
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    w = synth.make_workload("T")
+    return w
+
+
+def test_duplicate_seed_rejected(dg, tiny):
+    seeds = tiny.seeds.clone()
+    seeds[1, 5] = seeds[1, 9]
+    with pytest.raises(dg.DGError) as e:
+        dg.sample_group(tiny.offsets.to(DEV), tiny.indices.to(DEV), seeds.to(DEV), [5, 5], 1)
+    assert e.value.status == -1 and "twice" in str(e.value)
+
+
+def test_seed_out_of_range_rejected(dg, tiny):
+    seeds = tiny.seeds.clone()
+    seeds[0, 0] = tiny.cfg.n + 3
+    with pytest.raises(dg.DGError) as e:
+        dg.sample_group(tiny.offsets.to(DEV), tiny.indices.to(DEV), seeds.to(DEV), [5, 5], 1)
+    assert e.value.status == -1 and "outside" in str(e.value)
+
+
+def test_bad_neighbour_id_rejected(dg, tiny):
+    idx = tiny.indices.clone()
+    idx[::7] = -5
+    with pytest.raises(dg.DGError) as e:
+        dg.sample_group(tiny.offsets.to(DEV), idx.to(DEV), tiny.seeds.to(DEV), [5, 5], 1)
+    assert e.value.status == -1 and "neighbour" in str(e.value)
+
+
+def test_bad_offsets_rejected(dg, tiny):
+    off = tiny.offsets.clone()
+    off[100:200] = 10 ** 9  # beyond num_edges
+    seeds = torch.arange(100, 164, dtype=torch.int32).reshape(1, 64)
+    with pytest.raises(dg.DGError) as e:
+        dg.sample_group(off.to(DEV), tiny.indices.to(DEV), seeds.to(DEV), [5, 5], 1)
+    assert e.value.status == -1 and "CSR" in str(e.value)
+
+
+def test_sample_capacity_reported(dg, tiny):
+    off, idx, seeds = tiny.offsets.to(DEV), tiny.indices.to(DEV), tiny.seeds.to(DEV)
+    full = dg.sample_group(off, idx, seeds, [5, 5], 1)
+    need_n = full.sizes["max_batch_nodes"]
+    need_e = full.sizes["max_batch_edges"]
+    # node capacity one short: hop 2 overflows; outputs never written past the cap
+    B = seeds.shape[0]
+    guard = 4096
+    nodes = torch.full((B * (need_n - 1) + guard,), 7777, dtype=torch.int32, device=DEV)
+    res = dg.SampleResult(nodes=nodes[:B * (need_n - 1)].view(B, need_n - 1),
+                          hop_ptr=np.zeros((B, 4), dtype=np.int64),
+                          edge_src=torch.empty((B, need_e), dtype=torch.int32, device=DEV),
+                          edge_dst=torch.empty((B, need_e), dtype=torch.int32, device=DEV),
+                          edge_ptr=np.zeros((B, 3), dtype=np.int64), sizes={}, timing=None)
+    with pytest.raises(dg.DGError) as e:
+        dg.sample_group(off, idx, seeds, [5, 5], 1, out=res)
+    assert e.value.status == -2
+    assert res.sizes["max_batch_nodes"] >= need_n - 1 + 1 or res.sizes["exact"] == 0
+    assert bool((nodes[B * (need_n - 1):] == 7777).all())
+    # edge capacity one short
+    res2 = dg.SampleResult(nodes=torch.empty((B, need_n), dtype=torch.int32, device=DEV),
+                           hop_ptr=np.zeros((B, 4), dtype=np.int64),
+                           edge_src=torch.empty((B, need_e - 1), dtype=torch.int32, device=DEV),
+                           edge_dst=torch.empty((B, need_e - 1), dtype=torch.int32, device=DEV),
+                           edge_ptr=np.zeros((B, 3), dtype=np.int64), sizes={}, timing=None)
+    with pytest.raises(dg.DGError) as e:
+        dg.sample_group(off, idx, seeds, [5, 5], 1, out=res2)
+    assert e.value.status == -2 and res2.sizes["max_batch_edges"] == need_e
+
+
+def test_pack_duplicate_and_range_rejected(dg, tiny):
+    X = tiny.feats.to(DEV)
+    slot = tiny.cache_slot.to(DEV)
+    nodes = torch.tensor([[1, 2, 3, 2], [4, 5, 6, 7]], dtype=torch.int32, device=DEV)
+    with pytest.raises(dg.DGError) as e:
+        dg.pack_group(X, slot, nodes, [4, 4])
+    assert e.value.status == -1 and "twice" in str(e.value)
+    nodes = torch.tensor([[1, 2, 3, 10 ** 6]], dtype=torch.int32, device=DEV)
+    with pytest.raises(dg.DGError) as e:
+        dg.pack_group(X, slot, nodes, [4])
+    assert e.value.status == -1 and "outside" in str(e.value)
+    bad = slot.clone()
+    bad[3] = -7
+    nodes = torch.tensor([[1, 2, 3]], dtype=torch.int32, device=DEV)
+    with pytest.raises(dg.DGError) as e:
+        dg.pack_group(X, bad, nodes, [3])
+    assert e.value.status == -1 and "cache_slot" in str(e.value)
+
+
+def test_pack_capacity_reported(dg, tiny):
+    X = tiny.feats.to(DEV)
+    slot = torch.full((tiny.cfg.n,), -1, dtype=torch.int32, device=DEV)
+    nodes = torch.tensor([[1, 2, 3, 4], [3, 4, 5, 6]], dtype=torch.int32, device=DEV)
+    full = dg.pack_group(X, slot, nodes, [4, 4], with_unique=True)
+    assert full.sizes["packed_rows"] == 8 and full.sizes["unique_nodes"] == 6
+    R = tiny.cfg.row_bytes
+    guard = torch.full((8 * R,), 0xAB, dtype=torch.uint8, device=DEV)
+    small = dg.PackResult(packed=guard[:7 * R].view(7, R),
+                          packed_ids=torch.empty(7, dtype=torch.int32, device=DEV),
+                          packed_ptr=torch.empty(3, dtype=torch.int64, device=DEV),
+                          packed_ptr_host=np.zeros(3, dtype=np.int64),
+                          loc=torch.empty((2, 4), dtype=torch.int32, device=DEV),
+                          unique=None, sizes={}, timing=None, row_bytes=R)
+    with pytest.raises(dg.DGError) as e:
+        dg.pack_group(X, slot, nodes, [4, 4], out=small)
+    assert e.value.status == -2 and small.sizes["packed_rows"] == 8
+    assert bool((guard == 0xAB).all())  # nothing written anywhere
+
+
+def test_assemble_bad_address_flags_and_zeroes(dg):
+    R = 64
+    cache = torch.arange(4 * R, dtype=torch.int32, device=DEV).to(torch.uint8).view(4, R)
+    packed = torch.full((3, R), 9, dtype=torch.uint8, device=DEV)
+    loc = torch.tensor([-1, 0, 5, -9, 2], dtype=torch.int32, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    out = dg.assemble_batch(cache, packed, loc, R, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 1
+    assert torch.equal(out[0], cache[0]) and torch.equal(out[1], packed[0])
+    assert torch.equal(out[4], packed[2])
+    assert int(out[2].sum()) == 0 and int(out[3].sum()) == 0

@@ -207,3 +207,42 @@ def test_fig1_example_on_device(dg, orc):
                          fx["fanouts"], 0)
     assert to_np(sr.batch_nodes(0)).tolist() == fx["expect"]["nodes"]
     assert sr.hop_ptr[0].tolist() == fx["expect"]["hop_ptr"]
+
+
+def test_membership_handoff_matches_standalone_pack(dg):
+    """dg_sample_group's membership mask handed to dg_pack_group gives the
+    same packing as rebuilding it from the lists; masks that disagree with the
+    lists are rejected."""
+    w = synth.make_workload("T")
+    X, slot = w.feats.to(DEV), w.cache_slot.to(DEV)
+    mem = torch.empty(w.cfg.n, dtype=torch.int64, device=DEV)
+    sr = dg.sample_group(w.offsets.to(DEV), w.indices.to(DEV), w.seeds.to(DEV),
+                         list(w.cfg.fanouts), w.rng_seed, membership=mem)
+    # the mask is exactly the lists' membership
+    want = torch.zeros(w.cfg.n, dtype=torch.int64)
+    for b in range(w.cfg.B):
+        want[sr.batch_nodes(b).long().cpu()] |= (1 << b)
+    assert torch.equal(mem.cpu(), want)
+    a = dg.pack_group(X, slot, sr.nodes, sr.node_count, with_unique=True)
+    b = dg.pack_group(X, slot, sr.nodes, sr.node_count, with_unique=True, membership=mem)
+    for key in ("packed_rows", "unique_nodes", "unique_packed"):
+        assert a.sizes[key] == b.sizes[key]
+    rows = a.sizes["packed_rows"]
+    assert torch.equal(a.packed[:rows], b.packed[:rows])
+    assert torch.equal(a.packed_ids[:rows], b.packed_ids[:rows])
+    assert torch.equal(a.unique, b.unique)
+    for bb in range(w.cfg.B):
+        n = int(sr.hop_ptr[bb, -1])
+        assert torch.equal(a.loc[bb, :n], b.loc[bb, :n])
+    # a list entry missing from the mask
+    bad = mem.clone()
+    u = int(sr.batch_nodes(2)[5])
+    bad[u] &= ~(1 << 2)
+    with pytest.raises(dg.DGError):
+        dg.pack_group(X, slot, sr.nodes, sr.node_count, membership=bad)
+    # an extra (node, batch) pair in the mask
+    bad = mem.clone()
+    free = int((mem == 0).nonzero()[0])
+    bad[free] = 1
+    with pytest.raises(dg.DGError):
+        dg.pack_group(X, slot, sr.nodes, sr.node_count, membership=bad)

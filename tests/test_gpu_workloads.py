@@ -1,4 +1,5 @@
-"""Parity on the named workloads, in the launch configuration bench.py times.
+"""Parity on the named workloads, in the launch configuration bench.py times
+(the sampler's membership mask handed to the packer).
 
 M1 (1M nodes) compares every integer output with the oracle and every row on
 the device.  The full-size workloads (L100, W120, H65 at three cache shares)
@@ -43,9 +44,10 @@ def run_and_check(dg, orc, w, oracle_batches):
     cfg = w.cfg
     fan = list(cfg.fanouts)
     R = cfg.row_bytes
-    sr = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed)
+    mem = torch.empty(cfg.n, dtype=torch.int64, device=DEV)
+    sr = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, membership=mem)
     counts = sr.node_count.copy()
-    pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, with_unique=True)
+    pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, with_unique=True, membership=mem)
     torch.cuda.synchronize()
     print(f"[{cfg.name}] nodes {sr.sizes['total_nodes']:,} edges {sr.sizes['total_edges']:,} "
           f"packed {pr.sizes['packed_rows']:,} U {pr.sizes['unique_nodes']:,}", flush=True)
