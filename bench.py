@@ -68,6 +68,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calib", action="store_true",
                     help="also run a plain copy of known size (counter calibration)")
+    ap.add_argument("--experiment", choices=["pack_ab", "cache"], default=None,
+                    help="instead of the step benchmark: batched vs individual packing "
+                         "(pack_ab) or access-frequency vs in-degree cache (cache)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -96,6 +99,11 @@ def main():
     R = cfg.row_bytes
     B = cfg.B
     stream = torch.cuda.current_stream()
+    if args.experiment:
+        out = {"pack_ab": experiment_pack_ab, "cache": experiment_cache}[args.experiment](
+            dg, w, cfg, args.steps)
+        print(json.dumps(out), flush=True)
+        return
 
     # first pass: sizes and buffers (outside the timed region)
     mem = torch.empty(cfg.n, dtype=torch.int64, device=dev)  # (node, batch) membership
@@ -214,6 +222,83 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, cfg, args.cpu_batches or cfg.B)
     print(json.dumps(out), flush=True)
+
+
+def _median(v):
+    v = sorted(v)
+    return v[len(v) // 2]
+
+
+def experiment_pack_ab(dg, w, cfg, reps):
+    """Batched packing (one fan-out gather that reads each non-cached row once)
+    against individual packing (one gather per mini-batch, a row read per
+    mini-batch that needs it), on the same packing tables; paper §5.2, Fig. 6,
+    Fig. 17."""
+    import torch
+    R, B = cfg.row_bytes, cfg.B
+    mem = torch.empty(cfg.n, dtype=torch.int64, device="cuda")
+    sr = dg.sample_group(w.offsets, w.indices, w.seeds, list(cfg.fanouts), w.rng_seed,
+                         membership=mem)
+    pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, sr.node_count, membership=mem)
+    buf = torch.empty_like(pr.packed)
+    t_b, t_i = [], []
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for _ in range(reps + 1):
+        p = dg.pack_group(w.feats, w.cache_slot, sr.nodes, sr.node_count, out=pr,
+                          membership=mem, timing=True)
+        t_b.append(p.timing["gather_ms"])
+        ev[0].record()
+        dg.pack_individual(w.feats, pr.packed_ids, pr.packed_ptr_host, buf)
+        ev[1].record()
+        ev[1].synchronize()
+        t_i.append(ev[0].elapsed_time(ev[1]))
+    rows = pr.sizes["packed_rows"]
+    same = bool(torch.equal(buf[:rows], pr.packed[:rows]))
+    Uc = pr.sizes["unique_packed"]
+    tb, ti = _median(t_b[1:]), _median(t_i[1:])
+    return {"experiment": "batched vs individual packing (row copy only)", "workload": cfg.name,
+            "cache_rows": int(w.cache_nodes.numel()), "row_bytes": R, "batches": B,
+            "packed_rows": rows, "unique_packed": Uc,
+            "batched": {"ms": round(tb, 3), "row_reads": Uc,
+                        "bytes": R * (Uc + rows), "GBps": round(R * (Uc + rows) / tb / 1e6, 1)},
+            "individual": {"ms": round(ti, 3), "row_reads": rows, "launches": B,
+                           "bytes": 2 * R * rows, "GBps": round(2 * R * rows / ti / 1e6, 1)},
+            "speedup": round(ti / tb, 3), "read_ratio": round(rows / max(Uc, 1), 3),
+            "identical_output": same}
+
+
+def experiment_cache(dg, w, cfg, reps):
+    """Cache by access frequency (popcount of the group's membership words;
+    §3, §4) against cache by in-degree, same size: packed rows and pack time."""
+    import torch
+    B = cfg.B
+    C = int(w.cache_nodes.numel())
+    mem = torch.empty(cfg.n, dtype=torch.int64, device="cuda")
+    sr = dg.sample_group(w.offsets, w.indices, w.seeds, list(cfg.fanouts), w.rng_seed,
+                         membership=mem)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    t_sel = []
+    for _ in range(reps + 1):
+        ev[0].record()
+        slot_f, nodes_f, cached = dg.cache_by_frequency(mem, B, C)
+        ev[1].record()
+        ev[1].synchronize()
+        t_sel.append(ev[0].elapsed_time(ev[1]))
+    cache_f = dg.gather_rows(w.feats, nodes_f[:cached])
+    res = {}
+    for name, slot in (("in_degree", w.cache_slot), ("frequency", slot_f)):
+        ts = []
+        for _ in range(reps + 1):
+            p = dg.pack_group(w.feats, slot, sr.nodes, sr.node_count, membership=mem, timing=True)
+            ts.append(p.timing["total_ms"])
+        res[name] = {"packed_rows": p.sizes["packed_rows"], "unique_packed": p.sizes["unique_packed"],
+                     "pack_ms": round(_median(ts[1:]), 3)}
+    accesses = sr.sizes["total_nodes"]
+    return {"experiment": "cache by access frequency vs by in-degree", "workload": cfg.name,
+            "cache_rows": C, "cached": cached, "accesses": accesses,
+            "select_ms": round(_median(t_sel[1:]), 3), "cache_table_bytes": int(cache_f.numel()),
+            "in_degree": res["in_degree"], "frequency": res["frequency"],
+            "hit_share": {k: round(1 - v["packed_rows"] / accesses, 4) for k, v in res.items()}}
 
 
 def cpu_baseline(w, cfg, nb):

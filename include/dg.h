@@ -225,7 +225,8 @@ size_t dg_pack_workspace_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes
  *               lists may come from any sampler, §3 "Generality").
  *   node_count  [host] [B] int64: n_b (0 <= n_b <= node_stride).
  * Outputs:
- *   packed      [packed_cap*row_bytes] bytes: the packed chunks, batch-major.
+ *   packed      [packed_cap*row_bytes] bytes: the packed chunks, batch-major;
+ *               NULL = build the tables below without copying any row.
  *   packed_ids  [packed_cap] int32: node ID of each packed row (P_0 || P_1 ...).
  *   packed_ptr  [B+1] int64 (device) and packed_ptr_host [host] [B+1] int64:
  *               chunk b is rows packed_ptr[b] .. packed_ptr[b+1).
@@ -270,6 +271,38 @@ int dg_assemble_batch(const void *cache, int64_t cache_rows, const void *packed_
                       int64_t packed_rows_b, const int32_t *loc_b, int64_t n_b,
                       int64_t row_bytes, void *out, int32_t *status,
                       hipStream_t stream);
+
+/* Workspace bytes dg_cache_by_frequency needs for N nodes. */
+size_t dg_cache_workspace_bytes(int64_t num_nodes);
+
+/* Cache configuration by access frequency (§4 "Four-level hierarchical feature
+ * store": a counter per node over the graph samples; §3 "Cache configuration":
+ * caching the most frequently accessed features minimises the features left to
+ * fetch from slower storage).  The access count of node u is the number of the
+ * group's mini-batches that require it: popcount(membership[u] & batch bits),
+ * with membership as dg_sample_group returns it.  Nodes are ranked by count,
+ * descending, ties by ascending ID; the first min(cache_rows, #accessed)
+ * nodes are cached.
+ *   cache_slot   [N] int32 out: rank of u if cached, else -1.
+ *   cache_nodes  [cache_rows] int32 out: cached node of each slot; -1 for
+ *                slots left empty (fewer accessed nodes than cache_rows).
+ *   cached       [host] out: number of cached nodes.
+ * Returns after completion.  DG_EINVAL for null pointers, B outside 1..64,
+ * cache_rows outside [0, N]; DG_EWORKSPACE for a small workspace. */
+int dg_cache_by_frequency(const uint64_t *membership, int64_t N, int32_t B, int64_t cache_rows,
+                          int32_t *cache_slot, int32_t *cache_nodes, int64_t *cached, void *ws,
+                          size_t ws_bytes, hipStream_t stream);
+
+/* Row gather: out[i] = feats[ids[i]] for i in [0, n) (rows of row_bytes
+ * bytes).  Fills the cache table from dg_cache_by_frequency's cache_nodes (the
+ * paper fills its caches by batched packing, treating each cache as one more
+ * mini-batch, §5.2), and, called once per mini-batch over that batch's
+ * packed_ids, performs the individual packing of §5.2 (Fig. 6a) that batched
+ * packing replaces.  An id outside [0, N) writes a zero row and ORs bit 0
+ * into the optional device int32 *status.  Asynchronous on `stream`.
+ * DG_EINVAL for bad sizes, null pointers or an output overlapping an input. */
+int dg_gather_rows(const void *feats, int64_t N, int64_t row_bytes, const int32_t *ids,
+                   int64_t n, void *out, int32_t *status, hipStream_t stream);
 
 #ifdef __cplusplus
 }

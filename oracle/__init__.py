@@ -62,6 +62,9 @@ def lib():
         L.or_pack_group.argtypes = [
             ctypes.c_int64, ctypes.c_int64, VP, I32P, ctypes.c_int32, I32P, ctypes.c_int64, I64P,
             ctypes.c_int64, VP, I32P, I64P, I32P, I32P, ctypes.c_int64, I64P]
+        L.or_cache_by_frequency.restype = ctypes.c_int
+        L.or_cache_by_frequency.argtypes = [ctypes.c_int64, ctypes.c_int32, I32P, ctypes.c_int64,
+                                            I64P, ctypes.c_int64, I32P, I32P, I64P]
         L.or_assemble_batch.restype = ctypes.c_int
         L.or_assemble_batch.argtypes = [VP, ctypes.c_int64, VP, ctypes.c_int64, I32P,
                                         ctypes.c_int64, ctypes.c_int64, VP]
@@ -214,3 +217,22 @@ def assemble_batch(cache, packed_b, loc_b, row_bytes):
     if rc:
         raise OracleError(f"or_assemble_batch rc={rc}")
     return out
+
+
+def cache_by_frequency(N, node_lists, cache_rows):
+    """Access-frequency cache: (cache_slot int32 [N], cache_nodes int32
+    [cache_rows] with -1 for empty slots, cached count)."""
+    B = len(node_lists)
+    counts = np.array([len(x) for x in node_lists], dtype=np.int64)
+    stride = max(int(counts.max()) if B else 0, 1)
+    nodes = np.zeros(B * stride, dtype=np.int32)
+    for b, x in enumerate(node_lists):
+        nodes[b * stride:b * stride + len(x)] = x
+    slot = np.zeros(N, dtype=np.int32)
+    cn = np.zeros(max(cache_rows, 1), dtype=np.int32)
+    cached = np.zeros(1, dtype=np.int64)
+    rc = lib().or_cache_by_frequency(N, B, _p(nodes, I32P), stride, _p(counts, I64P), cache_rows,
+                                     _p(slot, I32P), _p(cn, I32P), _p(cached, I64P))
+    if rc:
+        raise OracleError(f"or_cache_by_frequency rc={rc}")
+    return slot, cn[:cache_rows], int(cached[0])

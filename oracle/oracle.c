@@ -327,3 +327,47 @@ int or_assemble_batch(const void *cache, int64_t cache_rows, const void *packed_
   }
   return 0;
 }
+
+/* ---------------------------------------------------------------------------
+ * Cache configuration by access frequency (§4: one counter per node, streamed
+ * over the graph samples; the most popular features go to the fastest tier).
+ * A mini-batch requires each of its nodes once, so a node's count is the
+ * number of node lists that hold it.  Ranking: count descending, ties by
+ * ascending node ID; only accessed nodes are cached.
+ * ------------------------------------------------------------------------- */
+static const int64_t *g_rank_count; /* qsort has no context argument */
+
+static int cmp_by_count(const void *a, const void *b) {
+  int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
+  if (g_rank_count[x] != g_rank_count[y]) return g_rank_count[x] > g_rank_count[y] ? -1 : 1;
+  return (x > y) - (x < y);
+}
+
+int or_cache_by_frequency(int64_t N, int32_t B, const int32_t *nodes, int64_t node_stride,
+                          const int64_t *node_count, int64_t cache_rows, int32_t *cache_slot,
+                          int32_t *cache_nodes, int64_t *cached) {
+  if (N < 1 || B < 1 || cache_rows < 0 || cache_rows > N) return -1;
+  int64_t *count = (int64_t *)calloc((size_t)N, sizeof(int64_t));
+  for (int32_t b = 0; b < B; ++b)
+    for (int64_t j = 0; j < node_count[b]; ++j) {
+      int32_t u = nodes[(int64_t)b * node_stride + j];
+      if (u < 0 || u >= N) { free(count); return -1; }
+      count[u] += 1;
+    }
+  int32_t *order = (int32_t *)malloc((size_t)N * sizeof(int32_t));
+  for (int64_t v = 0; v < N; ++v) order[v] = (int32_t)v;
+  g_rank_count = count;
+  qsort(order, (size_t)N, sizeof(int32_t), cmp_by_count);
+  int64_t c = 0;
+  for (int64_t v = 0; v < N; ++v) cache_slot[v] = -1;
+  for (int64_t r = 0; r < cache_rows; ++r) cache_nodes[r] = -1;
+  for (int64_t r = 0; r < cache_rows && count[order[r]] > 0; ++r) {
+    cache_slot[order[r]] = (int32_t)r;
+    cache_nodes[r] = order[r];
+    ++c;
+  }
+  *cached = c;
+  free(order);
+  free(count);
+  return 0;
+}

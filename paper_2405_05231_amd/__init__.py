@@ -18,8 +18,8 @@ from . import _lib
 from ._lib import (DG_ECAPACITY, DG_MAX_BATCHES, DG_OK, DGError, Csr, Sizes, Timing, check,
                    load)
 
-__all__ = ["sample_bounds", "sample_group", "pack_group", "assemble_batch", "DGError",
-           "SampleResult", "PackResult", "version"]
+__all__ = ["sample_bounds", "sample_group", "pack_group", "assemble_batch", "cache_by_frequency",
+           "gather_rows", "pack_individual", "DGError", "SampleResult", "PackResult", "version"]
 
 _L = load()
 
@@ -163,10 +163,12 @@ def _row_bytes(feats: torch.Tensor) -> int:
 def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tensor, node_count,
                with_unique: bool = False, out: PackResult | None = None,
                workspace: torch.Tensor | None = None, stream=None, timing: bool = False,
-               membership: torch.Tensor | None = None) -> PackResult:
+               membership: torch.Tensor | None = None, tables_only: bool = False
+               ) -> PackResult:
     """Batched packing (dg_pack_group).  nodes: int32 [B, node_stride];
     node_count: the B list lengths (host).  membership: optional int64 [N]
-    mask from sample_group (skips rebuilding it)."""
+    mask from sample_group (skips rebuilding it).  tables_only: build the
+    packed order and address tables without copying rows (packed = None)."""
     dev = feats.device
     _need(feats, "feats", None)
     _need(cache_slot, "cache_slot", torch.int32, dev)
@@ -186,6 +188,14 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
     ws = _workspace(ws_bytes, dev, workspace)
     ptr_host = np.zeros(B + 1, dtype=np.int64)
     sz, tm = Sizes(), Timing()
+    if out is None and tables_only:
+        out = PackResult(packed=None, packed_ids=torch.empty(max(total, 1), dtype=torch.int32,
+                                                             device=dev),
+                         packed_ptr=torch.empty(B + 1, dtype=torch.int64, device=dev),
+                         packed_ptr_host=ptr_host, loc=torch.empty((B, stride), dtype=torch.int32,
+                                                                   device=dev),
+                         unique=torch.empty(max(total, 1), dtype=torch.int32, device=dev)
+                         if with_unique else None, sizes={}, timing=None, row_bytes=R)
     if out is None:
         loc = torch.empty((B, stride), dtype=torch.int32, device=dev)
         ptr = torch.empty(B + 1, dtype=torch.int64, device=dev)
@@ -205,7 +215,7 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
             unique=torch.empty(max(nu, 1), dtype=torch.int32, device=dev) if with_unique else None,
             sizes={}, timing=None, row_bytes=R)
     cap = out.packed_ids.numel()
-    if out.packed.numel() < cap * R:
+    if out.packed is not None and out.packed.numel() < cap * R:
         raise ValueError("packed buffer smaller than packed_ids")
     st = _L.dg_pack_group(_ptr(feats), N, R, _ptr(cache_slot), B, _ptr(nodes), stride,
                           counts.ctypes.data_as(_lib.I64P), cap, _ptr(out.packed),
@@ -246,3 +256,50 @@ def assemble_batch(cache: torch.Tensor | None, packed_b: torch.Tensor, loc_b: to
                                _ptr(packed_b) if pr else None, pr, _ptr(loc_b), n, row_bytes,
                                _ptr(out), _ptr(status), _stream(stream)))
     return out
+
+
+def cache_by_frequency(membership: torch.Tensor, B: int, cache_rows: int,
+                       workspace: torch.Tensor | None = None, stream=None):
+    """Access-frequency cache (dg_cache_by_frequency).  Returns (cache_slot
+    int32 [N], cache_nodes int32 [cache_rows], cached count)."""
+    _need(membership, "membership", torch.int64)
+    dev = membership.device
+    N = membership.numel()
+    slot = torch.empty(N, dtype=torch.int32, device=dev)
+    nodes = torch.empty(max(cache_rows, 1), dtype=torch.int32, device=dev)
+    ws = _workspace(_L.dg_cache_workspace_bytes(N), dev, workspace)
+    cached = ctypes.c_int64()
+    check(_L.dg_cache_by_frequency(_ptr(membership), N, B, cache_rows, _ptr(slot), _ptr(nodes),
+                                   ctypes.byref(cached), _ptr(ws), ws.numel(), _stream(stream)))
+    return slot, nodes[:cache_rows], cached.value
+
+
+def gather_rows(feats: torch.Tensor, ids: torch.Tensor, out: torch.Tensor | None = None,
+                status: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """out[i] = feats[ids[i]] as bytes (dg_gather_rows), asynchronous.  Returns
+    out viewed as uint8 [n, row_bytes]."""
+    _need(feats, "feats", None)
+    _need(ids, "ids", torch.int32, feats.device)
+    R = _row_bytes(feats)
+    n = ids.numel()
+    if out is None:
+        out = torch.empty((n, R), dtype=torch.uint8, device=feats.device)
+    _need(out, "out", None, feats.device)
+    if out.numel() * out.element_size() < n * R:
+        raise ValueError("out is too small")
+    check(_L.dg_gather_rows(_ptr(feats), feats.shape[0], R, _ptr(ids), n, _ptr(out),
+                            _ptr(status), _stream(stream)))
+    return out
+
+
+def pack_individual(feats: torch.Tensor, packed_ids: torch.Tensor, packed_ptr_host,
+                    packed: torch.Tensor, stream=None) -> torch.Tensor:
+    """Individual packing (the paper's naive scheme, Fig. 6a): one row gather
+    per mini-batch over its packed IDs, reading a row once per mini-batch that
+    needs it.  Fills the same packed buffer dg_pack_group would."""
+    R = _row_bytes(feats)
+    for b in range(len(packed_ptr_host) - 1):
+        lo, hi = int(packed_ptr_host[b]), int(packed_ptr_host[b + 1])
+        if hi > lo:
+            gather_rows(feats, packed_ids[lo:hi], out=packed[lo:hi], stream=stream)
+    return packed

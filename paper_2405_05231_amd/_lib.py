@@ -59,6 +59,9 @@ SIGNATURES = {
                                      VP, VP, I64, VP, VP, SZ, VP, ctypes.POINTER(Sizes),
                                      ctypes.POINTER(Timing)]),
     "dg_assemble_batch": (ctypes.c_int, [VP, I64, VP, I64, VP, I64, I64, VP, VP, VP]),
+    "dg_cache_workspace_bytes": (SZ, [I64]),
+    "dg_cache_by_frequency": (ctypes.c_int, [VP, I64, I32, I64, VP, VP, I64P, VP, SZ, VP]),
+    "dg_gather_rows": (ctypes.c_int, [VP, I64, I64, VP, I64, VP, VP, VP]),
 }
 
 _lib = None

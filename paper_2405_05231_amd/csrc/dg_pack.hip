@@ -271,8 +271,8 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
     L.start[b + 1] = L.start[b] + node_count[b];
   }
   const int64_t total = L.start[B];
-  if (total > 0 && (!packed || !packed_ids) && packed_cap > 0)
-    return set_error(DG_EINVAL, "dg_pack_group: null output buffer");
+  if (packed_cap > 0 && !packed_ids)
+    return set_error(DG_EINVAL, "dg_pack_group: null packed_ids");
   const size_t need_ws = dg_pack_workspace_bytes(N, B, total);
   if (!ws || ws_bytes < need_ws || ((uintptr_t)ws & 255))
     return set_error(DG_EWORKSPACE, "dg_pack_group: workspace needs %zu bytes, 256-aligned",
@@ -346,7 +346,8 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
     DG_HIP(hipGetLastError());
   }
   const int e3 = tm.mark();
-  if ((rc = launch_fanout(feats, w.unc_ids, w.unc_off, sizes->unique_packed, rows, w.pairdest,
+  if (packed &&  // packed == NULL: address tables only, no row copy
+      (rc = launch_fanout(feats, w.unc_ids, w.unc_off, sizes->unique_packed, rows, w.pairdest,
                           row_bytes, packed, s)))
     return rc;
   const int e4 = tm.mark();

@@ -316,3 +316,42 @@ def test_sample_rejects_duplicate_seed(orc):
     off, idx = csr_from_rows(3, {0: [1], 1: [2], 2: [0]})
     with pytest.raises(orc.OracleError):
         orc.sample_group(off, idx, np.array([[1, 1]], dtype=np.int32), [1], 0)
+
+
+# ------------------------------------------------------------------ access-frequency cache
+def packed_volume(slot, lists):
+    return sum(int((slot[np.asarray(l, dtype=np.int64)] < 0).sum()) for l in lists)
+
+
+@pytest.mark.parametrize("trial", range(20))
+def test_cache_by_frequency_bruteforce_and_optimal(orc, trial):
+    """Counts = number of lists holding the node; ranking count-descending,
+    ID-ascending; and (the placement claim of §3) no other cache of the same
+    size leaves fewer rows to pack."""
+    rnd = random.Random(700 + trial)
+    n = rnd.randint(1, 60)
+    B = rnd.randint(1, 6)
+    lists = [np.array(rnd.sample(range(n), rnd.randint(0, n)), dtype=np.int32) for _ in range(B)]
+    C = rnd.randint(0, n)
+    slot, nodes, cached = orc.cache_by_frequency(n, lists, C)
+    count = {u: sum(u in set(l.tolist()) for l in lists) for u in range(n)}
+    want = sorted((u for u in range(n) if count[u] > 0), key=lambda u: (-count[u], u))[:C]
+    assert nodes[:len(want)].tolist() == want and cached == len(want)
+    assert all(x == -1 for x in nodes[len(want):].tolist())
+    assert [int(slot[u]) for u in want] == list(range(len(want)))
+    assert sum(int(s >= 0) for s in slot) == len(want)
+    best = packed_volume(slot, lists)
+    for _ in range(30):
+        other = np.full(n, -1, dtype=np.int32)
+        for s, u in enumerate(rnd.sample(range(n), min(C, n))):
+            other[u] = s
+        assert best <= packed_volume(other, lists)
+
+
+def test_cache_by_frequency_small_example(orc):
+    # node 2 in three lists, 0 and 5 in two, 7 in one
+    lists = [np.array(x, dtype=np.int32) for x in ([2, 0, 7], [5, 2], [0, 2, 5])]
+    slot, nodes, cached = orc.cache_by_frequency(8, lists, 3)
+    assert nodes.tolist() == [2, 0, 5] and cached == 3
+    slot, nodes, cached = orc.cache_by_frequency(8, lists, 6)
+    assert nodes.tolist() == [2, 0, 5, 7, -1, -1] and cached == 4
