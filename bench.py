@@ -68,9 +68,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calib", action="store_true",
                     help="also run a plain copy of known size (counter calibration)")
-    ap.add_argument("--experiment", choices=["pack_ab", "cache"], default=None,
+    ap.add_argument("--experiment", choices=["pack_ab", "cache", "layered"], default=None,
                     help="instead of the step benchmark: batched vs individual packing "
-                         "(pack_ab) or access-frequency vs in-degree cache (cache)")
+                         "(pack_ab), access-frequency vs in-degree cache (cache), or "
+                         "layer-wise (DGL-style) vs new-node frontier sampling (layered)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -100,8 +101,8 @@ def main():
     B = cfg.B
     stream = torch.cuda.current_stream()
     if args.experiment:
-        out = {"pack_ab": experiment_pack_ab, "cache": experiment_cache}[args.experiment](
-            dg, w, cfg, args.steps)
+        out = {"pack_ab": experiment_pack_ab, "cache": experiment_cache,
+               "layered": experiment_layered}[args.experiment](dg, w, cfg, args.steps)
         print(json.dumps(out), flush=True)
         return
 
@@ -299,6 +300,27 @@ def experiment_cache(dg, w, cfg, reps):
             "select_ms": round(_median(t_sel[1:]), 3), "cache_table_bytes": int(cache_f.numel()),
             "in_degree": res["in_degree"], "frequency": res["frequency"],
             "hit_share": {k: round(1 - v["packed_rows"] / accesses, 4) for k, v in res.items()}}
+
+
+def experiment_layered(dg, w, cfg, reps):
+    """Sampling with the paper's frontier rule (only newly reached nodes sample
+    next, Fig. 1) against the layer-wise rule (every node so far samples)."""
+    res = {}
+    for name, layered in (("new_nodes", False), ("layered", True)):
+        sr = dg.sample_group(w.offsets, w.indices, w.seeds, list(cfg.fanouts), w.rng_seed,
+                             layered=layered)
+        ts = []
+        for _ in range(reps + 1):
+            t0 = time.perf_counter()
+            dg.sample_group(w.offsets, w.indices, w.seeds, list(cfg.fanouts), w.rng_seed,
+                            out=sr, layered=layered)
+            ts.append(time.perf_counter() - t0)
+        t = _median(ts[1:])
+        res[name] = {"ms": round(1e3 * t, 3), "edges": sr.sizes["total_edges"],
+                     "nodes": sr.sizes["total_nodes"],
+                     "edges_per_s": round(sr.sizes["total_edges"] / t, 1)}
+    return {"experiment": "sampling frontier rule", "workload": cfg.name, "fanouts":
+            list(cfg.fanouts), "batches": cfg.B, **res}
 
 
 def cpu_baseline(w, cfg, nb):

@@ -107,6 +107,11 @@ extern "C" {
 
 #define DG_MAX_BATCHES 64 /* a group holds at most 64 mini-batches (one bit each) */
 
+/* dg_sample_group / dg_sample_bounds flags */
+#define DG_SAMPLE_LAYERED 1u /* every node of the mini-batch so far samples at each hop
+                                (layer-wise blocks as DGL builds them), instead of only
+                                the nodes new at the previous hop */
+
 typedef enum dg_status {
   DG_OK = 0,
   DG_EINVAL = -1,     /* bad argument, or bad input data found by a device check */
@@ -161,13 +166,16 @@ const char *dg_version(void);
 const char *dg_last_error(void);
 
 /* [host only, no device work] Upper bounds on n_b and e_b for any graph with
- * `num_nodes` nodes and `num_edges` edges: n_b <= min(N, S*(1 + f1 + f1*f2 + ...)),
- * e_b <= min(E, S*f1 + S*f1*f2 + ...), where a negative fan-out counts as
- * "all neighbours" (bounded by N for nodes and E for edges).  Capacities this
- * large never trigger DG_ECAPACITY.  Returns DG_EINVAL on a null pointer,
- * S < 1, K < 0 or num_nodes < 1. */
+ * `num_nodes` nodes and `num_edges` edges and the sampling mode in `flags`.
+ * Without DG_SAMPLE_LAYERED: hop k adds at most min(f_k * F_{k-1}, E) edges and
+ * as many nodes, where F_0 = S and F_k = the hop's edge bound (only new nodes
+ * sample next); with it, F_k = the node bound so far (every node samples).  A
+ * negative fan-out counts as E edges; node bounds are capped at N.  For the
+ * default mode this gives n_b <= min(N, S*(1 + f1 + f1*f2 + ...)).  Capacities
+ * this large never trigger DG_ECAPACITY.  Returns DG_EINVAL on a null pointer,
+ * S < 1, K < 0, num_nodes < 1 or unknown flags. */
 int dg_sample_bounds(int64_t num_nodes, int64_t num_edges, int32_t S,
-                     const int32_t *fanouts /*[host] K*/, int32_t K,
+                     const int32_t *fanouts /*[host] K*/, int32_t K, uint32_t flags,
                      int64_t *node_cap /*[host] out*/, int64_t *edge_cap /*[host] out*/);
 
 /* Workspace bytes dg_sample_group needs for N nodes, B batches and the given
@@ -186,6 +194,10 @@ size_t dg_sample_workspace_bytes(int64_t num_nodes, int32_t B, int64_t node_cap,
  *   fanouts    [host] K fan-outs, hop 1 first; f < 0 means "all neighbours",
  *              f = 0 samples nothing at that hop.  K >= 0.
  *   rng_seed   sampler seed.
+ *   flags      0, or DG_SAMPLE_LAYERED: at every hop all nodes of the mini-batch
+ *              so far sample (in list order), not only the previous hop's new
+ *              nodes; the node list then nests as DGL's layer-wise blocks do
+ *              (the first hop_ptr[k] nodes are the destinations of hop k+1).
  * Outputs (row b of each starts at b*cap):
  *   nodes      [B*node_cap] int32: nodes_b in the order above.
  *   hop_ptr    [host] [B*(K+2)] int64: hop_ptr[b*(K+2)+h] = start of hop h in
@@ -206,7 +218,7 @@ size_t dg_sample_workspace_bytes(int64_t num_nodes, int32_t B, int64_t node_cap,
  * outside [0,N).  Bad data never causes an access outside the given arrays. */
 int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S,
                     int64_t batch_base, const int32_t *fanouts, int32_t K,
-                    uint64_t rng_seed, int64_t node_cap, int32_t *nodes,
+                    uint64_t rng_seed, uint32_t flags, int64_t node_cap, int32_t *nodes,
                     int64_t *hop_ptr, int64_t edge_cap, int32_t *edge_src,
                     int32_t *edge_dst, int64_t *edge_ptr, uint64_t *membership, void *ws,
                     size_t ws_bytes, hipStream_t stream, dg_sizes *sizes, dg_timing *timing);

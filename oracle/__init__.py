@@ -56,8 +56,8 @@ def lib():
         L.or_sample_group.restype = ctypes.c_int
         L.or_sample_group.argtypes = [
             ctypes.c_int64, ctypes.c_int64, I64P, I32P, I32P, ctypes.c_int32, ctypes.c_int32,
-            ctypes.c_int64, I32P, ctypes.c_int32, ctypes.c_uint64, ctypes.c_int64, I32P, I64P,
-            ctypes.c_int64, I32P, I32P, I64P, I64P]
+            ctypes.c_int64, I32P, ctypes.c_int32, ctypes.c_uint64, ctypes.c_int32,
+            ctypes.c_int64, I32P, I64P, ctypes.c_int64, I32P, I32P, I64P, I64P]
         L.or_pack_group.restype = ctypes.c_int
         L.or_pack_group.argtypes = [
             ctypes.c_int64, ctypes.c_int64, VP, I32P, ctypes.c_int32, I32P, ctypes.c_int64, I64P,
@@ -106,21 +106,19 @@ def floyd(d: int, f: int, key: int) -> list[int]:
 
 
 # ---------------------------------------------------------------- sampling
-def sample_bounds(N: int, E: int, S: int, fanouts) -> tuple[int, int]:
-    """Per-batch upper bounds on node and edge counts (negative fan-out = all)."""
-    n, e, layer = S, 0, S
+def sample_bounds(N: int, E: int, S: int, fanouts, layered=False) -> tuple[int, int]:
+    """Per-batch upper bounds on node and edge counts (negative fan-out = all):
+    a hop adds at most min(f * frontier, E) edges and as many nodes."""
+    n, e, front = S, 0, S
     for f in fanouts:
-        if f < 0:
-            return N, E
-        layer = layer * f
-        e += layer
-        n += layer
-        if n >= N and e >= E:
-            break
-    return min(n, N), min(e, E)
+        hop_e = E if f < 0 else min(front * f, E)
+        e += hop_e
+        n = min(n + hop_e, N)
+        front = n if layered else min(hop_e, N)
+    return n, (e if layered else min(e, E))
 
 
-def sample_group(offsets, indices, seeds, fanouts, rng_seed, batch_base=0):
+def sample_group(offsets, indices, seeds, fanouts, rng_seed, batch_base=0, layered=False):
     """Group sampling.  seeds: int32 [B, S].  Returns a dict with per-batch
     numpy arrays: nodes[b], hop_ptr[b], edge_src[b], edge_dst[b], edge_ptr[b]."""
     off = np.ascontiguousarray(offsets, dtype=np.int64)
@@ -131,7 +129,7 @@ def sample_group(offsets, indices, seeds, fanouts, rng_seed, batch_base=0):
     K = len(fo)
     N = len(off) - 1
     E = int(off[-1])
-    ncap, ecap = sample_bounds(N, E, S, [int(x) for x in fo])
+    ncap, ecap = sample_bounds(N, E, S, [int(x) for x in fo], layered)
     ncap, ecap = max(ncap, 1), max(ecap, 1)
     nodes = np.zeros(B * ncap, dtype=np.int32)
     hop = np.zeros(B * (K + 2), dtype=np.int64)
@@ -140,7 +138,8 @@ def sample_group(offsets, indices, seeds, fanouts, rng_seed, batch_base=0):
     ep = np.zeros(B * (K + 1), dtype=np.int64)
     need = np.zeros(2, dtype=np.int64)
     rc = lib().or_sample_group(N, E, _p(off, I64P), _p(idx, I32P), _p(sd, I32P), B, S, batch_base,
-                               _p(fo, I32P), K, rng_seed & (2**64 - 1), ncap, _p(nodes, I32P),
+                               _p(fo, I32P), K, rng_seed & (2**64 - 1), int(layered), ncap,
+                               _p(nodes, I32P),
                                _p(hop, I64P), ecap, _p(es, I32P), _p(ed, I32P), _p(ep, I64P),
                                _p(need, I64P))
     if rc:

@@ -101,9 +101,13 @@ static int64_t draw_positions(int64_t d, int32_t f, uint64_t rng_seed, uint64_t 
   return f;
 }
 
+/* layered = 0: only the nodes first reached at hop k sample at hop k+1 (§2,
+ * Fig. 1: the seed does not sample again at the second step).
+ * layered = 1: every node of the mini-batch so far samples at each hop
+ * (layer-wise blocks as DGL builds them). */
 int or_sample_group(int64_t N, int64_t E, const int64_t *off, const int32_t *idx,
                     const int32_t *seeds, int32_t B, int32_t S, int64_t batch_base,
-                    const int32_t *fanouts, int32_t K, uint64_t rng_seed,
+                    const int32_t *fanouts, int32_t K, uint64_t rng_seed, int32_t layered,
                     int64_t node_cap, int32_t *nodes, int64_t *hop_ptr,
                     int64_t edge_cap, int32_t *edge_src, int32_t *edge_dst,
                     int64_t *edge_ptr, int64_t *need /* [2]: max n_b, max e_b */) {
@@ -197,7 +201,7 @@ int or_sample_group(int64_t N, int64_t E, const int64_t *off, const int32_t *idx
         ++e;
       }
       hp[k + 1] = n;
-      front_begin = front_end;
+      front_begin = layered ? 0 : front_end;
       front_end = n;
     }
     if (rc == 0) {

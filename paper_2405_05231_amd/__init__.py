@@ -57,10 +57,12 @@ def _workspace(nbytes: int, device, ws: torch.Tensor | None):
     return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
 
 
-def sample_bounds(num_nodes: int, num_edges: int, S: int, fanouts) -> tuple[int, int]:
+def sample_bounds(num_nodes: int, num_edges: int, S: int, fanouts,
+                  layered: bool = False) -> tuple[int, int]:
     fo = (ctypes.c_int32 * max(len(fanouts), 1))(*fanouts)
     nc, ec = ctypes.c_int64(), ctypes.c_int64()
-    check(_L.dg_sample_bounds(num_nodes, num_edges, S, fo, len(fanouts), ctypes.byref(nc),
+    check(_L.dg_sample_bounds(num_nodes, num_edges, S, fo, len(fanouts),
+                              _lib.DG_SAMPLE_LAYERED if layered else 0, ctypes.byref(nc),
                               ctypes.byref(ec)))
     return nc.value, ec.value
 
@@ -91,10 +93,12 @@ def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tens
                  rng_seed: int, batch_base: int = 0, node_cap: int | None = None,
                  edge_cap: int | None = None, out: SampleResult | None = None,
                  workspace: torch.Tensor | None = None, stream=None, timing: bool = False,
-                 membership: torch.Tensor | None = None) -> SampleResult:
+                 membership: torch.Tensor | None = None, layered: bool = False
+                 ) -> SampleResult:
     """Group sampling (dg_sample_group).  seeds: int32 [B, S] on the GPU.
     membership: optional int64 [N] tensor that receives the (node, batch)
-    membership mask (bit b of word u = u is in batch b)."""
+    membership mask (bit b of word u = u is in batch b).  layered: every node
+    of the mini-batch so far samples at each hop (DGL-style layer blocks)."""
     dev = offsets.device
     _need(offsets, "offsets", torch.int64)
     _need(indices, "indices", torch.int32, dev)
@@ -113,7 +117,7 @@ def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tens
     if out is not None:
         node_cap, edge_cap = out.nodes.shape[1], out.edge_src.shape[1]
     else:
-        bn, be = sample_bounds(N, E, S, fanouts)
+        bn, be = sample_bounds(N, E, S, fanouts, layered)
         node_cap = bn if node_cap is None else node_cap
         edge_cap = be if edge_cap is None else edge_cap
         out = SampleResult(
@@ -129,7 +133,7 @@ def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tens
     sz, tm = Sizes(), Timing()
     st = _L.dg_sample_group(
         ctypes.byref(g), _ptr(seeds), B, S, batch_base, fo, K, rng_seed & (2**64 - 1),
-        node_cap, _ptr(out.nodes), out.hop_ptr.ctypes.data_as(_lib.I64P), edge_cap,
+        _lib.DG_SAMPLE_LAYERED if layered else 0, node_cap, _ptr(out.nodes), out.hop_ptr.ctypes.data_as(_lib.I64P), edge_cap,
         _ptr(out.edge_src), _ptr(out.edge_dst), out.edge_ptr.ctypes.data_as(_lib.I64P),
         _ptr(membership), _ptr(ws), ws.numel(), _stream(stream), ctypes.byref(sz),
         ctypes.byref(tm) if timing else None)

@@ -300,26 +300,33 @@ int check_err(uint32_t *err_dev, hipStream_t s) {
 using namespace dg;
 
 extern "C" int dg_sample_bounds(int64_t num_nodes, int64_t num_edges, int32_t S,
-                                const int32_t *fanouts, int32_t K, int64_t *node_cap,
-                                int64_t *edge_cap) {
+                                const int32_t *fanouts, int32_t K, uint32_t flags,
+                                int64_t *node_cap, int64_t *edge_cap) {
   if (!node_cap || !edge_cap || (K > 0 && !fanouts) || S < 1 || K < 0 || num_nodes < 1 ||
-      num_edges < 0)
+      num_edges < 0 || (flags & ~DG_SAMPLE_LAYERED))
     return set_error(DG_EINVAL, "dg_sample_bounds: bad argument");
-  // Saturating arithmetic: once a layer reaches N nodes, nothing grows further.
-  int64_t n = S, e = 0, layer = S;
-  bool all = false;
-  for (int k = 0; k < K && !all; ++k) {
-    int32_t f = fanouts[k];
-    if (f < 0) { all = true; break; }
-    if (layer > 0 && f > 0 && layer > INT64_MAX / 4 / f) { all = true; break; }
-    layer *= f;
-    e += layer;
-    n += layer;
-    if (n > num_nodes && e > num_edges) { all = true; break; }
+  const bool layered = flags & DG_SAMPLE_LAYERED;
+  // Saturating arithmetic: once a count reaches its graph bound it stays there.
+  // n = nodes so far, front = nodes that sample at the next hop; per hop the
+  // edges are distinct CSR edges (each frontier node samples once), so a hop
+  // adds at most min(f * front, E) edges.
+  const int64_t big = INT64_MAX / 4;
+  int64_t n = S, e = 0, front = S;
+  for (int k = 0; k < K; ++k) {
+    const int32_t f = fanouts[k];
+    int64_t hop_e = f < 0 ? num_edges : (front > big / (f > 0 ? f : 1) ? big : front * f);
+    if (hop_e > num_edges) hop_e = num_edges;
+    e = e > big - hop_e ? big : e + hop_e;
+    const int64_t grown = n > big - hop_e ? big : n + hop_e;
+    front = layered ? (grown < num_nodes ? grown : num_nodes) : hop_e;
+    n = grown < num_nodes ? grown : num_nodes;
+    if (front > num_nodes) front = num_nodes;
   }
-  *node_cap = all ? num_nodes : (n < num_nodes ? n : num_nodes);
-  *edge_cap = all ? num_edges : (e < num_edges ? e : num_edges);
-  if (*edge_cap < 1) *edge_cap = 1;
+  // without layering a node samples at most once, so a batch's edges are
+  // distinct CSR edges
+  if (!layered && e > num_edges) e = num_edges;
+  *node_cap = n;
+  *edge_cap = e < 1 ? 1 : e;
   return DG_OK;
 }
 
@@ -335,7 +342,8 @@ extern "C" size_t dg_sample_workspace_bytes(int64_t num_nodes, int32_t B, int64_
 
 extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S,
                                int64_t batch_base, const int32_t *fanouts, int32_t K,
-                               uint64_t rng_seed, int64_t node_cap, int32_t *nodes,
+                               uint64_t rng_seed, uint32_t flags, int64_t node_cap,
+                               int32_t *nodes,
                                int64_t *hop_ptr, int64_t edge_cap, int32_t *edge_src,
                                int32_t *edge_dst, int64_t *edge_ptr, uint64_t *membership,
                                void *ws, size_t ws_bytes, hipStream_t stream, dg_sizes *sizes,
@@ -346,6 +354,9 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
   if (!g->offsets || (g->num_edges > 0 && !g->indices) || g->num_nodes < 1 ||
       g->num_nodes > 0x7fffffffll || g->num_edges < 0)
     return set_error(DG_EINVAL, "dg_sample_group: bad CSR description");
+  if (flags & ~DG_SAMPLE_LAYERED)
+    return set_error(DG_EINVAL, "dg_sample_group: unknown flags 0x%x", flags);
+  const bool layered = flags & DG_SAMPLE_LAYERED;
   if (B < 1 || B > DG_MAX_BATCHES || S < 1 || K < 0 || node_cap < S || edge_cap < 0 ||
       (int64_t)S > g->num_nodes)
     return set_error(DG_EINVAL, "dg_sample_group: bad sizes (B=%d S=%d K=%d node_cap=%lld)", B,
@@ -489,7 +500,8 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       }
     }
     for (int b = 0; b < B; ++b) {
-      fbeg[b] = n_b[b];
+      // next frontier: the nodes new at this hop, or (layered) every node so far
+      fbeg[b] = layered ? 0 : n_b[b];
       n_b[b] += new_b[b];
       fend[b] = n_b[b];
       hop_ptr[(int64_t)b * (K + 2) + k + 1] = n_b[b];

@@ -52,7 +52,10 @@ def test_sample_bounds(L):
     assert dg.sample_bounds(10_000, 105_000, 64, [5, 5]) == (64 * 31, 64 * 30)
     assert dg.sample_bounds(100_000_000, 1_600_000_000, 1024, [15, 10, 5]) == (937_984, 936_960)
     assert dg.sample_bounds(1000, 5000, 4, [-1, 2]) == (1000, 5000)
-    assert dg.sample_bounds(50, 10**9, 8, [10, 10]) == (50, 880)
+    assert dg.sample_bounds(50, 10**9, 8, [10, 10]) == (50, 580)  # hop-1 frontier <= N
+    # layered: every node so far samples again at each hop
+    assert dg.sample_bounds(10**6, 10**9, 4, [2, 3], layered=True) == (4 * 3 * 4, 8 + 12 * 3)
+    assert dg.sample_bounds(1000, 5000, 4, [-1, 2], layered=True) == (1000, 7000)
     with pytest.raises(dg.DGError):
         dg.sample_bounds(0, 10, 1, [1])
 
@@ -71,8 +74,8 @@ def test_host_side_argument_errors(L):
     from paper_2405_05231_amd import _lib
     sizes = _lib.Sizes()
     # null CSR / outputs: rejected before any device call
-    rc = L.dg_sample_group(None, None, 1, 1, 0, None, 0, 0, 1, None, None, 1, None, None, None,
-                           None, None, 0, None, ctypes.byref(sizes), None)
+    rc = L.dg_sample_group(None, None, 1, 1, 0, None, 0, 0, 0, 1, None, None, 1, None, None,
+                           None, None, None, 0, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL
     assert b"null" in L.dg_last_error()
     g = _lib.Csr(10, 0, 0x1000, 0)
@@ -81,13 +84,17 @@ def test_host_side_argument_errors(L):
     fo = (ctypes.c_int32 * 1)(2)
     fake = ctypes.c_void_p(0x1000)
     # B out of range
-    rc = L.dg_sample_group(ctypes.byref(g), fake, 65, 1, 0, fo, 1, 0, 4, fake, hop, 4, fake, fake,
-                           ep, None, fake, 1 << 20, None, ctypes.byref(sizes), None)
+    rc = L.dg_sample_group(ctypes.byref(g), fake, 65, 1, 0, fo, 1, 0, 0, 4, fake, hop, 4, fake,
+                           fake, ep, None, fake, 1 << 20, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL
     # workspace missing
-    rc = L.dg_sample_group(ctypes.byref(g), fake, 1, 1, 0, fo, 1, 0, 4, fake, hop, 4, fake, fake,
-                           ep, None, None, 0, None, ctypes.byref(sizes), None)
+    rc = L.dg_sample_group(ctypes.byref(g), fake, 1, 1, 0, fo, 1, 0, 0, 4, fake, hop, 4, fake,
+                           fake, ep, None, None, 0, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EWORKSPACE
+    # unknown flags
+    rc = L.dg_sample_group(ctypes.byref(g), fake, 1, 1, 0, fo, 1, 0, 8, 4, fake, hop, 4, fake,
+                           fake, ep, None, fake, 1 << 20, None, ctypes.byref(sizes), None)
+    assert rc == _lib.DG_EINVAL
     # pack: B = 0, row_bytes = 0, counts beyond the stride
     cnt = (ctypes.c_int64 * 2)(3, 9)
     ph = (ctypes.c_int64 * 3)()

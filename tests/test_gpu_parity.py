@@ -79,10 +79,10 @@ def compare_packing(pr, ref, B, full_rows=True):
 
 
 def oracle_full(orc, off, idx, seeds, fanouts, rng_seed, feats, cache_slot, cache_nodes,
-                batch_base=0):
+                batch_base=0, layered=False):
     X = to_np(feats)
     ref_s = orc.sample_group(to_np(off), to_np(idx), to_np(seeds), fanouts, rng_seed,
-                             batch_base=batch_base)
+                             batch_base=batch_base, layered=layered)
     ref_p = orc.pack_group(X, to_np(cache_slot), ref_s["nodes"])
     R = X[0].nbytes
     cache = X[to_np(cache_nodes)] if cache_nodes.numel() else np.zeros((0,) + X.shape[1:], X.dtype)
@@ -98,7 +98,8 @@ def check_all(dg, orc, off, idx, seeds, fanouts, rng_seed, feats, cache_slot, ca
     sr, pr, Y, _ = run_path(dg, off, idx, seeds, fanouts, rng_seed, feats, cache_slot,
                             cache_nodes, batch_base, sample_kw)
     ref_s, ref_p, ref_y = oracle_full(orc, off, idx, seeds, fanouts, rng_seed, feats, cache_slot,
-                                      cache_nodes, batch_base)
+                                      cache_nodes, batch_base,
+                                      layered=(sample_kw or {}).get("layered", False))
     B = seeds.shape[0]
     compare_sampling(sr, ref_s, B)
     compare_packing(pr, ref_p, B)
@@ -115,6 +116,12 @@ def test_tiny_workload_T(dg, orc):
     w = synth.make_workload("T")
     check_all(dg, orc, w.offsets, w.indices, w.seeds, list(w.cfg.fanouts), w.rng_seed, w.feats,
               w.cache_slot, w.cache_nodes)
+
+
+def test_tiny_workload_T_layered(dg, orc):
+    w = synth.make_workload("T")
+    check_all(dg, orc, w.offsets, w.indices, w.seeds, list(w.cfg.fanouts), w.rng_seed, w.feats,
+              w.cache_slot, w.cache_nodes, sample_kw={"layered": True})
 
 
 def test_tiny_workload_T_is_deterministic(dg):
@@ -171,8 +178,9 @@ CASES = [
 ]
 
 
+@pytest.mark.parametrize("layered", [False, True])
 @pytest.mark.parametrize("case", range(len(CASES)))
-def test_edge_cases(dg, orc, case):
+def test_edge_cases(dg, orc, case, layered):
     n, maxdeg, B, S, fan, dim, dtype, share = CASES[case]
     rnd = random.Random(900 + case)
     off, idx = random_case(rnd, n, maxdeg) if maxdeg else (
@@ -188,7 +196,7 @@ def test_edge_cases(dg, orc, case):
     slot = torch.full((n,), -1, dtype=torch.int32)
     slot[cache_nodes] = torch.arange(ncache, dtype=torch.int32)
     check_all(dg, orc, off, idx, seeds, fan, 12345 + case, feats, slot, cache_nodes,
-              batch_base=case)
+              batch_base=case, sample_kw={"layered": layered})
 
 
 def test_fig1_example_on_device(dg, orc):

@@ -124,6 +124,21 @@ def test_fig1_worked_example(orc):
     assert edges == ex["edges_global"]
 
 
+def test_fig1_worked_example_layered(orc):
+    """Layer-wise variant: at step 2 the seed samples again (its two neighbours
+    are already in the mini-batch), so hop 2 repeats (v0,v3),(v0,v5) and the
+    node list is unchanged."""
+    fx = load("fig1_sampling.json")
+    off, idx = csr_from_rows(fx["num_nodes"], fx["rows"])
+    r = orc.sample_group(off, idx, np.array(fx["seeds"], dtype=np.int32), fx["fanouts"], 0,
+                         layered=True)
+    nodes = r["nodes"][0]
+    assert nodes.tolist() == fx["expect"]["nodes"]
+    edges = [[int(nodes[s]), int(nodes[d])] for s, d in zip(r["edge_src"][0], r["edge_dst"][0])]
+    assert edges == [[0, 3], [0, 5], [0, 3], [0, 5], [3, 2], [3, 7], [5, 9], [5, 11]]
+    assert r["edge_ptr"][0].tolist() == [0, 2, 8]
+
+
 def test_fig3_worked_example(orc):
     fx = load("fig3_assembling.json")
     n = fx["num_nodes"]
@@ -167,9 +182,10 @@ def random_csr(rnd, n, maxdeg):
     return csr_from_rows(n, rows), rows
 
 
-def check_sample_invariants(rows, seeds, fanouts, r):
+def check_sample_invariants(rows, seeds, fanouts, r, layered=False):
     """Independent brute-force check of a sampling result (every rule except the
-    identity of the random subset)."""
+    identity of the random subset).  layered: every node so far samples at
+    each hop, instead of only the previous hop's new nodes."""
     K = len(fanouts)
     for b, sd in enumerate(seeds):
         nodes = [int(x) for x in r["nodes"][b]]
@@ -183,7 +199,7 @@ def check_sample_invariants(rows, seeds, fanouts, r):
         seen = set(nodes[:len(sd)])
         for k in range(1, K + 1):
             f = fanouts[k - 1]
-            frontier = list(range(hop[k - 1], hop[k]))
+            frontier = list(range(0 if layered else hop[k - 1], hop[k]))
             es = list(range(ep[k - 1], ep[k]))
             # parents: frontier positions, non-decreasing, each drawing min(d, f)
             parents = [src[e] for e in es]
@@ -210,8 +226,9 @@ def check_sample_invariants(rows, seeds, fanouts, r):
         assert all(0 <= x < len(nodes) for x in src + dst)
 
 
+@pytest.mark.parametrize("layered", [False, True])
 @pytest.mark.parametrize("trial", range(40))
-def test_sampling_bruteforce(orc, trial):
+def test_sampling_bruteforce(orc, trial, layered):
     rnd = random.Random(1000 + trial)
     n = rnd.randint(2, 40)
     (off, idx), rows = random_csr(rnd, n, rnd.choice([2, 5, 9]))
@@ -221,8 +238,8 @@ def test_sampling_bruteforce(orc, trial):
     K = rnd.randint(0, 3)
     fan = [rnd.choice([-1, 0, 1, 2, 3, 5]) for _ in range(K)]
     r = orc.sample_group(off, idx, np.array(seeds, dtype=np.int32), fan, rnd.getrandbits(64),
-                         batch_base=rnd.randint(0, 100))
-    check_sample_invariants(rows, seeds, fan, r)
+                         batch_base=rnd.randint(0, 100), layered=layered)
+    check_sample_invariants(rows, seeds, fan, r, layered)
 
 
 def test_sampling_batches_independent(orc):
@@ -238,8 +255,9 @@ def test_sampling_batches_independent(orc):
             assert np.array_equal(x, y)
 
 
+@pytest.mark.parametrize("layered", [False, True])
 @pytest.mark.parametrize("trial", range(12))
-def test_bfs_special_case(orc, trial):
+def test_bfs_special_case(orc, trial, layered):
     """With f < 0 (or f >= max degree) sampling is deterministic and the node
     list is the seeds followed by the breadth-first layers, each ascending."""
     rnd = random.Random(50 + trial)
@@ -249,7 +267,7 @@ def test_bfs_special_case(orc, trial):
     seeds = rnd.sample(range(n), S)
     K = rnd.randint(1, 4)
     fan = [rnd.choice([-1, 6, 100]) for _ in range(K)]
-    r = orc.sample_group(off, idx, np.array([seeds], dtype=np.int32), fan, 1)
+    r = orc.sample_group(off, idx, np.array([seeds], dtype=np.int32), fan, 1, layered=layered)
     dist = {s: 0 for s in seeds}
     q = deque(seeds)
     while q:
@@ -262,7 +280,10 @@ def test_bfs_special_case(orc, trial):
     for k in range(1, K + 1):
         want += sorted(u for u, d in dist.items() if d == k)
     assert r["nodes"][0].tolist() == want
-    frontier_edges = sum(len(rows[v]) for v, d in dist.items() if d < K)
+    if layered:  # hop k: every node within distance k-1 samples all its neighbours
+        frontier_edges = sum(len(rows[v]) * (K - d) for v, d in dist.items() if d < K)
+    else:
+        frontier_edges = sum(len(rows[v]) for v, d in dist.items() if d < K)
     assert r["edge_ptr"][0][K] == frontier_edges
 
 
