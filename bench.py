@@ -68,10 +68,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calib", action="store_true",
                     help="also run a plain copy of known size (counter calibration)")
-    ap.add_argument("--experiment", choices=["pack_ab", "cache", "layered"], default=None,
+    ap.add_argument("--experiment", choices=["pack_ab", "cache", "layered", "minhash"],
+                    default=None,
                     help="instead of the step benchmark: batched vs individual packing "
                          "(pack_ab), access-frequency vs in-degree cache (cache), or "
-                         "layer-wise (DGL-style) vs new-node frontier sampling (layered)")
+                         "layer-wise (DGL-style) vs new-node frontier sampling (layered), or "
+                         "disk-cache pages touched under ID vs MinHash order (minhash)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -102,7 +104,8 @@ def main():
     stream = torch.cuda.current_stream()
     if args.experiment:
         out = {"pack_ab": experiment_pack_ab, "cache": experiment_cache,
-               "layered": experiment_layered}[args.experiment](dg, w, cfg, args.steps)
+               "layered": experiment_layered,
+               "minhash": experiment_minhash}[args.experiment](dg, w, cfg, args.steps)
         print(json.dumps(out), flush=True)
         return
 
@@ -321,6 +324,49 @@ def experiment_layered(dg, w, cfg, reps):
                      "edges_per_s": round(sr.sizes["total_edges"] / t, 1)}
     return {"experiment": "sampling frontier rule", "workload": cfg.name, "fanouts":
             list(cfg.fanouts), "batches": cfg.B, **res}
+
+
+def experiment_minhash(dg, w, cfg, reps, k=4, page_bytes=4096):
+    """Disk-cache reordering by MinHash (§5.1, Alg. 1): the non-cached nodes the
+    group requires form the disk cache V_d; count the 4 KiB pages each
+    mini-batch touches when V_d is laid out in ID order and in MinHash order."""
+    import torch
+    B, R = cfg.B, cfg.row_bytes
+    rpp = max(1, page_bytes // R)  # rows per page
+    mem = torch.empty(cfg.n, dtype=torch.int64, device="cuda")
+    sr = dg.sample_group(w.offsets, w.indices, w.seeds, list(cfg.fanouts), w.rng_seed,
+                         membership=mem)
+    accessed = (mem != 0).nonzero().squeeze(1)
+    vd = accessed[w.cache_slot[accessed] < 0].to(torch.int32).contiguous()  # ascending IDs
+    g = torch.Generator().manual_seed(cfg.seed + 1)
+    perms = torch.stack([torch.randperm(B, generator=g) for _ in range(k)]).to(torch.int32).cuda()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ts = []
+    for _ in range(reps + 1):
+        ev[0].record()
+        order, sig = dg.minhash_order(mem, B, vd, perms)
+        ev[1].record()
+        ev[1].synchronize()
+        ts.append(ev[0].elapsed_time(ev[1]))
+
+    def pages(layout):
+        pos = torch.full((cfg.n,), -1, dtype=torch.int64, device="cuda")
+        pos[layout.long()] = torch.arange(layout.numel(), device="cuda")
+        total = 0
+        for b in range(B):
+            p = pos[sr.batch_nodes(b).long()]
+            p = p[p >= 0] // rpp
+            total += int(torch.unique(p).numel())
+        return total
+
+    lower = sum(-(-int((pos_b := w.cache_slot[sr.batch_nodes(b).long()] < 0).sum()) // rpp)
+                for b in range(B))
+    id_pages, mh_pages = pages(vd), pages(order)
+    return {"experiment": "disk-cache pages touched, ID order vs MinHash order",
+            "workload": cfg.name, "disk_cache_entries": int(vd.numel()), "hash_functions": k,
+            "rows_per_page": rpp, "order_ms": round(_median(ts[1:]), 3),
+            "pages_id_order": id_pages, "pages_minhash_order": mh_pages,
+            "pages_lower_bound": lower, "reduction": round(id_pages / max(mh_pages, 1), 3)}
 
 
 def cpu_baseline(w, cfg, nb):

@@ -316,6 +316,30 @@ int dg_cache_by_frequency(const uint64_t *membership, int64_t N, int32_t B, int6
 int dg_gather_rows(const void *feats, int64_t N, int64_t row_bytes, const int32_t *ids,
                    int64_t n, void *out, int32_t *status, hipStream_t stream);
 
+/* Workspace bytes dg_minhash_order needs for m disk-cache entries. */
+size_t dg_minhash_workspace_bytes(int64_t m);
+
+/* Disk-cache node reordering by MinHash (§5.1 "Node reordering for disk
+ * cache", Alg. 1, after HashOrder): features that the same graph samples
+ * require are placed next to each other.
+ *   membership  [N] uint64: bit i of membership[v] set iff graph sample
+ *               (mini-batch) i requires v, i < B (as dg_sample_group returns).
+ *   entries     [m] int32: the disk-cache nodes V_d, in their current order.
+ *   perms       [k*B] int32 (device): hash function j maps sample i to
+ *               perms[j*B + i], a permutation of 0..B-1 (the random
+ *               permutations are drawn by the caller).
+ *   S(v) = min over every j and every sample i requiring v of perms[j*B + i]
+ *   (one running minimum across the k functions, as the algorithm writes it);
+ *   S(v) = infinity when no sample requires v.
+ *   order       [m] int32 out: V_d stably sorted by S (ties keep entry order,
+ *               entries required by no sample last).
+ *   signature   [m] int32 out, optional: S of each entry (-1 = infinity).
+ * Returns after completion.  DG_EINVAL for null pointers, B outside 1..64,
+ * k < 1, an entry outside [0, N) or a hash value outside [0, B). */
+int dg_minhash_order(const uint64_t *membership, int64_t N, int32_t B, const int32_t *entries,
+                     int64_t m, const int32_t *perms, int32_t k, int32_t *order,
+                     int32_t *signature, void *ws, size_t ws_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

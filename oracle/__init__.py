@@ -65,6 +65,9 @@ def lib():
         L.or_cache_by_frequency.restype = ctypes.c_int
         L.or_cache_by_frequency.argtypes = [ctypes.c_int64, ctypes.c_int32, I32P, ctypes.c_int64,
                                             I64P, ctypes.c_int64, I32P, I32P, I64P]
+        L.or_minhash_order.restype = ctypes.c_int
+        L.or_minhash_order.argtypes = [ctypes.c_int64, ctypes.c_int32, I32P, ctypes.c_int64, I64P,
+                                       I32P, ctypes.c_int64, I32P, ctypes.c_int32, I32P, I32P]
         L.or_assemble_batch.restype = ctypes.c_int
         L.or_assemble_batch.argtypes = [VP, ctypes.c_int64, VP, ctypes.c_int64, I32P,
                                         ctypes.c_int64, ctypes.c_int64, VP]
@@ -235,3 +238,24 @@ def cache_by_frequency(N, node_lists, cache_rows):
     if rc:
         raise OracleError(f"or_cache_by_frequency rc={rc}")
     return slot, cn[:cache_rows], int(cached[0])
+
+
+def minhash_order(N, node_lists, entries, perms):
+    """Disk-cache reordering by MinHash (Alg. 1).  perms: int32 [k, B].
+    Returns (order int32 [m], signature int32 [m], -1 = in no sample)."""
+    B = len(node_lists)
+    counts = np.array([len(x) for x in node_lists], dtype=np.int64)
+    stride = max(int(counts.max()) if B else 0, 1)
+    nodes = np.zeros(B * stride, dtype=np.int32)
+    for b, x in enumerate(node_lists):
+        nodes[b * stride:b * stride + len(x)] = x
+    ent = np.ascontiguousarray(entries, dtype=np.int32)
+    pm = np.ascontiguousarray(perms, dtype=np.int32)
+    m = len(ent)
+    order = np.zeros(max(m, 1), dtype=np.int32)
+    sig = np.zeros(max(m, 1), dtype=np.int32)
+    rc = lib().or_minhash_order(N, B, _p(nodes, I32P), stride, _p(counts, I64P), _p(ent, I32P),
+                                m, _p(pm, I32P), pm.shape[0], _p(order, I32P), _p(sig, I32P))
+    if rc:
+        raise OracleError(f"or_minhash_order rc={rc}")
+    return order[:m], sig[:m]

@@ -375,3 +375,48 @@ int or_cache_by_frequency(int64_t N, int32_t B, const int32_t *nodes, int64_t no
   free(count);
   return 0;
 }
+
+/* ---------------------------------------------------------------------------
+ * Disk-cache reordering by MinHash (§5.1, Alg. 1), step by step: S starts at
+ * infinity for every disk-cache entry; for every graph sample i and every
+ * disk-cached node v it requires, and every hash function j, S(v) becomes
+ * min(S(v), H_j(i)); the entries are then sorted by S (stably, so ties keep
+ * entry order).  H_j(i) = perms[j*B + i] (permutations drawn by the caller).
+ * ------------------------------------------------------------------------- */
+typedef struct { int64_t s; int64_t pos; } or_sig;
+
+static int cmp_sig(const void *a, const void *b) {
+  const or_sig *x = (const or_sig *)a, *y = (const or_sig *)b;
+  if (x->s != y->s) return x->s < y->s ? -1 : 1;
+  return (x->pos > y->pos) - (x->pos < y->pos);
+}
+
+int or_minhash_order(int64_t N, int32_t B, const int32_t *nodes, int64_t node_stride,
+                     const int64_t *node_count, const int32_t *entries, int64_t m,
+                     const int32_t *perms, int32_t k, int32_t *order, int32_t *signature) {
+  const int64_t INF = INT64_MAX;
+  int64_t *where = (int64_t *)malloc((size_t)N * sizeof(int64_t)); /* entry index of v, or -1 */
+  or_sig *sig = (or_sig *)malloc((size_t)(m + 1) * sizeof(or_sig));
+  for (int64_t v = 0; v < N; ++v) where[v] = -1;
+  for (int64_t e = 0; e < m; ++e) {
+    if (entries[e] < 0 || entries[e] >= N) { free(where); free(sig); return -1; }
+    where[entries[e]] = e;
+    sig[e].s = INF;
+    sig[e].pos = e;
+  }
+  for (int32_t i = 0; i < B; ++i)                      /* every graph sample */
+    for (int64_t t = 0; t < node_count[i]; ++t) {
+      int32_t v = nodes[(int64_t)i * node_stride + t];
+      if (v < 0 || v >= N || where[v] < 0) continue;   /* V_i intersect V_d */
+      for (int32_t j = 0; j < k; ++j) {                /* every hash function */
+        int64_t h = perms[(int64_t)j * B + i];
+        if (h < sig[where[v]].s) sig[where[v]].s = h;
+      }
+    }
+  for (int64_t e = 0; e < m; ++e) signature[e] = sig[e].s == INF ? -1 : (int32_t)sig[e].s;
+  qsort(sig, (size_t)m, sizeof(or_sig), cmp_sig);
+  for (int64_t r = 0; r < m; ++r) order[r] = entries[sig[r].pos];
+  free(where);
+  free(sig);
+  return 0;
+}

@@ -19,7 +19,8 @@ from ._lib import (DG_ECAPACITY, DG_MAX_BATCHES, DG_OK, DGError, Csr, Sizes, Tim
                    load)
 
 __all__ = ["sample_bounds", "sample_group", "pack_group", "assemble_batch", "cache_by_frequency",
-           "gather_rows", "pack_individual", "DGError", "SampleResult", "PackResult", "version"]
+           "gather_rows", "pack_individual", "minhash_order", "DGError", "SampleResult",
+           "PackResult", "version"]
 
 _L = load()
 
@@ -307,3 +308,24 @@ def pack_individual(feats: torch.Tensor, packed_ids: torch.Tensor, packed_ptr_ho
         if hi > lo:
             gather_rows(feats, packed_ids[lo:hi], out=packed[lo:hi], stream=stream)
     return packed
+
+
+def minhash_order(membership: torch.Tensor, B: int, entries: torch.Tensor, perms: torch.Tensor,
+                  workspace: torch.Tensor | None = None, stream=None):
+    """Disk-cache reordering by MinHash (dg_minhash_order).  perms: int32
+    [k, B] on the GPU, each row a permutation of 0..B-1.  Returns (order
+    int32 [m], signature int32 [m], -1 = in no sample)."""
+    _need(membership, "membership", torch.int64)
+    dev = membership.device
+    _need(entries, "entries", torch.int32, dev)
+    _need(perms, "perms", torch.int32, dev)
+    if perms.dim() != 2 or perms.shape[1] != B:
+        raise ValueError("perms must be [k, B]")
+    m = entries.numel()
+    order = torch.empty(max(m, 1), dtype=torch.int32, device=dev)
+    sig = torch.empty(max(m, 1), dtype=torch.int32, device=dev)
+    ws = _workspace(_L.dg_minhash_workspace_bytes(m), dev, workspace)
+    check(_L.dg_minhash_order(_ptr(membership), membership.numel(), B, _ptr(entries), m,
+                              _ptr(perms), perms.shape[0], _ptr(order), _ptr(sig), _ptr(ws),
+                              ws.numel(), _stream(stream)))
+    return order[:m], sig[:m]

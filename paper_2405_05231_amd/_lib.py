@@ -64,6 +64,8 @@ SIGNATURES = {
     "dg_cache_workspace_bytes": (SZ, [I64]),
     "dg_cache_by_frequency": (ctypes.c_int, [VP, I64, I32, I64, VP, VP, I64P, VP, SZ, VP]),
     "dg_gather_rows": (ctypes.c_int, [VP, I64, I64, VP, I64, VP, VP, VP]),
+    "dg_minhash_workspace_bytes": (SZ, [I64]),
+    "dg_minhash_order": (ctypes.c_int, [VP, I64, I32, VP, I64, VP, I32, VP, VP, VP, SZ, VP]),
 }
 
 _lib = None

@@ -9,9 +9,13 @@
 //
 // Frequencies: a node's count is the number of mini-batches of the group that
 // require it, i.e. the popcount of its membership word.  Ranking (count
-// descending, then ID ascending) is a stable counting sort over 65 keys: per
-// block counts of every key, a scan down each key's column, then ranks from
-// block bases + wave prefixes + ballot prefixes, with no sort.
+// descending, then ID ascending) is a stable counting sort over 65 keys.
+//
+// The same counting sort orders the disk-cache entries by MinHash value
+// (§5.1, Alg. 1): with k hash functions H_j (permutations of the sample IDs,
+// given as input), S(v) is the minimum of H_j(i) over every hash function j
+// and every sample i that requires v, which equals the minimum over those
+// samples of M(i) = min_j H_j(i); entries are then sorted by S.
 #include <initializer_list>
 #include <string.h>
 
@@ -20,32 +24,71 @@
 namespace dg {
 namespace {
 
-constexpr int KEYS = 65;           // popcounts 0..64
+constexpr int KEYS = 65;  // keys 0..64
 constexpr int CF_WAVES = 4;
 constexpr int CF_THREADS = 64 * CF_WAVES;
 constexpr int CF_ROUNDS = 16;
 constexpr int CF_BLOCK = 64 * CF_ROUNDS * CF_WAVES;
 
-struct FreqScan {
+// A stable counting sort of a list by a key in 0..64: per-block counts of
+// every key, a scan down each key's column, then ranks from block bases +
+// earlier waves + earlier rounds + ballot prefixes.  Two uses:
+//   FREQ:    list = nodes 0..N-1, key = access count (popcount of the
+//            membership word), ranked by count descending;
+//   MINHASH: list = the disk-cache entries V_d, key = the entry's MinHash
+//            value (64 = in no sample), ranked ascending.
+enum Mode { FREQ = 0, MINHASH = 1 };
+
+struct KeySort {
   const uint64_t *mask;
   uint64_t keep;      // bits of the group's batches
-  int64_t N;
+  int64_t N;          // nodes
+  int64_t n;          // list length
   int64_t nblk;
   uint32_t *cnt;      // [nblk][KEYS]
   int64_t *base;      // [nblk][KEYS] exclusive scans down each key
   int64_t *totals;    // [KEYS]
-  int64_t first[KEYS];  // rank of the first node of each key (host-computed)
-  int64_t cap;          // cache rows
+  int64_t first[KEYS];  // rank of the first element of each key (host-computed)
+  uint32_t *err;
+  // FREQ outputs
+  int64_t cap;
   int32_t *cache_slot;
   int32_t *cache_nodes;
+  // MINHASH input / outputs
+  const int32_t *ids;    // V_d
+  const int32_t *minv;   // [64] min over hash functions of each sample's value
+  int32_t *order;        // V_r
+  int32_t *signature;    // S(v) per entry (-1: in no sample)
 };
 
-__device__ __forceinline__ int key_of(const FreqScan &a, int64_t u) {
-  return u < a.N ? __popcll(a.mask[u] & a.keep) : -1;
+template <int MODE>
+__device__ __forceinline__ int key_of(const KeySort &a, int64_t i, const int32_t *s_minv) {
+  if (i >= a.n) return -1;
+  if (MODE == FREQ) return __popcll(a.mask[i] & a.keep);
+  const int32_t v = a.ids[i];
+  if (v < 0 || (int64_t)v >= a.N) {
+    atomicOr(a.err, ERR_NODE_RANGE);
+    return 64;
+  }
+  uint64_t m = a.mask[v] & a.keep;
+  int key = 64;  // S(v) = inf: v is required by no sample
+  while (m) {
+    const int b = __ffsll((long long)m) - 1;
+    m &= m - 1;
+    key = min(key, s_minv[b]);
+  }
+  return key;
 }
 
-// Counts of every key in one wave tile (lane k < KEYS-1 keeps key k's count;
-// key 64 is returned separately).
+template <int MODE>
+__device__ __forceinline__ void load_keys(const KeySort &a, int64_t t0, int lane,
+                                          const int32_t *s_minv, int (&k)[CF_ROUNDS]) {
+#pragma unroll
+  for (int r = 0; r < CF_ROUNDS; ++r) k[r] = key_of<MODE>(a, t0 + r * 64 + lane, s_minv);
+}
+
+// Counts of every key in one wave tile (lane k < 64 keeps key k's count; key 64
+// is returned separately).
 __device__ __forceinline__ void wave_key_counts(const int (&k)[CF_ROUNDS], int lane,
                                                 uint32_t *mine, uint32_t *k64) {
   uint32_t c = 0, top = 0;
@@ -66,13 +109,21 @@ __device__ __forceinline__ void wave_key_counts(const int (&k)[CF_ROUNDS], int l
   *k64 = top;
 }
 
-__global__ __launch_bounds__(CF_THREADS) void k_freq_count(FreqScan a) {
+template <int MODE>
+__device__ __forceinline__ void stage_minv(const KeySort &a, int32_t *s_minv) {
+  if (MODE == MINHASH && threadIdx.x < 64) s_minv[threadIdx.x] = a.minv[threadIdx.x];
+  __syncthreads();
+}
+
+template <int MODE>
+__global__ __launch_bounds__(CF_THREADS) void k_key_count(KeySort a) {
   __shared__ uint32_t s_cnt[CF_WAVES][KEYS];
+  __shared__ int32_t s_minv[64];
+  stage_minv<MODE>(a, s_minv);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int64_t t0 = (int64_t)blockIdx.x * CF_BLOCK + (int64_t)w * 64 * CF_ROUNDS;
   int k[CF_ROUNDS];
-#pragma unroll
-  for (int r = 0; r < CF_ROUNDS; ++r) k[r] = key_of(a, t0 + r * 64 + lane);
+  load_keys<MODE>(a, t0, lane, s_minv, k);
   uint32_t mine, top;
   wave_key_counts(k, lane, &mine, &top);
   s_cnt[w][lane] = mine;
@@ -86,18 +137,14 @@ __global__ __launch_bounds__(CF_THREADS) void k_freq_count(FreqScan a) {
 }
 
 // One block per key: exclusive scan of that key's per-block counts.
-__global__ __launch_bounds__(1024) void k_freq_scan(FreqScan a) {
+__global__ __launch_bounds__(1024) void k_key_scan(KeySort a) {
   __shared__ int64_t s_w[16];
   const int key = blockIdx.x;
   int64_t carry = 0;
   for (int64_t c0 = 0; c0 < a.nblk; c0 += 1024) {
     const int64_t i = c0 + threadIdx.x;
     const int64_t v = i < a.nblk ? (int64_t)a.cnt[(size_t)i * KEYS + key] : 0;
-    int64_t incl = v;
-    for (int o = 1; o < 64; o <<= 1) {
-      int64_t y = __shfl_up(incl, o, 64);
-      if ((threadIdx.x & 63) >= o) incl += y;
-    }
+    int64_t incl = wave_incl_sum(v);
     if ((threadIdx.x & 63) == 63) s_w[threadIdx.x >> 6] = incl;
     __syncthreads();
     int64_t before = 0, sum = 0;
@@ -112,23 +159,22 @@ __global__ __launch_bounds__(1024) void k_freq_scan(FreqScan a) {
   if (threadIdx.x == 0) a.totals[key] = carry;
 }
 
-// Ranks: rank(u) = first[key] + block base + earlier waves + earlier rounds +
-// ballot prefix.  Nodes with rank < cap are cached.
-__global__ __launch_bounds__(CF_THREADS) void k_freq_place(FreqScan a) {
+template <int MODE>
+__global__ __launch_bounds__(CF_THREADS) void k_key_place(KeySort a) {
   __shared__ uint32_t s_cnt[CF_WAVES][KEYS];
+  __shared__ int32_t s_minv[64];
+  stage_minv<MODE>(a, s_minv);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int64_t t0 = (int64_t)blockIdx.x * CF_BLOCK + (int64_t)w * 64 * CF_ROUNDS;
   int k[CF_ROUNDS];
-#pragma unroll
-  for (int r = 0; r < CF_ROUNDS; ++r) k[r] = key_of(a, t0 + r * 64 + lane);
+  load_keys<MODE>(a, t0, lane, s_minv, k);
   uint32_t mine, top;
   wave_key_counts(k, lane, &mine, &top);
   s_cnt[w][lane] = mine;
   if (lane == 0) s_cnt[w][64] = top;
   __syncthreads();
-  // running rank of key (lane) for lanes 0..63, key 64 kept uniform
   const int64_t *bb = a.base + (size_t)blockIdx.x * KEYS;
-  int64_t run = a.first[lane] + bb[lane];
+  int64_t run = a.first[lane] + bb[lane];  // running rank of key `lane`
   int64_t run64 = a.first[64] + bb[64];
   for (int j = 0; j < w; ++j) {
     run += s_cnt[j][lane];
@@ -138,7 +184,7 @@ __global__ __launch_bounds__(CF_THREADS) void k_freq_place(FreqScan a) {
 #pragma unroll
   for (int r = 0; r < CF_ROUNDS; ++r) {
     const int key = k[r];
-    const int64_t u = t0 + r * 64 + lane;
+    const int64_t i = t0 + r * 64 + lane;
     uint64_t pending = __ballot(key >= 0);
     int64_t rank = -1;
     while (pending) {
@@ -152,9 +198,14 @@ __global__ __launch_bounds__(CF_THREADS) void k_freq_place(FreqScan a) {
       else if (lane == kk) run += __popcll(bal);
     }
     if (key >= 0) {
-      const bool cached = key > 0 && rank < a.cap;
-      a.cache_slot[u] = cached ? (int32_t)rank : -1;
-      if (cached) a.cache_nodes[rank] = (int32_t)u;
+      if (MODE == FREQ) {
+        const bool cached = key > 0 && rank < a.cap;
+        a.cache_slot[i] = cached ? (int32_t)rank : -1;
+        if (cached) a.cache_nodes[rank] = (int32_t)i;
+      } else {
+        a.order[rank] = a.ids[i];
+        if (a.signature) a.signature[i] = key == 64 ? -1 : key;
+      }
     }
   }
 }
@@ -163,6 +214,46 @@ __global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
     p[i] = v;
+}
+
+// M(i) = min over the k hash functions of H_j(i); values checked to lie in [0, B).
+__global__ void k_minhash_min(const int32_t *perms, int32_t k, int32_t B, int32_t *minv,
+                              uint32_t *err) {
+  const int i = threadIdx.x;
+  if (i >= 64) return;
+  int32_t m = 64;
+  if (i < B) {
+    for (int j = 0; j < k; ++j) {
+      const int32_t h = perms[(int64_t)j * B + i];
+      if (h < 0 || h >= B) atomicOr(err, ERR_ROW_RANGE);
+      else m = min(m, h);
+    }
+  }
+  minv[i] = m;
+}
+
+int64_t key_blocks(int64_t n) { return (n + CF_BLOCK - 1) / CF_BLOCK; }
+
+void carve_keysort(KeySort &a, Carve &c) {
+  a.nblk = key_blocks(a.n);
+  a.cnt = c.take<uint32_t>((size_t)a.nblk * KEYS);
+  a.base = c.take<int64_t>((size_t)a.nblk * KEYS);
+  a.totals = c.take<int64_t>(KEYS);
+}
+
+// count pass + scans; returns the per-key totals on the host.
+template <int MODE>
+int keysort_count(KeySort &a, int64_t *totals, hipStream_t s) {
+  if (a.nblk == 0) {
+    for (int k = 0; k < KEYS; ++k) totals[k] = 0;
+    return DG_OK;
+  }
+  hipLaunchKernelGGL(k_key_count<MODE>, dim3((unsigned)a.nblk), dim3(CF_THREADS), 0, s, a);
+  hipLaunchKernelGGL(k_key_scan, dim3(KEYS), dim3(1024), 0, s, a);
+  DG_HIP(hipGetLastError());
+  DG_HIP(hipMemcpyAsync(totals, a.totals, sizeof(int64_t) * KEYS, hipMemcpyDeviceToHost, s));
+  DG_HIP(hipStreamSynchronize(s));
+  return DG_OK;
 }
 
 // ------------------------------------------------------------------ row gather
@@ -290,11 +381,11 @@ using namespace dg;
 
 extern "C" size_t dg_cache_workspace_bytes(int64_t num_nodes) {
   if (num_nodes < 1) return 0;
-  const int64_t nblk = (num_nodes + CF_BLOCK - 1) / CF_BLOCK;
+  KeySort a;
+  memset(&a, 0, sizeof(a));
+  a.n = num_nodes;
   Carve c(nullptr);
-  (void)c.take<uint32_t>((size_t)nblk * KEYS);
-  (void)c.take<int64_t>((size_t)nblk * KEYS);
-  (void)c.take<int64_t>(KEYS);
+  carve_keysort(a, c);
   return c.used;
 }
 
@@ -311,25 +402,20 @@ extern "C" int dg_cache_by_frequency(const uint64_t *membership, int64_t N, int3
   if (!ws || ws_bytes < need || ((uintptr_t)ws & 255))
     return set_error(DG_EWORKSPACE, "dg_cache_by_frequency: workspace needs %zu bytes", need);
   hipStream_t s = stream;
-  FreqScan a;
+  KeySort a;
   memset(&a, 0, sizeof(a));
   a.mask = membership;
   a.keep = B == 64 ? ~0ull : ((1ull << B) - 1ull);
   a.N = N;
-  a.nblk = (N + CF_BLOCK - 1) / CF_BLOCK;
+  a.n = N;
   Carve c(ws);
-  a.cnt = c.take<uint32_t>((size_t)a.nblk * KEYS);
-  a.base = c.take<int64_t>((size_t)a.nblk * KEYS);
-  a.totals = c.take<int64_t>(KEYS);
+  carve_keysort(a, c);
   a.cap = cache_rows;
   a.cache_slot = cache_slot;
   a.cache_nodes = cache_nodes;
-  hipLaunchKernelGGL(k_freq_count, dim3((unsigned)a.nblk), dim3(CF_THREADS), 0, s, a);
-  hipLaunchKernelGGL(k_freq_scan, dim3(KEYS), dim3(1024), 0, s, a);
-  DG_HIP(hipGetLastError());
   int64_t totals[KEYS];
-  DG_HIP(hipMemcpyAsync(totals, a.totals, sizeof(totals), hipMemcpyDeviceToHost, s));
-  DG_HIP(hipStreamSynchronize(s));
+  int rc;
+  if ((rc = keysort_count<FREQ>(a, totals, s))) return rc;
   // keys in rank order: 64, 63, ..., 1, then 0 (never cached)
   int64_t run = 0;
   for (int k = 64; k >= 1; --k) {
@@ -337,13 +423,73 @@ extern "C" int dg_cache_by_frequency(const uint64_t *membership, int64_t N, int3
     run += totals[k];
   }
   a.first[0] = run;
-  const int64_t accessed = run;
-  *cached = accessed < cache_rows ? accessed : cache_rows;
+  *cached = run < cache_rows ? run : cache_rows;
   if (cache_rows > 0)
     hipLaunchKernelGGL(k_fill_i32, dim3(256), dim3(256), 0, s, cache_nodes, cache_rows, -1);
-  hipLaunchKernelGGL(k_freq_place, dim3((unsigned)a.nblk), dim3(CF_THREADS), 0, s, a);
+  hipLaunchKernelGGL(k_key_place<FREQ>, dim3((unsigned)a.nblk), dim3(CF_THREADS), 0, s, a);
   DG_HIP(hipGetLastError());
   DG_HIP(hipStreamSynchronize(s));
+  return DG_OK;
+}
+
+extern "C" size_t dg_minhash_workspace_bytes(int64_t m) {
+  if (m < 0) return 0;
+  KeySort a;
+  memset(&a, 0, sizeof(a));
+  a.n = m;
+  Carve c(nullptr);
+  (void)c.take<uint32_t>(64);  // error word
+  (void)c.take<int32_t>(64);   // per-sample minima
+  carve_keysort(a, c);
+  return c.used;
+}
+
+extern "C" int dg_minhash_order(const uint64_t *membership, int64_t N, int32_t B,
+                                const int32_t *entries, int64_t m, const int32_t *perms,
+                                int32_t k, int32_t *order, int32_t *signature, void *ws,
+                                size_t ws_bytes, hipStream_t stream) {
+  if (!membership || (m > 0 && (!entries || !order)) || (k > 0 && !perms))
+    return set_error(DG_EINVAL, "dg_minhash_order: null pointer argument");
+  if (N < 1 || N > 0x7fffffffll || B < 1 || B > DG_MAX_BATCHES || m < 0 || k < 1)
+    return set_error(DG_EINVAL, "dg_minhash_order: bad sizes");
+  const size_t need = dg_minhash_workspace_bytes(m);
+  if (!ws || ws_bytes < need || ((uintptr_t)ws & 255))
+    return set_error(DG_EWORKSPACE, "dg_minhash_order: workspace needs %zu bytes", need);
+  hipStream_t s = stream;
+  KeySort a;
+  memset(&a, 0, sizeof(a));
+  Carve c(ws);
+  a.err = c.take<uint32_t>(64);
+  int32_t *minv = c.take<int32_t>(64);
+  a.mask = membership;
+  a.keep = B == 64 ? ~0ull : ((1ull << B) - 1ull);
+  a.N = N;
+  a.n = m;
+  carve_keysort(a, c);
+  a.ids = entries;
+  a.minv = minv;
+  a.order = order;
+  a.signature = signature;
+  int rc;
+  if ((rc = fill_u64(reinterpret_cast<uint64_t *>(a.err), 1, 0, s))) return rc;
+  hipLaunchKernelGGL(k_minhash_min, dim3(1), dim3(64), 0, s, perms, k, B, minv, a.err);
+  DG_HIP(hipGetLastError());
+  int64_t totals[KEYS];
+  if ((rc = keysort_count<MINHASH>(a, totals, s))) return rc;
+  int64_t run = 0;  // keys ascending; 64 (in no sample) last
+  for (int key = 0; key < KEYS; ++key) {
+    a.first[key] = run;
+    run += totals[key];
+  }
+  if (a.nblk > 0)
+    hipLaunchKernelGGL(k_key_place<MINHASH>, dim3((unsigned)a.nblk), dim3(CF_THREADS), 0, s, a);
+  DG_HIP(hipGetLastError());
+  uint32_t bits = 0;
+  DG_HIP(hipMemcpyAsync(&bits, a.err, sizeof(bits), hipMemcpyDeviceToHost, s));
+  DG_HIP(hipStreamSynchronize(s));
+  if (bits & ERR_ROW_RANGE)
+    return set_error(DG_EINVAL, "dg_minhash_order: a hash value is outside [0, B)");
+  if (bits) return set_error(DG_EINVAL, "invalid input data: %s", describe_device_error(bits));
   return DG_OK;
 }
 

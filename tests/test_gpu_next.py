@@ -100,3 +100,37 @@ def test_gather_rows_bad_id_flags_and_zeroes(dg):
     torch.cuda.synchronize()
     assert int(status.item()) == 1
     assert int(y[1].sum()) == 0 and int(y[2].sum()) == 0 and int(y[0].sum()) > 0
+
+
+def random_perms(k, B, seed):
+    g = torch.Generator().manual_seed(seed)
+    return torch.stack([torch.randperm(B, generator=g) for _ in range(k)]).to(torch.int32)
+
+
+@pytest.mark.parametrize("name,k", [("T", 1), ("T", 4), ("M1", 3)])
+def test_minhash_order_matches_oracle(dg, orc, name, k):
+    w = synth.make_workload(name, device=DEV) if name != "T" else synth.make_workload("T")
+    sr, mem = sampled(dg, w)
+    lists = [sr.batch_nodes(b).cpu().numpy() for b in range(w.cfg.B)]
+    # disk-cache entries: the non-cached accessed nodes plus a few never accessed
+    accessed = (mem != 0).nonzero().squeeze(1)
+    slot = w.cache_slot.to(DEV)
+    entries = accessed[slot[accessed] < 0]
+    extra = ((mem == 0).nonzero().squeeze(1))[:100]
+    entries = torch.cat([entries, extra]).to(torch.int32)
+    g = torch.Generator().manual_seed(k)
+    entries = entries[torch.randperm(entries.numel(), generator=g).to(DEV)].contiguous()
+    perms = random_perms(k, w.cfg.B, 11 * k)
+    order, sig = dg.minhash_order(mem, w.cfg.B, entries, perms.to(DEV))
+    r_order, r_sig = orc.minhash_order(w.cfg.n, lists, entries.cpu().numpy(), perms.numpy())
+    assert np.array_equal(sig.cpu().numpy(), r_sig)
+    assert np.array_equal(order.cpu().numpy(), r_order)
+
+
+def test_minhash_rejects_bad_hash_values(dg):
+    mem = torch.zeros(10, dtype=torch.int64, device=DEV)
+    mem[3] = 1
+    entries = torch.tensor([3, 4], dtype=torch.int32, device=DEV)
+    perms = torch.tensor([[0, 5]], dtype=torch.int32, device=DEV)
+    with pytest.raises(dg.DGError):
+        dg.minhash_order(mem, 2, entries, perms)

@@ -376,3 +376,41 @@ def test_cache_by_frequency_small_example(orc):
     assert nodes.tolist() == [2, 0, 5] and cached == 3
     slot, nodes, cached = orc.cache_by_frequency(8, lists, 6)
     assert nodes.tolist() == [2, 0, 5, 7, -1, -1] and cached == 4
+
+
+# ------------------------------------------------------------------ MinHash reordering
+@pytest.mark.parametrize("trial", range(20))
+def test_minhash_order_matches_set_definition(orc, trial):
+    """S(v) is the classic MinHash of v's sample set under each permutation
+    (the minimum permuted sample ID), minimised over the k permutations;
+    entries are stably sorted by it, samples-less entries last."""
+    rnd = random.Random(900 + trial)
+    n = rnd.randint(1, 50)
+    B = rnd.randint(1, 8)
+    lists = [np.array(rnd.sample(range(n), rnd.randint(0, n)), dtype=np.int32) for _ in range(B)]
+    m = rnd.randint(0, n)
+    entries = np.array(rnd.sample(range(n), m), dtype=np.int32)
+    k = rnd.randint(1, 4)
+    perms = np.array([rnd.sample(range(B), B) for _ in range(k)], dtype=np.int32)
+    order, sig = orc.minhash_order(n, lists, entries, perms)
+    samples = {v: {i for i in range(B) if v in set(lists[i].tolist())} for v in range(n)}
+    want_sig = []
+    for v in entries.tolist():
+        per_perm = [min((int(p[i]) for i in samples[v]), default=None) for p in perms]
+        want_sig.append(-1 if not samples[v] else min(per_perm))
+    assert sig.tolist() == want_sig
+    key = [(s if s >= 0 else 10**9, pos) for pos, s in enumerate(want_sig)]
+    want_order = [int(entries[pos]) for _, pos in sorted(key)]
+    assert order.tolist() == want_order
+
+
+def test_minhash_order_groups_nodes_with_equal_sample_sets(orc):
+    # nodes 1 and 6 are required by samples {0, 2}; 3 and 4 by {1}; 5 by none
+    lists = [np.array(x, dtype=np.int32) for x in ([1, 6, 2], [3, 4, 2], [6, 1])]
+    entries = np.array([1, 3, 5, 6, 4], dtype=np.int32)
+    perms = np.array([[2, 0, 1], [1, 2, 0]], dtype=np.int32)
+    order, sig = orc.minhash_order(8, lists, entries, perms)
+    # samples {0,2}: min(2,1) under perm 0 -> 1, under perm 1 -> min(1,0) = 0  => S = 0
+    # sample {1}:   perm 0 -> 0, perm 1 -> 2                                  => S = 0
+    assert sig.tolist() == [0, 0, -1, 0, 0]
+    assert order.tolist() == [1, 3, 6, 4, 5]
