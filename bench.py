@@ -32,12 +32,17 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+# The translation unit of the fan-out gather kernel: its source and the headers
+# it includes.
+GATHER_TU = ("dg_pack.hip", "dg_common.h", "dg_rows.h")
+
+
 def kernel_source_digest() -> str:
-    """Digest of the sources the timed kernels are built from (ties committed
+    """Digest of the sources the roofline kernel is built from (ties committed
     counter readings to the code they were taken on)."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2405_05231_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
+    for name in GATHER_TU:
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(name.encode() + f.read())
     return h.hexdigest()[:16]
