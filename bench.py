@@ -116,9 +116,11 @@ def main():
 
     # first pass: sizes and buffers (outside the timed region)
     mem = torch.empty(cfg.n, dtype=torch.int64, device=dev)  # (node, batch) membership
-    sr = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, membership=mem)
+    sr = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, membership=mem,
+                         direct=True)
     ws_s = torch.empty(dg._L.dg_sample_workspace_bytes(cfg.n, B, sr.nodes.shape[1],
-                                                       sr.edge_src.shape[1]),
+                                                       sr.edge_src.shape[1],
+                                                       dg.sample_flags(direct=True)),
                        dtype=torch.uint8, device=dev)
     counts = sr.node_count.copy()
     pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, membership=mem)
@@ -139,7 +141,7 @@ def main():
         # the fan-out gather is timed by HIP events inside dg_pack_group
         t0 = time.perf_counter()
         s_out = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, out=sr,
-                                workspace=ws_s, membership=mem)
+                                workspace=ws_s, membership=mem, direct=True)
         t1 = time.perf_counter()
         p_out = dg.pack_group(w.feats, w.cache_slot, s_out.nodes, counts, out=pr,
                               workspace=ws_p, timing=record, membership=mem)

@@ -111,6 +111,10 @@ extern "C" {
 #define DG_SAMPLE_LAYERED 1u /* every node of the mini-batch so far samples at each hop
                                 (layer-wise blocks as DGL builds them), instead of only
                                 the nodes new at the previous hop */
+#define DG_SAMPLE_DIRECT 2u  /* relabel sampled neighbours through a direct [N][B]
+                                int32 table of local indices (4*N*B workspace bytes)
+                                instead of a hash table sized for the group; same
+                                results, fewer device-wide atomics */
 
 typedef enum dg_status {
   DG_OK = 0,
@@ -178,10 +182,11 @@ int dg_sample_bounds(int64_t num_nodes, int64_t num_edges, int32_t S,
                      const int32_t *fanouts /*[host] K*/, int32_t K, uint32_t flags,
                      int64_t *node_cap /*[host] out*/, int64_t *edge_cap /*[host] out*/);
 
-/* Workspace bytes dg_sample_group needs for N nodes, B batches and the given
- * per-batch capacities. */
+/* Workspace bytes dg_sample_group needs for N nodes, B batches, the given
+ * per-batch capacities and the same flags (DG_SAMPLE_DIRECT adds 4*N*B bytes).
+ * Returns 0 for arguments dg_sample_group would reject. */
 size_t dg_sample_workspace_bytes(int64_t num_nodes, int32_t B, int64_t node_cap,
-                                 int64_t edge_cap);
+                                 int64_t edge_cap, uint32_t flags);
 
 /* Group sampling (§2 Fig. 1; §3: many mini-batches are sampled before any
  * computation).  Rule and randomness: see the top of this file.
@@ -194,10 +199,12 @@ size_t dg_sample_workspace_bytes(int64_t num_nodes, int32_t B, int64_t node_cap,
  *   fanouts    [host] K fan-outs, hop 1 first; f < 0 means "all neighbours",
  *              f = 0 samples nothing at that hop.  K >= 0.
  *   rng_seed   sampler seed.
- *   flags      0, or DG_SAMPLE_LAYERED: at every hop all nodes of the mini-batch
- *              so far sample (in list order), not only the previous hop's new
- *              nodes; the node list then nests as DGL's layer-wise blocks do
- *              (the first hop_ptr[k] nodes are the destinations of hop k+1).
+ *   flags      0, or an OR of: DG_SAMPLE_LAYERED: at every hop all nodes of the
+ *              mini-batch so far sample (in list order), not only the previous
+ *              hop's new nodes; the node list then nests as DGL's layer-wise
+ *              blocks do (the first hop_ptr[k] nodes are the destinations of
+ *              hop k+1).  DG_SAMPLE_DIRECT: the relabelling table is a direct
+ *              [N][B] array (outputs are identical either way).
  * Outputs (row b of each starts at b*cap):
  *   nodes      [B*node_cap] int32: nodes_b in the order above.
  *   hop_ptr    [host] [B*(K+2)] int64: hop_ptr[b*(K+2)+h] = start of hop h in

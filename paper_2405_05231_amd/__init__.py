@@ -90,16 +90,22 @@ class SampleResult:
         return self.edge_src[b, :e], self.edge_dst[b, :e]
 
 
+def sample_flags(layered: bool = False, direct: bool = False) -> int:
+    """dg_sample_group flag word."""
+    return (_lib.DG_SAMPLE_LAYERED if layered else 0) | (_lib.DG_SAMPLE_DIRECT if direct else 0)
+
+
 def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tensor, fanouts,
                  rng_seed: int, batch_base: int = 0, node_cap: int | None = None,
                  edge_cap: int | None = None, out: SampleResult | None = None,
                  workspace: torch.Tensor | None = None, stream=None, timing: bool = False,
-                 membership: torch.Tensor | None = None, layered: bool = False
-                 ) -> SampleResult:
+                 membership: torch.Tensor | None = None, layered: bool = False,
+                 direct: bool = False) -> SampleResult:
     """Group sampling (dg_sample_group).  seeds: int32 [B, S] on the GPU.
     membership: optional int64 [N] tensor that receives the (node, batch)
     membership mask (bit b of word u = u is in batch b).  layered: every node
-    of the mini-batch so far samples at each hop (DGL-style layer blocks)."""
+    of the mini-batch so far samples at each hop (DGL-style layer blocks).
+    direct: relabel through a direct [N][B] table (4*N*B workspace bytes)."""
     dev = offsets.device
     _need(offsets, "offsets", torch.int64)
     _need(indices, "indices", torch.int32, dev)
@@ -127,14 +133,15 @@ def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tens
             edge_src=torch.empty((B, max(edge_cap, 1)), dtype=torch.int32, device=dev),
             edge_dst=torch.empty((B, max(edge_cap, 1)), dtype=torch.int32, device=dev),
             edge_ptr=np.zeros((B, K + 1), dtype=np.int64), sizes={}, timing=None)
-    ws_bytes = _L.dg_sample_workspace_bytes(N, B, node_cap, edge_cap)
+    flags = sample_flags(layered, direct)
+    ws_bytes = _L.dg_sample_workspace_bytes(N, B, node_cap, edge_cap, flags)
     ws = _workspace(ws_bytes, dev, workspace)
     g = Csr(N, E, offsets.data_ptr(), indices.data_ptr())
     fo = (ctypes.c_int32 * max(K, 1))(*fanouts)
     sz, tm = Sizes(), Timing()
     st = _L.dg_sample_group(
         ctypes.byref(g), _ptr(seeds), B, S, batch_base, fo, K, rng_seed & (2**64 - 1),
-        _lib.DG_SAMPLE_LAYERED if layered else 0, node_cap, _ptr(out.nodes), out.hop_ptr.ctypes.data_as(_lib.I64P), edge_cap,
+        flags, node_cap, _ptr(out.nodes), out.hop_ptr.ctypes.data_as(_lib.I64P), edge_cap,
         _ptr(out.edge_src), _ptr(out.edge_dst), out.edge_ptr.ctypes.data_as(_lib.I64P),
         _ptr(membership), _ptr(ws), ws.numel(), _stream(stream), ctypes.byref(sz),
         ctypes.byref(tm) if timing else None)

@@ -10,6 +10,7 @@ LIB_PATH = os.path.join(_HERE, "libdg.so")
 
 DG_OK, DG_EINVAL, DG_ECAPACITY, DG_EHIP, DG_EWORKSPACE = 0, -1, -2, -3, -4
 DG_SAMPLE_LAYERED = 1
+DG_SAMPLE_DIRECT = 2
 DG_MAX_BATCHES = 64
 STATUS_NAMES = {0: "DG_OK", -1: "DG_EINVAL", -2: "DG_ECAPACITY", -3: "DG_EHIP",
                 -4: "DG_EWORKSPACE"}
@@ -17,6 +18,7 @@ STATUS_NAMES = {0: "DG_OK", -1: "DG_EINVAL", -2: "DG_ECAPACITY", -3: "DG_EHIP",
 I64 = ctypes.c_int64
 I32 = ctypes.c_int32
 U64 = ctypes.c_uint64
+U32 = ctypes.c_uint32
 VP = ctypes.c_void_p
 SZ = ctypes.c_size_t
 I32P = ctypes.POINTER(ctypes.c_int32)
@@ -51,7 +53,7 @@ SIGNATURES = {
     "dg_version": (ctypes.c_char_p, []),
     "dg_last_error": (ctypes.c_char_p, []),
     "dg_sample_bounds": (ctypes.c_int, [I64, I64, I32, I32P, I32, ctypes.c_uint32, I64P, I64P]),
-    "dg_sample_workspace_bytes": (SZ, [I64, I32, I64, I64]),
+    "dg_sample_workspace_bytes": (SZ, [I64, I32, I64, I64, U32]),
     "dg_sample_group": (ctypes.c_int, [ctypes.POINTER(Csr), VP, I32, I32, I64, I32P, I32, U64,
                                        ctypes.c_uint32, I64, VP, I64P, I64, VP, VP, I64P, VP,
                                        VP, SZ, VP,

@@ -190,6 +190,8 @@ struct MaskScan {
   int64_t *unc_off;                  // first pair of each U_nc node
   int64_t *nodeoff;                  // [N] first pair of node u (U_nc nodes only)
   int64_t *pairdest;                 // per pair: seg_base[b] + rank of u in b's list
+  int32_t *local_out;                // [N][B]: local index of (u, b) = local_base[b] + rank
+  int64_t local_base[DG_MAX_BATCHES];
   uint64_t *prev;                    // nullable: members already listed; the passes
                                      // see mask & ~prev, and the write pass sets
                                      // prev = mask where they differ

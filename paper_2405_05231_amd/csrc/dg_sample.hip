@@ -6,9 +6,11 @@
 // hop is: degree pass over the frontier -> exclusive scan (edge slots) -> draw
 // + mark (fire-and-forget atomicOr on visited) -> compaction of visited & ~prev
 // (the nodes new at this hop) into each batch's new segment, ascending, with
-// no sort; the compaction also brings prev up to date.  At the end every node's
-// local index goes into a (node, batch) hash table sized for the group, and
-// sampled neighbours are relabelled from global to local IDs through it.
+// no sort; the compaction also brings prev up to date.  Sampled neighbours are
+// relabelled from global to local IDs at the end, through one of two tables:
+// a direct [N][B] array of local indices that the compaction fills as it
+// assigns them (DG_SAMPLE_DIRECT), or a (node, batch) hash table sized for the
+// group and filled after the last hop.
 #include <string.h>
 
 #include "dg_common.h"
@@ -39,16 +41,19 @@ struct Hop {
   uint64_t bstate[DG_MAX_BATCHES];     // mix64(rng_seed + gamma*(g+1)) per batch
 };
 
-// Flattened (batch, position) ranges, for passes over all node or edge lists.
+// Flattened (batch, position) ranges, for passes over all edge lists, with
+// each batch's node count.
 struct Lists {
   int B;
   int64_t start[DG_MAX_BATCHES + 1];
+  int64_t n[DG_MAX_BATCHES];
 };
 
 __global__ __launch_bounds__(THREADS) void k_seed_init(const int32_t *seeds, int B, int S,
                                                        int64_t N, int64_t node_cap,
                                                        int32_t *nodes, uint64_t *visited,
-                                                       uint64_t *prev, uint32_t *err) {
+                                                       uint64_t *prev, int32_t *local,
+                                                       uint32_t *err) {
   int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (i >= (int64_t)B * S) return;
   int b = (int)(i / S);
@@ -63,6 +68,7 @@ __global__ __launch_bounds__(THREADS) void k_seed_init(const int32_t *seeds, int
   unsigned long long old = atomicOr((unsigned long long *)&visited[v], bit);
   if (old & bit) atomicOr(err, ERR_DUP_NODE);
   atomicOr((unsigned long long *)&prev[v], bit);  // seeds are not new at hop 1
+  if (local) local[(int64_t)v * B + b] = (int32_t)j;
 }
 
 __global__ __launch_bounds__(THREADS) void k_frontier_degree(
@@ -233,7 +239,7 @@ __global__ __launch_bounds__(THREADS) void k_table_insert(Segs L, const int32_t 
 }
 
 // Sampled neighbours' global IDs -> local indices through the group's
-// (node, batch) table.
+// (node, batch) hash table.
 __global__ __launch_bounds__(THREADS) void k_relabel(Lists L, int64_t edge_cap, int32_t *edge_dst,
                                                      LocalTable table, int64_t N, uint32_t *err) {
   int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
@@ -250,6 +256,26 @@ __global__ __launch_bounds__(THREADS) void k_relabel(Lists L, int64_t edge_cap, 
   edge_dst[e] = (int32_t)j;
 }
 
+// The same through the direct [N][B] table.  Every looked-up pair was written
+// when its node entered the batch; the range check guards that invariant.
+__global__ __launch_bounds__(THREADS) void k_relabel_direct(Lists L, int64_t edge_cap,
+                                                            int32_t *edge_dst,
+                                                            const int32_t *local, int64_t N,
+                                                            uint32_t *err) {
+  int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
+  if (i >= L.start[L.B]) return;
+  int b = find_batch(L.start, L.B, i);
+  int64_t e = (int64_t)b * edge_cap + (i - L.start[b]);
+  int32_t u = edge_dst[e];
+  if (u < 0 || (int64_t)u >= N) return;  // already reported
+  int32_t j = local[(int64_t)u * L.B + b];
+  if (j < 0 || (int64_t)j >= L.n[b]) {
+    atomicOr(err, ERR_INTERNAL);
+    return;
+  }
+  edge_dst[e] = j;
+}
+
 // eoff at each batch's first frontier entry (and at the end).
 __global__ void k_batch_bounds(Hop h, const int64_t *f_eoff, int64_t *out) {
   int b = threadIdx.x;
@@ -262,12 +288,13 @@ struct SampleWs {
   uint32_t *err;
   uint64_t *visited, *prev;
   int64_t *f_off, *f_deg, *f_cnt, *f_eoff, *tiles;
-  LocalTable table;
-  int64_t *small;  // staging for a few counts
+  LocalTable table;  // hash relabelling
+  int32_t *local;    // direct relabelling: [N][B]
+  int64_t *small;    // staging for a few counts
   MaskScan ms;
 };
 
-void carve_sample(SampleWs &w, Carve &c, int64_t N, int B, int64_t node_cap) {
+void carve_sample(SampleWs &w, Carve &c, int64_t N, int B, int64_t node_cap, bool direct) {
   int64_t fmax = (int64_t)B * node_cap;  // frontier entries never exceed the node lists
   w.err = c.take<uint32_t>(64);
   w.visited = c.take<uint64_t>((size_t)N);
@@ -277,8 +304,9 @@ void carve_sample(SampleWs &w, Carve &c, int64_t N, int B, int64_t node_cap) {
   w.f_cnt = c.take<int64_t>((size_t)fmax);
   w.f_eoff = c.take<int64_t>((size_t)fmax + 1);
   w.tiles = c.take<int64_t>(scan_tile_count(fmax));
-  w.table.bits = lt_bits_for(fmax);
-  w.table.slots = c.take<uint64_t>((size_t)1 << w.table.bits);
+  w.table.bits = direct ? 0 : lt_bits_for(fmax);
+  w.table.slots = direct ? nullptr : c.take<uint64_t>((size_t)1 << w.table.bits);
+  w.local = direct ? c.take<int32_t>((size_t)N * (size_t)B) : nullptr;
   w.small = c.take<int64_t>(2 * (DG_MAX_BATCHES + 1));
   w.ms = MaskScan{};
   w.ms.N = N;
@@ -331,12 +359,14 @@ extern "C" int dg_sample_bounds(int64_t num_nodes, int64_t num_edges, int32_t S,
 }
 
 extern "C" size_t dg_sample_workspace_bytes(int64_t num_nodes, int32_t B, int64_t node_cap,
-                                            int64_t edge_cap) {
+                                            int64_t edge_cap, uint32_t flags) {
   (void)edge_cap;
-  if (num_nodes < 1 || B < 1 || B > DG_MAX_BATCHES || node_cap < 1) return 0;
+  if (num_nodes < 1 || B < 1 || B > DG_MAX_BATCHES || node_cap < 1 ||
+      (flags & ~(DG_SAMPLE_LAYERED | DG_SAMPLE_DIRECT)))
+    return 0;
   Carve c(nullptr);
   SampleWs w;
-  carve_sample(w, c, num_nodes, B, node_cap);
+  carve_sample(w, c, num_nodes, B, node_cap, (flags & DG_SAMPLE_DIRECT) != 0);
   return c.used;
 }
 
@@ -354,16 +384,17 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
   if (!g->offsets || (g->num_edges > 0 && !g->indices) || g->num_nodes < 1 ||
       g->num_nodes > 0x7fffffffll || g->num_edges < 0)
     return set_error(DG_EINVAL, "dg_sample_group: bad CSR description");
-  if (flags & ~DG_SAMPLE_LAYERED)
+  if (flags & ~(DG_SAMPLE_LAYERED | DG_SAMPLE_DIRECT))
     return set_error(DG_EINVAL, "dg_sample_group: unknown flags 0x%x", flags);
   const bool layered = flags & DG_SAMPLE_LAYERED;
+  const bool direct = flags & DG_SAMPLE_DIRECT;
   if (B < 1 || B > DG_MAX_BATCHES || S < 1 || K < 0 || node_cap < S || edge_cap < 0 ||
       (int64_t)S > g->num_nodes)
     return set_error(DG_EINVAL, "dg_sample_group: bad sizes (B=%d S=%d K=%d node_cap=%lld)", B,
                      S, K, (long long)node_cap);
   if (node_cap > LT_MAX_VALUE)
     return set_error(DG_EINVAL, "dg_sample_group: node_cap above 2^27 - 1 is not supported");
-  const size_t need_ws = dg_sample_workspace_bytes(g->num_nodes, B, node_cap, edge_cap);
+  const size_t need_ws = dg_sample_workspace_bytes(g->num_nodes, B, node_cap, edge_cap, flags);
   if (!ws || ws_bytes < need_ws || ((uintptr_t)ws & 255))
     return set_error(DG_EWORKSPACE, "dg_sample_group: workspace needs %zu bytes, 256-aligned",
                      need_ws);
@@ -372,7 +403,7 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
   hipStream_t s = stream;
   SampleWs w;
   Carve c(ws);
-  carve_sample(w, c, N, B, node_cap);
+  carve_sample(w, c, N, B, node_cap, direct);
   w.ms.err = w.err;
 
   memset(sizes, 0, sizeof(*sizes));
@@ -391,7 +422,7 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
   if ((rc = fill_u64(w.visited, (size_t)N, 0, s))) return rc;
   if ((rc = fill_u64(w.prev, (size_t)N, 0, s))) return rc;
   hipLaunchKernelGGL(k_seed_init, dim3(blocks_for((int64_t)B * S)), dim3(THREADS), 0, s, seeds,
-                     B, S, N, node_cap, nodes, w.visited, w.prev, w.err);
+                     B, S, N, node_cap, nodes, w.visited, w.prev, w.local, w.err);
   DG_HIP(hipGetLastError());
   if ((rc = check_err(w.err, s))) return rc;
 
@@ -482,8 +513,12 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
         return set_error(DG_ECAPACITY, "dg_sample_group: node_cap %lld too small at hop %d",
                          (long long)node_cap, k);
       }
-      for (int b = 0; b < B; ++b) w.ms.seg_base[b] = (int64_t)b * node_cap + n_b[b];
+      for (int b = 0; b < B; ++b) {
+        w.ms.seg_base[b] = (int64_t)b * node_cap + n_b[b];
+        w.ms.local_base[b] = n_b[b];
+      }
       w.ms.seg_out = nodes;
+      w.ms.local_out = w.local;
       w.ms.uniq_out = nullptr;
       w.ms.unc_ids = nullptr;
       w.ms.unc_off = nullptr;
@@ -514,8 +549,15 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
   Lists LE;
   LE.B = B;
   LE.start[0] = 0;
-  for (int b = 0; b < B; ++b) LE.start[b + 1] = LE.start[b] + e_b[b];
-  if (LE.start[B] > 0) {
+  for (int b = 0; b < B; ++b) {
+    LE.start[b + 1] = LE.start[b] + e_b[b];
+    LE.n[b] = n_b[b];
+  }
+  if (LE.start[B] > 0 && direct) {
+    hipLaunchKernelGGL(k_relabel_direct, dim3(blocks_for(LE.start[B])), dim3(THREADS), 0, s, LE,
+                       edge_cap, edge_dst, w.local, N, w.err);
+    DG_HIP(hipGetLastError());
+  } else if (LE.start[B] > 0) {
     // the table holds every (node, batch) pair of the group, at load <= 1/2
     Segs LS;
     LS.B = B;

@@ -203,33 +203,36 @@ __device__ __forceinline__ void load_tile(const MaskScan &a, int64_t t0, int lan
 }
 
 // Per-wave counts of one tile: lane b returns batch b's non-cached members;
-// *cu, *cnc, *cp (wave-uniform) get the members of U, of U_nc and U_nc's pairs.
+// *cu, *cnc, *cp, *call (wave-uniform) get the members of U, of U_nc, U_nc's
+// pairs and all pairs.  Per-batch counts walk the tile's non-empty words one at
+// a time: the word is read out of its lane (v_readlane), and lane b tests bit b,
+// so the work follows the words present rather than the batches they touch.
 __device__ __forceinline__ uint32_t tile_counts(const TileBits &t, int lane, uint32_t *cu,
                                                 uint32_t *cnc, uint32_t *cp, uint32_t *call) {
-  uint32_t mine = 0, u = 0, nc = 0, p = 0;
-  int32_t all = 0;
+  uint32_t mine = 0, u = 0, nc = 0;
+  int32_t pl = 0, al = 0;  // this lane's pair counts (U_nc pairs, all pairs)
 #pragma unroll
   for (int r = 0; r < MC_ROUNDS; ++r) {
-    uint64_t m = t.m[r];
-    uint64_t any = __ballot(m != 0ull);
+    const uint64_t m = t.m[r];
+    const uint64_t any = __ballot(m != 0ull);
     if (any == 0ull) continue;  // wave-uniform
-    all += __popcll(m);
-    uint64_t mnc = ((t.cached >> r) & 1u) ? 0ull : m;
+    const uint64_t mnc = ((t.cached >> r) & 1u) ? 0ull : m;
+    al += __popcll(m);
+    pl += __popcll(mnc);
     u += (uint32_t)__popcll(any);
-    nc += (uint32_t)__popcll(__ballot(mnc != 0ull));
-    uint64_t uni = wave_or(mnc);
-    while (uni) {
-      int b = __ffsll((long long)uni) - 1;
-      uni &= uni - 1;
-      uint32_t c = (uint32_t)__popcll(__ballot((mnc >> b) & 1ull));
-      p += c;
-      if (lane == b) mine += c;
+    uint64_t anc = __ballot(mnc != 0ull);
+    nc += (uint32_t)__popcll(anc);
+    while (anc) {
+      const int l = __ffsll((long long)anc) - 1;
+      anc &= anc - 1;
+      const uint64_t w = (uint64_t)read_lane((int64_t)mnc, l);
+      mine += (uint32_t)((w >> lane) & 1ull);
     }
   }
   *cu = u;
   *cnc = nc;
-  *cp = p;
-  *call = (uint32_t)__ockl_wfred_add_i32(all);
+  *cp = (uint32_t)__ockl_wfred_add_i32(pl);
+  *call = (uint32_t)__ockl_wfred_add_i32(al);
   return mine;
 }
 
@@ -331,10 +334,11 @@ int mask_scan_count(MaskScan &m, int64_t *host_totals, hipStream_t s) {
   return DG_OK;
 }
 
-// Write pass: every rank is the block's base from the row scan, plus the
-// counts of the block's earlier waves, plus the running counts of the wave's
-// earlier rounds (lane b holds batch b's), plus the ballot prefix within the
-// round.
+// Write pass: batch b's next rank is the block's base from the row scan, plus
+// the counts of the block's earlier waves, plus what lane b has emitted so far.
+// Per-node outputs use ballot prefixes within a round; the (node, batch) pairs
+// are emitted word by word in node order (lane b handles bit b), so each
+// batch's list comes out ascending.
 __global__ __launch_bounds__(MC_THREADS) void k_mask_write(MaskScan a) {
   __shared__ uint32_t s_cnt[MC_WAVES][DG_MAX_BATCHES + 4];
   const int lane = lane_id(), w = threadIdx.x >> 6;
@@ -354,25 +358,30 @@ __global__ __launch_bounds__(MC_THREADS) void k_mask_write(MaskScan a) {
     for (int j = 0; j < w; ++j) v += s_cnt[j][row];
     return v;
   };
-  int64_t run_b = lane < B ? bb[lane] + before(lane) : 0;
-  const int64_t seg_b = lane < B ? a.seg_base[lane] : 0;
+  const int64_t run0 = lane < B ? bb[lane] + before(lane) : 0;
+  int64_t dest_b = lane < B ? a.seg_base[lane] + run0 : 0;       // next list slot of batch b
+  int64_t local_b = lane < B ? a.local_base[lane] + run0 : 0;    // its local index
   int64_t run_u = bb[row_all(B)] + before(row_all(B));
   int64_t run_nc = bb[row_packed(B)] + before(row_packed(B));
   int64_t run_p = bb[row_pairs(B)] + before(row_pairs(B));
   const uint64_t lt = lanes_below();
+  const bool node_pair0 = a.unc_off || a.nodeoff;
 #pragma unroll
   for (int r = 0; r < MC_ROUNDS; ++r) {
     const uint64_t m = t.m[r];
     const uint64_t any = __ballot(m != 0ull);
     if (any == 0ull) continue;  // wave-uniform
-    const int32_t u = (int32_t)(t0 + r * 64 + lane);
+    const int32_t u0 = (int32_t)(t0 + r * 64);
+    const int32_t u = u0 + lane;
     const uint64_t mnc = ((t.cached >> r) & 1u) ? 0ull : m;
     if (m != 0ull && a.uniq_out) a.uniq_out[run_u + __popcll(any & lt)] = u;
     run_u += __popcll(any);
-    const uint64_t anc = __ballot(mnc != 0ull);
-    const int32_t pc = __popcll(mnc);
-    const int32_t pincl = wave_incl_sum_i32(pc);
-    const int64_t pair0 = run_p + (pincl - pc);
+    uint64_t anc = __ballot(mnc != 0ull);
+    int64_t pair0 = 0;
+    if (node_pair0) {  // uniform: the scan runs on the full wave
+      const int32_t pc = __popcll(mnc);
+      pair0 = run_p + (wave_incl_sum_i32(pc) - pc);
+    }
     if (mnc != 0ull) {
       const int64_t rk = run_nc + __popcll(anc & lt);
       if (a.unc_ids) a.unc_ids[rk] = u;
@@ -380,20 +389,18 @@ __global__ __launch_bounds__(MC_THREADS) void k_mask_write(MaskScan a) {
       if (a.nodeoff) a.nodeoff[u] = pair0;
     }
     run_nc += __popcll(anc);
-    run_p += __builtin_amdgcn_readlane(pincl, 63);
-    uint64_t uni = wave_or(mnc);
-    while (uni) {
-      const int b = __ffsll((long long)uni) - 1;
-      uni &= uni - 1;
-      const uint64_t bal = __ballot((mnc >> b) & 1ull);
-      const int64_t rb = read_lane(run_b, b);
-      const int64_t sb = read_lane(seg_b, b);
-      if ((mnc >> b) & 1ull) {
-        const int64_t dest = sb + rb + __popcll(bal & lt);
-        if (a.seg_out) a.seg_out[dest] = u;
-        if (a.pairdest) a.pairdest[pair0 + __popcll(mnc & ((1ull << b) - 1ull))] = dest;
+    while (anc) {
+      const int l = __ffsll((long long)anc) - 1;
+      anc &= anc - 1;
+      const uint64_t wd = (uint64_t)read_lane((int64_t)mnc, l);
+      if ((wd >> lane) & 1ull) {
+        if (a.seg_out) a.seg_out[dest_b] = u0 + l;
+        if (a.pairdest) a.pairdest[run_p + __popcll(wd & lt)] = dest_b;
+        if (a.local_out) a.local_out[(int64_t)(u0 + l) * B + lane] = (int32_t)local_b;
+        ++dest_b;
+        ++local_b;
       }
-      if (lane == b) run_b += __popcll(bal);
+      run_p += __popcll(wd);
     }
     if (a.prev && m != 0ull) a.prev[t0 + r * 64 + lane] |= m;
   }

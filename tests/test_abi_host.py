@@ -61,10 +61,17 @@ def test_sample_bounds(L):
 
 
 def test_workspace_queries(L):
-    a = L.dg_sample_workspace_bytes(10_000, 4, 2000, 2000)
-    b = L.dg_sample_workspace_bytes(20_000, 4, 2000, 2000)
+    a = L.dg_sample_workspace_bytes(10_000, 4, 2000, 2000, 0)
+    b = L.dg_sample_workspace_bytes(20_000, 4, 2000, 2000, 0)
     assert 0 < a < b and a % 256 == 0
-    assert L.dg_sample_workspace_bytes(10_000, 65, 2000, 2000) == 0
+    assert L.dg_sample_workspace_bytes(10_000, 65, 2000, 2000, 0) == 0
+    assert L.dg_sample_workspace_bytes(10_000, 4, 2000, 2000, 8) == 0  # unknown flag
+    # the direct relabelling table replaces the hash table: 4*N*B bytes
+    d = L.dg_sample_workspace_bytes(10_000_000, 64, 2000, 2000, 2)
+    h = L.dg_sample_workspace_bytes(10_000_000, 64, 2000, 2000, 0)
+    assert d > h and d - 4 * 10_000_000 * 64 < h
+    assert L.dg_sample_workspace_bytes(10_000, 4, 2000, 2000, 3) == \
+        L.dg_sample_workspace_bytes(10_000, 4, 2000, 2000, 2)
     p = L.dg_pack_workspace_bytes(10_000, 4, 8000)
     assert p > 8 * 10_000 and p % 256 == 0
     assert L.dg_pack_workspace_bytes(10_000, 0, 10) == 0

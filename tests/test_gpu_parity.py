@@ -124,6 +124,13 @@ def test_tiny_workload_T_layered(dg, orc):
               w.cache_slot, w.cache_nodes, sample_kw={"layered": True})
 
 
+@pytest.mark.parametrize("layered", [False, True])
+def test_tiny_workload_T_direct_relabel(dg, orc, layered):
+    w = synth.make_workload("T")
+    check_all(dg, orc, w.offsets, w.indices, w.seeds, list(w.cfg.fanouts), w.rng_seed, w.feats,
+              w.cache_slot, w.cache_nodes, sample_kw={"layered": layered, "direct": True})
+
+
 def test_tiny_workload_T_is_deterministic(dg):
     w = synth.make_workload("T")
     a, pa, ya, _ = run_path(dg, w.offsets, w.indices, w.seeds, list(w.cfg.fanouts), w.rng_seed,
@@ -178,9 +185,10 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("layered", [False, True])
+@pytest.mark.parametrize("layered,direct", [(False, False), (True, False), (False, True),
+                                            (True, True)])
 @pytest.mark.parametrize("case", range(len(CASES)))
-def test_edge_cases(dg, orc, case, layered):
+def test_edge_cases(dg, orc, case, layered, direct):
     n, maxdeg, B, S, fan, dim, dtype, share = CASES[case]
     rnd = random.Random(900 + case)
     off, idx = random_case(rnd, n, maxdeg) if maxdeg else (
@@ -196,7 +204,7 @@ def test_edge_cases(dg, orc, case, layered):
     slot = torch.full((n,), -1, dtype=torch.int32)
     slot[cache_nodes] = torch.arange(ncache, dtype=torch.int32)
     check_all(dg, orc, off, idx, seeds, fan, 12345 + case, feats, slot, cache_nodes,
-              batch_base=case, sample_kw={"layered": layered})
+              batch_base=case, sample_kw={"layered": layered, "direct": direct})
 
 
 def test_fig1_example_on_device(dg, orc):

@@ -8,7 +8,8 @@ mini-batch (an oracle run over those batches alone, with their global batch
 numbers) and every packing table of the whole group (U, P_b order,
 packed_ptr, address tables); feature rows are checked on the device against
 an independent library gather (torch.index_select) of the feature table, for
-every packed row and every assembled row."""
+every packed row and every assembled row.  L100, H65 and M1 relabel through
+the direct [N][B] table (as bench.py does), W120 through the hash table."""
 import numpy as np
 import pytest
 import torch
@@ -40,12 +41,13 @@ def check_rows_on_device(X, ids, got, chunk=1 << 20):
         assert rows_equal(got[lo:hi], ref), (lo, hi)
 
 
-def run_and_check(dg, orc, w, oracle_batches):
+def run_and_check(dg, orc, w, oracle_batches, direct=True):
     cfg = w.cfg
     fan = list(cfg.fanouts)
     R = cfg.row_bytes
     mem = torch.empty(cfg.n, dtype=torch.int64, device=DEV)
-    sr = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, membership=mem)
+    sr = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, membership=mem,
+                         direct=direct)
     counts = sr.node_count.copy()
     pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, with_unique=True, membership=mem)
     torch.cuda.synchronize()
@@ -124,7 +126,7 @@ def test_workload_L100(dg, orc):
 @pytest.mark.timeout(900)
 def test_workload_W120(dg, orc):
     w = big("W120")
-    run_and_check(dg, orc, w, oracle_batches=(0, w.cfg.B - 1))
+    run_and_check(dg, orc, w, oracle_batches=(0, w.cfg.B - 1), direct=False)
 
 
 @pytest.mark.big
