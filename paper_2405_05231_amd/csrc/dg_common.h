@@ -178,12 +178,17 @@ struct MaskScan {
   int B;
   int64_t nblk;        // blocks of MC_BLOCK_NODES nodes
   uint32_t *cnt;       // [nblk][rows] per-block counts
+  uint32_t *wpre;      // [nblk][MC_WAVES][rows] each wave's exclusive prefix in its block
+  uint32_t *wcnt;      // [nblk][MC_WAVES] non-empty words of each wave's tile
+  uint64_t *cw_mask;   // [nblk][MC_WAVES][MC_TILE] those words (count pass -> write pass)
+  uint16_t *cw_off;    // ... their node offsets in the tile; bit 15 = cached
   int64_t *base;       // [nblk][rows] exclusive scans down each row
   int64_t *chunk_sum;  // [chunks][rows]
   int64_t *totals;     // [rows]
   uint32_t *err;
   // write pass (each output nullable)
   int64_t seg_base[DG_MAX_BATCHES];  // start index of batch b's list in seg_out
+  int64_t seg_end[DG_MAX_BATCHES];   // sampling: end of batch b's room in seg_out
   int32_t *seg_out;                  // per-batch ascending lists of non-cached members
   int32_t *uniq_out;                 // U ascending
   int32_t *unc_ids;                  // U_nc ascending
@@ -193,16 +198,20 @@ struct MaskScan {
   int32_t *local_out;                // [N][B]: local index of (u, b) = local_base[b] + rank
   int64_t local_base[DG_MAX_BATCHES];
   uint64_t *prev;                    // nullable: members already listed; the passes
-                                     // see mask & ~prev, and the write pass sets
-                                     // prev = mask where they differ
+                                     // see mask & ~prev, and the write pass adds
+                                     // the new bits to prev
+  // The write pass runs in one of two modes: packing (pairdest set: seg_out,
+  // unc_ids, unc_off, nodeoff required, uniq_out optional, cached nodes left out
+  // of the lists) or sampling (pairdest NULL: prev and seg_out required,
+  // local_out optional, no cache_slot).
 };
 
 
 size_t mask_scan_ws_bytes(int64_t N, int B);
 void mask_scan_carve(MaskScan &m, Carve &c);
-// Count pass + per-row scans; totals are copied to host_totals (B+3 values)
-// after a stream synchronisation.
-int mask_scan_count(MaskScan &m, int64_t *host_totals, hipStream_t s);
+// Count pass + per-row scans (asynchronous); m.totals[row] receives each row's
+// total (B+4 values) on the device.
+int mask_scan_count(MaskScan &m, hipStream_t s);
 // Write pass (uses the scans of the preceding count pass).
 int mask_scan_write(const MaskScan &m, hipStream_t s);
 

@@ -308,7 +308,10 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
   int64_t totals[DG_MAX_BATCHES + 4];
   w.ms.mask = w.mask;
   w.ms.cache_slot = cache_slot;
-  if ((rc = mask_scan_count(w.ms, totals, s))) return rc;
+  if ((rc = mask_scan_count(w.ms, s))) return rc;
+  DG_HIP(hipMemcpyAsync(totals, w.ms.totals, sizeof(int64_t) * mc_rows(B), hipMemcpyDeviceToHost,
+                        s));
+  DG_HIP(hipStreamSynchronize(s));
   if ((rc = read_err(w.err, s))) return rc;
   int64_t rows = 0;
   packed_ptr_host[0] = 0;

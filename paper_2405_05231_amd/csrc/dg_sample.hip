@@ -36,7 +36,6 @@ struct Hop {
   int64_t ftot;     // frontier entries over all batches
   int64_t fstart[DG_MAX_BATCHES + 1];  // prefix of frontier sizes
   int64_t fpos[DG_MAX_BATCHES];        // local position of b's first frontier node
-  int64_t estart[DG_MAX_BATCHES + 1];  // prefix of this hop's edge counts
   int64_t ebase[DG_MAX_BATCHES];       // edges of b before this hop
   uint64_t bstate[DG_MAX_BATCHES];     // mix64(rng_seed + gamma*(g+1)) per batch
 };
@@ -125,16 +124,22 @@ __device__ __forceinline__ void emit_chunk(const int32_t (&u)[EMIT], const int64
 // unrolled, so the arrays stay in VGPRs); each drawn position's rank among the
 // f positions gives its slot, so no sort is needed.  Neighbour loads and
 // membership atomics are issued EMIT at a time so their latencies overlap.
+// estart[b] = f_eoff at batch b's first frontier entry (written on the device
+// by k_batch_bounds).  A node whose edges would pass edge_cap writes nothing;
+// the host sees the overflow in the edge counts and reports it.
 __global__ __launch_bounds__(THREADS) void k_hop_sample(
     Hop h, const int32_t *nodes, int64_t node_cap, const int32_t *idx, const int64_t *f_off,
-    const int64_t *f_deg, const int64_t *f_eoff, int64_t edge_cap, int32_t *edge_src,
-    int32_t *edge_dst, uint64_t *visited, int64_t N, uint32_t *err) {
+    const int64_t *f_deg, const int64_t *f_eoff, const int64_t *estart, int64_t edge_cap,
+    int32_t *edge_src, int32_t *edge_dst, uint64_t *visited, int64_t N, uint32_t *err) {
   int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (i >= h.ftot) return;
   int b = find_batch(h.fstart, h.B, i);
   int64_t p = h.fpos[b] + (i - h.fstart[b]);
   int64_t o0 = f_off[i], d = f_deg[i];
-  int64_t base = (int64_t)b * edge_cap + h.ebase[b] + (f_eoff[i] - h.estart[b]);
+  const int64_t first = h.ebase[b] + (f_eoff[i] - estart[b]);  // local index of the 1st edge
+  const int64_t cnt = (h.f < 0 || d <= (int64_t)h.f) ? d : (int64_t)h.f;
+  if (first + cnt > edge_cap) return;
+  int64_t base = (int64_t)b * edge_cap + first;
   int32_t parent = (int32_t)p;
   int32_t u[EMIT];
   int64_t slot[EMIT];
@@ -276,6 +281,14 @@ __global__ __launch_bounds__(THREADS) void k_relabel_direct(Lists L, int64_t edg
   edge_dst[e] = j;
 }
 
+// Host staging block (int64 entries): edge bounds, compaction totals, error word.
+constexpr int ST_BOUNDS = 0;                              // [B+1]
+constexpr int ST_TOTALS = ST_BOUNDS + DG_MAX_BATCHES + 1; // [B+4]
+constexpr int ST_ERR = ST_TOTALS + DG_MAX_BATCHES + 4;
+constexpr int ST_SIZE = ST_ERR + 1;
+
+__global__ void k_stage_err(const uint32_t *err, int64_t *out) { *out = (int64_t)*err; }
+
 // eoff at each batch's first frontier entry (and at the end).
 __global__ void k_batch_bounds(Hop h, const int64_t *f_eoff, int64_t *out) {
   int b = threadIdx.x;
@@ -307,7 +320,7 @@ void carve_sample(SampleWs &w, Carve &c, int64_t N, int B, int64_t node_cap, boo
   w.table.bits = direct ? 0 : lt_bits_for(fmax);
   w.table.slots = direct ? nullptr : c.take<uint64_t>((size_t)1 << w.table.bits);
   w.local = direct ? c.take<int32_t>((size_t)N * (size_t)B) : nullptr;
-  w.small = c.take<int64_t>(2 * (DG_MAX_BATCHES + 1));
+  w.small = c.take<int64_t>(ST_SIZE);
   w.ms = MaskScan{};
   w.ms.N = N;
   w.ms.B = B;
@@ -423,8 +436,7 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
   if ((rc = fill_u64(w.prev, (size_t)N, 0, s))) return rc;
   hipLaunchKernelGGL(k_seed_init, dim3(blocks_for((int64_t)B * S)), dim3(THREADS), 0, s, seeds,
                      B, S, N, node_cap, nodes, w.visited, w.prev, w.local, w.err);
-  DG_HIP(hipGetLastError());
-  if ((rc = check_err(w.err, s))) return rc;
+  DG_HIP(hipGetLastError());  // bad seeds are reported at the first hop's round trip
 
   int64_t n_b[DG_MAX_BATCHES], e_b[DG_MAX_BATCHES];
   for (int b = 0; b < B; ++b) {
@@ -444,8 +456,6 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
     fbeg[b] = 0;
     fend[b] = S;
   }
-  int64_t totals[DG_MAX_BATCHES + 4];
-
   for (int k = 1; k <= K; ++k) {
     for (int b = 0; b < B; ++b) edge_ptr[(int64_t)b * (K + 1) + (k - 1)] = e_b[b];
     const int32_t f = fanouts[k - 1];
@@ -467,54 +477,25 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
                          nodes, node_cap, g->offsets, N, E, w.f_off, w.f_deg, w.f_cnt, w.err);
       DG_HIP(hipGetLastError());
       if ((rc = scan_exclusive(w.f_cnt, w.f_eoff, h.ftot, w.tiles, s))) return rc;
-      // edge counts per batch: f_eoff at the batch boundaries
-      int64_t bound[DG_MAX_BATCHES + 1];
+      // edge offsets at the batch boundaries, kept on the device
       hipLaunchKernelGGL(k_batch_bounds, dim3(1), dim3(DG_MAX_BATCHES + 1), 0, s, h, w.f_eoff,
-                         w.small);
-      DG_HIP(hipGetLastError());
-      DG_HIP(hipMemcpyAsync(bound, w.small, sizeof(int64_t) * (B + 1), hipMemcpyDeviceToHost, s));
-      DG_HIP(hipStreamSynchronize(s));
-      h.estart[0] = 0;
-      bool over = false;
-      for (int b = 0; b < B; ++b) {
-        h.estart[b + 1] = bound[b + 1];
-        int64_t cnt = bound[b + 1] - bound[b];
-        if (e_b[b] + cnt > edge_cap) over = true;
-        if (e_b[b] + cnt > sizes->max_batch_edges) sizes->max_batch_edges = e_b[b] + cnt;
-      }
-      if (over) {
-        sizes->exact = 0;
-        for (int b = 0; b < B; ++b)
-          if (n_b[b] > sizes->max_batch_nodes) sizes->max_batch_nodes = n_b[b];
-        return set_error(DG_ECAPACITY, "dg_sample_group: edge_cap %lld too small at hop %d",
-                         (long long)edge_cap, k);
-      }
+                         w.small + ST_BOUNDS);
       hipLaunchKernelGGL(k_hop_sample, dim3(blocks_for(h.ftot)), dim3(THREADS), 0, s, h, nodes,
-                         node_cap, g->indices, w.f_off, w.f_deg, w.f_eoff, edge_cap, edge_src,
-                         edge_dst, w.visited, N, w.err);
+                         node_cap, g->indices, w.f_off, w.f_deg, w.f_eoff, w.small + ST_BOUNDS,
+                         edge_cap, edge_src, edge_dst, w.visited, N, w.err);
       DG_HIP(hipGetLastError());
       const int ev1 = tm.mark();
-      // new nodes of this hop, per batch, ascending
+      // new nodes of this hop, per batch, ascending; the write pass needs only
+      // the list starts known before the hop, so it is queued before the host
+      // reads this hop's counts (it stops at each list's capacity)
       w.ms.mask = w.visited;
       w.ms.prev = w.prev;
       w.ms.cache_slot = nullptr;
-      if ((rc = mask_scan_count(w.ms, totals, s))) return rc;
-      bool nover = false;
-      for (int b = 0; b < B; ++b) {
-        new_b[b] = totals[b];
-        if (n_b[b] + new_b[b] > node_cap) nover = true;
-      }
-      for (int b = 0; b < B; ++b) {
-        e_b[b] += bound[b + 1] - bound[b];
-        if (n_b[b] + new_b[b] > sizes->max_batch_nodes) sizes->max_batch_nodes = n_b[b] + new_b[b];
-      }
-      if (nover) {
-        sizes->exact = 0;
-        return set_error(DG_ECAPACITY, "dg_sample_group: node_cap %lld too small at hop %d",
-                         (long long)node_cap, k);
-      }
+      w.ms.totals = w.small + ST_TOTALS;
+      if ((rc = mask_scan_count(w.ms, s))) return rc;
       for (int b = 0; b < B; ++b) {
         w.ms.seg_base[b] = (int64_t)b * node_cap + n_b[b];
+        w.ms.seg_end[b] = (int64_t)(b + 1) * node_cap;
         w.ms.local_base[b] = n_b[b];
       }
       w.ms.seg_out = nodes;
@@ -525,8 +506,40 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       w.ms.nodeoff = nullptr;
       w.ms.pairdest = nullptr;
       if ((rc = mask_scan_write(w.ms, s))) return rc;
-
       const int ev2 = tm.mark();
+      // one round trip per hop: edge bounds, node counts and the error word
+      int64_t st[ST_SIZE];
+      hipLaunchKernelGGL(k_stage_err, dim3(1), dim3(1), 0, s, w.err, w.small + ST_ERR);
+      DG_HIP(hipGetLastError());
+      DG_HIP(hipMemcpyAsync(st, w.small, sizeof(st), hipMemcpyDeviceToHost, s));
+      DG_HIP(hipStreamSynchronize(s));
+      if (st[ST_ERR])
+        return set_error(DG_EINVAL, "invalid input data: %s",
+                         describe_device_error((uint32_t)st[ST_ERR]));
+      const int64_t *bound = st + ST_BOUNDS;
+      bool over = false, nover = false;
+      for (int b = 0; b < B; ++b) {
+        const int64_t cnt = bound[b + 1] - bound[b];
+        new_b[b] = st[ST_TOTALS + b];
+        if (e_b[b] + cnt > edge_cap) over = true;
+        if (n_b[b] + new_b[b] > node_cap) nover = true;
+        if (e_b[b] + cnt > sizes->max_batch_edges) sizes->max_batch_edges = e_b[b] + cnt;
+        e_b[b] += cnt;
+      }
+      if (over) {  // the node counts of this hop are not meaningful
+        sizes->exact = 0;
+        for (int b = 0; b < B; ++b)
+          if (n_b[b] > sizes->max_batch_nodes) sizes->max_batch_nodes = n_b[b];
+        return set_error(DG_ECAPACITY, "dg_sample_group: edge_cap %lld too small at hop %d",
+                         (long long)edge_cap, k);
+      }
+      for (int b = 0; b < B; ++b)
+        if (n_b[b] + new_b[b] > sizes->max_batch_nodes) sizes->max_batch_nodes = n_b[b] + new_b[b];
+      if (nover) {
+        sizes->exact = 0;
+        return set_error(DG_ECAPACITY, "dg_sample_group: node_cap %lld too small at hop %d",
+                         (long long)node_cap, k);
+      }
       if (nhop_ev < 8) {
         hop_ev[nhop_ev][0] = ev0;
         hop_ev[nhop_ev][1] = ev1;

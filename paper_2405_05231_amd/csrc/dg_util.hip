@@ -157,20 +157,28 @@ void mask_scan_carve(MaskScan &m, Carve &c) {
   m.nblk = mc_blocks(m.N);
   size_t rows = (size_t)mc_rows(m.B);
   m.cnt = c.take<uint32_t>(rows * (size_t)m.nblk);
+  m.wpre = c.take<uint32_t>(rows * (size_t)m.nblk * MC_WAVES);
+  m.wcnt = c.take<uint32_t>((size_t)m.nblk * MC_WAVES);
+  m.cw_mask = c.take<uint64_t>((size_t)m.nblk * MC_BLOCK_NODES);
+  m.cw_off = c.take<uint16_t>((size_t)m.nblk * MC_BLOCK_NODES);
   m.base = c.take<int64_t>(rows * (size_t)m.nblk);
   m.chunk_sum = c.take<int64_t>(rows * (size_t)mc_chunks(m.nblk));
   m.totals = c.take<int64_t>(rows);
 }
 
-// Tile loads: all MC_ROUNDS mask words (and the cached flags of non-empty
-// ones) are requested before any is used, so a wave keeps 16 loads in flight.
+// Tile loads: all MC_ROUNDS mask words (and the prev words and cached flags of
+// non-empty ones) are requested before any is used, so a wave keeps 16 loads in
+// flight.
 struct TileBits {
   uint64_t m[MC_ROUNDS];
   uint32_t cached;  // bit r: node of round r is cached
 };
 
+// With update_prev, prev takes the listed bits as soon as they are known
+// (prev |= the new bits; the word is owned by this lane), so no second load is
+// needed later.
 __device__ __forceinline__ void load_tile(const MaskScan &a, int64_t t0, int lane, TileBits &t,
-                                          bool check_slots) {
+                                          bool check_slots, bool update_prev) {
 #pragma unroll
   for (int r = 0; r < MC_ROUNDS; ++r) {
     int64_t u = t0 + r * 64 + lane;
@@ -186,7 +194,10 @@ __device__ __forceinline__ void load_tile(const MaskScan &a, int64_t t0, int lan
 #pragma unroll
     for (int r = 0; r < MC_ROUNDS; ++r) p[r] = t.m[r] ? a.prev[t0 + r * 64 + lane] : 0ull;
 #pragma unroll
-    for (int r = 0; r < MC_ROUNDS; ++r) t.m[r] &= ~p[r];
+    for (int r = 0; r < MC_ROUNDS; ++r) {
+      t.m[r] &= ~p[r];
+      if (update_prev && t.m[r] != 0ull) a.prev[t0 + r * 64 + lane] = p[r] | t.m[r];
+    }
   }
   t.cached = 0;
   if (a.cache_slot) {
@@ -236,37 +247,53 @@ __device__ __forceinline__ uint32_t tile_counts(const TileBits &t, int lane, uin
   return mine;
 }
 
-// Stores one wave's counts into its LDS row (rows = B + 3).
-__device__ __forceinline__ void stash_counts(uint32_t *row, int B, int lane, uint32_t mine,
-                                             uint32_t cu, uint32_t cnc, uint32_t cp,
-                                             uint32_t call) {
-  if (lane < B) row[lane] = mine;
-  if (lane == 0) {
-    row[row_all(B)] = cu;
-    row[row_packed(B)] = cnc;
-    row[row_pairs(B)] = cp;
-    row[row_all_pairs(B)] = call;
-  }
-}
-
 // Count pass: per block, the number of members of every batch (non-cached
 // only), of U, of U_nc, and of U_nc's (node, batch) pairs; stored as one
-// contiguous row per block.
+// contiguous row per block, plus each wave's exclusive prefix within the block
+// (so the write pass does not count again).
 __global__ __launch_bounds__(MC_THREADS) void k_mask_count(MaskScan a) {
   __shared__ uint32_t s_cnt[MC_WAVES][DG_MAX_BATCHES + 4];
   const int lane = lane_id(), w = threadIdx.x >> 6;
   const int B = a.B, rows = mc_rows(B);
   const int64_t t0 = (int64_t)blockIdx.x * MC_BLOCK_NODES + (int64_t)w * MC_TILE;
   TileBits t;
-  load_tile(a, t0, lane, t, true);
+  load_tile(a, t0, lane, t, true, true);
   uint32_t cu, cnc, cp, call;
   uint32_t mine = tile_counts(t, lane, &cu, &cnc, &cp, &call);
-  stash_counts(s_cnt[w], B, lane, mine, cu, cnc, cp, call);
+  // the tile's non-empty words, in node order, for the write pass
+  {
+    const size_t gw = ((size_t)blockIdx.x * MC_WAVES + w) * MC_TILE;
+    const uint64_t lt = lanes_below();
+    uint32_t run = 0;
+#pragma unroll
+    for (int r = 0; r < MC_ROUNDS; ++r) {
+      const uint64_t any = __ballot(t.m[r] != 0ull);
+      if (any == 0ull) continue;
+      if (t.m[r] != 0ull) {
+        const size_t at = gw + run + (uint32_t)__popcll(any & lt);
+        a.cw_mask[at] = t.m[r];
+        a.cw_off[at] = (uint16_t)((r * 64 + lane) | ((int)((t.cached >> r) & 1u) << 15));
+      }
+      run += (uint32_t)__popcll(any);
+    }
+    if (lane == 0) a.wcnt[(size_t)blockIdx.x * MC_WAVES + w] = run;
+  }
+  if (lane < B) s_cnt[w][lane] = mine;
+  if (lane == 0) {
+    s_cnt[w][row_all(B)] = cu;
+    s_cnt[w][row_packed(B)] = cnc;
+    s_cnt[w][row_pairs(B)] = cp;
+    s_cnt[w][row_all_pairs(B)] = call;
+  }
   __syncthreads();
+  uint32_t *pre = a.wpre + (size_t)blockIdx.x * MC_WAVES * rows;
   for (int i = threadIdx.x; i < rows; i += MC_THREADS) {
     uint32_t v = 0;
 #pragma unroll
-    for (int j = 0; j < MC_WAVES; ++j) v += s_cnt[j][i];
+    for (int j = 0; j < MC_WAVES; ++j) {
+      pre[j * rows + i] = v;
+      v += s_cnt[j][i];
+    }
     a.cnt[(size_t)blockIdx.x * rows + i] = v;
   }
 }
@@ -317,98 +344,106 @@ __global__ __launch_bounds__(128) void k_rows_apply(MaskScan a) {
   }
 }
 
-int mask_scan_count(MaskScan &m, int64_t *host_totals, hipStream_t s) {
-  if (m.nblk == 0) {
-    for (int i = 0; i < mc_rows(m.B); ++i) host_totals[i] = 0;
-    return DG_OK;
-  }
+int mask_scan_count(MaskScan &m, hipStream_t s) {
+  if (m.nblk == 0) return fill_u64(reinterpret_cast<uint64_t *>(m.totals), mc_rows(m.B), 0, s);
   const unsigned nch = (unsigned)mc_chunks(m.nblk);
   hipLaunchKernelGGL(k_mask_count, dim3((unsigned)m.nblk), dim3(MC_THREADS), 0, s, m);
   hipLaunchKernelGGL(k_rows_chunk_sum, dim3(nch), dim3(128), 0, s, m);
   hipLaunchKernelGGL(k_rows_chunk_scan, dim3((unsigned)mc_rows(m.B)), dim3(1024), 0, s, m);
   hipLaunchKernelGGL(k_rows_apply, dim3(nch), dim3(128), 0, s, m);
   DG_HIP(hipGetLastError());
-  DG_HIP(hipMemcpyAsync(host_totals, m.totals, sizeof(int64_t) * mc_rows(m.B),
-                        hipMemcpyDeviceToHost, s));
-  DG_HIP(hipStreamSynchronize(s));
   return DG_OK;
 }
 
-// Write pass: batch b's next rank is the block's base from the row scan, plus
-// the counts of the block's earlier waves, plus what lane b has emitted so far.
-// Per-node outputs use ballot prefixes within a round; the (node, batch) pairs
-// are emitted word by word in node order (lane b handles bit b), so each
-// batch's list comes out ascending.
+// Write pass, over the compact list of non-empty words the count pass left for
+// each wave (no second read of the mask).  Batch b's next rank is the block's
+// base from the row scan, plus the wave's prefix within the block, plus what
+// lane b has emitted so far.  Per-node outputs use ballot prefixes within a
+// chunk of 64 words; the (node, batch) pairs are emitted word by word in node
+// order (lane b handles bit b), so each batch's list comes out ascending.
+//   PACK:  packing outputs (U, U_nc, pair offsets, pair destinations); cached
+//          nodes are left out of the per-batch lists.
+//   LOCAL: sampling, also recording each pair's local index in local_out.
+template <bool PACK, bool LOCAL>
 __global__ __launch_bounds__(MC_THREADS) void k_mask_write(MaskScan a) {
-  __shared__ uint32_t s_cnt[MC_WAVES][DG_MAX_BATCHES + 4];
   const int lane = lane_id(), w = threadIdx.x >> 6;
   const int B = a.B, rows = mc_rows(B);
   const int64_t t0 = (int64_t)blockIdx.x * MC_BLOCK_NODES + (int64_t)w * MC_TILE;
-  TileBits t;
-  load_tile(a, t0, lane, t, false);
-  {
-    uint32_t cu, cnc, cp, call;
-    uint32_t mine = tile_counts(t, lane, &cu, &cnc, &cp, &call);
-    stash_counts(s_cnt[w], B, lane, mine, cu, cnc, cp, call);
-  }
-  __syncthreads();
+  const size_t gwi = (size_t)blockIdx.x * MC_WAVES + w;
+  const uint32_t n = a.wcnt[gwi];
+  if (n == 0) return;  // wave-uniform
+  const uint64_t *cm = a.cw_mask + gwi * MC_TILE;
+  const uint16_t *co = a.cw_off + gwi * MC_TILE;
   const int64_t *bb = a.base + (size_t)blockIdx.x * rows;
-  auto before = [&](int row) {
-    int64_t v = 0;
-    for (int j = 0; j < w; ++j) v += s_cnt[j][row];
-    return v;
-  };
-  const int64_t run0 = lane < B ? bb[lane] + before(lane) : 0;
-  int64_t dest_b = lane < B ? a.seg_base[lane] + run0 : 0;       // next list slot of batch b
-  int64_t local_b = lane < B ? a.local_base[lane] + run0 : 0;    // its local index
-  int64_t run_u = bb[row_all(B)] + before(row_all(B));
-  int64_t run_nc = bb[row_packed(B)] + before(row_packed(B));
-  int64_t run_p = bb[row_pairs(B)] + before(row_pairs(B));
+  const uint32_t *pre = a.wpre + gwi * rows;
+  const int64_t run0 = lane < B ? bb[lane] + pre[lane] : 0;
+  int64_t dest_b = lane < B ? a.seg_base[lane] + run0 : 0;  // next list slot of batch b
+  const int64_t end_b = (!PACK && lane < B) ? a.seg_end[lane] : 0;
+  int32_t local_b = 0;                                      // its local index
+  if (LOCAL) local_b = lane < B ? (int32_t)(a.local_base[lane] + run0) : 0;
+  int64_t run_u = 0, run_nc = 0, run_p = 0;
+  if (PACK) {
+    run_u = bb[row_all(B)] + pre[row_all(B)];
+    run_nc = bb[row_packed(B)] + pre[row_packed(B)];
+    run_p = bb[row_pairs(B)] + pre[row_pairs(B)];
+  }
   const uint64_t lt = lanes_below();
-  const bool node_pair0 = a.unc_off || a.nodeoff;
-#pragma unroll
-  for (int r = 0; r < MC_ROUNDS; ++r) {
-    const uint64_t m = t.m[r];
-    const uint64_t any = __ballot(m != 0ull);
-    if (any == 0ull) continue;  // wave-uniform
-    const int32_t u0 = (int32_t)(t0 + r * 64);
-    const int32_t u = u0 + lane;
-    const uint64_t mnc = ((t.cached >> r) & 1u) ? 0ull : m;
-    if (m != 0ull && a.uniq_out) a.uniq_out[run_u + __popcll(any & lt)] = u;
-    run_u += __popcll(any);
+  for (uint32_t c0 = 0; c0 < n; c0 += 64) {
+    const uint32_t i = c0 + lane;
+    uint64_t m = 0;
+    uint32_t off = 0;
+    if (i < n) {
+      m = cm[i];
+      off = co[i];
+    }
+    const int32_t u = (int32_t)(t0 + (off & 1023u));
+    const uint64_t mnc = (PACK && (off >> 15)) ? 0ull : m;
     uint64_t anc = __ballot(mnc != 0ull);
-    int64_t pair0 = 0;
-    if (node_pair0) {  // uniform: the scan runs on the full wave
+    if (PACK) {
+      const uint64_t any = __ballot(m != 0ull);
+      if (m != 0ull && a.uniq_out) a.uniq_out[run_u + __popcll(any & lt)] = u;
+      run_u += __popcll(any);
       const int32_t pc = __popcll(mnc);
-      pair0 = run_p + (wave_incl_sum_i32(pc) - pc);
+      const int64_t pair0 = run_p + (wave_incl_sum_i32(pc) - pc);
+      if (mnc != 0ull) {
+        const int64_t rk = run_nc + __popcll(anc & lt);
+        a.unc_ids[rk] = u;
+        a.unc_off[rk] = pair0;
+        a.nodeoff[u] = pair0;
+      }
+      run_nc += __popcll(anc);
     }
-    if (mnc != 0ull) {
-      const int64_t rk = run_nc + __popcll(anc & lt);
-      if (a.unc_ids) a.unc_ids[rk] = u;
-      if (a.unc_off) a.unc_off[rk] = pair0;
-      if (a.nodeoff) a.nodeoff[u] = pair0;
-    }
-    run_nc += __popcll(anc);
     while (anc) {
       const int l = __ffsll((long long)anc) - 1;
-      anc &= anc - 1;
+      anc &= ~(1ull << l);
       const uint64_t wd = (uint64_t)read_lane((int64_t)mnc, l);
+      const int32_t ul = __builtin_amdgcn_readlane(u, l);
       if ((wd >> lane) & 1ull) {
-        if (a.seg_out) a.seg_out[dest_b] = u0 + l;
-        if (a.pairdest) a.pairdest[run_p + __popcll(wd & lt)] = dest_b;
-        if (a.local_out) a.local_out[(int64_t)(u0 + l) * B + lane] = (int32_t)local_b;
+        if (PACK || dest_b < end_b) a.seg_out[dest_b] = ul;
+        if (PACK) a.pairdest[run_p + __popcll(wd & lt)] = dest_b;
+        if (LOCAL) a.local_out[(int64_t)ul * B + lane] = local_b;
         ++dest_b;
         ++local_b;
       }
-      run_p += __popcll(wd);
+      if (PACK) run_p += __popcll(wd);
     }
-    if (a.prev && m != 0ull) a.prev[t0 + r * 64 + lane] |= m;
   }
 }
 
 int mask_scan_write(const MaskScan &m, hipStream_t s) {
   if (m.nblk == 0) return DG_OK;
-  hipLaunchKernelGGL(k_mask_write, dim3((unsigned)m.nblk), dim3(MC_THREADS), 0, s, m);
+  const bool pack = m.pairdest != nullptr;
+  // seg_out may be NULL only when no pair is listed (packing with every node cached)
+  if ((pack && (!m.unc_ids || !m.unc_off || !m.nodeoff)) ||
+      (!pack && (!m.prev || !m.seg_out || m.cache_slot || m.uniq_out)))
+    return set_error(DG_EINVAL, "internal: inconsistent compaction outputs");
+  const dim3 g((unsigned)m.nblk), bl(MC_THREADS);
+  if (pack)
+    hipLaunchKernelGGL((k_mask_write<true, false>), g, bl, 0, s, m);
+  else if (m.local_out)
+    hipLaunchKernelGGL((k_mask_write<false, true>), g, bl, 0, s, m);
+  else
+    hipLaunchKernelGGL((k_mask_write<false, false>), g, bl, 0, s, m);
   DG_HIP(hipGetLastError());
   return DG_OK;
 }

@@ -77,15 +77,20 @@ def test_sample_capacity_reported(dg, tiny):
     assert e.value.status == -2
     assert res.sizes["max_batch_nodes"] >= need_n - 1 + 1 or res.sizes["exact"] == 0
     assert bool((nodes[B * (need_n - 1):] == 7777).all())
-    # edge capacity one short
-    res2 = dg.SampleResult(nodes=torch.empty((B, need_n), dtype=torch.int32, device=DEV),
-                           hop_ptr=np.zeros((B, 4), dtype=np.int64),
-                           edge_src=torch.empty((B, need_e - 1), dtype=torch.int32, device=DEV),
-                           edge_dst=torch.empty((B, need_e - 1), dtype=torch.int32, device=DEV),
-                           edge_ptr=np.zeros((B, 3), dtype=np.int64), sizes={}, timing=None)
-    with pytest.raises(dg.DGError) as e:
-        dg.sample_group(off, idx, seeds, [5, 5], 1, out=res2)
-    assert e.value.status == -2 and res2.sizes["max_batch_edges"] == need_e
+    # edge capacity one short (both relabelling modes)
+    for direct in (False, True):
+        es = torch.full((B * (need_e - 1) + guard,), 7777, dtype=torch.int32, device=DEV)
+        ed = torch.full((B * (need_e - 1) + guard,), 7777, dtype=torch.int32, device=DEV)
+        res2 = dg.SampleResult(nodes=torch.empty((B, need_n), dtype=torch.int32, device=DEV),
+                               hop_ptr=np.zeros((B, 4), dtype=np.int64),
+                               edge_src=es[:B * (need_e - 1)].view(B, need_e - 1),
+                               edge_dst=ed[:B * (need_e - 1)].view(B, need_e - 1),
+                               edge_ptr=np.zeros((B, 3), dtype=np.int64), sizes={}, timing=None)
+        with pytest.raises(dg.DGError) as e:
+            dg.sample_group(off, idx, seeds, [5, 5], 1, out=res2, direct=direct)
+        assert e.value.status == -2 and res2.sizes["max_batch_edges"] == need_e
+        assert bool((es[B * (need_e - 1):] == 7777).all())
+        assert bool((ed[B * (need_e - 1):] == 7777).all())
 
 
 def test_pack_duplicate_and_range_rejected(dg, tiny):
