@@ -30,7 +30,9 @@
  *  - The caller owns every buffer.  The library never allocates device memory:
  *    scratch space is the caller's workspace `ws`, sized by the matching
  *    *_workspace_bytes() query and aligned to 256 bytes.  Workspace contents on
- *    entry are irrelevant; on return they are unspecified.
+ *    entry are irrelevant; on return they are unspecified.  The only memory the
+ *    library takes for itself is a 4 KB page-locked host buffer per calling
+ *    thread (for reading counts back), held until the process ends.
  *  - Work is enqueued on the caller's stream `stream` (NULL = the default
  *    stream).  dg_sample_group and dg_pack_group return only when their work has
  *    completed (their output sizes are data-dependent and are reported in

@@ -251,8 +251,7 @@ int keysort_count(KeySort &a, int64_t *totals, hipStream_t s) {
   hipLaunchKernelGGL(k_key_count<MODE>, dim3((unsigned)a.nblk), dim3(CF_THREADS), 0, s, a);
   hipLaunchKernelGGL(k_key_scan, dim3(KEYS), dim3(1024), 0, s, a);
   DG_HIP(hipGetLastError());
-  DG_HIP(hipMemcpyAsync(totals, a.totals, sizeof(int64_t) * KEYS, hipMemcpyDeviceToHost, s));
-  DG_HIP(hipStreamSynchronize(s));
+  DG_TRY(read_to_host(totals, a.totals, sizeof(int64_t) * KEYS, s));
   return DG_OK;
 }
 
@@ -485,8 +484,7 @@ extern "C" int dg_minhash_order(const uint64_t *membership, int64_t N, int32_t B
     hipLaunchKernelGGL(k_key_place<MINHASH>, dim3((unsigned)a.nblk), dim3(CF_THREADS), 0, s, a);
   DG_HIP(hipGetLastError());
   uint32_t bits = 0;
-  DG_HIP(hipMemcpyAsync(&bits, a.err, sizeof(bits), hipMemcpyDeviceToHost, s));
-  DG_HIP(hipStreamSynchronize(s));
+  DG_TRY(read_to_host(&bits, a.err, sizeof(bits), s));
   if (bits & ERR_ROW_RANGE)
     return set_error(DG_EINVAL, "dg_minhash_order: a hash value is outside [0, B)");
   if (bits) return set_error(DG_EINVAL, "invalid input data: %s", describe_device_error(bits));

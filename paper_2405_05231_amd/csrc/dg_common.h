@@ -32,6 +32,12 @@ const char *describe_device_error(uint32_t bits);
       return ::dg::set_error(DG_EHIP, "%s failed: %s", #call, hipGetErrorString(e_)); \
   } while (0)
 
+#define DG_TRY(call)                  \
+  do {                                \
+    const int r_ = (call);            \
+    if (r_ != DG_OK) return r_;       \
+  } while (0)
+
 // ---------------------------------------------------------------- workspace
 // Bump allocator over the caller's workspace (256-byte aligned pieces).
 struct Carve {
@@ -139,6 +145,13 @@ inline int lt_bits_for(int64_t entries) {
   while ((1ll << bits) < 2 * entries) ++bits;
   return bits;
 }
+
+// ---------------------------------------------------------------- host reads
+// Copies `bytes` from device memory to host memory after the stream's earlier
+// work and waits for it.  Small reads go through a page-locked buffer kept per
+// host thread (allocated on first use, held until the process ends), which
+// shortens each round trip; otherwise the copy goes to dst directly.
+int read_to_host(void *dst, const void *src, size_t bytes, hipStream_t s);
 
 // ---------------------------------------------------------------- fill / scan
 int fill_u64(uint64_t *p, size_t n, uint64_t value, hipStream_t s);

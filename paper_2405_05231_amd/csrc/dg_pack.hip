@@ -226,8 +226,7 @@ void carve_pack(PackWs &w, Carve &c, int64_t N, int B, int64_t total_nodes) {
 
 int read_err(uint32_t *err, hipStream_t s) {
   uint32_t bits = 0;
-  DG_HIP(hipMemcpyAsync(&bits, err, sizeof(bits), hipMemcpyDeviceToHost, s));
-  DG_HIP(hipStreamSynchronize(s));
+  DG_TRY(read_to_host(&bits, err, sizeof(bits), s));
   if (bits) return set_error(DG_EINVAL, "invalid input data: %s", describe_device_error(bits));
   return DG_OK;
 }
@@ -309,9 +308,7 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
   w.ms.mask = w.mask;
   w.ms.cache_slot = cache_slot;
   if ((rc = mask_scan_count(w.ms, s))) return rc;
-  DG_HIP(hipMemcpyAsync(totals, w.ms.totals, sizeof(int64_t) * mc_rows(B), hipMemcpyDeviceToHost,
-                        s));
-  DG_HIP(hipStreamSynchronize(s));
+  DG_TRY(read_to_host(totals, w.ms.totals, sizeof(int64_t) * mc_rows(B), s));
   if ((rc = read_err(w.err, s))) return rc;
   int64_t rows = 0;
   packed_ptr_host[0] = 0;

@@ -329,8 +329,7 @@ void carve_sample(SampleWs &w, Carve &c, int64_t N, int B, int64_t node_cap, boo
 
 int check_err(uint32_t *err_dev, hipStream_t s) {
   uint32_t bits = 0;
-  DG_HIP(hipMemcpyAsync(&bits, err_dev, sizeof(bits), hipMemcpyDeviceToHost, s));
-  DG_HIP(hipStreamSynchronize(s));
+  DG_TRY(read_to_host(&bits, err_dev, sizeof(bits), s));
   if (bits) return set_error(DG_EINVAL, "invalid input data: %s", describe_device_error(bits));
   return DG_OK;
 }
@@ -511,8 +510,7 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       int64_t st[ST_SIZE];
       hipLaunchKernelGGL(k_stage_err, dim3(1), dim3(1), 0, s, w.err, w.small + ST_ERR);
       DG_HIP(hipGetLastError());
-      DG_HIP(hipMemcpyAsync(st, w.small, sizeof(st), hipMemcpyDeviceToHost, s));
-      DG_HIP(hipStreamSynchronize(s));
+      DG_TRY(read_to_host(st, w.small, sizeof(st), s));
       if (st[ST_ERR])
         return set_error(DG_EINVAL, "invalid input data: %s",
                          describe_device_error((uint32_t)st[ST_ERR]));

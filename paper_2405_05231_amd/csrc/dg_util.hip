@@ -30,6 +30,30 @@ const char *describe_device_error(uint32_t bits) {
   return "unknown device error";
 }
 
+// ---------------------------------------------------------------- host reads
+constexpr size_t STAGE_BYTES = 4096;
+
+int read_to_host(void *dst, const void *src, size_t bytes, hipStream_t s) {
+  static thread_local void *stage = nullptr;
+  static thread_local bool tried = false;
+  if (!tried) {
+    tried = true;
+    if (hipHostMalloc(&stage, STAGE_BYTES, hipHostMallocDefault) != hipSuccess) {
+      (void)hipGetLastError();
+      stage = nullptr;
+    }
+  }
+  if (stage && bytes <= STAGE_BYTES) {
+    DG_HIP(hipMemcpyAsync(stage, src, bytes, hipMemcpyDeviceToHost, s));
+    DG_HIP(hipStreamSynchronize(s));
+    memcpy(dst, stage, bytes);
+    return DG_OK;
+  }
+  DG_HIP(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, s));
+  DG_HIP(hipStreamSynchronize(s));
+  return DG_OK;
+}
+
 // ---------------------------------------------------------------- fill
 __global__ void k_fill_u64(uint64_t *p, size_t n, uint64_t v) {
   size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
