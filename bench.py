@@ -123,7 +123,11 @@ def main():
                                                        dg.sample_flags(direct=True)),
                        dtype=torch.uint8, device=dev)
     counts = sr.node_count.copy()
-    pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, membership=mem)
+    # two packing outputs, so that packing step k+1 never overwrites what
+    # assembly step k is still reading
+    pr2 = [dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, membership=mem)
+           for _ in range(2)]
+    pr = pr2[0]
     ws_p = torch.empty(dg._L.dg_pack_workspace_bytes(cfg.n, B, int(counts.sum())),
                        dtype=torch.uint8, device=dev)
     nmax = int(counts.max())
@@ -133,48 +137,61 @@ def main():
         f"edges {sizes_s['total_edges']:,} packed rows {sizes_p['packed_rows']:,} "
         f"|U| {sizes_p['unique_nodes']:,} |U_nc| {sizes_p['unique_packed']:,}")
 
-    ev_asm = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-    chunks = [(b, int(counts[b])) for b in range(B)]
+    # Sampling and packing run on `stream` and return when their work is done;
+    # the fan-out gather is timed by HIP events inside dg_pack_group.  Assembly
+    # runs on `s_asm`: serially (the host waits for it) or pipelined, where
+    # assembly of step k overlaps sampling and packing of step k+1 (both
+    # streams at default priority).
+    s_asm = torch.cuda.Stream(device=dev)
+    asm_done = [torch.cuda.Event(), torch.cuda.Event()]
 
-    def step(record, marks):
-        # sampling and packing return when their work is done (host wall clock);
-        # the fan-out gather is timed by HIP events inside dg_pack_group
-        t0 = time.perf_counter()
-        s_out = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, out=sr,
-                                workspace=ws_s, membership=mem, direct=True)
-        t1 = time.perf_counter()
-        p_out = dg.pack_group(w.feats, w.cache_slot, s_out.nodes, counts, out=pr,
-                              workspace=ws_p, timing=record, membership=mem)
-        t2 = time.perf_counter()
-        if record:
-            ev_asm[0].record(stream)
-        for b, n in chunks:
-            dg.assemble_batch(w.cache, p_out.chunk(b), p_out.loc[b, :n], R, out=ybuf[b & 1],
-                              stream=stream)
-        if record:
-            ev_asm[1].record(stream)
-        marks.append((t1 - t0, t2 - t1))
-        return s_out, p_out
+    def run(K, pipelined, record):
+        marks, gather_ms, asm_ms = [], [], []
+        evs = []
+        for k in range(K):
+            slot = k & 1
+            t0 = time.perf_counter()
+            s_out = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, out=sr,
+                                    workspace=ws_s, membership=mem, direct=True, stream=stream)
+            t1 = time.perf_counter()
+            stream.wait_event(asm_done[slot])  # the assembly that last read pr2[slot]
+            p_out = dg.pack_group(w.feats, w.cache_slot, s_out.nodes, counts, out=pr2[slot],
+                                  workspace=ws_p, timing=record, membership=mem,
+                                  stream=stream)
+            t2 = time.perf_counter()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            s_asm.wait_stream(stream)
+            e0.record(s_asm)
+            dg.assemble_batches(w.cache, p_out, counts, ybuf, stream=s_asm)
+            e1.record(s_asm)
+            asm_done[slot].record(s_asm)
+            if not pipelined:
+                e1.synchronize()
+            evs.append((e0, e1))
+            marks.append((t1 - t0, t2 - t1))
+            if record:
+                gather_ms.append(p_out.timing["gather_ms"])
+        torch.cuda.synchronize()
+        asm_ms = [a.elapsed_time(b) for a, b in evs]
+        return marks, gather_ms, asm_ms, s_out, p_out
 
-    for _ in range(args.warmup):
-        step(False, [])
-    torch.cuda.synchronize()
+    def timed(pipelined):
+        run(args.warmup, pipelined, False)
+        torch.cuda.synchronize()
+        t_start = time.perf_counter()
+        res = run(args.steps, pipelined, True)
+        torch.cuda.synchronize()
+        t_total = time.perf_counter() - t_start
+        if res[3].sizes != sizes_s or res[4].sizes != sizes_p:
+            raise RuntimeError("sizes changed between steps")
+        return (t_total,) + res
 
-    # timed region: K whole steps
-    marks, gather_ms, asm_ms = [], [], []
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for _ in range(args.steps):
-        s_out, p_out = step(True, marks)
-        gather_ms.append(p_out.timing["gather_ms"])
-        ev_asm[1].synchronize()
-        asm_ms.append(ev_asm[0].elapsed_time(ev_asm[1]))
-    torch.cuda.synchronize()
-    t_total = time.perf_counter() - t_start
+    # timed regions: K whole steps serially, then K whole steps pipelined
+    t_serial, marks, gather_ms, asm_ms, _, _ = timed(False)
+    t_total, marks_p, _, asm_ms_p, _, _ = timed(True)
     samp_ms = [1e3 * a for a, _ in marks]
     pack_ms = [1e3 * b for _, b in marks]
-    if s_out.sizes != sizes_s or p_out.sizes != sizes_p:
-        raise RuntimeError("sizes changed between steps")
 
     Uc = sizes_p["unique_packed"]
     P = sizes_p["packed_rows"]
@@ -184,6 +201,7 @@ def main():
     F = F_pack + F_asm
     ms_step = 1e3 * t_total / args.steps
     value = F * args.steps / t_total / 1e9
+    ms_serial = 1e3 * t_serial / args.steps
     g_ms = float(np.mean(gather_ms))
     achieved = F_pack / (g_ms * 1e-3) / 1e9
     edges = sizes_s["total_edges"]
@@ -207,6 +225,13 @@ def main():
                    "row_bytes": R, "batches": B, "seeds_per_batch": cfg.S, "fanouts": fan,
                    "cache_rows": int(w.cache_nodes.numel()), "parallelism": "single-gpu"},
         "frac_hbm_peak": round(value / HBM_PEAK_GBPS, 4),
+        "pipelined": "assembly of step k (second stream) overlaps sampling and packing of "
+                     "step k+1; the serial figures below wait for each step's assembly",
+        "serial": {"ms_per_step": round(ms_serial, 3),
+                   "value": round(F * args.steps / t_serial / 1e9, 2)},
+        "pipelined_phases_ms": {"sample": round(1e3 * float(np.mean([a for a, _ in marks_p])), 3),
+                                "pack": round(1e3 * float(np.mean([b for _, b in marks_p])), 3),
+                                "assemble_all_batches": round(float(np.mean(asm_ms_p)), 3)},
         "sampled_edges_per_s": round(edges / (np.mean(samp_ms) * 1e-3), 1),
         "phases_ms": {"sample": round(float(np.mean(samp_ms)), 3),
                       "pack": round(float(np.mean(pack_ms)), 3),

@@ -262,3 +262,27 @@ def test_membership_handoff_matches_standalone_pack(dg):
     bad[free] = 1
     with pytest.raises(dg.DGError):
         dg.pack_group(X, slot, sr.nodes, sr.node_count, membership=bad)
+
+
+def test_assemble_batches_matches_per_batch_calls(dg):
+    """The group helper issues the same per-batch library call; outputs equal
+    dg_assemble_batch's, batch by batch, and out-of-range loc is flagged."""
+    w = synth.make_workload("T")
+    X, slot = w.feats.to(DEV), w.cache_slot.to(DEV)
+    sr = dg.sample_group(w.offsets.to(DEV), w.indices.to(DEV), w.seeds.to(DEV),
+                         list(w.cfg.fanouts), w.rng_seed)
+    pr = dg.pack_group(X, slot, sr.nodes, sr.node_count)
+    cache = X.index_select(0, w.cache_nodes.to(DEV))
+    R = pr.row_bytes
+    counts = sr.node_count
+    outs = [torch.full((int(counts.max()), R), 0xAB, dtype=torch.uint8, device=DEV)
+            for _ in range(len(counts))]
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    dg.assemble_batches(cache, pr, counts, outs, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    for b, n in enumerate(counts):
+        ref = dg.assemble_batch(cache, pr.chunk(b), pr.loc[b, :int(n)], R)
+        assert torch.equal(outs[b][:int(n)], ref), b
+    with pytest.raises(ValueError):
+        dg.assemble_batches(cache, pr, counts, [outs[0][:1]])
