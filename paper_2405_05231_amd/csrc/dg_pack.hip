@@ -88,7 +88,10 @@ __global__ __launch_bounds__(THREADS) void k_build_loc(Lists L, const int32_t *n
 }
 
 // Fan-out gather, 16-byte path: a group of LPR lanes reads the row of one U_nc
-// node once and stores it into each of its destination rows.
+// node once and stores it into each of its destination rows.  Every U_nc node
+// has at least one destination; its first destination index is loaded together
+// with the row, so the common single-destination case needs two dependent
+// round trips (indices, then row + destination) before its stores.
 template <int LPR, int CPL>
 __global__ __launch_bounds__(THREADS) void k_fanout16(const v4u *X, const int32_t *unc_ids,
                                                       const int64_t *unc_off, int64_t n_unc,
@@ -99,31 +102,44 @@ __global__ __launch_bounds__(THREADS) void k_fanout16(const v4u *X, const int32_
   const int64_t grp = (int64_t)blockIdx.x * GPB + threadIdx.x / LPR;
   const int64_t ngrp = (int64_t)gridDim.x * GPB;
   for (int64_t i0 = grp * UNROLL; i0 < n_unc; i0 += ngrp * UNROLL) {
-    int64_t p0[UNROLL], p1[UNROLL];
-    v4u v[UNROLL][CPL];
+    int64_t p0[UNROLL], p1[UNROLL], d0[UNROLL];
+    int32_t id[UNROLL];
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
-      int64_t i = i0 + u;
+      const int64_t i = i0 + u;
       p0[u] = p1[u] = 0;
-      const v4u *src = nullptr;
+      id[u] = -1;
       if (i < n_unc) {
-        src = X + (int64_t)unc_ids[i] * C;
+        id[u] = unc_ids[i];
         p0[u] = unc_off[i];
         p1[u] = i + 1 < n_unc ? unc_off[i + 1] : n_pairs;
       }
+    }
+    v4u v[UNROLL][CPL];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      d0[u] = p1[u] > p0[u] ? pairdest[p0[u]] : -1;
+      const v4u *src = id[u] >= 0 ? X + (int64_t)id[u] * C : nullptr;
 #pragma unroll
       for (int c = 0; c < CPL; ++c) {
-        int ch = sub + c * LPR;
+        const int ch = sub + c * LPR;
         v[u][c] = (src && ch < C) ? ld_stream(src + ch) : v4u{0u, 0u, 0u, 0u};
       }
     }
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
-      for (int64_t p = p0[u]; p < p1[u]; ++p) {
-        v4u *dst = packed + pairdest[p] * C;
+      if (d0[u] < 0) continue;
+      v4u *dst = packed + d0[u] * C;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        const int ch = sub + c * LPR;
+        if (ch < C) st_stream(v[u][c], dst + ch);
+      }
+      for (int64_t p = p0[u] + 1; p < p1[u]; ++p) {
+        dst = packed + pairdest[p] * C;
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
-          int ch = sub + c * LPR;
+          const int ch = sub + c * LPR;
           if (ch < C) st_stream(v[u][c], dst + ch);
         }
       }
