@@ -54,7 +54,7 @@ __global__ __launch_bounds__(THREADS) void k_assemble16(const v4u *cache, int64_
 #pragma unroll
       for (int c = 0; c < CPL; ++c) {
         int ch = sub + c * LPR;
-        v[u][c] = (src[u] && ch < C) ? ld_stream(src[u] + ch) : v4u{0u, 0u, 0u, 0u};
+        v[u][c] = (src[u] && ch < C) ? src[u][ch] : v4u{0u, 0u, 0u, 0u};
       }
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
