@@ -73,12 +73,15 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calib", action="store_true",
                     help="also run a plain copy of known size (counter calibration)")
-    ap.add_argument("--experiment", choices=["pack_ab", "cache", "layered", "minhash"],
+    ap.add_argument("--groups", type=int, default=16,
+                    help="groups of B mini-batches for --experiment regime")
+    ap.add_argument("--experiment", choices=["pack_ab", "cache", "layered", "minhash", "regime"],
                     default=None,
                     help="instead of the step benchmark: batched vs individual packing "
                          "(pack_ab), access-frequency vs in-degree cache (cache), or "
                          "layer-wise (DGL-style) vs new-node frontier sampling (layered), or "
-                         "disk-cache pages touched under ID vs MinHash order (minhash)")
+                         "disk-cache pages touched under ID vs MinHash order (minhash), or "
+                         "the node access distribution over several groups (regime)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -110,7 +113,9 @@ def main():
     if args.experiment:
         out = {"pack_ab": experiment_pack_ab, "cache": experiment_cache,
                "layered": experiment_layered,
-               "minhash": experiment_minhash}[args.experiment](dg, w, cfg, args.steps)
+               "minhash": experiment_minhash,
+               "regime": lambda *a: experiment_regime(*a, groups=args.groups)}[args.experiment](
+                   dg, w, cfg, args.steps)
         print(json.dumps(out), flush=True)
         return
 
@@ -220,6 +225,9 @@ def main():
         "vs_baseline": None,
         "dtype": "u8",
         "data": "synthetic",
+        "device": {"name": torch.cuda.get_device_name(dev),
+                   "arch": torch.cuda.get_device_properties(dev).gcnArchName,
+                   "hip": torch.version.hip},
         "config": {"workload": cfg.name, "nodes": cfg.n, "edges": w.num_edges,
                    "rmat_draws": cfg.draws, "feature": f"{cfg.dim}x{str(cfg.dtype)[6:]}",
                    "row_bytes": R, "batches": B, "seeds_per_batch": cfg.S, "fanouts": fan,
@@ -399,6 +407,61 @@ def experiment_minhash(dg, w, cfg, reps, k=4, page_bytes=4096):
             "rows_per_page": rpp, "order_ms": round(_median(ts[1:]), 3),
             "pages_id_order": id_pages, "pages_minhash_order": mh_pages,
             "pages_lower_bound": lower, "reduction": round(id_pages / max(mh_pages, 1), 3)}
+
+
+def _popcount64(x):
+    """Set bits of each int64 word (SWAR; masks keep arithmetic shifts exact)."""
+    x = x - ((x >> 1) & 0x5555555555555555)
+    x = (x & 0x3333333333333333) + ((x >> 2) & 0x3333333333333333)
+    x = (x + (x >> 4)) & 0x0F0F0F0F0F0F0F0F
+    return ((x * 0x0101010101010101) >> 56) & 0xFF
+
+
+# Node access distribution reported by the paper (Table 3), per dataset:
+# access share of the nodes ranked <1%, 1-5%, 5-10%, >10% by access frequency.
+PAPER_TABLE3 = {"FS": [14.1, 25.5, 18.2, 42.1], "PS": [43.2, 36.5, 11.2, 9.1],
+                "MG": [56.4, 32.3, 7.3, 4.0], "IG": [22.5, 30.0, 20.8, 26.7]}
+
+
+def experiment_regime(dg, w, cfg, reps, groups=16):
+    """Regime check of the synthetic workload: sample `groups` consecutive
+    groups of B mini-batches (about an epoch's seeds for L100), count each
+    node's accesses (the mini-batches that require it), rank nodes by count and
+    report the access share of the top <1%, 1-5%, 5-10% and >10% of nodes, next
+    to the paper's Table 3; also sum|P_b| / N per group and over all groups
+    (packed rows relative to the feature table, at the workload's cache)."""
+    import torch
+
+    import synth
+    B, N = cfg.B, cfg.n
+    dev = w.offsets.device
+    seeds = synth.seed_batches(N, groups * B, cfg.S, cfg.seed, dev, offsets=w.offsets)
+    assert torch.equal(seeds[:B], w.seeds), "the first group must be the benchmark group"
+    cnt = torch.zeros(N, dtype=torch.int32, device=dev)
+    mem = torch.empty(N, dtype=torch.int64, device=dev)
+    packed_rows = []
+    for g in range(groups):
+        sr = dg.sample_group(w.offsets, w.indices, seeds[g * B:(g + 1) * B].contiguous(),
+                             list(cfg.fanouts), w.rng_seed, batch_base=g * B, membership=mem,
+                             direct=True)
+        cnt += _popcount64(mem).to(torch.int32)
+        pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, sr.node_count, membership=mem,
+                           tables_only=True)
+        packed_rows.append(pr.sizes["packed_rows"])
+        del sr, pr
+    total = int(cnt.sum(dtype=torch.int64))
+    ranked = torch.sort(cnt, descending=True).values.to(torch.int64)
+    cuts = [0, N // 100, N // 20, N // 10, N]
+    shares = [round(100.0 * int(ranked[a:b].sum()) / total, 1) for a, b in zip(cuts, cuts[1:])]
+    return {"experiment": "node access distribution (regime check)", "workload": cfg.name,
+            "groups": groups, "mini_batches": groups * B, "seeds": groups * B * cfg.S,
+            "accesses": total, "accessed_nodes": int((cnt > 0).sum()),
+            "share_pct_by_rank": {"<1%": shares[0], "1-5%": shares[1], "5-10%": shares[2],
+                                  ">10%": shares[3]},
+            "paper_table3_pct": PAPER_TABLE3,
+            "packed_rows_over_N": {"first_group": round(packed_rows[0] / N, 4),
+                                   "all_groups": round(sum(packed_rows) / N, 4)},
+            "cache_rows": int(w.cache_nodes.numel())}
 
 
 def cpu_baseline(w, cfg, nb):
