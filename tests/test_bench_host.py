@@ -1,0 +1,42 @@
+"""Host-side pieces of bench.py (no GPU): the multi-GPU refusal, the popcount
+used by the regime check, and the traffic digest."""
+import os
+import random
+import subprocess
+import sys
+
+import torch
+
+from conftest import ROOT
+
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+
+
+def test_popcount64_matches_python():
+    rnd = random.Random(5)
+    vals = [0, 1, -1, 2**63 - 1, -2**63] + [rnd.getrandbits(64) - 2**63 for _ in range(500)]
+    got = bench._popcount64(torch.tensor(vals, dtype=torch.int64)).tolist()
+    assert got == [bin(v & (2**64 - 1)).count("1") for v in vals]
+
+
+def test_traffic_digest_covers_the_gather_translation_unit(tmp_path, monkeypatch):
+    d = bench.kernel_source_digest()
+    assert len(d) == 16
+    # the digest changes with any file of the translation unit
+    src = os.path.join(ROOT, "paper_2405_05231_amd", "csrc")
+    fake = tmp_path / "paper_2405_05231_amd" / "csrc"
+    fake.mkdir(parents=True)
+    for n in bench.GATHER_TU:
+        (fake / n).write_bytes(open(os.path.join(src, n), "rb").read())
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.kernel_source_digest() == d
+    (fake / "dg_pack.hip").write_bytes(b"// changed\n" + (fake / "dg_pack.hip").read_bytes())
+    assert bench.kernel_source_digest() != d
