@@ -211,8 +211,11 @@ struct MaskScan {
   int32_t *local_out;                // [N][B]: local index of (u, b) = local_base[b] + rank
   int64_t local_base[DG_MAX_BATCHES];
   uint64_t *prev;                    // nullable: members already listed; the passes
-                                     // see mask & ~prev, and the write pass adds
+                                     // see mask & ~prev, and the count pass adds
                                      // the new bits to prev
+  bool keep_prev;                    // false: leave prev as it is (nothing reads it later)
+  const uint8_t *touched;            // nullable: a byte per 64-node round; rounds
+                                     // whose byte is 0 hold no bit to list (not read)
   // The write pass runs in one of two modes: packing (pairdest set: seg_out,
   // unc_ids, unc_off, nodeoff required, uniq_out optional, cached nodes left out
   // of the lists) or sampling (pairdest NULL: prev and seg_out required,

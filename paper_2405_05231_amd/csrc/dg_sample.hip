@@ -38,6 +38,8 @@ struct Hop {
   int64_t fpos[DG_MAX_BATCHES];        // local position of b's first frontier node
   int64_t ebase[DG_MAX_BATCHES];       // edges of b before this hop
   uint64_t bstate[DG_MAX_BATCHES];     // mix64(rng_seed + gamma*(g+1)) per batch
+  uint8_t *touched;                    // nullable: byte per 64-node round, set for
+                                       // every round that gains a membership bit
 };
 
 // Flattened (batch, position) ranges, for passes over all edge lists, with
@@ -100,7 +102,7 @@ constexpr int EMIT = 8;
 __device__ __forceinline__ void emit_chunk(const int32_t (&u)[EMIT], const int64_t (&slot)[EMIT],
                                            int cnt, int b, int32_t parent, int32_t *edge_src,
                                            int32_t *edge_dst, uint64_t *visited, int64_t N,
-                                           uint32_t *err) {
+                                           uint8_t *touched, uint32_t *err) {
   const uint64_t bit = 1ull << b;
   uint64_t seen[EMIT];
 #pragma unroll
@@ -117,7 +119,10 @@ __device__ __forceinline__ void emit_chunk(const int32_t (&u)[EMIT], const int64
   }
 #pragma unroll
   for (int k = 0; k < EMIT; ++k)
-    if (k < cnt && !(seen[k] & bit)) atomicOr((unsigned long long *)&visited[u[k]], bit);
+    if (k < cnt && !(seen[k] & bit)) {
+      atomicOr((unsigned long long *)&visited[u[k]], bit);
+      if (touched) touched[u[k] >> 6] = 1;
+    }
 }
 
 // One lane per frontier node.  Floyd's subset is built in registers (fully
@@ -151,7 +156,7 @@ __global__ __launch_bounds__(THREADS) void k_hop_sample(
         slot[k] = base + q0 + k;
         u[k] = k < cnt ? idx[o0 + q0 + k] : 0;
       }
-      emit_chunk(u, slot, cnt, b, parent, edge_src, edge_dst, visited, N, err);
+      emit_chunk(u, slot, cnt, b, parent, edge_src, edge_dst, visited, N, h.touched, err);
     }
     return;
   }
@@ -190,7 +195,7 @@ __global__ __launch_bounds__(THREADS) void k_hop_sample(
           slot[k] = base + rank;
           u[k] = k < cnt ? idx[o0 + r[s]] : 0;
         }
-        emit_chunk(u, slot, cnt, b, parent, edge_src, edge_dst, visited, N, err);
+        emit_chunk(u, slot, cnt, b, parent, edge_src, edge_dst, visited, N, h.touched, err);
       }
     }
     return;
@@ -221,7 +226,7 @@ __global__ __launch_bounds__(THREADS) void k_hop_sample(
       slot[k] = base + s0 + k;
       u[k] = k < cnt ? idx[o0 + r[s0 + k]] : 0;
     }
-    emit_chunk(u, slot, cnt, b, parent, edge_src, edge_dst, visited, N, err);
+    emit_chunk(u, slot, cnt, b, parent, edge_src, edge_dst, visited, N, h.touched, err);
   }
 }
 
@@ -303,6 +308,7 @@ struct SampleWs {
   int64_t *f_off, *f_deg, *f_cnt, *f_eoff, *tiles;
   LocalTable table;  // hash relabelling
   int32_t *local;    // direct relabelling: [N][B]
+  uint8_t *touched;  // a byte per 64-node round (sparse hops)
   int64_t *small;    // staging for a few counts
   MaskScan ms;
 };
@@ -320,6 +326,7 @@ void carve_sample(SampleWs &w, Carve &c, int64_t N, int B, int64_t node_cap, boo
   w.table.bits = direct ? 0 : lt_bits_for(fmax);
   w.table.slots = direct ? nullptr : c.take<uint64_t>((size_t)1 << w.table.bits);
   w.local = direct ? c.take<int32_t>((size_t)N * (size_t)B) : nullptr;
+  w.touched = c.take<uint8_t>((size_t)mc_blocks(N) * (MC_BLOCK_NODES / 64));
   w.small = c.take<int64_t>(ST_SIZE);
   w.ms = MaskScan{};
   w.ms.N = N;
@@ -472,6 +479,13 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       for (int b = 0; b < B; ++b) new_b[b] = 0;
     } else {
       const int ev0 = tm.mark();
+      // A hop whose edges can reach only a small share of the nodes marks the
+      // 64-node rounds it touches, and its count pass skips the others.
+      const int64_t ebound = f < 0 ? E : h.ftot * (int64_t)f;
+      h.touched = ebound <= N / 32 ? w.touched : nullptr;
+      if (h.touched && (rc = fill_u64(reinterpret_cast<uint64_t *>(w.touched),
+                                      (size_t)mc_blocks(N) * (MC_BLOCK_NODES / 64) / 8, 0, s)))
+        return rc;
       hipLaunchKernelGGL(k_frontier_degree, dim3(blocks_for(h.ftot)), dim3(THREADS), 0, s, h,
                          nodes, node_cap, g->offsets, N, E, w.f_off, w.f_deg, w.f_cnt, w.err);
       DG_HIP(hipGetLastError());
@@ -489,6 +503,8 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       // reads this hop's counts (it stops at each list's capacity)
       w.ms.mask = w.visited;
       w.ms.prev = w.prev;
+      w.ms.keep_prev = k < K;  // after the last hop nothing reads prev
+      w.ms.touched = h.touched;
       w.ms.cache_slot = nullptr;
       w.ms.totals = w.small + ST_TOTALS;
       if ((rc = mask_scan_count(w.ms, s))) return rc;

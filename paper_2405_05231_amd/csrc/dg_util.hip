@@ -203,10 +203,17 @@ struct TileBits {
 // needed later.
 __device__ __forceinline__ void load_tile(const MaskScan &a, int64_t t0, int lane, TileBits &t,
                                           bool check_slots, bool update_prev) {
+  uint32_t live = 0xffffu;  // bit r: round r may hold bits to list
+  if (a.touched) {
+    const uint8_t *f = a.touched + (t0 >> 6);
+    live = 0;
+#pragma unroll
+    for (int r = 0; r < MC_ROUNDS; ++r) live |= (f[r] ? 1u : 0u) << r;
+  }
 #pragma unroll
   for (int r = 0; r < MC_ROUNDS; ++r) {
     int64_t u = t0 + r * 64 + lane;
-    t.m[r] = u < a.N ? a.mask[u] : 0ull;
+    t.m[r] = (u < a.N && ((live >> r) & 1u)) ? a.mask[u] : 0ull;
   }
   if (a.B < 64) {  // bits of batches outside the group are ignored
     const uint64_t keep = (1ull << a.B) - 1ull;
@@ -281,7 +288,7 @@ __global__ __launch_bounds__(MC_THREADS) void k_mask_count(MaskScan a) {
   const int B = a.B, rows = mc_rows(B);
   const int64_t t0 = (int64_t)blockIdx.x * MC_BLOCK_NODES + (int64_t)w * MC_TILE;
   TileBits t;
-  load_tile(a, t0, lane, t, true, true);
+  load_tile(a, t0, lane, t, true, a.keep_prev);
   uint32_t cu, cnc, cp, call;
   uint32_t mine = tile_counts(t, lane, &cu, &cnc, &cp, &call);
   // the tile's non-empty words, in node order, for the write pass
