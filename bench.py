@@ -86,7 +86,8 @@ def main():
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on exactly one GPU: the hot path is measured on one GPU's "
-              "share; see DESIGN.md for how it would shard.", file=sys.stderr)
+              "share of the work; running it across several GPUs is not implemented.",
+              file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
