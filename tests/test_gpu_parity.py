@@ -286,3 +286,23 @@ def test_assemble_batches_matches_per_batch_calls(dg):
         assert torch.equal(outs[b][:int(n)], ref), b
     with pytest.raises(ValueError):
         dg.assemble_batches(cache, pr, counts, [outs[0][:1]])
+
+
+@pytest.mark.parametrize("layered,direct", [(False, False), (True, True)])
+def test_sparse_hops_on_a_large_graph(dg, orc, layered, direct):
+    """A small frontier on a large graph: every hop's edges reach only a small
+    share of the nodes, so the sampler lists new nodes from the 64-node rounds
+    its draws touched (the count pass skips the others)."""
+    n = 200_000
+    off, idx = synth.uniform_graph(n, 0, 6, seed=31)
+    off, idx = torch.from_numpy(off), torch.from_numpy(idx)
+    rnd = random.Random(4242)
+    seeds = torch.tensor([rnd.sample(range(n), 16) for _ in range(4)], dtype=torch.int32)
+    gen = torch.Generator().manual_seed(7)
+    feats = torch.randn((n, 4), generator=gen)
+    ncache = n // 10
+    cache_nodes = torch.tensor(rnd.sample(range(n), ncache), dtype=torch.int64)
+    slot = torch.full((n,), -1, dtype=torch.int32)
+    slot[cache_nodes] = torch.arange(ncache, dtype=torch.int32)
+    check_all(dg, orc, off, idx, seeds, [3, 3, 2], 99, feats, slot, cache_nodes, batch_base=5,
+              sample_kw={"layered": layered, "direct": direct})
