@@ -83,6 +83,8 @@ def main():
                          "disk-cache pages touched under ID vs MinHash order (minhash), or "
                          "the node access distribution over several groups (regime)")
     args = ap.parse_args()
+    if args.steps < 1 or args.warmup < 0:
+        ap.error("--steps must be at least 1 and --warmup at least 0")
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on exactly one GPU: the hot path is measured on one GPU's "
@@ -154,6 +156,7 @@ def main():
     def run(K, pipelined, record):
         marks, gather_ms, asm_ms = [], [], []
         evs = []
+        s_out = p_out = None
         for k in range(K):
             slot = k & 1
             t0 = time.perf_counter()
