@@ -94,35 +94,35 @@ __global__ __launch_bounds__(THREADS) void k_frontier_degree(
   f_cnt[i] = (h.f < 0 || d <= (int64_t)h.f) ? d : (int64_t)h.f;
 }
 
-// Emits up to EMIT sampled edges whose neighbour IDs are already loaded:
-// edge stores, then plain loads of the membership words, then a
-// fire-and-forget atomicOr for each neighbour not yet in the batch.
+// Emits up to EMIT sampled edges whose neighbour IDs are already loaded: the
+// edge stores, then a fire-and-forget atomicOr of the batch's bit into each
+// neighbour's membership word (setting a bit that is already set changes
+// nothing, and skipping the atomic for seen pairs would cost a dependent read
+// of the word, which measures slower than the atomics it saves).
 constexpr int EMIT = 8;
 
 __device__ __forceinline__ void emit_chunk(const int32_t (&u)[EMIT], const int64_t (&slot)[EMIT],
                                            int cnt, int b, int32_t parent, int32_t *edge_src,
                                            int32_t *edge_dst, uint64_t *visited, int64_t N,
                                            uint8_t *touched, uint32_t *err) {
-  const uint64_t bit = 1ull << b;
-  uint64_t seen[EMIT];
+  const unsigned long long bit = 1ull << b;
 #pragma unroll
   for (int k = 0; k < EMIT; ++k) {
-    seen[k] = bit;
     if (k < cnt) {
       edge_src[slot[k]] = parent;
       edge_dst[slot[k]] = u[k];
-      if (u[k] >= 0 && (int64_t)u[k] < N)
-        seen[k] = visited[u[k]];
-      else
-        atomicOr(err, ERR_NBR_RANGE);
     }
   }
 #pragma unroll
-  for (int k = 0; k < EMIT; ++k)
-    if (k < cnt && !(seen[k] & bit)) {
+  for (int k = 0; k < EMIT; ++k) {
+    if (k >= cnt) continue;
+    if (u[k] >= 0 && (int64_t)u[k] < N) {
       atomicOr((unsigned long long *)&visited[u[k]], bit);
       if (touched) touched[u[k] >> 6] = 1;
+    } else {
+      atomicOr(err, ERR_NBR_RANGE);
     }
+  }
 }
 
 // One lane per frontier node.  Floyd's subset is built in registers (fully
