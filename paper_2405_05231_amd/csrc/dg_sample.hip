@@ -4,9 +4,11 @@
 // Device state: a node-major membership mask visited[u] (bit b = u is in
 // mini-batch b) and its copy prev[u] as of the start of the current hop.  A
 // hop is: degree pass over the frontier -> exclusive scan (edge slots) -> draw
-// + mark (fire-and-forget atomicOr on visited) -> compaction of visited & ~prev
-// (the nodes new at this hop) into each batch's new segment, ascending, with
-// no sort; the compaction also brings prev up to date.  Sampled neighbours are
+// + mark (a fire-and-forget atomicOr on visited per sampled edge; a hop that
+// can reach only a small share of the nodes also marks the 64-node rounds it
+// touches) -> compaction of visited & ~prev (the nodes new at this hop) into
+// each batch's new segment, ascending, with no sort; the compaction also brings
+// prev up to date -> one read-back of the hop's counts.  Sampled neighbours are
 // relabelled from global to local IDs at the end, through one of two tables:
 // a direct [N][B] array of local indices that the compaction fills as it
 // assigns them (DG_SAMPLE_DIRECT), or a (node, batch) hash table sized for the
