@@ -499,7 +499,15 @@ def cpu_baseline(w, cfg, nb):
     edges = sum(len(x) for x in rs["edge_src"])
     F = R * (rp["unique_packed"] + rp["packed_rows"]) + 2 * R * pairs
     what = "the whole group" if nb == cfg.B else f"the first {nb} of {cfg.B} mini-batches"
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")),
+                       cpu)
+    except OSError:
+        pass
     return {"value": round(F / (t4 - t1) / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "cpu_model": cpu,
             "sample": f"{what} of {cfg.name} (full graph and feature table on the host): "
                       f"sample + pack + assemble, single-threaded C, one pass",
             "seconds": {"sample": round(t2 - t1, 3), "pack": round(t3 - t2, 3),
