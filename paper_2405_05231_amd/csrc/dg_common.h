@@ -199,6 +199,7 @@ struct MaskScan {
   int64_t *chunk_sum;  // [chunks][rows]
   int64_t *totals;     // [rows]
   uint32_t *err;
+  int64_t *err_stage;  // nullable: receives *err after the count pass (for the read-back)
   // write pass outputs (which are required depends on the mode, see below)
   int64_t seg_base[DG_MAX_BATCHES];  // start index of batch b's list in seg_out
   int64_t seg_end[DG_MAX_BATCHES];   // sampling: end of batch b's room in seg_out

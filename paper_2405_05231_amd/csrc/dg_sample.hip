@@ -294,8 +294,6 @@ constexpr int ST_TOTALS = ST_BOUNDS + DG_MAX_BATCHES + 1; // [B+4]
 constexpr int ST_ERR = ST_TOTALS + DG_MAX_BATCHES + 4;
 constexpr int ST_SIZE = ST_ERR + 1;
 
-__global__ void k_stage_err(const uint32_t *err, int64_t *out) { *out = (int64_t)*err; }
-
 // eoff at each batch's first frontier entry (and at the end).
 __global__ void k_batch_bounds(Hop h, const int64_t *f_eoff, int64_t *out) {
   int b = threadIdx.x;
@@ -509,6 +507,7 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       w.ms.touched = h.touched;
       w.ms.cache_slot = nullptr;
       w.ms.totals = w.small + ST_TOTALS;
+      w.ms.err_stage = w.small + ST_ERR;
       if ((rc = mask_scan_count(w.ms, s))) return rc;
       for (int b = 0; b < B; ++b) {
         w.ms.seg_base[b] = (int64_t)b * node_cap + n_b[b];
@@ -526,8 +525,6 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       const int ev2 = tm.mark();
       // one round trip per hop: edge bounds, node counts and the error word
       int64_t st[ST_SIZE];
-      hipLaunchKernelGGL(k_stage_err, dim3(1), dim3(1), 0, s, w.err, w.small + ST_ERR);
-      DG_HIP(hipGetLastError());
       DG_TRY(read_to_host(st, w.small, sizeof(st), s));
       if (st[ST_ERR])
         return set_error(DG_EINVAL, "invalid input data: %s",

@@ -331,18 +331,34 @@ __global__ __launch_bounds__(MC_THREADS) void k_mask_count(MaskScan a) {
 
 // Row scan, three phases over the [nblk][rows] count matrix: chunk sums,
 // scan of chunk sums down each row, then per-block bases.
-__global__ __launch_bounds__(128) void k_rows_chunk_sum(MaskScan a) {
-  const int rows = mc_rows(a.B);
-  const int t = threadIdx.x;
-  if (t >= rows) return;
+// A chunk of the count matrix (MC_CHUNK consecutive blocks, all rows) is one
+// contiguous run of memory; it is staged through LDS so the global reads and
+// writes are coalesced and only the column walks stride.
+constexpr int RS_THREADS = 256;
+constexpr int RS_MAX = MC_CHUNK * (DG_MAX_BATCHES + 4);
+
+__device__ __forceinline__ int stage_chunk(const MaskScan &a, uint32_t *s, int rows) {
   const int64_t b0 = (int64_t)blockIdx.x * MC_CHUNK;
-  const int64_t n = a.nblk - b0 < MC_CHUNK ? a.nblk - b0 : MC_CHUNK;
-  int64_t acc = 0;
-#pragma unroll 16
-  for (int64_t i = 0; i < n; ++i) acc += a.cnt[(size_t)(b0 + i) * rows + t];
-  a.chunk_sum[(size_t)blockIdx.x * rows + t] = acc;
+  const int n = (int)(a.nblk - b0 < MC_CHUNK ? a.nblk - b0 : MC_CHUNK);
+  const uint32_t *src = a.cnt + (size_t)b0 * rows;
+  for (int i = threadIdx.x; i < n * rows; i += RS_THREADS) s[i] = src[i];
+  __syncthreads();
+  return n;
 }
 
+__global__ __launch_bounds__(RS_THREADS) void k_rows_chunk_sum(MaskScan a) {
+  __shared__ uint32_t s[RS_MAX];
+  const int rows = mc_rows(a.B);
+  const int n = stage_chunk(a, s, rows);
+  for (int t = threadIdx.x; t < rows; t += RS_THREADS) {
+    int64_t acc = 0;
+    for (int k = 0; k < n; ++k) acc += s[k * rows + t];
+    a.chunk_sum[(size_t)blockIdx.x * rows + t] = acc;
+  }
+}
+
+// Also stages the device error word for the caller's read-back (err_stage),
+// after every kernel of the pass so far has run.
 __global__ __launch_bounds__(1024) void k_rows_chunk_scan(MaskScan a) {
   const int rows = mc_rows(a.B);
   const int row = blockIdx.x;
@@ -357,31 +373,33 @@ __global__ __launch_bounds__(1024) void k_rows_chunk_scan(MaskScan a) {
     carry += total;
   }
   if (threadIdx.x == 0) a.totals[row] = carry;
+  if (row == 0 && threadIdx.x == 0 && a.err_stage) *a.err_stage = (int64_t)*a.err;
 }
 
-__global__ __launch_bounds__(128) void k_rows_apply(MaskScan a) {
+__global__ __launch_bounds__(RS_THREADS) void k_rows_apply(MaskScan a) {
+  __shared__ uint32_t s[RS_MAX];
+  __shared__ int64_t sb[RS_MAX];
   const int rows = mc_rows(a.B);
-  const int t = threadIdx.x;
-  if (t >= rows) return;
-  const int64_t b0 = (int64_t)blockIdx.x * MC_CHUNK;
-  const int64_t n = a.nblk - b0 < MC_CHUNK ? a.nblk - b0 : MC_CHUNK;
-  int64_t run = a.chunk_sum[(size_t)blockIdx.x * rows + t];
-#pragma unroll 16
-  for (int64_t i = 0; i < n; ++i) {
-    const size_t at = (size_t)(b0 + i) * rows + t;
-    const int64_t v = a.cnt[at];
-    a.base[at] = run;
-    run += v;
+  const int n = stage_chunk(a, s, rows);
+  for (int t = threadIdx.x; t < rows; t += RS_THREADS) {
+    int64_t run = a.chunk_sum[(size_t)blockIdx.x * rows + t];
+    for (int k = 0; k < n; ++k) {
+      sb[k * rows + t] = run;
+      run += s[k * rows + t];
+    }
   }
+  __syncthreads();
+  int64_t *dst = a.base + (size_t)blockIdx.x * MC_CHUNK * rows;
+  for (int i = threadIdx.x; i < n * rows; i += RS_THREADS) dst[i] = sb[i];
 }
 
 int mask_scan_count(MaskScan &m, hipStream_t s) {
   if (m.nblk == 0) return fill_u64(reinterpret_cast<uint64_t *>(m.totals), mc_rows(m.B), 0, s);
   const unsigned nch = (unsigned)mc_chunks(m.nblk);
   hipLaunchKernelGGL(k_mask_count, dim3((unsigned)m.nblk), dim3(MC_THREADS), 0, s, m);
-  hipLaunchKernelGGL(k_rows_chunk_sum, dim3(nch), dim3(128), 0, s, m);
+  hipLaunchKernelGGL(k_rows_chunk_sum, dim3(nch), dim3(RS_THREADS), 0, s, m);
   hipLaunchKernelGGL(k_rows_chunk_scan, dim3((unsigned)mc_rows(m.B)), dim3(1024), 0, s, m);
-  hipLaunchKernelGGL(k_rows_apply, dim3(nch), dim3(128), 0, s, m);
+  hipLaunchKernelGGL(k_rows_apply, dim3(nch), dim3(RS_THREADS), 0, s, m);
   DG_HIP(hipGetLastError());
   return DG_OK;
 }
