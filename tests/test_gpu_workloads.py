@@ -138,3 +138,34 @@ def test_workload_H65_cache_sweep(dg, orc):
         print(f"[H65] cache {pct}%", flush=True)
         run_and_check(dg, orc, w, oracle_batches=(0, w.cfg.B - 1) if pct == 0 else ())
         torch.cuda.empty_cache()
+
+
+def test_workload_M1_layered_full(dg, orc):
+    """Layer-wise frontiers at M1 scale, every batch against the oracle."""
+    w = synth.make_workload("M1", device=DEV)
+    fan = list(w.cfg.fanouts)
+    sr = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, layered=True,
+                         direct=True)
+    ref = orc.sample_group(w.offsets.cpu().numpy(), w.indices.cpu().numpy(),
+                           w.seeds.cpu().numpy(), fan, w.rng_seed, layered=True)
+    for b in range(w.cfg.B):
+        n, e = int(sr.hop_ptr[b, -1]), int(sr.edge_ptr[b, -1])
+        assert np.array_equal(sr.hop_ptr[b], ref["hop_ptr"][b]), b
+        assert np.array_equal(sr.edge_ptr[b], ref["edge_ptr"][b]), b
+        assert np.array_equal(sr.nodes[b, :n].cpu().numpy(), ref["nodes"][b]), b
+        assert np.array_equal(sr.edge_src[b, :e].cpu().numpy(), ref["edge_src"][b]), b
+        assert np.array_equal(sr.edge_dst[b, :e].cpu().numpy(), ref["edge_dst"][b]), b
+
+
+def test_workload_M1_relabelling_tables_agree(dg):
+    """The hash-table and direct-table relabelling give identical outputs."""
+    w = synth.make_workload("M1", device=DEV)
+    fan = list(w.cfg.fanouts)
+    a = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, direct=False)
+    b = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, direct=True)
+    assert np.array_equal(a.hop_ptr, b.hop_ptr) and np.array_equal(a.edge_ptr, b.edge_ptr)
+    for bb in range(w.cfg.B):
+        n, e = int(a.hop_ptr[bb, -1]), int(a.edge_ptr[bb, -1])
+        assert torch.equal(a.nodes[bb, :n], b.nodes[bb, :n])
+        assert torch.equal(a.edge_src[bb, :e], b.edge_src[bb, :e])
+        assert torch.equal(a.edge_dst[bb, :e], b.edge_dst[bb, :e])
