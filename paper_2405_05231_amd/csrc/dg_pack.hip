@@ -320,12 +320,15 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
   }
   const int e1 = tm.mark();
   // unique set, packed order, packed_ptr
-  int64_t totals[DG_MAX_BATCHES + 4];
+  int64_t totals[DG_MAX_BATCHES + 5];  // row totals, then the error word
   w.ms.mask = w.mask;
   w.ms.cache_slot = cache_slot;
+  w.ms.err_stage = w.ms.totals + mc_rows(B);  // staged by the count pass's row scan
   if ((rc = mask_scan_count(w.ms, s))) return rc;
-  DG_TRY(read_to_host(totals, w.ms.totals, sizeof(int64_t) * mc_rows(B), s));
-  if ((rc = read_err(w.err, s))) return rc;
+  DG_TRY(read_to_host(totals, w.ms.totals, sizeof(int64_t) * (mc_rows(B) + 1), s));
+  if (totals[mc_rows(B)])
+    return set_error(DG_EINVAL, "invalid input data: %s",
+                     describe_device_error((uint32_t)totals[mc_rows(B)]));
   int64_t rows = 0;
   packed_ptr_host[0] = 0;
   for (int b = 0; b < B; ++b) {

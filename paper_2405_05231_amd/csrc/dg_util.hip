@@ -187,7 +187,7 @@ void mask_scan_carve(MaskScan &m, Carve &c) {
   m.cw_off = c.take<uint16_t>((size_t)m.nblk * MC_BLOCK_NODES);
   m.base = c.take<int64_t>(rows * (size_t)m.nblk);
   m.chunk_sum = c.take<int64_t>(rows * (size_t)mc_chunks(m.nblk));
-  m.totals = c.take<int64_t>(rows);
+  m.totals = c.take<int64_t>(rows + 1);  // + a slot for the staged error word
 }
 
 // Tile loads: all MC_ROUNDS mask words (and the prev words and cached flags of
