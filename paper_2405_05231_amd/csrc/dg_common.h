@@ -233,25 +233,45 @@ int mask_scan_count(MaskScan &m, hipStream_t s);
 int mask_scan_write(const MaskScan &m, hipStream_t s);
 
 // ---------------------------------------------------------------- timing
+// Events are taken from a pool per host thread and device, created on first
+// use and reused by later calls (creating events inside a timed call would
+// delay its launches).  A call reads its times only after its final
+// synchronisation, and calls on one thread do not overlap, so reuse is safe.
+constexpr int TIMER_EVENTS = 24;
+constexpr int TIMER_DEVICES = 16;
+struct EventPool {
+  hipEvent_t ev[TIMER_EVENTS];
+  int made = 0;
+};
+inline EventPool *event_pool() {
+  static thread_local EventPool p[TIMER_DEVICES];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= TIMER_DEVICES) return nullptr;
+  return &p[dev];
+}
+
 struct PhaseTimer {
   bool on;
   hipStream_t s;
-  hipEvent_t ev[24];
+  EventPool *p = nullptr;
   int used = 0;
-  explicit PhaseTimer(bool enable, hipStream_t st) : on(enable), s(st) {}
-  ~PhaseTimer() {
-    for (int i = 0; i < used; ++i) (void)hipEventDestroy(ev[i]);
+  explicit PhaseTimer(bool enable, hipStream_t st) : on(enable), s(st) {
+    if (on) p = event_pool();
+    if (!p) on = false;
   }
   int mark() {  // returns the index of a new recorded event, or -1
-    if (!on || used >= 24) return -1;
-    if (hipEventCreate(&ev[used]) != hipSuccess) return -1;
-    (void)hipEventRecord(ev[used], s);
+    if (!on || used >= TIMER_EVENTS) return -1;
+    if (used >= p->made) {
+      if (hipEventCreate(&p->ev[p->made]) != hipSuccess) return -1;
+      ++p->made;
+    }
+    if (hipEventRecord(p->ev[used], s) != hipSuccess) return -1;
     return used++;
   }
   float ms(int a, int b) const {
-    if (a < 0 || b < 0) return 0.f;
+    if (!on || a < 0 || b < 0) return 0.f;
     float t = 0.f;
-    (void)hipEventElapsedTime(&t, ev[a], ev[b]);
+    (void)hipEventElapsedTime(&t, p->ev[a], p->ev[b]);
     return t;
   }
 };
