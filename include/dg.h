@@ -30,9 +30,11 @@
  *  - The caller owns every buffer.  The library never allocates device memory:
  *    scratch space is the caller's workspace `ws`, sized by the matching
  *    *_workspace_bytes() query and aligned to 256 bytes.  Workspace contents on
- *    entry are irrelevant; on return they are unspecified.  The only memory the
- *    library takes for itself is a 4 KB page-locked host buffer per calling
- *    thread (for reading counts back), held until the process ends.
+ *    entry are irrelevant; on return they are unspecified.  The only resources
+ *    the library takes for itself are a 4 KB page-locked host buffer per calling
+ *    thread (for reading counts back) and, per calling thread and device, a few
+ *    timing events and a second stream (default priority) on which
+ *    dg_pack_group runs part of its work; all are held until the process ends.
  *  - Work is enqueued on the caller's stream `stream` (NULL = the default
  *    stream).  dg_sample_group and dg_pack_group return only when their work has
  *    completed (their output sizes are data-dependent and are reported in
@@ -261,7 +263,10 @@ size_t dg_pack_workspace_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes
  *               lists have entries (DG_EINVAL otherwise); a mask that passes these
  *               checks and still differs from the lists gives unspecified packing
  *               outputs, never an access outside the given buffers.
- *   sizes, timing as for dg_sample_group.
+ *   sizes, timing as for dg_sample_group.  Without timing the address tables
+ *               are built on the library's second stream while the row copy
+ *               runs on `stream` (both done before the call returns); with
+ *               timing the phases run one after the other.
  * Errors: DG_EINVAL for null pointers, B outside 1..64, row_bytes < 1, n_b out of
  * range, and on the device a node ID outside [0,N), a node repeated within a
  * batch, or cache_slot[v] < -1.  DG_ECAPACITY when packed_cap < sum|P_b| or

@@ -153,6 +153,16 @@ inline int lt_bits_for(int64_t entries) {
 // shortens each round trip; otherwise the copy goes to dst directly.
 int read_to_host(void *dst, const void *src, size_t bytes, hipStream_t s);
 
+// ---------------------------------------------------------------- side stream
+// A second stream per host thread and device, for kernels a call runs beside
+// the caller's stream, with the events that fork from and join back to it.
+// Created on first use at default priority and held until the process ends.
+struct SideStream {
+  hipStream_t s;
+  hipEvent_t fork, join;
+};
+int side_stream(SideStream **out);
+
 // ---------------------------------------------------------------- fill / scan
 int fill_u64(uint64_t *p, size_t n, uint64_t value, hipStream_t s);
 

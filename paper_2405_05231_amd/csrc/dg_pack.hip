@@ -359,16 +359,29 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
   w.ms.pairdest = w.pairdest;
   if ((rc = mask_scan_write(w.ms, s))) return rc;
   const int e2 = tm.mark();
+  // The address tables (random reads) and the fan-out gather (HBM streaming)
+  // are independent.  Untimed calls run them side by side, the tables on a side
+  // stream joined back before the call returns; timed calls run them one after
+  // the other so that each phase has its own time.
+  SideStream *side = nullptr;
+  if (!timing && packed && total > 0) {
+    DG_TRY(side_stream(&side));
+    DG_HIP(hipEventRecord(side->fork, s));
+    DG_HIP(hipStreamWaitEvent(side->s, side->fork, 0));
+  }
   if (total > 0) {
-    hipLaunchKernelGGL(k_build_loc, dim3(blocks_for(total)), dim3(THREADS), 0, s, L, nodes,
-                       cache_slot, w.mask, w.nodeoff, w.pairdest, packed_ptr, loc, N, w.err);
+    hipLaunchKernelGGL(k_build_loc, dim3(blocks_for(total)), dim3(THREADS), 0,
+                       side ? side->s : s, L, nodes, cache_slot, w.mask, w.nodeoff, w.pairdest,
+                       packed_ptr, loc, N, w.err);
     DG_HIP(hipGetLastError());
   }
+  if (side) DG_HIP(hipEventRecord(side->join, side->s));
   const int e3 = tm.mark();
   if (packed &&  // packed == NULL: address tables only, no row copy
       (rc = launch_fanout(feats, w.unc_ids, w.unc_off, sizes->unique_packed, rows, w.pairdest,
                           row_bytes, packed, s)))
     return rc;
+  if (side) DG_HIP(hipStreamWaitEvent(s, side->join, 0));
   const int e4 = tm.mark();
   if ((rc = read_err(w.err, s))) return rc;
   if (timing) {

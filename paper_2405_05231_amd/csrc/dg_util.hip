@@ -54,6 +54,24 @@ int read_to_host(void *dst, const void *src, size_t bytes, hipStream_t s) {
   return DG_OK;
 }
 
+// ---------------------------------------------------------------- side stream
+int side_stream(SideStream **out) {
+  constexpr int MAX_DEV = 16;
+  static thread_local SideStream ss[MAX_DEV];
+  static thread_local bool made[MAX_DEV] = {};
+  int dev = 0;
+  DG_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= MAX_DEV) return set_error(DG_EHIP, "device index %d out of range", dev);
+  if (!made[dev]) {
+    DG_HIP(hipStreamCreateWithFlags(&ss[dev].s, hipStreamNonBlocking));
+    DG_HIP(hipEventCreateWithFlags(&ss[dev].fork, hipEventDisableTiming));
+    DG_HIP(hipEventCreateWithFlags(&ss[dev].join, hipEventDisableTiming));
+    made[dev] = true;
+  }
+  *out = &ss[dev];
+  return DG_OK;
+}
+
 // ---------------------------------------------------------------- fill
 __global__ void k_fill_u64(uint64_t *p, size_t n, uint64_t v) {
   size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
