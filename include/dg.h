@@ -298,6 +298,26 @@ int dg_assemble_batch(const void *cache, int64_t cache_rows, const void *packed_
                       int64_t row_bytes, void *out, int32_t *status,
                       hipStream_t stream);
 
+/* dg_assemble_batch for batches 0..B-1 of one packing result, in batch order on
+ * `stream`, issued by one call (the per-batch host cost is one kernel launch).
+ *   packed, packed_ptr_host [host] [B+1]  the packed chunks and their bounds as
+ *              dg_pack_group returned them (packed may be NULL if every chunk is
+ *              empty).
+ *   loc        [B*loc_stride] address tables; node_count [host] [B] the n_b.
+ *   outs       [host] [n_outs] output buffers; batch b goes to outs[b % n_outs],
+ *              each buffer at least max_b n_b * row_bytes bytes.  Batches that
+ *              share a buffer overwrite it in batch order.
+ * Asynchronous on `stream`.  Each batch is checked as dg_assemble_batch checks
+ * it; the call stops at the first batch that fails (batches before it are
+ * already enqueued) and returns that status.  Also DG_EINVAL for B < 0,
+ * n_outs < 1, a null outs/packed_ptr_host/node_count, n_b > loc_stride or
+ * chunk bounds that decrease. */
+int dg_assemble_batches(const void *cache, int64_t cache_rows, const void *packed,
+                        const int64_t *packed_ptr_host, const int32_t *loc,
+                        int64_t loc_stride, const int64_t *node_count, int32_t B,
+                        int64_t row_bytes, void *const *outs, int32_t n_outs,
+                        int32_t *status, hipStream_t stream);
+
 /* Workspace bytes dg_cache_by_frequency needs for N nodes. */
 size_t dg_cache_workspace_bytes(int64_t num_nodes);
 

@@ -272,45 +272,38 @@ def assemble_batch(cache: torch.Tensor | None, packed_b: torch.Tensor, loc_b: to
 
 def assemble_batches(cache: torch.Tensor | None, pr: PackResult, node_count, outs,
                      status: torch.Tensor | None = None, stream=None) -> None:
-    """dg_assemble_batch for every batch of a packing result, asynchronous:
-    batch b goes to outs[b % len(outs)] (uint8 [>= n_b, row_bytes] buffers, in
-    order on one stream).  Checks are done once, so the per-batch host cost is
-    one library call."""
+    """dg_assemble_batches: dg_assemble_batch for every batch of a packing
+    result, asynchronous, issued by one library call.  Batch b goes to
+    outs[b % len(outs)] (uint8 [>= n_b, row_bytes] buffers, in order on one
+    stream)."""
     R = pr.row_bytes
-    counts = [int(c) for c in np.asarray(node_count).reshape(-1)]
+    counts = np.ascontiguousarray(np.asarray(node_count, dtype=np.int64).reshape(-1))
     B = pr.loc.shape[0]
-    if len(counts) != B:
+    if counts.shape[0] != B:
         raise ValueError("node_count must have one entry per batch")
     _need(pr.loc, "loc", torch.int32)
     dev = pr.loc.device
-    stride = pr.loc.shape[1]
-    if max(counts, default=0) > stride:
-        raise ValueError("node_count exceeds the address-table stride")
+    if not len(outs):
+        raise ValueError("at least one output buffer is needed")
+    nmax = int(counts.max()) if B else 0
+    for o in outs:
+        _need(o, "out", None, dev)
+        if o.numel() * o.element_size() < nmax * R:
+            raise ValueError("an output buffer is too small")
     cache_rows = 0
-    cptr = None
     if cache is not None and cache.numel():
         _need(cache, "cache", None, dev)
         cache_rows = cache.numel() * cache.element_size() // R
-        cptr = cache.data_ptr()
-    for o in outs:
-        _need(o, "out", None, dev)
-        if o.numel() * o.element_size() < max(counts, default=0) * R:
-            raise ValueError("an output buffer is too small")
+    packed = None
     if pr.packed is not None and pr.packed.numel():
         _need(pr.packed, "packed", None, dev)
-    base = pr.packed.data_ptr() if pr.packed is not None and pr.packed.numel() else 0
-    ptr = [int(x) for x in pr.packed_ptr_host]
-    loc0 = pr.loc.data_ptr()
-    optr = [o.data_ptr() for o in outs]
-    st = status.data_ptr() if status is not None else None
-    sp = _stream(stream)
-    f = _L.dg_assemble_batch
-    for b, n in enumerate(counts):
-        rows = ptr[b + 1] - ptr[b]
-        rc = f(cptr, cache_rows, base + ptr[b] * R if rows else None, rows, loc0 + 4 * b * stride,
-               n, R, optr[b % len(optr)], st, sp)
-        if rc != DG_OK:
-            check(rc)
+        packed = pr.packed
+    ptr = np.ascontiguousarray(pr.packed_ptr_host, dtype=np.int64)
+    optr = (ctypes.c_void_p * len(outs))(*[o.data_ptr() for o in outs])
+    check(_L.dg_assemble_batches(_ptr(cache) if cache_rows else None, cache_rows, _ptr(packed),
+                                 ptr.ctypes.data_as(_lib.I64P), _ptr(pr.loc), pr.loc.shape[1],
+                                 counts.ctypes.data_as(_lib.I64P), B, R, optr, len(outs),
+                                 _ptr(status), _stream(stream)))
 
 
 def cache_by_frequency(membership: torch.Tensor, B: int, cache_rows: int,

@@ -63,6 +63,8 @@ SIGNATURES = {
                                      VP, VP, I64, VP, VP, SZ, VP, ctypes.POINTER(Sizes),
                                      ctypes.POINTER(Timing)]),
     "dg_assemble_batch": (ctypes.c_int, [VP, I64, VP, I64, VP, I64, I64, VP, VP, VP]),
+    "dg_assemble_batches": (ctypes.c_int, [VP, I64, VP, I64P, VP, I64, I64P, I32, I64,
+                                           ctypes.POINTER(VP), I32, VP, VP]),
     "dg_cache_workspace_bytes": (SZ, [I64]),
     "dg_cache_by_frequency": (ctypes.c_int, [VP, I64, I32, I64, VP, VP, I64P, VP, SZ, VP]),
     "dg_gather_rows": (ctypes.c_int, [VP, I64, I64, VP, I64, VP, VP, VP]),
@@ -85,7 +87,7 @@ def load():
         if not os.path.exists(LIB_PATH):
             raise ImportError(
                 f"libdg.so not found at {LIB_PATH}: build it first "
-                "(python -m paper_2405_05231_amd.build, or __graft_entry__.build())")
+                "(python paper_2405_05231_amd/build.py, or __graft_entry__.build())")
         L = ctypes.CDLL(LIB_PATH)
         for name, (res, args) in SIGNATURES.items():
             fn = getattr(L, name)

@@ -163,3 +163,26 @@ extern "C" int dg_assemble_batch(const void *cache, int64_t cache_rows, const vo
   if (w == 2) return launch_any<uint16_t>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, row_bytes, out, status, stream);
   return launch_any<uint8_t>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, row_bytes, out, status, stream);
 }
+
+extern "C" int dg_assemble_batches(const void *cache, int64_t cache_rows, const void *packed,
+                                   const int64_t *packed_ptr_host, const int32_t *loc,
+                                   int64_t loc_stride, const int64_t *node_count, int32_t B,
+                                   int64_t row_bytes, void *const *outs, int32_t n_outs,
+                                   int32_t *status, hipStream_t stream) {
+  if (B < 0 || n_outs < 1 || !outs || (B > 0 && (!packed_ptr_host || !node_count)) ||
+      row_bytes < 1 || loc_stride < 0)
+    return set_error(DG_EINVAL, "dg_assemble_batches: bad argument");
+  for (int32_t b = 0; b < B; ++b) {
+    const int64_t p0 = packed_ptr_host[b], p1 = packed_ptr_host[b + 1];
+    const int64_t n = node_count[b];
+    if (p0 < 0 || p1 < p0 || n < 0 || n > loc_stride)
+      return set_error(DG_EINVAL, "dg_assemble_batches: batch %d: bad chunk bounds or n_b", b);
+    const char *pb = (p1 > p0 && packed) ? static_cast<const char *>(packed) + p0 * row_bytes
+                                          : nullptr;
+    const int rc = dg_assemble_batch(cache, cache_rows, pb, p1 - p0,
+                                     loc ? loc + (int64_t)b * loc_stride : nullptr, n, row_bytes,
+                                     outs[b % n_outs], status, stream);
+    if (rc != DG_OK) return rc;
+  }
+  return DG_OK;
+}
