@@ -71,6 +71,9 @@ def main():
     ap.add_argument("--cpu-batches", type=int, default=0,
                     help="mini-batches in the CPU-oracle sample (0 = the whole group)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="issue each step's assembly calls directly instead of replaying "
+                         "them from a captured HIP graph")
     ap.add_argument("--copy-calib", action="store_true",
                     help="also run a plain copy of known size (counter calibration)")
     ap.add_argument("--groups", type=int, default=16,
@@ -164,6 +167,27 @@ def main():
         e_.record(s_asm)
     torch.cuda.synchronize()
 
+    # Each step's 64 assembly launches, captured once per packing output set into
+    # a HIP graph (kernel launches only) and replayed on s_asm: one host call
+    # per step instead of one launch per mini-batch.
+    asm_graph = None
+    if not args.no_graph:
+        s_cap = torch.cuda.Stream(device=dev)
+        s_cap.wait_stream(stream)
+        with torch.cuda.stream(s_cap):
+            for pr_ in pr2:
+                dg.assemble_batches(w.cache, pr_, counts, ybuf, stream=s_cap)
+        stream.wait_stream(s_cap)
+        torch.cuda.synchronize()
+        asm_graph = []
+        for pr_ in pr2:
+            g_ = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g_):
+                dg.assemble_batches(w.cache, pr_, counts, ybuf,
+                                    stream=torch.cuda.current_stream())
+            asm_graph.append(g_)
+        torch.cuda.synchronize()
+
     def run(K, pipelined, record):
         marks, gather_ms, asm_ms = [], [], []
         evs = []
@@ -183,7 +207,11 @@ def main():
             pack_done.record(stream)
             s_asm.wait_event(pack_done)
             e0.record(s_asm)
-            dg.assemble_batches(w.cache, p_out, counts, ybuf, stream=s_asm)
+            if asm_graph is not None:
+                with torch.cuda.stream(s_asm):
+                    asm_graph[slot].replay()
+            else:
+                dg.assemble_batches(w.cache, p_out, counts, ybuf, stream=s_asm)
             e1.record(s_asm)
             asm_done[slot].record(s_asm)
             t3 = time.perf_counter()
@@ -253,6 +281,7 @@ def main():
         "frac_hbm_peak": round(value / HBM_PEAK_GBPS, 4),
         "pipelined": "assembly of step k (second stream) overlaps sampling and packing of "
                      "step k+1; the serial figures below wait for each step's assembly",
+        "assembly_issue": "HIP graph replay" if asm_graph is not None else "direct calls",
         "serial": {"ms_per_step": round(ms_serial, 3),
                    "value": round(F * args.steps / t_serial / 1e9, 2)},
         "pipelined_phases_ms": {"sample": round(1e3 * float(np.mean([m[0] for m in marks_p])), 3),

@@ -306,3 +306,38 @@ def test_sparse_hops_on_a_large_graph(dg, orc, layered, direct):
     slot[cache_nodes] = torch.arange(ncache, dtype=torch.int32)
     check_all(dg, orc, off, idx, seeds, [3, 3, 2], 99, feats, slot, cache_nodes, batch_base=5,
               sample_kw={"layered": layered, "direct": direct})
+
+
+def test_assemble_batches_in_a_hip_graph(dg):
+    """dg_assemble_batches captured into a HIP graph (kernel launches only, no
+    memset) replays to the eager result, replay after replay, with eager work
+    in between."""
+    w = synth.make_workload("T")
+    X, slot = w.feats.to(DEV), w.cache_slot.to(DEV)
+    sr = dg.sample_group(w.offsets.to(DEV), w.indices.to(DEV), w.seeds.to(DEV),
+                         list(w.cfg.fanouts), w.rng_seed)
+    pr = dg.pack_group(X, slot, sr.nodes, sr.node_count)
+    cache = X.index_select(0, w.cache_nodes.to(DEV))
+    R = pr.row_bytes
+    counts = sr.node_count
+    nmax = int(counts.max())
+    ref = [torch.empty((nmax, R), dtype=torch.uint8, device=DEV) for _ in range(len(counts))]
+    dg.assemble_batches(cache, pr, counts, ref)
+    outs = [torch.empty((nmax, R), dtype=torch.uint8, device=DEV) for _ in range(len(counts))]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):  # warm up on the capture stream
+        dg.assemble_batches(cache, pr, counts, outs, stream=s)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        dg.assemble_batches(cache, pr, counts, outs, stream=torch.cuda.current_stream())
+    for rep in range(3):
+        for o in outs:
+            o.fill_(rep + 1)
+        dg.assemble_batch(cache, pr.chunk(0), pr.loc[0, :int(counts[0])], R)  # eager work
+        g.replay()
+        torch.cuda.synchronize()
+        for b, n in enumerate(counts):
+            assert torch.equal(outs[b][:int(n)], ref[b][:int(n)]), (rep, b)
