@@ -307,11 +307,12 @@ int dg_assemble_batch(const void *cache, int64_t cache_rows, const void *packed_
  *   outs       [host] [n_outs] output buffers; batch b goes to outs[b % n_outs],
  *              each buffer at least max_b n_b * row_bytes bytes.  Batches that
  *              share a buffer overwrite it in batch order.
- * Asynchronous on `stream`.  Each batch is checked as dg_assemble_batch checks
- * it; the call stops at the first batch that fails (batches before it are
- * already enqueued) and returns that status.  Also DG_EINVAL for B < 0,
- * n_outs < 1, a null outs/packed_ptr_host/node_count, n_b > loc_stride or
- * chunk bounds that decrease. */
+ * Asynchronous on `stream`.  DG_EINVAL, before anything is enqueued, for
+ * B < 0, n_outs < 1, row_bytes < 1, a null outs/packed_ptr_host/node_count, or
+ * any batch with n_b > loc_stride or chunk bounds that decrease.  Each batch is
+ * then checked as dg_assemble_batch checks it; the call stops at the first
+ * batch that fails (batches before it are already enqueued) and returns that
+ * status. */
 int dg_assemble_batches(const void *cache, int64_t cache_rows, const void *packed,
                         const int64_t *packed_ptr_host, const int32_t *loc,
                         int64_t loc_stride, const int64_t *node_count, int32_t B,

@@ -172,11 +172,15 @@ extern "C" int dg_assemble_batches(const void *cache, int64_t cache_rows, const 
   if (B < 0 || n_outs < 1 || !outs || (B > 0 && (!packed_ptr_host || !node_count)) ||
       row_bytes < 1 || loc_stride < 0)
     return set_error(DG_EINVAL, "dg_assemble_batches: bad argument");
-  for (int32_t b = 0; b < B; ++b) {
+  for (int32_t b = 0; b < B; ++b) {  // every batch is checked before any launch
     const int64_t p0 = packed_ptr_host[b], p1 = packed_ptr_host[b + 1];
     const int64_t n = node_count[b];
     if (p0 < 0 || p1 < p0 || n < 0 || n > loc_stride)
       return set_error(DG_EINVAL, "dg_assemble_batches: batch %d: bad chunk bounds or n_b", b);
+  }
+  for (int32_t b = 0; b < B; ++b) {
+    const int64_t p0 = packed_ptr_host[b], p1 = packed_ptr_host[b + 1];
+    const int64_t n = node_count[b];
     const char *pb = (p1 > p0 && packed) ? static_cast<const char *>(packed) + p0 * row_bytes
                                           : nullptr;
     const int rc = dg_assemble_batch(cache, cache_rows, pb, p1 - p0,

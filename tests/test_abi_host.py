@@ -118,3 +118,29 @@ def test_host_side_argument_errors(L):
     rc = L.dg_assemble_batch(buf, 100, ctypes.c_void_p(0x900000), 10, ctypes.c_void_p(0xF00000), 4,
                              16, ctypes.c_void_p(0x100010), None, None)
     assert rc == _lib.DG_EINVAL and b"overlap" in L.dg_last_error()
+
+
+def test_assemble_batches_host_checks(L):
+    from paper_2405_05231_amd import _lib
+    ptr = (ctypes.c_int64 * 3)(0, 2, 5)
+    cnt = (ctypes.c_int64 * 2)(3, 4)
+    outs = (ctypes.c_void_p * 1)(0x100000)
+    fake = ctypes.c_void_p(0x200000)
+    # B = 0: nothing to do
+    assert L.dg_assemble_batches(None, 0, None, ptr, None, 0, cnt, 0, 16, outs, 1, None,
+                                 None) == _lib.DG_OK
+    # no output buffer, bad row size, negative B
+    assert L.dg_assemble_batches(None, 0, fake, ptr, fake, 8, cnt, 2, 16, outs, 0, None,
+                                 None) == _lib.DG_EINVAL
+    assert L.dg_assemble_batches(None, 0, fake, ptr, fake, 8, cnt, 2, 0, outs, 1, None,
+                                 None) == _lib.DG_EINVAL
+    assert L.dg_assemble_batches(None, 0, fake, ptr, fake, 8, cnt, -1, 16, outs, 1, None,
+                                 None) == _lib.DG_EINVAL
+    # n_b beyond the address-table stride (batch 1), decreasing chunk bounds:
+    # rejected before any batch is enqueued
+    assert L.dg_assemble_batches(None, 0, fake, ptr, fake, 3, cnt, 2, 16, outs, 1, None,
+                                 None) == _lib.DG_EINVAL
+    bad = (ctypes.c_int64 * 3)(0, 4, 2)
+    rc = L.dg_assemble_batches(None, 0, fake, bad, fake, 8, cnt, 2, 16, outs, 1, None, None)
+    assert rc == _lib.DG_EINVAL and b"bounds" in L.dg_last_error()
+
