@@ -71,6 +71,12 @@ def main():
     ap.add_argument("--cpu-batches", type=int, default=0,
                     help="mini-batches in the CPU-oracle sample (0 = the whole group)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-pipeline", action="store_true",
+                    help="time the serial region only (value = the serial rate)")
+    ap.add_argument("--timed-pack", action="store_true",
+                    help="request per-phase timing from every packing call (its phases then "
+                         "run one after the other, so a kernel trace sees the fan-out gather "
+                         "alone in every call)")
     ap.add_argument("--no-graph", action="store_true",
                     help="issue each step's assembly calls directly instead of replaying "
                          "them from a captured HIP graph")
@@ -136,8 +142,8 @@ def main():
     counts = sr.node_count.copy()
     # two packing outputs, so that packing step k+1 never overwrites what
     # assembly step k is still reading
-    pr2 = [dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, membership=mem)
-           for _ in range(2)]
+    pr2 = [dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, membership=mem,
+                         timing=args.timed_pack) for _ in range(2)]
     pr = pr2[0]
     ws_p = torch.empty(dg._L.dg_pack_workspace_bytes(cfg.n, B, int(counts.sum())),
                        dtype=torch.uint8, device=dev)
@@ -200,7 +206,8 @@ def main():
             t1 = time.perf_counter()
             stream.wait_event(asm_done[slot])  # the assembly that last read pr2[slot]
             p_out = dg.pack_group(w.feats, w.cache_slot, s_out.nodes, counts, out=pr2[slot],
-                                  workspace=ws_p, timing=record, membership=mem,
+                                  workspace=ws_p, timing=record or args.timed_pack,
+                                  membership=mem,
                                   stream=stream)
             t2 = time.perf_counter()
             e0, e1 = ev_pool[k]
@@ -240,7 +247,10 @@ def main():
 
     # timed regions: K whole steps serially, then K whole steps pipelined
     t_serial, marks, gather_ms, asm_ms, _, _ = timed(False)
-    t_total, marks_p, _, asm_ms_p, _, _ = timed(True)
+    if args.no_pipeline:
+        t_total, marks_p, asm_ms_p = t_serial, marks, asm_ms
+    else:
+        t_total, marks_p, _, asm_ms_p, _, _ = timed(True)
     samp_ms = [1e3 * m[0] for m in marks]
     pack_ms = [1e3 * m[1] for m in marks]
 
@@ -279,8 +289,9 @@ def main():
                    "row_bytes": R, "batches": B, "seeds_per_batch": cfg.S, "fanouts": fan,
                    "cache_rows": int(w.cache_nodes.numel()), "parallelism": "single-gpu"},
         "frac_hbm_peak": round(value / HBM_PEAK_GBPS, 4),
-        "pipelined": "assembly of step k (second stream) overlaps sampling and packing of "
-                     "step k+1; the serial figures below wait for each step's assembly",
+        "pipelined": ("no: --no-pipeline, value is the serial rate" if args.no_pipeline else
+                      "assembly of step k (second stream) overlaps sampling and packing of "
+                      "step k+1; the serial figures below wait for each step's assembly"),
         "assembly_issue": "HIP graph replay" if asm_graph is not None else "direct calls",
         "serial": {"ms_per_step": round(ms_serial, 3),
                    "value": round(F * args.steps / t_serial / 1e9, 2)},
