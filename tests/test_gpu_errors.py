@@ -25,36 +25,41 @@ def tiny():
     return w
 
 
-def test_duplicate_seed_rejected(dg, tiny):
+@pytest.mark.parametrize("direct", [False, True])
+def test_duplicate_seed_rejected(dg, tiny, direct):
     seeds = tiny.seeds.clone()
     seeds[1, 5] = seeds[1, 9]
     with pytest.raises(dg.DGError) as e:
-        dg.sample_group(tiny.offsets.to(DEV), tiny.indices.to(DEV), seeds.to(DEV), [5, 5], 1)
+        dg.sample_group(tiny.offsets.to(DEV), tiny.indices.to(DEV), seeds.to(DEV), [5, 5], 1, direct=direct)
     assert e.value.status == -1 and "twice" in str(e.value)
 
 
-def test_seed_out_of_range_rejected(dg, tiny):
+@pytest.mark.parametrize("direct", [False, True])
+def test_seed_out_of_range_rejected(dg, tiny, direct):
     seeds = tiny.seeds.clone()
     seeds[0, 0] = tiny.cfg.n + 3
     with pytest.raises(dg.DGError) as e:
-        dg.sample_group(tiny.offsets.to(DEV), tiny.indices.to(DEV), seeds.to(DEV), [5, 5], 1)
+        dg.sample_group(tiny.offsets.to(DEV), tiny.indices.to(DEV), seeds.to(DEV), [5, 5], 1, direct=direct)
     assert e.value.status == -1 and "outside" in str(e.value)
 
 
-def test_bad_neighbour_id_rejected(dg, tiny):
+@pytest.mark.parametrize("direct", [False, True])
+def test_bad_neighbour_id_rejected(dg, tiny, direct):
     idx = tiny.indices.clone()
     idx[::7] = -5
     with pytest.raises(dg.DGError) as e:
-        dg.sample_group(tiny.offsets.to(DEV), idx.to(DEV), tiny.seeds.to(DEV), [5, 5], 1)
+        dg.sample_group(tiny.offsets.to(DEV), idx.to(DEV), tiny.seeds.to(DEV), [5, 5], 1,
+                        direct=direct)
     assert e.value.status == -1 and "neighbour" in str(e.value)
 
 
-def test_bad_offsets_rejected(dg, tiny):
+@pytest.mark.parametrize("direct", [False, True])
+def test_bad_offsets_rejected(dg, tiny, direct):
     off = tiny.offsets.clone()
     off[100:200] = 10 ** 9  # beyond num_edges
     seeds = torch.arange(100, 164, dtype=torch.int32).reshape(1, 64)
     with pytest.raises(dg.DGError) as e:
-        dg.sample_group(off.to(DEV), tiny.indices.to(DEV), seeds.to(DEV), [5, 5], 1)
+        dg.sample_group(off.to(DEV), tiny.indices.to(DEV), seeds.to(DEV), [5, 5], 1, direct=direct)
     assert e.value.status == -1 and "CSR" in str(e.value)
 
 
@@ -144,3 +149,27 @@ def test_assemble_bad_address_flags_and_zeroes(dg):
     assert torch.equal(out[0], cache[0]) and torch.equal(out[1], packed[0])
     assert torch.equal(out[4], packed[2])
     assert int(out[2].sum()) == 0 and int(out[3].sum()) == 0
+
+
+def test_assemble_batches_bad_address_flags(dg):
+    """The group call checks addresses like the per-batch call: an entry outside
+    its table is flagged and its row zeroed; the other batches are untouched."""
+    R = 64
+    cache = torch.arange(4 * R, dtype=torch.int32, device=DEV).to(torch.uint8).view(4, R)
+    packed = torch.full((5, R), 9, dtype=torch.uint8, device=DEV)
+    packed[3:] = 7
+    loc = torch.tensor([[-1, 0, 7], [1, -2, 0]], dtype=torch.int32, device=DEV)  # 7: beyond chunk 0
+    pr = dg.PackResult(packed=packed, packed_ids=torch.zeros(5, dtype=torch.int32, device=DEV),
+                       packed_ptr=torch.tensor([0, 3, 5], dtype=torch.int64, device=DEV),
+                       packed_ptr_host=np.array([0, 3, 5], dtype=np.int64), loc=loc,
+                       unique=None, sizes={}, timing=None, row_bytes=R)
+    outs = [torch.full((3, R), 0xCD, dtype=torch.uint8, device=DEV) for _ in range(2)]
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    dg.assemble_batches(cache, pr, [3, 3], outs, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 1
+    assert torch.equal(outs[0][0], cache[0]) and torch.equal(outs[0][1], packed[0])
+    assert int(outs[0][2].sum()) == 0
+    assert torch.equal(outs[1][0], packed[4]) and torch.equal(outs[1][1], cache[1])
+    assert torch.equal(outs[1][2], packed[3])
+
