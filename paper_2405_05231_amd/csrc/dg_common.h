@@ -183,9 +183,15 @@ constexpr int MC_ROUNDS = 16;
 constexpr int MC_TILE = 64 * MC_ROUNDS;
 constexpr int MC_BLOCK_NODES = MC_TILE * MC_WAVES;
 constexpr int MC_CHUNK = 64;  // blocks per chunk of the row scan
+// Touched marks: one byte per 2^MC_TOUCH_SHIFT consecutive nodes (one 64-byte
+// line of the mask).
+constexpr int MC_TOUCH_SHIFT = 3;
 
 __host__ __device__ inline int64_t mc_blocks(int64_t N) { return (N + MC_BLOCK_NODES - 1) / MC_BLOCK_NODES; }
 __host__ __device__ inline int64_t mc_chunks(int64_t nblk) { return (nblk + MC_CHUNK - 1) / MC_CHUNK; }
+__host__ __device__ inline int64_t mc_touch_bytes(int64_t N) {
+  return mc_blocks(N) * (MC_BLOCK_NODES >> MC_TOUCH_SHIFT);
+}
 
 // Count-matrix rows: [0,B) per batch (non-cached members), then:
 __host__ __device__ inline int row_all(int B) { return B; }        // nodes with any bit set (U)
@@ -225,8 +231,9 @@ struct MaskScan {
                                      // see mask & ~prev, and the count pass adds
                                      // the new bits to prev
   bool keep_prev;                    // false: leave prev as it is (nothing reads it later)
-  const uint8_t *touched;            // nullable: a byte per 64-node round; rounds
-                                     // whose byte is 0 hold no bit to list (not read)
+  const uint8_t *touched;            // nullable: a byte per 2^MC_TOUCH_SHIFT nodes
+                                     // (mc_touch_bytes(N) in all); nodes whose byte
+                                     // is 0 hold no bit to list (not read)
   // The write pass runs in one of two modes: packing (pairdest set: seg_out,
   // unc_ids, unc_off, nodeoff required, uniq_out optional, cached nodes left out
   // of the lists) or sampling (pairdest NULL: prev and seg_out required,

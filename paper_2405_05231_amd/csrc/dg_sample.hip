@@ -5,8 +5,8 @@
 // mini-batch b) and its copy prev[u] as of the start of the current hop.  A
 // hop is: degree pass over the frontier -> exclusive scan (edge slots) -> draw
 // + mark (a fire-and-forget atomicOr on visited per sampled edge; a hop that
-// can reach only a small share of the nodes also marks the 64-node rounds it
-// touches) -> compaction of visited & ~prev (the nodes new at this hop) into
+// can reach only a small share of the nodes also marks the 8-node lines of the
+// mask it touches) -> compaction of visited & ~prev (the nodes new at this hop) into
 // each batch's new segment, ascending, with no sort; the compaction also brings
 // prev up to date -> one read-back of the hop's counts.  Sampled neighbours are
 // relabelled from global to local IDs at the end, through one of two tables:
@@ -40,8 +40,8 @@ struct Hop {
   int64_t fpos[DG_MAX_BATCHES];        // local position of b's first frontier node
   int64_t ebase[DG_MAX_BATCHES];       // edges of b before this hop
   uint64_t bstate[DG_MAX_BATCHES];     // mix64(rng_seed + gamma*(g+1)) per batch
-  uint8_t *touched;                    // nullable: byte per 64-node round, set for
-                                       // every round that gains a membership bit
+  uint8_t *touched;                    // nullable: a byte per 2^MC_TOUCH_SHIFT nodes, set
+                                       // for every node that gains a membership bit
 };
 
 // Flattened (batch, position) ranges, for passes over all edge lists, with
@@ -120,7 +120,7 @@ __device__ __forceinline__ void emit_chunk(const int32_t (&u)[EMIT], const int64
     if (k >= cnt) continue;
     if (u[k] >= 0 && (int64_t)u[k] < N) {
       atomicOr((unsigned long long *)&visited[u[k]], bit);
-      if (touched) touched[u[k] >> 6] = 1;
+      if (touched) touched[u[k] >> MC_TOUCH_SHIFT] = 1;
     } else {
       atomicOr(err, ERR_NBR_RANGE);
     }
@@ -308,7 +308,7 @@ struct SampleWs {
   int64_t *f_off, *f_deg, *f_cnt, *f_eoff, *tiles;
   LocalTable table;  // hash relabelling
   int32_t *local;    // direct relabelling: [N][B]
-  uint8_t *touched;  // a byte per 64-node round (sparse hops)
+  uint8_t *touched;  // touched marks (a byte per 2^MC_TOUCH_SHIFT nodes)
   int64_t *small;    // staging for a few counts
   MaskScan ms;
 };
@@ -326,7 +326,7 @@ void carve_sample(SampleWs &w, Carve &c, int64_t N, int B, int64_t node_cap, boo
   w.table.bits = direct ? 0 : lt_bits_for(fmax);
   w.table.slots = direct ? nullptr : c.take<uint64_t>((size_t)1 << w.table.bits);
   w.local = direct ? c.take<int32_t>((size_t)N * (size_t)B) : nullptr;
-  w.touched = c.take<uint8_t>((size_t)mc_blocks(N) * (MC_BLOCK_NODES / 64));
+  w.touched = c.take<uint8_t>((size_t)mc_touch_bytes(N));
   w.small = c.take<int64_t>(ST_SIZE);
   w.ms = MaskScan{};
   w.ms.N = N;
@@ -479,12 +479,13 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       for (int b = 0; b < B; ++b) new_b[b] = 0;
     } else {
       const int ev0 = tm.mark();
-      // A hop whose edges can reach only a small share of the nodes marks the
-      // 64-node rounds it touches, and its count pass skips the others.
+      // A hop whose edges can reach at most N/16 nodes marks the mask lines it
+      // touches (a byte store per edge), and its count pass reads only those.
+      // On larger hops the stores cost more time than the lines they spare.
       const int64_t ebound = f < 0 ? E : h.ftot * (int64_t)f;
-      h.touched = ebound <= N / 32 ? w.touched : nullptr;
+      h.touched = ebound <= N / 16 ? w.touched : nullptr;
       if (h.touched && (rc = fill_u64(reinterpret_cast<uint64_t *>(w.touched),
-                                      (size_t)mc_blocks(N) * (MC_BLOCK_NODES / 64) / 8, 0, s)))
+                                      (size_t)mc_touch_bytes(N) / 8, 0, s)))
         return rc;
       hipLaunchKernelGGL(k_frontier_degree, dim3(blocks_for(h.ftot)), dim3(THREADS), 0, s, h,
                          nodes, node_cap, g->offsets, N, E, w.f_off, w.f_deg, w.f_cnt, w.err);

@@ -208,125 +208,178 @@ void mask_scan_carve(MaskScan &m, Carve &c) {
   m.totals = c.take<int64_t>(rows + 1);  // + a slot for the staged error word
 }
 
-// Tile loads: all MC_ROUNDS mask words (and the prev words and cached flags of
-// non-empty ones) are requested before any is used, so a wave keeps 16 loads in
-// flight.
-struct TileBits {
-  uint64_t m[MC_ROUNDS];
-  uint32_t cached;  // bit r: node of round r is cached
-};
+// Count pass.  One wave per tile of MC_TILE nodes, MC_ROUNDS rounds of 64.
+// What is the same across the wave is kept in scalar registers: the tile base,
+// the rounds that may hold a word, and for each round the lanes whose word is
+// non-empty and the lanes whose node is cached; a round without a word costs a
+// scalar branch only.  With touched marks a lane reads its mask word only if
+// the word's 8-node line is marked.  All of a tile's mask words (then its
+// prev words, then its cache slots) are requested before any is used, so a
+// wave keeps up to 16 loads in flight.
+//
+// Per-batch counts: the tile's listed non-cached words are copied into LDS, a
+// chunk of MC_CROUNDS rounds at a time, low and high halves in separate
+// arrays.  Lane b then reads the halves holding bit b of four words with one
+// 128-bit load (lanes 0-31 the low halves, 32-63 the high ones) and adds bit
+// b mod 32 of each, so the cost per word is about 1.5 vector instructions.
+//
+// SAMPLE: sampling mode (prev required, no cache slots): the listed words are
+// mask & ~prev, and with keep_prev the new bits are added to prev at once.
+// Otherwise packing mode (no prev; cache_slot nullable).
+constexpr int MC_CROUNDS = 4;
+constexpr int MC_CWORDS = 64 * MC_CROUNDS + 4;  // + zero padding for the last read
 
-// With update_prev, prev takes the listed bits as soon as they are known
-// (prev |= the new bits; the word is owned by this lane), so no second load is
-// needed later.
-__device__ __forceinline__ void load_tile(const MaskScan &a, int64_t t0, int lane, TileBits &t,
-                                          bool check_slots, bool update_prev) {
-  uint32_t live = 0xffffu;  // bit r: round r may hold bits to list
-  if (a.touched) {
-    const uint8_t *f = a.touched + (t0 >> 6);
-    live = 0;
-#pragma unroll
-    for (int r = 0; r < MC_ROUNDS; ++r) live |= (f[r] ? 1u : 0u) << r;
-  }
-#pragma unroll
-  for (int r = 0; r < MC_ROUNDS; ++r) {
-    int64_t u = t0 + r * 64 + lane;
-    t.m[r] = (u < a.N && ((live >> r) & 1u)) ? a.mask[u] : 0ull;
-  }
-  if (a.B < 64) {  // bits of batches outside the group are ignored
-    const uint64_t keep = (1ull << a.B) - 1ull;
-#pragma unroll
-    for (int r = 0; r < MC_ROUNDS; ++r) t.m[r] &= keep;
-  }
-  if (a.prev) {
-    uint64_t p[MC_ROUNDS];
-#pragma unroll
-    for (int r = 0; r < MC_ROUNDS; ++r) p[r] = t.m[r] ? a.prev[t0 + r * 64 + lane] : 0ull;
-#pragma unroll
-    for (int r = 0; r < MC_ROUNDS; ++r) {
-      t.m[r] &= ~p[r];
-      if (update_prev && t.m[r] != 0ull) a.prev[t0 + r * 64 + lane] = p[r] | t.m[r];
-    }
-  }
-  t.cached = 0;
-  if (a.cache_slot) {
-    int32_t sl[MC_ROUNDS];
-#pragma unroll
-    for (int r = 0; r < MC_ROUNDS; ++r)
-      sl[r] = t.m[r] ? a.cache_slot[t0 + r * 64 + lane] : -1;
-#pragma unroll
-    for (int r = 0; r < MC_ROUNDS; ++r) {
-      if (check_slots && sl[r] < -1) atomicOr(a.err, ERR_CACHE_SLOT);
-      t.cached |= (sl[r] >= 0 ? 1u : 0u) << r;
-    }
-  }
+__device__ __forceinline__ uint32_t rank_below(uint64_t set, uint32_t base) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(set >> 32),
+                                   __builtin_amdgcn_mbcnt_lo((uint32_t)set, base));
 }
 
-// Per-wave counts of one tile: lane b returns batch b's non-cached members;
-// *cu, *cnc, *cp, *call (wave-uniform) get the members of U, of U_nc, U_nc's
-// pairs and all pairs.  Per-batch counts walk the tile's non-empty words one at
-// a time: the word is read out of its lane (v_readlane), and lane b tests bit b,
-// so the work follows the words present rather than the batches they touch.
-__device__ __forceinline__ uint32_t tile_counts(const TileBits &t, int lane, uint32_t *cu,
-                                                uint32_t *cnc, uint32_t *cp, uint32_t *call) {
-  uint32_t mine = 0, u = 0, nc = 0;
-  int32_t pl = 0, al = 0;  // this lane's pair counts (U_nc pairs, all pairs)
-#pragma unroll
-  for (int r = 0; r < MC_ROUNDS; ++r) {
-    const uint64_t m = t.m[r];
-    const uint64_t any = __ballot(m != 0ull);
-    if (any == 0ull) continue;  // wave-uniform
-    const uint64_t mnc = ((t.cached >> r) & 1u) ? 0ull : m;
-    al += __popcll(m);
-    pl += __popcll(mnc);
-    u += (uint32_t)__popcll(any);
-    uint64_t anc = __ballot(mnc != 0ull);
-    nc += (uint32_t)__popcll(anc);
-    while (anc) {
-      const int l = __ffsll((long long)anc) - 1;
-      anc &= anc - 1;
-      const uint64_t w = (uint64_t)read_lane((int64_t)mnc, l);
-      mine += (uint32_t)((w >> lane) & 1ull);
-    }
-  }
-  *cu = u;
-  *cnc = nc;
-  *cp = (uint32_t)__ockl_wfred_add_i32(pl);
-  *call = (uint32_t)__ockl_wfred_add_i32(al);
-  return mine;
-}
+// Waits until every vector memory load and store of the wave has completed
+// (s_waitcnt vmcnt(0) in the gfx9 encoding; the other counters are left
+// alone).  Placed after each branchy load phase, it tells the compiler's wait
+// insertion that no load is outstanding, so no wait is placed after the stores
+// that follow (a wait there would also wait for those stores).
+__device__ __forceinline__ void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
-// Count pass: per block, the number of members of every batch (non-cached
-// only), of U, of U_nc, and of U_nc's (node, batch) pairs; stored as one
-// contiguous row per block, plus each wave's exclusive prefix within the block
-// (so the write pass does not count again).
+template <bool SAMPLE>
 __global__ __launch_bounds__(MC_THREADS) void k_mask_count(MaskScan a) {
   __shared__ uint32_t s_cnt[MC_WAVES][DG_MAX_BATCHES + 4];
-  const int lane = lane_id(), w = threadIdx.x >> 6;
+  __shared__ __align__(16) uint32_t s_w[MC_WAVES][2][MC_CWORDS];
+  const int lane = lane_id();
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int B = a.B, rows = mc_rows(B);
   const int64_t t0 = (int64_t)blockIdx.x * MC_BLOCK_NODES + (int64_t)w * MC_TILE;
-  TileBits t;
-  load_tile(a, t0, lane, t, true, a.keep_prev);
-  uint32_t cu, cnc, cp, call;
-  uint32_t mine = tile_counts(t, lane, &cu, &cnc, &cp, &call);
-  // the tile's non-empty words, in node order, for the write pass
-  {
-    const size_t gw = ((size_t)blockIdx.x * MC_WAVES + w) * MC_TILE;
-    const uint64_t lt = lanes_below();
-    uint32_t run = 0;
+  const int64_t rem = a.N - t0;  // nodes of the tile inside [0, N) (may exceed MC_TILE)
+
+  // Touched marks: byte i of the tile's covers nodes t0 + 8i .. t0 + 8i + 7, so
+  // round r's marks are the 8 bytes at 8r, and lane l's is byte l/8 of them.
+  uint32_t live = 0xffffu;   // bit r: round r may hold a word (uniform)
+  uint32_t lmask = 0xffffu;  // bit r: this lane's node of round r may hold one
+  if (a.touched) {
+    const uint64_t *f = reinterpret_cast<const uint64_t *>(a.touched + (t0 >> MC_TOUCH_SHIFT));
+    const uint32_t sh = 8u * ((uint32_t)lane >> 3);
+    uint32_t l = 0, lm = 0;
 #pragma unroll
     for (int r = 0; r < MC_ROUNDS; ++r) {
-      const uint64_t any = __ballot(t.m[r] != 0ull);
-      if (any == 0ull) continue;
-      if (t.m[r] != 0ull) {
-        const size_t at = gw + run + (uint32_t)__popcll(any & lt);
-        a.cw_mask[at] = t.m[r];
-        a.cw_off[at] = (uint16_t)((r * 64 + lane) | ((int)((t.cached >> r) & 1u) << 15));
-      }
-      run += (uint32_t)__popcll(any);
+      const uint64_t x = f[r];
+      l |= (x != 0ull ? 1u : 0u) << r;
+      lm |= (((x >> sh) & 0xffull) != 0ull ? 1u : 0u) << r;
     }
-    if (lane == 0) a.wcnt[(size_t)blockIdx.x * MC_WAVES + w] = run;
+    live = __builtin_amdgcn_readfirstlane(l);
+    lmask = lm;
   }
+
+  uint64_t m[MC_ROUNDS];
+  {
+    const uint64_t *mk = a.mask + t0;
+    if (rem >= MC_TILE) {
+#pragma unroll
+      for (int r = 0; r < MC_ROUNDS; ++r)
+        m[r] = (((live >> r) & 1u) && ((lmask >> r) & 1u)) ? mk[r * 64 + lane] : 0ull;
+    } else {
+#pragma unroll
+      for (int r = 0; r < MC_ROUNDS; ++r)
+        m[r] = (((live >> r) & 1u) && ((lmask >> r) & 1u) && r * 64 + lane < rem)
+                   ? mk[r * 64 + lane]
+                   : 0ull;
+    }
+  }
+  wait_vm_all();
+  if (B < 64) {  // bits of batches outside the group are ignored
+    const uint64_t keep = (1ull << B) - 1ull;
+#pragma unroll
+    for (int r = 0; r < MC_ROUNDS; ++r) m[r] &= keep;
+  }
+  uint64_t any[MC_ROUNDS];  // lanes of round r with a word to list (uniform)
+#pragma unroll
+  for (int r = 0; r < MC_ROUNDS; ++r) any[r] = ((live >> r) & 1u) ? __ballot(m[r] != 0ull) : 0ull;
+
+  uint64_t cmask[MC_ROUNDS];  // lanes of round r whose node is cached (uniform)
+#pragma unroll
+  for (int r = 0; r < MC_ROUNDS; ++r) cmask[r] = 0ull;
+  if (SAMPLE) {
+    uint64_t *pv = a.prev + t0;
+    uint64_t p[MC_ROUNDS];
+#pragma unroll
+    for (int r = 0; r < MC_ROUNDS; ++r) p[r] = (any[r] && m[r] != 0ull) ? pv[r * 64 + lane] : 0ull;
+    wait_vm_all();
+#pragma unroll
+    for (int r = 0; r < MC_ROUNDS; ++r) {
+      if (!any[r]) continue;
+      const uint64_t nw = m[r] & ~p[r];
+      if (a.keep_prev && nw != 0ull) pv[r * 64 + lane] = p[r] | nw;
+      m[r] = nw;
+      any[r] = __ballot(nw != 0ull);
+    }
+  } else if (a.cache_slot) {
+    const int32_t *cs = a.cache_slot + t0;
+    int32_t sl[MC_ROUNDS];
+#pragma unroll
+    for (int r = 0; r < MC_ROUNDS; ++r) sl[r] = (any[r] && m[r] != 0ull) ? cs[r * 64 + lane] : -1;
+    wait_vm_all();
+    uint64_t bad = 0;
+#pragma unroll
+    for (int r = 0; r < MC_ROUNDS; ++r) {
+      if (!any[r]) continue;
+      bad |= __ballot(sl[r] < -1);
+      cmask[r] = __ballot(sl[r] >= 0);
+    }
+    if (bad && lane == 0) atomicOr(a.err, ERR_CACHE_SLOT);
+  }
+
+  // List the non-empty words (global, for the write pass) and count.
+  const size_t gw = ((size_t)blockIdx.x * MC_WAVES + w) * MC_TILE;
+  uint32_t *lo_w = s_w[w][0], *hi_w = s_w[w][1];
+  const uint4 *src4 = reinterpret_cast<const uint4 *>(lane < 32 ? lo_w : hi_w);
+  const uint32_t sh = (uint32_t)lane & 31u;
+  uint32_t run = 0, cu = 0, cnc = 0;  // uniform
+  uint32_t al = 0, pl = 0, mine = 0;  // this lane's pairs (all, non-cached), batch `lane`
+#pragma unroll
+  for (int c = 0; c < MC_ROUNDS; c += MC_CROUNDS) {
+    uint32_t k = 0;  // non-cached words of the chunk (uniform)
+#pragma unroll
+    for (int r = c; r < c + MC_CROUNDS; ++r) {
+      const uint64_t an = any[r];
+      if (!an) continue;
+      const uint64_t anc = an & ~cmask[r];
+      const uint32_t pc = (uint32_t)__popcll(m[r]);
+      al += pc;
+      if (m[r] != 0ull) {
+        const bool cached = (cmask[r] >> lane) & 1ull;
+        const size_t at = gw + rank_below(an, run);
+        a.cw_mask[at] = m[r];
+        a.cw_off[at] = (uint16_t)((r * 64 + lane) | ((int)cached << 15));
+        if (!cached) {
+          pl += pc;
+          const uint32_t j = rank_below(anc, k);
+          lo_w[j] = (uint32_t)m[r];
+          hi_w[j] = (uint32_t)(m[r] >> 32);
+        }
+      }
+      run += (uint32_t)__popcll(an);
+      cu += (uint32_t)__popcll(an);
+      cnc += (uint32_t)__popcll(anc);
+      k += (uint32_t)__popcll(anc);
+    }
+    if (k == 0) continue;
+    if (lane < 4) {  // zeros after the last word: the final 128-bit read may pass it
+      lo_w[k + lane] = 0u;
+      hi_w[k + lane] = 0u;
+    }
+    // LDS operations of one wave complete in order, so these reads see the
+    // stores above and the next chunk's stores follow them.
+    __builtin_amdgcn_wave_barrier();
+    for (uint32_t i = 0; i < k; i += 4) {
+      const uint4 v = src4[i >> 2];
+      mine += __builtin_amdgcn_ubfe(v.x, sh, 1) + __builtin_amdgcn_ubfe(v.y, sh, 1);
+      mine += __builtin_amdgcn_ubfe(v.z, sh, 1) + __builtin_amdgcn_ubfe(v.w, sh, 1);
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+  if (lane == 0) a.wcnt[(size_t)blockIdx.x * MC_WAVES + w] = run;
+  const uint32_t call = (uint32_t)__ockl_wfred_add_i32((int32_t)al);
+  const uint32_t cp = SAMPLE ? call : (uint32_t)__ockl_wfred_add_i32((int32_t)pl);
+
   if (lane < B) s_cnt[w][lane] = mine;
   if (lane == 0) {
     s_cnt[w][row_all(B)] = cu;
@@ -413,8 +466,13 @@ __global__ __launch_bounds__(RS_THREADS) void k_rows_apply(MaskScan a) {
 
 int mask_scan_count(MaskScan &m, hipStream_t s) {
   if (m.nblk == 0) return fill_u64(reinterpret_cast<uint64_t *>(m.totals), mc_rows(m.B), 0, s);
+  if (m.prev && m.cache_slot)
+    return set_error(DG_EINVAL, "internal: compaction with both prev and cache slots");
   const unsigned nch = (unsigned)mc_chunks(m.nblk);
-  hipLaunchKernelGGL(k_mask_count, dim3((unsigned)m.nblk), dim3(MC_THREADS), 0, s, m);
+  if (m.prev)
+    hipLaunchKernelGGL(k_mask_count<true>, dim3((unsigned)m.nblk), dim3(MC_THREADS), 0, s, m);
+  else
+    hipLaunchKernelGGL(k_mask_count<false>, dim3((unsigned)m.nblk), dim3(MC_THREADS), 0, s, m);
   hipLaunchKernelGGL(k_rows_chunk_sum, dim3(nch), dim3(RS_THREADS), 0, s, m);
   hipLaunchKernelGGL(k_rows_chunk_scan, dim3((unsigned)mc_rows(m.B)), dim3(1024), 0, s, m);
   hipLaunchKernelGGL(k_rows_apply, dim3(nch), dim3(RS_THREADS), 0, s, m);
