@@ -77,6 +77,9 @@ def main():
                     help="request per-phase timing from every packing call (its phases then "
                          "run one after the other, so a kernel trace sees the fan-out gather "
                          "alone in every call)")
+    ap.add_argument("--fill-masks", action="store_true",
+                    help="clear the membership mask and the sampler's state with full fills "
+                         "in every sampling call, instead of the clearing flags (comparison)")
     ap.add_argument("--no-graph", action="store_true",
                     help="issue each step's assembly calls directly instead of replaying "
                          "them from a captured HIP graph")
@@ -194,6 +197,14 @@ def main():
             asm_graph.append(g_)
         torch.cuda.synchronize()
 
+    # Mask state across steps: each sampling call leaves its workspace state
+    # clear (DG_SAMPLE_EXIT_CLEAR) and each packing call clears the membership
+    # mask as it reads it (DG_PACK_CLEAR_MEMBERSHIP), so from the second step on
+    # sampling is told both are clear (DG_SAMPLE_ENTRY_CLEAR) and skips its two
+    # full-mask fills.  The first call on ws_s starts from unknown contents.
+    clearing = not args.fill_masks
+    state = {"clear": False}
+
     def run(K, pipelined, record):
         marks, gather_ms, asm_ms = [], [], []
         evs = []
@@ -201,14 +212,18 @@ def main():
         for k in range(K):
             slot = k & 1
             t0 = time.perf_counter()
+            entry_clear = clearing and state["clear"]
+            state["clear"] = False
             s_out = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, out=sr,
-                                    workspace=ws_s, membership=mem, direct=True, stream=stream)
+                                    workspace=ws_s, membership=mem, direct=True, stream=stream,
+                                    exit_clear=clearing, entry_clear=entry_clear)
             t1 = time.perf_counter()
             stream.wait_event(asm_done[slot])  # the assembly that last read pr2[slot]
             p_out = dg.pack_group(w.feats, w.cache_slot, s_out.nodes, counts, out=pr2[slot],
                                   workspace=ws_p, timing=record or args.timed_pack,
-                                  membership=mem,
+                                  membership=mem, clear_membership=clearing,
                                   stream=stream)
+            state["clear"] = clearing
             t2 = time.perf_counter()
             e0, e1 = ev_pool[k]
             pack_done.record(stream)
@@ -293,6 +308,9 @@ def main():
                       "assembly of step k (second stream) overlaps sampling and packing of "
                       "step k+1; the serial figures below wait for each step's assembly"),
         "assembly_issue": "HIP graph replay" if asm_graph is not None else "direct calls",
+        "mask_clearing": ("clearing flags: packing clears the membership words it reads and "
+                          "sampling leaves its state clear, so no full-mask fill runs per step"
+                          if clearing else "two full-mask fills in every sampling call"),
         "serial": {"ms_per_step": round(ms_serial, 3),
                    "value": round(F * args.steps / t_serial / 1e9, 2)},
         "pipelined_phases_ms": {"sample": round(1e3 * float(np.mean([m[0] for m in marks_p])), 3),

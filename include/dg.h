@@ -30,7 +30,8 @@
  *  - The caller owns every buffer.  The library never allocates device memory:
  *    scratch space is the caller's workspace `ws`, sized by the matching
  *    *_workspace_bytes() query and aligned to 256 bytes.  Workspace contents on
- *    entry are irrelevant; on return they are unspecified.  The only resources
+ *    entry are irrelevant and on return unspecified, except where the flags
+ *    DG_SAMPLE_ENTRY_CLEAR / DG_SAMPLE_EXIT_CLEAR say otherwise.  The only resources
  *    the library takes for itself are a 4 KB page-locked host buffer per calling
  *    thread (for reading counts back) and, per calling thread and device, a few
  *    timing events and a second stream (default priority) on which
@@ -119,6 +120,23 @@ extern "C" {
                                 int32 table of local indices (4*N*B workspace bytes)
                                 instead of a hash table sized for the group; same
                                 results, fewer device-wide atomics */
+/* The two flags below let a loop that samples and packs group after group skip
+ * clearing two N-word masks per group (2 x 8*N bytes of writes).  Outputs are
+ * the same with or without them. */
+#define DG_SAMPLE_EXIT_CLEAR 4u   /* on DG_OK, leave the workspace's sampling state
+                                     clear (costs a few writes of the last hop) */
+#define DG_SAMPLE_ENTRY_CLEAR 8u  /* the caller asserts that `membership` (required)
+                                     is all-zero and that the workspace was last used
+                                     by a call with DG_SAMPLE_EXIT_CLEAR that returned
+                                     DG_OK for the same num_nodes; the call then does
+                                     not clear them.  If the assertion is false the
+                                     outputs are unspecified (the call still never
+                                     accesses memory outside the given buffers). */
+
+/* dg_pack_group flags */
+#define DG_PACK_CLEAR_MEMBERSHIP 1u /* on DG_OK, `membership` (required) is left
+                                       all-zero: the call clears each word as it
+                                       reads it */
 
 typedef enum dg_status {
   DG_OK = 0,
@@ -209,6 +227,11 @@ size_t dg_sample_workspace_bytes(int64_t num_nodes, int32_t B, int64_t node_cap,
  *              blocks do (the first hop_ptr[k] nodes are the destinations of
  *              hop k+1).  DG_SAMPLE_DIRECT: the relabelling table is a direct
  *              [N][B] array (outputs are identical either way).
+ *              DG_SAMPLE_EXIT_CLEAR, DG_SAMPLE_ENTRY_CLEAR: see their definitions.
+ *              A loop passes EXIT_CLEAR on every call and ENTRY_CLEAR from its
+ *              second call on, after a dg_pack_group with
+ *              DG_PACK_CLEAR_MEMBERSHIP has cleared the membership words; after
+ *              any non-OK return it starts again without ENTRY_CLEAR.
  * Outputs (row b of each starts at b*cap):
  *   nodes      [B*node_cap] int32: nodes_b in the order above.
  *   hop_ptr    [host] [B*(K+2)] int64: hop_ptr[b*(K+2)+h] = start of hop h in
@@ -224,7 +247,8 @@ size_t dg_sample_workspace_bytes(int64_t num_nodes, int32_t B, int64_t node_cap,
  *   timing     [host] optional (NULL = not measured).
  * node_cap must be below 2^27.
  * Errors: DG_EINVAL for null pointers, B outside 1..64, S < 1, K < 0, caps < S,
- * and for bad data found on the device: a seed outside [0,N), a seed repeated in
+ * unknown flags or DG_SAMPLE_ENTRY_CLEAR without membership, and for bad data
+ * found on the device: a seed outside [0,N), a seed repeated in
  * a batch, a CSR row with offsets outside [0,E] or decreasing, a neighbour ID
  * outside [0,N).  Bad data never causes an access outside the given arrays. */
 int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S,
@@ -258,6 +282,8 @@ size_t dg_pack_workspace_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes
  *   membership  optional [N] uint64 input (NULL = built here from the lists):
  *               bit b of membership[u] set iff u is in batch b's list, as
  *               dg_sample_group returns it; bits of batches >= B are ignored.
+ *               Read only, unless flags holds DG_PACK_CLEAR_MEMBERSHIP.
+ *   flags       0 or DG_PACK_CLEAR_MEMBERSHIP.
  *               The call checks that the bit of every non-cached list entry is
  *               set and that the mask holds as many (node, batch) pairs as the
  *               lists have entries (DG_EINVAL otherwise); a mask that passes these
@@ -268,15 +294,16 @@ size_t dg_pack_workspace_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes
  *               runs on `stream` (both done before the call returns); with
  *               timing the phases run one after the other.
  * Errors: DG_EINVAL for null pointers, B outside 1..64, row_bytes < 1, n_b out of
- * range, and on the device a node ID outside [0,N), a node repeated within a
- * batch, or cache_slot[v] < -1.  DG_ECAPACITY when packed_cap < sum|P_b| or
+ * range, unknown flags (or DG_PACK_CLEAR_MEMBERSHIP without membership), and on
+ * the device a node ID outside [0,N), a node repeated within a batch, or
+ * cache_slot[v] < -1.  DG_ECAPACITY when packed_cap < sum|P_b| or
  * (group_unique != NULL and) unique_cap < |U|. */
 int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
                   const int32_t *cache_slot, int32_t B, const int32_t *nodes,
                   int64_t node_stride, const int64_t *node_count, int64_t packed_cap,
                   void *packed, int32_t *packed_ids, int64_t *packed_ptr,
                   int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique,
-                  int64_t unique_cap, const uint64_t *membership, void *ws,
+                  int64_t unique_cap, uint64_t *membership, uint32_t flags, void *ws,
                   size_t ws_bytes, hipStream_t stream, dg_sizes *sizes,
                   dg_timing *timing);
 

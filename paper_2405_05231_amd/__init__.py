@@ -90,9 +90,12 @@ class SampleResult:
         return self.edge_src[b, :e], self.edge_dst[b, :e]
 
 
-def sample_flags(layered: bool = False, direct: bool = False) -> int:
+def sample_flags(layered: bool = False, direct: bool = False, entry_clear: bool = False,
+                 exit_clear: bool = False) -> int:
     """dg_sample_group flag word."""
-    return (_lib.DG_SAMPLE_LAYERED if layered else 0) | (_lib.DG_SAMPLE_DIRECT if direct else 0)
+    return ((_lib.DG_SAMPLE_LAYERED if layered else 0) | (_lib.DG_SAMPLE_DIRECT if direct else 0)
+            | (_lib.DG_SAMPLE_ENTRY_CLEAR if entry_clear else 0)
+            | (_lib.DG_SAMPLE_EXIT_CLEAR if exit_clear else 0))
 
 
 def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tensor, fanouts,
@@ -100,12 +103,16 @@ def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tens
                  edge_cap: int | None = None, out: SampleResult | None = None,
                  workspace: torch.Tensor | None = None, stream=None, timing: bool = False,
                  membership: torch.Tensor | None = None, layered: bool = False,
-                 direct: bool = False) -> SampleResult:
+                 direct: bool = False, entry_clear: bool = False,
+                 exit_clear: bool = False) -> SampleResult:
     """Group sampling (dg_sample_group).  seeds: int32 [B, S] on the GPU.
     membership: optional int64 [N] tensor that receives the (node, batch)
     membership mask (bit b of word u = u is in batch b).  layered: every node
     of the mini-batch so far samples at each hop (DGL-style layer blocks).
-    direct: relabel through a direct [N][B] table (4*N*B workspace bytes)."""
+    direct: relabel through a direct [N][B] table (4*N*B workspace bytes).
+    exit_clear / entry_clear: DG_SAMPLE_EXIT_CLEAR / DG_SAMPLE_ENTRY_CLEAR (a
+    loop over groups that reuses `workspace` and `membership`, packing each
+    group with clear_membership=True, skips two mask clears per group)."""
     dev = offsets.device
     _need(offsets, "offsets", torch.int64)
     _need(indices, "indices", torch.int32, dev)
@@ -133,7 +140,7 @@ def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tens
             edge_src=torch.empty((B, max(edge_cap, 1)), dtype=torch.int32, device=dev),
             edge_dst=torch.empty((B, max(edge_cap, 1)), dtype=torch.int32, device=dev),
             edge_ptr=np.zeros((B, K + 1), dtype=np.int64), sizes={}, timing=None)
-    flags = sample_flags(layered, direct)
+    flags = sample_flags(layered, direct, entry_clear, exit_clear)
     ws_bytes = _L.dg_sample_workspace_bytes(N, B, node_cap, edge_cap, flags)
     ws = _workspace(ws_bytes, dev, workspace)
     g = Csr(N, E, offsets.data_ptr(), indices.data_ptr())
@@ -175,12 +182,14 @@ def _row_bytes(feats: torch.Tensor) -> int:
 def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tensor, node_count,
                with_unique: bool = False, out: PackResult | None = None,
                workspace: torch.Tensor | None = None, stream=None, timing: bool = False,
-               membership: torch.Tensor | None = None, tables_only: bool = False
-               ) -> PackResult:
+               membership: torch.Tensor | None = None, tables_only: bool = False,
+               clear_membership: bool = False) -> PackResult:
     """Batched packing (dg_pack_group).  nodes: int32 [B, node_stride];
     node_count: the B list lengths (host).  membership: optional int64 [N]
     mask from sample_group (skips rebuilding it).  tables_only: build the
-    packed order and address tables without copying rows (packed = None)."""
+    packed order and address tables without copying rows (packed = None).
+    clear_membership: DG_PACK_CLEAR_MEMBERSHIP (membership is all-zero after
+    the call)."""
     dev = feats.device
     _need(feats, "feats", None)
     _need(cache_slot, "cache_slot", torch.int32, dev)
@@ -215,7 +224,7 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
         st = _L.dg_pack_group(_ptr(feats), N, R, _ptr(cache_slot), B, _ptr(nodes), stride,
                               counts.ctypes.data_as(_lib.I64P), 0, None, None, _ptr(ptr),
                               ptr_host.ctypes.data_as(_lib.I64P), _ptr(loc), None, 0,
-                              _ptr(membership), _ptr(ws), ws.numel(), _stream(stream),
+                              _ptr(membership), 0, _ptr(ws), ws.numel(), _stream(stream),
                               ctypes.byref(sz), None)
         if st not in (DG_OK, DG_ECAPACITY):
             check(st)
@@ -234,7 +243,9 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
                           _ptr(out.packed_ids), _ptr(out.packed_ptr),
                           out.packed_ptr_host.ctypes.data_as(_lib.I64P), _ptr(out.loc),
                           _ptr(out.unique), out.unique.numel() if out.unique is not None else 0,
-                          _ptr(membership), _ptr(ws), ws.numel(), _stream(stream),
+                          _ptr(membership),
+                          _lib.DG_PACK_CLEAR_MEMBERSHIP if clear_membership else 0,
+                          _ptr(ws), ws.numel(), _stream(stream),
                           ctypes.byref(sz),
                           ctypes.byref(tm) if timing else None)
     out.sizes = sz.as_dict()

@@ -231,6 +231,8 @@ struct MaskScan {
                                      // see mask & ~prev, and the count pass adds
                                      // the new bits to prev
   bool keep_prev;                    // false: leave prev as it is (nothing reads it later)
+  bool clear_prev;                   // (without keep_prev) zero each non-zero prev word read
+  bool clear_mask;                   // zero each non-zero mask word read (packing mode)
   const uint8_t *touched;            // nullable: a byte per 2^MC_TOUCH_SHIFT nodes
                                      // (mc_touch_bytes(N) in all); nodes whose byte
                                      // is 0 hold no bit to list (not read)

@@ -56,12 +56,18 @@ __global__ void k_packed_ptr(const int64_t *totals, int B, int64_t *packed_ptr) 
   }
 }
 
-// loc_b[j] = -(slot+1) for a cached node, else its rank in P_b.
+// loc_b[j] = -(slot+1) for a cached node, else its rank in P_b.  A non-cached
+// node's pairs start at nodeoff[u], one per batch that holds it, in batch
+// order, each naming its packed row; the entry takes the first pair whose row
+// lies in chunk b and checks that the row is u's (packed_ids).  An entry whose
+// node has no such pair (a given membership mask that misses it) is reported,
+// so no unchecked address reaches the table.  The mask itself is not read
+// here: the count pass may have cleared it already.
 __global__ __launch_bounds__(THREADS) void k_build_loc(Lists L, const int32_t *nodes,
                                                        const int32_t *cache_slot,
-                                                       const uint64_t *mask,
                                                        const int64_t *nodeoff,
-                                                       const int64_t *pairdest,
+                                                       const int64_t *pairdest, int64_t n_pairs,
+                                                       const int32_t *packed_ids,
                                                        const int64_t *packed_ptr, int32_t *loc,
                                                        int64_t N, uint32_t *err) {
   const int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
@@ -78,11 +84,22 @@ __global__ __launch_bounds__(THREADS) void k_build_loc(Lists L, const int32_t *n
   if (sl >= 0) {
     out = -(sl + 1);
   } else {
-    const uint64_t m = mask[u];
-    if (!((m >> b) & 1ull))  // only a given (external) mask can miss an entry
-      atomicOr(err, ERR_MEMBERSHIP);
-    else
-      out = (int32_t)(pairdest[nodeoff[u] + __popcll(m & ((1ull << b) - 1ull))] - packed_ptr[b]);
+    bool found = false;
+    int64_t p = nodeoff[u];  // meaningful only for nodes of U_nc; checked below
+    if (packed_ids && p >= 0 && p < n_pairs) {
+      const int64_t lo = packed_ptr[b], hi = packed_ptr[b + 1];
+      const int64_t pend = n_pairs - p > DG_MAX_BATCHES ? p + DG_MAX_BATCHES : n_pairs;
+      for (; p < pend; ++p) {
+        const int64_t d = pairdest[p];
+        if (d < lo) continue;  // a pair of an earlier batch
+        if (d < hi && packed_ids[d] == u) {
+          out = (int32_t)(d - lo);
+          found = true;
+        }
+        break;
+      }
+    }
+    if (!found) atomicOr(err, ERR_MEMBERSHIP);
   }
   loc[at] = out;
 }
@@ -265,8 +282,8 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
                              int64_t node_stride, const int64_t *node_count, int64_t packed_cap,
                              void *packed, int32_t *packed_ids, int64_t *packed_ptr,
                              int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique,
-                             int64_t unique_cap, const uint64_t *membership, void *ws,
-                             size_t ws_bytes, hipStream_t stream, dg_sizes *sizes,
+                             int64_t unique_cap, uint64_t *membership, uint32_t flags,
+                             void *ws, size_t ws_bytes, hipStream_t stream, dg_sizes *sizes,
                              dg_timing *timing) {
   if (!feats || !cache_slot || !nodes || !node_count || !packed_ptr || !packed_ptr_host ||
       !loc || !sizes)
@@ -275,6 +292,11 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
       node_stride < 0 || packed_cap < 0 || unique_cap < 0)
     return set_error(DG_EINVAL, "dg_pack_group: bad sizes (N=%lld row_bytes=%lld B=%d)",
                      (long long)N, (long long)row_bytes, B);
+  if (flags & ~DG_PACK_CLEAR_MEMBERSHIP)
+    return set_error(DG_EINVAL, "dg_pack_group: unknown flags 0x%x", flags);
+  const bool clear_membership = flags & DG_PACK_CLEAR_MEMBERSHIP;
+  if (clear_membership && !membership)
+    return set_error(DG_EINVAL, "dg_pack_group: DG_PACK_CLEAR_MEMBERSHIP needs membership");
   Lists L;
   L.B = B;
   L.stride = node_stride;
@@ -309,7 +331,7 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
   const int e0 = tm.mark();
   if ((rc = fill_u64(reinterpret_cast<uint64_t *>(w.err), 16, 0, s))) return rc;
   if (membership) {
-    w.mask = const_cast<uint64_t *>(membership);  // read only below
+    w.mask = membership;  // written only with DG_PACK_CLEAR_MEMBERSHIP
   } else {
     if ((rc = fill_u64(w.mask, (size_t)N, 0, s))) return rc;
     if (total > 0) {
@@ -322,6 +344,7 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
   // unique set, packed order, packed_ptr
   int64_t totals[DG_MAX_BATCHES + 5];  // row totals, then the error word
   w.ms.mask = w.mask;
+  w.ms.clear_mask = clear_membership;
   w.ms.cache_slot = cache_slot;
   w.ms.err_stage = w.ms.totals + mc_rows(B);  // staged by the count pass's row scan
   if ((rc = mask_scan_count(w.ms, s))) return rc;
@@ -371,8 +394,8 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
   }
   if (total > 0) {
     hipLaunchKernelGGL(k_build_loc, dim3(blocks_for(total)), dim3(THREADS), 0,
-                       side ? side->s : s, L, nodes, cache_slot, w.mask, w.nodeoff, w.pairdest,
-                       packed_ptr, loc, N, w.err);
+                       side ? side->s : s, L, nodes, cache_slot, w.nodeoff, w.pairdest, rows,
+                       packed_ids, packed_ptr, loc, N, w.err);
     DG_HIP(hipGetLastError());
   }
   if (side) DG_HIP(hipEventRecord(side->join, side->s));

@@ -302,6 +302,9 @@ __global__ void k_batch_bounds(Hop h, const int64_t *f_eoff, int64_t *out) {
 
 inline unsigned blocks_for(int64_t n) { return (unsigned)((n + THREADS - 1) / THREADS); }
 
+constexpr uint32_t SAMPLE_FLAGS =
+    DG_SAMPLE_LAYERED | DG_SAMPLE_DIRECT | DG_SAMPLE_EXIT_CLEAR | DG_SAMPLE_ENTRY_CLEAR;
+
 struct SampleWs {
   uint32_t *err;
   uint64_t *visited, *prev;
@@ -380,8 +383,7 @@ extern "C" int dg_sample_bounds(int64_t num_nodes, int64_t num_edges, int32_t S,
 extern "C" size_t dg_sample_workspace_bytes(int64_t num_nodes, int32_t B, int64_t node_cap,
                                             int64_t edge_cap, uint32_t flags) {
   (void)edge_cap;
-  if (num_nodes < 1 || B < 1 || B > DG_MAX_BATCHES || node_cap < 1 ||
-      (flags & ~(DG_SAMPLE_LAYERED | DG_SAMPLE_DIRECT)))
+  if (num_nodes < 1 || B < 1 || B > DG_MAX_BATCHES || node_cap < 1 || (flags & ~SAMPLE_FLAGS))
     return 0;
   Carve c(nullptr);
   SampleWs w;
@@ -403,10 +405,14 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
   if (!g->offsets || (g->num_edges > 0 && !g->indices) || g->num_nodes < 1 ||
       g->num_nodes > 0x7fffffffll || g->num_edges < 0)
     return set_error(DG_EINVAL, "dg_sample_group: bad CSR description");
-  if (flags & ~(DG_SAMPLE_LAYERED | DG_SAMPLE_DIRECT))
+  if (flags & ~SAMPLE_FLAGS)
     return set_error(DG_EINVAL, "dg_sample_group: unknown flags 0x%x", flags);
   const bool layered = flags & DG_SAMPLE_LAYERED;
   const bool direct = flags & DG_SAMPLE_DIRECT;
+  const bool entry_clear = flags & DG_SAMPLE_ENTRY_CLEAR;
+  const bool exit_clear = flags & DG_SAMPLE_EXIT_CLEAR;
+  if (entry_clear && !membership)
+    return set_error(DG_EINVAL, "dg_sample_group: DG_SAMPLE_ENTRY_CLEAR needs membership");
   if (B < 1 || B > DG_MAX_BATCHES || S < 1 || K < 0 || node_cap < S || edge_cap < 0 ||
       (int64_t)S > g->num_nodes)
     return set_error(DG_EINVAL, "dg_sample_group: bad sizes (B=%d S=%d K=%d node_cap=%lld)", B,
@@ -438,8 +444,13 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
   int rc;
   if ((rc = fill_u64(reinterpret_cast<uint64_t *>(w.err), 32, 0, s))) return rc;
   if (membership) w.visited = membership;
-  if ((rc = fill_u64(w.visited, (size_t)N, 0, s))) return rc;
-  if ((rc = fill_u64(w.prev, (size_t)N, 0, s))) return rc;
+  // prev (workspace) and visited must start all-zero: cleared here unless the
+  // caller asserts that they already are (see DG_SAMPLE_ENTRY_CLEAR)
+  if (!entry_clear) {
+    if ((rc = fill_u64(w.visited, (size_t)N, 0, s))) return rc;
+    if ((rc = fill_u64(w.prev, (size_t)N, 0, s))) return rc;
+  }
+  bool prev_cleared = false;  // the last hop's count pass zeroed prev
   hipLaunchKernelGGL(k_seed_init, dim3(blocks_for((int64_t)B * S)), dim3(THREADS), 0, s, seeds,
                      B, S, N, node_cap, nodes, w.visited, w.prev, w.local, w.err);
   DG_HIP(hipGetLastError());  // bad seeds are reported at the first hop's round trip
@@ -506,6 +517,11 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       w.ms.prev = w.prev;
       w.ms.keep_prev = k < K;  // after the last hop nothing reads prev
       w.ms.touched = h.touched;
+      // With DG_SAMPLE_EXIT_CLEAR the last hop's count pass zeroes every prev
+      // word it reads; that is all non-zero ones (prev is a subset of visited)
+      // unless touched marks leave some lines unread.
+      w.ms.clear_prev = exit_clear && k == K && !h.touched;
+      prev_cleared = w.ms.clear_prev;
       w.ms.cache_slot = nullptr;
       w.ms.totals = w.small + ST_TOTALS;
       w.ms.err_stage = w.small + ST_ERR;
@@ -603,6 +619,7 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
     DG_HIP(hipGetLastError());
   }
   const int ev_r1 = tm.mark();
+  if (exit_clear && !prev_cleared && (rc = fill_u64(w.prev, (size_t)N, 0, s))) return rc;
   if ((rc = check_err(w.err, s))) return rc;
 
   int64_t tn = 0, te = 0, mn = 0, me = 0;

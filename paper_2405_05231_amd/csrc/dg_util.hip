@@ -224,8 +224,10 @@ void mask_scan_carve(MaskScan &m, Carve &c) {
 // b mod 32 of each, so the cost per word is about 1.5 vector instructions.
 //
 // SAMPLE: sampling mode (prev required, no cache slots): the listed words are
-// mask & ~prev, and with keep_prev the new bits are added to prev at once.
-// Otherwise packing mode (no prev; cache_slot nullable).
+// mask & ~prev, and with keep_prev the new bits are added to prev at once
+// (with clear_prev the prev words read are zeroed instead).  Otherwise packing
+// mode (no prev; cache_slot nullable; with clear_mask each non-zero mask word
+// is zeroed once read).
 constexpr int MC_CROUNDS = 4;
 constexpr int MC_CWORDS = 64 * MC_CROUNDS + 4;  // + zero padding for the last read
 
@@ -285,6 +287,12 @@ __global__ __launch_bounds__(MC_THREADS) void k_mask_count(MaskScan a) {
     }
   }
   wait_vm_all();
+  if (!SAMPLE && a.clear_mask) {
+    uint64_t *mk = a.mask + t0;
+#pragma unroll
+    for (int r = 0; r < MC_ROUNDS; ++r)
+      if (m[r] != 0ull) mk[r * 64 + lane] = 0ull;
+  }
   if (B < 64) {  // bits of batches outside the group are ignored
     const uint64_t keep = (1ull << B) - 1ull;
 #pragma unroll
@@ -308,6 +316,7 @@ __global__ __launch_bounds__(MC_THREADS) void k_mask_count(MaskScan a) {
       if (!any[r]) continue;
       const uint64_t nw = m[r] & ~p[r];
       if (a.keep_prev && nw != 0ull) pv[r * 64 + lane] = p[r] | nw;
+      if (a.clear_prev && p[r] != 0ull) pv[r * 64 + lane] = 0ull;
       m[r] = nw;
       any[r] = __ballot(nw != 0ull);
     }
@@ -466,8 +475,9 @@ __global__ __launch_bounds__(RS_THREADS) void k_rows_apply(MaskScan a) {
 
 int mask_scan_count(MaskScan &m, hipStream_t s) {
   if (m.nblk == 0) return fill_u64(reinterpret_cast<uint64_t *>(m.totals), mc_rows(m.B), 0, s);
-  if (m.prev && m.cache_slot)
-    return set_error(DG_EINVAL, "internal: compaction with both prev and cache slots");
+  if ((m.prev && (m.cache_slot || m.clear_mask)) || (m.keep_prev && m.clear_prev) ||
+      (!m.prev && (m.keep_prev || m.clear_prev)))
+    return set_error(DG_EINVAL, "internal: inconsistent count-pass mode");
   const unsigned nch = (unsigned)mc_chunks(m.nblk);
   if (m.prev)
     hipLaunchKernelGGL(k_mask_count<true>, dim3((unsigned)m.nblk), dim3(MC_THREADS), 0, s, m);

@@ -65,7 +65,10 @@ def test_workspace_queries(L):
     b = L.dg_sample_workspace_bytes(20_000, 4, 2000, 2000, 0)
     assert 0 < a < b and a % 256 == 0
     assert L.dg_sample_workspace_bytes(10_000, 65, 2000, 2000, 0) == 0
-    assert L.dg_sample_workspace_bytes(10_000, 4, 2000, 2000, 8) == 0  # unknown flag
+    assert L.dg_sample_workspace_bytes(10_000, 4, 2000, 2000, 16) == 0  # unknown flag
+    # the clear flags do not change the workspace size
+    assert L.dg_sample_workspace_bytes(10_000, 4, 2000, 2000, 2 | 4 | 8) == \
+        L.dg_sample_workspace_bytes(10_000, 4, 2000, 2000, 2)
     # the direct relabelling table replaces the hash table: 4*N*B bytes
     d = L.dg_sample_workspace_bytes(10_000_000, 64, 2000, 2000, 2)
     h = L.dg_sample_workspace_bytes(10_000_000, 64, 2000, 2000, 0)
@@ -99,18 +102,32 @@ def test_host_side_argument_errors(L):
                            fake, ep, None, None, 0, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EWORKSPACE
     # unknown flags
-    rc = L.dg_sample_group(ctypes.byref(g), fake, 1, 1, 0, fo, 1, 0, 8, 4, fake, hop, 4, fake,
+    rc = L.dg_sample_group(ctypes.byref(g), fake, 1, 1, 0, fo, 1, 0, 16, 4, fake, hop, 4, fake,
                            fake, ep, None, fake, 1 << 20, None, ctypes.byref(sizes), None)
-    assert rc == _lib.DG_EINVAL
+    assert rc == _lib.DG_EINVAL and b"flags" in L.dg_last_error()
+    # DG_SAMPLE_ENTRY_CLEAR asserts something about `membership`, so it needs one
+    rc = L.dg_sample_group(ctypes.byref(g), fake, 1, 1, 0, fo, 1, 0,
+                           _lib.DG_SAMPLE_ENTRY_CLEAR, 4, fake, hop, 4, fake,
+                           fake, ep, None, fake, 1 << 20, None, ctypes.byref(sizes), None)
+    assert rc == _lib.DG_EINVAL and b"membership" in L.dg_last_error()
     # pack: B = 0, row_bytes = 0, counts beyond the stride
     cnt = (ctypes.c_int64 * 2)(3, 9)
     ph = (ctypes.c_int64 * 3)()
     rc = L.dg_pack_group(fake, 10, 0, fake, 2, fake, 8, cnt, 0, None, None, fake, ph, fake, None,
-                         0, None, fake, 1 << 20, None, ctypes.byref(sizes), None)
+                         0, None, 0, fake, 1 << 20, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL
     rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, cnt, 0, None, None, fake, ph, fake, None,
-                         0, None, fake, 1 << 20, None, ctypes.byref(sizes), None)
+                         0, None, 0, fake, 1 << 20, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL and b"node_count" in L.dg_last_error()
+    # pack flags: unknown bits, and a clear request without a membership mask
+    ok_cnt = (ctypes.c_int64 * 2)(3, 5)
+    rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, ok_cnt, 0, None, None, fake, ph, fake,
+                         None, 0, fake, 2, fake, 1 << 20, None, ctypes.byref(sizes), None)
+    assert rc == _lib.DG_EINVAL and b"flags" in L.dg_last_error()
+    rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, ok_cnt, 0, None, None, fake, ph, fake,
+                         None, 0, None, _lib.DG_PACK_CLEAR_MEMBERSHIP, fake, 1 << 20, None,
+                         ctypes.byref(sizes), None)
+    assert rc == _lib.DG_EINVAL and b"membership" in L.dg_last_error()
     # assemble: n_b = 0 is a no-op; negative sizes and overlap are rejected
     assert L.dg_assemble_batch(None, 0, None, 0, None, 0, 16, None, None, None) == _lib.DG_OK
     assert L.dg_assemble_batch(None, 0, None, 0, fake, -1, 16, fake, None, None) == _lib.DG_EINVAL

@@ -1,0 +1,105 @@
+"""Loops over groups with the mask-clearing flags: sampling with
+DG_SAMPLE_EXIT_CLEAR (and DG_SAMPLE_ENTRY_CLEAR from the second group on),
+packing with DG_PACK_CLEAR_MEMBERSHIP, on one workspace per call and one
+membership buffer.  Every output must equal that of independent calls without
+the flags, the membership output must equal theirs, and packing must leave the
+mask all-zero.  The workspaces and the mask start filled with garbage, which
+the first call (without DG_SAMPLE_ENTRY_CLEAR) must not see."""
+import random
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module")
+def dg():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2405_05231_amd as m
+    return m
+
+
+def same_sample(a, b):
+    assert np.array_equal(a.hop_ptr, b.hop_ptr) and np.array_equal(a.edge_ptr, b.edge_ptr)
+    for bb in range(a.hop_ptr.shape[0]):
+        n, e = int(a.hop_ptr[bb, -1]), int(a.edge_ptr[bb, -1])
+        assert torch.equal(a.nodes[bb, :n], b.nodes[bb, :n]), bb
+        assert torch.equal(a.edge_src[bb, :e], b.edge_src[bb, :e]), bb
+        assert torch.equal(a.edge_dst[bb, :e], b.edge_dst[bb, :e]), bb
+
+
+def same_pack(a, b, counts):
+    assert a.sizes == b.sizes
+    rows = a.sizes["packed_rows"]
+    assert np.array_equal(a.packed_ptr_host, b.packed_ptr_host)
+    assert torch.equal(a.packed_ids[:rows], b.packed_ids[:rows])
+    assert torch.equal(a.packed[:rows], b.packed[:rows])
+    nu = a.sizes["unique_nodes"]
+    assert torch.equal(a.unique[:nu], b.unique[:nu])
+    for bb, n in enumerate(counts):
+        assert torch.equal(a.loc[bb, :int(n)], b.loc[bb, :int(n)]), bb
+
+
+def sparse_graph():
+    """200k nodes, degrees 0..6, 4 batches of 16 seeds: every hop is small
+    enough to use touched marks, so the sampler clears its state with a fill."""
+    n = 200_000
+    off, idx = synth.uniform_graph(n, 0, 6, seed=31)
+    rnd = random.Random(99)
+    gen = torch.Generator().manual_seed(3)
+    feats = torch.randn((n, 4), generator=gen).to(DEV)
+    slot = torch.full((n,), -1, dtype=torch.int32)
+    slot[torch.tensor(rnd.sample(range(n), n // 10))] = torch.arange(n // 10, dtype=torch.int32)
+    seeds = [torch.tensor([rnd.sample(range(n), 16) for _ in range(4)], dtype=torch.int32,
+                          device=DEV) for _ in range(3)]
+    return (torch.from_numpy(off).to(DEV), torch.from_numpy(idx).to(DEV), feats, slot.to(DEV),
+            seeds, [3, 3, 2], 1234)
+
+
+def workload_groups(name):
+    w = synth.make_workload(name, device=DEV)
+    cfg = w.cfg
+    seeds = [synth.seed_batches(cfg.n, cfg.B, cfg.S, cfg.seed + 1 + g, DEV, offsets=w.offsets)
+             for g in range(3)]
+    return w.offsets, w.indices, w.feats, w.cache_slot, seeds, list(cfg.fanouts), w.rng_seed
+
+
+@pytest.mark.parametrize("case,layered,direct", [("M1", False, True), ("M1", False, False),
+                                                 ("M1", True, True), ("sparse", False, True)])
+def test_group_loop_with_clear_flags(dg, case, layered, direct):
+    off, idx, feats, slot, groups, fan, rng = (sparse_graph() if case == "sparse"
+                                               else workload_groups(case))
+    N = off.numel() - 1
+    B, S = groups[0].shape
+    node_cap, edge_cap = dg.sample_bounds(N, idx.numel(), S, fan, layered)
+    flags = dg.sample_flags(layered, direct)
+    ws_s = torch.full((dg._L.dg_sample_workspace_bytes(N, B, node_cap, edge_cap, flags),), 0xA5,
+                      dtype=torch.uint8, device=DEV)
+    mem = torch.full((N,), -1, dtype=torch.int64, device=DEV)
+    ws_p = None
+    for g, seeds in enumerate(groups):
+        print(f"[{case} layered={layered} direct={direct}] group {g}", flush=True)
+        sr = dg.sample_group(off, idx, seeds, fan, rng, batch_base=g * B, membership=mem,
+                             workspace=ws_s, layered=layered, direct=direct, exit_clear=True,
+                             entry_clear=g > 0)
+        mem_f = torch.empty(N, dtype=torch.int64, device=DEV)
+        sr_f = dg.sample_group(off, idx, seeds, fan, rng, batch_base=g * B, membership=mem_f,
+                               layered=layered, direct=direct)
+        same_sample(sr, sr_f)
+        assert torch.equal(mem, mem_f)
+        counts = sr.hop_ptr[:, -1].copy()
+        if ws_p is None:
+            ws_p = torch.full((dg._L.dg_pack_workspace_bytes(N, B, int(counts.sum())) * 2,), 0x5A,
+                              dtype=torch.uint8, device=DEV)
+        pr = dg.pack_group(feats, slot, sr.nodes, counts, with_unique=True, membership=mem,
+                           workspace=ws_p, clear_membership=True)
+        torch.cuda.synchronize()
+        assert int(mem.count_nonzero()) == 0
+        pr_f = dg.pack_group(feats, slot, sr_f.nodes, counts, with_unique=True, membership=mem_f)
+        same_pack(pr, pr_f, counts)

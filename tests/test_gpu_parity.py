@@ -291,8 +291,8 @@ def test_assemble_batches_matches_per_batch_calls(dg):
 @pytest.mark.parametrize("layered,direct", [(False, False), (True, True)])
 def test_sparse_hops_on_a_large_graph(dg, orc, layered, direct):
     """A small frontier on a large graph: every hop's edges reach only a small
-    share of the nodes, so the sampler lists new nodes from the 64-node rounds
-    its draws touched (the count pass skips the others)."""
+    share of the nodes, so the sampler lists new nodes from the 8-node mask
+    lines its draws touched (the count pass skips the others)."""
     n = 200_000
     off, idx = synth.uniform_graph(n, 0, 6, seed=31)
     off, idx = torch.from_numpy(off), torch.from_numpy(idx)
