@@ -127,18 +127,24 @@ __device__ __forceinline__ void emit_chunk(const int32_t (&u)[EMIT], const int64
   }
 }
 
-// One lane per frontier node.  Floyd's subset is built in registers (fully
-// unrolled, so the arrays stay in VGPRs); each drawn position's rank among the
-// f positions gives its slot, so no sort is needed.  Neighbour loads and
-// membership atomics are issued EMIT at a time so their latencies overlap.
-// estart[b] = f_eoff at batch b's first frontier entry (written on the device
-// by k_batch_bounds).  A node whose edges would pass edge_cap writes nothing;
-// the host sees the overflow in the edge counts and reports it.
+// LPN lanes per frontier node (LPN = 1, 2, 4 or 8; more lanes when the
+// frontier is small, so that short hops still keep enough loads in flight).
+// Floyd's subset is built in registers (fully unrolled, so the arrays stay in
+// VGPRs), by every lane of the node; each drawn position's rank among the f
+// positions gives its slot, so no sort is needed, and lane `sub` takes the
+// draws s with s mod LPN = sub.  Neighbour loads and membership atomics are
+// issued EMIT at a time so their latencies overlap.  estart[b] = f_eoff at
+// batch b's first frontier entry (written on the device by k_batch_bounds).  A
+// node whose edges would pass edge_cap writes nothing; the host sees the
+// overflow in the edge counts and reports it.
+template <int LPN>
 __global__ __launch_bounds__(THREADS) void k_hop_sample(
     Hop h, const int32_t *nodes, int64_t node_cap, const int32_t *idx, const int64_t *f_off,
     const int64_t *f_deg, const int64_t *f_eoff, const int64_t *estart, int64_t edge_cap,
     int32_t *edge_src, int32_t *edge_dst, uint64_t *visited, int64_t N, uint32_t *err) {
-  int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
+  const int64_t t = (int64_t)blockIdx.x * THREADS + threadIdx.x;
+  const int64_t i = t / LPN;
+  const int sub = (int)(t % LPN);
   if (i >= h.ftot) return;
   int b = find_batch(h.fstart, h.B, i);
   int64_t p = h.fpos[b] + (i - h.fstart[b]);
@@ -151,14 +157,18 @@ __global__ __launch_bounds__(THREADS) void k_hop_sample(
   int32_t u[EMIT];
   int64_t slot[EMIT];
   if (h.f < 0 || d <= (int64_t)h.f) {  // every neighbour, in CSR order
-    for (int64_t q0 = 0; q0 < d; q0 += EMIT) {
-      const int cnt = d - q0 < EMIT ? (int)(d - q0) : EMIT;
+    // lane sub takes positions q0 + sub + LPN*k, so the lanes of a node read
+    // consecutive positions in one instruction
+    for (int64_t q0 = 0; q0 < d; q0 += (int64_t)LPN * EMIT) {
+      int n = 0;
 #pragma unroll
       for (int k = 0; k < EMIT; ++k) {
-        slot[k] = base + q0 + k;
-        u[k] = k < cnt ? idx[o0 + q0 + k] : 0;
+        const int64_t q = q0 + sub + (int64_t)LPN * k;
+        slot[k] = base + q;
+        u[k] = q < d ? idx[o0 + q] : 0;
+        n += q < d ? 1 : 0;
       }
-      emit_chunk(u, slot, cnt, b, parent, edge_src, edge_dst, visited, N, h.touched, err);
+      emit_chunk(u, slot, n, b, parent, edge_src, edge_dst, visited, N, h.touched, err);
     }
     return;
   }
@@ -166,7 +176,7 @@ __global__ __launch_bounds__(THREADS) void k_hop_sample(
   int32_t v = nodes[(int64_t)b * node_cap + p];
   uint64_t key = mix64(h.bstate[b] ^ (((uint64_t)(uint32_t)h.k << 32) | (uint64_t)(uint32_t)v));
   if (d > 0x7fffffffll) {  // positions are kept as 32-bit values
-    atomicOr(err, ERR_CSR);
+    if (sub == 0) atomicOr(err, ERR_CSR);
     return;
   }
   if (f <= FMAX) {
@@ -177,40 +187,56 @@ __global__ __launch_bounds__(THREADS) void k_hop_sample(
       if (s < f) {
         uint32_t j = (uint32_t)(d - f + s);
         uint64_t hs = mix64(key + GAMMA * (uint64_t)(s + 1));
-        uint32_t t = (uint32_t)__umul64hi(hs, (uint64_t)j + 1ull);
+        uint32_t tt = (uint32_t)__umul64hi(hs, (uint64_t)j + 1ull);
         bool seen = false;
 #pragma unroll
-        for (int m = 0; m < s; ++m) seen |= (r[m] == t);
-        r[s] = seen ? j : t;
+        for (int m = 0; m < s; ++m) seen |= (r[m] == tt);
+        r[s] = seen ? j : tt;
       }
     }
+    // this lane's draws: s = j*LPN + sub for j = 0, 1, ... (a static j, so the
+    // register arrays are indexed by constants only)
+    constexpr int SPL = FMAX / LPN;
+    uint32_t rv[SPL];
 #pragma unroll
-    for (int s0 = 0; s0 < FMAX; s0 += EMIT) {
-      if (s0 < f) {
-        const int cnt = f - s0 < EMIT ? f - s0 : EMIT;
+    for (int j = 0; j < SPL; ++j) {
+      rv[j] = 0xffffffffu;
+#pragma unroll
+      for (int q = 0; q < LPN; ++q)
+        if (q == sub) rv[j] = r[j * LPN + q];
+    }
+#pragma unroll
+    for (int j0 = 0; j0 < SPL; j0 += EMIT) {
+      if (j0 * LPN < f) {
+        int n = 0;
 #pragma unroll
         for (int k = 0; k < EMIT; ++k) {
-          const int s = s0 + k;
+          const int j = j0 + k;
+          const bool mine = j < SPL && j * LPN + sub < f;
+          const uint32_t x = j < SPL ? rv[j] : 0xffffffffu;
           int rank = 0;
 #pragma unroll
-          for (int m = 0; m < FMAX; ++m) rank += (m < f && r[m] < r[s]) ? 1 : 0;
+          for (int m = 0; m < FMAX; ++m) rank += (m < f && r[m] < x) ? 1 : 0;
           slot[k] = base + rank;
-          u[k] = k < cnt ? idx[o0 + r[s]] : 0;
+          u[k] = mine ? idx[o0 + x] : 0;
+          n += mine ? 1 : 0;
         }
-        emit_chunk(u, slot, cnt, b, parent, edge_src, edge_dst, visited, N, h.touched, err);
+        emit_chunk(u, slot, n, b, parent, edge_src, edge_dst, visited, N, h.touched, err);
       }
     }
     return;
   }
-  // Larger fan-outs: the subset is built in this node's edge slots, then sorted.
+  // Larger fan-outs (one lane per node): the subset is built in this node's
+  // edge slots, then sorted.
+  if (sub != 0) return;
   int32_t *r = edge_dst + base;
   for (int s = 0; s < f; ++s) {
     int64_t j = d - f + s;
     uint64_t hs = mix64(key + GAMMA * (uint64_t)(s + 1));
-    int32_t t = (int32_t)__umul64hi(hs, (uint64_t)(j + 1));
+    int32_t tt = (int32_t)__umul64hi(hs, (uint64_t)(j + 1));
     bool seen = false;
-    for (int m = 0; m < s; ++m) seen |= (r[m] == t);
-    r[s] = seen ? (int32_t)j : t;
+    for (int m = 0; m < s; ++m) seen |= (r[m] == tt);
+    r[s] = seen ? (int32_t)j : tt;
   }
   for (int s = 1; s < f; ++s) {  // insertion sort
     int32_t x = r[s];
@@ -222,13 +248,13 @@ __global__ __launch_bounds__(THREADS) void k_hop_sample(
     r[m + 1] = x;
   }
   for (int s0 = 0; s0 < f; s0 += EMIT) {
-    const int cnt = f - s0 < EMIT ? f - s0 : EMIT;
+    const int n = f - s0 < EMIT ? f - s0 : EMIT;
 #pragma unroll
     for (int k = 0; k < EMIT; ++k) {
       slot[k] = base + s0 + k;
-      u[k] = k < cnt ? idx[o0 + r[s0 + k]] : 0;
+      u[k] = k < n ? idx[o0 + r[s0 + k]] : 0;
     }
-    emit_chunk(u, slot, cnt, b, parent, edge_src, edge_dst, visited, N, h.touched, err);
+    emit_chunk(u, slot, n, b, parent, edge_src, edge_dst, visited, N, h.touched, err);
   }
 }
 
@@ -505,9 +531,28 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       // edge offsets at the batch boundaries, kept on the device
       hipLaunchKernelGGL(k_batch_bounds, dim3(1), dim3(DG_MAX_BATCHES + 1), 0, s, h, w.f_eoff,
                          w.small + ST_BOUNDS);
-      hipLaunchKernelGGL(k_hop_sample, dim3(blocks_for(h.ftot)), dim3(THREADS), 0, s, h, nodes,
-                         node_cap, g->indices, w.f_off, w.f_deg, w.f_eoff, w.small + ST_BOUNDS,
-                         edge_cap, edge_src, edge_dst, w.visited, N, w.err);
+      // lanes per frontier node: up to 8 while the frontier has fewer than 2^20
+      // entries (never more lanes than draws; fan-outs above FMAX keep one)
+      int lpn = 1;
+      while (lpn < 8 && h.ftot * lpn < (1 << 20) && (f < 0 || (f <= FMAX && 2 * lpn <= f)))
+        lpn *= 2;
+      const dim3 hg(blocks_for(h.ftot * lpn)), hb(THREADS);
+      if (lpn == 8)
+        hipLaunchKernelGGL(k_hop_sample<8>, hg, hb, 0, s, h, nodes, node_cap, g->indices, w.f_off,
+                           w.f_deg, w.f_eoff, w.small + ST_BOUNDS, edge_cap, edge_src, edge_dst,
+                           w.visited, N, w.err);
+      else if (lpn == 4)
+        hipLaunchKernelGGL(k_hop_sample<4>, hg, hb, 0, s, h, nodes, node_cap, g->indices, w.f_off,
+                           w.f_deg, w.f_eoff, w.small + ST_BOUNDS, edge_cap, edge_src, edge_dst,
+                           w.visited, N, w.err);
+      else if (lpn == 2)
+        hipLaunchKernelGGL(k_hop_sample<2>, hg, hb, 0, s, h, nodes, node_cap, g->indices, w.f_off,
+                           w.f_deg, w.f_eoff, w.small + ST_BOUNDS, edge_cap, edge_src, edge_dst,
+                           w.visited, N, w.err);
+      else
+        hipLaunchKernelGGL(k_hop_sample<1>, hg, hb, 0, s, h, nodes, node_cap, g->indices, w.f_off,
+                           w.f_deg, w.f_eoff, w.small + ST_BOUNDS, edge_cap, edge_src, edge_dst,
+                           w.visited, N, w.err);
       DG_HIP(hipGetLastError());
       const int ev1 = tm.mark();
       // new nodes of this hop, per batch, ascending; the write pass needs only
