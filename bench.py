@@ -77,6 +77,9 @@ def main():
                     help="request per-phase timing from every packing call (its phases then "
                          "run one after the other, so a kernel trace sees the fan-out gather "
                          "alone in every call)")
+    ap.add_argument("--rows-inline", action="store_true",
+                    help="pipelined region: keep packing's row copy inside the packing call "
+                         "instead of queueing it on the assembly stream (comparison)")
     ap.add_argument("--fill-masks", action="store_true",
                     help="clear the membership mask and the sampler's state with full fills "
                          "in every sampling call, instead of the clearing flags (comparison)")
@@ -148,8 +151,10 @@ def main():
     pr2 = [dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, membership=mem,
                          timing=args.timed_pack) for _ in range(2)]
     pr = pr2[0]
-    ws_p = torch.empty(dg._L.dg_pack_workspace_bytes(cfg.n, B, int(counts.sum())),
-                       dtype=torch.uint8, device=dev)
+    # two packing workspaces: in the pipelined region a packing call's row copy
+    # may still be queued on the assembly stream when the next call starts
+    ws_p2 = [torch.empty(dg._L.dg_pack_workspace_bytes(cfg.n, B, int(counts.sum())),
+                         dtype=torch.uint8, device=dev) for _ in range(2)]
     nmax = int(counts.max())
     ybuf = [torch.empty((nmax, R), dtype=torch.uint8, device=dev) for _ in range(2)]
     sizes_s, sizes_p = dict(sr.sizes), dict(pr.sizes)
@@ -161,7 +166,10 @@ def main():
     # the fan-out gather is timed by HIP events inside dg_pack_group.  Assembly
     # runs on `s_asm`: serially (the host waits for it) or pipelined, where
     # assembly of step k overlaps sampling and packing of step k+1 (both
-    # streams at default priority).
+    # streams at default priority).  In the pipelined region packing also leaves
+    # its row copy (the fan-out gather) queued on s_asm ahead of the assembly
+    # (DG_PACK_ROWS_STREAM), so the bandwidth-bound copy runs beside the next
+    # step's sampling instead of on the sampling stream.
     s_asm = torch.cuda.Stream(device=dev)
     asm_done = [torch.cuda.Event(), torch.cuda.Event()]
     pack_done = torch.cuda.Event()
@@ -219,10 +227,11 @@ def main():
                                     exit_clear=clearing, entry_clear=entry_clear)
             t1 = time.perf_counter()
             stream.wait_event(asm_done[slot])  # the assembly that last read pr2[slot]
+            rows_async = pipelined and not args.rows_inline and not args.timed_pack
             p_out = dg.pack_group(w.feats, w.cache_slot, s_out.nodes, counts, out=pr2[slot],
-                                  workspace=ws_p, timing=record or args.timed_pack,
+                                  workspace=ws_p2[slot], timing=record or args.timed_pack,
                                   membership=mem, clear_membership=clearing,
-                                  stream=stream)
+                                  stream=stream, rows_stream=s_asm if rows_async else None)
             state["clear"] = clearing
             t2 = time.perf_counter()
             e0, e1 = ev_pool[k]
@@ -308,6 +317,10 @@ def main():
                       "assembly of step k (second stream) overlaps sampling and packing of "
                       "step k+1; the serial figures below wait for each step's assembly"),
         "assembly_issue": "HIP graph replay" if asm_graph is not None else "direct calls",
+        "pack_rows": ("pipelined region: packing's row copy queued on the assembly stream "
+                      "(DG_PACK_ROWS_STREAM)" if not (args.rows_inline or args.timed_pack
+                                                      or args.no_pipeline)
+                      else "inside the packing call"),
         "mask_clearing": ("clearing flags: packing clears the membership words it reads and "
                           "sampling leaves its state clear, so no full-mask fill runs per step"
                           if clearing else "two full-mask fills in every sampling call"),

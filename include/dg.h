@@ -39,7 +39,8 @@
  *  - Work is enqueued on the caller's stream `stream` (NULL = the default
  *    stream).  dg_sample_group and dg_pack_group return only when their work has
  *    completed (their output sizes are data-dependent and are reported in
- *    `*sizes`); dg_assemble_batch is asynchronous.
+ *    `*sizes`), except for a row copy that dg_pack_group is told to leave on a
+ *    second stream (DG_PACK_ROWS_STREAM); dg_assemble_batch is asynchronous.
  *  - Return value: a dg_status.  On a non-OK return dg_last_error() gives a
  *    message (per calling thread).  No exception or abort crosses the ABI.
  *    On DG_ECAPACITY the call stops before writing past any output buffer;
@@ -137,6 +138,8 @@ extern "C" {
 #define DG_PACK_CLEAR_MEMBERSHIP 1u /* on DG_OK, `membership` (required) is left
                                        all-zero: the call clears each word as it
                                        reads it */
+#define DG_PACK_ROWS_STREAM 2u      /* enqueue the row copy on `rows_stream`, behind the
+                                       tables, and return without waiting for it */
 
 typedef enum dg_status {
   DG_OK = 0,
@@ -283,7 +286,16 @@ size_t dg_pack_workspace_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes
  *               bit b of membership[u] set iff u is in batch b's list, as
  *               dg_sample_group returns it; bits of batches >= B are ignored.
  *               Read only, unless flags holds DG_PACK_CLEAR_MEMBERSHIP.
- *   flags       0 or DG_PACK_CLEAR_MEMBERSHIP.
+ *   flags       0, or an OR of DG_PACK_CLEAR_MEMBERSHIP and DG_PACK_ROWS_STREAM.
+ *   rows_stream used only with DG_PACK_ROWS_STREAM (and packed != NULL): the row
+ *               copy, which reads feats and the workspace and writes packed, is
+ *               enqueued there after an event that follows the tables on
+ *               `stream`, and the call returns when the tables are done.  Work
+ *               the caller queues on rows_stream after the call sees `packed`
+ *               complete.  Until the copy has run, the workspace must not be
+ *               reused and feats and packed must not be written.  This lets a
+ *               pipeline run the bandwidth-bound copy beside the next group's
+ *               sampling.
  *               The call checks that the bit of every non-cached list entry is
  *               set and that the mask holds as many (node, batch) pairs as the
  *               lists have entries (DG_EINVAL otherwise); a mask that passes these
@@ -292,7 +304,8 @@ size_t dg_pack_workspace_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes
  *   sizes, timing as for dg_sample_group.  Without timing the address tables
  *               are built on the library's second stream while the row copy
  *               runs on `stream` (both done before the call returns); with
- *               timing the phases run one after the other.
+ *               timing the phases run one after the other.  timing cannot be
+ *               combined with DG_PACK_ROWS_STREAM.
  * Errors: DG_EINVAL for null pointers, B outside 1..64, row_bytes < 1, n_b out of
  * range, unknown flags (or DG_PACK_CLEAR_MEMBERSHIP without membership), and on
  * the device a node ID outside [0,N), a node repeated within a batch, or
@@ -304,8 +317,8 @@ int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
                   void *packed, int32_t *packed_ids, int64_t *packed_ptr,
                   int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique,
                   int64_t unique_cap, uint64_t *membership, uint32_t flags, void *ws,
-                  size_t ws_bytes, hipStream_t stream, dg_sizes *sizes,
-                  dg_timing *timing);
+                  size_t ws_bytes, hipStream_t stream, hipStream_t rows_stream,
+                  dg_sizes *sizes, dg_timing *timing);
 
 /* Feature assembling for one mini-batch (§4 Fig. 3, second step; addresses come
  * from the precomputed table of §6, so no lookup structure is consulted):

@@ -183,13 +183,15 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
                with_unique: bool = False, out: PackResult | None = None,
                workspace: torch.Tensor | None = None, stream=None, timing: bool = False,
                membership: torch.Tensor | None = None, tables_only: bool = False,
-               clear_membership: bool = False) -> PackResult:
+               clear_membership: bool = False, rows_stream=None) -> PackResult:
     """Batched packing (dg_pack_group).  nodes: int32 [B, node_stride];
     node_count: the B list lengths (host).  membership: optional int64 [N]
     mask from sample_group (skips rebuilding it).  tables_only: build the
     packed order and address tables without copying rows (packed = None).
     clear_membership: DG_PACK_CLEAR_MEMBERSHIP (membership is all-zero after
-    the call)."""
+    the call).  rows_stream: DG_PACK_ROWS_STREAM, the row copy is left queued on
+    that stream (the call returns once the tables are done; keep `workspace`,
+    `feats` and the packed buffer untouched until the copy has run)."""
     dev = feats.device
     _need(feats, "feats", None)
     _need(cache_slot, "cache_slot", torch.int32, dev)
@@ -224,7 +226,7 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
         st = _L.dg_pack_group(_ptr(feats), N, R, _ptr(cache_slot), B, _ptr(nodes), stride,
                               counts.ctypes.data_as(_lib.I64P), 0, None, None, _ptr(ptr),
                               ptr_host.ctypes.data_as(_lib.I64P), _ptr(loc), None, 0,
-                              _ptr(membership), 0, _ptr(ws), ws.numel(), _stream(stream),
+                              _ptr(membership), 0, _ptr(ws), ws.numel(), _stream(stream), None,
                               ctypes.byref(sz), None)
         if st not in (DG_OK, DG_ECAPACITY):
             check(st)
@@ -244,8 +246,10 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
                           out.packed_ptr_host.ctypes.data_as(_lib.I64P), _ptr(out.loc),
                           _ptr(out.unique), out.unique.numel() if out.unique is not None else 0,
                           _ptr(membership),
-                          _lib.DG_PACK_CLEAR_MEMBERSHIP if clear_membership else 0,
+                          (_lib.DG_PACK_CLEAR_MEMBERSHIP if clear_membership else 0)
+                          | (_lib.DG_PACK_ROWS_STREAM if rows_stream is not None else 0),
                           _ptr(ws), ws.numel(), _stream(stream),
+                          _stream(rows_stream) if rows_stream is not None else None,
                           ctypes.byref(sz),
                           ctypes.byref(tm) if timing else None)
     out.sizes = sz.as_dict()

@@ -14,6 +14,7 @@ DG_SAMPLE_DIRECT = 2
 DG_SAMPLE_EXIT_CLEAR = 4
 DG_SAMPLE_ENTRY_CLEAR = 8
 DG_PACK_CLEAR_MEMBERSHIP = 1
+DG_PACK_ROWS_STREAM = 2
 DG_MAX_BATCHES = 64
 STATUS_NAMES = {0: "DG_OK", -1: "DG_EINVAL", -2: "DG_ECAPACITY", -3: "DG_EHIP",
                 -4: "DG_EWORKSPACE"}
@@ -63,8 +64,8 @@ SIGNATURES = {
                                        ctypes.POINTER(Sizes), ctypes.POINTER(Timing)]),
     "dg_pack_workspace_bytes": (SZ, [I64, I32, I64]),
     "dg_pack_group": (ctypes.c_int, [VP, I64, I64, VP, I32, VP, I64, I64P, I64, VP, VP, VP, I64P,
-                                     VP, VP, I64, VP, U32, VP, SZ, VP, ctypes.POINTER(Sizes),
-                                     ctypes.POINTER(Timing)]),
+                                     VP, VP, I64, VP, U32, VP, SZ, VP, VP,
+                                     ctypes.POINTER(Sizes), ctypes.POINTER(Timing)]),
     "dg_assemble_batch": (ctypes.c_int, [VP, I64, VP, I64, VP, I64, I64, VP, VP, VP]),
     "dg_assemble_batches": (ctypes.c_int, [VP, I64, VP, I64P, VP, I64, I64P, I32, I64,
                                            ctypes.POINTER(VP), I32, VP, VP]),

@@ -155,11 +155,12 @@ int read_to_host(void *dst, const void *src, size_t bytes, hipStream_t s);
 
 // ---------------------------------------------------------------- side stream
 // A second stream per host thread and device, for kernels a call runs beside
-// the caller's stream, with the events that fork from and join back to it.
+// the caller's stream, with the events that fork from and join back to it (and
+// one that orders work the caller's second stream runs behind the call's).
 // Created on first use at default priority and held until the process ends.
 struct SideStream {
   hipStream_t s;
-  hipEvent_t fork, join;
+  hipEvent_t fork, join, handoff;
 };
 int side_stream(SideStream **out);
 

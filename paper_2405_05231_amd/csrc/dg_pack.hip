@@ -283,8 +283,8 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
                              void *packed, int32_t *packed_ids, int64_t *packed_ptr,
                              int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique,
                              int64_t unique_cap, uint64_t *membership, uint32_t flags,
-                             void *ws, size_t ws_bytes, hipStream_t stream, dg_sizes *sizes,
-                             dg_timing *timing) {
+                             void *ws, size_t ws_bytes, hipStream_t stream,
+                             hipStream_t rows_stream, dg_sizes *sizes, dg_timing *timing) {
   if (!feats || !cache_slot || !nodes || !node_count || !packed_ptr || !packed_ptr_host ||
       !loc || !sizes)
     return set_error(DG_EINVAL, "dg_pack_group: null pointer argument");
@@ -292,11 +292,14 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
       node_stride < 0 || packed_cap < 0 || unique_cap < 0)
     return set_error(DG_EINVAL, "dg_pack_group: bad sizes (N=%lld row_bytes=%lld B=%d)",
                      (long long)N, (long long)row_bytes, B);
-  if (flags & ~DG_PACK_CLEAR_MEMBERSHIP)
+  if (flags & ~(DG_PACK_CLEAR_MEMBERSHIP | DG_PACK_ROWS_STREAM))
     return set_error(DG_EINVAL, "dg_pack_group: unknown flags 0x%x", flags);
   const bool clear_membership = flags & DG_PACK_CLEAR_MEMBERSHIP;
   if (clear_membership && !membership)
     return set_error(DG_EINVAL, "dg_pack_group: DG_PACK_CLEAR_MEMBERSHIP needs membership");
+  if ((flags & DG_PACK_ROWS_STREAM) && timing)
+    return set_error(DG_EINVAL, "dg_pack_group: timing cannot be combined with "
+                                "DG_PACK_ROWS_STREAM");
   Lists L;
   L.B = B;
   L.stride = node_stride;
@@ -383,11 +386,22 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
   if ((rc = mask_scan_write(w.ms, s))) return rc;
   const int e2 = tm.mark();
   // The address tables (random reads) and the fan-out gather (HBM streaming)
-  // are independent.  Untimed calls run them side by side, the tables on a side
-  // stream joined back before the call returns; timed calls run them one after
-  // the other so that each phase has its own time.
+  // are independent.  With DG_PACK_ROWS_STREAM the gather goes to the caller's
+  // rows_stream and is not waited for.  Otherwise untimed calls run them side by
+  // side, the tables on a side stream joined back before the call returns, and
+  // timed calls run them one after the other so that each phase has its own
+  // time.
+  const bool rows_async = (flags & DG_PACK_ROWS_STREAM) && packed;
   SideStream *side = nullptr;
-  if (!timing && packed && total > 0) {
+  if (rows_async && total > 0) {
+    SideStream *ss = nullptr;
+    DG_TRY(side_stream(&ss));
+    DG_HIP(hipEventRecord(ss->handoff, s));
+    DG_HIP(hipStreamWaitEvent(rows_stream, ss->handoff, 0));
+    if ((rc = launch_fanout(feats, w.unc_ids, w.unc_off, sizes->unique_packed, rows, w.pairdest,
+                            row_bytes, packed, rows_stream)))
+      return rc;
+  } else if (!timing && packed && total > 0) {
     DG_TRY(side_stream(&side));
     DG_HIP(hipEventRecord(side->fork, s));
     DG_HIP(hipStreamWaitEvent(side->s, side->fork, 0));
@@ -400,7 +414,7 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
   }
   if (side) DG_HIP(hipEventRecord(side->join, side->s));
   const int e3 = tm.mark();
-  if (packed &&  // packed == NULL: address tables only, no row copy
+  if (packed && !rows_async &&  // packed == NULL: address tables only, no row copy
       (rc = launch_fanout(feats, w.unc_ids, w.unc_off, sizes->unique_packed, rows, w.pairdest,
                           row_bytes, packed, s)))
     return rc;

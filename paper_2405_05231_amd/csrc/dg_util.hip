@@ -66,6 +66,7 @@ int side_stream(SideStream **out) {
     DG_HIP(hipStreamCreateWithFlags(&ss[dev].s, hipStreamNonBlocking));
     DG_HIP(hipEventCreateWithFlags(&ss[dev].fork, hipEventDisableTiming));
     DG_HIP(hipEventCreateWithFlags(&ss[dev].join, hipEventDisableTiming));
+    DG_HIP(hipEventCreateWithFlags(&ss[dev].handoff, hipEventDisableTiming));
     made[dev] = true;
   }
   *out = &ss[dev];

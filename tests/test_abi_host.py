@@ -114,20 +114,27 @@ def test_host_side_argument_errors(L):
     cnt = (ctypes.c_int64 * 2)(3, 9)
     ph = (ctypes.c_int64 * 3)()
     rc = L.dg_pack_group(fake, 10, 0, fake, 2, fake, 8, cnt, 0, None, None, fake, ph, fake, None,
-                         0, None, 0, fake, 1 << 20, None, ctypes.byref(sizes), None)
+                         0, None, 0, fake, 1 << 20, None, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL
     rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, cnt, 0, None, None, fake, ph, fake, None,
-                         0, None, 0, fake, 1 << 20, None, ctypes.byref(sizes), None)
+                         0, None, 0, fake, 1 << 20, None, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL and b"node_count" in L.dg_last_error()
     # pack flags: unknown bits, and a clear request without a membership mask
     ok_cnt = (ctypes.c_int64 * 2)(3, 5)
     rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, ok_cnt, 0, None, None, fake, ph, fake,
-                         None, 0, fake, 2, fake, 1 << 20, None, ctypes.byref(sizes), None)
+                         None, 0, fake, 4, fake, 1 << 20, None, None, ctypes.byref(sizes),
+                         None)
     assert rc == _lib.DG_EINVAL and b"flags" in L.dg_last_error()
     rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, ok_cnt, 0, None, None, fake, ph, fake,
                          None, 0, None, _lib.DG_PACK_CLEAR_MEMBERSHIP, fake, 1 << 20, None,
-                         ctypes.byref(sizes), None)
+                         None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL and b"membership" in L.dg_last_error()
+    # a row copy left on a second stream cannot be timed by the call
+    tm = _lib.Timing()
+    rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, ok_cnt, 0, fake, None, fake, ph, fake,
+                         None, 0, None, _lib.DG_PACK_ROWS_STREAM, fake, 1 << 20, None, None,
+                         ctypes.byref(sizes), ctypes.byref(tm))
+    assert rc == _lib.DG_EINVAL and b"timing" in L.dg_last_error()
     # assemble: n_b = 0 is a no-op; negative sizes and overlap are rejected
     assert L.dg_assemble_batch(None, 0, None, 0, None, 0, 16, None, None, None) == _lib.DG_OK
     assert L.dg_assemble_batch(None, 0, None, 0, fake, -1, 16, fake, None, None) == _lib.DG_EINVAL

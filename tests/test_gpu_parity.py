@@ -341,3 +341,42 @@ def test_assemble_batches_in_a_hip_graph(dg):
         torch.cuda.synchronize()
         for b, n in enumerate(counts):
             assert torch.equal(outs[b][:int(n)], ref[b][:int(n)]), (rep, b)
+
+
+@pytest.mark.parametrize("name", ["T", "M1"])
+def test_pack_rows_on_a_second_stream(dg, name):
+    """DG_PACK_ROWS_STREAM: the row copy left queued on a second stream, and the
+    assembly queued behind it on that stream without a host wait, give the
+    outputs of the ordinary call."""
+    w = synth.make_workload(name, device=DEV)
+    X, slot = w.feats, w.cache_slot
+    sr = dg.sample_group(w.offsets, w.indices, w.seeds, list(w.cfg.fanouts), w.rng_seed)
+    counts = sr.node_count
+    ref = dg.pack_group(X, slot, sr.nodes, counts, with_unique=True)
+    R = ref.row_bytes
+    out = dg.pack_group(X, slot, sr.nodes, counts, with_unique=True)  # same-size buffers
+    out.packed.zero_()
+    nmax = int(counts.max())
+    ys = [torch.full((nmax, R), 0xEE, dtype=torch.uint8, device=DEV) for _ in counts]
+    side = torch.cuda.Stream(device=DEV)
+    torch.cuda.synchronize()
+    for rep in range(2):  # twice on the same buffers and workspace
+        ws = torch.empty(dg._L.dg_pack_workspace_bytes(w.cfg.n, w.cfg.B, int(counts.sum())),
+                         dtype=torch.uint8, device=DEV)
+        pr = dg.pack_group(X, slot, sr.nodes, counts, with_unique=True, out=out, workspace=ws,
+                           rows_stream=side)
+        done = torch.cuda.Event()
+        done.record(torch.cuda.current_stream())
+        side.wait_event(done)  # the address tables are on the caller's stream
+        dg.assemble_batches(w.cache, pr, counts, ys, stream=side)
+        side.synchronize()
+        rows = ref.sizes["packed_rows"]
+        assert pr.sizes == ref.sizes
+        assert torch.equal(pr.packed[:rows], ref.packed[:rows]), rep
+        assert torch.equal(pr.packed_ids[:rows], ref.packed_ids[:rows])
+        for b, n in enumerate(counts):
+            n = int(n)
+            assert torch.equal(pr.loc[b, :n], ref.loc[b, :n]), b
+            assert torch.equal(ys[b][:n], X.index_select(0, sr.nodes[b, :n].long())
+                               .view(torch.uint8).reshape(n, R)), b
+        del ws
