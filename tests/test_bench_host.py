@@ -5,6 +5,7 @@ import random
 import subprocess
 import sys
 
+import pytest
 import torch
 
 from conftest import ROOT
@@ -27,16 +28,18 @@ def test_popcount64_matches_python():
     assert got == [bin(v & (2**64 - 1)).count("1") for v in vals]
 
 
-def test_traffic_digest_covers_the_gather_translation_unit(tmp_path, monkeypatch):
-    d = bench.kernel_source_digest()
+@pytest.mark.parametrize("kernel,main", [("fanout_gather", "dg_pack.hip"),
+                                         ("assemble", "dg_assemble.hip")])
+def test_traffic_digest_covers_the_kernel_translation_unit(tmp_path, monkeypatch, kernel, main):
+    d = bench.kernel_source_digest(kernel)
     assert len(d) == 16
     # the digest changes with any file of the translation unit
     src = os.path.join(ROOT, "paper_2405_05231_amd", "csrc")
     fake = tmp_path / "paper_2405_05231_amd" / "csrc"
     fake.mkdir(parents=True)
-    for n in bench.GATHER_TU:
+    for n in bench.KERNEL_TU[kernel]:
         (fake / n).write_bytes(open(os.path.join(src, n), "rb").read())
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
-    assert bench.kernel_source_digest() == d
-    (fake / "dg_pack.hip").write_bytes(b"// changed\n" + (fake / "dg_pack.hip").read_bytes())
-    assert bench.kernel_source_digest() != d
+    assert bench.kernel_source_digest(kernel) == d
+    (fake / main).write_bytes(b"// changed\n" + (fake / main).read_bytes())
+    assert bench.kernel_source_digest(kernel) != d
