@@ -1,5 +1,8 @@
-"""Parity on the named workloads, in the launch configuration bench.py times
-(the sampler's membership mask handed to the packer).
+"""Parity on the named workloads, in the launch configuration bench.py times:
+the sampler's membership mask handed to the packer, the mask-clearing flags
+(two groups in a row on the same membership buffer and workspaces, the second
+sampling call told that the state is clear), and packing's row copy queued on
+a second stream with the assembly behind it.
 
 M1 (1M nodes) compares every integer output with the oracle and every row on
 the device.  The full-size workloads (L100, W120, H65 at three cache shares)
@@ -41,16 +44,34 @@ def check_rows_on_device(X, ids, got, chunk=1 << 20):
         assert rows_equal(got[lo:hi], ref), (lo, hi)
 
 
+def bench_path(dg, w, fan, mem, ws_s, ws_p, direct, entry_clear, out=None):
+    """One group as bench.py runs it: sampling with the clearing flags, packing
+    that clears the mask and leaves its row copy on a second stream."""
+    sr = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, membership=mem,
+                         workspace=ws_s, direct=direct, exit_clear=True,
+                         entry_clear=entry_clear, out=out)
+    counts = sr.node_count.copy()
+    side = torch.cuda.Stream(device=DEV)
+    pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, with_unique=True, membership=mem,
+                       workspace=ws_p, clear_membership=True, rows_stream=side)
+    side.synchronize()
+    torch.cuda.synchronize()
+    return sr, counts, pr
+
+
 def run_and_check(dg, orc, w, oracle_batches, direct=True):
     cfg = w.cfg
     fan = list(cfg.fanouts)
     R = cfg.row_bytes
-    mem = torch.empty(cfg.n, dtype=torch.int64, device=DEV)
-    sr = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, membership=mem,
-                         direct=direct)
-    counts = sr.node_count.copy()
-    pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, with_unique=True, membership=mem)
-    torch.cuda.synchronize()
+    mem = torch.full((cfg.n,), -1, dtype=torch.int64, device=DEV)  # garbage on entry
+    node_cap, edge_cap = dg.sample_bounds(cfg.n, w.num_edges, cfg.S, fan)
+    ws_s = torch.empty(dg._L.dg_sample_workspace_bytes(cfg.n, cfg.B, node_cap, edge_cap,
+                                                       dg.sample_flags(direct=direct)),
+                       dtype=torch.uint8, device=DEV)
+    ws_p = torch.empty(dg._L.dg_pack_workspace_bytes(cfg.n, cfg.B, cfg.B * node_cap),
+                       dtype=torch.uint8, device=DEV)
+    sr, counts, pr = bench_path(dg, w, fan, mem, ws_s, ws_p, direct, entry_clear=False)
+    assert int(mem.count_nonzero()) == 0
     print(f"[{cfg.name}] nodes {sr.sizes['total_nodes']:,} edges {sr.sizes['total_edges']:,} "
           f"packed {pr.sizes['packed_rows']:,} U {pr.sizes['unique_nodes']:,}", flush=True)
 
@@ -90,7 +111,26 @@ def run_and_check(dg, orc, w, oracle_batches, direct=True):
         y = dg.assemble_batch(w.cache, pr.chunk(b), pr.loc[b, :n], R, out=out, status=status)
         check_rows_on_device(w.feats, sr.nodes[b, :n], y[:n].view(w.feats.dtype).reshape(n, -1))
     assert int(status.item()) == 0
-    return sr, pr
+
+    # a second group on the same buffers, told that the state is clear: the
+    # same seeds give the same outputs
+    keep = (sr.nodes.clone(), sr.edge_src.clone(), sr.edge_dst.clone(), sr.hop_ptr.copy(),
+            sr.edge_ptr.copy(), pr.packed_ids[:rows].clone(), pr.loc.clone(),
+            pr.packed[:rows].clone())
+    del pr
+    sr2, counts2, pr2 = bench_path(dg, w, fan, mem, ws_s, ws_p, direct, entry_clear=True)
+    assert np.array_equal(counts2, counts) and np.array_equal(sr2.hop_ptr, keep[3])
+    assert np.array_equal(sr2.edge_ptr, keep[4])
+    for b in range(cfg.B):
+        n, e = int(counts[b]), int(keep[4][b, -1])
+        assert torch.equal(sr2.nodes[b, :n], keep[0][b, :n]), b
+        assert torch.equal(sr2.edge_src[b, :e], keep[1][b, :e]), b
+        assert torch.equal(sr2.edge_dst[b, :e], keep[2][b, :e]), b
+        assert torch.equal(pr2.loc[b, :n], keep[6][b, :n]), b
+    assert torch.equal(pr2.packed_ids[:rows], keep[5])
+    assert torch.equal(pr2.packed[:rows], keep[7])
+    assert int(mem.count_nonzero()) == 0
+    return sr2, pr2
 
 
 def test_workload_M1_full(dg, orc):
