@@ -79,6 +79,9 @@ def main():
                     help="request per-phase timing from every packing call (its phases then "
                          "run one after the other, so a kernel trace sees the fan-out gather "
                          "alone in every call)")
+    ap.add_argument("--no-member-lines", action="store_true",
+                    help="packing reads every membership word instead of only the lines "
+                         "sampling marked as holding a member (comparison)")
     ap.add_argument("--rows-inline", action="store_true",
                     help="pipelined region: keep packing's row copy inside the packing call "
                          "instead of queueing it on the assembly stream (comparison)")
@@ -214,6 +217,10 @@ def main():
     # full-mask fills.  The first call on ws_s starts from unknown contents.
     clearing = not args.fill_masks
     state = {"clear": False}
+    # sampling's last count pass marks the 8-node lines that hold a member, and
+    # packing's count pass reads only those lines
+    lines = (None if args.no_member_lines else
+             torch.empty(dg.member_lines_bytes(cfg.n), dtype=torch.uint8, device=dev))
 
     def run(K, pipelined, record):
         marks, gather_ms, asm_ms = [], [], []
@@ -226,14 +233,16 @@ def main():
             state["clear"] = False
             s_out = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, out=sr,
                                     workspace=ws_s, membership=mem, direct=True, stream=stream,
-                                    exit_clear=clearing, entry_clear=entry_clear)
+                                    exit_clear=clearing, entry_clear=entry_clear,
+                                    member_lines=lines)
             t1 = time.perf_counter()
             stream.wait_event(asm_done[slot])  # the assembly that last read pr2[slot]
             rows_async = pipelined and not args.rows_inline and not args.timed_pack
             p_out = dg.pack_group(w.feats, w.cache_slot, s_out.nodes, counts, out=pr2[slot],
                                   workspace=ws_p2[slot], timing=record or args.timed_pack,
                                   membership=mem, clear_membership=clearing,
-                                  stream=stream, rows_stream=s_asm if rows_async else None)
+                                  stream=stream, rows_stream=s_asm if rows_async else None,
+                                  member_lines=lines)
             state["clear"] = clearing
             t2 = time.perf_counter()
             e0, e1 = ev_pool[k]
@@ -327,6 +336,8 @@ def main():
                       "(DG_PACK_ROWS_STREAM)" if not (args.rows_inline or args.timed_pack
                                                       or args.no_pipeline)
                       else "inside the packing call"),
+        "member_lines": ("packing reads only the membership lines sampling marked"
+                         if lines is not None else "packing reads every membership word"),
         "mask_clearing": ("clearing flags: packing clears the membership words it reads and "
                           "sampling leaves its state clear, so no full-mask fill runs per step"
                           if clearing else "two full-mask fills in every sampling call"),

@@ -213,6 +213,10 @@ int dg_sample_bounds(int64_t num_nodes, int64_t num_edges, int32_t S,
 size_t dg_sample_workspace_bytes(int64_t num_nodes, int32_t B, int64_t node_cap,
                                  int64_t edge_cap, uint32_t flags);
 
+/* Bytes of a member-lines map for N nodes: one byte per 8 consecutive nodes,
+ * rounded up to whole blocks of 4096 nodes (512 bytes each). */
+size_t dg_member_lines_bytes(int64_t num_nodes);
+
 /* Group sampling (§2 Fig. 1; §3: many mini-batches are sampled before any
  * computation).  Rule and randomness: see the top of this file.
  *   g          CSR graph [host struct, device arrays].
@@ -246,6 +250,13 @@ size_t dg_sample_workspace_bytes(int64_t num_nodes, int32_t B, int64_t node_cap,
  *   membership optional [N] uint64 output (NULL = kept in the workspace): on
  *              return bit b of membership[u] is set iff u is in nodes_b.  It can
  *              be handed to dg_pack_group, which then skips building it.
+ *   member_lines  optional [dg_member_lines_bytes(N)] uint8 output: byte i is
+ *              non-zero iff one of nodes 8i .. 8i+7 is in some list (bytes past
+ *              the last node are 0).  Handed to dg_pack_group with the
+ *              membership words, it lets packing read only the words of marked
+ *              lines.  The last hop's compaction writes it as it reads every
+ *              word; when that hop reads only part of the words (small hops),
+ *              a pass over the membership words writes it instead.
  *   sizes      [host] filled on DG_OK and DG_ECAPACITY.
  *   timing     [host] optional (NULL = not measured).
  * node_cap must be below 2^27.
@@ -258,8 +269,9 @@ int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S,
                     int64_t batch_base, const int32_t *fanouts, int32_t K,
                     uint64_t rng_seed, uint32_t flags, int64_t node_cap, int32_t *nodes,
                     int64_t *hop_ptr, int64_t edge_cap, int32_t *edge_src,
-                    int32_t *edge_dst, int64_t *edge_ptr, uint64_t *membership, void *ws,
-                    size_t ws_bytes, hipStream_t stream, dg_sizes *sizes, dg_timing *timing);
+                    int32_t *edge_dst, int64_t *edge_ptr, uint64_t *membership,
+                    uint8_t *member_lines, void *ws, size_t ws_bytes, hipStream_t stream,
+                    dg_sizes *sizes, dg_timing *timing);
 
 /* Workspace bytes dg_pack_group needs for N nodes, B batches whose node lists
  * hold `total_nodes` entries in all. */
@@ -286,6 +298,10 @@ size_t dg_pack_workspace_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes
  *               bit b of membership[u] set iff u is in batch b's list, as
  *               dg_sample_group returns it; bits of batches >= B are ignored.
  *               Read only, unless flags holds DG_PACK_CLEAR_MEMBERSHIP.
+ *   member_lines  optional (with membership) [dg_member_lines_bytes(N)] uint8, as
+ *               dg_sample_group writes it: words of lines whose byte is 0 are
+ *               not read.  A member in an unmarked line is missed, which the
+ *               pair-count check reports (DG_EINVAL).
  *   flags       0, or an OR of DG_PACK_CLEAR_MEMBERSHIP and DG_PACK_ROWS_STREAM.
  *   rows_stream used only with DG_PACK_ROWS_STREAM (and packed != NULL): the row
  *               copy, which reads feats and the workspace and writes packed, is
@@ -307,7 +323,8 @@ size_t dg_pack_workspace_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes
  *               timing the phases run one after the other.  timing cannot be
  *               combined with DG_PACK_ROWS_STREAM.
  * Errors: DG_EINVAL for null pointers, B outside 1..64, row_bytes < 1, n_b out of
- * range, unknown flags (or DG_PACK_CLEAR_MEMBERSHIP without membership), and on
+ * range, unknown flags (or DG_PACK_CLEAR_MEMBERSHIP or member_lines without
+ * membership), and on
  * the device a node ID outside [0,N), a node repeated within a batch, or
  * cache_slot[v] < -1.  DG_ECAPACITY when packed_cap < sum|P_b| or
  * (group_unique != NULL and) unique_cap < |U|. */
@@ -316,7 +333,8 @@ int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
                   int64_t node_stride, const int64_t *node_count, int64_t packed_cap,
                   void *packed, int32_t *packed_ids, int64_t *packed_ptr,
                   int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique,
-                  int64_t unique_cap, uint64_t *membership, uint32_t flags, void *ws,
+                  int64_t unique_cap, uint64_t *membership, const uint8_t *member_lines,
+                  uint32_t flags, void *ws,
                   size_t ws_bytes, hipStream_t stream, hipStream_t rows_stream,
                   dg_sizes *sizes, dg_timing *timing);
 

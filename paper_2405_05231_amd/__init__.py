@@ -18,7 +18,8 @@ from . import _lib
 from ._lib import (DG_ECAPACITY, DG_MAX_BATCHES, DG_OK, DGError, Csr, Sizes, Timing, check,
                    load)
 
-__all__ = ["sample_bounds", "sample_group", "pack_group", "assemble_batch", "cache_by_frequency",
+__all__ = ["sample_bounds", "member_lines_bytes", "sample_group", "pack_group", "assemble_batch",
+           "assemble_batches", "cache_by_frequency",
            "gather_rows", "pack_individual", "minhash_order", "DGError", "SampleResult",
            "PackResult", "version"]
 
@@ -56,6 +57,11 @@ def _workspace(nbytes: int, device, ws: torch.Tensor | None):
     if ws is not None and ws.numel() * ws.element_size() >= nbytes:
         return ws
     return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+def member_lines_bytes(num_nodes: int) -> int:
+    """Bytes of a member-lines map (dg_member_lines_bytes)."""
+    return int(_L.dg_member_lines_bytes(num_nodes))
 
 
 def sample_bounds(num_nodes: int, num_edges: int, S: int, fanouts,
@@ -104,7 +110,8 @@ def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tens
                  workspace: torch.Tensor | None = None, stream=None, timing: bool = False,
                  membership: torch.Tensor | None = None, layered: bool = False,
                  direct: bool = False, entry_clear: bool = False,
-                 exit_clear: bool = False) -> SampleResult:
+                 exit_clear: bool = False, member_lines: torch.Tensor | None = None
+                 ) -> SampleResult:
     """Group sampling (dg_sample_group).  seeds: int32 [B, S] on the GPU.
     membership: optional int64 [N] tensor that receives the (node, batch)
     membership mask (bit b of word u = u is in batch b).  layered: every node
@@ -112,7 +119,9 @@ def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tens
     direct: relabel through a direct [N][B] table (4*N*B workspace bytes).
     exit_clear / entry_clear: DG_SAMPLE_EXIT_CLEAR / DG_SAMPLE_ENTRY_CLEAR (a
     loop over groups that reuses `workspace` and `membership`, packing each
-    group with clear_membership=True, skips two mask clears per group)."""
+    group with clear_membership=True, skips two mask clears per group).
+    member_lines: optional uint8 tensor of member_lines_bytes(N) bytes that
+    receives a byte per 8 nodes, non-zero iff one of them is in some list."""
     dev = offsets.device
     _need(offsets, "offsets", torch.int64)
     _need(indices, "indices", torch.int32, dev)
@@ -123,6 +132,10 @@ def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tens
             raise ValueError("membership must hold one word per node")
     if seeds.dim() != 2:
         raise ValueError("seeds must be [B, S]")
+    if member_lines is not None:
+        _need(member_lines, "member_lines", torch.uint8, dev)
+        if member_lines.numel() < member_lines_bytes(offsets.numel() - 1):
+            raise ValueError("member_lines holds fewer than member_lines_bytes(N) bytes")
     B, S = seeds.shape
     N = offsets.numel() - 1
     E = indices.numel()
@@ -150,7 +163,8 @@ def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tens
         ctypes.byref(g), _ptr(seeds), B, S, batch_base, fo, K, rng_seed & (2**64 - 1),
         flags, node_cap, _ptr(out.nodes), out.hop_ptr.ctypes.data_as(_lib.I64P), edge_cap,
         _ptr(out.edge_src), _ptr(out.edge_dst), out.edge_ptr.ctypes.data_as(_lib.I64P),
-        _ptr(membership), _ptr(ws), ws.numel(), _stream(stream), ctypes.byref(sz),
+        _ptr(membership), _ptr(member_lines), _ptr(ws), ws.numel(), _stream(stream),
+        ctypes.byref(sz),
         ctypes.byref(tm) if timing else None)
     out.sizes = sz.as_dict()
     check(st)
@@ -183,7 +197,8 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
                with_unique: bool = False, out: PackResult | None = None,
                workspace: torch.Tensor | None = None, stream=None, timing: bool = False,
                membership: torch.Tensor | None = None, tables_only: bool = False,
-               clear_membership: bool = False, rows_stream=None) -> PackResult:
+               clear_membership: bool = False, rows_stream=None,
+               member_lines: torch.Tensor | None = None) -> PackResult:
     """Batched packing (dg_pack_group).  nodes: int32 [B, node_stride];
     node_count: the B list lengths (host).  membership: optional int64 [N]
     mask from sample_group (skips rebuilding it).  tables_only: build the
@@ -191,7 +206,9 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
     clear_membership: DG_PACK_CLEAR_MEMBERSHIP (membership is all-zero after
     the call).  rows_stream: DG_PACK_ROWS_STREAM, the row copy is left queued on
     that stream (the call returns once the tables are done; keep `workspace`,
-    `feats` and the packed buffer untouched until the copy has run)."""
+    `feats` and the packed buffer untouched until the copy has run).
+    member_lines: the map sample_group wrote (with membership): only the
+    words of marked lines are read."""
     dev = feats.device
     _need(feats, "feats", None)
     _need(cache_slot, "cache_slot", torch.int32, dev)
@@ -203,6 +220,10 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
         _need(membership, "membership", torch.int64, dev)
         if membership.numel() != N:
             raise ValueError("membership must hold one word per node")
+    if member_lines is not None:
+        _need(member_lines, "member_lines", torch.uint8, dev)
+        if member_lines.numel() < member_lines_bytes(N):
+            raise ValueError("member_lines holds fewer than member_lines_bytes(N) bytes")
     counts = np.ascontiguousarray(np.asarray(node_count, dtype=np.int64).reshape(-1))
     if counts.shape[0] != B:
         raise ValueError("node_count must have one entry per batch")
@@ -226,7 +247,8 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
         st = _L.dg_pack_group(_ptr(feats), N, R, _ptr(cache_slot), B, _ptr(nodes), stride,
                               counts.ctypes.data_as(_lib.I64P), 0, None, None, _ptr(ptr),
                               ptr_host.ctypes.data_as(_lib.I64P), _ptr(loc), None, 0,
-                              _ptr(membership), 0, _ptr(ws), ws.numel(), _stream(stream), None,
+                              _ptr(membership), _ptr(member_lines), 0, _ptr(ws), ws.numel(),
+                              _stream(stream), None,
                               ctypes.byref(sz), None)
         if st not in (DG_OK, DG_ECAPACITY):
             check(st)
@@ -245,7 +267,7 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
                           _ptr(out.packed_ids), _ptr(out.packed_ptr),
                           out.packed_ptr_host.ctypes.data_as(_lib.I64P), _ptr(out.loc),
                           _ptr(out.unique), out.unique.numel() if out.unique is not None else 0,
-                          _ptr(membership),
+                          _ptr(membership), _ptr(member_lines),
                           (_lib.DG_PACK_CLEAR_MEMBERSHIP if clear_membership else 0)
                           | (_lib.DG_PACK_ROWS_STREAM if rows_stream is not None else 0),
                           _ptr(ws), ws.numel(), _stream(stream),

@@ -58,13 +58,14 @@ SIGNATURES = {
     "dg_last_error": (ctypes.c_char_p, []),
     "dg_sample_bounds": (ctypes.c_int, [I64, I64, I32, I32P, I32, ctypes.c_uint32, I64P, I64P]),
     "dg_sample_workspace_bytes": (SZ, [I64, I32, I64, I64, U32]),
+    "dg_member_lines_bytes": (SZ, [I64]),
     "dg_sample_group": (ctypes.c_int, [ctypes.POINTER(Csr), VP, I32, I32, I64, I32P, I32, U64,
                                        ctypes.c_uint32, I64, VP, I64P, I64, VP, VP, I64P, VP,
-                                       VP, SZ, VP,
+                                       VP, VP, SZ, VP,
                                        ctypes.POINTER(Sizes), ctypes.POINTER(Timing)]),
     "dg_pack_workspace_bytes": (SZ, [I64, I32, I64]),
     "dg_pack_group": (ctypes.c_int, [VP, I64, I64, VP, I32, VP, I64, I64P, I64, VP, VP, VP, I64P,
-                                     VP, VP, I64, VP, U32, VP, SZ, VP, VP,
+                                     VP, VP, I64, VP, VP, U32, VP, SZ, VP, VP,
                                      ctypes.POINTER(Sizes), ctypes.POINTER(Timing)]),
     "dg_assemble_batch": (ctypes.c_int, [VP, I64, VP, I64, VP, I64, I64, VP, VP, VP]),
     "dg_assemble_batches": (ctypes.c_int, [VP, I64, VP, I64P, VP, I64, I64P, I32, I64,

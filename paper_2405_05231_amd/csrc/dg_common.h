@@ -234,6 +234,9 @@ struct MaskScan {
   bool keep_prev;                    // false: leave prev as it is (nothing reads it later)
   bool clear_prev;                   // (without keep_prev) zero each non-zero prev word read
   bool clear_mask;                   // zero each non-zero mask word read (packing mode)
+  uint8_t *lines_out;                // sampling, whole sweeps only (nullable): a byte per
+                                     // 2^MC_TOUCH_SHIFT nodes, non-zero iff one of them
+                                     // holds a bit of the (keep-masked) mask
   const uint8_t *touched;            // nullable: a byte per 2^MC_TOUCH_SHIFT nodes
                                      // (mc_touch_bytes(N) in all); nodes whose byte
                                      // is 0 hold no bit to list (not read)
@@ -251,6 +254,8 @@ void mask_scan_carve(MaskScan &m, Carve &c);
 int mask_scan_count(MaskScan &m, hipStream_t s);
 // Write pass (uses the scans of the preceding count pass).
 int mask_scan_write(const MaskScan &m, hipStream_t s);
+// Member lines of the whole mask (mc_touch_bytes(N) bytes), by a pass of its own.
+int member_lines_pass(const uint64_t *mask, int64_t N, int B, uint8_t *out, hipStream_t s);
 
 // ---------------------------------------------------------------- timing
 // Events are taken from a pool per host thread and device, created on first

@@ -282,7 +282,8 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
                              int64_t node_stride, const int64_t *node_count, int64_t packed_cap,
                              void *packed, int32_t *packed_ids, int64_t *packed_ptr,
                              int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique,
-                             int64_t unique_cap, uint64_t *membership, uint32_t flags,
+                             int64_t unique_cap, uint64_t *membership,
+                             const uint8_t *member_lines, uint32_t flags,
                              void *ws, size_t ws_bytes, hipStream_t stream,
                              hipStream_t rows_stream, dg_sizes *sizes, dg_timing *timing) {
   if (!feats || !cache_slot || !nodes || !node_count || !packed_ptr || !packed_ptr_host ||
@@ -297,6 +298,8 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
   const bool clear_membership = flags & DG_PACK_CLEAR_MEMBERSHIP;
   if (clear_membership && !membership)
     return set_error(DG_EINVAL, "dg_pack_group: DG_PACK_CLEAR_MEMBERSHIP needs membership");
+  if (member_lines && !membership)
+    return set_error(DG_EINVAL, "dg_pack_group: member_lines needs membership");
   if ((flags & DG_PACK_ROWS_STREAM) && timing)
     return set_error(DG_EINVAL, "dg_pack_group: timing cannot be combined with "
                                 "DG_PACK_ROWS_STREAM");
@@ -347,6 +350,7 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
   // unique set, packed order, packed_ptr
   int64_t totals[DG_MAX_BATCHES + 5];  // row totals, then the error word
   w.ms.mask = w.mask;
+  w.ms.touched = member_lines;  // lines without a member are not read
   w.ms.clear_mask = clear_membership;
   w.ms.cache_slot = cache_slot;
   w.ms.err_stage = w.ms.totals + mc_rows(B);  // staged by the count pass's row scan

@@ -423,8 +423,8 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
                                int32_t *nodes,
                                int64_t *hop_ptr, int64_t edge_cap, int32_t *edge_src,
                                int32_t *edge_dst, int64_t *edge_ptr, uint64_t *membership,
-                               void *ws, size_t ws_bytes, hipStream_t stream, dg_sizes *sizes,
-                               dg_timing *timing) {
+                               uint8_t *member_lines, void *ws, size_t ws_bytes,
+                               hipStream_t stream, dg_sizes *sizes, dg_timing *timing) {
   if (!g || !seeds || !nodes || !hop_ptr || !edge_src || !edge_dst || !edge_ptr || !sizes ||
       (K > 0 && !fanouts))
     return set_error(DG_EINVAL, "dg_sample_group: null pointer argument");
@@ -477,6 +477,7 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
     if ((rc = fill_u64(w.prev, (size_t)N, 0, s))) return rc;
   }
   bool prev_cleared = false;  // the last hop's count pass zeroed prev
+  bool lines_done = false;    // the last hop's count pass wrote member_lines
   hipLaunchKernelGGL(k_seed_init, dim3(blocks_for((int64_t)B * S)), dim3(THREADS), 0, s, seeds,
                      B, S, N, node_cap, nodes, w.visited, w.prev, w.local, w.err);
   DG_HIP(hipGetLastError());  // bad seeds are reported at the first hop's round trip
@@ -567,6 +568,9 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       // unless touched marks leave some lines unread.
       w.ms.clear_prev = exit_clear && k == K && !h.touched;
       prev_cleared = w.ms.clear_prev;
+      // the last hop's count pass reads every word unless touched marks limit it
+      w.ms.lines_out = (member_lines && k == K && !h.touched) ? member_lines : nullptr;
+      lines_done = w.ms.lines_out != nullptr;
       w.ms.cache_slot = nullptr;
       w.ms.totals = w.small + ST_TOTALS;
       w.ms.err_stage = w.small + ST_ERR;
@@ -665,6 +669,8 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
   }
   const int ev_r1 = tm.mark();
   if (exit_clear && !prev_cleared && (rc = fill_u64(w.prev, (size_t)N, 0, s))) return rc;
+  if (member_lines && !lines_done && (rc = member_lines_pass(w.visited, N, B, member_lines, s)))
+    return rc;
   if ((rc = check_err(w.err, s))) return rc;
 
   int64_t tn = 0, te = 0, mn = 0, me = 0;

@@ -299,6 +299,21 @@ __global__ __launch_bounds__(MC_THREADS) void k_mask_count(MaskScan a) {
 #pragma unroll
     for (int r = 0; r < MC_ROUNDS; ++r) m[r] &= keep;
   }
+  if (SAMPLE && a.lines_out) {
+    // member lines: round r's 8 bytes are built from its ballot (uniform) and
+    // stored by lane r, 128 bytes per tile (every word was read: no marks)
+    uint64_t lb = 0;
+#pragma unroll
+    for (int r = 0; r < MC_ROUNDS; ++r) {
+      const uint64_t nz = __ballot(m[r] != 0ull);
+      uint64_t v = 0;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) v |= (((nz >> (8 * k)) & 0xffull) ? 1ull : 0ull) << (8 * k);
+      if (lane == r) lb = v;
+    }
+    if (lane < MC_ROUNDS)
+      reinterpret_cast<uint64_t *>(a.lines_out + (t0 >> MC_TOUCH_SHIFT))[lane] = lb;
+  }
   uint64_t any[MC_ROUNDS];  // lanes of round r with a word to list (uniform)
 #pragma unroll
   for (int r = 0; r < MC_ROUNDS; ++r) any[r] = ((live >> r) & 1u) ? __ballot(m[r] != 0ull) : 0ull;
@@ -474,10 +489,33 @@ __global__ __launch_bounds__(RS_THREADS) void k_rows_apply(MaskScan a) {
   for (int i = threadIdx.x; i < n * rows; i += RS_THREADS) dst[i] = sb[i];
 }
 
+// Member lines from the mask alone (for sweeps that did not read every word):
+// byte i = 1 iff one of words 8i .. 8i+7 (below N) has a bit of batches < B.
+__global__ __launch_bounds__(256) void k_member_lines(const uint64_t *mask, int64_t N, int B,
+                                                      int64_t nbytes, uint8_t *out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= nbytes) return;
+  const uint64_t keep = B < 64 ? (1ull << B) - 1ull : ~0ull;
+  uint64_t any = 0;
+  const int64_t u0 = i << MC_TOUCH_SHIFT;
+  for (int k = 0; k < (1 << MC_TOUCH_SHIFT); ++k)
+    if (u0 + k < N) any |= mask[u0 + k] & keep;
+  out[i] = any ? 1 : 0;
+}
+
+int member_lines_pass(const uint64_t *mask, int64_t N, int B, uint8_t *out, hipStream_t s) {
+  const int64_t nbytes = mc_touch_bytes(N);
+  if (nbytes == 0) return DG_OK;
+  hipLaunchKernelGGL(k_member_lines, dim3((unsigned)((nbytes + 255) / 256)), dim3(256), 0, s,
+                     mask, N, B, nbytes, out);
+  DG_HIP(hipGetLastError());
+  return DG_OK;
+}
+
 int mask_scan_count(MaskScan &m, hipStream_t s) {
   if (m.nblk == 0) return fill_u64(reinterpret_cast<uint64_t *>(m.totals), mc_rows(m.B), 0, s);
   if ((m.prev && (m.cache_slot || m.clear_mask)) || (m.keep_prev && m.clear_prev) ||
-      (!m.prev && (m.keep_prev || m.clear_prev)))
+      (!m.prev && (m.keep_prev || m.clear_prev || m.lines_out)) || (m.lines_out && m.touched))
     return set_error(DG_EINVAL, "internal: inconsistent count-pass mode");
   const unsigned nch = (unsigned)mc_chunks(m.nblk);
   if (m.prev)
@@ -587,4 +625,7 @@ int mask_scan_write(const MaskScan &m, hipStream_t s) {
 }  // namespace dg
 
 extern "C" const char *dg_last_error(void) { return dg::g_err; }
+extern "C" size_t dg_member_lines_bytes(int64_t num_nodes) {
+  return num_nodes < 1 ? 0 : (size_t)dg::mc_touch_bytes(num_nodes);
+}
 extern "C" const char *dg_version(void) { return "libdg 0.1 (gfx950)"; }

@@ -85,7 +85,7 @@ def test_host_side_argument_errors(L):
     sizes = _lib.Sizes()
     # null CSR / outputs: rejected before any device call
     rc = L.dg_sample_group(None, None, 1, 1, 0, None, 0, 0, 0, 1, None, None, 1, None, None,
-                           None, None, None, 0, None, ctypes.byref(sizes), None)
+                           None, None, None, None, 0, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL
     assert b"null" in L.dg_last_error()
     g = _lib.Csr(10, 0, 0x1000, 0)
@@ -95,46 +95,59 @@ def test_host_side_argument_errors(L):
     fake = ctypes.c_void_p(0x1000)
     # B out of range
     rc = L.dg_sample_group(ctypes.byref(g), fake, 65, 1, 0, fo, 1, 0, 0, 4, fake, hop, 4, fake,
-                           fake, ep, None, fake, 1 << 20, None, ctypes.byref(sizes), None)
+                           fake, ep, None, None, fake, 1 << 20, None, ctypes.byref(sizes),
+                           None)
     assert rc == _lib.DG_EINVAL
     # workspace missing
     rc = L.dg_sample_group(ctypes.byref(g), fake, 1, 1, 0, fo, 1, 0, 0, 4, fake, hop, 4, fake,
-                           fake, ep, None, None, 0, None, ctypes.byref(sizes), None)
+                           fake, ep, None, None, None, 0, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EWORKSPACE
     # unknown flags
     rc = L.dg_sample_group(ctypes.byref(g), fake, 1, 1, 0, fo, 1, 0, 16, 4, fake, hop, 4, fake,
-                           fake, ep, None, fake, 1 << 20, None, ctypes.byref(sizes), None)
+                           fake, ep, None, None, fake, 1 << 20, None, ctypes.byref(sizes),
+                           None)
     assert rc == _lib.DG_EINVAL and b"flags" in L.dg_last_error()
     # DG_SAMPLE_ENTRY_CLEAR asserts something about `membership`, so it needs one
     rc = L.dg_sample_group(ctypes.byref(g), fake, 1, 1, 0, fo, 1, 0,
                            _lib.DG_SAMPLE_ENTRY_CLEAR, 4, fake, hop, 4, fake,
-                           fake, ep, None, fake, 1 << 20, None, ctypes.byref(sizes), None)
+                           fake, ep, None, None, fake, 1 << 20, None, ctypes.byref(sizes),
+                           None)
     assert rc == _lib.DG_EINVAL and b"membership" in L.dg_last_error()
     # pack: B = 0, row_bytes = 0, counts beyond the stride
     cnt = (ctypes.c_int64 * 2)(3, 9)
     ph = (ctypes.c_int64 * 3)()
     rc = L.dg_pack_group(fake, 10, 0, fake, 2, fake, 8, cnt, 0, None, None, fake, ph, fake, None,
-                         0, None, 0, fake, 1 << 20, None, None, ctypes.byref(sizes), None)
+                         0, None, None, 0, fake, 1 << 20, None, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL
     rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, cnt, 0, None, None, fake, ph, fake, None,
-                         0, None, 0, fake, 1 << 20, None, None, ctypes.byref(sizes), None)
+                         0, None, None, 0, fake, 1 << 20, None, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL and b"node_count" in L.dg_last_error()
     # pack flags: unknown bits, and a clear request without a membership mask
     ok_cnt = (ctypes.c_int64 * 2)(3, 5)
     rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, ok_cnt, 0, None, None, fake, ph, fake,
-                         None, 0, fake, 4, fake, 1 << 20, None, None, ctypes.byref(sizes),
+                         None, 0, fake, None, 4, fake, 1 << 20, None, None, ctypes.byref(sizes),
                          None)
     assert rc == _lib.DG_EINVAL and b"flags" in L.dg_last_error()
     rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, ok_cnt, 0, None, None, fake, ph, fake,
-                         None, 0, None, _lib.DG_PACK_CLEAR_MEMBERSHIP, fake, 1 << 20, None,
+                         None, 0, None, None, _lib.DG_PACK_CLEAR_MEMBERSHIP, fake, 1 << 20, None,
                          None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL and b"membership" in L.dg_last_error()
     # a row copy left on a second stream cannot be timed by the call
     tm = _lib.Timing()
     rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, ok_cnt, 0, fake, None, fake, ph, fake,
-                         None, 0, None, _lib.DG_PACK_ROWS_STREAM, fake, 1 << 20, None, None,
+                         None, 0, None, None, _lib.DG_PACK_ROWS_STREAM, fake, 1 << 20, None, None,
                          ctypes.byref(sizes), ctypes.byref(tm))
     assert rc == _lib.DG_EINVAL and b"timing" in L.dg_last_error()
+    # member lines come with a membership mask
+    rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, ok_cnt, 0, None, None, fake, ph, fake,
+                         None, 0, None, fake, 0, fake, 1 << 20, None, None,
+                         ctypes.byref(sizes), None)
+    assert rc == _lib.DG_EINVAL and b"member_lines" in L.dg_last_error()
+    # member-lines map size: a byte per 8 nodes, in blocks of 4096 nodes
+    assert L.dg_member_lines_bytes(0) == 0
+    assert L.dg_member_lines_bytes(1) == 512
+    assert L.dg_member_lines_bytes(4096) == 512
+    assert L.dg_member_lines_bytes(4097) == 1024
     # assemble: n_b = 0 is a no-op; negative sizes and overlap are rejected
     assert L.dg_assemble_batch(None, 0, None, 0, None, 0, 16, None, None, None) == _lib.DG_OK
     assert L.dg_assemble_batch(None, 0, None, 0, fake, -1, 16, fake, None, None) == _lib.DG_EINVAL

@@ -1,7 +1,7 @@
 """Loops over groups with the mask-clearing flags: sampling with
 DG_SAMPLE_EXIT_CLEAR (and DG_SAMPLE_ENTRY_CLEAR from the second group on),
-packing with DG_PACK_CLEAR_MEMBERSHIP, on one workspace per call and one
-membership buffer.  Every output must equal that of independent calls without
+packing with DG_PACK_CLEAR_MEMBERSHIP and the member-lines map sampling
+writes, on one workspace per call and one membership buffer.  Every output must equal that of independent calls without
 the flags, the membership output must equal theirs, and packing must leave the
 mask all-zero.  The workspaces and the mask start filled with garbage, which
 the first call (without DG_SAMPLE_ENTRY_CLEAR) must not see."""
@@ -82,12 +82,13 @@ def test_group_loop_with_clear_flags(dg, case, layered, direct):
     ws_s = torch.full((dg._L.dg_sample_workspace_bytes(N, B, node_cap, edge_cap, flags),), 0xA5,
                       dtype=torch.uint8, device=DEV)
     mem = torch.full((N,), -1, dtype=torch.int64, device=DEV)
+    lines = torch.full((dg.member_lines_bytes(N),), 0xAB, dtype=torch.uint8, device=DEV)
     ws_p = None
     for g, seeds in enumerate(groups):
         print(f"[{case} layered={layered} direct={direct}] group {g}", flush=True)
         sr = dg.sample_group(off, idx, seeds, fan, rng, batch_base=g * B, membership=mem,
                              workspace=ws_s, layered=layered, direct=direct, exit_clear=True,
-                             entry_clear=g > 0)
+                             entry_clear=g > 0, member_lines=lines)
         mem_f = torch.empty(N, dtype=torch.int64, device=DEV)
         sr_f = dg.sample_group(off, idx, seeds, fan, rng, batch_base=g * B, membership=mem_f,
                                layered=layered, direct=direct)
@@ -98,8 +99,51 @@ def test_group_loop_with_clear_flags(dg, case, layered, direct):
             ws_p = torch.full((dg._L.dg_pack_workspace_bytes(N, B, int(counts.sum())) * 2,), 0x5A,
                               dtype=torch.uint8, device=DEV)
         pr = dg.pack_group(feats, slot, sr.nodes, counts, with_unique=True, membership=mem,
-                           workspace=ws_p, clear_membership=True)
+                           workspace=ws_p, clear_membership=True, member_lines=lines)
         torch.cuda.synchronize()
         assert int(mem.count_nonzero()) == 0
         pr_f = dg.pack_group(feats, slot, sr_f.nodes, counts, with_unique=True, membership=mem_f)
         same_pack(pr, pr_f, counts)
+
+
+def lines_ref(dg, mem):
+    """The member-lines map computed from the membership words by torch."""
+    N = mem.numel()
+    nbytes = dg.member_lines_bytes(N)
+    pad = torch.zeros(nbytes * 8, dtype=torch.int64, device=DEV)
+    pad[:N] = mem
+    return (pad.view(-1, 8) != 0).any(dim=1)
+
+
+@pytest.mark.parametrize("case,layered,direct", [("M1", False, True), ("M1", True, False),
+                                                 ("sparse", False, True)])
+def test_member_lines(dg, case, layered, direct):
+    """The map sampling writes (by its last count pass on M1, by a pass of its
+    own when every hop uses touched marks) marks exactly the 8-node lines that
+    hold a member; packing with it gives the outputs of packing without it, and
+    a map that misses a member line is reported."""
+    off, idx, feats, slot, groups, fan, rng = (sparse_graph() if case == "sparse"
+                                               else workload_groups(case))
+    N = off.numel() - 1
+    seeds = groups[0]
+    B = seeds.shape[0]
+    mem = torch.empty(N, dtype=torch.int64, device=DEV)
+    lines = torch.full((dg.member_lines_bytes(N),), 0xAB, dtype=torch.uint8, device=DEV)
+    sr = dg.sample_group(off, idx, seeds, fan, rng, membership=mem, member_lines=lines,
+                         layered=layered, direct=direct)
+    torch.cuda.synchronize()
+    assert torch.equal(lines != 0, lines_ref(dg, mem))
+    counts = sr.node_count
+    ref = dg.pack_group(feats, slot, sr.nodes, counts, with_unique=True, membership=mem)
+    mem2 = mem.clone()
+    got = dg.pack_group(feats, slot, sr.nodes, counts, with_unique=True, membership=mem2,
+                        member_lines=lines, clear_membership=True)
+    torch.cuda.synchronize()
+    assert int(mem2.count_nonzero()) == 0
+    same_pack(got, ref, counts)
+    # a map that misses a line holding a member
+    bad = lines.clone()
+    bad[int((lines != 0).nonzero()[0])] = 0
+    with pytest.raises(dg.DGError) as e:
+        dg.pack_group(feats, slot, sr.nodes, counts, membership=mem, member_lines=bad)
+    assert e.value.status == -1
