@@ -1,0 +1,97 @@
+"""The pipelined loop bench.py times, checked for correctness under real
+concurrency.  Sampling and packing run on one stream, the row copy and the
+assembly on a second one, with two packing output sets and two packing
+workspaces; each packing call waits for the assembly that last read its set;
+the clearing flags and the member-lines map carry state from step to step.
+Every step takes a different seed group, so an output read or written by the
+wrong step would show up as a wrong row.  Each step assembles into buffers of
+its own, and all are checked against a library gather (torch.index_select) at
+the end."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module")
+def dg():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2405_05231_amd as m
+    return m
+
+
+def test_pipelined_steps_are_each_correct(dg):
+    w = synth.make_workload("M1", device=DEV)
+    cfg = w.cfg
+    fan = list(cfg.fanouts)
+    B, R, steps = cfg.B, cfg.row_bytes, 6
+    groups = [synth.seed_batches(cfg.n, B, cfg.S, cfg.seed + 100 + k, DEV, offsets=w.offsets)
+              for k in range(steps)]
+    node_cap, edge_cap = dg.sample_bounds(cfg.n, w.num_edges, cfg.S, fan)
+    flags = dg.sample_flags(direct=True)
+    ws_s = torch.empty(dg._L.dg_sample_workspace_bytes(cfg.n, B, node_cap, edge_cap, flags),
+                       dtype=torch.uint8, device=DEV)
+    ws_p = [torch.empty(dg._L.dg_pack_workspace_bytes(cfg.n, B, B * node_cap),
+                        dtype=torch.uint8, device=DEV) for _ in range(2)]
+    mem = torch.empty(cfg.n, dtype=torch.int64, device=DEV)
+    lines = torch.empty(dg.member_lines_bytes(cfg.n), dtype=torch.uint8, device=DEV)
+    # output capacity fixed up front (the largest group) so every step reuses it
+    sizes = []
+    for g in groups:
+        sr = dg.sample_group(w.offsets, w.indices, g, fan, w.rng_seed, direct=True)
+        pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, sr.node_count)
+        sizes.append((int(sr.node_count.max()), pr.sizes["packed_rows"]))
+    nmax = max(s[0] for s in sizes)
+    rows_max = max(s[1] for s in sizes)
+    pr2 = []
+    for _ in range(2):
+        pr_ = dg.pack_group(w.feats, w.cache_slot, sr.nodes, sr.node_count)
+        pr_.packed = torch.empty((rows_max, R), dtype=torch.uint8, device=DEV)
+        pr_.packed_ids = torch.empty(rows_max, dtype=torch.int32, device=DEV)
+        pr2.append(pr_)
+    kept = [[torch.empty((nmax, R), dtype=torch.uint8, device=DEV) for _ in range(B)]
+            for _ in range(steps)]
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    s_asm = torch.cuda.Stream(device=DEV)
+    asm_done = [torch.cuda.Event(), torch.cuda.Event()]
+    pack_done = torch.cuda.Event()
+    for e in asm_done:
+        e.record(s_asm)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    results = []
+    clear = False
+    for k in range(steps):
+        slot = k & 1
+        print(f"[pipeline] step {k}", flush=True)
+        sr = dg.sample_group(w.offsets, w.indices, groups[k], fan, w.rng_seed, membership=mem,
+                             workspace=ws_s, direct=True, exit_clear=True, entry_clear=clear,
+                             member_lines=lines, stream=stream)
+        counts = sr.node_count.copy()
+        nodes = sr.nodes.clone()  # the next step's sampling overwrites sr.nodes
+        stream.wait_event(asm_done[slot])
+        pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, out=pr2[slot],
+                           workspace=ws_p[slot], membership=mem, clear_membership=True,
+                           member_lines=lines, stream=stream, rows_stream=s_asm)
+        clear = True
+        pack_done.record(stream)
+        s_asm.wait_event(pack_done)
+        # one output buffer per batch and step, so that every step's rows stay
+        # for the check (the bench alternates two buffers instead)
+        dg.assemble_batches(w.cache, pr, counts, kept[k], status=status, stream=s_asm)
+        asm_done[slot].record(s_asm)
+        results.append((nodes, counts))
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    assert int(mem.count_nonzero()) == 0
+    for k, (nodes, counts) in enumerate(results):
+        for b in range(B):
+            n = int(counts[b])
+            ref = w.feats.index_select(0, nodes[b, :n].long()).view(torch.uint8).reshape(n, R)
+            assert torch.equal(kept[k][b][:n], ref), (k, b)
