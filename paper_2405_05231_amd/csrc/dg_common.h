@@ -96,6 +96,24 @@ __device__ __forceinline__ int find_batch(const int64_t *p, int n, int64_t i) {
   return lo;
 }
 
+// The same for a wave whose active lanes hold non-decreasing i (lane order):
+// when its first and last active lanes fall in one batch, which is the case
+// for all but the waves at batch boundaries, the search runs once on values
+// that are the same across the wave (scalar loads, no per-lane chain of
+// dependent loads); otherwise every lane searches.
+__device__ __forceinline__ int find_batch_wave(const int64_t *p, int n, int64_t i) {
+  const uint64_t act = __ballot(1);
+  const int first = __builtin_ctzll(act), last = 63 - __builtin_clzll(act);
+  const int64_t lo = read_lane(i, first), hi = read_lane(i, last);
+  int b = 0, top = n;  // invariant p[b] <= lo < p[top]
+  while (top - b > 1) {
+    const int mid = (b + top) >> 1;
+    if (p[mid] <= lo) b = mid; else top = mid;
+  }
+  if (hi < p[b + 1]) return b;
+  return find_batch(p, n, i);
+}
+
 // ---------------------------------------------------------------- local-index table
 // (node u, batch b) -> local index j of u in batch b's node list.  Open
 // addressing with linear probing over 2^bits 64-bit slots; an entry is

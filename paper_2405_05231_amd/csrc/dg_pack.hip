@@ -33,7 +33,7 @@ __global__ __launch_bounds__(THREADS) void k_pack_mark(Lists L, const int32_t *n
                                                        uint64_t *mask, uint32_t *err) {
   int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (i >= L.start[L.B]) return;
-  int b = find_batch(L.start, L.B, i);
+  int b = find_batch_wave(L.start, L.B, i);
   int32_t u = nodes[(int64_t)b * L.stride + (i - L.start[b])];
   if (u < 0 || (int64_t)u >= N) {
     atomicOr(err, ERR_NODE_RANGE);
@@ -72,7 +72,7 @@ __global__ __launch_bounds__(THREADS) void k_build_loc(Lists L, const int32_t *n
                                                        int64_t N, uint32_t *err) {
   const int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (i >= L.start[L.B]) return;
-  const int b = find_batch(L.start, L.B, i);
+  const int b = find_batch_wave(L.start, L.B, i);
   const int64_t at = (int64_t)b * L.stride + (i - L.start[b]);
   const int32_t u = nodes[at];
   if (u < 0 || (int64_t)u >= N) {

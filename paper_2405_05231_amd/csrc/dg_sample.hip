@@ -79,7 +79,7 @@ __global__ __launch_bounds__(THREADS) void k_frontier_degree(
     int64_t *f_off, int64_t *f_deg, int64_t *f_cnt, uint32_t *err) {
   int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (i >= h.ftot) return;
-  int b = find_batch(h.fstart, h.B, i);
+  int b = find_batch_wave(h.fstart, h.B, i);
   int32_t v = nodes[(int64_t)b * node_cap + h.fpos[b] + (i - h.fstart[b])];
   int64_t o0 = 0, d = 0;
   if (v >= 0 && (int64_t)v < N) {
@@ -146,7 +146,7 @@ __global__ __launch_bounds__(THREADS) void k_hop_sample(
   const int64_t i = t / LPN;
   const int sub = (int)(t % LPN);
   if (i >= h.ftot) return;
-  int b = find_batch(h.fstart, h.B, i);
+  int b = find_batch_wave(h.fstart, h.B, i);
   int64_t p = h.fpos[b] + (i - h.fstart[b]);
   int64_t o0 = f_off[i], d = f_deg[i];
   const int64_t first = h.ebase[b] + (f_eoff[i] - estart[b]);  // local index of the 1st edge
@@ -271,7 +271,7 @@ __global__ __launch_bounds__(THREADS) void k_table_insert(Segs L, const int32_t 
                                                           uint32_t *err) {
   int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (i >= L.start[L.B]) return;
-  int b = find_batch(L.start, L.B, i);
+  int b = find_batch_wave(L.start, L.B, i);
   int64_t j = L.seg0[b] + (i - L.start[b]);
   if (!lt_insert(table, nodes[(int64_t)b * node_cap + j], b, j)) atomicOr(err, ERR_INTERNAL);
 }
@@ -282,7 +282,7 @@ __global__ __launch_bounds__(THREADS) void k_relabel(Lists L, int64_t edge_cap, 
                                                      LocalTable table, int64_t N, uint32_t *err) {
   int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (i >= L.start[L.B]) return;
-  int b = find_batch(L.start, L.B, i);
+  int b = find_batch_wave(L.start, L.B, i);
   int64_t e = (int64_t)b * edge_cap + (i - L.start[b]);
   int32_t u = edge_dst[e];
   if (u < 0 || (int64_t)u >= N) return;  // already reported
@@ -302,7 +302,7 @@ __global__ __launch_bounds__(THREADS) void k_relabel_direct(Lists L, int64_t edg
                                                             uint32_t *err) {
   int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (i >= L.start[L.B]) return;
-  int b = find_batch(L.start, L.B, i);
+  int b = find_batch_wave(L.start, L.B, i);
   int64_t e = (int64_t)b * edge_cap + (i - L.start[b]);
   int32_t u = edge_dst[e];
   if (u < 0 || (int64_t)u >= N) return;  // already reported
