@@ -3,16 +3,20 @@
 //
 // Device state: a node-major membership mask visited[u] (bit b = u is in
 // mini-batch b) and its copy prev[u] as of the start of the current hop.  A
-// hop is: degree pass over the frontier -> exclusive scan (edge slots) -> draw
-// + mark (a fire-and-forget atomicOr on visited per sampled edge; a hop that
-// can reach only a small share of the nodes also marks the 8-node lines of the
-// mask it touches) -> compaction of visited & ~prev (the nodes new at this hop) into
-// each batch's new segment, ascending, with no sort; the compaction also brings
-// prev up to date -> one read-back of the hop's counts.  Sampled neighbours are
-// relabelled from global to local IDs at the end, through one of two tables:
-// a direct [N][B] array of local indices that the compaction fills as it
-// assigns them (DG_SAMPLE_DIRECT), or a (node, batch) hash table sized for the
-// group and filled after the last hop.
+// hop is:
+//   degree pass over the frontier -> exclusive scan (edge slots) ->
+//   draw + mark: 1-8 lanes per frontier node, a fire-and-forget atomicOr on
+//     visited per sampled edge; a hop that can reach only a small share of the
+//     nodes also marks the 8-node lines of the mask it touches ->
+//   compaction of visited & ~prev (the nodes new at this hop) into each
+//     batch's new segment, ascending, with no sort; it also brings prev up to
+//     date (the last hop instead clears prev with DG_SAMPLE_EXIT_CLEAR, and
+//     writes the member-lines map when asked) ->
+//   one read-back of the hop's counts.
+// Sampled neighbours are relabelled from global to local IDs at the end,
+// through one of two tables: a direct [N][B] array of local indices that the
+// compaction fills as it assigns them (DG_SAMPLE_DIRECT), or a (node, batch)
+// hash table sized for the group and filled after the last hop.
 #include <string.h>
 
 #include "dg_common.h"
