@@ -137,7 +137,9 @@ extern "C" {
 /* dg_pack_group flags */
 #define DG_PACK_CLEAR_MEMBERSHIP 1u /* on DG_OK, `membership` (required) is left
                                        all-zero: the call clears each word as it
-                                       reads it */
+                                       reads it (with member_lines it reads only
+                                       the words of marked lines, so the others
+                                       must be zero already) */
 #define DG_PACK_ROWS_STREAM 2u      /* enqueue the row copy on `rows_stream`, behind the
                                        tables, and return without waiting for it */
 
