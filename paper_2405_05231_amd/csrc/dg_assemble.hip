@@ -10,7 +10,6 @@ namespace dg {
 namespace {
 
 constexpr int THREADS = 256;
-constexpr int UNROLL = 4;
 
 __device__ __forceinline__ const char *row_source(int32_t l, const char *cache, int64_t cache_rows,
                                                   const char *packed, int64_t packed_rows,
@@ -30,6 +29,7 @@ __global__ __launch_bounds__(THREADS) void k_assemble16(const v4u *cache, int64_
                                                         const v4u *packed, int64_t packed_rows,
                                                         const int32_t *loc, int64_t n, int C,
                                                         v4u *out, int32_t *status) {
+  constexpr int UNROLL = rows_in_flight(CPL);
   constexpr int GPB = THREADS / LPR;  // row groups per block
   const int sub = threadIdx.x % LPR;
   const int64_t grp = (int64_t)blockIdx.x * GPB + threadIdx.x / LPR;
@@ -106,6 +106,7 @@ template <int LPR, int CPL>
 int launch16(const void *cache, int64_t cache_rows, const void *packed, int64_t packed_rows,
              const int32_t *loc, int64_t n, int C, void *out, int32_t *status, hipStream_t s) {
   constexpr int GPB = THREADS / LPR;
+  constexpr int UNROLL = rows_in_flight(CPL);
   int64_t groups = (n + UNROLL - 1) / UNROLL;
   int64_t blocks = (groups + GPB - 1) / GPB;
   if (blocks > (1ll << 20)) blocks = 1ll << 20;

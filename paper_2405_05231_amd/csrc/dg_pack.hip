@@ -19,7 +19,6 @@ namespace dg {
 namespace {
 
 constexpr int THREADS = 256;
-constexpr int UNROLL = 4;
 
 struct Lists {
   int B;
@@ -114,6 +113,7 @@ __global__ __launch_bounds__(THREADS) void k_fanout16(const v4u *X, const int32_
                                                       const int64_t *unc_off, int64_t n_unc,
                                                       int64_t n_pairs, const int64_t *pairdest,
                                                       int C, v4u *packed) {
+  constexpr int UNROLL = rows_in_flight(CPL);
   constexpr int GPB = THREADS / LPR;
   const int sub = threadIdx.x % LPR;
   const int64_t grp = (int64_t)blockIdx.x * GPB + threadIdx.x / LPR;
@@ -187,6 +187,7 @@ template <int LPR, int CPL>
 void launch16(const void *X, const int32_t *ids, const int64_t *off, int64_t n, int64_t pairs,
               const int64_t *dest, int C, void *packed, hipStream_t s) {
   constexpr int GPB = THREADS / LPR;
+  constexpr int UNROLL = rows_in_flight(CPL);
   int64_t groups = (n + UNROLL - 1) / UNROLL;
   int64_t blocks = (groups + GPB - 1) / GPB;
   if (blocks > (1ll << 20)) blocks = 1ll << 20;

@@ -32,6 +32,11 @@ inline bool row_shape16(int64_t C, RowShape *s) {
   return false;  // longer rows: generic path
 }
 
+// Rows in flight per lane group: four for rows of one vector per lane, two
+// when each lane moves two or more vectors of a row (keeps registers, and so
+// occupancy, in check for wide rows).
+__host__ __device__ constexpr int rows_in_flight(int cpl) { return cpl >= 2 ? 2 : 4; }
+
 inline int word_bytes(int64_t row_bytes, std::initializer_list<const void *> ptrs) {
   int w = 16;
   auto fits = [&](int a) {
