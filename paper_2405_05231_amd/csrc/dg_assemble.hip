@@ -153,7 +153,6 @@ extern "C" int dg_assemble_batch(const void *cache, int64_t cache_rows, const vo
       if (sh.lpr == 16) return launch16<16, 1>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, c, out, status, stream);
       if (sh.lpr == 32 && sh.cpl == 1) return launch16<32, 1>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, c, out, status, stream);
       if (sh.lpr == 64 && sh.cpl == 1) return launch16<64, 1>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, c, out, status, stream);
-      if (sh.lpr == 32 && sh.cpl == 3) return launch16<32, 3>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, c, out, status, stream);
       if (sh.lpr == 64 && sh.cpl == 2) return launch16<64, 2>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, c, out, status, stream);
       if (sh.lpr == 64 && sh.cpl == 4) return launch16<64, 4>(cache, cache_rows, packed_b, packed_rows_b, loc_b, n_b, c, out, status, stream);
     }

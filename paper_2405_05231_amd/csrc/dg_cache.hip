@@ -356,7 +356,6 @@ int launch_gather(const void *X, int64_t N, int64_t row_bytes, const int32_t *id
     else if (sh.lpr == 16) gather16<16, 1>(X, N, ids, n, C, out, err, s);
     else if (sh.lpr == 32 && sh.cpl == 1) gather16<32, 1>(X, N, ids, n, C, out, err, s);
     else if (sh.lpr == 64 && sh.cpl == 1) gather16<64, 1>(X, N, ids, n, C, out, err, s);
-    else if (sh.lpr == 32 && sh.cpl == 3) gather16<32, 3>(X, N, ids, n, C, out, err, s);
     else if (sh.lpr == 64 && sh.cpl == 2) gather16<64, 2>(X, N, ids, n, C, out, err, s);
     else gather16<64, 4>(X, N, ids, n, C, out, err, s);
   } else if (w == 16) {

@@ -216,7 +216,6 @@ int launch_fanout(const void *X, const int32_t *ids, const int64_t *off, int64_t
     else if (sh.lpr == 16) launch16<16, 1>(X, ids, off, n, pairs, dest, C, packed, s);
     else if (sh.lpr == 32 && sh.cpl == 1) launch16<32, 1>(X, ids, off, n, pairs, dest, C, packed, s);
     else if (sh.lpr == 64 && sh.cpl == 1) launch16<64, 1>(X, ids, off, n, pairs, dest, C, packed, s);
-    else if (sh.lpr == 32 && sh.cpl == 3) launch16<32, 3>(X, ids, off, n, pairs, dest, C, packed, s);
     else if (sh.lpr == 64 && sh.cpl == 2) launch16<64, 2>(X, ids, off, n, pairs, dest, C, packed, s);
     else launch16<64, 4>(X, ids, off, n, pairs, dest, C, packed, s);
   } else if (w == 16) {

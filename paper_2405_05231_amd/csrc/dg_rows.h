@@ -26,7 +26,6 @@ inline bool row_shape16(int64_t C, RowShape *s) {
   if (C <= 16) { *s = {16, 1}; return true; }
   if (C <= 32) { *s = {32, 1}; return true; }
   if (C <= 64) { *s = {64, 1}; return true; }
-  if (C <= 96) { *s = {32, 3}; return true; }
   if (C <= 128) { *s = {64, 2}; return true; }
   if (C <= 256) { *s = {64, 4}; return true; }
   return false;  // longer rows: generic path
