@@ -95,13 +95,15 @@ def main():
                     help="also run a plain copy of known size (counter calibration)")
     ap.add_argument("--groups", type=int, default=16,
                     help="groups of B mini-batches for --experiment regime")
-    ap.add_argument("--experiment", choices=["pack_ab", "cache", "layered", "minhash", "regime"],
+    ap.add_argument("--experiment",
+                    choices=["pack_ab", "cache", "layered", "minhash", "regime", "ceiling"],
                     default=None,
                     help="instead of the step benchmark: batched vs individual packing "
                          "(pack_ab), access-frequency vs in-degree cache (cache), or "
                          "layer-wise (DGL-style) vs new-node frontier sampling (layered), or "
                          "disk-cache pages touched under ID vs MinHash order (minhash), or "
-                         "the node access distribution over several groups (regime)")
+                         "the node access distribution over several groups (regime), or "
+                         "the rate of plain row copies on this memory system (ceiling)")
     args = ap.parse_args()
     if args.steps < 1 or args.warmup < 0:
         ap.error("--steps must be at least 1 and --warmup at least 0")
@@ -137,6 +139,7 @@ def main():
         out = {"pack_ab": experiment_pack_ab, "cache": experiment_cache,
                "layered": experiment_layered,
                "minhash": experiment_minhash,
+               "ceiling": experiment_ceiling,
                "regime": lambda *a: experiment_regime(*a, groups=args.groups)}[args.experiment](
                    dg, w, cfg, args.steps)
         print(json.dumps(out), flush=True)
@@ -539,6 +542,73 @@ def _popcount64(x):
 # access share of the nodes ranked <1%, 1-5%, 5-10%, >10% by access frequency.
 PAPER_TABLE3 = {"FS": [14.1, 25.5, 18.2, 42.1], "PS": [43.2, 36.5, 11.2, 9.1],
                 "MG": [56.4, 32.3, 7.3, 4.0], "IG": [22.5, 30.0, 20.8, 26.7]}
+
+
+def experiment_ceiling(dg, w, cfg, reps, out_bytes=2 << 30):
+    """What a row copy can reach on this memory system, to read the row
+    kernels' fraction of the 8 TB/s peak against: the library's plain row
+    gather (dg_gather_rows, the same 16-byte row machinery as the fan-out
+    gather and the assembly) of about out_bytes (at least 2M rows) from the
+    workload's feature table,
+    with ids drawn uniformly over the whole table, over the first C rows (the
+    size of the cache table the assembly reads; only with a cache) and in order
+    (a streaming copy); and, for comparison, the runtime's own device-to-device
+    copy (2 * row_bytes * n_rows bytes, like the gathers: each row read once and
+    written once), fill (writes only) and fp32 sum (reads only) of the in-order
+    rows (row_bytes * n_rows bytes each)."""
+    import torch
+    R = cfg.row_bytes
+    N = w.feats.shape[0]
+    C = int(w.cache_nodes.numel())
+    n = min(max(1 << 21, out_bytes // R), N)
+    dev = w.feats.device
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(cfg.seed + 7)
+    cases = {"random_over_table": torch.randint(0, N, (n,), generator=gen, device=dev,
+                                                dtype=torch.int32)}
+    if C > 0:
+        cases["random_over_cache_rows"] = torch.randint(0, min(C, N), (n,), generator=gen,
+                                                        device=dev, dtype=torch.int32)
+    cases["in_order"] = torch.arange(n, dtype=torch.int32, device=dev)
+    out = torch.empty((n, R), dtype=torch.uint8, device=dev)
+    table = w.feats.view(torch.uint8).view(N, R)
+    src = table[:n]  # the in-order rows, for the runtime's copy
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    nbytes = 2 * R * n
+
+    def timed(fn, batch=10):
+        # back-to-back launches between one pair of events, so that the host's
+        # time to issue a call is hidden behind the previous one
+        t = []
+        fn()
+        torch.cuda.synchronize()
+        for _ in range(reps):
+            ev[0].record()
+            for _ in range(batch):
+                fn()
+            ev[1].record()
+            ev[1].synchronize()
+            t.append(ev[0].elapsed_time(ev[1]) / batch)
+        return _median(t)
+
+    res = {}
+    for name, ids in cases.items():
+        ms = timed(lambda: dg.gather_rows(w.feats, ids, out=out))
+        ok = bool(torch.equal(out[:1024], table.index_select(0, ids[:1024].long())))
+        res[name] = {"ms": round(ms, 4), "bytes": nbytes, "GBps": round(nbytes / ms / 1e6, 1),
+                     "checked": ok}
+    ms = timed(lambda: out.copy_(src))
+    res["runtime_device_copy"] = {"ms": round(ms, 4), "bytes": nbytes,
+                                  "GBps": round(nbytes / ms / 1e6, 1)}
+    # the runtime's write-only fill and read-only reduction of the same rows
+    ms = timed(lambda: out.fill_(1))
+    res["runtime_fill"] = {"ms": round(ms, 4), "bytes": R * n, "GBps": round(R * n / ms / 1e6, 1)}
+    words = src.view(torch.float32)  # the rows' bytes as fp32 words: only the read is timed
+    ms = timed(lambda: words.sum())
+    res["runtime_sum"] = {"ms": round(ms, 4), "bytes": R * n, "GBps": round(R * n / ms / 1e6, 1)}
+    return {"experiment": "row copy ceilings (dg_gather_rows and the runtime's copy)",
+            "workload": cfg.name, "row_bytes": R, "rows": n, "table_rows": N, "cache_rows": C,
+            "reps": reps, "peak_GBps": HBM_PEAK_GBPS, "cases": res}
 
 
 def experiment_regime(dg, w, cfg, reps, groups=16):

@@ -35,35 +35,45 @@ __global__ __launch_bounds__(THREADS) void k_assemble16(const v4u *cache, int64_
   const int64_t grp = (int64_t)blockIdx.x * GPB + threadIdx.x / LPR;
   const int64_t ngrp = (int64_t)gridDim.x * GPB;
   for (int64_t j0 = grp * UNROLL; j0 < n; j0 += ngrp * UNROLL) {
+    // Every load below is unconditional, at an address that is always valid,
+    // and what is not needed is discarded afterwards: with no branch between
+    // them, all table entries go out together and then all row vectors.  The
+    // table entry of a position past n is read at n - 1.
+    int32_t l[UNROLL];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) l[u] = loc[j0 + u < n ? j0 + u : n - 1];
+    // Each row's source: the cache table or the packed chunk.  An entry outside
+    // both reads the output row it would write (always allocated) instead, is
+    // written as zeros, and sets status.
     const v4u *src[UNROLL];
+    bool ok[UNROLL];
+    bool bad = false;
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
-      int64_t j = j0 + u;
-      src[u] = nullptr;
-      if (j < n) {
-        int32_t l = loc[j];
-        src[u] = reinterpret_cast<const v4u *>(
-            row_source(l, reinterpret_cast<const char *>(cache), cache_rows,
-                       reinterpret_cast<const char *>(packed), packed_rows, (int64_t)C * 16,
-                       sub == 0 ? status : nullptr));
-      }
+      const int64_t j = j0 + u < n ? j0 + u : n - 1;
+      const bool cached = l[u] < 0;
+      const int64_t r = cached ? -(int64_t)l[u] - 1 : (int64_t)l[u];
+      ok[u] = r < (cached ? cache_rows : packed_rows);
+      bad |= j0 + u < n && !ok[u];
+      src[u] = ok[u] ? (cached ? cache : packed) + r * C : out + j * C;
     }
     v4u v[UNROLL][CPL];
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u)
 #pragma unroll
       for (int c = 0; c < CPL; ++c) {
-        int ch = sub + c * LPR;
-        v[u][c] = (src[u] && ch < C) ? src[u][ch] : v4u{0u, 0u, 0u, 0u};
+        const int ch = sub + c * LPR;
+        v[u][c] = src[u][ch < C ? ch : C - 1];  // a lane past the row reads its last vector
       }
+    if (bad && sub == 0 && status) atomicOr(status, 1);
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
-      int64_t j = j0 + u;
+      const int64_t j = j0 + u;
       if (j < n) {
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
-          int ch = sub + c * LPR;
-          if (ch < C) st_stream(v[u][c], out + j * C + ch);
+          const int ch = sub + c * LPR;
+          if (ch < C) st_stream(ok[u] ? v[u][c] : v4u{0u, 0u, 0u, 0u}, out + j * C + ch);
         }
       }
     }

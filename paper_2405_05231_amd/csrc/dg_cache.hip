@@ -268,16 +268,22 @@ __global__ __launch_bounds__(G_THREADS) void k_gather16(const v4u *X, int64_t N,
   const int64_t grp = (int64_t)blockIdx.x * GPB + threadIdx.x / LPR;
   const int64_t ngrp = (int64_t)gridDim.x * GPB;
   for (int64_t j0 = grp * G_UNROLL; j0 < n; j0 += ngrp * G_UNROLL) {
+    // Unconditional loads at always-valid addresses, as in the assembly
+    // kernel: ids of positions past n are read at n - 1, an id outside [0, N)
+    // reads the output row it would write (its row is written as zeros and
+    // the error flag set), and a lane past the row reads the row's last vector.
+    int32_t id[G_UNROLL];
+#pragma unroll
+    for (int u = 0; u < G_UNROLL; ++u) id[u] = ids[j0 + u < n ? j0 + u : n - 1];
     const v4u *src[G_UNROLL];
+    bool ok[G_UNROLL];
+    bool bad = false;
 #pragma unroll
     for (int u = 0; u < G_UNROLL; ++u) {
-      const int64_t j = j0 + u;
-      src[u] = nullptr;
-      if (j < n) {
-        const int32_t id = ids[j];
-        if (id >= 0 && (int64_t)id < N) src[u] = X + (int64_t)id * C;
-        else if (sub == 0 && err) atomicOr(err, ERR_NODE_RANGE);
-      }
+      const int64_t j = j0 + u < n ? j0 + u : n - 1;
+      ok[u] = id[u] >= 0 && (int64_t)id[u] < N;
+      bad |= j0 + u < n && !ok[u];
+      src[u] = ok[u] ? X + (int64_t)id[u] * C : out + j * C;
     }
     v4u v[G_UNROLL][CPL];
 #pragma unroll
@@ -285,8 +291,9 @@ __global__ __launch_bounds__(G_THREADS) void k_gather16(const v4u *X, int64_t N,
 #pragma unroll
       for (int c = 0; c < CPL; ++c) {
         const int ch = sub + c * LPR;
-        v[u][c] = (src[u] && ch < C) ? ld_stream(src[u] + ch) : v4u{0u, 0u, 0u, 0u};
+        v[u][c] = ld_stream(src[u] + (ch < C ? ch : C - 1));
       }
+    if (bad && sub == 0 && err) atomicOr(err, ERR_NODE_RANGE);
 #pragma unroll
     for (int u = 0; u < G_UNROLL; ++u) {
       const int64_t j = j0 + u;
@@ -294,7 +301,7 @@ __global__ __launch_bounds__(G_THREADS) void k_gather16(const v4u *X, int64_t N,
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
           const int ch = sub + c * LPR;
-          if (ch < C) st_stream(v[u][c], out + j * C + ch);
+          if (ch < C) st_stream(ok[u] ? v[u][c] : v4u{0u, 0u, 0u, 0u}, out + j * C + ch);
         }
       }
     }
