@@ -173,3 +173,34 @@ def test_assemble_batches_bad_address_flags(dg):
     assert torch.equal(outs[1][0], packed[4]) and torch.equal(outs[1][1], cache[1])
     assert torch.equal(outs[1][2], packed[3])
 
+
+
+@pytest.mark.parametrize("R", [64, 512, 1536, 2048, 4096])
+def test_assemble_bad_entries_every_row_shape(dg, R):
+    """Every launch shape of the 16-byte path (one to four vectors per lane,
+    the last one partly used at 1536 bytes), over several lane groups and a
+    ragged tail: entries outside both tables, the int32 limits among them, are
+    flagged and their rows zeroed; every other row is the addressed one."""
+    g = torch.Generator().manual_seed(R)
+    n_cache, n_packed, n = 40, 30, 1003
+    cache = torch.randint(0, 256, (n_cache, R), generator=g, dtype=torch.int32).to(torch.uint8)
+    packed = torch.randint(0, 256, (n_packed, R), generator=g, dtype=torch.int32).to(torch.uint8)
+    loc = torch.randint(-n_cache, n_packed, (n,), generator=g, dtype=torch.int32)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    out = dg.assemble_batch(cache.to(DEV), packed.to(DEV), loc.to(DEV), R, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    want = torch.where((loc < 0).unsqueeze(1), cache[(-loc - 1).clamp(min=0).long()],
+                       packed[loc.clamp(min=0).long()])
+    assert torch.equal(out.cpu(), want)
+    for p, v in [(0, -n_cache - 1), (5, n_packed), (6, 2**31 - 1), (7, -2**31), (500, 31),
+                 (n - 1, -1000)]:
+        loc[p] = v
+    bad = torch.zeros(n, dtype=torch.bool)
+    bad[[0, 5, 6, 7, 500, n - 1]] = True
+    out = dg.assemble_batch(cache.to(DEV), packed.to(DEV), loc.to(DEV), R, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 1
+    got = out.cpu()
+    assert int(got[bad].to(torch.int64).sum()) == 0
+    assert torch.equal(got[~bad], want[~bad])

@@ -102,6 +102,30 @@ def test_gather_rows_bad_id_flags_and_zeroes(dg):
     assert int(y[1].sum()) == 0 and int(y[2].sum()) == 0 and int(y[0].sum()) > 0
 
 
+@pytest.mark.parametrize("dim", [16, 128, 384, 512, 1024])
+def test_gather_rows_bad_ids_every_row_shape(dg, dim):
+    """Each launch shape of the 16-byte row gather (fp32 rows of 64 B to 4 KiB),
+    over several lane groups and a ragged tail, with ids outside [0, N) at the
+    first and last positions and at the int32 limits: those rows are zeroed and
+    flagged, every other row is X[id]."""
+    gen = torch.Generator().manual_seed(dim)
+    N, n = 500, 1003
+    X = torch.randn((N, dim), generator=gen).to(DEV)
+    ids = torch.randint(0, N, (n,), generator=gen, dtype=torch.int32)
+    bad = torch.zeros(n, dtype=torch.bool)
+    for p, v in [(0, -1), (9, N), (10, 2**31 - 1), (11, -2**31), (n - 1, N + 7)]:
+        ids[p] = v
+        bad[p] = True
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    y = dg.gather_rows(X, ids.to(DEV), status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 1
+    got = y.cpu()
+    ref = X.cpu().index_select(0, ids.clamp(0, N - 1).long()).view(torch.uint8).reshape(n, -1)
+    assert int(got[bad].to(torch.int64).sum()) == 0
+    assert torch.equal(got[~bad], ref[~bad])
+
+
 def random_perms(k, B, seed):
     g = torch.Generator().manual_seed(seed)
     return torch.stack([torch.randperm(B, generator=g) for _ in range(k)]).to(torch.int32)
