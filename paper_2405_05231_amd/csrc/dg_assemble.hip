@@ -42,6 +42,9 @@ __global__ __launch_bounds__(THREADS) void k_assemble16(const v4u *cache, int64_
     int32_t l[UNROLL];
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) l[u] = loc[j0 + u < n ? j0 + u : n - 1];
+    // scheduling fence (no instruction): no use of an entry is placed between
+    // the entry loads, which would make the first one wait alone
+    __builtin_amdgcn_sched_barrier(0);
     // Each row's source: the cache table or the packed chunk.  An entry outside
     // both reads the output row it would write (always allocated) instead, is
     // written as zeros, and sets status.

@@ -182,7 +182,7 @@ CASES = [
     (100, 99, 2, 4, [99, 99], 4, torch.float32, 0.0),          # f = d on full rows
     (2, 1, 2, 1, [1, 1, 1], 4, torch.float32, 0.0),            # tiny graph, cycles
     (64, 0, 3, 5, [3, 3], 4, torch.float32, 0.0),              # no edges at all
-    (600, 20, 4, 8, [6, 6], 768, torch.float16, 0.1),          # 1536-byte rows (3 vectors/lane)
+    (600, 20, 4, 8, [6, 6], 768, torch.float16, 0.1),          # 1536-byte rows (2 vectors/lane, 2nd half used)
     (600, 20, 4, 8, [6, 6], 512, torch.float32, 0.1),          # 2048-byte rows (2 vectors/lane)
     (600, 20, 4, 8, [6, 6], 1024, torch.float32, 0.1),         # 4096-byte rows (4 vectors/lane)
 ]
