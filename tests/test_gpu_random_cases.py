@@ -11,6 +11,8 @@
    that hops fall on both sides of the touched-marks limit): every group's
    outputs must equal those of independent calls without the flags, and
    packing must leave the mask all-zero.
+3. Frequency-ranked cache selection and the MinHash disk-cache order on random
+   small groups, bit-exact against the oracle.
 
 Each case is fixed by its index, so a failure names a reproducible
 configuration."""
@@ -153,3 +155,53 @@ def test_random_group_loop_with_flags(dg, case):
         assert int(mem.count_nonzero()) == 0, g
         pr_f = dg.pack_group(feats, slot, sr_f.nodes, counts, with_unique=True, membership=mem_f)
         same_pack(pr, pr_f, counts)
+
+
+N_NEXT_CASES = 30
+
+
+def small_sampled(dg, case):
+    """A random small graph and group, sampled on the device with the
+    membership words kept; returns (n, B, mem, the batches' node lists, rnd)."""
+    rnd = random.Random(12000 + case)
+    n = rnd.choice([3, 40, 300, 2000])
+    maxdeg = rnd.randint(0, min(n - 1, 30))
+    B = rnd.choice([1, 3, 32, 33, 64])
+    S = rnd.randint(1, min(n, 20))
+    fan = [rnd.choice([-1, 1, 3, 8, 20]) for _ in range(rnd.randint(1, 3))]
+    off, idx = (random_case(rnd, n, maxdeg) if maxdeg else
+                (torch.zeros(n + 1, dtype=torch.int64), torch.zeros(0, dtype=torch.int32)))
+    seeds = torch.tensor([rnd.sample(range(n), S) for _ in range(B)], dtype=torch.int32)
+    mem = torch.empty(n, dtype=torch.int64, device=DEV)
+    sr = dg.sample_group(off.to(DEV), idx.to(DEV), seeds.to(DEV), fan, 55 + case,
+                         membership=mem, layered=rnd.random() < 0.3)
+    lists = [sr.batch_nodes(b).cpu().numpy() for b in range(B)]
+    return n, B, mem, lists, rnd
+
+
+@pytest.mark.parametrize("case", range(N_NEXT_CASES))
+def test_random_cache_by_frequency(dg, orc, case):
+    n, B, mem, lists, rnd = small_sampled(dg, case)
+    for C in sorted({0, 1, rnd.randint(0, n), n // 2, n}):
+        print(f"cache case {case}: n={n} B={B} C={C}", flush=True)
+        slot, nodes, cached = dg.cache_by_frequency(mem, B, C)
+        r_slot, r_nodes, r_cached = orc.cache_by_frequency(n, lists, C)
+        assert cached == r_cached, C
+        assert np.array_equal(slot.cpu().numpy(), r_slot), C
+        assert np.array_equal(nodes.cpu().numpy(), r_nodes), C
+
+
+@pytest.mark.parametrize("case", range(N_NEXT_CASES))
+def test_random_minhash_order(dg, orc, case):
+    n, B, mem, lists, rnd = small_sampled(dg, case)
+    k = rnd.choice([1, 2, 5])
+    # disk-cache entries: a random subset of all nodes, accessed or not, in random order
+    m = rnd.randint(1, n)
+    entries = torch.tensor(rnd.sample(range(n), m), dtype=torch.int32, device=DEV)
+    g = torch.Generator().manual_seed(case)
+    perms = torch.stack([torch.randperm(B, generator=g) for _ in range(k)]).to(torch.int32)
+    print(f"minhash case {case}: n={n} B={B} k={k} m={m}", flush=True)
+    order, sig = dg.minhash_order(mem, B, entries, perms.to(DEV))
+    r_order, r_sig = orc.minhash_order(n, lists, entries.cpu().numpy(), perms.numpy())
+    assert np.array_equal(sig.cpu().numpy(), r_sig)
+    assert np.array_equal(order.cpu().numpy(), r_order)
