@@ -95,3 +95,54 @@ def test_pipelined_steps_are_each_correct(dg):
             n = int(counts[b])
             ref = w.feats.index_select(0, nodes[b, :n].long()).view(torch.uint8).reshape(n, R)
             assert torch.equal(kept[k][b][:n], ref), (k, b)
+
+
+def test_two_host_threads_at_once(dg):
+    """The library keeps host state per thread only (error text, side streams,
+    events, staging): two host threads, each with its own stream, workspaces
+    and membership buffer, sample and pack different groups at the same time
+    (ctypes releases the interpreter lock during each call), and every result
+    equals that of the same group run alone."""
+    import threading
+
+    from test_gpu_clear import same_pack, same_sample
+    w = synth.make_workload("M1", device=DEV)
+    cfg = w.cfg
+    fan, B = list(cfg.fanouts), cfg.B
+    groups = [synth.seed_batches(cfg.n, B, cfg.S, cfg.seed + 300 + k, DEV, offsets=w.offsets)
+              for k in range(4)]
+    refs = []
+    for k, g in enumerate(groups):
+        sr = dg.sample_group(w.offsets, w.indices, g, fan, w.rng_seed, batch_base=k * B,
+                             direct=True)
+        pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, sr.node_count, with_unique=True)
+        refs.append((sr, pr))
+    torch.cuda.synchronize()
+    results, errors = [None] * len(groups), []
+
+    def worker(ks):
+        try:
+            s = torch.cuda.Stream(device=DEV)
+            with torch.cuda.stream(s):
+                for k in ks:
+                    mem = torch.empty(cfg.n, dtype=torch.int64, device=DEV)
+                    sr = dg.sample_group(w.offsets, w.indices, groups[k], fan, w.rng_seed,
+                                         batch_base=k * B, membership=mem, direct=True,
+                                         stream=s)
+                    pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, sr.node_count,
+                                       with_unique=True, membership=mem, stream=s)
+                    results[k] = (sr, pr)
+            s.synchronize()
+        except Exception as e:  # reported by the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(ks,)) for ks in ([0, 2], [1, 3])]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=100)
+    assert not any(t.is_alive() for t in threads)
+    assert not errors, errors
+    for k, (sr, pr) in enumerate(results):
+        same_sample(sr, refs[k][0])
+        same_pack(pr, refs[k][1], sr.node_count)
