@@ -1,5 +1,5 @@
 """Host-side pieces of bench.py (no GPU): the multi-GPU refusal, the popcount
-used by the regime check, and the traffic digest."""
+used by the regime check, the traffic digest and the CPU baseline leg."""
 import os
 import random
 import subprocess
@@ -43,3 +43,16 @@ def test_traffic_digest_covers_the_kernel_translation_unit(tmp_path, monkeypatch
     assert bench.kernel_source_digest(kernel) == d
     (fake / main).write_bytes(b"// changed\n" + (fake / main).read_bytes())
     assert bench.kernel_source_digest(kernel) != d
+
+
+def test_cpu_baseline_runs_two_groups_on_the_host():
+    """The CPU baseline leg (the oracle on the host) on the tiny workload: two
+    consecutive groups, the first of which is the benchmark's own."""
+    import synth
+    w = synth.make_workload("T")
+    cfg = w.cfg
+    r = bench.cpu_baseline(w, cfg, cfg.B, groups=2)
+    assert r["kind"] == "oracle" and r["cores"] == 1 and r["unit"] == "GB/s"
+    assert r["value"] > 0 and r["sampled_edges_per_s"] > 0
+    assert "2 consecutive groups" in r["sample"]
+    assert set(r["seconds"]) == {"sample", "pack", "assemble"}
