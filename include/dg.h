@@ -349,7 +349,9 @@ int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
  *   loc_b      [n_b] int32;  out [n_b*row_bytes].
  *   status     optional device int32: on an entry of loc_b outside
  *              [-cache_rows, packed_rows_b) the kernel writes a zero row and ORs
- *              bit 1 into *status (no access outside the given buffers).
+ *              1 (bit 0) into *status.  It reads no table row for such an entry
+ *              (only the out row it then overwrites), so no access falls outside
+ *              the given buffers.
  * Asynchronous on `stream`.  Returns DG_EINVAL for null pointers (other than
  * cache with cache_rows = 0 and status), n_b < 0, row_bytes < 1, or buffers that
  * overlap; n_b = 0 is a no-op. */
@@ -405,8 +407,9 @@ int dg_cache_by_frequency(const uint64_t *membership, int64_t N, int32_t B, int6
  * paper fills its caches by batched packing, treating each cache as one more
  * mini-batch, §5.2), and, called once per mini-batch over that batch's
  * packed_ids, performs the individual packing of §5.2 (Fig. 6a) that batched
- * packing replaces.  An id outside [0, N) writes a zero row and ORs bit 0
- * into the optional device int32 *status.  Asynchronous on `stream`.
+ * packing replaces.  An id outside [0, N) writes a zero row and ORs 1 (bit 0)
+ * into the optional device int32 *status; it reads no row of feats (only the
+ * out row it then overwrites).  Asynchronous on `stream`.
  * DG_EINVAL for bad sizes, null pointers or an output overlapping an input. */
 int dg_gather_rows(const void *feats, int64_t N, int64_t row_bytes, const int32_t *ids,
                    int64_t n, void *out, int32_t *status, hipStream_t stream);
