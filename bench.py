@@ -497,12 +497,12 @@ def experiment_layered(dg, w, cfg, reps):
     res = {}
     for name, layered in (("new_nodes", False), ("layered", True)):
         sr = dg.sample_group(w.offsets, w.indices, w.seeds, list(cfg.fanouts), w.rng_seed,
-                             layered=layered)
+                             layered=layered, direct=True)
         ts = []
         for _ in range(reps + 1):
             t0 = time.perf_counter()
             dg.sample_group(w.offsets, w.indices, w.seeds, list(cfg.fanouts), w.rng_seed,
-                            out=sr, layered=layered)
+                            out=sr, layered=layered, direct=True)
             ts.append(time.perf_counter() - t0)
         t = _median(ts[1:])
         res[name] = {"ms": round(1e3 * t, 3), "edges": sr.sizes["total_edges"],
