@@ -19,6 +19,8 @@
 // hash table sized for the group and filled after the last hop.
 #include <string.h>
 
+#include <type_traits>
+
 #include "dg_common.h"
 
 namespace dg {
@@ -134,14 +136,16 @@ __device__ __forceinline__ void emit_chunk(const int32_t (&u)[EMIT], const int64
 // LPN lanes per frontier node (LPN = 1, 2, 4 or 8; more lanes when the
 // frontier is small, so that short hops still keep enough loads in flight).
 // Floyd's subset is built in registers (fully unrolled, so the arrays stay in
-// VGPRs), by every lane of the node; each drawn position's rank among the f
+// VGPRs) when f <= FM, by every lane of the node; FM (8, 16 or 32) is the
+// smallest capacity that holds the hop's fan-out, since the arrays' registers
+// bound the waves per SIMD and so the loads in flight; each drawn position's rank among the f
 // positions gives its slot, so no sort is needed, and lane `sub` takes the
 // draws s with s mod LPN = sub.  Neighbour loads and membership atomics are
 // issued EMIT at a time so their latencies overlap.  estart[b] = f_eoff at
 // batch b's first frontier entry (written on the device by k_batch_bounds).  A
 // node whose edges would pass edge_cap writes nothing; the host sees the
 // overflow in the edge counts and reports it.
-template <int LPN>
+template <int LPN, int FM>
 __global__ __launch_bounds__(THREADS) void k_hop_sample(
     Hop h, const int32_t *nodes, int64_t node_cap, const int32_t *idx, const int64_t *f_off,
     const int64_t *f_deg, const int64_t *f_eoff, const int64_t *estart, int64_t edge_cap,
@@ -183,10 +187,10 @@ __global__ __launch_bounds__(THREADS) void k_hop_sample(
     if (sub == 0) atomicOr(err, ERR_CSR);
     return;
   }
-  if (f <= FMAX) {
-    uint32_t r[FMAX];
+  if (f <= FM) {
+    uint32_t r[FM];
 #pragma unroll
-    for (int s = 0; s < FMAX; ++s) {
+    for (int s = 0; s < FM; ++s) {
       r[s] = 0xffffffffu;
       if (s < f) {
         uint32_t j = (uint32_t)(d - f + s);
@@ -200,7 +204,7 @@ __global__ __launch_bounds__(THREADS) void k_hop_sample(
     }
     // this lane's draws: s = j*LPN + sub for j = 0, 1, ... (a static j, so the
     // register arrays are indexed by constants only)
-    constexpr int SPL = FMAX / LPN;
+    constexpr int SPL = FM / LPN;
     uint32_t rv[SPL];
 #pragma unroll
     for (int j = 0; j < SPL; ++j) {
@@ -220,7 +224,7 @@ __global__ __launch_bounds__(THREADS) void k_hop_sample(
           const uint32_t x = j < SPL ? rv[j] : 0xffffffffu;
           int rank = 0;
 #pragma unroll
-          for (int m = 0; m < FMAX; ++m) rank += (m < f && r[m] < x) ? 1 : 0;
+          for (int m = 0; m < FM; ++m) rank += (m < f && r[m] < x) ? 1 : 0;
           slot[k] = base + rank;
           u[k] = mine ? idx[o0 + x] : 0;
           n += mine ? 1 : 0;
@@ -542,22 +546,24 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       while (lpn < 8 && h.ftot * lpn < (1 << 20) && (f < 0 || (f <= FMAX && 2 * lpn <= f)))
         lpn *= 2;
       const dim3 hg(blocks_for(h.ftot * lpn)), hb(THREADS);
-      if (lpn == 8)
-        hipLaunchKernelGGL(k_hop_sample<8>, hg, hb, 0, s, h, nodes, node_cap, g->indices, w.f_off,
-                           w.f_deg, w.f_eoff, w.small + ST_BOUNDS, edge_cap, edge_src, edge_dst,
-                           w.visited, N, w.err);
-      else if (lpn == 4)
-        hipLaunchKernelGGL(k_hop_sample<4>, hg, hb, 0, s, h, nodes, node_cap, g->indices, w.f_off,
-                           w.f_deg, w.f_eoff, w.small + ST_BOUNDS, edge_cap, edge_src, edge_dst,
-                           w.visited, N, w.err);
-      else if (lpn == 2)
-        hipLaunchKernelGGL(k_hop_sample<2>, hg, hb, 0, s, h, nodes, node_cap, g->indices, w.f_off,
-                           w.f_deg, w.f_eoff, w.small + ST_BOUNDS, edge_cap, edge_src, edge_dst,
-                           w.visited, N, w.err);
-      else
-        hipLaunchKernelGGL(k_hop_sample<1>, hg, hb, 0, s, h, nodes, node_cap, g->indices, w.f_off,
-                           w.f_deg, w.f_eoff, w.small + ST_BOUNDS, edge_cap, edge_src, edge_dst,
-                           w.visited, N, w.err);
+      // register-path capacity: the smallest that holds f (8 when f does not
+      // take the register path at all)
+      const int fm = (f < 0 || f > FMAX || f <= 8) ? 8 : (f <= 16 ? 16 : 32);
+      auto launch = [&](auto lpn_c, auto fm_c) {
+        hipLaunchKernelGGL((k_hop_sample<decltype(lpn_c)::value, decltype(fm_c)::value>), hg, hb,
+                           0, s, h, nodes, node_cap, g->indices, w.f_off, w.f_deg, w.f_eoff,
+                           w.small + ST_BOUNDS, edge_cap, edge_src, edge_dst, w.visited, N,
+                           w.err);
+      };
+      auto launch_fm = [&](auto lpn_c) {
+        if (fm == 8) launch(lpn_c, std::integral_constant<int, 8>());
+        else if (fm == 16) launch(lpn_c, std::integral_constant<int, 16>());
+        else launch(lpn_c, std::integral_constant<int, 32>());
+      };
+      if (lpn == 8) launch_fm(std::integral_constant<int, 8>());
+      else if (lpn == 4) launch_fm(std::integral_constant<int, 4>());
+      else if (lpn == 2) launch_fm(std::integral_constant<int, 2>());
+      else launch_fm(std::integral_constant<int, 1>());
       DG_HIP(hipGetLastError());
       const int ev1 = tm.mark();
       // new nodes of this hop, per batch, ascending; the write pass needs only
