@@ -73,6 +73,8 @@ def main():
     ap.add_argument("--cpu-batches", type=int, default=0,
                     help="mini-batches in the CPU-oracle sample (0 = the whole group)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the row-copy ceiling measured after the timed regions")
     ap.add_argument("--no-pipeline", action="store_true",
                     help="time the serial region only (value = the serial rate)")
     ap.add_argument("--timed-pack", action="store_true",
@@ -384,6 +386,17 @@ def main():
         torch.cuda.synchronize()
         del a, b
 
+    if not args.no_ceiling:
+        # what a plain copy of rows reaches on this machine, outside the timed
+        # regions: the row kernels' fraction of 8 TB/s is read against it
+        c = experiment_ceiling(dg, w, cfg, 3)
+        out["row_copy_ceiling"] = {
+            "kind": "dg_gather_rows of 2 GiB of this workload's rows, same process",
+            "unit": "GB/s",
+            "random_rows": c["cases"]["random_over_table"]["GBps"],
+            "in_order": c["cases"]["in_order"]["GBps"],
+            "assembly_achieved_over_in_order": round(
+                out["roofline"]["achieved"] / c["cases"]["in_order"]["GBps"], 3)}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, cfg, args.cpu_batches or cfg.B)
     print(json.dumps(out), flush=True)
