@@ -244,8 +244,12 @@ __device__ __forceinline__ uint32_t rank_below(uint64_t set, uint32_t base) {
 // that follow (a wait there would also wait for those stores).
 __device__ __forceinline__ void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
+// Eight waves per SIMD: the pass is latency-bound under load, and with the
+// prev words read in two halves it fits in 64 VGPRs (a few spill to scratch);
+// without the hint it takes 72 and runs seven.
 template <bool SAMPLE>
-__global__ __launch_bounds__(MC_THREADS) void k_mask_count(MaskScan a) {
+__global__ __launch_bounds__(MC_THREADS) __attribute__((amdgpu_waves_per_eu(8, 8)))
+void k_mask_count(MaskScan a) {
   __shared__ uint32_t s_cnt[MC_WAVES][DG_MAX_BATCHES + 4];
   __shared__ __align__(16) uint32_t s_w[MC_WAVES][2][MC_CWORDS];
   const int lane = lane_id();
@@ -322,19 +326,29 @@ __global__ __launch_bounds__(MC_THREADS) void k_mask_count(MaskScan a) {
 #pragma unroll
   for (int r = 0; r < MC_ROUNDS; ++r) cmask[r] = 0ull;
   if (SAMPLE) {
+    // prev words in two halves of the rounds: half the registers (so more
+    // waves per SIMD) for one more round trip
     uint64_t *pv = a.prev + t0;
-    uint64_t p[MC_ROUNDS];
+    constexpr int H = MC_ROUNDS / 2;
 #pragma unroll
-    for (int r = 0; r < MC_ROUNDS; ++r) p[r] = (any[r] && m[r] != 0ull) ? pv[r * 64 + lane] : 0ull;
-    wait_vm_all();
+    for (int h0 = 0; h0 < MC_ROUNDS; h0 += H) {
+      uint64_t p[H];
 #pragma unroll
-    for (int r = 0; r < MC_ROUNDS; ++r) {
-      if (!any[r]) continue;
-      const uint64_t nw = m[r] & ~p[r];
-      if (a.keep_prev && nw != 0ull) pv[r * 64 + lane] = p[r] | nw;
-      if (a.clear_prev && p[r] != 0ull) pv[r * 64 + lane] = 0ull;
-      m[r] = nw;
-      any[r] = __ballot(nw != 0ull);
+      for (int q = 0; q < H; ++q) {
+        const int r = h0 + q;
+        p[q] = (any[r] && m[r] != 0ull) ? pv[r * 64 + lane] : 0ull;
+      }
+      wait_vm_all();
+#pragma unroll
+      for (int q = 0; q < H; ++q) {
+        const int r = h0 + q;
+        if (!any[r]) continue;
+        const uint64_t nw = m[r] & ~p[q];
+        if (a.keep_prev && nw != 0ull) pv[r * 64 + lane] = p[q] | nw;
+        if (a.clear_prev && p[q] != 0ull) pv[r * 64 + lane] = 0ull;
+        m[r] = nw;
+        any[r] = __ballot(nw != 0ull);
+      }
     }
   } else if (a.cache_slot) {
     const int32_t *cs = a.cache_slot + t0;
