@@ -73,6 +73,9 @@ def main():
     ap.add_argument("--cpu-batches", type=int, default=0,
                     help="mini-batches in the CPU-oracle sample (0 = the whole group)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sample-timing", action="store_true",
+                    help="time the sampling call's phases (draw, compaction, relabelling) with "
+                         "the library's HIP events in both regions and report their medians")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the row-copy ceiling measured after the timed regions")
     ap.add_argument("--no-pipeline", action="store_true",
@@ -226,6 +229,7 @@ def main():
     # packing's count pass reads only those lines
     lines = (None if args.no_member_lines else
              torch.empty(dg.member_lines_bytes(cfg.n), dtype=torch.uint8, device=dev))
+    samp_phases = {False: [], True: []}  # per region, with --sample-timing
 
     def run(K, pipelined, record):
         marks, gather_ms, asm_ms = [], [], []
@@ -239,7 +243,9 @@ def main():
             s_out = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, out=sr,
                                     workspace=ws_s, membership=mem, direct=True, stream=stream,
                                     exit_clear=clearing, entry_clear=entry_clear,
-                                    member_lines=lines)
+                                    member_lines=lines, timing=args.sample_timing)
+            if args.sample_timing:
+                samp_phases[pipelined].append(dict(s_out.timing))
             t1 = time.perf_counter()
             stream.wait_event(asm_done[slot])  # the assembly that last read pr2[slot]
             rows_async = pipelined and not args.rows_inline and not args.timed_pack
@@ -386,6 +392,13 @@ def main():
         torch.cuda.synchronize()
         del a, b
 
+    if args.sample_timing:
+        keys = ("sample_ms", "dedup_ms", "relabel_ms", "total_ms")
+        out["sampling_phases_ms"] = {
+            name: {k.replace("_ms", ""): round(_median([t[k] for t in v[-args.steps:]]), 3)
+                   for k in keys}
+            for name, v in (("serial", samp_phases[False]), ("pipelined", samp_phases[True]))
+            if v}
     if not args.no_ceiling:
         # what a plain copy of rows reaches on this machine, outside the timed
         # regions: the row kernels' fraction of 8 TB/s is read against it
