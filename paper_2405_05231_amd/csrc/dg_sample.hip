@@ -528,8 +528,13 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       // A hop whose edges can reach at most N/16 nodes marks the mask lines it
       // touches (a byte store per edge), and its count pass reads only those.
       // On larger hops the stores cost more time than the lines they spare.
+      // The last hop never marks when the call must write the member-lines map
+      // or leave prev clear: its count pass then reads every word anyway and
+      // does both on the way, where marks would need a pass over the whole mask
+      // for the map and a fill of prev afterwards.
       const int64_t ebound = f < 0 ? E : h.ftot * (int64_t)f;
-      h.touched = ebound <= N / 16 ? w.touched : nullptr;
+      const bool full_last = k == K && (member_lines || exit_clear);
+      h.touched = (ebound <= N / 16 && !full_last) ? w.touched : nullptr;
       if (h.touched && (rc = fill_u64(reinterpret_cast<uint64_t *>(w.touched),
                                       (size_t)mc_touch_bytes(N) / 8, 0, s)))
         return rc;

@@ -46,9 +46,12 @@ def same_pack(a, b, counts):
         assert torch.equal(a.loc[bb, :int(n)], b.loc[bb, :int(n)]), bb
 
 
-def sparse_graph():
+def sparse_graph(fan=(3, 3, 2)):
     """200k nodes, degrees 0..6, 4 batches of 16 seeds: every hop is small
-    enough to use touched marks, so the sampler clears its state with a fill."""
+    enough to use touched marks, except that the last one reads every word when
+    the call asks for the member-lines map or a clear exit.  With a last
+    fan-out of 0 the last hop runs no count pass, and the sampler writes the map
+    with a pass of its own and clears its state with a fill."""
     n = 200_000
     off, idx = synth.uniform_graph(n, 0, 6, seed=31)
     rnd = random.Random(99)
@@ -59,7 +62,7 @@ def sparse_graph():
     seeds = [torch.tensor([rnd.sample(range(n), 16) for _ in range(4)], dtype=torch.int32,
                           device=DEV) for _ in range(3)]
     return (torch.from_numpy(off).to(DEV), torch.from_numpy(idx).to(DEV), feats, slot.to(DEV),
-            seeds, [3, 3, 2], 1234)
+            seeds, list(fan), 1234)
 
 
 def workload_groups(name):
@@ -70,11 +73,19 @@ def workload_groups(name):
     return w.offsets, w.indices, w.feats, w.cache_slot, seeds, list(cfg.fanouts), w.rng_seed
 
 
+def case_inputs(case):
+    if case == "sparse":
+        return sparse_graph()
+    if case == "sparse_f0":
+        return sparse_graph((3, 3, 0))
+    return workload_groups(case)
+
+
 @pytest.mark.parametrize("case,layered,direct", [("M1", False, True), ("M1", False, False),
-                                                 ("M1", True, True), ("sparse", False, True)])
+                                                 ("M1", True, True), ("sparse", False, True),
+                                                 ("sparse_f0", False, True)])
 def test_group_loop_with_clear_flags(dg, case, layered, direct):
-    off, idx, feats, slot, groups, fan, rng = (sparse_graph() if case == "sparse"
-                                               else workload_groups(case))
+    off, idx, feats, slot, groups, fan, rng = case_inputs(case)
     N = off.numel() - 1
     B, S = groups[0].shape
     node_cap, edge_cap = dg.sample_bounds(N, idx.numel(), S, fan, layered)
@@ -116,14 +127,14 @@ def lines_ref(dg, mem):
 
 
 @pytest.mark.parametrize("case,layered,direct", [("M1", False, True), ("M1", True, False),
-                                                 ("sparse", False, True)])
+                                                 ("sparse", False, True),
+                                                 ("sparse_f0", False, True)])
 def test_member_lines(dg, case, layered, direct):
-    """The map sampling writes (by its last count pass on M1, by a pass of its
-    own when every hop uses touched marks) marks exactly the 8-node lines that
-    hold a member; packing with it gives the outputs of packing without it, and
-    a map that misses a member line is reported."""
-    off, idx, feats, slot, groups, fan, rng = (sparse_graph() if case == "sparse"
-                                               else workload_groups(case))
+    """The map sampling writes (by its last count pass, or by a pass of its own
+    when the last hop runs none) marks exactly the 8-node lines that hold a
+    member; packing with it gives the outputs of packing without it, and a map
+    that misses a member line is reported."""
+    off, idx, feats, slot, groups, fan, rng = case_inputs(case)
     N = off.numel() - 1
     seeds = groups[0]
     B = seeds.shape[0]
