@@ -27,22 +27,34 @@ I32P = ctypes.POINTER(ctypes.c_int32)
 VP = ctypes.c_void_p
 
 
+# A test may load another build of the oracle (a sanitizer build, or a copy with
+# a planted mistake) by naming its shared library here.
+LIB_ENV = "DG_ORACLE_LIB"
+
+
+def compile_oracle(out: str, src: str = _SRC, extra=()) -> str:
+    """gcc build of an oracle source into the shared library `out`."""
+    tmp = out + ".tmp"
+    subprocess.run(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-Wall", "-Werror", *extra,
+                    src, "-o", tmp], check=True)
+    os.replace(tmp, out)
+    return out
+
+
 def build(force: bool = True) -> str:
     """Compile oracle.c into liboracle.so with gcc (no GPU code involved)."""
     if force or not os.path.exists(_LIB_PATH):
-        tmp = _LIB_PATH + ".tmp"
-        subprocess.run(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-Wall", "-Werror",
-                        _SRC, "-o", tmp], check=True)
-        os.replace(tmp, _LIB_PATH)
+        compile_oracle(_LIB_PATH)
     return _LIB_PATH
 
 
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB_PATH):
+        path = os.environ.get(LIB_ENV) or _LIB_PATH
+        if path == _LIB_PATH and not os.path.exists(_LIB_PATH):
             build()
-        L = ctypes.CDLL(_LIB_PATH)
+        L = ctypes.CDLL(path)
         L.or_mix64.restype = ctypes.c_uint64
         L.or_mix64.argtypes = [ctypes.c_uint64]
         L.or_splitmix_nth.restype = ctypes.c_uint64
@@ -121,9 +133,47 @@ def sample_bounds(N: int, E: int, S: int, fanouts, layered=False) -> tuple[int, 
     return n, (e if layered else min(e, E))
 
 
-def sample_group(offsets, indices, seeds, fanouts, rng_seed, batch_base=0, layered=False):
+def host_threads(cap: int = 16) -> int:
+    """Host threads for running the oracle on several batches at once: the
+    cores this process may run on, at most `cap`."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        n = os.cpu_count() or 1
+    return max(1, min(cap, n))
+
+
+def sample_group(offsets, indices, seeds, fanouts, rng_seed, batch_base=0, layered=False,
+                 threads=1):
     """Group sampling.  seeds: int32 [B, S].  Returns a dict with per-batch
-    numpy arrays: nodes[b], hop_ptr[b], edge_src[b], edge_dst[b], edge_ptr[b]."""
+    numpy arrays: nodes[b], hop_ptr[b], edge_src[b], edge_dst[b], edge_ptr[b].
+
+    threads > 1 runs the (single-threaded) C oracle on runs of consecutive
+    batches in that many host threads at once.  Mini-batches are sampled
+    independently and each draw is keyed by its global batch number, so the
+    result is the same as one call over the whole group."""
+    sd = np.ascontiguousarray(seeds, dtype=np.int32)
+    B = sd.shape[0]
+    threads = max(1, min(int(threads), B))
+    if threads > 1:
+        from concurrent.futures import ThreadPoolExecutor
+        off = np.ascontiguousarray(offsets, dtype=np.int64)
+        idx = np.ascontiguousarray(indices, dtype=np.int32)
+        cuts = [B * t // threads for t in range(threads + 1)]
+        with ThreadPoolExecutor(threads) as ex:  # ctypes calls release the GIL
+            parts = list(ex.map(
+                lambda t: _sample_one(off, idx, sd[cuts[t]:cuts[t + 1]], fanouts, rng_seed,
+                                      batch_base + cuts[t], layered),
+                range(threads)))
+        out = {k: [x for p in parts for x in p[k]]
+               for k in ("nodes", "hop_ptr", "edge_src", "edge_dst", "edge_ptr")}
+        out["max_nodes"] = max(p["max_nodes"] for p in parts)
+        out["max_edges"] = max(p["max_edges"] for p in parts)
+        return out
+    return _sample_one(offsets, indices, sd, fanouts, rng_seed, batch_base, layered)
+
+
+def _sample_one(offsets, indices, seeds, fanouts, rng_seed, batch_base, layered):
     off = np.ascontiguousarray(offsets, dtype=np.int64)
     idx = np.ascontiguousarray(indices, dtype=np.int32)
     sd = np.ascontiguousarray(seeds, dtype=np.int32)

@@ -377,11 +377,13 @@ int or_cache_by_frequency(int64_t N, int32_t B, const int32_t *nodes, int64_t no
 }
 
 /* ---------------------------------------------------------------------------
- * Disk-cache reordering by MinHash (§5.1, Alg. 1), step by step: S starts at
- * infinity for every disk-cache entry; for every graph sample i and every
- * disk-cached node v it requires, and every hash function j, S(v) becomes
- * min(S(v), H_j(i)); the entries are then sorted by S (stably, so ties keep
- * entry order).  H_j(i) = perms[j*B + i] (permutations drawn by the caller).
+ * Disk-cache reordering by MinHash (§5.1, Alg. 1), from its definition: the
+ * value of a disk-cache entry v is
+ *     S(v) = min { H_j(i) : j a hash function, i a graph sample requiring v },
+ * one minimum over all functions and samples together, as the algorithm keeps
+ * a single running minimum per node (infinity when no sample requires v);
+ * H_j(i) = perms[j*B + i] (permutations drawn by the caller).  The entries are
+ * then ordered by S, stably, so ties keep entry order.
  * ------------------------------------------------------------------------- */
 typedef struct { int64_t s; int64_t pos; } or_sig;
 
@@ -395,28 +397,37 @@ int or_minhash_order(int64_t N, int32_t B, const int32_t *nodes, int64_t node_st
                      const int64_t *node_count, const int32_t *entries, int64_t m,
                      const int32_t *perms, int32_t k, int32_t *order, int32_t *signature) {
   const int64_t INF = INT64_MAX;
-  int64_t *where = (int64_t *)malloc((size_t)N * sizeof(int64_t)); /* entry index of v, or -1 */
-  or_sig *sig = (or_sig *)malloc((size_t)(m + 1) * sizeof(or_sig));
-  for (int64_t v = 0; v < N; ++v) where[v] = -1;
-  for (int64_t e = 0; e < m; ++e) {
-    if (entries[e] < 0 || entries[e] >= N) { free(where); free(sig); return -1; }
-    where[entries[e]] = e;
-    sig[e].s = INF;
-    sig[e].pos = e;
+  if (N < 1 || B < 1 || k < 1 || m < 0) return -1;
+  /* each sample's node set, as a sorted array for membership tests */
+  int32_t **set = (int32_t **)malloc((size_t)B * sizeof(int32_t *));
+  for (int32_t i = 0; i < B; ++i) {
+    set[i] = (int32_t *)malloc((size_t)(node_count[i] + 1) * sizeof(int32_t));
+    memcpy(set[i], nodes + (int64_t)i * node_stride, (size_t)node_count[i] * sizeof(int32_t));
+    qsort(set[i], (size_t)node_count[i], sizeof(int32_t), cmp_i32);
   }
-  for (int32_t i = 0; i < B; ++i)                      /* every graph sample */
-    for (int64_t t = 0; t < node_count[i]; ++t) {
-      int32_t v = nodes[(int64_t)i * node_stride + t];
-      if (v < 0 || v >= N || where[v] < 0) continue;   /* V_i intersect V_d */
-      for (int32_t j = 0; j < k; ++j) {                /* every hash function */
+  or_sig *sig = (or_sig *)malloc((size_t)(m + 1) * sizeof(or_sig));
+  int rc = 0;
+  for (int64_t e = 0; e < m && rc == 0; ++e) {
+    int32_t v = entries[e];
+    if (v < 0 || v >= N) { rc = -1; break; }
+    int64_t s = INF;
+    for (int32_t i = 0; i < B; ++i) {
+      if (find_i32(set[i], node_count[i], v) < 0) continue; /* sample i does not require v */
+      for (int32_t j = 0; j < k; ++j) {
         int64_t h = perms[(int64_t)j * B + i];
-        if (h < sig[where[v]].s) sig[where[v]].s = h;
+        if (h < s) s = h;
       }
     }
-  for (int64_t e = 0; e < m; ++e) signature[e] = sig[e].s == INF ? -1 : (int32_t)sig[e].s;
-  qsort(sig, (size_t)m, sizeof(or_sig), cmp_sig);
-  for (int64_t r = 0; r < m; ++r) order[r] = entries[sig[r].pos];
-  free(where);
+    sig[e].s = s;
+    sig[e].pos = e;
+  }
+  if (rc == 0) {
+    for (int64_t e = 0; e < m; ++e) signature[e] = sig[e].s == INF ? -1 : (int32_t)sig[e].s;
+    qsort(sig, (size_t)m, sizeof(or_sig), cmp_sig);
+    for (int64_t r = 0; r < m; ++r) order[r] = entries[sig[r].pos];
+  }
+  for (int32_t i = 0; i < B; ++i) free(set[i]);
+  free(set);
   free(sig);
-  return 0;
+  return rc;
 }
