@@ -93,9 +93,6 @@ def main():
     ap.add_argument("--fill-masks", action="store_true",
                     help="clear the membership mask and the sampler's state with full fills "
                          "in every sampling call, instead of the clearing flags (comparison)")
-    ap.add_argument("--no-graph", action="store_true",
-                    help="issue each step's assembly calls directly instead of replaying "
-                         "them from a captured HIP graph")
     ap.add_argument("--copy-calib", action="store_true",
                     help="also run a plain copy of known size (counter calibration)")
     ap.add_argument("--groups", type=int, default=16,
@@ -150,30 +147,70 @@ def main():
         print(json.dumps(out), flush=True)
         return
 
-    # first pass: sizes and buffers (outside the timed region)
+    # The stream of groups.  Offline sampling (§3) samples many mini-batches
+    # ahead of training: here consecutive groups of B mini-batches from one seed
+    # stream (seeds drawn without replacement across the whole stream, so no
+    # two groups share a seed; group g holds global mini-batches g*B .. g*B+B-1).
+    # Every timed step takes a group of its own: the serial region the first
+    # warmup+steps groups, the pipelined region the next ones.  Group 0 is the
+    # workload's own group.
+    n_region = args.warmup + args.steps
+    n_groups = 2 * n_region
+    seeds_all = synth.seed_batches(cfg.n, n_groups * B, cfg.S, cfg.seed, dev, offsets=w.offsets)
+    groups = [seeds_all[g * B:(g + 1) * B] for g in range(n_groups)]
+    assert torch.equal(groups[0], w.seeds), "the first group must be the workload's group"
+
+    # Buffers (outside the timed regions): sampling outputs at the per-batch
+    # bounds dg_sample_bounds gives, packing outputs at the largest size any
+    # group of the stream needs (a pre-pass samples and packs every group
+    # without copying rows).
+    node_cap, edge_cap = dg.sample_bounds(cfg.n, w.num_edges, cfg.S, fan)
     mem = torch.empty(cfg.n, dtype=torch.int64, device=dev)  # (node, batch) membership
-    sr = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, membership=mem,
-                         direct=True)
-    ws_s = torch.empty(dg._L.dg_sample_workspace_bytes(cfg.n, B, sr.nodes.shape[1],
-                                                       sr.edge_src.shape[1],
+    ws_s = torch.empty(dg._L.dg_sample_workspace_bytes(cfg.n, B, node_cap, edge_cap,
                                                        dg.sample_flags(direct=True)),
                        dtype=torch.uint8, device=dev)
-    counts = sr.node_count.copy()
+    sr = dg.sample_group(w.offsets, w.indices, groups[0], fan, w.rng_seed, membership=mem,
+                         workspace=ws_s, direct=True, node_cap=node_cap, edge_cap=edge_cap)
+    pre = []
+    ws_pre = None
+    for g in range(n_groups):
+        s_ = dg.sample_group(w.offsets, w.indices, groups[g], fan, w.rng_seed, batch_base=g * B,
+                             out=sr, workspace=ws_s, membership=mem, direct=True)
+        cnt_ = s_.node_count.copy()
+        need_ws = dg._L.dg_pack_workspace_bytes(cfg.n, B, int(cnt_.sum()))
+        if ws_pre is None or ws_pre.numel() < need_ws:
+            ws_pre = torch.empty(need_ws, dtype=torch.uint8, device=dev)
+        p_ = dg.pack_group(w.feats, w.cache_slot, s_.nodes, cnt_, membership=mem,
+                           tables_only=True, workspace=ws_pre)
+        pre.append({**s_.sizes, **{k: p_.sizes[k] for k in
+                                   ("packed_rows", "unique_nodes", "unique_packed")}})
+        del p_
+    del ws_pre
+    torch.cuda.empty_cache()
+    max_rows = max(p["packed_rows"] for p in pre)
+    max_total = max(p["total_nodes"] for p in pre)
+    nmax = max(p["max_batch_nodes"] for p in pre)
+
+    def pack_out():
+        return dg.PackResult(
+            packed=torch.empty((max(max_rows, 1), R), dtype=torch.uint8, device=dev),
+            packed_ids=torch.empty(max(max_rows, 1), dtype=torch.int32, device=dev),
+            packed_ptr=torch.empty(B + 1, dtype=torch.int64, device=dev),
+            packed_ptr_host=np.zeros(B + 1, dtype=np.int64),
+            loc=torch.empty((B, node_cap), dtype=torch.int32, device=dev), unique=None,
+            sizes={}, timing=None, row_bytes=R)
+
     # two packing outputs, so that packing step k+1 never overwrites what
-    # assembly step k is still reading
-    pr2 = [dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, membership=mem,
-                         timing=args.timed_pack) for _ in range(2)]
-    pr = pr2[0]
-    # two packing workspaces: in the pipelined region a packing call's row copy
-    # may still be queued on the assembly stream when the next call starts
-    ws_p2 = [torch.empty(dg._L.dg_pack_workspace_bytes(cfg.n, B, int(counts.sum())),
-                         dtype=torch.uint8, device=dev) for _ in range(2)]
-    nmax = int(counts.max())
+    # assembly step k is still reading; two packing workspaces, since in the
+    # pipelined region a packing call's row copy may still be queued on the
+    # assembly stream when the next call starts
+    pr2 = [pack_out() for _ in range(2)]
+    ws_p2 = [torch.empty(dg._L.dg_pack_workspace_bytes(cfg.n, B, max_total), dtype=torch.uint8,
+                         device=dev) for _ in range(2)]
     ybuf = [torch.empty((nmax, R), dtype=torch.uint8, device=dev) for _ in range(2)]
-    sizes_s, sizes_p = dict(sr.sizes), dict(pr.sizes)
-    log(f"sizes: nodes/batch max {sizes_s['max_batch_nodes']:,} total {sizes_s['total_nodes']:,} "
-        f"edges {sizes_s['total_edges']:,} packed rows {sizes_p['packed_rows']:,} "
-        f"|U| {sizes_p['unique_nodes']:,} |U_nc| {sizes_p['unique_packed']:,}")
+    log(f"{n_groups} groups: pairs {min(p['total_nodes'] for p in pre):,}.."
+        f"{max_total:,} edges {min(p['total_edges'] for p in pre):,}.."
+        f"{max(p['total_edges'] for p in pre):,} packed rows up to {max_rows:,}")
 
     # Sampling and packing run on `stream` and return when their work is done;
     # the fan-out gather is timed by HIP events inside dg_pack_group.  Assembly
@@ -182,7 +219,9 @@ def main():
     # streams at default priority).  In the pipelined region packing also leaves
     # its row copy (the fan-out gather) queued on s_asm ahead of the assembly
     # (DG_PACK_ROWS_STREAM), so the bandwidth-bound copy runs beside the next
-    # step's sampling instead of on the sampling stream.
+    # step's sampling instead of on the sampling stream.  Each step's B
+    # assembly launches are issued by one dg_assemble_batches call with that
+    # step's own sizes; its host time is reported.
     s_asm = torch.cuda.Stream(device=dev)
     asm_done = [torch.cuda.Event(), torch.cuda.Event()]
     pack_done = torch.cuda.Event()
@@ -197,27 +236,6 @@ def main():
         e_.record(s_asm)
     torch.cuda.synchronize()
 
-    # Each step's 64 assembly launches, captured once per packing output set into
-    # a HIP graph (kernel launches only) and replayed on s_asm: one host call
-    # per step instead of one launch per mini-batch.
-    asm_graph = None
-    if not args.no_graph:
-        s_cap = torch.cuda.Stream(device=dev)
-        s_cap.wait_stream(stream)
-        with torch.cuda.stream(s_cap):
-            for pr_ in pr2:
-                dg.assemble_batches(w.cache, pr_, counts, ybuf, stream=s_cap)
-        stream.wait_stream(s_cap)
-        torch.cuda.synchronize()
-        asm_graph = []
-        for pr_ in pr2:
-            g_ = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g_):
-                dg.assemble_batches(w.cache, pr_, counts, ybuf,
-                                    stream=torch.cuda.current_stream())
-            asm_graph.append(g_)
-        torch.cuda.synchronize()
-
     # Mask state across steps: each sampling call leaves its workspace state
     # clear (DG_SAMPLE_EXIT_CLEAR) and each packing call clears the membership
     # mask as it reads it (DG_PACK_CLEAR_MEMBERSHIP), so from the second step on
@@ -231,19 +249,21 @@ def main():
              torch.empty(dg.member_lines_bytes(cfg.n), dtype=torch.uint8, device=dev))
     samp_phases = {False: [], True: []}  # per region, with --sample-timing
 
-    def run(K, pipelined, record):
-        marks, gather_ms, asm_ms = [], [], []
-        evs = []
-        s_out = p_out = None
-        for k in range(K):
+    def run(gs, pipelined, record):
+        """One step per group index in gs; returns per-step host marks, gather
+        times, assembly times (events) and the step's sizes."""
+        marks, gather_ms, evs, steps = [], [], [], []
+        for k, g in enumerate(gs):
             slot = k & 1
             t0 = time.perf_counter()
             entry_clear = clearing and state["clear"]
             state["clear"] = False
-            s_out = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, out=sr,
-                                    workspace=ws_s, membership=mem, direct=True, stream=stream,
-                                    exit_clear=clearing, entry_clear=entry_clear,
-                                    member_lines=lines, timing=args.sample_timing)
+            s_out = dg.sample_group(w.offsets, w.indices, groups[g], fan, w.rng_seed,
+                                    batch_base=g * B, out=sr, workspace=ws_s, membership=mem,
+                                    direct=True, stream=stream, exit_clear=clearing,
+                                    entry_clear=entry_clear, member_lines=lines,
+                                    timing=args.sample_timing)
+            counts = s_out.node_count.copy()
             if args.sample_timing:
                 samp_phases[pipelined].append(dict(s_out.timing))
             t1 = time.perf_counter()
@@ -256,67 +276,83 @@ def main():
                                   member_lines=lines)
             state["clear"] = clearing
             t2 = time.perf_counter()
-            e0, e1 = ev_pool[k]
+            e0, e1 = ev_pool[k % nev]
             pack_done.record(stream)
             s_asm.wait_event(pack_done)
             e0.record(s_asm)
-            if asm_graph is not None:
-                with torch.cuda.stream(s_asm):
-                    asm_graph[slot].replay()
-            else:
-                dg.assemble_batches(w.cache, p_out, counts, ybuf, stream=s_asm)
+            dg.assemble_batches(w.cache, p_out, counts, ybuf, stream=s_asm)
             e1.record(s_asm)
             asm_done[slot].record(s_asm)
             t3 = time.perf_counter()
             if not pipelined:
                 e1.synchronize()
-            evs.append((e0, e1))
+                evs.append(e0.elapsed_time(e1))
             marks.append((t1 - t0, t2 - t1, t3 - t2))
+            steps.append({**s_out.sizes, **{k_: p_out.sizes[k_] for k_ in
+                                            ("packed_rows", "unique_nodes", "unique_packed")}})
             if record:
                 gather_ms.append(p_out.timing["gather_ms"])
         torch.cuda.synchronize()
-        asm_ms = [a.elapsed_time(b) for a, b in evs]
-        return marks, gather_ms, asm_ms, s_out, p_out
+        return marks, gather_ms, evs, steps
 
-    def timed(pipelined):
-        run(args.warmup, pipelined, False)
+    def timed(gs, pipelined):
+        run(gs[:args.warmup], pipelined, False)
         torch.cuda.synchronize()
         t_start = time.perf_counter()
         # per-phase timing (which runs the packing call's phases one after the
         # other) only in the serial region
-        res = run(args.steps, pipelined, not pipelined)
+        res = run(gs[args.warmup:], pipelined, not pipelined)
         torch.cuda.synchronize()
         t_total = time.perf_counter() - t_start
-        if res[3].sizes != sizes_s or res[4].sizes != sizes_p:
-            raise RuntimeError("sizes changed between steps")
+        for g, st in zip(gs[args.warmup:], res[3]):  # the pre-pass saw the same sizes
+            if any(st[k] != pre[g][k] for k in ("total_nodes", "total_edges", "packed_rows")):
+                raise RuntimeError(f"group {g}: sizes differ from the pre-pass")
         return (t_total,) + res
 
-    # timed regions: K whole steps serially, then K whole steps pipelined
-    t_serial, marks, gather_ms, asm_ms, _, _ = timed(False)
+    def feature_bytes(st):
+        """Feature bytes the method must move for one group: packing reads each
+        non-cached unique row once and writes one row per packed row; assembly
+        reads and writes one row per (node, batch) pair."""
+        return R * (st["unique_packed"] + st["packed_rows"]), 2 * R * st["total_nodes"]
+
+    # timed regions: K whole steps serially, then K whole steps pipelined, each
+    # over groups of its own
+    serial_groups = list(range(n_region))
+    pipe_groups = list(range(n_region, 2 * n_region))
+    t_serial, marks, gather_ms, asm_ms, steps_s = timed(serial_groups, False)
     if args.no_pipeline:
-        t_total, marks_p, asm_ms_p = t_serial, marks, asm_ms
+        t_total, marks_p, steps_p = t_serial, marks, steps_s
     else:
-        t_total, marks_p, _, asm_ms_p, _, _ = timed(True)
+        t_total, marks_p, _, _, steps_p = timed(pipe_groups, True)
+    # secondary figure: the workload's own group repeated in every step (the
+    # same index working set and hot rows each time), pipelined
+    t_rep, _, _, _, steps_r = timed([0] * n_region, not args.no_pipeline)
     samp_ms = [1e3 * m[0] for m in marks]
     pack_ms = [1e3 * m[1] for m in marks]
 
-    Uc = sizes_p["unique_packed"]
-    P = sizes_p["packed_rows"]
-    n_pairs = sizes_s["total_nodes"]
-    F_pack = R * (Uc + P)
-    F_asm = 2 * R * n_pairs
-    F = F_pack + F_asm
+    Fp_s = [feature_bytes(st) for st in steps_s]
+    F_pack_s = sum(a for a, _ in Fp_s)
+    F_asm_s = sum(b for _, b in Fp_s)
+    F_main = sum(sum(feature_bytes(st)) for st in steps_p)
     ms_step = 1e3 * t_total / args.steps
-    value = F * args.steps / t_total / 1e9
+    value = F_main / t_total / 1e9
     ms_serial = 1e3 * t_serial / args.steps
+    # fan-out gather: one k_fanout16 launch per step, timed by the library's
+    # HIP events on the call's stream (serial region)
     g_ms = float(np.mean(gather_ms))
-    achieved = F_pack / (g_ms * 1e-3) / 1e9
+    achieved = F_pack_s / (sum(gather_ms) * 1e-3) / 1e9
     # assembly: one k_assemble16 launch per mini-batch; its average launch time
-    # is the step's assembly time (HIP events on its stream, serial region) / B
-    a_ms = float(np.mean(asm_ms)) / B
-    F_asm_launch = F_asm / B
+    # is the steps' assembly time (HIP events on its stream, serial region)
+    # over the K*B launches, and its bytes the steps' assembly bytes over them
+    a_ms = float(np.sum(asm_ms)) / (args.steps * B)
+    F_asm_launch = F_asm_s / (args.steps * B)
     achieved_asm = F_asm_launch / (a_ms * 1e-3) / 1e9
-    edges = sizes_s["total_edges"]
+    edges = sum(st["total_edges"] for st in steps_s)
+    sizes_rep = steps_r[0]
+
+    def span(key, steps):
+        v = [st[key] for st in steps]
+        return [min(v), max(v)] if min(v) != max(v) else v[0]
 
     out = {
         "metric": "packed+assembled feature GB/s (and % HBM peak); sampled edges/s, 1 MI355X",
@@ -339,10 +375,14 @@ def main():
                    "row_bytes": R, "batches": B, "seeds_per_batch": cfg.S, "fanouts": fan,
                    "cache_rows": int(w.cache_nodes.numel()), "parallelism": "single-gpu"},
         "frac_hbm_peak": round(value / HBM_PEAK_GBPS, 4),
+        "groups": (f"a stream of distinct groups: every step samples, packs and assembles a group "
+                   f"of its own ({B} mini-batches x {cfg.S} seeds, consecutive groups of one "
+                   f"seed stream drawn without replacement); value = the timed steps' own "
+                   f"feature bytes over their wall time"),
         "pipelined": ("no: --no-pipeline, value is the serial rate" if args.no_pipeline else
                       "assembly of step k (second stream) overlaps sampling and packing of "
                       "step k+1; the serial figures below wait for each step's assembly"),
-        "assembly_issue": "HIP graph replay" if asm_graph is not None else "direct calls",
+        "assembly_issue": "direct calls: one dg_assemble_batches call (B launches) per step",
         "pack_rows": ("pipelined region: packing's row copy queued on the assembly stream "
                       "(DG_PACK_ROWS_STREAM)" if not (args.rows_inline or args.timed_pack
                                                       or args.no_pipeline)
@@ -353,22 +393,29 @@ def main():
                           "sampling leaves its state clear, so no full-mask fill runs per step"
                           if clearing else "two full-mask fills in every sampling call"),
         "serial": {"ms_per_step": round(ms_serial, 3),
-                   "value": round(F * args.steps / t_serial / 1e9, 2)},
+                   "value": round((F_pack_s + F_asm_s) / t_serial / 1e9, 2)},
+        "repeated_group": {"what": "the workload's group sampled, packed and assembled in every "
+                                   "step (same seeds each time)",
+                           "ms_per_step": round(1e3 * t_rep / args.steps, 3),
+                           "value": round(args.steps * sum(feature_bytes(sizes_rep)) / t_rep
+                                          / 1e9, 2)},
         "pipelined_phases_ms": {"sample": round(1e3 * float(np.mean([m[0] for m in marks_p])), 3),
                                 "pack": round(1e3 * float(np.mean([m[1] for m in marks_p])), 3),
-                                "assemble_all_batches": round(float(np.mean(asm_ms_p)), 3),
                                 "host_enqueue_assembly": round(
                                     1e3 * float(np.mean([m[2] for m in marks_p])), 3)},
-        "sampled_edges_per_s": round(edges / (np.mean(samp_ms) * 1e-3), 1),
+        "sampled_edges_per_s": round(edges / (np.sum(samp_ms) * 1e-3), 1),
         "phases_ms": {"sample": round(float(np.mean(samp_ms)), 3),
                       "pack": round(float(np.mean(pack_ms)), 3),
                       "fanout_gather": round(g_ms, 3),
-                      "assemble_all_batches": round(float(np.mean(asm_ms)), 3)},
-        "phase_gbps": {"pack_call": round(F_pack / (np.mean(pack_ms) * 1e-3) / 1e9, 1),
-                       "assemble_calls": round(F_asm / (np.mean(asm_ms) * 1e-3) / 1e9, 1)},
-        "sizes": {"total_nodes": n_pairs, "total_edges": edges, "packed_rows": P,
-                  "unique_nodes": sizes_p["unique_nodes"], "unique_packed": Uc},
-        # the dominant kernel by time: batch assembly (64 launches per step)
+                      "assemble_all_batches": round(float(np.mean(asm_ms)), 3),
+                      "host_enqueue_assembly": round(
+                          1e3 * float(np.mean([m[2] for m in marks])), 3)},
+        "phase_gbps": {"pack_call": round(F_pack_s / (np.sum(pack_ms) * 1e-3) / 1e9, 1),
+                       "assemble_calls": round(F_asm_s / (np.sum(asm_ms) * 1e-3) / 1e9, 1)},
+        "sizes": {k: span(k, steps_p) for k in
+                  ("total_nodes", "total_edges", "packed_rows", "unique_nodes",
+                   "unique_packed")},
+        # the dominant kernel by time: batch assembly (B launches per step)
         "roofline": {"kernel": "k_assemble16 (batch assembly, one launch per mini-batch)",
                      "bound": "hbm", "achieved": round(achieved_asm, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved_asm / HBM_PEAK_GBPS, 4),
@@ -380,8 +427,8 @@ def main():
                             "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                             "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                             "traffic": load_traffic(cfg.name, "fanout_gather"),
-                            "algorithmic_bytes": F_pack, "launch_ms": round(g_ms, 4),
-                            "launches_per_step": 1},
+                            "algorithmic_bytes": int(round(F_pack_s / args.steps)),
+                            "launch_ms": round(g_ms, 4), "launches_per_step": 1},
     }
 
     if args.copy_calib:
@@ -703,18 +750,91 @@ def experiment_regime(dg, w, cfg, reps, groups=16):
             "cache_rows": int(w.cache_nodes.numel())}
 
 
-def cpu_baseline(w, cfg, nb, groups=2):
-    """The oracle (single-threaded C) timed on the host on a bounded sample of
-    the same workload: the first `nb` mini-batches of `groups` consecutive
-    groups (the benchmark's group and the next ones of the same seed stream),
-    on the full graph and full feature table; about 12 s of CPU work for two
-    groups of L100."""
+def cpu_model() -> str:
+    """The host CPU's model name, as lscpu reports it."""
+    import subprocess
+    try:
+        txt = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for ln in txt.splitlines():
+            if ln.startswith("Model name:"):
+                return ln.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        with open("/proc/cpuinfo") as f:
+            return next((ln.split(":", 1)[1].strip() for ln in f
+                         if ln.startswith("model name")), "unknown")
+    except OSError:
+        return "unknown"
+
+
+def _oracle_pass(oracle, off, idx, X, slot, cache, seeds, fan, rng, batch_base, R, threads):
+    """One group through the oracle: sampling, packing and assembly, timed per
+    phase.  With threads > 1 each phase runs on runs of consecutive mini-batches
+    in that many host threads: sampling is independent per mini-batch (draws are
+    keyed by the global batch number), and a mini-batch's packed chunk, packed
+    order and address table depend on its own node list only, so packing a run
+    of batches gives the same per-batch outputs as packing the whole group.
+    Returns (seconds per phase, sampled lists, packing results, their batch
+    runs)."""
+    from concurrent.futures import ThreadPoolExecutor
+    nb = seeds.shape[0]
+    cuts = [nb * t // threads for t in range(threads + 1)]
+    t1 = time.perf_counter()
+    rs = oracle.sample_group(off, idx, seeds, fan, rng, batch_base=batch_base, threads=threads)
+    t2 = time.perf_counter()
+    if threads == 1:
+        parts = [oracle.pack_group(X, slot, rs["nodes"], with_unique=False)]
+        runs = [(0, nb)]
+    else:
+        runs = [(cuts[t], cuts[t + 1]) for t in range(threads) if cuts[t + 1] > cuts[t]]
+        with ThreadPoolExecutor(len(runs)) as ex:
+            parts = list(ex.map(lambda r: oracle.pack_group(X, slot, rs["nodes"][r[0]:r[1]],
+                                                            with_unique=False), runs))
+    t3 = time.perf_counter()
+
+    def assemble(i):
+        rp, (lo_b, hi_b) = parts[i], runs[i]
+        for b in range(hi_b - lo_b):
+            lo, hi = rp["packed_ptr"][b], rp["packed_ptr"][b + 1]
+            oracle.assemble_batch(cache, rp["packed"][lo:hi], rp["loc"][b], R)
+
+    if threads == 1:
+        assemble(0)
+    else:
+        with ThreadPoolExecutor(len(runs)) as ex:
+            list(ex.map(assemble, range(len(runs))))
+    t4 = time.perf_counter()
+    return {"sample": t2 - t1, "pack": t3 - t2, "assemble": t4 - t3}, rs, parts, runs
+
+
+def _group_bytes(rs, slot, R):
+    """Algorithmic feature bytes of one group (the GPU's definition)."""
+    import numpy as np
+    allnodes = np.concatenate(rs["nodes"])
+    u = np.unique(allnodes)
+    unc = int((slot[u] < 0).sum())
+    packed = int((slot[allnodes] < 0).sum())
+    return R * (unc + packed) + 2 * R * allnodes.size, sum(len(x) for x in rs["edge_src"])
+
+
+def cpu_baseline(w, cfg, nb, groups=2, small=True):
+    """The oracle (single-threaded C, as it stands) timed on the host on a
+    bounded sample of the same workload: the first `nb` mini-batches of
+    `groups` consecutive groups of the seed stream (the benchmark's first groups),
+    on the full graph and feature table, run on the host's cores (runs of
+    mini-batches in parallel threads, at most 16: the host share of one GPU);
+    beside it the same oracle on one core over the first group, and on one core
+    over the small workloads T and M1."""
     import numpy as np
     import torch
 
     import oracle
     import synth
 
+    threads = oracle.host_threads()
+    if w.feats.numel() * w.feats.element_size() > (96 << 30):
+        return {"skipped": "feature table above 96 GB: not copied to host memory"}
     t0 = time.perf_counter()
     log("cpu baseline: copying graph and features to host")
     off = w.offsets.cpu().numpy()
@@ -723,48 +843,70 @@ def cpu_baseline(w, cfg, nb, groups=2):
     all_seeds = synth.seed_batches(cfg.n, groups * B, cfg.S, cfg.seed, w.offsets.device,
                                    offsets=w.offsets)
     assert torch.equal(all_seeds[:B], w.seeds), "the first group must be the benchmark group"
+    all_seeds = all_seeds.cpu().numpy()
     X = w.feats.cpu().numpy()
     slot = w.cache_slot.cpu().numpy()
     cache = w.cache.cpu().numpy()
-    log(f"host copies in {time.perf_counter() - t0:.1f}s; running the oracle on {groups} x {nb} "
-        f"batches")
     R = cfg.row_bytes
-    secs = {"sample": 0.0, "pack": 0.0, "assemble": 0.0}
-    F = edges = 0
-    for g in range(groups):
-        seeds = all_seeds[g * B:g * B + nb].cpu().numpy()
-        t1 = time.perf_counter()
-        rs = oracle.sample_group(off, idx, seeds, list(cfg.fanouts), w.rng_seed, batch_base=g * B)
-        t2 = time.perf_counter()
-        rp = oracle.pack_group(X, slot, rs["nodes"], with_unique=False)
-        t3 = time.perf_counter()
-        for b in range(nb):
-            lo, hi = rp["packed_ptr"][b], rp["packed_ptr"][b + 1]
-            oracle.assemble_batch(cache, rp["packed"][lo:hi], rp["loc"][b], R)
-        t4 = time.perf_counter()
-        secs["sample"] += t2 - t1
-        secs["pack"] += t3 - t2
-        secs["assemble"] += t4 - t3
-        pairs = sum(len(x) for x in rs["nodes"])
-        edges += sum(len(x) for x in rs["edge_src"])
-        F += R * (rp["unique_packed"] + rp["packed_rows"]) + 2 * R * pairs
-        del rs, rp
-    total = sum(secs.values())
+    fan = list(cfg.fanouts)
+    log(f"host copies in {time.perf_counter() - t0:.1f}s; oracle on {groups} x {nb} batches in "
+        f"{threads} threads, then 1 x {nb} batches on one core")
+
+    def measure(ngroups, nthreads):
+        secs = {"sample": 0.0, "pack": 0.0, "assemble": 0.0}
+        F = edges = 0
+        for g in range(ngroups):
+            s, rs, _, _ = _oracle_pass(oracle, off, idx, X, slot, cache,
+                                       all_seeds[g * B:g * B + nb], fan, w.rng_seed, g * B, R,
+                                       nthreads)
+            for k in secs:
+                secs[k] += s[k]
+            f, e = _group_bytes(rs, slot, R)
+            F += f
+            edges += e
+            del rs
+        total = sum(secs.values())
+        return {"value": round(F / total / 1e9, 4), "seconds": {k: round(v, 3)
+                                                                for k, v in secs.items()},
+                "sampled_edges_per_s": round(edges / secs["sample"], 1)}
+
+    multi = measure(groups, threads)
+    one = measure(1, 1)
     what = "the whole group" if nb == cfg.B else f"the first {nb} of {cfg.B} mini-batches"
-    cpu = "unknown"
-    try:
-        with open("/proc/cpuinfo") as f:
-            cpu = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")),
-                       cpu)
-    except OSError:
-        pass
-    return {"value": round(F / total / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "cpu_model": cpu,
-            "sample": f"{what}, for {groups} consecutive groups of {cfg.name} (the benchmark's "
-                      f"group and the next of the same seed stream; full graph and feature table "
-                      f"on the host): sample + pack + assemble, single-threaded C, one pass each",
-            "seconds": {k: round(v, 3) for k, v in secs.items()},
-            "sampled_edges_per_s": round(edges / secs["sample"], 1)}
+    out = {"value": multi["value"], "unit": "GB/s", "cores": threads, "kind": "oracle",
+           "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
+           "sample": f"{what}, for {groups} consecutive groups of {cfg.name} (the benchmark's "
+                     f"first groups of the seed stream; full graph and feature table on the "
+                     f"host): sample + pack + assemble, one pass each, runs of mini-batches in "
+                     f"{threads} host threads (the oracle itself is single-threaded C)",
+           "seconds": multi["seconds"], "sampled_edges_per_s": multi["sampled_edges_per_s"],
+           "one_core": {"value": one["value"], "unit": "GB/s", "cores": 1,
+                        "sample": f"{what}, first group only",
+                        "seconds": one["seconds"],
+                        "sampled_edges_per_s": one["sampled_edges_per_s"]}}
+    del X, off, idx
+    if small:
+        out["one_core_small"] = {}
+        for name in ("T", "M1"):
+            ws_ = synth.make_workload(name, device=w.offsets.device)
+            c_ = ws_.cfg
+            o_, i_ = ws_.offsets.cpu().numpy(), ws_.indices.cpu().numpy()
+            X_, sl_, ca_ = ws_.feats.cpu().numpy(), ws_.cache_slot.cpu().numpy(), \
+                ws_.cache.cpu().numpy()
+            times = []
+            for _ in range(3):  # the median of 3 runs
+                s, rs, _, _ = _oracle_pass(oracle, o_, i_, X_, sl_, ca_,
+                                           ws_.seeds.cpu().numpy(), list(c_.fanouts),
+                                           ws_.rng_seed, 0, c_.row_bytes, 1)
+                times.append(s)
+            s = sorted(times, key=lambda x: sum(x.values()))[1]
+            tot = sum(s.values())
+            f, e = _group_bytes(rs, sl_, c_.row_bytes)
+            out["one_core_small"][name] = {"value": round(f / tot / 1e9, 4), "unit": "GB/s",
+                                           "seconds": {k: round(v, 4) for k, v in s.items()},
+                                           "sampled_edges_per_s": round(e / s["sample"], 1)}
+            del ws_, X_
+    return out
 
 
 if __name__ == "__main__":

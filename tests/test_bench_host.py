@@ -47,12 +47,43 @@ def test_traffic_digest_covers_the_kernel_translation_unit(tmp_path, monkeypatch
 
 def test_cpu_baseline_runs_two_groups_on_the_host():
     """The CPU baseline leg (the oracle on the host) on the tiny workload: two
-    consecutive groups, the first of which is the benchmark's own."""
+    consecutive groups (the first is the benchmark's own) on the host's cores,
+    and the first group on one core."""
+    import oracle
     import synth
     w = synth.make_workload("T")
     cfg = w.cfg
-    r = bench.cpu_baseline(w, cfg, cfg.B, groups=2)
-    assert r["kind"] == "oracle" and r["cores"] == 1 and r["unit"] == "GB/s"
-    assert r["value"] > 0 and r["sampled_edges_per_s"] > 0
+    r = bench.cpu_baseline(w, cfg, cfg.B, groups=2, small=False)
+    assert r["kind"] == "oracle" and r["unit"] == "GB/s"
+    assert r["cores"] == oracle.host_threads() and r["one_core"]["cores"] == 1
+    assert r["value"] > 0 and r["sampled_edges_per_s"] > 0 and r["one_core"]["value"] > 0
     assert "2 consecutive groups" in r["sample"]
     assert set(r["seconds"]) == {"sample", "pack", "assemble"}
+    assert r["cpu_model"]
+
+
+def test_oracle_on_runs_of_batches_gives_the_group_result():
+    """Splitting a group into runs of mini-batches over host threads (as the
+    CPU baseline does) gives every mini-batch the outputs of one pass over the
+    whole group: sampled lists, packed chunk, packed order, address table."""
+    import numpy as np
+
+    import oracle
+    import synth
+    w = synth.make_workload("T")
+    cfg = w.cfg
+    args = (w.offsets.numpy(), w.indices.numpy(), w.feats.numpy(), w.cache_slot.numpy(),
+            w.cache.numpy(), w.seeds.numpy(), list(cfg.fanouts), w.rng_seed, 0, cfg.row_bytes)
+    _, rs1, p1, _ = bench._oracle_pass(oracle, *args, 1)
+    _, rs3, p3, runs = bench._oracle_pass(oracle, *args, 3)
+    assert len(runs) == 3
+    for k in ("nodes", "edge_src", "edge_dst", "hop_ptr", "edge_ptr"):
+        assert all(np.array_equal(a, b) for a, b in zip(rs1[k], rs3[k])), k
+    whole = p1[0]
+    for (lo, hi), part in zip(runs, p3):
+        for b in range(lo, hi):
+            assert np.array_equal(whole["loc"][b], part["loc"][b - lo])
+            w0, w1 = whole["packed_ptr"][b], whole["packed_ptr"][b + 1]
+            q0, q1 = part["packed_ptr"][b - lo], part["packed_ptr"][b - lo + 1]
+            assert np.array_equal(whole["packed_ids"][w0:w1], part["packed_ids"][q0:q1])
+            assert np.array_equal(whole["packed"][w0:w1], part["packed"][q0:q1])

@@ -4,15 +4,18 @@ the sampler's membership mask handed to the packer, the mask-clearing flags
 sampling call told that the state is clear), and packing's row copy queued on
 a second stream with the assembly behind it.
 
-M1 (1M nodes) compares every integer output with the oracle and every row on
-the device.  The full-size workloads (L100, W120, H65 at three cache shares)
-compare, against the oracle: the sampled lists of the first and last
-mini-batch (an oracle run over those batches alone, with their global batch
-numbers) and every packing table of the whole group (U, P_b order,
-packed_ptr, address tables); feature rows are checked on the device against
-an independent library gather (torch.index_select) of the feature table, for
-every packed row and every assembled row.  L100, H65 and M1 relabel through
-the direct [N][B] table (as bench.py does), W120 through the hash table."""
+Every workload compares, for every mini-batch of the group, the sampled node
+list, hop bounds, edge lists and edge bounds with the oracle's (one oracle run
+over the whole group, split over host threads by runs of batches; each draw is
+keyed by its global batch number, so the split changes nothing), and every
+packing table of the whole group (U, P_b order, packed_ptr, address tables)
+with the oracle's packing of those same lists.  M1 also compares feature rows
+with the oracle's own copies; at full size (L100, W120, H65 at every cache
+share) every packed and every assembled row is checked on the device against
+an independent library gather (torch.index_select) of the feature table.
+L100, H65 and M1 relabel through the direct [N][B] table (as bench.py does),
+W120 through the hash table.  L100 and M1 are also sampled with layer-wise
+frontiers and compared with the oracle batch by batch."""
 import numpy as np
 import pytest
 import torch
@@ -59,7 +62,25 @@ def bench_path(dg, w, fan, mem, ws_s, ws_p, direct, entry_clear, out=None):
     return sr, counts, pr
 
 
-def run_and_check(dg, orc, w, oracle_batches, direct=True):
+def oracle_sample(orc, w, layered=False):
+    """The oracle's sampling of the workload's whole group, every batch."""
+    return orc.sample_group(w.offsets.cpu().numpy(), w.indices.cpu().numpy(),
+                            w.seeds.cpu().numpy(), list(w.cfg.fanouts), w.rng_seed,
+                            layered=layered, threads=orc.host_threads())
+
+
+def compare_samples(sr, ref, B):
+    for b in range(B):
+        n, e = int(sr.hop_ptr[b, -1]), int(sr.edge_ptr[b, -1])
+        assert np.array_equal(sr.hop_ptr[b], ref["hop_ptr"][b]), b
+        assert np.array_equal(sr.edge_ptr[b], ref["edge_ptr"][b]), b
+        assert np.array_equal(sr.nodes[b, :n].cpu().numpy(), ref["nodes"][b]), b
+        assert np.array_equal(sr.edge_src[b, :e].cpu().numpy(), ref["edge_src"][b]), b
+        assert np.array_equal(sr.edge_dst[b, :e].cpu().numpy(), ref["edge_dst"][b]), b
+
+
+def run_and_check(dg, orc, w, ref, direct=True):
+    """ref: the oracle's sampling of the whole group (oracle_sample)."""
     cfg = w.cfg
     fan = list(cfg.fanouts)
     R = cfg.row_bytes
@@ -75,23 +96,13 @@ def run_and_check(dg, orc, w, oracle_batches, direct=True):
     print(f"[{cfg.name}] nodes {sr.sizes['total_nodes']:,} edges {sr.sizes['total_edges']:,} "
           f"packed {pr.sizes['packed_rows']:,} U {pr.sizes['unique_nodes']:,}", flush=True)
 
-    # sampling: oracle on selected batches (same global batch numbers)
-    off = w.offsets.cpu().numpy()
-    idx = w.indices.cpu().numpy()
-    for b in oracle_batches:
-        ref = orc.sample_group(off, idx, w.seeds[b:b + 1].cpu().numpy(), fan, w.rng_seed,
-                               batch_base=b)
-        n, e = int(sr.hop_ptr[b, -1]), int(sr.edge_ptr[b, -1])
-        assert np.array_equal(sr.hop_ptr[b], ref["hop_ptr"][0]), b
-        assert np.array_equal(sr.edge_ptr[b], ref["edge_ptr"][0]), b
-        assert np.array_equal(sr.nodes[b, :n].cpu().numpy(), ref["nodes"][0]), b
-        assert np.array_equal(sr.edge_src[b, :e].cpu().numpy(), ref["edge_src"][0]), b
-        assert np.array_equal(sr.edge_dst[b, :e].cpu().numpy(), ref["edge_dst"][0]), b
-    del off, idx
+    # sampling: every batch against the oracle
+    compare_samples(sr, ref, cfg.B)
 
-    # packing tables of the whole group: oracle over the device's node lists
-    lists = [sr.nodes[b, :int(counts[b])].cpu().numpy() for b in range(cfg.B)]
-    refp = orc.pack_group(None, w.cache_slot.cpu().numpy(), lists, rows=False, row_bytes=R)
+    # packing tables of the whole group: the oracle's packing of its own lists
+    # (equal to the device's, as just checked)
+    refp = orc.pack_group(None, w.cache_slot.cpu().numpy(), ref["nodes"], rows=False,
+                          row_bytes=R)
     rows = refp["packed_rows"]
     assert pr.sizes["packed_rows"] == rows
     assert pr.sizes["unique_nodes"] == refp["unique_nodes"]
@@ -135,7 +146,7 @@ def run_and_check(dg, orc, w, oracle_batches, direct=True):
 
 def test_workload_M1_full(dg, orc):
     w = synth.make_workload("M1", device=DEV)
-    sr, pr = run_and_check(dg, orc, w, oracle_batches=range(w.cfg.B))
+    sr, pr = run_and_check(dg, orc, w, oracle_sample(orc, w))
     # every row also against the oracle's own copies on a few batches
     X = w.feats.cpu().numpy()
     lists = [sr.nodes[b, :int(sr.hop_ptr[b, -1])].cpu().numpy() for b in (0, 1)]
@@ -155,46 +166,48 @@ def big(name, cache_pct=None):
     return w
 
 
+def layered_check(dg, orc, w):
+    """Layer-wise frontiers (every node so far samples at each hop), every
+    batch against the oracle, direct relabelling table."""
+    fan = list(w.cfg.fanouts)
+    sr = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, layered=True,
+                         direct=True)
+    print(f"[{w.cfg.name} layered] nodes {sr.sizes['total_nodes']:,} "
+          f"edges {sr.sizes['total_edges']:,}", flush=True)
+    compare_samples(sr, oracle_sample(orc, w, layered=True), w.cfg.B)
+
+
 @pytest.mark.big
 @pytest.mark.timeout(900)
 def test_workload_L100(dg, orc):
     w = big("L100")
-    run_and_check(dg, orc, w, oracle_batches=(0, w.cfg.B - 1))
+    run_and_check(dg, orc, w, oracle_sample(orc, w))
+    torch.cuda.empty_cache()
+    layered_check(dg, orc, w)
 
 
 @pytest.mark.big
 @pytest.mark.timeout(900)
 def test_workload_W120(dg, orc):
     w = big("W120")
-    run_and_check(dg, orc, w, oracle_batches=(0, w.cfg.B - 1), direct=False)
+    run_and_check(dg, orc, w, oracle_sample(orc, w), direct=False)
 
 
 @pytest.mark.big
 @pytest.mark.timeout(1200)
 def test_workload_H65_cache_sweep(dg, orc):
     w = big("H65", cache_pct=0)
+    ref = oracle_sample(orc, w)  # sampling does not depend on the cache
     for pct in synth.CONFIGS["H65"].cache_pct:
         synth.set_cache(w, pct)
         print(f"[H65] cache {pct}%", flush=True)
-        run_and_check(dg, orc, w, oracle_batches=(0, w.cfg.B - 1) if pct == 0 else ())
+        run_and_check(dg, orc, w, ref)
         torch.cuda.empty_cache()
 
 
 def test_workload_M1_layered_full(dg, orc):
     """Layer-wise frontiers at M1 scale, every batch against the oracle."""
-    w = synth.make_workload("M1", device=DEV)
-    fan = list(w.cfg.fanouts)
-    sr = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, layered=True,
-                         direct=True)
-    ref = orc.sample_group(w.offsets.cpu().numpy(), w.indices.cpu().numpy(),
-                           w.seeds.cpu().numpy(), fan, w.rng_seed, layered=True)
-    for b in range(w.cfg.B):
-        n, e = int(sr.hop_ptr[b, -1]), int(sr.edge_ptr[b, -1])
-        assert np.array_equal(sr.hop_ptr[b], ref["hop_ptr"][b]), b
-        assert np.array_equal(sr.edge_ptr[b], ref["edge_ptr"][b]), b
-        assert np.array_equal(sr.nodes[b, :n].cpu().numpy(), ref["nodes"][b]), b
-        assert np.array_equal(sr.edge_src[b, :e].cpu().numpy(), ref["edge_src"][b]), b
-        assert np.array_equal(sr.edge_dst[b, :e].cpu().numpy(), ref["edge_dst"][b]), b
+    layered_check(dg, orc, synth.make_workload("M1", device=DEV))
 
 
 def test_workload_M1_relabelling_tables_agree(dg):
