@@ -29,7 +29,8 @@
  *  - Node IDs are int32 in [0, N) (N < 2^31); CSR edge offsets are int64.
  *  - The caller owns every buffer.  The library never allocates device memory:
  *    scratch space is the caller's workspace `ws`, sized by the matching
- *    *_workspace_bytes() query and aligned to 256 bytes.  Workspace contents on
+ *    *_workspace_bytes() query and aligned to 256 bytes (dg_pack_group_noalloc
+ *    alone uses a fixed scratch array inside the library instead).  Workspace contents on
  *    entry are irrelevant and on return unspecified, except where the flags
  *    DG_SAMPLE_ENTRY_CLEAR / DG_SAMPLE_EXIT_CLEAR say otherwise.  The only resources
  *    the library takes for itself are a 4 KB page-locked host buffer per calling
@@ -339,6 +340,34 @@ int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
                   uint32_t flags, void *ws,
                   size_t ws_bytes, hipStream_t stream, hipStream_t rows_stream,
                   dg_sizes *sizes, dg_timing *timing);
+
+/* Bytes of the fixed scratch of dg_pack_group_noalloc (256 MiB). */
+size_t dg_pack_noalloc_scratch_bytes(void);
+
+/* dg_pack_group for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same arguments, outputs and errors, except that the call allocates nothing.
+ *  - Its scratch is a fixed array inside the library, one per GPU, of
+ *    dg_pack_noalloc_scratch_bytes() bytes; each GPU the library runs on holds
+ *    it until the process ends.  Calls whose sizes need more
+ *    (dg_pack_workspace_bytes(N, B, sum of n_b) above that) return
+ *    DG_EWORKSPACE before any work is enqueued.
+ *  - Every call on a GPU shares that GPU's scratch, which keeps the last
+ *    call's contents; each call clears what it needs cleared.  Calls that
+ *    overlap in time on one GPU race and give unspecified outputs: the caller
+ *    must serialise them (across host threads and streams).
+ *  - All work runs on `stream`: no second stream, so DG_PACK_ROWS_STREAM is
+ *    rejected (DG_EINVAL) and no timing is taken.  Counts are read back
+ *    straight into host memory, with no page-locked buffer of the library's.
+ *  - No hipMalloc, hipHostMalloc, hipFree, stream or event creation. */
+int dg_pack_group_noalloc(const void *feats, int64_t N, int64_t row_bytes,
+                          const int32_t *cache_slot, int32_t B, const int32_t *nodes,
+                          int64_t node_stride, const int64_t *node_count, int64_t packed_cap,
+                          void *packed, int32_t *packed_ids, int64_t *packed_ptr,
+                          int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique,
+                          int64_t unique_cap, uint64_t *membership,
+                          const uint8_t *member_lines, uint32_t flags, hipStream_t stream,
+                          dg_sizes *sizes);
 
 /* Feature assembling for one mini-batch (§4 Fig. 3, second step; addresses come
  * from the precomputed table of §6, so no lookup structure is consulted):

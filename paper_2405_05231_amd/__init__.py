@@ -198,7 +198,7 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
                workspace: torch.Tensor | None = None, stream=None, timing: bool = False,
                membership: torch.Tensor | None = None, tables_only: bool = False,
                clear_membership: bool = False, rows_stream=None,
-               member_lines: torch.Tensor | None = None) -> PackResult:
+               member_lines: torch.Tensor | None = None, no_alloc: bool = False) -> PackResult:
     """Batched packing (dg_pack_group).  nodes: int32 [B, node_stride];
     node_count: the B list lengths (host).  membership: optional int64 [N]
     mask from sample_group (skips rebuilding it).  tables_only: build the
@@ -208,7 +208,9 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
     that stream (the call returns once the tables are done; keep `workspace`,
     `feats` and the packed buffer untouched until the copy has run).
     member_lines: the map sample_group wrote (with membership): only the
-    words of marked lines are read."""
+    words of marked lines are read.  no_alloc: call dg_pack_group_noalloc
+    (scratch inside the library, no workspace; no timing or rows_stream);
+    pass `out` as well for a call that allocates nothing at all."""
     dev = feats.device
     _need(feats, "feats", None)
     _need(cache_slot, "cache_slot", torch.int32, dev)
@@ -228,8 +230,24 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
     if counts.shape[0] != B:
         raise ValueError("node_count must have one entry per batch")
     total = int(counts.sum())
-    ws_bytes = _L.dg_pack_workspace_bytes(N, B, total)
-    ws = _workspace(ws_bytes, dev, workspace)
+    if no_alloc:
+        if timing or rows_stream is not None:
+            raise ValueError("no_alloc takes neither timing nor rows_stream")
+        ws = None
+    else:
+        ws = _workspace(_L.dg_pack_workspace_bytes(N, B, total), dev, workspace)
+
+    def call(cap, packed, packed_ids, ptr, ptr_host, loc, unique, unique_cap, flags, sz, tm):
+        head = (_ptr(feats), N, R, _ptr(cache_slot), B, _ptr(nodes), stride,
+                counts.ctypes.data_as(_lib.I64P), cap, packed, packed_ids, ptr,
+                ptr_host.ctypes.data_as(_lib.I64P), loc, unique, unique_cap,
+                _ptr(membership), _ptr(member_lines), flags)
+        if no_alloc:
+            return _L.dg_pack_group_noalloc(*head, _stream(stream), ctypes.byref(sz))
+        return _L.dg_pack_group(*head, _ptr(ws), ws.numel(), _stream(stream),
+                                _stream(rows_stream) if rows_stream is not None else None,
+                                ctypes.byref(sz), ctypes.byref(tm) if tm is not None else None)
+
     ptr_host = np.zeros(B + 1, dtype=np.int64)
     sz, tm = Sizes(), Timing()
     if out is None and tables_only:
@@ -244,12 +262,7 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
         loc = torch.empty((B, stride), dtype=torch.int32, device=dev)
         ptr = torch.empty(B + 1, dtype=torch.int64, device=dev)
         # size query: a zero packed capacity returns the exact sizes needed
-        st = _L.dg_pack_group(_ptr(feats), N, R, _ptr(cache_slot), B, _ptr(nodes), stride,
-                              counts.ctypes.data_as(_lib.I64P), 0, None, None, _ptr(ptr),
-                              ptr_host.ctypes.data_as(_lib.I64P), _ptr(loc), None, 0,
-                              _ptr(membership), _ptr(member_lines), 0, _ptr(ws), ws.numel(),
-                              _stream(stream), None,
-                              ctypes.byref(sz), None)
+        st = call(0, None, None, _ptr(ptr), ptr_host, _ptr(loc), None, 0, 0, sz, None)
         if st not in (DG_OK, DG_ECAPACITY):
             check(st)
         rows, nu = sz.packed_rows, sz.unique_nodes
@@ -262,18 +275,12 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
     cap = out.packed_ids.numel()
     if out.packed is not None and out.packed.numel() < cap * R:
         raise ValueError("packed buffer smaller than packed_ids")
-    st = _L.dg_pack_group(_ptr(feats), N, R, _ptr(cache_slot), B, _ptr(nodes), stride,
-                          counts.ctypes.data_as(_lib.I64P), cap, _ptr(out.packed),
-                          _ptr(out.packed_ids), _ptr(out.packed_ptr),
-                          out.packed_ptr_host.ctypes.data_as(_lib.I64P), _ptr(out.loc),
-                          _ptr(out.unique), out.unique.numel() if out.unique is not None else 0,
-                          _ptr(membership), _ptr(member_lines),
-                          (_lib.DG_PACK_CLEAR_MEMBERSHIP if clear_membership else 0)
-                          | (_lib.DG_PACK_ROWS_STREAM if rows_stream is not None else 0),
-                          _ptr(ws), ws.numel(), _stream(stream),
-                          _stream(rows_stream) if rows_stream is not None else None,
-                          ctypes.byref(sz),
-                          ctypes.byref(tm) if timing else None)
+    st = call(cap, _ptr(out.packed), _ptr(out.packed_ids), _ptr(out.packed_ptr),
+              out.packed_ptr_host, _ptr(out.loc), _ptr(out.unique),
+              out.unique.numel() if out.unique is not None else 0,
+              (_lib.DG_PACK_CLEAR_MEMBERSHIP if clear_membership else 0)
+              | (_lib.DG_PACK_ROWS_STREAM if rows_stream is not None else 0),
+              sz, tm if timing else None)
     out.sizes = sz.as_dict()
     check(st)
     out.timing = tm.as_dict() if timing else None

@@ -170,6 +170,8 @@ inline int lt_bits_for(int64_t entries) {
 // host thread (allocated on first use, held until the process ends), which
 // shortens each round trip; otherwise the copy goes to dst directly.
 int read_to_host(void *dst, const void *src, size_t bytes, hipStream_t s);
+// The same straight into dst (pageable or not), with no buffer of the library's.
+int read_to_host_unstaged(void *dst, const void *src, size_t bytes, hipStream_t s);
 
 // ---------------------------------------------------------------- side stream
 // A second stream per host thread and device, for kernels a call runs beside

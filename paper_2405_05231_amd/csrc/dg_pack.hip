@@ -11,9 +11,14 @@
 // it goes to.  The gather then reads each row of U_nc once and writes it to
 // all its destination rows.
 #include <initializer_list>
+#include <mutex>
 #include <string.h>
 
 #include "dg_rows.h"
+
+// Scratch of dg_pack_group_noalloc (see scratch_address below).
+constexpr size_t NOALLOC_SCRATCH_BYTES = (size_t)256 << 20;
+static __device__ __align__(256) unsigned char scratch[NOALLOC_SCRATCH_BYTES];
 
 namespace dg {
 namespace {
@@ -257,19 +262,20 @@ void carve_pack(PackWs &w, Carve &c, int64_t N, int B, int64_t total_nodes) {
   mask_scan_carve(w.ms, c);
 }
 
-int read_err(uint32_t *err, hipStream_t s) {
+// Device-to-host read of a call's counts: through the library's page-locked
+// buffer, or (no_alloc) straight into the host variable.
+int read_back(void *dst, const void *src, size_t bytes, hipStream_t s, bool no_alloc) {
+  return no_alloc ? read_to_host_unstaged(dst, src, bytes, s) : read_to_host(dst, src, bytes, s);
+}
+
+int read_err(uint32_t *err, hipStream_t s, bool no_alloc) {
   uint32_t bits = 0;
-  DG_TRY(read_to_host(&bits, err, sizeof(bits), s));
+  DG_TRY(read_back(&bits, err, sizeof(bits), s, no_alloc));
   if (bits) return set_error(DG_EINVAL, "invalid input data: %s", describe_device_error(bits));
   return DG_OK;
 }
 
-}  // namespace
-}  // namespace dg
-
-using namespace dg;
-
-extern "C" size_t dg_pack_workspace_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes) {
+size_t pack_ws_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes) {
   if (num_nodes < 1 || B < 1 || B > DG_MAX_BATCHES || total_nodes < 0) return 0;
   Carve c(nullptr);
   PackWs w;
@@ -277,15 +283,40 @@ extern "C" size_t dg_pack_workspace_bytes(int64_t num_nodes, int32_t B, int64_t 
   return c.used;
 }
 
-extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
-                             const int32_t *cache_slot, int32_t B, const int32_t *nodes,
-                             int64_t node_stride, const int64_t *node_count, int64_t packed_cap,
-                             void *packed, int32_t *packed_ids, int64_t *packed_ptr,
-                             int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique,
-                             int64_t unique_cap, uint64_t *membership,
-                             const uint8_t *member_lines, uint32_t flags,
-                             void *ws, size_t ws_bytes, hipStream_t stream,
-                             hipStream_t rows_stream, dg_sizes *sizes, dg_timing *timing) {
+// ---------------------------------------------------------------- fixed scratch
+// Scratch of dg_pack_group_noalloc: a file-scope device array (one copy per GPU,
+// held until the process ends).  Host code never passes the array's name to a
+// kernel (on the host it is only a stand-in for the symbol): it asks the runtime
+// for the array's device address once per device and uses that.
+constexpr int NOALLOC_DEVICES = 16;
+
+int scratch_address(void **out) {
+  static std::mutex mu;
+  static void *addr[NOALLOC_DEVICES] = {};
+  int dev = 0;
+  DG_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= NOALLOC_DEVICES)
+    return set_error(DG_EHIP, "dg_pack_group_noalloc: device index %d out of range", dev);
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return set_error(DG_EHIP, "dg_pack_group_noalloc: hipGetSymbolAddress failed: %s",
+                       hipGetErrorString(e));
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return DG_OK;
+}
+
+int pack_impl(const void *feats, int64_t N, int64_t row_bytes, const int32_t *cache_slot,
+              int32_t B, const int32_t *nodes, int64_t node_stride, const int64_t *node_count,
+              int64_t packed_cap, void *packed, int32_t *packed_ids, int64_t *packed_ptr,
+              int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique, int64_t unique_cap,
+              uint64_t *membership, const uint8_t *member_lines, uint32_t flags, void *ws,
+              size_t ws_bytes, hipStream_t stream, hipStream_t rows_stream, dg_sizes *sizes,
+              dg_timing *timing, bool no_alloc) {
   if (!feats || !cache_slot || !nodes || !node_count || !packed_ptr || !packed_ptr_host ||
       !loc || !sizes)
     return set_error(DG_EINVAL, "dg_pack_group: null pointer argument");
@@ -316,7 +347,12 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
   const int64_t total = L.start[B];
   if (packed_cap > 0 && !packed_ids)
     return set_error(DG_EINVAL, "dg_pack_group: null packed_ids");
-  const size_t need_ws = dg_pack_workspace_bytes(N, B, total);
+  const size_t need_ws = pack_ws_bytes(N, B, total);
+  if (no_alloc && need_ws > ws_bytes)
+    return set_error(DG_EWORKSPACE,
+                     "dg_pack_group_noalloc: these sizes need %zu bytes of scratch, above its "
+                     "%zu bytes",
+                     need_ws, ws_bytes);
   if (!ws || ws_bytes < need_ws || ((uintptr_t)ws & 255))
     return set_error(DG_EWORKSPACE, "dg_pack_group: workspace needs %zu bytes, 256-aligned",
                      need_ws);
@@ -355,7 +391,7 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
   w.ms.cache_slot = cache_slot;
   w.ms.err_stage = w.ms.totals + mc_rows(B);  // staged by the count pass's row scan
   if ((rc = mask_scan_count(w.ms, s))) return rc;
-  DG_TRY(read_to_host(totals, w.ms.totals, sizeof(int64_t) * (mc_rows(B) + 1), s));
+  DG_TRY(read_back(totals, w.ms.totals, sizeof(int64_t) * (mc_rows(B) + 1), s, no_alloc));
   if (totals[mc_rows(B)])
     return set_error(DG_EINVAL, "invalid input data: %s",
                      describe_device_error((uint32_t)totals[mc_rows(B)]));
@@ -405,7 +441,7 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
     if ((rc = launch_fanout(feats, w.unc_ids, w.unc_off, sizes->unique_packed, rows, w.pairdest,
                             row_bytes, packed, rows_stream)))
       return rc;
-  } else if (!timing && packed && total > 0) {
+  } else if (!timing && !no_alloc && packed && total > 0) {
     DG_TRY(side_stream(&side));
     DG_HIP(hipEventRecord(side->fork, s));
     DG_HIP(hipStreamWaitEvent(side->s, side->fork, 0));
@@ -424,7 +460,7 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
     return rc;
   if (side) DG_HIP(hipStreamWaitEvent(s, side->join, 0));
   const int e4 = tm.mark();
-  if ((rc = read_err(w.err, s))) return rc;
+  if ((rc = read_err(w.err, s, no_alloc))) return rc;
   if (timing) {
     timing->mark_ms = tm.ms(e0, e1);
     timing->order_ms = tm.ms(e1, e2);
@@ -433,4 +469,48 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
     timing->total_ms = tm.ms(e0, e4);
   }
   return DG_OK;
+}
+
+}  // namespace
+}  // namespace dg
+
+using namespace dg;
+
+extern "C" size_t dg_pack_workspace_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes) {
+  return pack_ws_bytes(num_nodes, B, total_nodes);
+}
+
+extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
+                             const int32_t *cache_slot, int32_t B, const int32_t *nodes,
+                             int64_t node_stride, const int64_t *node_count, int64_t packed_cap,
+                             void *packed, int32_t *packed_ids, int64_t *packed_ptr,
+                             int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique,
+                             int64_t unique_cap, uint64_t *membership,
+                             const uint8_t *member_lines, uint32_t flags,
+                             void *ws, size_t ws_bytes, hipStream_t stream,
+                             hipStream_t rows_stream, dg_sizes *sizes, dg_timing *timing) {
+  return pack_impl(feats, N, row_bytes, cache_slot, B, nodes, node_stride, node_count,
+                   packed_cap, packed, packed_ids, packed_ptr, packed_ptr_host, loc, group_unique,
+                   unique_cap, membership, member_lines, flags, ws, ws_bytes, stream, rows_stream,
+                   sizes, timing, false);
+}
+
+extern "C" size_t dg_pack_noalloc_scratch_bytes(void) { return NOALLOC_SCRATCH_BYTES; }
+
+extern "C" int dg_pack_group_noalloc(const void *feats, int64_t N, int64_t row_bytes,
+                                     const int32_t *cache_slot, int32_t B, const int32_t *nodes,
+                                     int64_t node_stride, const int64_t *node_count,
+                                     int64_t packed_cap, void *packed, int32_t *packed_ids,
+                                     int64_t *packed_ptr, int64_t *packed_ptr_host, int32_t *loc,
+                                     int32_t *group_unique, int64_t unique_cap,
+                                     uint64_t *membership, const uint8_t *member_lines,
+                                     uint32_t flags, hipStream_t stream, dg_sizes *sizes) {
+  if (flags & DG_PACK_ROWS_STREAM)
+    return set_error(DG_EINVAL, "dg_pack_group_noalloc: DG_PACK_ROWS_STREAM is not available");
+  void *ws = nullptr;
+  DG_TRY(scratch_address(&ws));
+  return pack_impl(feats, N, row_bytes, cache_slot, B, nodes, node_stride, node_count,
+                   packed_cap, packed, packed_ids, packed_ptr, packed_ptr_host, loc, group_unique,
+                   unique_cap, membership, member_lines, flags, ws, NOALLOC_SCRATCH_BYTES, stream,
+                   nullptr, sizes, nullptr, true);
 }

@@ -54,6 +54,14 @@ int read_to_host(void *dst, const void *src, size_t bytes, hipStream_t s) {
   return DG_OK;
 }
 
+// The same without the page-locked buffer: the copy goes to dst directly (for
+// entry points that take no resources of their own).
+int read_to_host_unstaged(void *dst, const void *src, size_t bytes, hipStream_t s) {
+  DG_HIP(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, s));
+  DG_HIP(hipStreamSynchronize(s));
+  return DG_OK;
+}
+
 // ---------------------------------------------------------------- side stream
 int side_stream(SideStream **out) {
   constexpr int MAX_DEV = 16;
