@@ -19,7 +19,9 @@ import argparse
 import hashlib
 import json
 import os
+import queue
 import sys
+import threading
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -90,6 +92,12 @@ def main():
     ap.add_argument("--rows-inline", action="store_true",
                     help="pipelined region: keep packing's row copy inside the packing call "
                          "instead of queueing it on the assembly stream (comparison)")
+    ap.add_argument("--no-loc-handoff", action="store_true",
+                    help="packing builds every address-table entry itself, instead of "
+                         "completing the ones sampling wrote for cached nodes (comparison)")
+    ap.add_argument("--asm-inline", action="store_true",
+                    help="pipelined region: issue each step's assembly from the main thread "
+                         "instead of a host thread of its own (comparison)")
     ap.add_argument("--fill-masks", action="store_true",
                     help="clear the membership mask and the sampler's state with full fills "
                          "in every sampling call, instead of the clearing flags (comparison)")
@@ -224,7 +232,7 @@ def main():
     # step's own sizes; its host time is reported.
     s_asm = torch.cuda.Stream(device=dev)
     asm_done = [torch.cuda.Event(), torch.cuda.Event()]
-    pack_done = torch.cuda.Event()
+    pack_done = [torch.cuda.Event(), torch.cuda.Event()]
     # timing events, created (by a first record) before any timed region
     nev = max(args.steps, args.warmup)
     ev_pool = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -232,9 +240,59 @@ def main():
     for a_, b_ in ev_pool:
         a_.record(s_asm)
         b_.record(s_asm)
-    for e_ in asm_done + [pack_done]:
+    for e_ in asm_done + pack_done:
         e_.record(s_asm)
     torch.cuda.synchronize()
+
+    class Assembler:
+        """Issues each pipelined step's assembly from a host thread of its own,
+        as the trainer stage of the paper's pipeline (§5.3) consumes assembled
+        batches while the next group is sampled: the main thread goes on to
+        the next sampling call while the B launches are enqueued.  Steps are
+        handed over in order; a packing output set (slot) is packed again only
+        after the assembly that reads it has been enqueued."""
+
+        def __init__(self):
+            self.q = queue.Queue()
+            self.free = [threading.Event(), threading.Event()]
+            for f in self.free:
+                f.set()
+            self.err = None
+            self.enqueue_s = []
+            self.t = threading.Thread(target=self._loop, daemon=True)
+            self.t.start()
+
+        def _loop(self):
+            while True:
+                item = self.q.get()
+                if item is None:
+                    self.q.task_done()
+                    return
+                slot, p_out, counts, e0, e1 = item
+                try:
+                    t0 = time.perf_counter()
+                    s_asm.wait_event(pack_done[slot])
+                    e0.record(s_asm)
+                    dg.assemble_batches(w.cache, p_out, counts, ybuf, stream=s_asm)
+                    e1.record(s_asm)
+                    asm_done[slot].record(s_asm)
+                    self.enqueue_s.append(time.perf_counter() - t0)
+                except BaseException as e:  # reported by the main thread
+                    self.err = e
+                finally:
+                    self.free[slot].set()
+                    self.q.task_done()
+
+        def drain(self):
+            self.q.join()
+            if self.err is not None:
+                raise self.err
+
+        def close(self):
+            self.q.put(None)
+            self.t.join()
+
+    asm_thread = None if args.asm_inline else Assembler()
 
     # Mask state across steps: each sampling call leaves its workspace state
     # clear (DG_SAMPLE_EXIT_CLEAR) and each packing call clears the membership
@@ -256,33 +314,46 @@ def main():
         for k, g in enumerate(gs):
             slot = k & 1
             t0 = time.perf_counter()
+            # Sampling writes the cached nodes' address-table entries into this
+            # step's packing set (pr2[slot].loc), so the assembly that last read
+            # that set must have been enqueued (by the assembly thread) and run.
+            threaded = pipelined and asm_thread is not None
+            if threaded:
+                asm_thread.free[slot].wait()
+                asm_thread.free[slot].clear()
+            stream.wait_event(asm_done[slot])
             entry_clear = clearing and state["clear"]
             state["clear"] = False
+            handoff = not args.no_loc_handoff
             s_out = dg.sample_group(w.offsets, w.indices, groups[g], fan, w.rng_seed,
                                     batch_base=g * B, out=sr, workspace=ws_s, membership=mem,
                                     direct=True, stream=stream, exit_clear=clearing,
                                     entry_clear=entry_clear, member_lines=lines,
-                                    timing=args.sample_timing)
+                                    timing=args.sample_timing,
+                                    cache_slot=w.cache_slot if handoff else None,
+                                    loc=pr2[slot].loc if handoff else None)
             counts = s_out.node_count.copy()
             if args.sample_timing:
                 samp_phases[pipelined].append(dict(s_out.timing))
             t1 = time.perf_counter()
-            stream.wait_event(asm_done[slot])  # the assembly that last read pr2[slot]
             rows_async = pipelined and not args.rows_inline and not args.timed_pack
             p_out = dg.pack_group(w.feats, w.cache_slot, s_out.nodes, counts, out=pr2[slot],
                                   workspace=ws_p2[slot], timing=record or args.timed_pack,
                                   membership=mem, clear_membership=clearing,
                                   stream=stream, rows_stream=s_asm if rows_async else None,
-                                  member_lines=lines)
+                                  member_lines=lines, loc_pending=handoff)
             state["clear"] = clearing
             t2 = time.perf_counter()
             e0, e1 = ev_pool[k % nev]
-            pack_done.record(stream)
-            s_asm.wait_event(pack_done)
-            e0.record(s_asm)
-            dg.assemble_batches(w.cache, p_out, counts, ybuf, stream=s_asm)
-            e1.record(s_asm)
-            asm_done[slot].record(s_asm)
+            pack_done[slot].record(stream)
+            if threaded:
+                asm_thread.q.put((slot, p_out, counts, e0, e1))
+            else:
+                s_asm.wait_event(pack_done[slot])
+                e0.record(s_asm)
+                dg.assemble_batches(w.cache, p_out, counts, ybuf, stream=s_asm)
+                e1.record(s_asm)
+                asm_done[slot].record(s_asm)
             t3 = time.perf_counter()
             if not pipelined:
                 e1.synchronize()
@@ -292,12 +363,16 @@ def main():
                                             ("packed_rows", "unique_nodes", "unique_packed")}})
             if record:
                 gather_ms.append(p_out.timing["gather_ms"])
+        if asm_thread is not None:
+            asm_thread.drain()
         torch.cuda.synchronize()
         return marks, gather_ms, evs, steps
 
     def timed(gs, pipelined):
         run(gs[:args.warmup], pipelined, False)
         torch.cuda.synchronize()
+        if asm_thread is not None:
+            asm_thread.enqueue_s.clear()
         t_start = time.perf_counter()
         # per-phase timing (which runs the packing call's phases one after the
         # other) only in the serial region
@@ -307,7 +382,8 @@ def main():
         for g, st in zip(gs[args.warmup:], res[3]):  # the pre-pass saw the same sizes
             if any(st[k] != pre[g][k] for k in ("total_nodes", "total_edges", "packed_rows")):
                 raise RuntimeError(f"group {g}: sizes differ from the pre-pass")
-        return (t_total,) + res
+        enq = list(asm_thread.enqueue_s) if (asm_thread is not None and pipelined) else []
+        return (t_total,) + res + (enq,)
 
     def feature_bytes(st):
         """Feature bytes the method must move for one group: packing reads each
@@ -319,14 +395,16 @@ def main():
     # over groups of its own
     serial_groups = list(range(n_region))
     pipe_groups = list(range(n_region, 2 * n_region))
-    t_serial, marks, gather_ms, asm_ms, steps_s = timed(serial_groups, False)
+    t_serial, marks, gather_ms, asm_ms, steps_s, _ = timed(serial_groups, False)
     if args.no_pipeline:
-        t_total, marks_p, steps_p = t_serial, marks, steps_s
+        t_total, marks_p, steps_p, enq_p = t_serial, marks, steps_s, []
     else:
-        t_total, marks_p, _, _, steps_p = timed(pipe_groups, True)
+        t_total, marks_p, _, _, steps_p, enq_p = timed(pipe_groups, True)
     # secondary figure: the workload's own group repeated in every step (the
     # same index working set and hot rows each time), pipelined
-    t_rep, _, _, _, steps_r = timed([0] * n_region, not args.no_pipeline)
+    t_rep, _, _, _, steps_r, _ = timed([0] * n_region, not args.no_pipeline)
+    if asm_thread is not None:
+        asm_thread.close()
     samp_ms = [1e3 * m[0] for m in marks]
     pack_ms = [1e3 * m[1] for m in marks]
 
@@ -382,11 +460,17 @@ def main():
         "pipelined": ("no: --no-pipeline, value is the serial rate" if args.no_pipeline else
                       "assembly of step k (second stream) overlaps sampling and packing of "
                       "step k+1; the serial figures below wait for each step's assembly"),
-        "assembly_issue": "direct calls: one dg_assemble_batches call (B launches) per step",
+        "assembly_issue": ("direct calls: one dg_assemble_batches call (B launches) per step, "
+                           + ("issued by the main thread" if asm_thread is None else
+                              "issued by a host thread of its own in the pipelined region "
+                              "(the trainer side), by the main thread in the serial region")),
         "pack_rows": ("pipelined region: packing's row copy queued on the assembly stream "
                       "(DG_PACK_ROWS_STREAM)" if not (args.rows_inline or args.timed_pack
                                                       or args.no_pipeline)
                       else "inside the packing call"),
+        "address_tables": ("sampling writes the cached nodes' entries as it lists them; "
+                           "packing completes the others (DG_PACK_LOC_PENDING)"
+                           if not args.no_loc_handoff else "built by packing alone"),
         "member_lines": ("packing reads only the membership lines sampling marked"
                          if lines is not None else "packing reads every membership word"),
         "mask_clearing": ("clearing flags: packing clears the membership words it reads and "
@@ -401,8 +485,11 @@ def main():
                                           / 1e9, 2)},
         "pipelined_phases_ms": {"sample": round(1e3 * float(np.mean([m[0] for m in marks_p])), 3),
                                 "pack": round(1e3 * float(np.mean([m[1] for m in marks_p])), 3),
-                                "host_enqueue_assembly": round(
-                                    1e3 * float(np.mean([m[2] for m in marks_p])), 3)},
+                                "host_enqueue_assembly": round(1e3 * float(np.mean(
+                                    enq_p or [m[2] for m in marks_p])), 3),
+                                "host_enqueue_assembly_on": ("the assembly thread"
+                                                             if asm_thread is not None
+                                                             else "the main thread")},
         "sampled_edges_per_s": round(edges / (np.sum(samp_ms) * 1e-3), 1),
         "phases_ms": {"sample": round(float(np.mean(samp_ms)), 3),
                       "pack": round(float(np.mean(pack_ms)), 3),

@@ -143,6 +143,15 @@ extern "C" {
                                        must be zero already) */
 #define DG_PACK_ROWS_STREAM 2u      /* enqueue the row copy on `rows_stream`, behind the
                                        tables, and return without waiting for it */
+#define DG_PACK_LOC_PENDING 4u      /* `loc` already holds what dg_sample_group wrote
+                                       into it for these lists and this cache_slot (see
+                                       DG_LOC_PENDING): the call completes only the
+                                       pending entries and keeps the others */
+
+/* Address-table entry that dg_sample_group leaves for dg_pack_group to fill in
+ * (a node that is not cached: its rank in the packed chunk is known only once
+ * the whole group is sampled). */
+#define DG_LOC_PENDING 0x7fffffff
 
 typedef enum dg_status {
   DG_OK = 0,
@@ -260,6 +269,16 @@ size_t dg_member_lines_bytes(int64_t num_nodes);
  *              lines.  The last hop's compaction writes it as it reads every
  *              word; when that hop reads only part of the words (small hops),
  *              a pass over the membership words writes it instead.
+ *   cache_slot, loc  optional, both or neither: the address tables of §6 for
+ *              the cached nodes, written as the lists are built.  cache_slot
+ *              [N] int32 as dg_pack_group takes it (-1 = not cached); loc
+ *              [B*node_cap] int32, laid out as nodes: for each entry j of
+ *              nodes_b, loc[b*node_cap+j] = -(cache_slot[u]+1) if its node u
+ *              is cached, else DG_LOC_PENDING.  dg_pack_group, given the same
+ *              lists (node_stride = node_cap), the same cache_slot, this loc and
+ *              DG_PACK_LOC_PENDING, completes the pending entries, so that no
+ *              cache slot is looked up per entry there.  A cache_slot value
+ *              below -1 is reported (DG_EINVAL).
  *   sizes      [host] filled on DG_OK and DG_ECAPACITY.
  *   timing     [host] optional (NULL = not measured).
  * node_cap must be below 2^27.
@@ -273,8 +292,9 @@ int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S,
                     uint64_t rng_seed, uint32_t flags, int64_t node_cap, int32_t *nodes,
                     int64_t *hop_ptr, int64_t edge_cap, int32_t *edge_src,
                     int32_t *edge_dst, int64_t *edge_ptr, uint64_t *membership,
-                    uint8_t *member_lines, void *ws, size_t ws_bytes, hipStream_t stream,
-                    dg_sizes *sizes, dg_timing *timing);
+                    uint8_t *member_lines, const int32_t *cache_slot, int32_t *loc,
+                    void *ws, size_t ws_bytes, hipStream_t stream, dg_sizes *sizes,
+                    dg_timing *timing);
 
 /* Workspace bytes dg_pack_group needs for N nodes, B batches whose node lists
  * hold `total_nodes` entries in all. */
@@ -305,7 +325,13 @@ size_t dg_pack_workspace_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes
  *               dg_sample_group writes it: words of lines whose byte is 0 are
  *               not read.  A member in an unmarked line is missed, which the
  *               pair-count check reports (DG_EINVAL).
- *   flags       0, or an OR of DG_PACK_CLEAR_MEMBERSHIP and DG_PACK_ROWS_STREAM.
+ *   flags       0, or an OR of DG_PACK_CLEAR_MEMBERSHIP, DG_PACK_ROWS_STREAM and
+ *               DG_PACK_LOC_PENDING.  With DG_PACK_LOC_PENDING, loc must hold
+ *               what dg_sample_group wrote for these lists and this cache_slot:
+ *               entries that are not DG_LOC_PENDING are kept as they are (a
+ *               cached node's entry), and a pending entry whose node turns out
+ *               to be cached, or to lack its membership bit, is reported
+ *               (DG_EINVAL).
  *   rows_stream used only with DG_PACK_ROWS_STREAM (and packed != NULL): the row
  *               copy, which reads feats and the workspace and writes packed, is
  *               enqueued there after an event that follows the tables on

@@ -110,7 +110,8 @@ def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tens
                  workspace: torch.Tensor | None = None, stream=None, timing: bool = False,
                  membership: torch.Tensor | None = None, layered: bool = False,
                  direct: bool = False, entry_clear: bool = False,
-                 exit_clear: bool = False, member_lines: torch.Tensor | None = None
+                 exit_clear: bool = False, member_lines: torch.Tensor | None = None,
+                 cache_slot: torch.Tensor | None = None, loc: torch.Tensor | None = None
                  ) -> SampleResult:
     """Group sampling (dg_sample_group).  seeds: int32 [B, S] on the GPU.
     membership: optional int64 [N] tensor that receives the (node, batch)
@@ -121,7 +122,10 @@ def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tens
     loop over groups that reuses `workspace` and `membership`, packing each
     group with clear_membership=True, skips two mask clears per group).
     member_lines: optional uint8 tensor of member_lines_bytes(N) bytes that
-    receives a byte per 8 nodes, non-zero iff one of them is in some list."""
+    receives a byte per 8 nodes, non-zero iff one of them is in some list.
+    cache_slot, loc: int32 [N] and int32 [B, node_cap] (both or neither): loc
+    receives the address-table entries of cached nodes, DG_LOC_PENDING for the
+    others, for pack_group(..., loc_pending=True) to complete."""
     dev = offsets.device
     _need(offsets, "offsets", torch.int64)
     _need(indices, "indices", torch.int32, dev)
@@ -136,6 +140,13 @@ def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tens
         _need(member_lines, "member_lines", torch.uint8, dev)
         if member_lines.numel() < member_lines_bytes(offsets.numel() - 1):
             raise ValueError("member_lines holds fewer than member_lines_bytes(N) bytes")
+    if (cache_slot is None) != (loc is None):
+        raise ValueError("cache_slot and loc go together")
+    if cache_slot is not None:
+        _need(cache_slot, "cache_slot", torch.int32, dev)
+        _need(loc, "loc", torch.int32, dev)
+        if cache_slot.numel() != offsets.numel() - 1:
+            raise ValueError("cache_slot must hold one entry per node")
     B, S = seeds.shape
     N = offsets.numel() - 1
     E = indices.numel()
@@ -153,6 +164,8 @@ def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tens
             edge_src=torch.empty((B, max(edge_cap, 1)), dtype=torch.int32, device=dev),
             edge_dst=torch.empty((B, max(edge_cap, 1)), dtype=torch.int32, device=dev),
             edge_ptr=np.zeros((B, K + 1), dtype=np.int64), sizes={}, timing=None)
+    if loc is not None and (loc.dim() != 2 or tuple(loc.shape) != (B, node_cap)):
+        raise ValueError("loc must be [B, node_cap], laid out as the node lists")
     flags = sample_flags(layered, direct, entry_clear, exit_clear)
     ws_bytes = _L.dg_sample_workspace_bytes(N, B, node_cap, edge_cap, flags)
     ws = _workspace(ws_bytes, dev, workspace)
@@ -163,7 +176,8 @@ def sample_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tens
         ctypes.byref(g), _ptr(seeds), B, S, batch_base, fo, K, rng_seed & (2**64 - 1),
         flags, node_cap, _ptr(out.nodes), out.hop_ptr.ctypes.data_as(_lib.I64P), edge_cap,
         _ptr(out.edge_src), _ptr(out.edge_dst), out.edge_ptr.ctypes.data_as(_lib.I64P),
-        _ptr(membership), _ptr(member_lines), _ptr(ws), ws.numel(), _stream(stream),
+        _ptr(membership), _ptr(member_lines), _ptr(cache_slot), _ptr(loc), _ptr(ws),
+        ws.numel(), _stream(stream),
         ctypes.byref(sz),
         ctypes.byref(tm) if timing else None)
     out.sizes = sz.as_dict()
@@ -198,7 +212,8 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
                workspace: torch.Tensor | None = None, stream=None, timing: bool = False,
                membership: torch.Tensor | None = None, tables_only: bool = False,
                clear_membership: bool = False, rows_stream=None,
-               member_lines: torch.Tensor | None = None, no_alloc: bool = False) -> PackResult:
+               member_lines: torch.Tensor | None = None, no_alloc: bool = False,
+               loc_pending: bool = False) -> PackResult:
     """Batched packing (dg_pack_group).  nodes: int32 [B, node_stride];
     node_count: the B list lengths (host).  membership: optional int64 [N]
     mask from sample_group (skips rebuilding it).  tables_only: build the
@@ -210,7 +225,9 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
     member_lines: the map sample_group wrote (with membership): only the
     words of marked lines are read.  no_alloc: call dg_pack_group_noalloc
     (scratch inside the library, no workspace; no timing or rows_stream);
-    pass `out` as well for a call that allocates nothing at all."""
+    pass `out` as well for a call that allocates nothing at all.
+    loc_pending: DG_PACK_LOC_PENDING, out.loc already holds what sample_group
+    wrote into it for these lists and this cache_slot (`out` required)."""
     dev = feats.device
     _need(feats, "feats", None)
     _need(cache_slot, "cache_slot", torch.int32, dev)
@@ -230,6 +247,8 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
     if counts.shape[0] != B:
         raise ValueError("node_count must have one entry per batch")
     total = int(counts.sum())
+    if loc_pending and (out is None or tuple(out.loc.shape) != (B, stride)):
+        raise ValueError("loc_pending needs `out` whose loc is laid out as the node lists")
     if no_alloc:
         if timing or rows_stream is not None:
             raise ValueError("no_alloc takes neither timing nor rows_stream")
@@ -279,7 +298,8 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
               out.packed_ptr_host, _ptr(out.loc), _ptr(out.unique),
               out.unique.numel() if out.unique is not None else 0,
               (_lib.DG_PACK_CLEAR_MEMBERSHIP if clear_membership else 0)
-              | (_lib.DG_PACK_ROWS_STREAM if rows_stream is not None else 0),
+              | (_lib.DG_PACK_ROWS_STREAM if rows_stream is not None else 0)
+              | (_lib.DG_PACK_LOC_PENDING if loc_pending else 0),
               sz, tm if timing else None)
     out.sizes = sz.as_dict()
     check(st)

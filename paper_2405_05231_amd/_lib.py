@@ -15,6 +15,8 @@ DG_SAMPLE_EXIT_CLEAR = 4
 DG_SAMPLE_ENTRY_CLEAR = 8
 DG_PACK_CLEAR_MEMBERSHIP = 1
 DG_PACK_ROWS_STREAM = 2
+DG_PACK_LOC_PENDING = 4
+DG_LOC_PENDING = 0x7fffffff
 DG_MAX_BATCHES = 64
 STATUS_NAMES = {0: "DG_OK", -1: "DG_EINVAL", -2: "DG_ECAPACITY", -3: "DG_EHIP",
                 -4: "DG_EWORKSPACE"}
@@ -61,7 +63,7 @@ SIGNATURES = {
     "dg_member_lines_bytes": (SZ, [I64]),
     "dg_sample_group": (ctypes.c_int, [ctypes.POINTER(Csr), VP, I32, I32, I64, I32P, I32, U64,
                                        ctypes.c_uint32, I64, VP, I64P, I64, VP, VP, I64P, VP,
-                                       VP, VP, SZ, VP,
+                                       VP, VP, VP, VP, SZ, VP,
                                        ctypes.POINTER(Sizes), ctypes.POINTER(Timing)]),
     "dg_pack_workspace_bytes": (SZ, [I64, I32, I64]),
     "dg_pack_group": (ctypes.c_int, [VP, I64, I64, VP, I32, VP, I64, I64P, I64, VP, VP, VP, I64P,

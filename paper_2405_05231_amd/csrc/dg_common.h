@@ -260,10 +260,15 @@ struct MaskScan {
   const uint8_t *touched;            // nullable: a byte per 2^MC_TOUCH_SHIFT nodes
                                      // (mc_touch_bytes(N) in all); nodes whose byte
                                      // is 0 hold no bit to list (not read)
+  // sampling only (both or neither): for each listed pair, the address-table
+  // entry at the same index as its seg_out slot: -(loc_slot[u]+1) for a cached
+  // node, DG_LOC_PENDING otherwise
+  const int32_t *loc_slot;
+  int32_t *loc_out;
   // The write pass runs in one of two modes: packing (pairdest set: seg_out,
   // unc_ids, unc_off, nodeoff required, uniq_out optional, cached nodes left out
   // of the lists) or sampling (pairdest NULL: prev and seg_out required,
-  // local_out optional, no cache_slot).
+  // local_out and loc_slot/loc_out optional, no cache_slot).
 };
 
 

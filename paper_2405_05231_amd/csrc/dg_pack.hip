@@ -67,6 +67,10 @@ __global__ void k_packed_ptr(const int64_t *totals, int B, int64_t *packed_ptr) 
 // node has no such pair (a given membership mask that misses it) is reported,
 // so no unchecked address reaches the table.  The mask itself is not read
 // here: the count pass may have cleared it already.
+// PENDING: loc already holds the sampler's entries; only entries equal to
+// DG_LOC_PENDING (non-cached nodes) are completed, and no cache slot is read
+// (a pending node that is cached has no pair, and is reported as above).
+template <bool PENDING>
 __global__ __launch_bounds__(THREADS) void k_build_loc(Lists L, const int32_t *nodes,
                                                        const int32_t *cache_slot,
                                                        const int64_t *nodeoff,
@@ -78,12 +82,13 @@ __global__ __launch_bounds__(THREADS) void k_build_loc(Lists L, const int32_t *n
   if (i >= L.start[L.B]) return;
   const int b = find_batch_wave(L.start, L.B, i);
   const int64_t at = (int64_t)b * L.stride + (i - L.start[b]);
+  if (PENDING && loc[at] != (int32_t)DG_LOC_PENDING) return;
   const int32_t u = nodes[at];
   if (u < 0 || (int64_t)u >= N) {
     atomicOr(err, ERR_NODE_RANGE);
     return;
   }
-  const int32_t sl = cache_slot[u];
+  const int32_t sl = PENDING ? -1 : cache_slot[u];
   int32_t out = 0;
   if (sl >= 0) {
     out = -(sl + 1);
@@ -324,7 +329,7 @@ int pack_impl(const void *feats, int64_t N, int64_t row_bytes, const int32_t *ca
       node_stride < 0 || packed_cap < 0 || unique_cap < 0)
     return set_error(DG_EINVAL, "dg_pack_group: bad sizes (N=%lld row_bytes=%lld B=%d)",
                      (long long)N, (long long)row_bytes, B);
-  if (flags & ~(DG_PACK_CLEAR_MEMBERSHIP | DG_PACK_ROWS_STREAM))
+  if (flags & ~(DG_PACK_CLEAR_MEMBERSHIP | DG_PACK_ROWS_STREAM | DG_PACK_LOC_PENDING))
     return set_error(DG_EINVAL, "dg_pack_group: unknown flags 0x%x", flags);
   const bool clear_membership = flags & DG_PACK_CLEAR_MEMBERSHIP;
   if (clear_membership && !membership)
@@ -447,9 +452,14 @@ int pack_impl(const void *feats, int64_t N, int64_t row_bytes, const int32_t *ca
     DG_HIP(hipStreamWaitEvent(side->s, side->fork, 0));
   }
   if (total > 0) {
-    hipLaunchKernelGGL(k_build_loc, dim3(blocks_for(total)), dim3(THREADS), 0,
-                       side ? side->s : s, L, nodes, cache_slot, w.nodeoff, w.pairdest, rows,
-                       packed_ids, packed_ptr, loc, N, w.err);
+    const dim3 lg(blocks_for(total)), lb(THREADS);
+    hipStream_t ls = side ? side->s : s;
+    if (flags & DG_PACK_LOC_PENDING)
+      hipLaunchKernelGGL(k_build_loc<true>, lg, lb, 0, ls, L, nodes, cache_slot, w.nodeoff,
+                         w.pairdest, rows, packed_ids, packed_ptr, loc, N, w.err);
+    else
+      hipLaunchKernelGGL(k_build_loc<false>, lg, lb, 0, ls, L, nodes, cache_slot, w.nodeoff,
+                         w.pairdest, rows, packed_ids, packed_ptr, loc, N, w.err);
     DG_HIP(hipGetLastError());
   }
   if (side) DG_HIP(hipEventRecord(side->join, side->s));

@@ -58,10 +58,13 @@ struct Lists {
   int64_t n[DG_MAX_BATCHES];
 };
 
+// Seeds -> node lists, membership bits and local indices; with loc, also the
+// seeds' address-table entries (final for cached seeds, pending otherwise).
 __global__ __launch_bounds__(THREADS) void k_seed_init(const int32_t *seeds, int B, int S,
                                                        int64_t N, int64_t node_cap,
                                                        int32_t *nodes, uint64_t *visited,
                                                        uint64_t *prev, int32_t *local,
+                                                       const int32_t *cache_slot, int32_t *loc,
                                                        uint32_t *err) {
   int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (i >= (int64_t)B * S) return;
@@ -72,6 +75,11 @@ __global__ __launch_bounds__(THREADS) void k_seed_init(const int32_t *seeds, int
   if (v < 0 || (int64_t)v >= N) {
     atomicOr(err, ERR_NODE_RANGE);
     return;
+  }
+  if (loc) {
+    const int32_t sl = cache_slot[v];
+    if (sl < -1) atomicOr(err, ERR_CACHE_SLOT);
+    loc[(int64_t)b * node_cap + j] = sl >= 0 ? -(sl + 1) : (int32_t)DG_LOC_PENDING;
   }
   unsigned long long bit = 1ull << b;
   unsigned long long old = atomicOr((unsigned long long *)&visited[v], bit);
@@ -431,11 +439,14 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
                                int32_t *nodes,
                                int64_t *hop_ptr, int64_t edge_cap, int32_t *edge_src,
                                int32_t *edge_dst, int64_t *edge_ptr, uint64_t *membership,
-                               uint8_t *member_lines, void *ws, size_t ws_bytes,
-                               hipStream_t stream, dg_sizes *sizes, dg_timing *timing) {
+                               uint8_t *member_lines, const int32_t *cache_slot, int32_t *loc,
+                               void *ws, size_t ws_bytes, hipStream_t stream, dg_sizes *sizes,
+                               dg_timing *timing) {
   if (!g || !seeds || !nodes || !hop_ptr || !edge_src || !edge_dst || !edge_ptr || !sizes ||
       (K > 0 && !fanouts))
     return set_error(DG_EINVAL, "dg_sample_group: null pointer argument");
+  if (!cache_slot != !loc)
+    return set_error(DG_EINVAL, "dg_sample_group: cache_slot and loc go together");
   if (!g->offsets || (g->num_edges > 0 && !g->indices) || g->num_nodes < 1 ||
       g->num_nodes > 0x7fffffffll || g->num_edges < 0)
     return set_error(DG_EINVAL, "dg_sample_group: bad CSR description");
@@ -487,7 +498,8 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
   bool prev_cleared = false;  // the last hop's count pass zeroed prev
   bool lines_done = false;    // the last hop's count pass wrote member_lines
   hipLaunchKernelGGL(k_seed_init, dim3(blocks_for((int64_t)B * S)), dim3(THREADS), 0, s, seeds,
-                     B, S, N, node_cap, nodes, w.visited, w.prev, w.local, w.err);
+                     B, S, N, node_cap, nodes, w.visited, w.prev, w.local, cache_slot, loc,
+                     w.err);
   DG_HIP(hipGetLastError());  // bad seeds are reported at the first hop's round trip
 
   int64_t n_b[DG_MAX_BATCHES], e_b[DG_MAX_BATCHES];
@@ -597,6 +609,8 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       }
       w.ms.seg_out = nodes;
       w.ms.local_out = w.local;
+      w.ms.loc_slot = cache_slot;  // the list's address-table entries beside it
+      w.ms.loc_out = loc;
       w.ms.uniq_out = nullptr;
       w.ms.unc_ids = nullptr;
       w.ms.unc_off = nullptr;

@@ -560,6 +560,10 @@ int mask_scan_count(MaskScan &m, hipStream_t s) {
 //   PACK:  packing outputs (U, U_nc, pair offsets, pair destinations); cached
 //          nodes are left out of the per-batch lists.
 //   LOCAL: sampling, also recording each pair's local index in local_out.
+// Sampling with loc_out also writes each listed pair's address-table entry,
+// at the index of its list slot: the entry of a cached node is final, the
+// others are left DG_LOC_PENDING for packing.  Each lane loads the cache slot
+// of its own word before the pairs are emitted.
 template <bool PACK, bool LOCAL>
 __global__ __launch_bounds__(MC_THREADS) void k_mask_write(MaskScan a) {
   const int lane = lane_id(), w = threadIdx.x >> 6;
@@ -593,6 +597,11 @@ __global__ __launch_bounds__(MC_THREADS) void k_mask_write(MaskScan a) {
       off = co[i];
     }
     const int32_t u = (int32_t)(t0 + (off & 1023u));
+    int32_t sl = -1;  // sampling with loc_out: this lane's node's cache slot
+    if (!PACK && a.loc_out && i < n) {
+      sl = a.loc_slot[u];
+      if (sl < -1) atomicOr(a.err, ERR_CACHE_SLOT);
+    }
     const uint64_t mnc = (PACK && (off >> 15)) ? 0ull : m;
     uint64_t anc = __ballot(mnc != 0ull);
     if (PACK) {
@@ -614,8 +623,11 @@ __global__ __launch_bounds__(MC_THREADS) void k_mask_write(MaskScan a) {
       anc &= ~(1ull << l);
       const uint64_t wd = (uint64_t)read_lane((int64_t)mnc, l);
       const int32_t ul = __builtin_amdgcn_readlane(u, l);
+      const int32_t sll = PACK ? -1 : __builtin_amdgcn_readlane(sl, l);
       if ((wd >> lane) & 1ull) {
         if (PACK || dest_b < end_b) a.seg_out[dest_b] = ul;
+        if (!PACK && a.loc_out && dest_b < end_b)
+          a.loc_out[dest_b] = sll >= 0 ? -(sll + 1) : (int32_t)DG_LOC_PENDING;
         if (PACK) a.pairdest[run_p + __popcll(wd & lt)] = dest_b;
         if (LOCAL) a.local_out[(int64_t)ul * B + lane] = local_b;
         ++dest_b;
@@ -631,7 +643,8 @@ int mask_scan_write(const MaskScan &m, hipStream_t s) {
   const bool pack = m.pairdest != nullptr;
   // seg_out may be NULL only when no pair is listed (packing with every node cached)
   if ((pack && (!m.unc_ids || !m.unc_off || !m.nodeoff)) ||
-      (!pack && (!m.prev || !m.seg_out || m.cache_slot || m.uniq_out)))
+      (!pack && (!m.prev || !m.seg_out || m.cache_slot || m.uniq_out)) ||
+      (pack && m.loc_out) || (!m.loc_out != !m.loc_slot))
     return set_error(DG_EINVAL, "internal: inconsistent compaction outputs");
   const dim3 g((unsigned)m.nblk), bl(MC_THREADS);
   if (pack)

@@ -85,7 +85,8 @@ def test_host_side_argument_errors(L):
     sizes = _lib.Sizes()
     # null CSR / outputs: rejected before any device call
     rc = L.dg_sample_group(None, None, 1, 1, 0, None, 0, 0, 0, 1, None, None, 1, None, None,
-                           None, None, None, None, 0, None, ctypes.byref(sizes), None)
+                           None, None, None, None, None, None, 0, None, ctypes.byref(sizes),
+                           None)
     assert rc == _lib.DG_EINVAL
     assert b"null" in L.dg_last_error()
     g = _lib.Csr(10, 0, 0x1000, 0)
@@ -95,23 +96,29 @@ def test_host_side_argument_errors(L):
     fake = ctypes.c_void_p(0x1000)
     # B out of range
     rc = L.dg_sample_group(ctypes.byref(g), fake, 65, 1, 0, fo, 1, 0, 0, 4, fake, hop, 4, fake,
-                           fake, ep, None, None, fake, 1 << 20, None, ctypes.byref(sizes),
-                           None)
+                           fake, ep, None, None, None, None, fake, 1 << 20, None,
+                           ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL
     # workspace missing
     rc = L.dg_sample_group(ctypes.byref(g), fake, 1, 1, 0, fo, 1, 0, 0, 4, fake, hop, 4, fake,
-                           fake, ep, None, None, None, 0, None, ctypes.byref(sizes), None)
+                           fake, ep, None, None, None, None, None, 0, None, ctypes.byref(sizes),
+                           None)
     assert rc == _lib.DG_EWORKSPACE
+    # the cached address-table entries need both the cache slots and the table
+    rc = L.dg_sample_group(ctypes.byref(g), fake, 1, 1, 0, fo, 1, 0, 0, 4, fake, hop, 4, fake,
+                           fake, ep, None, None, fake, None, fake, 1 << 20, None,
+                           ctypes.byref(sizes), None)
+    assert rc == _lib.DG_EINVAL and b"cache_slot and loc" in L.dg_last_error()
     # unknown flags
     rc = L.dg_sample_group(ctypes.byref(g), fake, 1, 1, 0, fo, 1, 0, 16, 4, fake, hop, 4, fake,
-                           fake, ep, None, None, fake, 1 << 20, None, ctypes.byref(sizes),
-                           None)
+                           fake, ep, None, None, None, None, fake, 1 << 20, None,
+                           ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL and b"flags" in L.dg_last_error()
     # DG_SAMPLE_ENTRY_CLEAR asserts something about `membership`, so it needs one
     rc = L.dg_sample_group(ctypes.byref(g), fake, 1, 1, 0, fo, 1, 0,
                            _lib.DG_SAMPLE_ENTRY_CLEAR, 4, fake, hop, 4, fake,
-                           fake, ep, None, None, fake, 1 << 20, None, ctypes.byref(sizes),
-                           None)
+                           fake, ep, None, None, None, None, fake, 1 << 20, None,
+                           ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL and b"membership" in L.dg_last_error()
     # pack: B = 0, row_bytes = 0, counts beyond the stride
     cnt = (ctypes.c_int64 * 2)(3, 9)
@@ -125,7 +132,7 @@ def test_host_side_argument_errors(L):
     # pack flags: unknown bits, and a clear request without a membership mask
     ok_cnt = (ctypes.c_int64 * 2)(3, 5)
     rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, ok_cnt, 0, None, None, fake, ph, fake,
-                         None, 0, fake, None, 4, fake, 1 << 20, None, None, ctypes.byref(sizes),
+                         None, 0, fake, None, 8, fake, 1 << 20, None, None, ctypes.byref(sizes),
                          None)
     assert rc == _lib.DG_EINVAL and b"flags" in L.dg_last_error()
     rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, ok_cnt, 0, None, None, fake, ph, fake,

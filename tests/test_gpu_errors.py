@@ -204,3 +204,53 @@ def test_assemble_bad_entries_every_row_shape(dg, R):
     got = out.cpu()
     assert int(got[bad].to(torch.int64).sum()) == 0
     assert torch.equal(got[~bad], want[~bad])
+
+
+def handoff_setup(dg, tiny):
+    off, idx = tiny.offsets.to(DEV), tiny.indices.to(DEV)
+    seeds = tiny.seeds.to(DEV)
+    ncap, ecap = dg.sample_bounds(tiny.cfg.n, tiny.num_edges, tiny.cfg.S, [5, 5])
+    loc = torch.full((tiny.cfg.B, ncap), -3, dtype=torch.int32, device=DEV)
+    return off, idx, seeds, ncap, ecap, loc
+
+
+@pytest.mark.parametrize("direct", [False, True])
+def test_handoff_bad_cache_slot_rejected_by_sampling(dg, tiny, direct):
+    """A cache_slot value below -1 given to sampling for the address tables."""
+    off, idx, seeds, ncap, ecap, loc = handoff_setup(dg, tiny)
+    slot = tiny.cache_slot.to(DEV).clone()
+    slot[::3] = -9  # reaches seeds and sampled nodes alike
+    with pytest.raises(dg.DGError) as e:
+        dg.sample_group(off, idx, seeds, [5, 5], 1, direct=direct, node_cap=ncap, edge_cap=ecap,
+                        cache_slot=slot, loc=loc)
+    assert e.value.status == -1 and "cache_slot" in str(e.value)
+
+
+def test_handoff_pending_entry_of_a_cached_node_rejected(dg, tiny):
+    """Packing told that loc came from sampling with another cache_slot: a
+    pending entry whose node is cached now has no packed row, and is reported;
+    the entries it keeps are never followed."""
+    off, idx, seeds, ncap, ecap, loc = handoff_setup(dg, tiny)
+    X = tiny.feats.to(DEV)
+    slot = tiny.cache_slot.to(DEV)
+    sr = dg.sample_group(off, idx, seeds, [5, 5], 1, node_cap=ncap, edge_cap=ecap,
+                         cache_slot=slot, loc=loc)
+    ref = dg.pack_group(X, slot, sr.nodes, sr.node_count, with_unique=True)
+    # a node that was not cached at sampling time becomes cached
+    u = int(sr.batch_nodes(1)[3])
+    assert int(slot[u]) == -1
+    slot2 = slot.clone()
+    slot2[u] = 0
+    out = dg.pack_group(X, slot, sr.nodes, sr.node_count, with_unique=True)  # buffers
+    out.loc.copy_(loc)
+    with pytest.raises(dg.DGError) as e:
+        dg.pack_group(X, slot2, sr.nodes, sr.node_count, with_unique=True, out=out,
+                      loc_pending=True)
+    assert e.value.status == -1
+    # and with the same cache_slot the completed table equals packing's own
+    out.loc.copy_(loc)
+    pr = dg.pack_group(X, slot, sr.nodes, sr.node_count, with_unique=True, out=out,
+                       loc_pending=True)
+    for b in range(tiny.cfg.B):
+        n = int(sr.hop_ptr[b, -1])
+        assert torch.equal(pr.loc[b, :n], ref.loc[b, :n]), b

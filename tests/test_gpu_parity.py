@@ -31,16 +31,38 @@ def to_np(t):
 
 def run_path(dg, off, idx, seeds, fanouts, rng_seed, feats, cache_slot, cache_nodes,
              batch_base=0, sample_kw=None):
-    """The device path: sample -> pack -> assemble every batch."""
+    """The device path: sample -> pack -> assemble every batch.  With
+    sample_kw["handoff"], sampling also writes the cached nodes' address-table
+    entries (garbage in the table beforehand) and packing completes the rest
+    (DG_PACK_LOC_PENDING)."""
+    kw = dict(sample_kw or {})
+    handoff = kw.pop("handoff", False)
     off_d, idx_d = off.to(DEV), idx.to(DEV)
     seeds_d = seeds.to(DEV)
-    sr = dg.sample_group(off_d, idx_d, seeds_d, fanouts, rng_seed, batch_base=batch_base,
-                         **(sample_kw or {}))
     X = feats.to(DEV)
     slot = cache_slot.to(DEV)
     cache = X.index_select(0, cache_nodes.to(DEV)) if cache_nodes.numel() else None
     R = X[0].numel() * X.element_size()
-    pr = dg.pack_group(X, slot, sr.nodes, sr.node_count, with_unique=True)
+    if not handoff:
+        sr = dg.sample_group(off_d, idx_d, seeds_d, fanouts, rng_seed, batch_base=batch_base,
+                             **kw)
+        pr = dg.pack_group(X, slot, sr.nodes, sr.node_count, with_unique=True)
+    else:
+        B = seeds.shape[0]
+        ncap, ecap = dg.sample_bounds(off.numel() - 1, idx.numel(), seeds.shape[1], fanouts,
+                                      kw.get("layered", False))
+        loc = torch.full((B, ncap), -3, dtype=torch.int32, device=DEV)
+        sr = dg.sample_group(off_d, idx_d, seeds_d, fanouts, rng_seed, batch_base=batch_base,
+                             node_cap=ncap, edge_cap=ecap, cache_slot=slot, loc=loc, **kw)
+        cap = max(int(sr.node_count.sum()), 1)
+        out = dg.PackResult(packed=torch.empty((cap, R), dtype=torch.uint8, device=DEV),
+                            packed_ids=torch.empty(cap, dtype=torch.int32, device=DEV),
+                            packed_ptr=torch.empty(B + 1, dtype=torch.int64, device=DEV),
+                            packed_ptr_host=np.zeros(B + 1, dtype=np.int64), loc=loc,
+                            unique=torch.empty(cap, dtype=torch.int32, device=DEV), sizes={},
+                            timing=None, row_bytes=R)
+        pr = dg.pack_group(X, slot, sr.nodes, sr.node_count, with_unique=True, out=out,
+                           loc_pending=True)
     status = torch.zeros(1, dtype=torch.int32, device=DEV)
     Y = []
     for b in range(seeds.shape[0]):
@@ -131,6 +153,16 @@ def test_tiny_workload_T_direct_relabel(dg, orc, layered):
               w.cache_slot, w.cache_nodes, sample_kw={"layered": layered, "direct": True})
 
 
+@pytest.mark.parametrize("direct", [False, True])
+def test_tiny_workload_T_address_tables_from_sampling(dg, orc, direct):
+    """Sampling writes the cached nodes' address-table entries as it lists
+    them, and packing completes the others (DG_PACK_LOC_PENDING): every output
+    equals the oracle's."""
+    w = synth.make_workload("T")
+    check_all(dg, orc, w.offsets, w.indices, w.seeds, list(w.cfg.fanouts), w.rng_seed, w.feats,
+              w.cache_slot, w.cache_nodes, sample_kw={"direct": direct, "handoff": True})
+
+
 def test_tiny_workload_T_is_deterministic(dg):
     w = synth.make_workload("T")
     a, pa, ya, _ = run_path(dg, w.offsets, w.indices, w.seeds, list(w.cfg.fanouts), w.rng_seed,
@@ -188,10 +220,11 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("layered,direct", [(False, False), (True, False), (False, True),
-                                            (True, True)])
+@pytest.mark.parametrize("layered,direct,handoff", [
+    (False, False, False), (True, False, False), (False, True, False), (True, True, False),
+    (False, True, True), (True, False, True)])
 @pytest.mark.parametrize("case", range(len(CASES)))
-def test_edge_cases(dg, orc, case, layered, direct):
+def test_edge_cases(dg, orc, case, layered, direct, handoff):
     n, maxdeg, B, S, fan, dim, dtype, share = CASES[case]
     rnd = random.Random(900 + case)
     off, idx = random_case(rnd, n, maxdeg) if maxdeg else (
@@ -207,7 +240,8 @@ def test_edge_cases(dg, orc, case, layered, direct):
     slot = torch.full((n,), -1, dtype=torch.int32)
     slot[cache_nodes] = torch.arange(ncache, dtype=torch.int32)
     check_all(dg, orc, off, idx, seeds, fan, 12345 + case, feats, slot, cache_nodes,
-              batch_base=case, sample_kw={"layered": layered, "direct": direct})
+              batch_base=case, sample_kw={"layered": layered, "direct": direct,
+                                          "handoff": handoff})
 
 
 def test_fig1_example_on_device(dg, orc):
@@ -291,8 +325,9 @@ def test_assemble_batches_matches_per_batch_calls(dg):
         dg.assemble_batches(cache, pr, counts, [outs[0][:1]])
 
 
-@pytest.mark.parametrize("layered,direct", [(False, False), (True, True)])
-def test_sparse_hops_on_a_large_graph(dg, orc, layered, direct):
+@pytest.mark.parametrize("layered,direct,handoff", [(False, False, False), (True, True, False),
+                                                    (False, True, True)])
+def test_sparse_hops_on_a_large_graph(dg, orc, layered, direct, handoff):
     """A small frontier on a large graph: every hop's edges reach only a small
     share of the nodes, so the sampler lists new nodes from the 8-node mask
     lines its draws touched (the count pass skips the others)."""
@@ -308,7 +343,7 @@ def test_sparse_hops_on_a_large_graph(dg, orc, layered, direct):
     slot = torch.full((n,), -1, dtype=torch.int32)
     slot[cache_nodes] = torch.arange(ncache, dtype=torch.int32)
     check_all(dg, orc, off, idx, seeds, [3, 3, 2], 99, feats, slot, cache_nodes, batch_base=5,
-              sample_kw={"layered": layered, "direct": direct})
+              sample_kw={"layered": layered, "direct": direct, "handoff": handoff})
 
 
 def test_assemble_batches_in_a_hip_graph(dg):

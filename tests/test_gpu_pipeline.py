@@ -2,7 +2,9 @@
 concurrency.  Sampling and packing run on one stream, the row copy and the
 assembly on a second one, with two packing output sets and two packing
 workspaces; each packing call waits for the assembly that last read its set;
-the clearing flags and the member-lines map carry state from step to step.
+the clearing flags and the member-lines map carry state from step to step;
+sampling writes the cached nodes' address-table entries into the step's
+packing set, which packing completes.
 Every step takes a different seed group, so an output read or written by the
 wrong step would show up as a wrong row.  Each step assembles into buffers of
 its own, and all are checked against a library gather (torch.index_select) at
@@ -70,15 +72,19 @@ def test_pipelined_steps_are_each_correct(dg):
     for k in range(steps):
         slot = k & 1
         print(f"[pipeline] step {k}", flush=True)
+        # sampling writes the cached nodes' address-table entries into this
+        # step's packing set, so it waits for the assembly that last read it
+        stream.wait_event(asm_done[slot])
         sr = dg.sample_group(w.offsets, w.indices, groups[k], fan, w.rng_seed, membership=mem,
                              workspace=ws_s, direct=True, exit_clear=True, entry_clear=clear,
-                             member_lines=lines, stream=stream)
+                             member_lines=lines, stream=stream, cache_slot=w.cache_slot,
+                             loc=pr2[slot].loc, node_cap=node_cap, edge_cap=edge_cap)
         counts = sr.node_count.copy()
         nodes = sr.nodes.clone()  # the next step's sampling overwrites sr.nodes
-        stream.wait_event(asm_done[slot])
         pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, out=pr2[slot],
                            workspace=ws_p[slot], membership=mem, clear_membership=True,
-                           member_lines=lines, stream=stream, rows_stream=s_asm)
+                           member_lines=lines, stream=stream, rows_stream=s_asm,
+                           loc_pending=True)
         clear = True
         pack_done.record(stream)
         s_asm.wait_event(pack_done)

@@ -1,8 +1,9 @@
 """Parity on the named workloads, in the launch configuration bench.py times:
 the sampler's membership mask handed to the packer, the mask-clearing flags
 (two groups in a row on the same membership buffer and workspaces, the second
-sampling call told that the state is clear), and packing's row copy queued on
-a second stream with the assembly behind it.
+sampling call told that the state is clear, and the second also taking the
+cached nodes' address-table entries from sampling), and packing's row copy
+queued on a second stream with the assembly behind it.
 
 Every workload compares, for every mini-batch of the group, the sampled node
 list, hop bounds, edge lists and edge bounds with the oracle's (one oracle run
@@ -47,16 +48,22 @@ def check_rows_on_device(X, ids, got, chunk=1 << 20):
         assert rows_equal(got[lo:hi], ref), (lo, hi)
 
 
-def bench_path(dg, w, fan, mem, ws_s, ws_p, direct, entry_clear, out=None):
+def bench_path(dg, w, fan, mem, ws_s, ws_p, direct, entry_clear, out=None, pack_out=None):
     """One group as bench.py runs it: sampling with the clearing flags, packing
-    that clears the mask and leaves its row copy on a second stream."""
+    that clears the mask and leaves its row copy on a second stream.  With
+    pack_out (a packing output set of this group's sizes, its address table
+    laid out as the node lists), sampling also writes the cached nodes'
+    address-table entries into it and packing completes the others."""
     sr = dg.sample_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, membership=mem,
                          workspace=ws_s, direct=direct, exit_clear=True,
-                         entry_clear=entry_clear, out=out)
+                         entry_clear=entry_clear, out=out,
+                         cache_slot=w.cache_slot if pack_out is not None else None,
+                         loc=pack_out.loc if pack_out is not None else None)
     counts = sr.node_count.copy()
     side = torch.cuda.Stream(device=DEV)
     pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, with_unique=True, membership=mem,
-                       workspace=ws_p, clear_membership=True, rows_stream=side)
+                       workspace=ws_p, clear_membership=True, rows_stream=side, out=pack_out,
+                       loc_pending=pack_out is not None)
     side.synchronize()
     torch.cuda.synchronize()
     return sr, counts, pr
@@ -123,13 +130,17 @@ def run_and_check(dg, orc, w, ref, direct=True):
         check_rows_on_device(w.feats, sr.nodes[b, :n], y[:n].view(w.feats.dtype).reshape(n, -1))
     assert int(status.item()) == 0
 
-    # a second group on the same buffers, told that the state is clear: the
-    # same seeds give the same outputs
+    # a second group on the same buffers, told that the state is clear, with
+    # the address tables of cached nodes written by sampling (into the first
+    # call's packing set, garbage first) and completed by packing: the same
+    # seeds give the same outputs
     keep = (sr.nodes.clone(), sr.edge_src.clone(), sr.edge_dst.clone(), sr.hop_ptr.copy(),
             sr.edge_ptr.copy(), pr.packed_ids[:rows].clone(), pr.loc.clone(),
             pr.packed[:rows].clone())
-    del pr
-    sr2, counts2, pr2 = bench_path(dg, w, fan, mem, ws_s, ws_p, direct, entry_clear=True)
+    pr.loc.fill_(-3)
+    pr.packed[:rows].zero_()
+    sr2, counts2, pr2 = bench_path(dg, w, fan, mem, ws_s, ws_p, direct, entry_clear=True,
+                                   pack_out=pr)
     assert np.array_equal(counts2, counts) and np.array_equal(sr2.hop_ptr, keep[3])
     assert np.array_equal(sr2.edge_ptr, keep[4])
     for b in range(cfg.B):
