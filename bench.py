@@ -95,6 +95,9 @@ def main():
     ap.add_argument("--no-loc-handoff", action="store_true",
                     help="packing builds every address-table entry itself, instead of "
                          "completing the ones sampling wrote for cached nodes (comparison)")
+    ap.add_argument("--sets", type=int, default=3,
+                    help="packing output sets (and workspaces) used in turn: step k waits for "
+                         "the assembly of step k - sets before it writes into its set")
     ap.add_argument("--asm-inline", action="store_true",
                     help="pipelined region: issue each step's assembly from the main thread "
                          "instead of a host thread of its own (comparison)")
@@ -106,17 +109,19 @@ def main():
     ap.add_argument("--groups", type=int, default=16,
                     help="groups of B mini-batches for --experiment regime")
     ap.add_argument("--experiment",
-                    choices=["pack_ab", "cache", "layered", "minhash", "regime", "ceiling"],
+                    choices=["pack_ab", "cache", "cache_fill", "layered", "minhash", "regime",
+                             "ceiling"],
                     default=None,
                     help="instead of the step benchmark: batched vs individual packing "
-                         "(pack_ab), access-frequency vs in-degree cache (cache), or "
+                         "(pack_ab), access-frequency vs in-degree cache (cache), the cache "
+                         "filled by the packing gather vs a separate gather (cache_fill), or "
                          "layer-wise (DGL-style) vs new-node frontier sampling (layered), or "
                          "disk-cache pages touched under ID vs MinHash order (minhash), or "
                          "the node access distribution over several groups (regime), or "
                          "the rate of plain row copies on this memory system (ceiling)")
     args = ap.parse_args()
-    if args.steps < 1 or args.warmup < 0:
-        ap.error("--steps must be at least 1 and --warmup at least 0")
+    if args.steps < 1 or args.warmup < 0 or args.sets < 2:
+        ap.error("--steps must be at least 1, --warmup at least 0 and --sets at least 2")
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on exactly one GPU: the hot path is measured on one GPU's "
@@ -147,6 +152,7 @@ def main():
     stream = torch.cuda.current_stream()
     if args.experiment:
         out = {"pack_ab": experiment_pack_ab, "cache": experiment_cache,
+               "cache_fill": experiment_cache_fill,
                "layered": experiment_layered,
                "minhash": experiment_minhash,
                "ceiling": experiment_ceiling,
@@ -208,13 +214,15 @@ def main():
             loc=torch.empty((B, node_cap), dtype=torch.int32, device=dev), unique=None,
             sizes={}, timing=None, row_bytes=R)
 
-    # two packing outputs, so that packing step k+1 never overwrites what
-    # assembly step k is still reading; two packing workspaces, since in the
-    # pipelined region a packing call's row copy may still be queued on the
-    # assembly stream when the next call starts
-    pr2 = [pack_out() for _ in range(2)]
+    # `sets` packing output sets used in turn, so that step k never overwrites
+    # what the assembly of an earlier step is still reading, and as many packing
+    # workspaces, since in the pipelined region a packing call's row copy may
+    # still be queued on the assembly stream when the next call starts; step k
+    # waits only for the assembly of step k - sets
+    n_sets = args.sets
+    pr2 = [pack_out() for _ in range(n_sets)]
     ws_p2 = [torch.empty(dg._L.dg_pack_workspace_bytes(cfg.n, B, max_total), dtype=torch.uint8,
-                         device=dev) for _ in range(2)]
+                         device=dev) for _ in range(n_sets)]
     ybuf = [torch.empty((nmax, R), dtype=torch.uint8, device=dev) for _ in range(2)]
     log(f"{n_groups} groups: pairs {min(p['total_nodes'] for p in pre):,}.."
         f"{max_total:,} edges {min(p['total_edges'] for p in pre):,}.."
@@ -231,8 +239,8 @@ def main():
     # assembly launches are issued by one dg_assemble_batches call with that
     # step's own sizes; its host time is reported.
     s_asm = torch.cuda.Stream(device=dev)
-    asm_done = [torch.cuda.Event(), torch.cuda.Event()]
-    pack_done = [torch.cuda.Event(), torch.cuda.Event()]
+    asm_done = [torch.cuda.Event() for _ in range(n_sets)]
+    pack_done = [torch.cuda.Event() for _ in range(n_sets)]
     # timing events, created (by a first record) before any timed region
     nev = max(args.steps, args.warmup)
     ev_pool = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -254,7 +262,7 @@ def main():
 
         def __init__(self):
             self.q = queue.Queue()
-            self.free = [threading.Event(), threading.Event()]
+            self.free = [threading.Event() for _ in range(n_sets)]
             for f in self.free:
                 f.set()
             self.err = None
@@ -312,7 +320,7 @@ def main():
         times, assembly times (events) and the step's sizes."""
         marks, gather_ms, evs, steps = [], [], [], []
         for k, g in enumerate(gs):
-            slot = k & 1
+            slot = k % n_sets
             t0 = time.perf_counter()
             # Sampling writes the cached nodes' address-table entries into this
             # step's packing set (pr2[slot].loc), so the assembly that last read
@@ -460,6 +468,7 @@ def main():
         "pipelined": ("no: --no-pipeline, value is the serial rate" if args.no_pipeline else
                       "assembly of step k (second stream) overlaps sampling and packing of "
                       "step k+1; the serial figures below wait for each step's assembly"),
+        "packing_sets": n_sets,
         "assembly_issue": ("direct calls: one dg_assemble_batches call (B launches) per step, "
                            + ("issued by the main thread" if asm_thread is None else
                               "issued by a host thread of its own in the pipelined region "
@@ -615,6 +624,52 @@ def experiment_pack_ab(dg, w, cfg, reps):
                            "ms_issued_call_by_call": round(te, 3)},
             "speedup": round(ti / tb, 3), "read_ratio": round(rows / max(Uc, 1), 3),
             "identical_output": same}
+
+
+def experiment_cache_fill(dg, w, cfg, reps):
+    """The cache filled by batched packing as one more mini-batch (§5.2): one
+    packing call whose fan-out gather also writes the cache table, against the
+    same packing call followed by a separate row gather of the cache
+    (dg_gather_rows over cache_nodes).  Times are the gather launches' own
+    (the library's HIP events for the packing gather, events around
+    dg_gather_rows), median over reps."""
+    import torch
+    R, B = cfg.row_bytes, cfg.B
+    C = int(w.cache_nodes.numel())
+    nodes = w.cache_nodes.to(torch.int32)
+    mem = torch.empty(cfg.n, dtype=torch.int64, device="cuda")
+    sr = dg.sample_group(w.offsets, w.indices, w.seeds, list(cfg.fanouts), w.rng_seed,
+                         membership=mem, direct=True)
+    table = torch.empty((C, R), dtype=torch.uint8, device="cuda")
+    pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, sr.node_count, membership=mem)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    one, two_pack, two_cache = [], [], []
+    for _ in range(reps + 1):
+        p = dg.pack_group(w.feats, w.cache_slot, sr.nodes, sr.node_count, out=pr,
+                          membership=mem, timing=True, cache_nodes=nodes, cache_table=table)
+        one.append(p.timing["gather_ms"])
+        p = dg.pack_group(w.feats, w.cache_slot, sr.nodes, sr.node_count, out=pr,
+                          membership=mem, timing=True)
+        two_pack.append(p.timing["gather_ms"])
+        ev[0].record()
+        dg.gather_rows(w.feats, nodes, out=table)
+        ev[1].record()
+        ev[1].synchronize()
+        two_cache.append(ev[0].elapsed_time(ev[1]))
+    ok = bool(torch.equal(table[:1024], w.feats.index_select(0, w.cache_nodes[:1024])
+                          .view(torch.uint8).reshape(-1, R)))
+    Uc, rows = pr.sizes["unique_packed"], pr.sizes["packed_rows"]
+    t1 = _median(one[1:])
+    t2 = _median(two_pack[1:]) + _median(two_cache[1:])
+    bytes_ = R * (Uc + rows) + 2 * R * C
+    return {"experiment": "cache filled by the packing gather vs a separate gather",
+            "workload": cfg.name, "cache_rows": C, "row_bytes": R, "batches": B,
+            "packed_rows": rows, "unique_packed": Uc, "bytes": bytes_,
+            "one_launch": {"ms": round(t1, 3), "GBps": round(bytes_ / t1 / 1e6, 1)},
+            "two_launches": {"ms": round(t2, 3), "GBps": round(bytes_ / t2 / 1e6, 1),
+                             "pack_gather_ms": round(_median(two_pack[1:]), 3),
+                             "cache_gather_ms": round(_median(two_cache[1:]), 3)},
+            "speedup": round(t2 / t1, 3), "cache_table_checked": ok}
 
 
 def experiment_cache(dg, w, cfg, reps):

@@ -325,6 +325,14 @@ size_t dg_pack_workspace_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes
  *               dg_sample_group writes it: words of lines whose byte is 0 are
  *               not read.  A member in an unmarked line is missed, which the
  *               pair-count check reports (DG_EINVAL).
+ *   cache_nodes, cache_rows, cache_table  optional cache fill (NULL cache_table =
+ *               none): the caches are filled by batched packing as special
+ *               mini-batches (§5.2), so the row copy also reads the row of each
+ *               cache_nodes[s] (s < cache_rows) once and writes it to row s of
+ *               cache_table [cache_rows*row_bytes], in the same gather launch as
+ *               the packed chunks.  A slot holding -1 is left as it is; another
+ *               ID outside [0, N) is reported (DG_EINVAL).  Needs packed, and
+ *               cannot be combined with DG_PACK_ROWS_STREAM.
  *   flags       0, or an OR of DG_PACK_CLEAR_MEMBERSHIP, DG_PACK_ROWS_STREAM and
  *               DG_PACK_LOC_PENDING.  With DG_PACK_LOC_PENDING, loc must hold
  *               what dg_sample_group wrote for these lists and this cache_slot:
@@ -363,9 +371,9 @@ int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
                   void *packed, int32_t *packed_ids, int64_t *packed_ptr,
                   int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique,
                   int64_t unique_cap, uint64_t *membership, const uint8_t *member_lines,
-                  uint32_t flags, void *ws,
-                  size_t ws_bytes, hipStream_t stream, hipStream_t rows_stream,
-                  dg_sizes *sizes, dg_timing *timing);
+                  const int32_t *cache_nodes, int64_t cache_rows, void *cache_table,
+                  uint32_t flags, void *ws, size_t ws_bytes, hipStream_t stream,
+                  hipStream_t rows_stream, dg_sizes *sizes, dg_timing *timing);
 
 /* Bytes of the fixed scratch of dg_pack_group_noalloc (256 MiB). */
 size_t dg_pack_noalloc_scratch_bytes(void);
@@ -392,8 +400,9 @@ int dg_pack_group_noalloc(const void *feats, int64_t N, int64_t row_bytes,
                           void *packed, int32_t *packed_ids, int64_t *packed_ptr,
                           int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique,
                           int64_t unique_cap, uint64_t *membership,
-                          const uint8_t *member_lines, uint32_t flags, hipStream_t stream,
-                          dg_sizes *sizes);
+                          const uint8_t *member_lines, const int32_t *cache_nodes,
+                          int64_t cache_rows, void *cache_table, uint32_t flags,
+                          hipStream_t stream, dg_sizes *sizes);
 
 /* Feature assembling for one mini-batch (§4 Fig. 3, second step; addresses come
  * from the precomputed table of §6, so no lookup structure is consulted):

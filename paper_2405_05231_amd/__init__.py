@@ -213,7 +213,8 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
                membership: torch.Tensor | None = None, tables_only: bool = False,
                clear_membership: bool = False, rows_stream=None,
                member_lines: torch.Tensor | None = None, no_alloc: bool = False,
-               loc_pending: bool = False) -> PackResult:
+               loc_pending: bool = False, cache_nodes: torch.Tensor | None = None,
+               cache_table: torch.Tensor | None = None) -> PackResult:
     """Batched packing (dg_pack_group).  nodes: int32 [B, node_stride];
     node_count: the B list lengths (host).  membership: optional int64 [N]
     mask from sample_group (skips rebuilding it).  tables_only: build the
@@ -227,7 +228,10 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
     (scratch inside the library, no workspace; no timing or rows_stream);
     pass `out` as well for a call that allocates nothing at all.
     loc_pending: DG_PACK_LOC_PENDING, out.loc already holds what sample_group
-    wrote into it for these lists and this cache_slot (`out` required)."""
+    wrote into it for these lists and this cache_slot (`out` required).
+    cache_nodes, cache_table: int32 [C] and a [C, row_bytes]-byte buffer: the
+    row copy also fills cache row s with the features of cache_nodes[s] (the
+    cache as one more mini-batch of the same gather)."""
     dev = feats.device
     _need(feats, "feats", None)
     _need(cache_slot, "cache_slot", torch.int32, dev)
@@ -247,6 +251,15 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
     if counts.shape[0] != B:
         raise ValueError("node_count must have one entry per batch")
     total = int(counts.sum())
+    n_cache = 0
+    if (cache_nodes is None) != (cache_table is None):
+        raise ValueError("cache_nodes and cache_table go together")
+    if cache_nodes is not None:
+        _need(cache_nodes, "cache_nodes", torch.int32, dev)
+        _need(cache_table, "cache_table", None, dev)
+        n_cache = cache_nodes.numel()
+        if cache_table.numel() * cache_table.element_size() < n_cache * R:
+            raise ValueError("cache_table holds fewer than len(cache_nodes) rows")
     if loc_pending and (out is None or tuple(out.loc.shape) != (B, stride)):
         raise ValueError("loc_pending needs `out` whose loc is laid out as the node lists")
     if no_alloc:
@@ -256,11 +269,14 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
     else:
         ws = _workspace(_L.dg_pack_workspace_bytes(N, B, total), dev, workspace)
 
-    def call(cap, packed, packed_ids, ptr, ptr_host, loc, unique, unique_cap, flags, sz, tm):
+    def call(cap, packed, packed_ids, ptr, ptr_host, loc, unique, unique_cap, flags, sz, tm,
+             fill_cache=True):
+        fill = fill_cache and cache_nodes is not None
         head = (_ptr(feats), N, R, _ptr(cache_slot), B, _ptr(nodes), stride,
                 counts.ctypes.data_as(_lib.I64P), cap, packed, packed_ids, ptr,
                 ptr_host.ctypes.data_as(_lib.I64P), loc, unique, unique_cap,
-                _ptr(membership), _ptr(member_lines), flags)
+                _ptr(membership), _ptr(member_lines), _ptr(cache_nodes) if fill else None,
+                n_cache if fill else 0, _ptr(cache_table) if fill else None, flags)
         if no_alloc:
             return _L.dg_pack_group_noalloc(*head, _stream(stream), ctypes.byref(sz))
         return _L.dg_pack_group(*head, _ptr(ws), ws.numel(), _stream(stream),
@@ -281,7 +297,8 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
         loc = torch.empty((B, stride), dtype=torch.int32, device=dev)
         ptr = torch.empty(B + 1, dtype=torch.int64, device=dev)
         # size query: a zero packed capacity returns the exact sizes needed
-        st = call(0, None, None, _ptr(ptr), ptr_host, _ptr(loc), None, 0, 0, sz, None)
+        st = call(0, None, None, _ptr(ptr), ptr_host, _ptr(loc), None, 0, 0, sz, None,
+                  fill_cache=False)
         if st not in (DG_OK, DG_ECAPACITY):
             check(st)
         rows, nu = sz.packed_rows, sz.unique_nodes

@@ -67,12 +67,12 @@ SIGNATURES = {
                                        ctypes.POINTER(Sizes), ctypes.POINTER(Timing)]),
     "dg_pack_workspace_bytes": (SZ, [I64, I32, I64]),
     "dg_pack_group": (ctypes.c_int, [VP, I64, I64, VP, I32, VP, I64, I64P, I64, VP, VP, VP, I64P,
-                                     VP, VP, I64, VP, VP, U32, VP, SZ, VP, VP,
+                                     VP, VP, I64, VP, VP, VP, I64, VP, U32, VP, SZ, VP, VP,
                                      ctypes.POINTER(Sizes), ctypes.POINTER(Timing)]),
     "dg_pack_noalloc_scratch_bytes": (SZ, []),
     "dg_pack_group_noalloc": (ctypes.c_int, [VP, I64, I64, VP, I32, VP, I64, I64P, I64, VP, VP,
-                                             VP, I64P, VP, VP, I64, VP, VP, U32, VP,
-                                             ctypes.POINTER(Sizes)]),
+                                             VP, I64P, VP, VP, I64, VP, VP, VP, I64, VP, U32,
+                                             VP, ctypes.POINTER(Sizes)]),
     "dg_assemble_batch": (ctypes.c_int, [VP, I64, VP, I64, VP, I64, I64, VP, VP, VP]),
     "dg_assemble_batches": (ctypes.c_int, [VP, I64, VP, I64P, VP, I64, I64P, I32, I64,
                                            ctypes.POINTER(VP), I32, VP, VP]),

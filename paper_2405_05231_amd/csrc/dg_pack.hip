@@ -118,17 +118,26 @@ __global__ __launch_bounds__(THREADS) void k_build_loc(Lists L, const int32_t *n
 // has at least one destination; its first destination index is loaded together
 // with the row, so the common single-destination case needs two dependent
 // round trips (indices, then row + destination) before its stores.
+// Items n_unc .. n_unc + n_cache - 1 fill the cache table, the cache taken as
+// one more mini-batch of the same pass: item n_unc + s copies the row of
+// cache_nodes[s] into cache row s (a slot holding -1 is left as it is; an ID
+// outside [0, N) is reported and its row left as it is).
 template <int LPR, int CPL>
-__global__ __launch_bounds__(THREADS) void k_fanout16(const v4u *X, const int32_t *unc_ids,
+__global__ __launch_bounds__(THREADS) void k_fanout16(const v4u *X, int64_t N,
+                                                      const int32_t *unc_ids,
                                                       const int64_t *unc_off, int64_t n_unc,
                                                       int64_t n_pairs, const int64_t *pairdest,
-                                                      int C, v4u *packed) {
+                                                      int C, v4u *packed,
+                                                      const int32_t *cache_nodes,
+                                                      int64_t n_cache, v4u *cache_table,
+                                                      uint32_t *err) {
   constexpr int UNROLL = rows_in_flight(CPL);
   constexpr int GPB = THREADS / LPR;
   const int sub = threadIdx.x % LPR;
   const int64_t grp = (int64_t)blockIdx.x * GPB + threadIdx.x / LPR;
   const int64_t ngrp = (int64_t)gridDim.x * GPB;
-  for (int64_t i0 = grp * UNROLL; i0 < n_unc; i0 += ngrp * UNROLL) {
+  const int64_t n_items = n_unc + n_cache;
+  for (int64_t i0 = grp * UNROLL; i0 < n_items; i0 += ngrp * UNROLL) {
     int64_t p0[UNROLL], p1[UNROLL], d0[UNROLL];
     int32_t id[UNROLL];
 #pragma unroll
@@ -140,6 +149,10 @@ __global__ __launch_bounds__(THREADS) void k_fanout16(const v4u *X, const int32_
         id[u] = unc_ids[i];
         p0[u] = unc_off[i];
         p1[u] = i + 1 < n_unc ? unc_off[i + 1] : n_pairs;
+      } else if (i < n_items) {
+        const int32_t v = cache_nodes[i - n_unc];
+        if (v >= 0 && (int64_t)v < N) id[u] = v;
+        else if (v != -1 && sub == 0) atomicOr(err, ERR_NODE_RANGE);
       }
     }
     v4u v[UNROLL][CPL];
@@ -155,8 +168,15 @@ __global__ __launch_bounds__(THREADS) void k_fanout16(const v4u *X, const int32_
     }
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
-      if (d0[u] < 0) continue;
-      v4u *dst = packed + d0[u] * C;
+      const int64_t i = i0 + u;
+      v4u *dst;
+      if (i >= n_unc) {  // a cache row
+        if (i >= n_items || id[u] < 0) continue;
+        dst = cache_table + (i - n_unc) * C;
+      } else {
+        if (d0[u] < 0) continue;
+        dst = packed + d0[u] * C;
+      }
 #pragma unroll
       for (int c = 0; c < CPL; ++c) {
         const int ch = sub + c * LPR;
@@ -174,16 +194,31 @@ __global__ __launch_bounds__(THREADS) void k_fanout16(const v4u *X, const int32_
   }
 }
 
-// Any row size / alignment: one wave per U_nc node, words of sizeof(T).
+// Any row size / alignment: one wave per item (U_nc node, then cache row), words
+// of sizeof(T).
 template <typename T>
-__global__ __launch_bounds__(THREADS) void k_fanout_any(const T *X, const int32_t *unc_ids,
+__global__ __launch_bounds__(THREADS) void k_fanout_any(const T *X, int64_t N,
+                                                        const int32_t *unc_ids,
                                                         const int64_t *unc_off, int64_t n_unc,
                                                         int64_t n_pairs, const int64_t *pairdest,
-                                                        int64_t W, T *packed) {
+                                                        int64_t W, T *packed,
+                                                        const int32_t *cache_nodes,
+                                                        int64_t n_cache, T *cache_table,
+                                                        uint32_t *err) {
   const int lane = threadIdx.x & 63;
   const int64_t wave = ((int64_t)blockIdx.x * THREADS + threadIdx.x) >> 6;
   const int64_t nwave = ((int64_t)gridDim.x * THREADS) >> 6;
-  for (int64_t i = wave; i < n_unc; i += nwave) {
+  for (int64_t i = wave; i < n_unc + n_cache; i += nwave) {
+    if (i >= n_unc) {
+      const int64_t s = i - n_unc;
+      const int32_t v = cache_nodes[s];
+      if (v < 0 || (int64_t)v >= N) {
+        if (v != -1 && lane == 0) atomicOr(err, ERR_NODE_RANGE);
+        continue;
+      }
+      for (int64_t c = lane; c < W; c += 64) cache_table[s * W + c] = X[(int64_t)v * W + c];
+      continue;
+    }
     const T *src = X + (int64_t)unc_ids[i] * W;
     int64_t p0 = unc_off[i], p1 = i + 1 < n_unc ? unc_off[i + 1] : n_pairs;
     for (int64_t c = lane; c < W; c += 64) {
@@ -193,51 +228,67 @@ __global__ __launch_bounds__(THREADS) void k_fanout_any(const T *X, const int32_
   }
 }
 
+// The row copy of one packing call: the fan-out gather over U_nc, plus the
+// cache rows when a cache table is given.
+struct RowCopy {
+  const void *X;
+  int64_t N, row_bytes;
+  const int32_t *ids;
+  const int64_t *off;
+  int64_t n, pairs;
+  const int64_t *dest;
+  void *packed;
+  const int32_t *cache_nodes;
+  int64_t n_cache;
+  void *cache_table;
+  uint32_t *err;
+};
+
 template <int LPR, int CPL>
-void launch16(const void *X, const int32_t *ids, const int64_t *off, int64_t n, int64_t pairs,
-              const int64_t *dest, int C, void *packed, hipStream_t s) {
+void launch16(const RowCopy &r, int C, hipStream_t s) {
   constexpr int GPB = THREADS / LPR;
   constexpr int UNROLL = rows_in_flight(CPL);
-  int64_t groups = (n + UNROLL - 1) / UNROLL;
+  int64_t groups = (r.n + r.n_cache + UNROLL - 1) / UNROLL;
   int64_t blocks = (groups + GPB - 1) / GPB;
   if (blocks > (1ll << 20)) blocks = 1ll << 20;
   hipLaunchKernelGGL((k_fanout16<LPR, CPL>), dim3((unsigned)blocks), dim3(THREADS), 0, s,
-                     (const v4u *)X, ids, off, n, pairs, dest, C, (v4u *)packed);
+                     (const v4u *)r.X, r.N, r.ids, r.off, r.n, r.pairs, r.dest, C,
+                     (v4u *)r.packed, r.cache_nodes, r.n_cache, (v4u *)r.cache_table, r.err);
 }
 
 template <typename T>
-void launch_any(const void *X, const int32_t *ids, const int64_t *off, int64_t n, int64_t pairs,
-                const int64_t *dest, int64_t row_bytes, void *packed, hipStream_t s) {
-  int64_t blocks = (n + 3) / 4;
+void launch_any(const RowCopy &r, hipStream_t s) {
+  int64_t blocks = (r.n + r.n_cache + 3) / 4;
   if (blocks > 65536) blocks = 65536;
-  hipLaunchKernelGGL(k_fanout_any<T>, dim3((unsigned)blocks), dim3(THREADS), 0, s, (const T *)X,
-                     ids, off, n, pairs, dest, row_bytes / (int64_t)sizeof(T), (T *)packed);
+  hipLaunchKernelGGL(k_fanout_any<T>, dim3((unsigned)blocks), dim3(THREADS), 0, s,
+                     (const T *)r.X, r.N, r.ids, r.off, r.n, r.pairs, r.dest,
+                     r.row_bytes / (int64_t)sizeof(T), (T *)r.packed, r.cache_nodes, r.n_cache,
+                     (T *)r.cache_table, r.err);
 }
 
-int launch_fanout(const void *X, const int32_t *ids, const int64_t *off, int64_t n, int64_t pairs,
-                  const int64_t *dest, int64_t row_bytes, void *packed, hipStream_t s) {
-  if (n == 0) return DG_OK;
-  const int w = word_bytes(row_bytes, {X, packed});
+int launch_fanout(const RowCopy &r, hipStream_t s) {
+  if (r.n + r.n_cache == 0) return DG_OK;
+  const int w = word_bytes(r.row_bytes, {r.X, r.packed, r.cache_table});
   RowShape sh;
-  if (w == 16 && row_shape16(row_bytes / 16, &sh)) {
-    const int C = (int)(row_bytes / 16);
-    if (sh.lpr == 4) launch16<4, 1>(X, ids, off, n, pairs, dest, C, packed, s);
-    else if (sh.lpr == 8) launch16<8, 1>(X, ids, off, n, pairs, dest, C, packed, s);
-    else if (sh.lpr == 16) launch16<16, 1>(X, ids, off, n, pairs, dest, C, packed, s);
-    else if (sh.lpr == 32 && sh.cpl == 1) launch16<32, 1>(X, ids, off, n, pairs, dest, C, packed, s);
-    else if (sh.lpr == 64 && sh.cpl == 1) launch16<64, 1>(X, ids, off, n, pairs, dest, C, packed, s);
-    else if (sh.lpr == 64 && sh.cpl == 2) launch16<64, 2>(X, ids, off, n, pairs, dest, C, packed, s);
-    else launch16<64, 4>(X, ids, off, n, pairs, dest, C, packed, s);
+  if (w == 16 && row_shape16(r.row_bytes / 16, &sh)) {
+    const int C = (int)(r.row_bytes / 16);
+    if (sh.lpr == 4) launch16<4, 1>(r, C, s);
+    else if (sh.lpr == 8) launch16<8, 1>(r, C, s);
+    else if (sh.lpr == 16) launch16<16, 1>(r, C, s);
+    else if (sh.lpr == 32 && sh.cpl == 1) launch16<32, 1>(r, C, s);
+    else if (sh.lpr == 64 && sh.cpl == 1) launch16<64, 1>(r, C, s);
+    else if (sh.lpr == 64 && sh.cpl == 2) launch16<64, 2>(r, C, s);
+    else launch16<64, 4>(r, C, s);
   } else if (w == 16) {
-    launch_any<uint4>(X, ids, off, n, pairs, dest, row_bytes, packed, s);
+    launch_any<uint4>(r, s);
   } else if (w == 8) {
-    launch_any<uint2>(X, ids, off, n, pairs, dest, row_bytes, packed, s);
+    launch_any<uint2>(r, s);
   } else if (w == 4) {
-    launch_any<uint32_t>(X, ids, off, n, pairs, dest, row_bytes, packed, s);
+    launch_any<uint32_t>(r, s);
   } else if (w == 2) {
-    launch_any<uint16_t>(X, ids, off, n, pairs, dest, row_bytes, packed, s);
+    launch_any<uint16_t>(r, s);
   } else {
-    launch_any<uint8_t>(X, ids, off, n, pairs, dest, row_bytes, packed, s);
+    launch_any<uint8_t>(r, s);
   }
   DG_HIP(hipGetLastError());
   return DG_OK;
@@ -319,12 +370,18 @@ int pack_impl(const void *feats, int64_t N, int64_t row_bytes, const int32_t *ca
               int32_t B, const int32_t *nodes, int64_t node_stride, const int64_t *node_count,
               int64_t packed_cap, void *packed, int32_t *packed_ids, int64_t *packed_ptr,
               int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique, int64_t unique_cap,
-              uint64_t *membership, const uint8_t *member_lines, uint32_t flags, void *ws,
+              uint64_t *membership, const uint8_t *member_lines, const int32_t *cache_nodes,
+              int64_t cache_rows, void *cache_table, uint32_t flags, void *ws,
               size_t ws_bytes, hipStream_t stream, hipStream_t rows_stream, dg_sizes *sizes,
               dg_timing *timing, bool no_alloc) {
   if (!feats || !cache_slot || !nodes || !node_count || !packed_ptr || !packed_ptr_host ||
       !loc || !sizes)
     return set_error(DG_EINVAL, "dg_pack_group: null pointer argument");
+  if (cache_table && (!cache_nodes || cache_rows < 0 || !packed ||
+                      (flags & DG_PACK_ROWS_STREAM)))
+    return set_error(DG_EINVAL, "dg_pack_group: the cache fill needs cache_nodes, "
+                                "cache_rows >= 0 and packed, and no DG_PACK_ROWS_STREAM");
+  const int64_t n_cache = cache_table ? cache_rows : 0;
   if (N < 1 || N > 0x7fffffffll || row_bytes < 1 || B < 1 || B > DG_MAX_BATCHES ||
       node_stride < 0 || packed_cap < 0 || unique_cap < 0)
     return set_error(DG_EINVAL, "dg_pack_group: bad sizes (N=%lld row_bytes=%lld B=%d)",
@@ -436,6 +493,11 @@ int pack_impl(const void *feats, int64_t N, int64_t row_bytes, const int32_t *ca
   // side, the tables on a side stream joined back before the call returns, and
   // timed calls run them one after the other so that each phase has its own
   // time.
+  // The row copy also fills the cache table when one is given (the cache as
+  // one more mini-batch of the same gather, §5.2).
+  const RowCopy rc_rows{feats,      N,      row_bytes,   w.unc_ids, w.unc_off,
+                        sizes->unique_packed,  rows, w.pairdest, packed,
+                        cache_nodes, n_cache, cache_table, w.err};
   const bool rows_async = (flags & DG_PACK_ROWS_STREAM) && packed;
   SideStream *side = nullptr;
   if (rows_async && total > 0) {
@@ -443,9 +505,7 @@ int pack_impl(const void *feats, int64_t N, int64_t row_bytes, const int32_t *ca
     DG_TRY(side_stream(&ss));
     DG_HIP(hipEventRecord(ss->handoff, s));
     DG_HIP(hipStreamWaitEvent(rows_stream, ss->handoff, 0));
-    if ((rc = launch_fanout(feats, w.unc_ids, w.unc_off, sizes->unique_packed, rows, w.pairdest,
-                            row_bytes, packed, rows_stream)))
-      return rc;
+    if ((rc = launch_fanout(rc_rows, rows_stream))) return rc;
   } else if (!timing && !no_alloc && packed && total > 0) {
     DG_TRY(side_stream(&side));
     DG_HIP(hipEventRecord(side->fork, s));
@@ -465,8 +525,7 @@ int pack_impl(const void *feats, int64_t N, int64_t row_bytes, const int32_t *ca
   if (side) DG_HIP(hipEventRecord(side->join, side->s));
   const int e3 = tm.mark();
   if (packed && !rows_async &&  // packed == NULL: address tables only, no row copy
-      (rc = launch_fanout(feats, w.unc_ids, w.unc_off, sizes->unique_packed, rows, w.pairdest,
-                          row_bytes, packed, s)))
+      (rc = launch_fanout(rc_rows, s)))
     return rc;
   if (side) DG_HIP(hipStreamWaitEvent(s, side->join, 0));
   const int e4 = tm.mark();
@@ -496,13 +555,14 @@ extern "C" int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
                              void *packed, int32_t *packed_ids, int64_t *packed_ptr,
                              int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique,
                              int64_t unique_cap, uint64_t *membership,
-                             const uint8_t *member_lines, uint32_t flags,
+                             const uint8_t *member_lines, const int32_t *cache_nodes,
+                             int64_t cache_rows, void *cache_table, uint32_t flags,
                              void *ws, size_t ws_bytes, hipStream_t stream,
                              hipStream_t rows_stream, dg_sizes *sizes, dg_timing *timing) {
   return pack_impl(feats, N, row_bytes, cache_slot, B, nodes, node_stride, node_count,
                    packed_cap, packed, packed_ids, packed_ptr, packed_ptr_host, loc, group_unique,
-                   unique_cap, membership, member_lines, flags, ws, ws_bytes, stream, rows_stream,
-                   sizes, timing, false);
+                   unique_cap, membership, member_lines, cache_nodes, cache_rows, cache_table,
+                   flags, ws, ws_bytes, stream, rows_stream, sizes, timing, false);
 }
 
 extern "C" size_t dg_pack_noalloc_scratch_bytes(void) { return NOALLOC_SCRATCH_BYTES; }
@@ -514,13 +574,15 @@ extern "C" int dg_pack_group_noalloc(const void *feats, int64_t N, int64_t row_b
                                      int64_t *packed_ptr, int64_t *packed_ptr_host, int32_t *loc,
                                      int32_t *group_unique, int64_t unique_cap,
                                      uint64_t *membership, const uint8_t *member_lines,
-                                     uint32_t flags, hipStream_t stream, dg_sizes *sizes) {
+                                     const int32_t *cache_nodes, int64_t cache_rows,
+                                     void *cache_table, uint32_t flags, hipStream_t stream,
+                                     dg_sizes *sizes) {
   if (flags & DG_PACK_ROWS_STREAM)
     return set_error(DG_EINVAL, "dg_pack_group_noalloc: DG_PACK_ROWS_STREAM is not available");
   void *ws = nullptr;
   DG_TRY(scratch_address(&ws));
   return pack_impl(feats, N, row_bytes, cache_slot, B, nodes, node_stride, node_count,
                    packed_cap, packed, packed_ids, packed_ptr, packed_ptr_host, loc, group_unique,
-                   unique_cap, membership, member_lines, flags, ws, NOALLOC_SCRATCH_BYTES, stream,
-                   nullptr, sizes, nullptr, true);
+                   unique_cap, membership, member_lines, cache_nodes, cache_rows, cache_table,
+                   flags, ws, NOALLOC_SCRATCH_BYTES, stream, nullptr, sizes, nullptr, true);
 }

@@ -330,6 +330,139 @@ __global__ __launch_bounds__(THREADS) void k_relabel_direct(Lists L, int64_t edg
   edge_dst[e] = j;
 }
 
+// ---------------------------------------------------------------- last-hop relabelling by search
+// The last hop's new nodes form one ascending segment at the end of each
+// batch's list, so a last-hop edge whose neighbour is one of them gets its
+// local index as the neighbour's rank in that segment; only edges into nodes
+// listed earlier look the direct table up.  The last hop then writes no table
+// entries at all.  Each batch's segment is copied into a padded, aligned buffer
+// together with a sparse index (every S-th element); a block stages its batch's
+// sparse index in LDS, searches it, and reads one S-element block of the
+// segment (from L2: blocks are ordered so that all blocks of a batch run on one
+// XCD).
+constexpr int RL_THREADS = 512;
+constexpr int RL_CHUNKS = 4;          // edge chunks per block (one staging of the index)
+constexpr int RL_SPARSE_MAX = 16384;  // sparse-index entries per batch (64 KB of LDS)
+constexpr int RL_S_MAX_LOG2 = 6;      // block length S = 16, 32 or 64
+constexpr int RL_S_MIN_LOG2 = 4;
+constexpr int64_t RL_SEGMENT_MAX = (int64_t)RL_SPARSE_MAX << RL_S_MAX_LOG2;
+
+// edges per thread for block length 2^SLOG2 (keeps the block reads within registers)
+__host__ __device__ constexpr int rl_edges(int slog2) { return slog2 <= 4 ? 4 : (slog2 == 5 ? 2 : 1); }
+
+inline int64_t rl_segcap(int64_t node_cap) {
+  return (node_cap + (1 << RL_S_MAX_LOG2) + 63) & ~(int64_t)63;
+}
+
+struct LastHop {
+  int B;
+  int s_log2;                           // block length S = 2^s_log2
+  int32_t bstart[DG_MAX_BATCHES + 1];   // logical blocks before batch b
+  int32_t m[DG_MAX_BATCHES];            // length of b's last-hop segment
+  int32_t ecount[DG_MAX_BATCHES];       // b's last-hop edges
+  int64_t seg0[DG_MAX_BATCHES];         // local index of the segment's first node
+  int64_t e0[DG_MAX_BATCHES];           // index of b's first last-hop edge
+  int64_t cstart[DG_MAX_BATCHES + 1];   // prefix of the padded segment lengths
+};
+
+// Copies each batch's last-hop segment into segbuf (row b at b*segcap), padded
+// with INT32_MAX to a multiple of S, and every S-th element into sparse.
+__global__ __launch_bounds__(THREADS) void k_last_segments(LastHop h, const int32_t *nodes,
+                                                           int64_t node_cap, int32_t *segbuf,
+                                                           int64_t segcap, int32_t *sparse) {
+  const int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
+  if (i >= h.cstart[h.B]) return;
+  const int b = find_batch_wave(h.cstart, h.B, i);
+  const int64_t r = i - h.cstart[b];
+  const int32_t v = r < h.m[b] ? nodes[(int64_t)b * node_cap + h.seg0[b] + r] : INT32_MAX;
+  segbuf[(int64_t)b * segcap + r] = v;
+  if ((r & ((1 << h.s_log2) - 1)) == 0) sparse[(int64_t)b * RL_SPARSE_MAX + (r >> h.s_log2)] = v;
+}
+
+template <int SLOG2>
+__global__ __launch_bounds__(RL_THREADS) void k_relabel_last(LastHop h, const int32_t *segbuf,
+                                                             int64_t segcap,
+                                                             const int32_t *sparse,
+                                                             int64_t edge_cap, int32_t *edge_dst,
+                                                             const int32_t *local, int64_t N,
+                                                             uint32_t *err) {
+  constexpr int S = 1 << SLOG2;
+  constexpr int EPT = rl_edges(SLOG2);
+  constexpr int PER_CHUNK = RL_THREADS * EPT;
+  extern __shared__ int32_t s_sp[];
+  // The hardware hands consecutive blocks to the 8 XCDs in turn; logical block
+  // numbers are assigned so that each XCD takes one contiguous run of them (the
+  // grid is a multiple of 8), i.e. whole batches, one after the other.
+  const int per = (int)(gridDim.x >> 3);
+  const int lb = (int)(blockIdx.x & 7u) * per + (int)(blockIdx.x >> 3);
+  if (lb >= h.bstart[h.B]) return;  // whole block
+  int b = 0;
+  while (b + 1 < h.B && h.bstart[b + 1] <= lb) ++b;
+  const int R = (h.m[b] + S - 1) >> SLOG2;
+  const int32_t *sp = sparse + (int64_t)b * RL_SPARSE_MAX;
+  for (int i = threadIdx.x; i < R; i += RL_THREADS) s_sp[i] = sp[i];
+  __syncthreads();
+  int top = 1;  // highest power of two <= R (uniform)
+  while (top * 2 <= R) top *= 2;
+  const int64_t eend = h.e0[b] + h.ecount[b];
+  int32_t *ed = edge_dst + (int64_t)b * edge_cap;
+  const int32_t *seg = segbuf + (int64_t)b * segcap;
+  const int B = h.B;
+  const int64_t seg0 = h.seg0[b];
+  for (int ch = 0; ch < RL_CHUNKS; ++ch) {
+    const int64_t ebase = h.e0[b] + ((int64_t)(lb - h.bstart[b]) * RL_CHUNKS + ch) * PER_CHUNK +
+                          threadIdx.x;
+    if (ebase - threadIdx.x >= eend) break;  // uniform
+    int32_t u[EPT];
+#pragma unroll
+    for (int k = 0; k < EPT; ++k) {
+      const int64_t e = ebase + (int64_t)k * RL_THREADS;
+      u[k] = e < eend ? ed[e] : -1;
+    }
+    // pos = number of sparse entries <= u: the block that may hold u is pos - 1
+    int pos[EPT];
+#pragma unroll
+    for (int k = 0; k < EPT; ++k) pos[k] = 0;
+    if (R > 0) {
+      for (int step = top; step > 0; step >>= 1) {
+#pragma unroll
+        for (int k = 0; k < EPT; ++k)
+          if (pos[k] + step <= R && s_sp[pos[k] + step - 1] <= u[k]) pos[k] += step;
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < EPT; ++k) {
+      const int64_t e = ebase + (int64_t)k * RL_THREADS;
+      if (e >= eend || u[k] < 0 || (int64_t)u[k] >= N) continue;  // bad IDs already reported
+      int c = 0;
+      bool found = false;
+      const int blk = pos[k] - 1;
+      if (blk >= 0) {
+        const uint4 *bp = reinterpret_cast<const uint4 *>(seg + ((int64_t)blk << SLOG2));
+#pragma unroll
+        for (int q = 0; q < S / 4; ++q) {
+          const uint4 x = bp[q];
+          const int32_t a0 = (int32_t)x.x, a1 = (int32_t)x.y;
+          const int32_t a2 = (int32_t)x.z, a3 = (int32_t)x.w;
+          c += (a0 < u[k]) + (a1 < u[k]) + (a2 < u[k]) + (a3 < u[k]);
+          found |= (a0 == u[k]) | (a1 == u[k]) | (a2 == u[k]) | (a3 == u[k]);
+        }
+      }
+      int64_t j;
+      if (found) {
+        j = seg0 + ((int64_t)blk << SLOG2) + c;
+      } else {  // a node listed before the last hop
+        j = local[(int64_t)u[k] * B + b];
+        if (j < 0 || j >= seg0) {
+          atomicOr(err, ERR_INTERNAL);
+          continue;
+        }
+      }
+      ed[e] = (int32_t)j;
+    }
+  }
+}
+
 // Host staging block (int64 entries): edge bounds, compaction totals, error word.
 constexpr int ST_BOUNDS = 0;                              // [B+1]
 constexpr int ST_TOTALS = ST_BOUNDS + DG_MAX_BATCHES + 1; // [B+4]
@@ -353,6 +486,8 @@ struct SampleWs {
   int64_t *f_off, *f_deg, *f_cnt, *f_eoff, *tiles;
   LocalTable table;  // hash relabelling
   int32_t *local;    // direct relabelling: [N][B]
+  int32_t *segbuf;   // direct relabelling: last-hop segments, [B][rl_segcap(node_cap)]
+  int32_t *sparse;   // ... and their sparse indices, [B][RL_SPARSE_MAX]
   uint8_t *touched;  // touched marks (a byte per 2^MC_TOUCH_SHIFT nodes)
   int64_t *small;    // staging for a few counts
   MaskScan ms;
@@ -371,6 +506,8 @@ void carve_sample(SampleWs &w, Carve &c, int64_t N, int B, int64_t node_cap, boo
   w.table.bits = direct ? 0 : lt_bits_for(fmax);
   w.table.slots = direct ? nullptr : c.take<uint64_t>((size_t)1 << w.table.bits);
   w.local = direct ? c.take<int32_t>((size_t)N * (size_t)B) : nullptr;
+  w.segbuf = direct ? c.take<int32_t>((size_t)B * (size_t)rl_segcap(node_cap)) : nullptr;
+  w.sparse = direct ? c.take<int32_t>((size_t)B * RL_SPARSE_MAX) : nullptr;
   w.touched = c.take<uint8_t>((size_t)mc_touch_bytes(N));
   w.small = c.take<int64_t>(ST_SIZE);
   w.ms = MaskScan{};
@@ -497,6 +634,7 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
   }
   bool prev_cleared = false;  // the last hop's count pass zeroed prev
   bool lines_done = false;    // the last hop's count pass wrote member_lines
+  bool rl_search = false;     // the last hop's edges are relabelled by search
   hipLaunchKernelGGL(k_seed_init, dim3(blocks_for((int64_t)B * S)), dim3(THREADS), 0, s, seeds,
                      B, S, N, node_cap, nodes, w.visited, w.prev, w.local, cache_slot, loc,
                      w.err);
@@ -607,8 +745,25 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
         w.ms.seg_end[b] = (int64_t)(b + 1) * node_cap;
         w.ms.local_base[b] = n_b[b];
       }
+      // Direct relabelling: the last hop's edges find their new neighbours by
+      // search in the hop's segment, so that hop writes no table entries,
+      // unless a segment could outgrow the sparse index (an upper bound is all
+      // that is known before the hop's counts come back).
+      if (direct && k == K) {
+        int64_t mbound = 0, ebound = 0;
+        for (int b = 0; b < B; ++b) {
+          const int64_t front = h.fstart[b + 1] - h.fstart[b];
+          int64_t mb = node_cap - n_b[b];
+          const int64_t eb = f < 0 ? E : (front > E / (f > 0 ? f : 1) ? E : front * f);
+          if (eb < mb) mb = eb;
+          if (N < mb) mb = N;
+          if (mb > mbound) mbound = mb;
+          if (eb > ebound) ebound = eb;
+        }
+        rl_search = mbound <= RL_SEGMENT_MAX && ebound <= INT32_MAX;
+      }
       w.ms.seg_out = nodes;
-      w.ms.local_out = w.local;
+      w.ms.local_out = (k == K && rl_search) ? nullptr : w.local;
       w.ms.loc_slot = cache_slot;  // the list's address-table entries beside it
       w.ms.loc_out = loc;
       w.ms.uniq_out = nullptr;
@@ -674,7 +829,59 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
     LE.start[b + 1] = LE.start[b] + e_b[b];
     LE.n[b] = n_b[b];
   }
-  if (LE.start[B] > 0 && direct) {
+  if (LE.start[B] > 0 && direct && rl_search) {
+    // edges of the hops before the last through the table, the last hop's by
+    // search in its segment
+    LastHop lh;
+    memset(&lh, 0, sizeof(lh));
+    lh.B = B;
+    int64_t m_max = 0;
+    for (int b = 0; b < B; ++b) {
+      const int64_t before = edge_ptr[(int64_t)b * (K + 1) + (K - 1)];
+      LE.start[b + 1] = LE.start[b] + before;
+      lh.seg0[b] = hop_ptr[(int64_t)b * (K + 2) + K];
+      lh.m[b] = (int32_t)(n_b[b] - lh.seg0[b]);
+      lh.e0[b] = before;
+      lh.ecount[b] = (int32_t)(e_b[b] - before);
+      if (lh.m[b] > m_max) m_max = lh.m[b];
+    }
+    lh.s_log2 = RL_S_MIN_LOG2;
+    while (lh.s_log2 < RL_S_MAX_LOG2 && (m_max + (1 << lh.s_log2) - 1) >> lh.s_log2 > RL_SPARSE_MAX)
+      ++lh.s_log2;
+    const int S = 1 << lh.s_log2;
+    const int per_block = RL_THREADS * rl_edges(lh.s_log2) * RL_CHUNKS;
+    lh.cstart[0] = 0;
+    lh.bstart[0] = 0;
+    int64_t r_max = 0;
+    for (int b = 0; b < B; ++b) {
+      const int64_t r = (lh.m[b] + S - 1) / S;
+      if (r > r_max) r_max = r;
+      lh.cstart[b + 1] = lh.cstart[b] + r * S;
+      lh.bstart[b + 1] = lh.bstart[b] + (int32_t)((lh.ecount[b] + per_block - 1) / per_block);
+    }
+    if (r_max > RL_SPARSE_MAX)
+      return set_error(DG_EINVAL, "internal: last-hop segment of %lld nodes", (long long)m_max);
+    if (LE.start[B] > 0) {
+      hipLaunchKernelGGL(k_relabel_direct, dim3(blocks_for(LE.start[B])), dim3(THREADS), 0, s,
+                         LE, edge_cap, edge_dst, w.local, N, w.err);
+    }
+    if (lh.cstart[B] > 0)
+      hipLaunchKernelGGL(k_last_segments, dim3(blocks_for(lh.cstart[B])), dim3(THREADS), 0, s,
+                         lh, nodes, node_cap, w.segbuf, rl_segcap(node_cap), w.sparse);
+    if (lh.bstart[B] > 0) {
+      const unsigned grid = (unsigned)((lh.bstart[B] + 7) & ~7);
+      const size_t lds = (size_t)(r_max > 0 ? r_max : 1) * sizeof(int32_t);
+      auto go = [&](auto slog2) {
+        hipLaunchKernelGGL((k_relabel_last<decltype(slog2)::value>), dim3(grid),
+                           dim3(RL_THREADS), lds, s, lh, w.segbuf, rl_segcap(node_cap),
+                           w.sparse, edge_cap, edge_dst, w.local, N, w.err);
+      };
+      if (lh.s_log2 == 4) go(std::integral_constant<int, 4>());
+      else if (lh.s_log2 == 5) go(std::integral_constant<int, 5>());
+      else go(std::integral_constant<int, 6>());
+    }
+    DG_HIP(hipGetLastError());
+  } else if (LE.start[B] > 0 && direct) {
     hipLaunchKernelGGL(k_relabel_direct, dim3(blocks_for(LE.start[B])), dim3(THREADS), 0, s, LE,
                        edge_cap, edge_dst, w.local, N, w.err);
     DG_HIP(hipGetLastError());

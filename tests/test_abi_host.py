@@ -69,10 +69,13 @@ def test_workspace_queries(L):
     # the clear flags do not change the workspace size
     assert L.dg_sample_workspace_bytes(10_000, 4, 2000, 2000, 2 | 4 | 8) == \
         L.dg_sample_workspace_bytes(10_000, 4, 2000, 2000, 2)
-    # the direct relabelling table replaces the hash table: 4*N*B bytes
+    # the direct relabelling table replaces the hash table: 4*N*B bytes, plus the
+    # last hop's segments (at most node_cap + 192 per batch) and sparse indices
+    # (16384 entries per batch), 4 bytes each
     d = L.dg_sample_workspace_bytes(10_000_000, 64, 2000, 2000, 2)
     h = L.dg_sample_workspace_bytes(10_000_000, 64, 2000, 2000, 0)
-    assert d > h and d - 4 * 10_000_000 * 64 < h
+    search = 4 * 64 * (2000 + 192) + 4 * 64 * 16384
+    assert d > h and d - 4 * 10_000_000 * 64 - search < h
     assert L.dg_sample_workspace_bytes(10_000, 4, 2000, 2000, 3) == \
         L.dg_sample_workspace_bytes(10_000, 4, 2000, 2000, 2)
     p = L.dg_pack_workspace_bytes(10_000, 4, 8000)
@@ -124,32 +127,43 @@ def test_host_side_argument_errors(L):
     cnt = (ctypes.c_int64 * 2)(3, 9)
     ph = (ctypes.c_int64 * 3)()
     rc = L.dg_pack_group(fake, 10, 0, fake, 2, fake, 8, cnt, 0, None, None, fake, ph, fake, None,
-                         0, None, None, 0, fake, 1 << 20, None, None, ctypes.byref(sizes), None)
+                         0, None, None, None, 0, None, 0, fake, 1 << 20, None, None,
+                         ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL
     rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, cnt, 0, None, None, fake, ph, fake, None,
-                         0, None, None, 0, fake, 1 << 20, None, None, ctypes.byref(sizes), None)
+                         0, None, None, None, 0, None, 0, fake, 1 << 20, None, None,
+                         ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL and b"node_count" in L.dg_last_error()
     # pack flags: unknown bits, and a clear request without a membership mask
     ok_cnt = (ctypes.c_int64 * 2)(3, 5)
     rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, ok_cnt, 0, None, None, fake, ph, fake,
-                         None, 0, fake, None, 8, fake, 1 << 20, None, None, ctypes.byref(sizes),
-                         None)
+                         None, 0, fake, None, None, 0, None, 8, fake, 1 << 20, None, None,
+                         ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL and b"flags" in L.dg_last_error()
     rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, ok_cnt, 0, None, None, fake, ph, fake,
-                         None, 0, None, None, _lib.DG_PACK_CLEAR_MEMBERSHIP, fake, 1 << 20, None,
-                         None, ctypes.byref(sizes), None)
+                         None, 0, None, None, None, 0, None, _lib.DG_PACK_CLEAR_MEMBERSHIP, fake,
+                         1 << 20, None, None, ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL and b"membership" in L.dg_last_error()
     # a row copy left on a second stream cannot be timed by the call
     tm = _lib.Timing()
     rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, ok_cnt, 0, fake, None, fake, ph, fake,
-                         None, 0, None, None, _lib.DG_PACK_ROWS_STREAM, fake, 1 << 20, None, None,
-                         ctypes.byref(sizes), ctypes.byref(tm))
+                         None, 0, None, None, None, 0, None, _lib.DG_PACK_ROWS_STREAM, fake,
+                         1 << 20, None, None, ctypes.byref(sizes), ctypes.byref(tm))
     assert rc == _lib.DG_EINVAL and b"timing" in L.dg_last_error()
     # member lines come with a membership mask
     rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, ok_cnt, 0, None, None, fake, ph, fake,
-                         None, 0, None, fake, 0, fake, 1 << 20, None, None,
+                         None, 0, None, fake, None, 0, None, 0, fake, 1 << 20, None, None,
                          ctypes.byref(sizes), None)
     assert rc == _lib.DG_EINVAL and b"member_lines" in L.dg_last_error()
+    # the cache fill needs its node list, a packed buffer and no rows stream
+    rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, ok_cnt, 0, None, None, fake, ph, fake,
+                         None, 0, None, None, None, 4, fake, 0, fake, 1 << 20, None, None,
+                         ctypes.byref(sizes), None)
+    assert rc == _lib.DG_EINVAL and b"cache fill" in L.dg_last_error()
+    rc = L.dg_pack_group(fake, 10, 4, fake, 2, fake, 8, ok_cnt, 0, fake, None, fake, ph, fake,
+                         None, 0, None, None, fake, 4, fake, _lib.DG_PACK_ROWS_STREAM, fake,
+                         1 << 20, None, fake, ctypes.byref(sizes), None)
+    assert rc == _lib.DG_EINVAL and b"cache fill" in L.dg_last_error()
     # member-lines map size: a byte per 8 nodes, in blocks of 4096 nodes
     assert L.dg_member_lines_bytes(0) == 0
     assert L.dg_member_lines_bytes(1) == 512

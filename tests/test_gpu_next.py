@@ -158,3 +158,93 @@ def test_minhash_rejects_bad_hash_values(dg):
     perms = torch.tensor([[0, 5]], dtype=torch.int32, device=DEV)
     with pytest.raises(dg.DGError):
         dg.minhash_order(mem, 2, entries, perms)
+
+
+@pytest.mark.parametrize("name", ["T", "M1"])
+@pytest.mark.parametrize("ranking", ["in_degree", "frequency"])
+def test_cache_filled_by_the_packing_gather(dg, orc, name, ranking):
+    """The cache taken as one more mini-batch of batched packing (§5.2): one
+    gather launch writes the packed chunks and the cache table.  The cache table
+    equals X[cache_nodes] byte for byte (empty slots left as they were), the
+    packed chunks equal those of packing without it, and every batch assembled
+    from this cache equals the oracle's assembly."""
+    w = synth.make_workload(name, device=DEV) if name != "T" else synth.make_workload("T")
+    X = w.feats.to(DEV)
+    sr, mem = sampled(dg, w)
+    if ranking == "in_degree":
+        slot, nodes = w.cache_slot.to(DEV), w.cache_nodes.to(DEV).to(torch.int32)
+    else:  # more slots than accessed nodes: the last ones stay empty (-1)
+        C = int((mem != 0).sum()) + 37
+        slot, nodes, cached = dg.cache_by_frequency(mem, w.cfg.B, C)
+        assert cached == C - 37
+    R = w.cfg.row_bytes
+    C = nodes.numel()
+    plain = dg.pack_group(X, slot, sr.nodes, sr.node_count, with_unique=True)
+    table = torch.full((C, R), 0xCD, dtype=torch.uint8, device=DEV)
+    filled = dg.pack_group(X, slot, sr.nodes, sr.node_count, with_unique=True,
+                           cache_nodes=nodes, cache_table=table)
+    torch.cuda.synchronize()
+    rows = plain.sizes["packed_rows"]
+    assert filled.sizes == plain.sizes
+    assert torch.equal(filled.packed[:rows], plain.packed[:rows])
+    full = nodes >= 0
+    ref = X.index_select(0, nodes[full].long()).view(torch.uint8).reshape(-1, R)
+    assert torch.equal(table[full], ref)
+    assert bool((table[~full] == 0xCD).all())
+    # assembly from the filled cache equals the oracle's
+    Xh = w.feats.cpu().numpy()
+    lists = [sr.batch_nodes(b).cpu().numpy() for b in range(w.cfg.B)]
+    refp = orc.pack_group(Xh, slot.cpu().numpy(), lists)
+    cache_h = table.cpu().numpy()
+    for b in (0, w.cfg.B - 1):
+        lo, hi = refp["packed_ptr"][b], refp["packed_ptr"][b + 1]
+        y_ref = orc.assemble_batch(cache_h, refp["packed"][lo:hi], refp["loc"][b], R)
+        n = len(lists[b])
+        y = dg.assemble_batch(table, filled.chunk(b), filled.loc[b, :n], R)
+        assert np.array_equal(y.cpu().numpy(), y_ref), b
+        assert np.array_equal(y_ref, Xh.view(np.uint8).reshape(w.cfg.n, -1)[lists[b]]), b
+
+
+def test_cache_fill_reports_a_bad_cache_node(dg):
+    w = synth.make_workload("T")
+    X = w.feats.to(DEV)
+    sr, mem = sampled(dg, w)
+    nodes = w.cache_nodes.to(DEV).to(torch.int32).clone()
+    nodes[3] = w.cfg.n + 5
+    table = torch.zeros((nodes.numel(), w.cfg.row_bytes), dtype=torch.uint8, device=DEV)
+    with pytest.raises(dg.DGError) as e:
+        dg.pack_group(X, w.cache_slot.to(DEV), sr.nodes, sr.node_count, cache_nodes=nodes,
+                      cache_table=table)
+    assert e.value.status == -1
+    assert int(table[3].sum()) == 0  # its row is left as it was
+
+
+@pytest.mark.parametrize("dtype,dim", [(torch.uint8, 3), (torch.float16, 5), (torch.float32, 16),
+                                       (torch.float16, 768), (torch.float32, 1024)])
+def test_cache_fill_every_row_shape(dg, dtype, dim):
+    """The cache fill on each launch shape of the row copy (16-byte vectors and
+    the narrower words of odd row sizes)."""
+    n = 3000
+    off, idx = synth.uniform_graph(n, 1, 12, seed=dim)
+    off, idx = torch.from_numpy(off).to(DEV), torch.from_numpy(idx).to(DEV)
+    gen = torch.Generator().manual_seed(dim)
+    seeds = torch.stack([torch.randperm(n, generator=gen)[:40] for _ in range(3)]).to(torch.int32)
+    X = torch.randint(0, 120, (n, dim), generator=gen).to(dtype).to(DEV)
+    nodes = torch.randperm(n, generator=gen)[:300].to(torch.int32).to(DEV)
+    nodes[7] = -1  # an empty slot
+    slot = torch.full((n,), -1, dtype=torch.int32, device=DEV)
+    keep = nodes >= 0
+    slot[nodes[keep].long()] = torch.arange(300, dtype=torch.int32, device=DEV)[keep]
+    sr = dg.sample_group(off, idx, seeds.to(DEV), [4, 3], 5)
+    R = X[0].numel() * X.element_size()
+    table = torch.full((300, R), 0x5A, dtype=torch.uint8, device=DEV)
+    pr = dg.pack_group(X, slot, sr.nodes, sr.node_count, cache_nodes=nodes, cache_table=table)
+    torch.cuda.synchronize()
+    ref = X.index_select(0, nodes[keep].long()).contiguous().view(torch.uint8).reshape(-1, R)
+    assert torch.equal(table[keep], ref)
+    assert bool((table[7] == 0x5A).all())
+    for b in range(3):
+        n_b = int(sr.hop_ptr[b, -1])
+        y = dg.assemble_batch(table, pr.chunk(b), pr.loc[b, :n_b], R)
+        want = X.index_select(0, sr.batch_nodes(b).long()).contiguous().view(torch.uint8)
+        assert torch.equal(y, want.reshape(n_b, R)), b

@@ -418,3 +418,50 @@ def test_pack_rows_on_a_second_stream(dg, name):
             assert torch.equal(ys[b][:n], X.index_select(0, sr.nodes[b, :n].long())
                                .view(torch.uint8).reshape(n, R)), b
         del ws
+
+
+def layered_star_graph(n, n_seed, seed_deg, n_mid, mid_deg, seed=0):
+    """CSR where nodes [0, n_seed) point to `seed_deg` random nodes of the middle
+    range [n_seed, n_seed + n_mid), middle nodes to `mid_deg` random nodes of
+    [0, n), and every other node to none: a two-hop sample reaches a few
+    thousand middle nodes, then hundreds of thousands of new nodes."""
+    rng = np.random.default_rng(seed)
+    deg = np.zeros(n, dtype=np.int64)
+    deg[:n_seed] = seed_deg
+    deg[n_seed:n_seed + n_mid] = mid_deg
+    off = np.zeros(n + 1, dtype=np.int64)
+    off[1:] = np.cumsum(deg)
+    rows = []
+    for v in range(n_seed + n_mid):
+        if v < n_seed:
+            r = rng.choice(np.arange(n_seed, n_seed + n_mid), seed_deg, replace=False)
+        else:
+            r = rng.choice(n, mid_deg + 1, replace=False)
+            r = r[r != v][:mid_deg]
+        rows.append(np.sort(r))
+    return torch.from_numpy(off), torch.from_numpy(np.concatenate(rows).astype(np.int32))
+
+
+@pytest.mark.parametrize("last_fanout", [150, 260])
+def test_last_hop_segments_of_a_few_hundred_thousand_nodes(dg, orc, last_fanout):
+    """The last hop lists about 0.4M (fan-out 150) and 0.7M (260) new nodes in
+    one mini-batch, beyond the shortest block length of the last hop's search
+    (2^18 nodes), so both longer block lengths run; and its edges into nodes of
+    the first hop still go through the table.  Bit-exact against the oracle,
+    with and without the cached nodes' address tables from sampling."""
+    n, n_seed, n_mid = 4_000_000, 4096, 3000
+    off, idx = layered_star_graph(n, n_seed, 20, n_mid, 300, seed=last_fanout)
+    seeds = torch.stack([torch.arange(0, 2048, dtype=torch.int32),
+                         torch.arange(2048, 4096, dtype=torch.int32)])
+    gen = torch.Generator().manual_seed(3)
+    feats = torch.randn((n, 4), generator=gen)
+    rnd = random.Random(last_fanout)
+    ncache = n // 20
+    cache_nodes = torch.tensor(rnd.sample(range(n), ncache), dtype=torch.int64)
+    slot = torch.full((n,), -1, dtype=torch.int32)
+    slot[cache_nodes] = torch.arange(ncache, dtype=torch.int32)
+    for handoff in (False, True):
+        sr, _ = check_all(dg, orc, off, idx, seeds, [5, last_fanout], 77, feats, slot,
+                          cache_nodes, sample_kw={"direct": True, "handoff": handoff})
+        m = [int(sr.hop_ptr[b, -1] - sr.hop_ptr[b, -2]) for b in range(2)]
+        assert max(m) > (1 << 18), m  # beyond the shortest block length

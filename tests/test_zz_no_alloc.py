@@ -107,12 +107,13 @@ def test_noalloc_pack_rejects_sizes_beyond_its_scratch(dg):
     rc = L.dg_pack_group_noalloc(fake, N, 16, fake, 1, fake, 1,
                                  counts.ctypes.data_as(dg._lib.I64P), 1, fake, fake, fake,
                                  ptr_host.ctypes.data_as(dg._lib.I64P), fake, None, 0, None,
-                                 None, 0, None, ctypes.byref(sz))
+                                 None, None, 0, None, 0, None, ctypes.byref(sz))
     assert rc == dg._lib.DG_EWORKSPACE
     assert b"scratch" in L.dg_last_error()
     # and the rows stream, which needs a second stream, is refused
     rc = L.dg_pack_group_noalloc(fake, 16, 16, fake, 1, fake, 1,
                                  counts.ctypes.data_as(dg._lib.I64P), 1, fake, fake, fake,
                                  ptr_host.ctypes.data_as(dg._lib.I64P), fake, None, 0, None,
-                                 None, dg._lib.DG_PACK_ROWS_STREAM, None, ctypes.byref(sz))
+                                 None, None, 0, None, dg._lib.DG_PACK_ROWS_STREAM, None,
+                                 ctypes.byref(sz))
     assert rc == dg._lib.DG_EINVAL
