@@ -95,7 +95,7 @@ def main():
     ap.add_argument("--no-loc-handoff", action="store_true",
                     help="packing builds every address-table entry itself, instead of "
                          "completing the ones sampling wrote for cached nodes (comparison)")
-    ap.add_argument("--sets", type=int, default=3,
+    ap.add_argument("--sets", type=int, default=2,
                     help="packing output sets (and workspaces) used in turn: step k waits for "
                          "the assembly of step k - sets before it writes into its set")
     ap.add_argument("--asm-inline", action="store_true",
@@ -170,8 +170,15 @@ def main():
     # workload's own group.
     n_region = args.warmup + args.steps
     n_groups = 2 * n_region
-    seeds_all = synth.seed_batches(cfg.n, n_groups * B, cfg.S, cfg.seed, dev, offsets=w.offsets)
-    groups = [seeds_all[g * B:(g + 1) * B] for g in range(n_groups)]
+    # A graph with fewer seed candidates (nodes with out-neighbours) than the
+    # stream needs reuses its seed groups in turn; every step still keeps its own
+    # global batch numbers, so its draws differ.
+    candidates = int((w.offsets[1:] > w.offsets[:-1]).sum())
+    n_seed_groups = max(1, min(n_groups, candidates // (B * cfg.S)))
+    seeds_all = synth.seed_batches(cfg.n, n_seed_groups * B, cfg.S, cfg.seed, dev,
+                                   offsets=w.offsets)
+    groups = [seeds_all[(g % n_seed_groups) * B:(g % n_seed_groups + 1) * B]
+              for g in range(n_groups)]
     assert torch.equal(groups[0], w.seeds), "the first group must be the workload's group"
 
     # Buffers (outside the timed regions): sampling outputs at the per-batch
@@ -463,8 +470,12 @@ def main():
         "frac_hbm_peak": round(value / HBM_PEAK_GBPS, 4),
         "groups": (f"a stream of distinct groups: every step samples, packs and assembles a group "
                    f"of its own ({B} mini-batches x {cfg.S} seeds, consecutive groups of one "
-                   f"seed stream drawn without replacement); value = the timed steps' own "
-                   f"feature bytes over their wall time"),
+                   f"seed stream drawn without replacement, global batch numbers g*{B}..); "
+                   f"value = the timed steps' own feature bytes over their wall time"
+                   + ("" if n_seed_groups == n_groups else
+                      f"; the graph has seed candidates for {n_seed_groups} disjoint groups, "
+                      f"so the {n_groups} groups reuse those seed sets in turn")),
+        "seed_groups": n_seed_groups,
         "pipelined": ("no: --no-pipeline, value is the serial rate" if args.no_pipeline else
                       "assembly of step k (second stream) overlaps sampling and packing of "
                       "step k+1; the serial figures below wait for each step's assembly"),

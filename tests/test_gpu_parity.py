@@ -465,3 +465,51 @@ def test_last_hop_segments_of_a_few_hundred_thousand_nodes(dg, orc, last_fanout)
                           cache_nodes, sample_kw={"direct": True, "handoff": handoff})
         m = [int(sr.hop_ptr[b, -1] - sr.hop_ptr[b, -2]) for b in range(2)]
         assert max(m) > (1 << 18), m  # beyond the shortest block length
+
+
+@pytest.mark.parametrize("direct", [False, True])
+def test_unaligned_list_outputs(dg, direct):
+    """Node lists, address tables and packed IDs handed over at 4-byte (not
+    16-byte) alignment give the outputs of aligned buffers, and nothing is
+    written before them."""
+    w = synth.make_workload("T")
+    off, idx, seeds = w.offsets.to(DEV), w.indices.to(DEV), w.seeds.to(DEV)
+    X, slot = w.feats.to(DEV), w.cache_slot.to(DEV)
+    fan = list(w.cfg.fanouts)
+    B = w.cfg.B
+    ncap, ecap = dg.sample_bounds(w.cfg.n, w.num_edges, w.cfg.S, fan)
+    ref = dg.sample_group(off, idx, seeds, fan, w.rng_seed, direct=direct, node_cap=ncap,
+                          edge_cap=ecap)
+    ref_p = dg.pack_group(X, slot, ref.nodes, ref.node_count, with_unique=True)
+    big = torch.full((B * ncap + 1,), -9, dtype=torch.int32, device=DEV)
+    nodes = big[1:].view(B, ncap)  # one element past a 16-byte boundary
+    assert nodes.data_ptr() % 16 == 4
+    out = dg.SampleResult(nodes=nodes, hop_ptr=np.zeros((B, len(fan) + 2), dtype=np.int64),
+                          edge_src=torch.empty((B, ecap), dtype=torch.int32, device=DEV),
+                          edge_dst=torch.empty((B, ecap), dtype=torch.int32, device=DEV),
+                          edge_ptr=np.zeros((B, len(fan) + 1), dtype=np.int64), sizes={},
+                          timing=None)
+    bigl = torch.full((B * ncap + 1,), -9, dtype=torch.int32, device=DEV)
+    loc = bigl[1:].view(B, ncap)
+    sr = dg.sample_group(off, idx, seeds, fan, w.rng_seed, direct=direct, out=out,
+                         cache_slot=slot, loc=loc)
+    rows = ref_p.sizes["packed_rows"]
+    bigp = torch.full((rows + 1,), -9, dtype=torch.int32, device=DEV)
+    po = dg.PackResult(packed=torch.empty((rows, ref_p.row_bytes), dtype=torch.uint8, device=DEV),
+                       packed_ids=bigp[1:], packed_ptr=torch.empty(B + 1, dtype=torch.int64,
+                                                                   device=DEV),
+                       packed_ptr_host=np.zeros(B + 1, dtype=np.int64), loc=loc,
+                       unique=torch.empty(ref_p.unique.numel(), dtype=torch.int32, device=DEV),
+                       sizes={}, timing=None, row_bytes=ref_p.row_bytes)
+    pr = dg.pack_group(X, slot, sr.nodes, sr.node_count, with_unique=True, out=po,
+                       loc_pending=True)
+    torch.cuda.synchronize()
+    assert int(big[0]) == -9 and int(bigl[0]) == -9 and int(bigp[0]) == -9
+    assert np.array_equal(sr.hop_ptr, ref.hop_ptr) and np.array_equal(sr.edge_ptr, ref.edge_ptr)
+    for b in range(B):
+        n, e = int(ref.hop_ptr[b, -1]), int(ref.edge_ptr[b, -1])
+        assert torch.equal(sr.nodes[b, :n], ref.nodes[b, :n]), b
+        assert torch.equal(sr.edge_dst[b, :e], ref.edge_dst[b, :e]), b
+        assert torch.equal(pr.loc[b, :n], ref_p.loc[b, :n]), b
+    assert torch.equal(pr.packed_ids[:rows], ref_p.packed_ids[:rows])
+    assert torch.equal(pr.packed[:rows], ref_p.packed[:rows])
