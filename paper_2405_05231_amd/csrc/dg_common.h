@@ -114,6 +114,19 @@ __device__ __forceinline__ int find_batch_wave(const int64_t *p, int n, int64_t 
   return find_batch(p, n, i);
 }
 
+// ---------------------------------------------------------------- XCD-aware block order
+// The hardware hands consecutive blocks of a grid to the 8 XCDs (each with its
+// own L2) in turn.  xcd_block(i, n) renumbers block i so that each XCD takes one
+// contiguous run of the n block numbers (a bijection on [0, n) for any n): work
+// whose outputs are laid out in block order then writes neighbouring lines from
+// one L2, where partial lines merge before they reach HBM.
+constexpr int NUM_XCD = 8;
+__device__ __forceinline__ uint32_t xcd_block(uint32_t i, uint32_t n) {
+  const uint32_t x = i % NUM_XCD, k = i / NUM_XCD;
+  const uint32_t q = n / NUM_XCD, r = n % NUM_XCD;
+  return x * q + (x < r ? x : r) + k;
+}
+
 // ---------------------------------------------------------------- local-index table
 // (node u, batch b) -> local index j of u in batch b's node list.  Open
 // addressing with linear probing over 2^bits 64-bit slots; an entry is

@@ -390,11 +390,9 @@ __global__ __launch_bounds__(RL_THREADS) void k_relabel_last(LastHop h, const in
   constexpr int EPT = rl_edges(SLOG2);
   constexpr int PER_CHUNK = RL_THREADS * EPT;
   extern __shared__ int32_t s_sp[];
-  // The hardware hands consecutive blocks to the 8 XCDs in turn; logical block
-  // numbers are assigned so that each XCD takes one contiguous run of them (the
-  // grid is a multiple of 8), i.e. whole batches, one after the other.
-  const int per = (int)(gridDim.x >> 3);
-  const int lb = (int)(blockIdx.x & 7u) * per + (int)(blockIdx.x >> 3);
+  // Each XCD takes one contiguous run of logical blocks, i.e. whole batches, one
+  // after the other.
+  const int lb = (int)xcd_block(blockIdx.x, gridDim.x);
   if (lb >= h.bstart[h.B]) return;  // whole block
   int b = 0;
   while (b + 1 < h.B && h.bstart[b + 1] <= lb) ++b;

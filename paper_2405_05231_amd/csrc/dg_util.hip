@@ -568,13 +568,16 @@ template <bool PACK, bool LOCAL>
 __global__ __launch_bounds__(MC_THREADS) void k_mask_write(MaskScan a) {
   const int lane = lane_id(), w = threadIdx.x >> 6;
   const int B = a.B, rows = mc_rows(B);
-  const int64_t t0 = (int64_t)blockIdx.x * MC_BLOCK_NODES + (int64_t)w * MC_TILE;
-  const size_t gwi = (size_t)blockIdx.x * MC_WAVES + w;
+  // Neighbouring blocks append to the same stretch of every batch's list: run
+  // them on one XCD, so that lines shared between them merge in its L2.
+  const uint32_t blk = xcd_block(blockIdx.x, gridDim.x);
+  const int64_t t0 = (int64_t)blk * MC_BLOCK_NODES + (int64_t)w * MC_TILE;
+  const size_t gwi = (size_t)blk * MC_WAVES + w;
   const uint32_t n = a.wcnt[gwi];
   if (n == 0) return;  // wave-uniform
   const uint64_t *cm = a.cw_mask + gwi * MC_TILE;
   const uint16_t *co = a.cw_off + gwi * MC_TILE;
-  const int64_t *bb = a.base + (size_t)blockIdx.x * rows;
+  const int64_t *bb = a.base + (size_t)blk * rows;
   const uint32_t *pre = a.wpre + gwi * rows;
   const int64_t run0 = lane < B ? bb[lane] + pre[lane] : 0;
   int64_t dest_b = lane < B ? a.seg_base[lane] + run0 : 0;  // next list slot of batch b
