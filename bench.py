@@ -95,6 +95,10 @@ def main():
     ap.add_argument("--no-loc-handoff", action="store_true",
                     help="packing builds every address-table entry itself, instead of "
                          "completing the ones sampling wrote for cached nodes (comparison)")
+    ap.add_argument("--two-calls", action="store_true",
+                    help="sample with dg_sample_group and pack with dg_pack_group, instead of "
+                         "one dg_sample_pack_group call whose last compaction pass also does "
+                         "packing's pass (comparison)")
     ap.add_argument("--sets", type=int, default=2,
                     help="packing output sets (and workspaces) used in turn: step k waits for "
                          "the assembly of step k - sets before it writes into its set")
@@ -122,6 +126,9 @@ def main():
     args = ap.parse_args()
     if args.steps < 1 or args.warmup < 0 or args.sets < 2:
         ap.error("--steps must be at least 1, --warmup at least 0 and --sets at least 2")
+    if not args.two_calls and (args.no_loc_handoff or args.no_member_lines):
+        ap.error("--no-loc-handoff and --no-member-lines compare options of the two-call path: "
+                 "add --two-calls")
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on exactly one GPU: the hot path is measured on one GPU's "
@@ -227,8 +234,10 @@ def main():
     # still be queued on the assembly stream when the next call starts; step k
     # waits only for the assembly of step k - sets
     n_sets = args.sets
+    fused = not args.two_calls
     pr2 = [pack_out() for _ in range(n_sets)]
-    ws_p2 = [torch.empty(dg._L.dg_pack_workspace_bytes(cfg.n, B, max_total), dtype=torch.uint8,
+    ws_p2 = [torch.empty(dg._L.dg_sample_pack_workspace_bytes(cfg.n, B, node_cap) if fused else
+                         dg._L.dg_pack_workspace_bytes(cfg.n, B, max_total), dtype=torch.uint8,
                          device=dev) for _ in range(n_sets)]
     ybuf = [torch.empty((nmax, R), dtype=torch.uint8, device=dev) for _ in range(2)]
     log(f"{n_groups} groups: pairs {min(p['total_nodes'] for p in pre):,}.."
@@ -340,25 +349,40 @@ def main():
             entry_clear = clearing and state["clear"]
             state["clear"] = False
             handoff = not args.no_loc_handoff
-            s_out = dg.sample_group(w.offsets, w.indices, groups[g], fan, w.rng_seed,
-                                    batch_base=g * B, out=sr, workspace=ws_s, membership=mem,
-                                    direct=True, stream=stream, exit_clear=clearing,
-                                    entry_clear=entry_clear, member_lines=lines,
-                                    timing=args.sample_timing,
-                                    cache_slot=w.cache_slot if handoff else None,
-                                    loc=pr2[slot].loc if handoff else None)
-            counts = s_out.node_count.copy()
-            if args.sample_timing:
-                samp_phases[pipelined].append(dict(s_out.timing))
-            t1 = time.perf_counter()
             rows_async = pipelined and not args.rows_inline and not args.timed_pack
-            p_out = dg.pack_group(w.feats, w.cache_slot, s_out.nodes, counts, out=pr2[slot],
-                                  workspace=ws_p2[slot], timing=record or args.timed_pack,
-                                  membership=mem, clear_membership=clearing,
-                                  stream=stream, rows_stream=s_asm if rows_async else None,
-                                  member_lines=lines, loc_pending=handoff)
+            if fused:
+                # one call; a timed call runs its row copy inside it
+                timed_call = record or args.timed_pack or args.sample_timing
+                s_out, p_out = dg.sample_pack_group(
+                    w.offsets, w.indices, groups[g], fan, w.rng_seed, w.feats, w.cache_slot,
+                    batch_base=g * B, out=sr, pack_out=pr2[slot], workspace=ws_s,
+                    pack_workspace=ws_p2[slot], membership=mem, direct=True, stream=stream,
+                    exit_clear=clearing, entry_clear=entry_clear, timing=timed_call,
+                    rows_stream=s_asm if (rows_async and not timed_call) else None)
+                counts = s_out.node_count.copy()
+                if args.sample_timing:
+                    samp_phases[pipelined].append(dict(s_out.timing))
+                t1 = t2 = time.perf_counter()
+            else:
+                s_out = dg.sample_group(w.offsets, w.indices, groups[g], fan, w.rng_seed,
+                                        batch_base=g * B, out=sr, workspace=ws_s,
+                                        membership=mem, direct=True, stream=stream,
+                                        exit_clear=clearing, entry_clear=entry_clear,
+                                        member_lines=lines, timing=args.sample_timing,
+                                        cache_slot=w.cache_slot if handoff else None,
+                                        loc=pr2[slot].loc if handoff else None)
+                counts = s_out.node_count.copy()
+                if args.sample_timing:
+                    samp_phases[pipelined].append(dict(s_out.timing))
+                t1 = time.perf_counter()
+                p_out = dg.pack_group(w.feats, w.cache_slot, s_out.nodes, counts,
+                                      out=pr2[slot], workspace=ws_p2[slot],
+                                      timing=record or args.timed_pack, membership=mem,
+                                      clear_membership=clearing, stream=stream,
+                                      rows_stream=s_asm if rows_async else None,
+                                      member_lines=lines, loc_pending=handoff)
+                t2 = time.perf_counter()
             state["clear"] = clearing
-            t2 = time.perf_counter()
             e0, e1 = ev_pool[k % nev]
             pack_done[slot].record(stream)
             if threaded:
@@ -484,14 +508,22 @@ def main():
                            + ("issued by the main thread" if asm_thread is None else
                               "issued by a host thread of its own in the pipelined region "
                               "(the trainer side), by the main thread in the serial region")),
+        "sample_pack": ("one dg_sample_pack_group call per step: the last hop's compaction "
+                        "pass also does packing's pass over the membership words, and the "
+                        "address tables of non-cached entries follow from one kernel"
+                        if fused else "dg_sample_group, then dg_pack_group"),
         "pack_rows": ("pipelined region: packing's row copy queued on the assembly stream "
                       "(DG_PACK_ROWS_STREAM)" if not (args.rows_inline or args.timed_pack
                                                       or args.no_pipeline)
                       else "inside the packing call"),
-        "address_tables": ("sampling writes the cached nodes' entries as it lists them; "
+        "address_tables": ("sampling writes the cached nodes' entries as it lists them, the "
+                           "others come from the fused pass's packed rows" if fused else
+                           "sampling writes the cached nodes' entries as it lists them; "
                            "packing completes the others (DG_PACK_LOC_PENDING)"
                            if not args.no_loc_handoff else "built by packing alone"),
-        "member_lines": ("packing reads only the membership lines sampling marked"
+        "member_lines": ("not needed: packing's pass is the last hop's sweep of every word"
+                         if fused else
+                         "packing reads only the membership lines sampling marked"
                          if lines is not None else "packing reads every membership word"),
         "mask_clearing": ("clearing flags: packing clears the membership words it reads and "
                           "sampling leaves its state clear, so no full-mask fill runs per step"
@@ -503,21 +535,29 @@ def main():
                            "ms_per_step": round(1e3 * t_rep / args.steps, 3),
                            "value": round(args.steps * sum(feature_bytes(sizes_rep)) / t_rep
                                           / 1e9, 2)},
-        "pipelined_phases_ms": {"sample": round(1e3 * float(np.mean([m[0] for m in marks_p])), 3),
-                                "pack": round(1e3 * float(np.mean([m[1] for m in marks_p])), 3),
+        "pipelined_phases_ms": {**({"sample_and_pack_call": round(1e3 * float(np.mean(
+                                        [m[0] for m in marks_p])), 3)} if fused else
+                                     {"sample": round(1e3 * float(np.mean(
+                                         [m[0] for m in marks_p])), 3),
+                                      "pack": round(1e3 * float(np.mean(
+                                          [m[1] for m in marks_p])), 3)}),
                                 "host_enqueue_assembly": round(1e3 * float(np.mean(
                                     enq_p or [m[2] for m in marks_p])), 3),
                                 "host_enqueue_assembly_on": ("the assembly thread"
                                                              if asm_thread is not None
                                                              else "the main thread")},
         "sampled_edges_per_s": round(edges / (np.sum(samp_ms) * 1e-3), 1),
-        "phases_ms": {"sample": round(float(np.mean(samp_ms)), 3),
-                      "pack": round(float(np.mean(pack_ms)), 3),
+        "sampled_edges_per_s_over": ("the whole sample-and-pack call (serial region)" if fused
+                                     else "the sampling call (serial region)"),
+        "phases_ms": {**({"sample_and_pack_call": round(float(np.mean(samp_ms)), 3)} if fused
+                         else {"sample": round(float(np.mean(samp_ms)), 3),
+                               "pack": round(float(np.mean(pack_ms)), 3)}),
                       "fanout_gather": round(g_ms, 3),
                       "assemble_all_batches": round(float(np.mean(asm_ms)), 3),
                       "host_enqueue_assembly": round(
                           1e3 * float(np.mean([m[2] for m in marks])), 3)},
-        "phase_gbps": {"pack_call": round(F_pack_s / (np.sum(pack_ms) * 1e-3) / 1e9, 1),
+        "phase_gbps": {**({} if fused else
+                          {"pack_call": round(F_pack_s / (np.sum(pack_ms) * 1e-3) / 1e9, 1)}),
                        "assemble_calls": round(F_asm_s / (np.sum(asm_ms) * 1e-3) / 1e9, 1)},
         "sizes": {k: span(k, steps_p) for k in
                   ("total_nodes", "total_edges", "packed_rows", "unique_nodes",

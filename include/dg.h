@@ -375,6 +375,60 @@ int dg_pack_group(const void *feats, int64_t N, int64_t row_bytes,
                   uint32_t flags, void *ws, size_t ws_bytes, hipStream_t stream,
                   hipStream_t rows_stream, dg_sizes *sizes, dg_timing *timing);
 
+/* Bytes of the packing workspace dg_sample_pack_group needs for N nodes, B
+ * batches and per-batch capacity node_cap (room for B*node_cap list entries).
+ * Returns 0 for B outside 1..64, N < 1 or node_cap < 1. */
+size_t dg_sample_pack_workspace_bytes(int64_t num_nodes, int32_t B, int64_t node_cap);
+
+/* Group sampling and batched packing in one call (§3 offline sampling, §5.2
+ * batched packing, §6 address tables).  The outputs are those of
+ *   dg_sample_group(g, ..., flags, node_cap, nodes, hop_ptr, edge_cap, edge_src,
+ *                   edge_dst, edge_ptr, membership, NULL, cache_slot, loc, ws, ...)
+ * followed by
+ *   dg_pack_group(feats, N, row_bytes, cache_slot, B, nodes, node_cap, n_b,
+ *                 packed_cap, packed, packed_ids, packed_ptr, packed_ptr_host, loc,
+ *                 group_unique, unique_cap, membership, <member lines>, NULL, 0,
+ *                 NULL, DG_PACK_CLEAR_MEMBERSHIP | DG_PACK_LOC_PENDING | pack_flags,
+ *                 ...)
+ * with n_b = hop_ptr[b*(K+2)+K+1]: the same nodes, edges, address tables, U,
+ * P_b, packed_ptr and packed rows, and `membership` (or the workspace's copy)
+ * left all-zero on DG_OK.
+ * With DG_SAMPLE_DIRECT and a last hop that samples, the two do not run one
+ * after the other: the last hop's compaction, which reads every membership
+ * word once the group is complete, also produces packing's sets (U, U_nc,
+ * each P_b, every pair's packed row) from that same read, and the address
+ * tables of non-cached entries follow from one read of the direct table per
+ * older pair.  Otherwise (hash relabelling, a last hop with fan-out 0 or an
+ * empty frontier, K = 0) packing's own passes run after sampling.
+ *   Arguments as for dg_sample_group and dg_pack_group; cache_slot, loc and
+ *   feats are required, and loc is laid out as nodes (node_stride = node_cap).
+ *   pack_flags  0 or DG_PACK_ROWS_STREAM (rows_stream as for dg_pack_group: the
+ *               row copy is queued there and not waited for; until it has run,
+ *               pack_ws must not be reused and feats and packed must not be
+ *               written).
+ *   ws, ws_bytes        sampling's workspace (dg_sample_workspace_bytes).
+ *   pack_ws, pack_ws_bytes  packing's (dg_sample_pack_workspace_bytes), 256-aligned.
+ *   sizes       [host] every field (sampling's and packing's).
+ *   timing      optional: sampling's phases, then loc_ms (address tables after
+ *               the fused pass) and gather_ms; mark_ms and order_ms are 0 when
+ *               the passes were fused (their work is inside dedup_ms).
+ * Errors: those of the two calls; DG_EWORKSPACE for a missing, small or
+ * misaligned pack_ws.  After a non-OK return the membership words and the
+ * workspaces are in an unspecified state (start again without
+ * DG_SAMPLE_ENTRY_CLEAR). */
+int dg_sample_pack_group(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S,
+                         int64_t batch_base, const int32_t *fanouts, int32_t K,
+                         uint64_t rng_seed, uint32_t flags, int64_t node_cap, int32_t *nodes,
+                         int64_t *hop_ptr, int64_t edge_cap, int32_t *edge_src,
+                         int32_t *edge_dst, int64_t *edge_ptr, uint64_t *membership,
+                         const int32_t *cache_slot, int32_t *loc, const void *feats,
+                         int64_t row_bytes, int64_t packed_cap, void *packed,
+                         int32_t *packed_ids, int64_t *packed_ptr, int64_t *packed_ptr_host,
+                         int32_t *group_unique, int64_t unique_cap, uint32_t pack_flags,
+                         void *ws, size_t ws_bytes, void *pack_ws, size_t pack_ws_bytes,
+                         hipStream_t stream, hipStream_t rows_stream, dg_sizes *sizes,
+                         dg_timing *timing);
+
 /* Bytes of the fixed scratch of dg_pack_group_noalloc (256 MiB). */
 size_t dg_pack_noalloc_scratch_bytes(void);
 

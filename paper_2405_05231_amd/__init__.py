@@ -324,6 +324,117 @@ def pack_group(feats: torch.Tensor, cache_slot: torch.Tensor, nodes: torch.Tenso
     return out
 
 
+def sample_pack_group(offsets: torch.Tensor, indices: torch.Tensor, seeds: torch.Tensor,
+                      fanouts, rng_seed: int, feats: torch.Tensor, cache_slot: torch.Tensor,
+                      batch_base: int = 0, node_cap: int | None = None,
+                      edge_cap: int | None = None, out: SampleResult | None = None,
+                      pack_out: PackResult | None = None, with_unique: bool = False,
+                      tables_only: bool = False, workspace: torch.Tensor | None = None,
+                      pack_workspace: torch.Tensor | None = None, stream=None,
+                      rows_stream=None, timing: bool = False,
+                      membership: torch.Tensor | None = None, layered: bool = False,
+                      direct: bool = True, entry_clear: bool = False,
+                      exit_clear: bool = False) -> tuple[SampleResult, PackResult]:
+    """Group sampling and batched packing in one call (dg_sample_pack_group):
+    the results of sample_group(..., cache_slot=cache_slot, loc=...) followed by
+    pack_group(..., membership, clear_membership=True, loc_pending=True), with
+    the membership words consumed (all-zero afterwards).  With direct=True the
+    last hop's compaction also does packing's pass.  pack_out: buffers for the
+    packing outputs (loc [B, node_cap], packed_ids, packed, packed_ptr,
+    unique); without it the call first runs once with no packed capacity to
+    learn the sizes (so the group is sampled twice).  rows_stream: leave the
+    row copy queued there (DG_PACK_ROWS_STREAM; keep pack_workspace, feats and
+    the packed buffer untouched until it has run)."""
+    dev = offsets.device
+    _need(offsets, "offsets", torch.int64)
+    _need(indices, "indices", torch.int32, dev)
+    _need(seeds, "seeds", torch.int32, dev)
+    _need(feats, "feats", None, dev)
+    _need(cache_slot, "cache_slot", torch.int32, dev)
+    if seeds.dim() != 2:
+        raise ValueError("seeds must be [B, S]")
+    N = offsets.numel() - 1
+    E = indices.numel()
+    if feats.shape[0] != N or cache_slot.numel() != N:
+        raise ValueError("feats and cache_slot must hold one row / entry per node")
+    if membership is not None:
+        _need(membership, "membership", torch.int64, dev)
+        if membership.numel() != N:
+            raise ValueError("membership must hold one word per node")
+    B, S = seeds.shape
+    R = _row_bytes(feats)
+    fanouts = [int(f) for f in fanouts]
+    K = len(fanouts)
+    if out is not None:
+        node_cap, edge_cap = out.nodes.shape[1], out.edge_src.shape[1]
+    else:
+        bn, be = sample_bounds(N, E, S, fanouts, layered)
+        node_cap = bn if node_cap is None else node_cap
+        edge_cap = be if edge_cap is None else edge_cap
+        out = SampleResult(
+            nodes=torch.empty((B, node_cap), dtype=torch.int32, device=dev),
+            hop_ptr=np.zeros((B, K + 2), dtype=np.int64),
+            edge_src=torch.empty((B, max(edge_cap, 1)), dtype=torch.int32, device=dev),
+            edge_dst=torch.empty((B, max(edge_cap, 1)), dtype=torch.int32, device=dev),
+            edge_ptr=np.zeros((B, K + 1), dtype=np.int64), sizes={}, timing=None)
+    flags = sample_flags(layered, direct, entry_clear, exit_clear)
+    ws = _workspace(_L.dg_sample_workspace_bytes(N, B, node_cap, edge_cap, flags), dev,
+                    workspace)
+    pws = _workspace(_L.dg_sample_pack_workspace_bytes(N, B, node_cap), dev, pack_workspace)
+    g = Csr(N, E, offsets.data_ptr(), indices.data_ptr())
+    fo = (ctypes.c_int32 * max(K, 1))(*fanouts)
+
+    def call(po, cap, flags_, sz, tm):
+        return _L.dg_sample_pack_group(
+            ctypes.byref(g), _ptr(seeds), B, S, batch_base, fo, K, rng_seed & (2**64 - 1),
+            flags_, node_cap, _ptr(out.nodes), out.hop_ptr.ctypes.data_as(_lib.I64P), edge_cap,
+            _ptr(out.edge_src), _ptr(out.edge_dst), out.edge_ptr.ctypes.data_as(_lib.I64P),
+            _ptr(membership), _ptr(cache_slot), _ptr(po.loc), _ptr(feats), R, cap,
+            _ptr(po.packed) if cap > 0 else None, _ptr(po.packed_ids) if cap > 0 else None,
+            _ptr(po.packed_ptr), po.packed_ptr_host.ctypes.data_as(_lib.I64P),
+            _ptr(po.unique), po.unique.numel() if po.unique is not None else 0,
+            _lib.DG_PACK_ROWS_STREAM if (rows_stream is not None and cap > 0) else 0,
+            _ptr(ws), ws.numel(), _ptr(pws), pws.numel(), _stream(stream),
+            _stream(rows_stream) if rows_stream is not None else None, ctypes.byref(sz),
+            ctypes.byref(tm) if tm is not None else None)
+
+    sz, tm = Sizes(), Timing()
+    if pack_out is None:
+        loc = torch.empty((B, node_cap), dtype=torch.int32, device=dev)
+        ptr = torch.empty(B + 1, dtype=torch.int64, device=dev)
+        probe = PackResult(packed=None, packed_ids=None, packed_ptr=ptr,
+                           packed_ptr_host=np.zeros(B + 1, dtype=np.int64), loc=loc,
+                           unique=None, sizes={}, timing=None, row_bytes=R)
+        # size query: no packed capacity; the membership words are left in an
+        # unspecified state, so the real call clears them on entry
+        st = call(probe, 0, flags & ~_lib.DG_SAMPLE_ENTRY_CLEAR, sz, None)
+        if st not in (DG_OK, DG_ECAPACITY):
+            check(st)
+        if st == DG_ECAPACITY and sz.packed_rows <= 0 and sz.unique_nodes <= 0:
+            check(st)  # sampling itself ran out of room
+        rows, nu = max(sz.packed_rows, 0), max(sz.unique_nodes, 0)
+        pack_out = PackResult(
+            packed=None if tables_only else torch.empty((max(rows, 1), R), dtype=torch.uint8,
+                                                        device=dev),
+            packed_ids=torch.empty(max(rows, 1), dtype=torch.int32, device=dev),
+            packed_ptr=ptr, packed_ptr_host=probe.packed_ptr_host, loc=loc,
+            unique=torch.empty(max(nu, 1), dtype=torch.int32, device=dev) if with_unique else None,
+            sizes={}, timing=None, row_bytes=R)
+        flags &= ~_lib.DG_SAMPLE_ENTRY_CLEAR
+        sz = Sizes()
+    if tuple(pack_out.loc.shape) != (B, node_cap):
+        raise ValueError("pack_out.loc must be [B, node_cap], laid out as the node lists")
+    cap = pack_out.packed_ids.numel()
+    if pack_out.packed is not None and pack_out.packed.numel() < cap * R:
+        raise ValueError("packed buffer smaller than packed_ids")
+    st = call(pack_out, cap, flags, sz, tm if timing else None)
+    out.sizes = sz.as_dict()
+    pack_out.sizes = sz.as_dict()
+    check(st)
+    out.timing = pack_out.timing = tm.as_dict() if timing else None
+    return out, pack_out
+
+
 def assemble_batch(cache: torch.Tensor | None, packed_b: torch.Tensor, loc_b: torch.Tensor,
                    row_bytes: int, out: torch.Tensor | None = None,
                    status: torch.Tensor | None = None, stream=None) -> torch.Tensor:

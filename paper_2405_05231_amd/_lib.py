@@ -69,6 +69,12 @@ SIGNATURES = {
     "dg_pack_group": (ctypes.c_int, [VP, I64, I64, VP, I32, VP, I64, I64P, I64, VP, VP, VP, I64P,
                                      VP, VP, I64, VP, VP, VP, I64, VP, U32, VP, SZ, VP, VP,
                                      ctypes.POINTER(Sizes), ctypes.POINTER(Timing)]),
+    "dg_sample_pack_workspace_bytes": (SZ, [I64, I32, I64]),
+    "dg_sample_pack_group": (ctypes.c_int, [ctypes.POINTER(Csr), VP, I32, I32, I64, I32P, I32,
+                                            U64, ctypes.c_uint32, I64, VP, I64P, I64, VP, VP,
+                                            I64P, VP, VP, VP, VP, I64, I64, VP, VP, VP, I64P,
+                                            VP, I64, U32, VP, SZ, VP, SZ, VP, VP,
+                                            ctypes.POINTER(Sizes), ctypes.POINTER(Timing)]),
     "dg_pack_noalloc_scratch_bytes": (SZ, []),
     "dg_pack_group_noalloc": (ctypes.c_int, [VP, I64, I64, VP, I32, VP, I64, I64P, I64, VP, VP,
                                              VP, I64P, VP, VP, I64, VP, VP, VP, I64, VP, U32,

@@ -294,6 +294,116 @@ int mask_scan_count(MaskScan &m, hipStream_t s);
 int mask_scan_write(const MaskScan &m, hipStream_t s);
 // Member lines of the whole mask (mc_touch_bytes(N) bytes), by a pass of its own.
 int member_lines_pass(const uint64_t *mask, int64_t N, int B, uint8_t *out, hipStream_t s);
+// The row scans of a count matrix filled by a count pass (part of mask_scan_count).
+int mask_scan_rows(MaskScan &m, hipStream_t s);
+
+// ---------------------------------------------------------------- fused compaction
+// The last sampling hop's count and write passes doing batched packing's pass
+// over the membership words as well (dg_sample_pack_group).  The mask then
+// holds every (node, batch) pair of the group and prev the pairs listed before
+// the last hop, so one sweep gives both the hop's new pairs (m & ~prev) and
+// packing's sets.  The compact list holds every non-empty word: m, its new
+// bits and its offset (bit 15 = cached).  Two count matrices come out of the
+// count pass, each scanned by the row scans of a MaskScan view of its own:
+//   s: rows [0, B) = new pairs per batch (the other four rows as in sampling);
+//   p: packing's rows ([0, B) non-cached pairs per batch, U, U_nc, non-cached
+//      pairs, all pairs).
+// The count pass zeroes every mask word it reads, and the prev words too with
+// clear_prev.  The write pass writes sampling's lists and the address-table
+// entries of new cached pairs, and packing's U, U_nc, pair offsets, P_b and
+// pair destinations; for every packed pair it also records the list slot of
+// the pair when it is new at this hop (pslot, -1 for an older pair) for the
+// address tables that follow.  Every index is checked against its buffer:
+// counts beyond a capacity are found by the host after the read-back.
+struct FuseScan {
+  uint64_t *mask;
+  uint64_t *prev;
+  const int32_t *cache_slot;
+  int64_t N;
+  int B;
+  int64_t nblk;
+  bool clear_prev;
+  uint32_t *err;
+  // compact list (the sampling view's arrays, and the packing view's cw_mask
+  // for the new bits)
+  uint32_t *wcnt;
+  uint64_t *cw_mask;
+  uint64_t *cw_new;
+  uint16_t *cw_off;
+  uint32_t *cnt_s, *wpre_s, *cnt_p, *wpre_p;
+  const int64_t *base_s, *base_p;
+  // write pass, sampling: the hop's segments of the node lists
+  int64_t node_cap;
+  int64_t seg_base[DG_MAX_BATCHES];  // b*node_cap + n_b before the hop
+  int64_t seg_end[DG_MAX_BATCHES];   // (b+1)*node_cap
+  int32_t *seg_out;
+  int32_t *loc_out;    // [B*node_cap] address tables (cached entries written here)
+  int32_t *local_out;  // nullable: [N][B] local indices of the hop's pairs
+  // write pass, packing
+  const int64_t *packed_ptr;  // device [B+1], from the p view's totals
+  int64_t packed_cap;         // entries of packed_ids and pslot
+  int32_t *packed_ids;
+  int32_t *pslot;
+  int32_t *uniq_out;  // nullable
+  int64_t unique_cap;
+  int32_t *unc_ids;
+  int64_t *unc_off;
+  int64_t unc_cap;
+  int64_t *nodeoff;
+  int64_t *pairdest;
+  int64_t pair_cap;
+};
+// Count pass + the row scans of both views (asynchronous).
+int fuse_scan_count(const FuseScan &f, MaskScan &vs, MaskScan &vp, hipStream_t s);
+// Write pass (after the count pass): first packed_ptr (= f.packed_ptr, B+1
+// entries) from the p view's per-batch totals, then the pass itself.
+int fuse_scan_write(const FuseScan &f, const int64_t *totals_p, int64_t *packed_ptr,
+                    hipStream_t s);
+
+// ---------------------------------------------------------------- packing state
+// Workspace of batched packing (also carved by dg_sample_pack_group).
+struct PackWs {
+  uint32_t *err;
+  uint64_t *mask;
+  int64_t *nodeoff;
+  int32_t *unc_ids;
+  int64_t *unc_off;
+  int64_t *pairdest;
+  MaskScan ms;
+};
+void carve_pack(PackWs &w, Carve &c, int64_t N, int B, int64_t total_nodes);
+size_t pack_ws_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes);
+// dg_pack_group's body (no_alloc: dg_pack_group_noalloc's rules).
+int pack_impl(const void *feats, int64_t N, int64_t row_bytes, const int32_t *cache_slot,
+              int32_t B, const int32_t *nodes, int64_t node_stride, const int64_t *node_count,
+              int64_t packed_cap, void *packed, int32_t *packed_ids, int64_t *packed_ptr,
+              int64_t *packed_ptr_host, int32_t *loc, int32_t *group_unique, int64_t unique_cap,
+              uint64_t *membership, const uint8_t *member_lines, const int32_t *cache_nodes,
+              int64_t cache_rows, void *cache_table, uint32_t flags, void *ws,
+              size_t ws_bytes, hipStream_t stream, hipStream_t rows_stream, dg_sizes *sizes,
+              dg_timing *timing, bool no_alloc);
+// What follows a fused compaction: the address-table entries of the packed
+// pairs, loc[b*node_cap + j] = r for packed row packed_ptr[b] + r, with j =
+// pslot of the row for a pair new at the last hop, else local[u*B + b]; then
+// the row copy (on rows_stream, not waited for, when rows_async).
+struct PhaseTimer;
+struct FusedTail {
+  const void *feats;
+  int64_t N, row_bytes;
+  int B;
+  int64_t node_cap;
+  const int64_t *n_b;              // [host] list lengths
+  const int64_t *packed_ptr_host;  // [host] B+1
+  const int32_t *packed_ids, *pslot, *local;
+  int32_t *loc;
+  void *packed;  // nullable: no row copy
+  const int32_t *unc_ids;
+  const int64_t *unc_off, *pairdest;
+  int64_t n_unc, rows;
+  uint32_t *err;
+};
+int pack_fused_tail(const FusedTail &t, bool rows_async, hipStream_t s, hipStream_t rows_stream,
+                    PhaseTimer *tm, int *ev_loc, int *ev_gather);
 
 // ---------------------------------------------------------------- timing
 // Events are taken from a pool per host thread and device, created on first

@@ -294,15 +294,7 @@ int launch_fanout(const RowCopy &r, hipStream_t s) {
   return DG_OK;
 }
 
-struct PackWs {
-  uint32_t *err;
-  uint64_t *mask;
-  int64_t *nodeoff;
-  int32_t *unc_ids;
-  int64_t *unc_off;
-  int64_t *pairdest;
-  MaskScan ms;
-};
+}  // namespace
 
 void carve_pack(PackWs &w, Carve &c, int64_t N, int B, int64_t total_nodes) {
   int64_t ucap = total_nodes < N ? total_nodes : N;
@@ -318,6 +310,8 @@ void carve_pack(PackWs &w, Carve &c, int64_t N, int B, int64_t total_nodes) {
   mask_scan_carve(w.ms, c);
 }
 
+namespace {
+
 // Device-to-host read of a call's counts: through the library's page-locked
 // buffer, or (no_alloc) straight into the host variable.
 int read_back(void *dst, const void *src, size_t bytes, hipStream_t s, bool no_alloc) {
@@ -331,6 +325,8 @@ int read_err(uint32_t *err, hipStream_t s, bool no_alloc) {
   return DG_OK;
 }
 
+}  // namespace
+
 size_t pack_ws_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes) {
   if (num_nodes < 1 || B < 1 || B > DG_MAX_BATCHES || total_nodes < 0) return 0;
   Carve c(nullptr);
@@ -338,6 +334,8 @@ size_t pack_ws_bytes(int64_t num_nodes, int32_t B, int64_t total_nodes) {
   carve_pack(w, c, num_nodes, B, total_nodes);
   return c.used;
 }
+
+namespace {
 
 // ---------------------------------------------------------------- fixed scratch
 // Scratch of dg_pack_group_noalloc: a file-scope device array (one copy per GPU,
@@ -365,6 +363,8 @@ int scratch_address(void **out) {
   *out = addr[dev];
   return DG_OK;
 }
+
+}  // namespace
 
 int pack_impl(const void *feats, int64_t N, int64_t row_bytes, const int32_t *cache_slot,
               int32_t B, const int32_t *nodes, int64_t node_stride, const int64_t *node_count,
@@ -540,7 +540,70 @@ int pack_impl(const void *feats, int64_t N, int64_t row_bytes, const int32_t *ca
   return DG_OK;
 }
 
+namespace {
+
+struct LocFill {
+  int B;
+  int64_t node_cap;
+  int64_t start[DG_MAX_BATCHES + 1];  // packed_ptr
+  int64_t n[DG_MAX_BATCHES];          // list lengths
+};
+
+// Address-table entries of the packed pairs after a fused compaction: packed
+// row i of chunk b (node u = packed_ids[i]) is entry j of nodes_b, with j =
+// pslot[i] for a pair new at the last hop, else u's local index in the direct
+// table; loc_b[j] = i - packed_ptr[b], u's rank in P_b.  Every non-cached list
+// entry is reached once this way (its pair is in P_b).
+__global__ __launch_bounds__(THREADS) void k_loc_packed(LocFill F, const int32_t *packed_ids,
+                                                        const int32_t *pslot,
+                                                        const int32_t *local, int32_t *loc,
+                                                        uint32_t *err) {
+  const int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
+  if (i >= F.start[F.B]) return;
+  const int b = find_batch_wave(F.start, F.B, i);
+  int32_t j = pslot[i];
+  if (j < 0) j = local[(int64_t)packed_ids[i] * F.B + b];
+  if (j < 0 || (int64_t)j >= F.n[b]) {
+    atomicOr(err, ERR_INTERNAL);
+    return;
+  }
+  loc[(int64_t)b * F.node_cap + j] = (int32_t)(i - F.start[b]);
+}
+
 }  // namespace
+
+int pack_fused_tail(const FusedTail &t, bool rows_async, hipStream_t s, hipStream_t rows_stream,
+                    PhaseTimer *tm, int *ev_loc, int *ev_gather) {
+  // The row copy depends only on the write pass's U_nc lists: on a second
+  // stream it starts at once, beside the address tables.
+  const RowCopy rc_rows{t.feats,   t.N,       t.row_bytes, t.unc_ids, t.unc_off,
+                        t.n_unc,   t.rows,    t.pairdest,  t.packed,  nullptr,
+                        0,         nullptr,   t.err};
+  const bool copy = t.packed && t.n_unc > 0;
+  int rc;
+  if (copy && rows_async) {
+    SideStream *ss = nullptr;
+    DG_TRY(side_stream(&ss));
+    DG_HIP(hipEventRecord(ss->handoff, s));
+    DG_HIP(hipStreamWaitEvent(rows_stream, ss->handoff, 0));
+    if ((rc = launch_fanout(rc_rows, rows_stream))) return rc;
+  }
+  if (t.rows > 0) {
+    LocFill F;
+    F.B = t.B;
+    F.node_cap = t.node_cap;
+    for (int b = 0; b <= t.B; ++b) F.start[b] = t.packed_ptr_host[b];
+    for (int b = 0; b < t.B; ++b) F.n[b] = t.n_b[b];
+    hipLaunchKernelGGL(k_loc_packed, dim3(blocks_for(t.rows)), dim3(THREADS), 0, s, F,
+                       t.packed_ids, t.pslot, t.local, t.loc, t.err);
+    DG_HIP(hipGetLastError());
+  }
+  *ev_loc = tm ? tm->mark() : -1;
+  if (copy && !rows_async && (rc = launch_fanout(rc_rows, s))) return rc;
+  *ev_gather = tm ? tm->mark() : -1;
+  return DG_OK;
+}
+
 }  // namespace dg
 
 using namespace dg;

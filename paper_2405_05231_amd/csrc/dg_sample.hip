@@ -465,7 +465,8 @@ __global__ __launch_bounds__(RL_THREADS) void k_relabel_last(LastHop h, const in
 constexpr int ST_BOUNDS = 0;                              // [B+1]
 constexpr int ST_TOTALS = ST_BOUNDS + DG_MAX_BATCHES + 1; // [B+4]
 constexpr int ST_ERR = ST_TOTALS + DG_MAX_BATCHES + 4;
-constexpr int ST_SIZE = ST_ERR + 1;
+constexpr int ST_PTOTALS = ST_ERR + 1;                      // [B+4] packing's, fused pass
+constexpr int ST_SIZE = ST_PTOTALS + DG_MAX_BATCHES + 4;
 
 // eoff at each batch's first frontier entry (and at the end).
 __global__ void k_batch_bounds(Hop h, const int64_t *f_eoff, int64_t *out) {
@@ -568,15 +569,56 @@ extern "C" size_t dg_sample_workspace_bytes(int64_t num_nodes, int32_t B, int64_
   return c.used;
 }
 
-extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S,
-                               int64_t batch_base, const int32_t *fanouts, int32_t K,
-                               uint64_t rng_seed, uint32_t flags, int64_t node_cap,
-                               int32_t *nodes,
-                               int64_t *hop_ptr, int64_t edge_cap, int32_t *edge_src,
-                               int32_t *edge_dst, int64_t *edge_ptr, uint64_t *membership,
-                               uint8_t *member_lines, const int32_t *cache_slot, int32_t *loc,
-                               void *ws, size_t ws_bytes, hipStream_t stream, dg_sizes *sizes,
-                               dg_timing *timing) {
+namespace dg {
+namespace {
+
+// Event indices of a sampling call's phases (read once the call's work is done).
+struct SampleMarks {
+  int start = -1, r0 = -1, r1 = -1, nhop = 0;
+  int hop[8][3];
+};
+
+// Packing state of dg_sample_pack_group, carved from its packing workspace:
+// what the fused last hop writes besides sampling's outputs, and what it
+// reports back.
+struct PackInto {
+  PackWs pw;          // packing's workspace (last in the carve, see carve_sample_pack)
+  size_t pw_offset;   // its offset in the packing workspace
+  int32_t *pslot;     // [pslot_cap] list slot of each packed pair new at the last hop
+  int64_t pslot_cap;
+  uint8_t *lines;     // member lines, for a group packed by packing's own passes
+  int64_t unc_cap, pair_cap;
+  int64_t *packed_ptr;
+  int64_t packed_cap;
+  int32_t *packed_ids;
+  int32_t *group_unique;
+  int64_t unique_cap;
+  // set by sample_impl
+  bool fused = false;                 // the last hop's compaction did packing's pass
+  int64_t ptot[DG_MAX_BATCHES + 4];  // packing's row totals (fused)
+  uint32_t *err = nullptr;            // sampling's device error word, not yet checked
+  uint64_t *visited = nullptr;        // the membership words sampling used
+  int32_t *local = nullptr;           // the direct table (DG_SAMPLE_DIRECT)
+};
+
+void carve_sample_pack(PackInto &pk, Carve &c, int64_t N, int B, int64_t node_cap) {
+  const int64_t total = (int64_t)B * node_cap;
+  pk.pslot = c.take<int32_t>((size_t)total);
+  pk.pslot_cap = total;
+  pk.lines = c.take<uint8_t>((size_t)mc_touch_bytes(N));
+  pk.pw_offset = c.used;  // packing's own workspace last: the unfused path hands it on whole
+  carve_pack(pk.pw, c, N, B, total);
+  pk.unc_cap = (total < N ? total : N) + 1;
+  pk.pair_cap = total + 1;
+}
+
+int sample_impl(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S, int64_t batch_base,
+                const int32_t *fanouts, int32_t K, uint64_t rng_seed, uint32_t flags,
+                int64_t node_cap, int32_t *nodes, int64_t *hop_ptr, int64_t edge_cap,
+                int32_t *edge_src, int32_t *edge_dst, int64_t *edge_ptr, uint64_t *membership,
+                uint8_t *member_lines, const int32_t *cache_slot, int32_t *loc, void *ws,
+                size_t ws_bytes, hipStream_t stream, dg_sizes *sizes, PhaseTimer &tm,
+                SampleMarks &mk, PackInto *pk) {
   if (!g || !seeds || !nodes || !hop_ptr || !edge_src || !edge_dst || !edge_ptr || !sizes ||
       (K > 0 && !fanouts))
     return set_error(DG_EINVAL, "dg_sample_group: null pointer argument");
@@ -614,12 +656,8 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
   memset(sizes, 0, sizeof(*sizes));
   sizes->packed_rows = sizes->unique_nodes = sizes->unique_packed = -1;
   sizes->exact = 1;
-  if (timing) memset(timing, 0, sizeof(*timing));
-  PhaseTimer tm(timing != nullptr, s);
-  float t_sample = 0.f, t_dedup = 0.f;
-  int hop_ev[8][3];
-  int nhop_ev = 0;
-  const int ev_start = tm.mark();
+  mk.nhop = 0;
+  mk.start = tm.mark();
 
   int rc;
   if ((rc = fill_u64(reinterpret_cast<uint64_t *>(w.err), 32, 0, s))) return rc;
@@ -681,7 +719,10 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       // does both on the way, where marks would need a pass over the whole mask
       // for the map and a fill of prev afterwards.
       const int64_t ebound = f < 0 ? E : h.ftot * (int64_t)f;
-      const bool full_last = k == K && (member_lines || exit_clear);
+      // With a packing state (and the direct table, which gives older pairs'
+      // list slots) the last hop's compaction also does packing's pass.
+      const bool fuse = pk && direct && k == K;
+      const bool full_last = k == K && (member_lines || exit_clear || fuse);
       h.touched = (ebound <= N / 16 && !full_last) ? w.touched : nullptr;
       if (h.touched && (rc = fill_u64(reinterpret_cast<uint64_t *>(w.touched),
                                       (size_t)mc_touch_bytes(N) / 8, 0, s)))
@@ -737,7 +778,37 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       w.ms.cache_slot = nullptr;
       w.ms.totals = w.small + ST_TOTALS;
       w.ms.err_stage = w.small + ST_ERR;
-      if ((rc = mask_scan_count(w.ms, s))) return rc;
+      FuseScan F;
+      if (fuse) {
+        MaskScan &vp = pk->pw.ms;
+        vp.totals = w.small + ST_PTOTALS;
+        vp.err_stage = nullptr;
+        vp.err = w.err;
+        memset(&F, 0, sizeof(F));
+        F.mask = w.visited;
+        F.prev = w.prev;
+        F.cache_slot = cache_slot;
+        F.N = N;
+        F.B = B;
+        F.nblk = w.ms.nblk;
+        F.clear_prev = w.ms.clear_prev;
+        F.err = w.err;
+        F.wcnt = w.ms.wcnt;
+        F.cw_mask = w.ms.cw_mask;
+        F.cw_new = vp.cw_mask;
+        F.cw_off = w.ms.cw_off;
+        F.cnt_s = w.ms.cnt;
+        F.wpre_s = w.ms.wpre;
+        F.cnt_p = vp.cnt;
+        F.wpre_p = vp.wpre;
+        F.base_s = w.ms.base;
+        F.base_p = vp.base;
+        w.ms.lines_out = nullptr;
+        lines_done = false;
+        if ((rc = fuse_scan_count(F, w.ms, vp, s))) return rc;
+      } else if ((rc = mask_scan_count(w.ms, s))) {
+        return rc;
+      }
       for (int b = 0; b < B; ++b) {
         w.ms.seg_base[b] = (int64_t)b * node_cap + n_b[b];
         w.ms.seg_end[b] = (int64_t)(b + 1) * node_cap;
@@ -769,11 +840,36 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
       w.ms.unc_off = nullptr;
       w.ms.nodeoff = nullptr;
       w.ms.pairdest = nullptr;
-      if ((rc = mask_scan_write(w.ms, s))) return rc;
+      if (fuse) {
+        F.node_cap = node_cap;
+        for (int b = 0; b < B; ++b) {
+          F.seg_base[b] = w.ms.seg_base[b];
+          F.seg_end[b] = w.ms.seg_end[b];
+        }
+        F.seg_out = nodes;
+        F.loc_out = loc;
+        F.local_out = w.ms.local_out;
+        F.packed_ptr = pk->packed_ptr;
+        F.packed_cap = pk->packed_cap < pk->pslot_cap ? pk->packed_cap : pk->pslot_cap;
+        F.packed_ids = pk->packed_ids;
+        F.pslot = pk->pslot;
+        F.uniq_out = pk->group_unique;
+        F.unique_cap = pk->unique_cap;
+        F.unc_ids = pk->pw.unc_ids;
+        F.unc_off = pk->pw.unc_off;
+        F.unc_cap = pk->unc_cap;
+        F.nodeoff = pk->pw.nodeoff;
+        F.pairdest = pk->pw.pairdest;
+        F.pair_cap = pk->pair_cap;
+        if ((rc = fuse_scan_write(F, w.small + ST_PTOTALS, pk->packed_ptr, s))) return rc;
+      } else if ((rc = mask_scan_write(w.ms, s))) {
+        return rc;
+      }
       const int ev2 = tm.mark();
       // one round trip per hop: edge bounds, node counts and the error word
+      // (and packing's totals after a fused pass)
       int64_t st[ST_SIZE];
-      DG_TRY(read_to_host(st, w.small, sizeof(st), s));
+      DG_TRY(read_to_host(st, w.small, sizeof(int64_t) * (fuse ? ST_SIZE : ST_PTOTALS), s));
       if (st[ST_ERR])
         return set_error(DG_EINVAL, "invalid input data: %s",
                          describe_device_error((uint32_t)st[ST_ERR]));
@@ -801,11 +897,15 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
         return set_error(DG_ECAPACITY, "dg_sample_group: node_cap %lld too small at hop %d",
                          (long long)node_cap, k);
       }
-      if (nhop_ev < 8) {
-        hop_ev[nhop_ev][0] = ev0;
-        hop_ev[nhop_ev][1] = ev1;
-        hop_ev[nhop_ev][2] = ev2;
-        ++nhop_ev;
+      if (fuse) {
+        pk->fused = true;
+        for (int r = 0; r < mc_rows(B); ++r) pk->ptot[r] = st[ST_PTOTALS + r];
+      }
+      if (mk.nhop < 8) {
+        mk.hop[mk.nhop][0] = ev0;
+        mk.hop[mk.nhop][1] = ev1;
+        mk.hop[mk.nhop][2] = ev2;
+        ++mk.nhop;
       }
     }
     for (int b = 0; b < B; ++b) {
@@ -819,7 +919,7 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
   for (int b = 0; b < B; ++b) edge_ptr[(int64_t)b * (K + 1) + K] = e_b[b];
 
   // Local IDs through the (node, batch) table.
-  const int ev_r0 = tm.mark();
+  mk.r0 = tm.mark();
   Lists LE;
   LE.B = B;
   LE.start[0] = 0;
@@ -901,11 +1001,18 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
                        edge_cap, edge_dst, table, N, w.err);
     DG_HIP(hipGetLastError());
   }
-  const int ev_r1 = tm.mark();
+  mk.r1 = tm.mark();
   if (exit_clear && !prev_cleared && (rc = fill_u64(w.prev, (size_t)N, 0, s))) return rc;
-  if (member_lines && !lines_done && (rc = member_lines_pass(w.visited, N, B, member_lines, s)))
+  if (member_lines && !lines_done && !(pk && pk->fused) &&
+      (rc = member_lines_pass(w.visited, N, B, member_lines, s)))
     return rc;
-  if ((rc = check_err(w.err, s))) return rc;
+  if (pk) {  // the caller checks the error word after its own work
+    pk->err = w.err;
+    pk->visited = w.visited;
+    pk->local = w.local;
+  } else if ((rc = check_err(w.err, s))) {
+    return rc;
+  }
 
   int64_t tn = 0, te = 0, mn = 0, me = 0;
   for (int b = 0; b < B; ++b) {
@@ -918,15 +1025,175 @@ extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B,
   sizes->max_batch_edges = me;
   sizes->total_nodes = tn;
   sizes->total_edges = te;
-  if (timing) {
-    for (int i = 0; i < nhop_ev && i < 8; ++i) {
-      t_sample += tm.ms(hop_ev[i][0], hop_ev[i][1]);
-      t_dedup += tm.ms(hop_ev[i][1], hop_ev[i][2]);
+  return DG_OK;
+}
+
+// Sampling's phase times from the marks of a finished call.
+void sample_times(const PhaseTimer &tm, const SampleMarks &mk, dg_timing *timing) {
+  float t_sample = 0.f, t_dedup = 0.f;
+  for (int i = 0; i < mk.nhop && i < 8; ++i) {
+    t_sample += tm.ms(mk.hop[i][0], mk.hop[i][1]);
+    t_dedup += tm.ms(mk.hop[i][1], mk.hop[i][2]);
+  }
+  timing->sample_ms = t_sample;
+  timing->dedup_ms = t_dedup;
+  timing->relabel_ms = tm.ms(mk.r0, mk.r1);
+  timing->total_ms = tm.ms(mk.start, mk.r1);
+}
+
+}  // namespace
+}  // namespace dg
+
+extern "C" int dg_sample_group(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S,
+                               int64_t batch_base, const int32_t *fanouts, int32_t K,
+                               uint64_t rng_seed, uint32_t flags, int64_t node_cap,
+                               int32_t *nodes,
+                               int64_t *hop_ptr, int64_t edge_cap, int32_t *edge_src,
+                               int32_t *edge_dst, int64_t *edge_ptr, uint64_t *membership,
+                               uint8_t *member_lines, const int32_t *cache_slot, int32_t *loc,
+                               void *ws, size_t ws_bytes, hipStream_t stream, dg_sizes *sizes,
+                               dg_timing *timing) {
+  if (timing) memset(timing, 0, sizeof(*timing));
+  PhaseTimer tm(timing != nullptr, stream);
+  SampleMarks mk;
+  const int rc = sample_impl(g, seeds, B, S, batch_base, fanouts, K, rng_seed, flags, node_cap,
+                             nodes, hop_ptr, edge_cap, edge_src, edge_dst, edge_ptr, membership,
+                             member_lines, cache_slot, loc, ws, ws_bytes, stream, sizes, tm, mk,
+                             nullptr);
+  if (rc == DG_OK && timing) sample_times(tm, mk, timing);
+  return rc;
+}
+
+extern "C" size_t dg_sample_pack_workspace_bytes(int64_t num_nodes, int32_t B,
+                                                 int64_t node_cap) {
+  if (num_nodes < 1 || B < 1 || B > DG_MAX_BATCHES || node_cap < 1 ||
+      node_cap > INT64_MAX / DG_MAX_BATCHES)
+    return 0;
+  Carve c(nullptr);
+  PackInto pk;
+  carve_sample_pack(pk, c, num_nodes, B, node_cap);
+  return c.used;
+}
+
+extern "C" int dg_sample_pack_group(
+    const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S, int64_t batch_base,
+    const int32_t *fanouts, int32_t K, uint64_t rng_seed, uint32_t flags, int64_t node_cap,
+    int32_t *nodes, int64_t *hop_ptr, int64_t edge_cap, int32_t *edge_src, int32_t *edge_dst,
+    int64_t *edge_ptr, uint64_t *membership, const int32_t *cache_slot, int32_t *loc,
+    const void *feats, int64_t row_bytes, int64_t packed_cap, void *packed, int32_t *packed_ids,
+    int64_t *packed_ptr, int64_t *packed_ptr_host, int32_t *group_unique, int64_t unique_cap,
+    uint32_t pack_flags, void *ws, size_t ws_bytes, void *pack_ws, size_t pack_ws_bytes,
+    hipStream_t stream, hipStream_t rows_stream, dg_sizes *sizes, dg_timing *timing) {
+  if (!g || !cache_slot || !loc || !feats || !packed_ptr || !packed_ptr_host || !sizes ||
+      !hop_ptr)
+    return set_error(DG_EINVAL, "dg_sample_pack_group: null pointer argument");
+  if (row_bytes < 1 || packed_cap < 0 || unique_cap < 0 || (packed_cap > 0 && !packed_ids))
+    return set_error(DG_EINVAL, "dg_sample_pack_group: bad packing sizes");
+  if (pack_flags & ~DG_PACK_ROWS_STREAM)
+    return set_error(DG_EINVAL, "dg_sample_pack_group: unknown pack flags 0x%x", pack_flags);
+  if ((pack_flags & DG_PACK_ROWS_STREAM) && timing)
+    return set_error(DG_EINVAL, "dg_sample_pack_group: timing cannot be combined with "
+                                "DG_PACK_ROWS_STREAM");
+  const size_t need = dg_sample_pack_workspace_bytes(g->num_nodes, B, node_cap);
+  if (need == 0 || K < 0)
+    return set_error(DG_EINVAL, "dg_sample_pack_group: bad sizes (B=%d K=%d node_cap=%lld)", B,
+                     K, (long long)node_cap);
+  if (!pack_ws || pack_ws_bytes < need || ((uintptr_t)pack_ws & 255))
+    return set_error(DG_EWORKSPACE,
+                     "dg_sample_pack_group: packing workspace needs %zu bytes, 256-aligned",
+                     need);
+  const bool rows_async = (pack_flags & DG_PACK_ROWS_STREAM) && packed;
+  const int64_t N = g->num_nodes;
+  PackInto pk;
+  Carve c(pack_ws);
+  carve_sample_pack(pk, c, N, B, node_cap);
+  pk.packed_ptr = packed_ptr;
+  pk.packed_cap = packed_cap;
+  pk.packed_ids = packed_ids;
+  pk.group_unique = group_unique;
+  pk.unique_cap = group_unique ? unique_cap : 0;
+  if (timing) memset(timing, 0, sizeof(*timing));
+  PhaseTimer tm(timing != nullptr, stream);
+  SampleMarks mk;
+  int rc = sample_impl(g, seeds, B, S, batch_base, fanouts, K, rng_seed, flags, node_cap, nodes,
+                       hop_ptr, edge_cap, edge_src, edge_dst, edge_ptr, membership, pk.lines,
+                       cache_slot, loc, ws, ws_bytes, stream, sizes, tm, mk, &pk);
+  if (rc) return rc;
+  int64_t n_b[DG_MAX_BATCHES];
+  for (int b = 0; b < B; ++b) n_b[b] = hop_ptr[(int64_t)b * (K + 2) + K + 1];
+
+  if (!pk.fused) {
+    // No fused pass (hash relabelling, or a last hop with nothing to sample):
+    // packing's own passes over the lists sampling wrote.
+    if ((rc = check_err(pk.err, stream))) return rc;
+    if (timing) sample_times(tm, mk, timing);
+    dg_sizes ps;
+    dg_timing pt;
+    rc = pack_impl(feats, N, row_bytes, cache_slot, B, nodes, node_cap, n_b, packed_cap, packed,
+                   packed_ids, packed_ptr, packed_ptr_host, loc, group_unique, unique_cap,
+                   membership ? membership : pk.visited, pk.lines, nullptr, 0, nullptr,
+                   DG_PACK_CLEAR_MEMBERSHIP | DG_PACK_LOC_PENDING |
+                       (pack_flags & DG_PACK_ROWS_STREAM),
+                   static_cast<char *>(pack_ws) + pk.pw_offset, pack_ws_bytes - pk.pw_offset,
+                   stream, rows_stream, &ps, timing ? &pt : nullptr, false);
+    sizes->packed_rows = ps.packed_rows;
+    sizes->unique_nodes = ps.unique_nodes;
+    sizes->unique_packed = ps.unique_packed;
+    if (rc) return rc;
+    if (timing) {
+      timing->mark_ms = pt.mark_ms;
+      timing->order_ms = pt.order_ms;
+      timing->loc_ms = pt.loc_ms;
+      timing->gather_ms = pt.gather_ms;
+      timing->total_ms += pt.total_ms;
     }
-    timing->sample_ms = t_sample;
-    timing->dedup_ms = t_dedup;
-    timing->relabel_ms = tm.ms(ev_r0, ev_r1);
-    timing->total_ms = tm.ms(ev_start, ev_r1);
+    return DG_OK;
+  }
+
+  // Packing's sizes came back with the last hop's counts.
+  int64_t rows = 0;
+  packed_ptr_host[0] = 0;
+  for (int b = 0; b < B; ++b) {
+    rows += pk.ptot[b];
+    packed_ptr_host[b + 1] = rows;
+  }
+  sizes->packed_rows = rows;
+  sizes->unique_nodes = pk.ptot[row_all(B)];
+  sizes->unique_packed = pk.ptot[row_packed(B)];
+  if (rows != pk.ptot[row_pairs(B)] || pk.ptot[row_all_pairs(B)] != sizes->total_nodes)
+    return set_error(DG_EINVAL, "dg_sample_pack_group: internal pair count mismatch");
+  if (rows > packed_cap || (group_unique && sizes->unique_nodes > unique_cap))
+    return set_error(DG_ECAPACITY,
+                     "dg_sample_pack_group: need packed_cap >= %lld and unique_cap >= %lld",
+                     (long long)rows, (long long)sizes->unique_nodes);
+  FusedTail t;
+  t.feats = feats;
+  t.N = N;
+  t.row_bytes = row_bytes;
+  t.B = B;
+  t.node_cap = node_cap;
+  t.n_b = n_b;
+  t.packed_ptr_host = packed_ptr_host;
+  t.packed_ids = packed_ids;
+  t.pslot = pk.pslot;
+  t.local = pk.local;
+  t.loc = loc;
+  t.packed = packed;
+  t.unc_ids = pk.pw.unc_ids;
+  t.unc_off = pk.pw.unc_off;
+  t.pairdest = pk.pw.pairdest;
+  t.n_unc = sizes->unique_packed;
+  t.rows = rows;
+  t.err = pk.err;
+  int ev_loc = -1, ev_gather = -1;
+  if ((rc = pack_fused_tail(t, rows_async, stream, rows_stream, &tm, &ev_loc, &ev_gather)))
+    return rc;
+  if ((rc = check_err(pk.err, stream))) return rc;
+  if (timing) {
+    sample_times(tm, mk, timing);
+    timing->loc_ms = tm.ms(mk.r1, ev_loc);
+    timing->gather_ms = tm.ms(ev_loc, ev_gather);
+    timing->total_ms = tm.ms(mk.start, ev_gather);
   }
   return DG_OK;
 }

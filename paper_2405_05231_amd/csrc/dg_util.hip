@@ -539,11 +539,17 @@ int mask_scan_count(MaskScan &m, hipStream_t s) {
   if ((m.prev && (m.cache_slot || m.clear_mask)) || (m.keep_prev && m.clear_prev) ||
       (!m.prev && (m.keep_prev || m.clear_prev || m.lines_out)) || (m.lines_out && m.touched))
     return set_error(DG_EINVAL, "internal: inconsistent count-pass mode");
-  const unsigned nch = (unsigned)mc_chunks(m.nblk);
   if (m.prev)
     hipLaunchKernelGGL(k_mask_count<true>, dim3((unsigned)m.nblk), dim3(MC_THREADS), 0, s, m);
   else
     hipLaunchKernelGGL(k_mask_count<false>, dim3((unsigned)m.nblk), dim3(MC_THREADS), 0, s, m);
+  DG_HIP(hipGetLastError());
+  return mask_scan_rows(m, s);
+}
+
+int mask_scan_rows(MaskScan &m, hipStream_t s) {
+  if (m.nblk == 0) return fill_u64(reinterpret_cast<uint64_t *>(m.totals), mc_rows(m.B), 0, s);
+  const unsigned nch = (unsigned)mc_chunks(m.nblk);
   hipLaunchKernelGGL(k_rows_chunk_sum, dim3(nch), dim3(RS_THREADS), 0, s, m);
   hipLaunchKernelGGL(k_rows_chunk_scan, dim3((unsigned)mc_rows(m.B)), dim3(1024), 0, s, m);
   hipLaunchKernelGGL(k_rows_apply, dim3(nch), dim3(RS_THREADS), 0, s, m);
@@ -656,6 +662,314 @@ int mask_scan_write(const MaskScan &m, hipStream_t s) {
     hipLaunchKernelGGL((k_mask_write<false, true>), g, bl, 0, s, m);
   else
     hipLaunchKernelGGL((k_mask_write<false, false>), g, bl, 0, s, m);
+  DG_HIP(hipGetLastError());
+  return DG_OK;
+}
+
+// ---------------------------------------------------------------- fused compaction
+// Adds bit `lane & 31` of the low (lanes < 32) or high (lanes >= 32) halves of
+// the k words staged in lo/hi to `mine` (batch `lane`'s count), four words
+// per 128-bit LDS read.  The staging areas hold MC_CWORDS entries.
+__device__ __forceinline__ void lds_count(uint32_t k, uint32_t *lo, uint32_t *hi, int lane,
+                                          uint32_t &mine) {
+  if (k == 0) return;  // uniform
+  if (lane < 4) {      // zeros after the last word: the final 128-bit read may pass it
+    lo[k + lane] = 0u;
+    hi[k + lane] = 0u;
+  }
+  // LDS operations of one wave complete in order, so these reads see the
+  // stores above and later stores follow them.
+  __builtin_amdgcn_wave_barrier();
+  const uint4 *src = reinterpret_cast<const uint4 *>(lane < 32 ? lo : hi);
+  const uint32_t sh = (uint32_t)lane & 31u;
+  for (uint32_t i = 0; i < k; i += 4) {
+    const uint4 v = src[i >> 2];
+    mine += __builtin_amdgcn_ubfe(v.x, sh, 1) + __builtin_amdgcn_ubfe(v.y, sh, 1);
+    mine += __builtin_amdgcn_ubfe(v.z, sh, 1) + __builtin_amdgcn_ubfe(v.w, sh, 1);
+  }
+  __builtin_amdgcn_wave_barrier();
+}
+
+// Fused count pass (FuseScan).  Every word is read (no touched marks).  The
+// tile is taken in two halves of eight rounds, so that a half's mask words,
+// prev words and cache slots are in registers together; within a half all
+// loads of a kind are requested before any is used.  Per-batch counts, a
+// chunk of MC_CROUNDS rounds at a time: the chunk's words with new bits are
+// staged in one LDS area and its non-cached words in another, and lane b
+// counts bit b of each.
+constexpr int FC_HALF = MC_ROUNDS / 4;
+
+__global__ __launch_bounds__(MC_THREADS) __attribute__((amdgpu_waves_per_eu(8, 8)))
+void k_fuse_count(FuseScan a) {
+  __shared__ uint32_t s_cs[MC_WAVES][DG_MAX_BATCHES + 4];
+  __shared__ uint32_t s_cp[MC_WAVES][DG_MAX_BATCHES + 4];
+  __shared__ __align__(16) uint32_t s_w[MC_WAVES][4][MC_CWORDS];
+  const int lane = lane_id();
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int B = a.B, rows = mc_rows(B);
+  const int64_t t0 = (int64_t)blockIdx.x * MC_BLOCK_NODES + (int64_t)w * MC_TILE;
+  const int64_t rem = a.N - t0;  // nodes of the tile inside [0, N) (may exceed MC_TILE)
+  const uint64_t keep = B < 64 ? (1ull << B) - 1ull : ~0ull;
+  const size_t gw = ((size_t)blockIdx.x * MC_WAVES + w) * MC_TILE;
+  uint32_t *ns_lo = s_w[w][0], *ns_hi = s_w[w][1];  // words with new bits
+  uint32_t *np_lo = s_w[w][2], *np_hi = s_w[w][3];  // words of non-cached nodes
+  uint64_t *mk = a.mask + t0;
+  uint64_t *pv = a.prev + t0;
+  const int32_t *cs = a.cache_slot + t0;
+  uint32_t run = 0, cu = 0, cnc = 0, cnew = 0;  // uniform: listed, U, U_nc, new words
+  uint32_t al = 0, pl = 0, nl = 0;  // this lane's word: all, non-cached, new pairs
+  uint32_t mine_s = 0, mine_p = 0;  // batch `lane`: new pairs, non-cached pairs
+  uint64_t bad = 0;
+#pragma unroll
+  for (int h0 = 0; h0 < MC_ROUNDS; h0 += FC_HALF) {
+    uint64_t m[FC_HALF];
+    if (rem >= MC_TILE) {
+#pragma unroll
+      for (int q = 0; q < FC_HALF; ++q) m[q] = mk[(h0 + q) * 64 + lane];
+    } else {
+#pragma unroll
+      for (int q = 0; q < FC_HALF; ++q)
+        m[q] = (h0 + q) * 64 + lane < rem ? mk[(h0 + q) * 64 + lane] : 0ull;
+    }
+    wait_vm_all();
+    uint64_t any[FC_HALF];  // lanes of round q with a word (uniform)
+    uint64_t nw[FC_HALF];
+    int32_t sl[FC_HALF];
+#pragma unroll
+    for (int q = 0; q < FC_HALF; ++q) {
+      const bool has = (m[q] & keep) != 0ull;
+      any[q] = __ballot(has);
+      nw[q] = has ? pv[(h0 + q) * 64 + lane] : 0ull;
+      sl[q] = has ? cs[(h0 + q) * 64 + lane] : -1;
+    }
+    wait_vm_all();
+    uint64_t cmask[FC_HALF];  // cached lanes of round q (uniform); the slots die here
+#pragma unroll
+    for (int q = 0; q < FC_HALF; ++q) {
+      cmask[q] = 0ull;
+      if (!any[q]) continue;
+      bad |= __ballot(sl[q] < -1);
+      cmask[q] = __ballot(sl[q] >= 0);
+    }
+#pragma unroll
+    for (int c = 0; c < FC_HALF; c += MC_CROUNDS) {
+      uint32_t ks = 0, kp = 0;  // staged new / non-cached words of the chunk (uniform)
+#pragma unroll
+      for (int q = c; q < c + MC_CROUNDS; ++q) {
+        const int r = h0 + q;
+        if (m[q] != 0ull) mk[r * 64 + lane] = 0ull;  // packing consumes the word
+        const uint64_t p = nw[q];
+        if (a.clear_prev && p != 0ull) pv[r * 64 + lane] = 0ull;
+        const uint64_t mq = m[q] & keep;
+        const uint64_t nq = mq & ~p;
+        const uint64_t an = any[q];
+        if (!an) continue;
+        const uint64_t cmq = cmask[q];
+        const uint64_t anw = __ballot(nq != 0ull);  // lanes with new bits (uniform)
+        const uint64_t anc = an & ~cmq;
+        if (mq != 0ull) {
+          const bool cached = (cmq >> lane) & 1ull;
+          const size_t at = gw + rank_below(an, run);
+          a.cw_mask[at] = mq;
+          a.cw_new[at] = nq;
+          a.cw_off[at] = (uint16_t)((r * 64 + lane) | ((int)cached << 15));
+          const uint32_t pc = (uint32_t)__popcll(mq);
+          al += pc;
+          if (nq != 0ull) {
+            nl += (uint32_t)__popcll(nq);
+            const uint32_t j = rank_below(anw, ks);
+            ns_lo[j] = (uint32_t)nq;
+            ns_hi[j] = (uint32_t)(nq >> 32);
+          }
+          if (!cached) {
+            pl += pc;
+            const uint32_t j = rank_below(anc, kp);
+            np_lo[j] = (uint32_t)mq;
+            np_hi[j] = (uint32_t)(mq >> 32);
+          }
+        }
+        run += (uint32_t)__popcll(an);
+        cu += (uint32_t)__popcll(an);
+        cnc += (uint32_t)__popcll(anc);
+        cnew += (uint32_t)__popcll(anw);
+        ks += (uint32_t)__popcll(anw);
+        kp += (uint32_t)__popcll(anc);
+      }
+      lds_count(ks, ns_lo, ns_hi, lane, mine_s);
+      lds_count(kp, np_lo, np_hi, lane, mine_p);
+    }
+  }
+  if (bad && lane == 0) atomicOr(a.err, ERR_CACHE_SLOT);
+  const size_t gwi = (size_t)blockIdx.x * MC_WAVES + w;
+  if (lane == 0) a.wcnt[gwi] = run;
+  const uint32_t sum_all = (uint32_t)__ockl_wfred_add_i32((int32_t)al);
+  const uint32_t sum_nc = (uint32_t)__ockl_wfred_add_i32((int32_t)pl);
+  const uint32_t sum_new = (uint32_t)__ockl_wfred_add_i32((int32_t)nl);
+  if (lane < B) {
+    s_cs[w][lane] = mine_s;
+    s_cp[w][lane] = mine_p;
+  }
+  if (lane == 0) {
+    s_cs[w][row_all(B)] = cnew;
+    s_cs[w][row_packed(B)] = cnew;
+    s_cs[w][row_pairs(B)] = sum_new;
+    s_cs[w][row_all_pairs(B)] = sum_new;
+    s_cp[w][row_all(B)] = cu;
+    s_cp[w][row_packed(B)] = cnc;
+    s_cp[w][row_pairs(B)] = sum_nc;
+    s_cp[w][row_all_pairs(B)] = sum_all;
+  }
+  __syncthreads();
+  uint32_t *pre_s = a.wpre_s + (size_t)blockIdx.x * MC_WAVES * rows;
+  uint32_t *pre_p = a.wpre_p + (size_t)blockIdx.x * MC_WAVES * rows;
+  for (int i = threadIdx.x; i < 2 * rows; i += MC_THREADS) {
+    const bool sv = i < rows;
+    const int row = sv ? i : i - rows;
+    uint32_t *pre = sv ? pre_s : pre_p;
+    uint32_t v = 0;
+#pragma unroll
+    for (int j = 0; j < MC_WAVES; ++j) {
+      pre[j * rows + row] = v;
+      v += sv ? s_cs[j][row] : s_cp[j][row];
+    }
+    (sv ? a.cnt_s : a.cnt_p)[(size_t)blockIdx.x * rows + row] = v;
+  }
+}
+
+// packed_ptr from the p view's per-batch totals.
+__global__ void k_fuse_ptr(const int64_t *totals, int B, int64_t *packed_ptr) {
+  if (threadIdx.x == 0) {
+    int64_t run = 0;
+    packed_ptr[0] = 0;
+    for (int b = 0; b < B; ++b) {
+      run += totals[b];
+      packed_ptr[b + 1] = run;
+    }
+  }
+}
+
+// Fused write pass (FuseScan), over the compact list.  Per-node outputs
+// (U, U_nc, pair offsets) by ballot prefixes within a chunk of 64 words, as in
+// packing's write pass; then the words with new or non-cached bits one by one,
+// lane b taking bit b: a new pair goes to batch b's segment (with its
+// address-table entry when the node is cached, and its local index when
+// local_out is given), a non-cached pair to P_b with its destination and list
+// slot.  Blocks run in XCD-contiguous order, as in the other write pass.
+__global__ __launch_bounds__(MC_THREADS) void k_fuse_write(FuseScan a) {
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+  const int B = a.B, rows = mc_rows(B);
+  const uint32_t blk = xcd_block(blockIdx.x, gridDim.x);
+  const int64_t t0 = (int64_t)blk * MC_BLOCK_NODES + (int64_t)w * MC_TILE;
+  const size_t gwi = (size_t)blk * MC_WAVES + w;
+  const uint32_t n = a.wcnt[gwi];
+  if (n == 0) return;  // wave-uniform
+  const uint64_t *cm = a.cw_mask + gwi * MC_TILE;
+  const uint64_t *cn = a.cw_new + gwi * MC_TILE;
+  const uint16_t *co = a.cw_off + gwi * MC_TILE;
+  const int64_t *bs = a.base_s + (size_t)blk * rows;
+  const int64_t *bp = a.base_p + (size_t)blk * rows;
+  const uint32_t *ps = a.wpre_s + gwi * rows;
+  const uint32_t *pp = a.wpre_p + gwi * rows;
+  int64_t dest_b = 0, end_b = 0, pd_b = 0, lbase = 0;  // batch `lane`
+  if (lane < B) {
+    dest_b = a.seg_base[lane] + bs[lane] + ps[lane];  // next slot of its segment
+    end_b = a.seg_end[lane];
+    pd_b = a.packed_ptr[lane] + bp[lane] + pp[lane];  // next row of its chunk
+    lbase = (int64_t)lane * a.node_cap;
+  }
+  int64_t run_u = bp[row_all(B)] + pp[row_all(B)];
+  int64_t run_nc = bp[row_packed(B)] + pp[row_packed(B)];
+  int64_t run_p = bp[row_pairs(B)] + pp[row_pairs(B)];
+  const uint64_t lt = lanes_below();
+  for (uint32_t c0 = 0; c0 < n; c0 += 64) {
+    const uint32_t i = c0 + lane;
+    uint64_t m = 0, nw = 0;
+    uint32_t off = 0;
+    if (i < n) {
+      m = cm[i];
+      nw = cn[i];
+      off = co[i];
+    }
+    const int32_t u = (int32_t)(t0 + (off & 1023u));
+    const bool cached = (off >> 15) & 1u;
+    int32_t sl = -1;  // a cached node's slot, for its new pairs' entries
+    if (cached && nw != 0ull) sl = a.cache_slot[u];
+    // Every load of the chunk has landed here: without this wait the compiler
+    // waits for sl inside the pair loop below, and so (one counter covers loads
+    // and stores) for each iteration's stores before the next.
+    wait_vm_all();
+    const uint64_t mnc = cached ? 0ull : m;
+    const uint64_t any = __ballot(m != 0ull);
+    if (m != 0ull && a.uniq_out) {
+      const int64_t at = run_u + __popcll(any & lt);
+      if (at < a.unique_cap) a.uniq_out[at] = u;
+    }
+    run_u += __popcll(any);
+    const uint64_t anc = __ballot(mnc != 0ull);
+    const int32_t pc = __popcll(mnc);
+    const int64_t pair0 = run_p + (wave_incl_sum_i32(pc) - pc);
+    if (mnc != 0ull) {
+      const int64_t rk = run_nc + __popcll(anc & lt);
+      if (rk < a.unc_cap) {
+        a.unc_ids[rk] = u;
+        a.unc_off[rk] = pair0;
+      }
+      a.nodeoff[u] = pair0;
+    }
+    run_nc += __popcll(anc);
+    uint64_t act = __ballot((nw | mnc) != 0ull);
+    while (act) {
+      const int l = __ffsll((long long)act) - 1;
+      act &= act - 1ull;
+      const uint64_t wn = (uint64_t)read_lane((int64_t)nw, l);
+      const uint64_t wp = (uint64_t)read_lane((int64_t)mnc, l);
+      const int32_t ul = __builtin_amdgcn_readlane(u, l);
+      const int32_t sll = __builtin_amdgcn_readlane(sl, l);
+      const bool is_new = (wn >> lane) & 1ull;
+      const int64_t slot = dest_b;
+      if (is_new) {
+        if (dest_b < end_b) {
+          a.seg_out[dest_b] = ul;
+          if (sll >= 0) a.loc_out[dest_b] = -(sll + 1);
+          if (a.local_out) a.local_out[(int64_t)ul * B + lane] = (int32_t)(dest_b - lbase);
+        }
+        ++dest_b;
+      }
+      if ((wp >> lane) & 1ull) {
+        if (pd_b < a.packed_cap) {
+          a.packed_ids[pd_b] = ul;
+          a.pslot[pd_b] = is_new ? (int32_t)(slot - lbase) : -1;
+        }
+        const int64_t q = run_p + __popcll(wp & lt);
+        if (q < a.pair_cap) a.pairdest[q] = pd_b;
+        ++pd_b;
+      }
+      run_p += __popcll(wp);
+    }
+  }
+}
+
+int fuse_scan_count(const FuseScan &f, MaskScan &vs, MaskScan &vp, hipStream_t s) {
+  if (!f.mask || !f.prev || !f.cache_slot || vs.nblk != f.nblk || vp.nblk != f.nblk ||
+      vs.B != f.B || vp.B != f.B)
+    return set_error(DG_EINVAL, "internal: inconsistent fused count pass");
+  if (f.nblk > 0) {
+    hipLaunchKernelGGL(k_fuse_count, dim3((unsigned)f.nblk), dim3(MC_THREADS), 0, s, f);
+    DG_HIP(hipGetLastError());
+  }
+  int rc;
+  if ((rc = mask_scan_rows(vs, s))) return rc;
+  return mask_scan_rows(vp, s);
+}
+
+int fuse_scan_write(const FuseScan &f, const int64_t *totals_p, int64_t *packed_ptr,
+                    hipStream_t s) {
+  if (!f.seg_out || !f.loc_out || !f.unc_ids || !f.unc_off || !f.nodeoff || !f.pairdest ||
+      (f.packed_cap > 0 && (!f.packed_ids || !f.pslot)) || f.packed_ptr != packed_ptr)
+    return set_error(DG_EINVAL, "internal: inconsistent fused write pass");
+  hipLaunchKernelGGL(k_fuse_ptr, dim3(1), dim3(64), 0, s, totals_p, f.B, packed_ptr);
+  if (f.nblk > 0)
+    hipLaunchKernelGGL(k_fuse_write, dim3((unsigned)f.nblk), dim3(MC_THREADS), 0, s, f);
   DG_HIP(hipGetLastError());
   return DG_OK;
 }

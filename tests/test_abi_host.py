@@ -81,6 +81,51 @@ def test_workspace_queries(L):
     p = L.dg_pack_workspace_bytes(10_000, 4, 8000)
     assert p > 8 * 10_000 and p % 256 == 0
     assert L.dg_pack_workspace_bytes(10_000, 0, 10) == 0
+    # the fused call's packing workspace: packing's for B*node_cap entries, plus
+    # a list slot per entry and a member-lines map
+    f = L.dg_sample_pack_workspace_bytes(10_000, 4, 2000)
+    assert f % 256 == 0
+    assert f >= p + 4 * 8000 + L.dg_member_lines_bytes(10_000)
+    assert L.dg_sample_pack_workspace_bytes(10_000, 65, 2000) == 0
+    assert L.dg_sample_pack_workspace_bytes(0, 4, 2000) == 0
+    assert L.dg_sample_pack_workspace_bytes(10_000, 4, 0) == 0
+
+
+def test_sample_pack_host_side_argument_errors(L):
+    from paper_2405_05231_amd import _lib
+    sizes = _lib.Sizes()
+    g = _lib.Csr(10, 0, 0x1000, 0)
+    hop = (ctypes.c_int64 * 4)()
+    ep = (ctypes.c_int64 * 3)()
+    ph = (ctypes.c_int64 * 2)()
+    fo = (ctypes.c_int32 * 1)(2)
+    fake = ctypes.c_void_p(0x1000)
+    pws = L.dg_sample_pack_workspace_bytes(10, 1, 4)
+
+    def call(cache_slot=fake, loc=fake, feats=fake, row_bytes=16, pack_flags=0, ws=fake,
+             ws_bytes=1 << 30, pack_ws=fake, pack_ws_bytes=pws, timing=None):
+        return L.dg_sample_pack_group(
+            ctypes.byref(g), fake, 1, 1, 0, fo, 1, 0, _lib.DG_SAMPLE_DIRECT, 4, fake, hop, 4,
+            fake, fake, ep, None, cache_slot, loc, feats, row_bytes, 0, None, None, fake, ph,
+            None, 0, pack_flags, ws, ws_bytes, pack_ws, pack_ws_bytes, None, None,
+            ctypes.byref(sizes), timing)
+
+    # packing needs the cache slots, the address tables and the features
+    for kw in ({"cache_slot": None}, {"loc": None}, {"feats": None}):
+        assert call(**kw) == _lib.DG_EINVAL and b"null" in L.dg_last_error()
+    assert call(row_bytes=0) == _lib.DG_EINVAL
+    assert call(pack_flags=_lib.DG_PACK_CLEAR_MEMBERSHIP) == _lib.DG_EINVAL
+    assert b"pack flags" in L.dg_last_error()
+    tm = _lib.Timing()
+    assert call(pack_flags=_lib.DG_PACK_ROWS_STREAM, timing=ctypes.byref(tm)) == _lib.DG_EINVAL
+    assert b"timing" in L.dg_last_error()
+    # packing's workspace: missing, small or misaligned
+    assert call(pack_ws=None) == _lib.DG_EWORKSPACE
+    assert call(pack_ws_bytes=pws - 256) == _lib.DG_EWORKSPACE
+    assert call(pack_ws=ctypes.c_void_p(0x1010)) == _lib.DG_EWORKSPACE
+    assert b"packing workspace" in L.dg_last_error()
+    # sampling's workspace is checked by sampling, before any device work
+    assert call(ws=None, ws_bytes=0) == _lib.DG_EWORKSPACE
 
 
 def test_host_side_argument_errors(L):

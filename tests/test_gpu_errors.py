@@ -254,3 +254,59 @@ def test_handoff_pending_entry_of_a_cached_node_rejected(dg, tiny):
     for b in range(tiny.cfg.B):
         n = int(sr.hop_ptr[b, -1])
         assert torch.equal(pr.loc[b, :n], ref.loc[b, :n]), b
+
+
+@pytest.mark.parametrize("direct", [False, True])
+def test_sample_pack_errors_and_capacity(dg, tiny, direct):
+    """dg_sample_pack_group: a bad cache slot is reported (in the fused pass and
+    in packing's own passes alike); too little packed or unique room gives
+    DG_ECAPACITY with the sizes needed, and writes nothing past the buffers; a
+    call with room afterwards (without DG_SAMPLE_ENTRY_CLEAR) equals the
+    separate calls."""
+    off, idx, seeds, ncap, ecap, loc = handoff_setup(dg, tiny)
+    X = tiny.feats.to(DEV)
+    slot = tiny.cache_slot.to(DEV)
+    bad = slot.clone()
+    bad[::3] = -9
+    with pytest.raises(dg.DGError) as e:
+        dg.sample_pack_group(off, idx, seeds, [5, 5], 1, X, bad, node_cap=ncap, edge_cap=ecap,
+                             direct=direct)
+    assert e.value.status == -1 and "cache_slot" in str(e.value)
+    sr = dg.sample_group(off, idx, seeds, [5, 5], 1, direct=direct, node_cap=ncap,
+                         edge_cap=ecap)
+    ref = dg.pack_group(X, slot, sr.nodes, sr.node_count, with_unique=True)
+    rows, nu = ref.sizes["packed_rows"], ref.sizes["unique_nodes"]
+    B, R = tiny.cfg.B, ref.row_bytes
+    mem = torch.empty(tiny.cfg.n, dtype=torch.int64, device=DEV)
+    # a guard element after each list output, which must stay untouched
+    ids = torch.full((rows + 1,), -11, dtype=torch.int32, device=DEV)
+    uq = torch.full((nu + 1,), -11, dtype=torch.int32, device=DEV)
+    packed = torch.full((rows + 1, R), 5, dtype=torch.uint8, device=DEV)
+
+    def out_set(n_rows, n_u):
+        return dg.PackResult(packed=packed[:n_rows], packed_ids=ids[:n_rows],
+                             packed_ptr=torch.empty(B + 1, dtype=torch.int64, device=DEV),
+                             packed_ptr_host=np.zeros(B + 1, dtype=np.int64), loc=loc,
+                             unique=uq[:n_u], sizes={}, timing=None, row_bytes=R)
+
+    for n_rows, n_u in ((rows - 1, nu), (rows, nu - 1)):
+        with pytest.raises(dg.DGError) as e:
+            dg.sample_pack_group(off, idx, seeds, [5, 5], 1, X, slot, node_cap=ncap,
+                                 edge_cap=ecap, pack_out=out_set(n_rows, n_u), membership=mem,
+                                 direct=direct, exit_clear=True)
+        assert e.value.status == -2
+        assert int(ids[rows]) == -11 and int(uq[nu]) == -11
+        assert int(packed[rows].to(torch.int64).sum()) == 5 * R
+    sr2, pr2 = dg.sample_pack_group(off, idx, seeds, [5, 5], 1, X, slot, node_cap=ncap,
+                                    edge_cap=ecap, pack_out=out_set(rows, nu), membership=mem,
+                                    direct=direct, exit_clear=True)
+    assert pr2.sizes["packed_rows"] == rows and pr2.sizes["unique_nodes"] == nu
+    assert torch.equal(pr2.packed_ids[:rows], ref.packed_ids[:rows])
+    assert torch.equal(pr2.unique[:nu], ref.unique[:nu])
+    assert torch.equal(pr2.packed[:rows], ref.packed[:rows])
+    for b in range(B):
+        n = int(sr.hop_ptr[b, -1])
+        assert torch.equal(sr2.nodes[b, :n], sr.nodes[b, :n]), b
+        assert torch.equal(pr2.loc[b, :n], ref.loc[b, :n]), b
+    assert int(ids[rows]) == -11 and int(uq[nu]) == -11
+    assert int(mem.count_nonzero()) == 0

@@ -43,7 +43,25 @@ def run_path(dg, off, idx, seeds, fanouts, rng_seed, feats, cache_slot, cache_no
     slot = cache_slot.to(DEV)
     cache = X.index_select(0, cache_nodes.to(DEV)) if cache_nodes.numel() else None
     R = X[0].numel() * X.element_size()
-    if not handoff:
+    if handoff == "fused":
+        # one dg_sample_pack_group call; garbage in every output beforehand
+        B = seeds.shape[0]
+        ncap, ecap = dg.sample_bounds(off.numel() - 1, idx.numel(), seeds.shape[1], fanouts,
+                                      kw.get("layered", False))
+        cap = B * ncap
+        out = dg.PackResult(packed=torch.full((cap, R), 7, dtype=torch.uint8, device=DEV),
+                            packed_ids=torch.full((cap,), -5, dtype=torch.int32, device=DEV),
+                            packed_ptr=torch.full((B + 1,), -5, dtype=torch.int64, device=DEV),
+                            packed_ptr_host=np.zeros(B + 1, dtype=np.int64),
+                            loc=torch.full((B, ncap), -3, dtype=torch.int32, device=DEV),
+                            unique=torch.full((cap,), -5, dtype=torch.int32, device=DEV),
+                            sizes={}, timing=None, row_bytes=R)
+        mem = torch.full((off.numel() - 1,), -1, dtype=torch.int64, device=DEV)
+        sr, pr = dg.sample_pack_group(off_d, idx_d, seeds_d, fanouts, rng_seed, X, slot,
+                                      batch_base=batch_base, node_cap=ncap, edge_cap=ecap,
+                                      pack_out=out, membership=mem, exit_clear=True, **kw)
+        assert int(torch.count_nonzero(mem)) == 0  # packing consumed the membership words
+    elif not handoff:
         sr = dg.sample_group(off_d, idx_d, seeds_d, fanouts, rng_seed, batch_base=batch_base,
                              **kw)
         pr = dg.pack_group(X, slot, sr.nodes, sr.node_count, with_unique=True)
@@ -153,6 +171,24 @@ def test_tiny_workload_T_direct_relabel(dg, orc, layered):
               w.cache_slot, w.cache_nodes, sample_kw={"layered": layered, "direct": True})
 
 
+@pytest.mark.parametrize("layered,direct", [(False, True), (True, True), (False, False)])
+def test_tiny_workload_T_sample_and_pack_in_one_call(dg, orc, layered, direct):
+    """dg_sample_pack_group: every output equals the oracle's, whether the
+    last hop's compaction does packing's pass (direct table) or packing's own
+    passes follow (hash relabelling)."""
+    w = synth.make_workload("T")
+    check_all(dg, orc, w.offsets, w.indices, w.seeds, list(w.cfg.fanouts), w.rng_seed, w.feats,
+              w.cache_slot, w.cache_nodes,
+              sample_kw={"layered": layered, "direct": direct, "handoff": "fused"})
+    # which of the two ran: packing's own count pass times its ordering phase
+    X, slot = w.feats.to(DEV), w.cache_slot.to(DEV)
+    _, pr = dg.sample_pack_group(w.offsets.to(DEV), w.indices.to(DEV), w.seeds.to(DEV),
+                                 list(w.cfg.fanouts), w.rng_seed, X, slot, timing=True,
+                                 layered=layered, direct=direct)
+    assert (pr.timing["order_ms"] == 0.0) == direct
+    assert pr.timing["gather_ms"] > 0.0 and pr.timing["total_ms"] > 0.0
+
+
 @pytest.mark.parametrize("direct", [False, True])
 def test_tiny_workload_T_address_tables_from_sampling(dg, orc, direct):
     """Sampling writes the cached nodes' address-table entries as it lists
@@ -217,12 +253,14 @@ CASES = [
     (600, 20, 4, 8, [6, 6], 768, torch.float16, 0.1),          # 1536-byte rows (2 vectors/lane, 2nd half used)
     (600, 20, 4, 8, [6, 6], 512, torch.float32, 0.1),          # 2048-byte rows (2 vectors/lane)
     (600, 20, 4, 8, [6, 6], 1024, torch.float32, 0.1),         # 4096-byte rows (4 vectors/lane)
+    (300, 20, 5, 6, [4, 0], 16, torch.float32, 0.2),           # f = 0 at the last hop
 ]
 
 
 @pytest.mark.parametrize("layered,direct,handoff", [
     (False, False, False), (True, False, False), (False, True, False), (True, True, False),
-    (False, True, True), (True, False, True)])
+    (False, True, True), (True, False, True), (False, True, "fused"), (True, True, "fused"),
+    (False, False, "fused")])
 @pytest.mark.parametrize("case", range(len(CASES)))
 def test_edge_cases(dg, orc, case, layered, direct, handoff):
     n, maxdeg, B, S, fan, dim, dtype, share = CASES[case]
@@ -326,7 +364,7 @@ def test_assemble_batches_matches_per_batch_calls(dg):
 
 
 @pytest.mark.parametrize("layered,direct,handoff", [(False, False, False), (True, True, False),
-                                                    (False, True, True)])
+                                                    (False, True, True), (False, True, "fused")])
 def test_sparse_hops_on_a_large_graph(dg, orc, layered, direct, handoff):
     """A small frontier on a large graph: every hop's edges reach only a small
     share of the nodes, so the sampler lists new nodes from the 8-node mask
@@ -460,7 +498,7 @@ def test_last_hop_segments_of_a_few_hundred_thousand_nodes(dg, orc, last_fanout)
     cache_nodes = torch.tensor(rnd.sample(range(n), ncache), dtype=torch.int64)
     slot = torch.full((n,), -1, dtype=torch.int32)
     slot[cache_nodes] = torch.arange(ncache, dtype=torch.int32)
-    for handoff in (False, True):
+    for handoff in (False, True, "fused"):
         sr, _ = check_all(dg, orc, off, idx, seeds, [5, last_fanout], 77, feats, slot,
                           cache_nodes, sample_kw={"direct": True, "handoff": handoff})
         m = [int(sr.hop_ptr[b, -1] - sr.hop_ptr[b, -2]) for b in range(2)]

@@ -27,7 +27,10 @@ def dg():
     return m
 
 
-def test_pipelined_steps_are_each_correct(dg):
+@pytest.mark.parametrize("fused", [False, True])
+def test_pipelined_steps_are_each_correct(dg, fused):
+    """fused: each step samples and packs in one dg_sample_pack_group call,
+    with a packing workspace per output set."""
     w = synth.make_workload("M1", device=DEV)
     cfg = w.cfg
     fan = list(cfg.fanouts)
@@ -38,7 +41,8 @@ def test_pipelined_steps_are_each_correct(dg):
     flags = dg.sample_flags(direct=True)
     ws_s = torch.empty(dg._L.dg_sample_workspace_bytes(cfg.n, B, node_cap, edge_cap, flags),
                        dtype=torch.uint8, device=DEV)
-    ws_p = [torch.empty(dg._L.dg_pack_workspace_bytes(cfg.n, B, B * node_cap),
+    ws_p = [torch.empty(dg._L.dg_sample_pack_workspace_bytes(cfg.n, B, node_cap) if fused
+                        else dg._L.dg_pack_workspace_bytes(cfg.n, B, B * node_cap),
                         dtype=torch.uint8, device=DEV) for _ in range(2)]
     mem = torch.empty(cfg.n, dtype=torch.int64, device=DEV)
     lines = torch.empty(dg.member_lines_bytes(cfg.n), dtype=torch.uint8, device=DEV)
@@ -75,16 +79,27 @@ def test_pipelined_steps_are_each_correct(dg):
         # sampling writes the cached nodes' address-table entries into this
         # step's packing set, so it waits for the assembly that last read it
         stream.wait_event(asm_done[slot])
-        sr = dg.sample_group(w.offsets, w.indices, groups[k], fan, w.rng_seed, membership=mem,
-                             workspace=ws_s, direct=True, exit_clear=True, entry_clear=clear,
-                             member_lines=lines, stream=stream, cache_slot=w.cache_slot,
-                             loc=pr2[slot].loc, node_cap=node_cap, edge_cap=edge_cap)
-        counts = sr.node_count.copy()
-        nodes = sr.nodes.clone()  # the next step's sampling overwrites sr.nodes
-        pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, out=pr2[slot],
-                           workspace=ws_p[slot], membership=mem, clear_membership=True,
-                           member_lines=lines, stream=stream, rows_stream=s_asm,
-                           loc_pending=True)
+        if fused:
+            sr, pr = dg.sample_pack_group(w.offsets, w.indices, groups[k], fan, w.rng_seed,
+                                          w.feats, w.cache_slot, node_cap=node_cap,
+                                          edge_cap=edge_cap, pack_out=pr2[slot],
+                                          workspace=ws_s, pack_workspace=ws_p[slot],
+                                          stream=stream, rows_stream=s_asm, membership=mem,
+                                          direct=True, exit_clear=True, entry_clear=clear)
+            counts = sr.node_count.copy()
+            nodes = sr.nodes.clone()
+        else:
+            sr = dg.sample_group(w.offsets, w.indices, groups[k], fan, w.rng_seed,
+                                 membership=mem, workspace=ws_s, direct=True, exit_clear=True,
+                                 entry_clear=clear, member_lines=lines, stream=stream,
+                                 cache_slot=w.cache_slot, loc=pr2[slot].loc, node_cap=node_cap,
+                                 edge_cap=edge_cap)
+            counts = sr.node_count.copy()
+            nodes = sr.nodes.clone()  # the next step's sampling overwrites sr.nodes
+            pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, counts, out=pr2[slot],
+                               workspace=ws_p[slot], membership=mem, clear_membership=True,
+                               member_lines=lines, stream=stream, rows_stream=s_asm,
+                               loc_pending=True)
         clear = True
         pack_done.record(stream)
         s_asm.wait_event(pack_done)

@@ -3,7 +3,8 @@ the sampler's membership mask handed to the packer, the mask-clearing flags
 (two groups in a row on the same membership buffer and workspaces, the second
 sampling call told that the state is clear, and the second also taking the
 cached nodes' address-table entries from sampling), and packing's row copy
-queued on a second stream with the assembly behind it.
+queued on a second stream with the assembly behind it.  A third run samples
+and packs the group in one dg_sample_pack_group call.
 
 Every workload compares, for every mini-batch of the group, the sampled node
 list, hop bounds, edge lists and edge bounds with the oracle's (one oracle run
@@ -152,7 +153,41 @@ def run_and_check(dg, orc, w, ref, direct=True):
     assert torch.equal(pr2.packed_ids[:rows], keep[5])
     assert torch.equal(pr2.packed[:rows], keep[7])
     assert int(mem.count_nonzero()) == 0
-    return sr2, pr2
+
+    # a third time in one dg_sample_pack_group call (with the direct table its
+    # last hop's compaction does packing's pass; with the hash table packing's
+    # own passes follow), still told that the state is clear, every output
+    # overwritten with garbage first
+    for t in (sr2.nodes, sr2.edge_src, sr2.edge_dst, pr2.packed_ids, pr2.unique):
+        t.fill_(-7)
+    pr2.loc.fill_(-3)
+    pr2.packed[:rows].zero_()
+    ws_f = torch.empty(dg._L.dg_sample_pack_workspace_bytes(cfg.n, cfg.B, node_cap),
+                       dtype=torch.uint8, device=DEV)
+    side = torch.cuda.Stream(device=DEV)
+    sr3, pr3 = dg.sample_pack_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, w.feats,
+                                    w.cache_slot, out=sr2, pack_out=pr2, workspace=ws_s,
+                                    pack_workspace=ws_f, rows_stream=side, membership=mem,
+                                    direct=direct, exit_clear=True, entry_clear=True)
+    side.synchronize()
+    torch.cuda.synchronize()
+    assert np.array_equal(sr3.hop_ptr, keep[3]) and np.array_equal(sr3.edge_ptr, keep[4])
+    for b in range(cfg.B):
+        n, e = int(counts[b]), int(keep[4][b, -1])
+        assert torch.equal(sr3.nodes[b, :n], keep[0][b, :n]), b
+        assert torch.equal(sr3.edge_src[b, :e], keep[1][b, :e]), b
+        assert torch.equal(sr3.edge_dst[b, :e], keep[2][b, :e]), b
+        assert torch.equal(pr3.loc[b, :n], keep[6][b, :n]), b
+    assert pr3.sizes["packed_rows"] == rows
+    assert pr3.sizes["unique_nodes"] == refp["unique_nodes"]
+    assert np.array_equal(pr3.packed_ptr_host, refp["packed_ptr"])
+    assert np.array_equal(pr3.packed_ptr.cpu().numpy(), refp["packed_ptr"])
+    assert torch.equal(pr3.packed_ids[:rows], keep[5])
+    assert np.array_equal(pr3.unique[:refp["unique_nodes"]].cpu().numpy(), refp["unique"])
+    assert torch.equal(pr3.packed[:rows], keep[7])
+    assert int(mem.count_nonzero()) == 0
+    print(f"[{cfg.name}] one-call sampling and packing equal", flush=True)
+    return sr3, pr3
 
 
 def test_workload_M1_full(dg, orc):
