@@ -310,10 +310,10 @@ int mask_scan_rows(MaskScan &m, hipStream_t s);
 //      pairs, all pairs).
 // The count pass zeroes every mask word it reads, and the prev words too with
 // clear_prev.  The write pass writes sampling's lists and the address-table
-// entries of new cached pairs, and packing's U, U_nc, pair offsets, P_b and
-// pair destinations; for every packed pair it also records the list slot of
-// the pair when it is new at this hop (pslot, -1 for an older pair) for the
-// address tables that follow.  Every index is checked against its buffer:
+// entries of new cached pairs, and packing's U, U_nc, pair offsets and pair
+// destinations; for every packed pair it records the node and, when the pair
+// is new at this hop, its list slot (pinfo), from which the address tables
+// and P_b follow.  Every index is checked against its buffer:
 // counts beyond a capacity are found by the host after the read-back.
 struct FuseScan {
   uint64_t *mask;
@@ -330,6 +330,7 @@ struct FuseScan {
   uint64_t *cw_mask;
   uint64_t *cw_new;
   uint16_t *cw_off;
+  int32_t *cw_slot;  // cache slot of each listed word's node (-1: not cached)
   uint32_t *cnt_s, *wpre_s, *cnt_p, *wpre_p;
   const int64_t *base_s, *base_p;
   // write pass, sampling: the hop's segments of the node lists
@@ -341,15 +342,15 @@ struct FuseScan {
   int32_t *local_out;  // nullable: [N][B] local indices of the hop's pairs
   // write pass, packing
   const int64_t *packed_ptr;  // device [B+1], from the p view's totals
-  int64_t packed_cap;         // entries of packed_ids and pslot
-  int32_t *packed_ids;
-  int32_t *pslot;
+  int64_t packed_cap;         // entries of pinfo
+  uint64_t *pinfo;            // per packed row: node ID (low half) and the pair's
+                              // list slot if new at this hop, else -1 (high half)
   int32_t *uniq_out;  // nullable
   int64_t unique_cap;
   int32_t *unc_ids;
   int64_t *unc_off;
   int64_t unc_cap;
-  int64_t *nodeoff;
+  int64_t *nodeoff;  // nullable
   int64_t *pairdest;
   int64_t pair_cap;
 };
@@ -382,10 +383,11 @@ int pack_impl(const void *feats, int64_t N, int64_t row_bytes, const int32_t *ca
               int64_t cache_rows, void *cache_table, uint32_t flags, void *ws,
               size_t ws_bytes, hipStream_t stream, hipStream_t rows_stream, dg_sizes *sizes,
               dg_timing *timing, bool no_alloc);
-// What follows a fused compaction: the address-table entries of the packed
-// pairs, loc[b*node_cap + j] = r for packed row packed_ptr[b] + r, with j =
-// pslot of the row for a pair new at the last hop, else local[u*B + b]; then
-// the row copy (on rows_stream, not waited for, when rows_async).
+// What follows a fused compaction: P_b (packed_ids) and the address-table
+// entries of the packed pairs, loc[b*node_cap + j] = r for packed row
+// packed_ptr[b] + r, with j the list slot in the row's pinfo for a pair new at
+// the last hop, else local[u*B + b]; then the row copy (on rows_stream, not
+// waited for, when rows_async).
 struct PhaseTimer;
 struct FusedTail {
   const void *feats;
@@ -394,7 +396,9 @@ struct FusedTail {
   int64_t node_cap;
   const int64_t *n_b;              // [host] list lengths
   const int64_t *packed_ptr_host;  // [host] B+1
-  const int32_t *packed_ids, *pslot, *local;
+  const uint64_t *pinfo;
+  const int32_t *local;
+  int32_t *packed_ids;
   int32_t *loc;
   void *packed;  // nullable: no row copy
   const int32_t *unc_ids;

@@ -549,20 +549,24 @@ struct LocFill {
   int64_t n[DG_MAX_BATCHES];          // list lengths
 };
 
-// Address-table entries of the packed pairs after a fused compaction: packed
-// row i of chunk b (node u = packed_ids[i]) is entry j of nodes_b, with j =
-// pslot[i] for a pair new at the last hop, else u's local index in the direct
-// table; loc_b[j] = i - packed_ptr[b], u's rank in P_b.  Every non-cached list
-// entry is reached once this way (its pair is in P_b).
-__global__ __launch_bounds__(THREADS) void k_loc_packed(LocFill F, const int32_t *packed_ids,
-                                                        const int32_t *pslot,
-                                                        const int32_t *local, int32_t *loc,
+// P_b and the address-table entries of the packed pairs after a fused
+// compaction: packed row i of chunk b holds node u (low half of pinfo[i]),
+// which is entry j of nodes_b, with j the list slot in the high half for a
+// pair new at the last hop, else u's local index in the direct table;
+// packed_ids[i] = u and loc_b[j] = i - packed_ptr[b], u's rank in P_b.  Every
+// non-cached list entry is reached once this way (its pair is in P_b).
+__global__ __launch_bounds__(THREADS) void k_loc_packed(LocFill F, const uint64_t *pinfo,
+                                                        const int32_t *local,
+                                                        int32_t *packed_ids, int32_t *loc,
                                                         uint32_t *err) {
   const int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (i >= F.start[F.B]) return;
   const int b = find_batch_wave(F.start, F.B, i);
-  int32_t j = pslot[i];
-  if (j < 0) j = local[(int64_t)packed_ids[i] * F.B + b];
+  const uint64_t e = pinfo[i];
+  const int32_t u = (int32_t)(uint32_t)e;
+  int32_t j = (int32_t)(e >> 32);
+  packed_ids[i] = u;
+  if (j < 0) j = local[(int64_t)u * F.B + b];
   if (j < 0 || (int64_t)j >= F.n[b]) {
     atomicOr(err, ERR_INTERNAL);
     return;
@@ -595,7 +599,7 @@ int pack_fused_tail(const FusedTail &t, bool rows_async, hipStream_t s, hipStrea
     for (int b = 0; b <= t.B; ++b) F.start[b] = t.packed_ptr_host[b];
     for (int b = 0; b < t.B; ++b) F.n[b] = t.n_b[b];
     hipLaunchKernelGGL(k_loc_packed, dim3(blocks_for(t.rows)), dim3(THREADS), 0, s, F,
-                       t.packed_ids, t.pslot, t.local, t.loc, t.err);
+                       t.pinfo, t.local, t.packed_ids, t.loc, t.err);
     DG_HIP(hipGetLastError());
   }
   *ev_loc = tm ? tm->mark() : -1;

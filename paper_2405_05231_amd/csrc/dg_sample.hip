@@ -584,13 +584,13 @@ struct SampleMarks {
 struct PackInto {
   PackWs pw;          // packing's workspace (last in the carve, see carve_sample_pack)
   size_t pw_offset;   // its offset in the packing workspace
-  int32_t *pslot;     // [pslot_cap] list slot of each packed pair new at the last hop
-  int64_t pslot_cap;
+  uint64_t *pinfo;    // [pinfo_cap] node and list slot of each packed pair (fused pass)
+  int64_t pinfo_cap;
+  int32_t *cw_slot;   // the fused pass's cache slot per listed word
   uint8_t *lines;     // member lines, for a group packed by packing's own passes
   int64_t unc_cap, pair_cap;
   int64_t *packed_ptr;
   int64_t packed_cap;
-  int32_t *packed_ids;
   int32_t *group_unique;
   int64_t unique_cap;
   // set by sample_impl
@@ -603,8 +603,9 @@ struct PackInto {
 
 void carve_sample_pack(PackInto &pk, Carve &c, int64_t N, int B, int64_t node_cap) {
   const int64_t total = (int64_t)B * node_cap;
-  pk.pslot = c.take<int32_t>((size_t)total);
-  pk.pslot_cap = total;
+  pk.pinfo = c.take<uint64_t>((size_t)total);
+  pk.pinfo_cap = total;
+  pk.cw_slot = c.take<int32_t>((size_t)mc_blocks(N) * MC_BLOCK_NODES);
   pk.lines = c.take<uint8_t>((size_t)mc_touch_bytes(N));
   pk.pw_offset = c.used;  // packing's own workspace last: the unfused path hands it on whole
   carve_pack(pk.pw, c, N, B, total);
@@ -797,6 +798,7 @@ int sample_impl(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S, int
         F.cw_mask = w.ms.cw_mask;
         F.cw_new = vp.cw_mask;
         F.cw_off = w.ms.cw_off;
+        F.cw_slot = pk->cw_slot;
         F.cnt_s = w.ms.cnt;
         F.wpre_s = w.ms.wpre;
         F.cnt_p = vp.cnt;
@@ -850,15 +852,14 @@ int sample_impl(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S, int
         F.loc_out = loc;
         F.local_out = w.ms.local_out;
         F.packed_ptr = pk->packed_ptr;
-        F.packed_cap = pk->packed_cap < pk->pslot_cap ? pk->packed_cap : pk->pslot_cap;
-        F.packed_ids = pk->packed_ids;
-        F.pslot = pk->pslot;
+        F.packed_cap = pk->packed_cap < pk->pinfo_cap ? pk->packed_cap : pk->pinfo_cap;
+        F.pinfo = pk->pinfo;
         F.uniq_out = pk->group_unique;
         F.unique_cap = pk->unique_cap;
         F.unc_ids = pk->pw.unc_ids;
         F.unc_off = pk->pw.unc_off;
         F.unc_cap = pk->unc_cap;
-        F.nodeoff = pk->pw.nodeoff;
+        F.nodeoff = nullptr;  // the address tables come from pinfo
         F.pairdest = pk->pw.pairdest;
         F.pair_cap = pk->pair_cap;
         if ((rc = fuse_scan_write(F, w.small + ST_PTOTALS, pk->packed_ptr, s))) return rc;
@@ -1109,7 +1110,6 @@ extern "C" int dg_sample_pack_group(
   carve_sample_pack(pk, c, N, B, node_cap);
   pk.packed_ptr = packed_ptr;
   pk.packed_cap = packed_cap;
-  pk.packed_ids = packed_ids;
   pk.group_unique = group_unique;
   pk.unique_cap = group_unique ? unique_cap : 0;
   if (timing) memset(timing, 0, sizeof(*timing));
@@ -1175,7 +1175,7 @@ extern "C" int dg_sample_pack_group(
   t.n_b = n_b;
   t.packed_ptr_host = packed_ptr_host;
   t.packed_ids = packed_ids;
-  t.pslot = pk.pslot;
+  t.pinfo = pk.pinfo;
   t.local = pk.local;
   t.loc = loc;
   t.packed = packed;

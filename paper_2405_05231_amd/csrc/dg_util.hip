@@ -772,6 +772,7 @@ void k_fuse_count(FuseScan a) {
           const size_t at = gw + rank_below(an, run);
           a.cw_mask[at] = mq;
           a.cw_new[at] = nq;
+          a.cw_slot[at] = sl[q];
           a.cw_off[at] = (uint16_t)((r * 64 + lane) | ((int)cached << 15));
           const uint32_t pc = (uint32_t)__popcll(mq);
           al += pc;
@@ -866,6 +867,7 @@ __global__ __launch_bounds__(MC_THREADS) void k_fuse_write(FuseScan a) {
   const uint64_t *cm = a.cw_mask + gwi * MC_TILE;
   const uint64_t *cn = a.cw_new + gwi * MC_TILE;
   const uint16_t *co = a.cw_off + gwi * MC_TILE;
+  const int32_t *csl = a.cw_slot + gwi * MC_TILE;
   const int64_t *bs = a.base_s + (size_t)blk * rows;
   const int64_t *bp = a.base_p + (size_t)blk * rows;
   const uint32_t *ps = a.wpre_s + gwi * rows;
@@ -885,19 +887,19 @@ __global__ __launch_bounds__(MC_THREADS) void k_fuse_write(FuseScan a) {
     const uint32_t i = c0 + lane;
     uint64_t m = 0, nw = 0;
     uint32_t off = 0;
+    int32_t sl = -1;  // the node's cache slot (for a cached node's new pairs)
     if (i < n) {
       m = cm[i];
       nw = cn[i];
       off = co[i];
+      sl = csl[i];
     }
+    // Every load of the chunk has landed here: without this wait the compiler
+    // waits for them inside the pair loop below, and so (one counter covers
+    // loads and stores) for each iteration's stores before the next.
+    wait_vm_all();
     const int32_t u = (int32_t)(t0 + (off & 1023u));
     const bool cached = (off >> 15) & 1u;
-    int32_t sl = -1;  // a cached node's slot, for its new pairs' entries
-    if (cached && nw != 0ull) sl = a.cache_slot[u];
-    // Every load of the chunk has landed here: without this wait the compiler
-    // waits for sl inside the pair loop below, and so (one counter covers loads
-    // and stores) for each iteration's stores before the next.
-    wait_vm_all();
     const uint64_t mnc = cached ? 0ull : m;
     const uint64_t any = __ballot(m != 0ull);
     if (m != 0ull && a.uniq_out) {
@@ -914,7 +916,7 @@ __global__ __launch_bounds__(MC_THREADS) void k_fuse_write(FuseScan a) {
         a.unc_ids[rk] = u;
         a.unc_off[rk] = pair0;
       }
-      a.nodeoff[u] = pair0;
+      if (a.nodeoff) a.nodeoff[u] = pair0;
     }
     run_nc += __popcll(anc);
     uint64_t act = __ballot((nw | mnc) != 0ull);
@@ -936,10 +938,9 @@ __global__ __launch_bounds__(MC_THREADS) void k_fuse_write(FuseScan a) {
         ++dest_b;
       }
       if ((wp >> lane) & 1ull) {
-        if (pd_b < a.packed_cap) {
-          a.packed_ids[pd_b] = ul;
-          a.pslot[pd_b] = is_new ? (int32_t)(slot - lbase) : -1;
-        }
+        if (pd_b < a.packed_cap)
+          a.pinfo[pd_b] = ((uint64_t)(uint32_t)(is_new ? (int32_t)(slot - lbase) : -1) << 32) |
+                          (uint32_t)ul;
         const int64_t q = run_p + __popcll(wp & lt);
         if (q < a.pair_cap) a.pairdest[q] = pd_b;
         ++pd_b;
@@ -950,7 +951,7 @@ __global__ __launch_bounds__(MC_THREADS) void k_fuse_write(FuseScan a) {
 }
 
 int fuse_scan_count(const FuseScan &f, MaskScan &vs, MaskScan &vp, hipStream_t s) {
-  if (!f.mask || !f.prev || !f.cache_slot || vs.nblk != f.nblk || vp.nblk != f.nblk ||
+  if (!f.mask || !f.prev || !f.cache_slot || !f.cw_slot || vs.nblk != f.nblk || vp.nblk != f.nblk ||
       vs.B != f.B || vp.B != f.B)
     return set_error(DG_EINVAL, "internal: inconsistent fused count pass");
   if (f.nblk > 0) {
@@ -964,8 +965,8 @@ int fuse_scan_count(const FuseScan &f, MaskScan &vs, MaskScan &vp, hipStream_t s
 
 int fuse_scan_write(const FuseScan &f, const int64_t *totals_p, int64_t *packed_ptr,
                     hipStream_t s) {
-  if (!f.seg_out || !f.loc_out || !f.unc_ids || !f.unc_off || !f.nodeoff || !f.pairdest ||
-      (f.packed_cap > 0 && (!f.packed_ids || !f.pslot)) || f.packed_ptr != packed_ptr)
+  if (!f.seg_out || !f.loc_out || !f.unc_ids || !f.unc_off || !f.pairdest || !f.cw_slot ||
+      (f.packed_cap > 0 && !f.pinfo) || f.packed_ptr != packed_ptr)
     return set_error(DG_EINVAL, "internal: inconsistent fused write pass");
   hipLaunchKernelGGL(k_fuse_ptr, dim3(1), dim3(64), 0, s, totals_p, f.B, packed_ptr);
   if (f.nblk > 0)
