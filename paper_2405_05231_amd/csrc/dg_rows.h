@@ -56,6 +56,25 @@ typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ v4u ld_stream(const v4u *p) { return __builtin_nontemporal_load(p); }
 __device__ __forceinline__ void st_stream(v4u x, v4u *p) { __builtin_nontemporal_store(x, p); }
 
+// The row copy of one packing call: the fan-out gather over U_nc, plus the
+// cache rows when a cache table is given.
+struct RowCopy {
+  const void *X;
+  int64_t N, row_bytes;
+  const int32_t *ids;
+  const int64_t *off;
+  int64_t n, pairs;
+  const int64_t *dest;
+  void *packed;
+  const int32_t *cache_nodes;
+  int64_t n_cache;
+  void *cache_table;
+  uint32_t *err;
+};
+// Launches the fan-out gather of one RowCopy on stream s (nothing when it has
+// no item); DG_EHIP when the launch fails.
+int launch_fanout(const RowCopy &r, hipStream_t s);
+
 template <typename T>
 __device__ __forceinline__ T zero_word() {
   T z;

@@ -21,7 +21,7 @@
 
 #include <type_traits>
 
-#include "dg_common.h"
+#include "dg_passes.h"
 
 namespace dg {
 namespace {

@@ -4,7 +4,7 @@
 #include <stdarg.h>
 #include <string.h>
 
-#include "dg_common.h"
+#include "dg_passes.h"
 
 namespace dg {
 
@@ -691,13 +691,13 @@ __device__ __forceinline__ void lds_count(uint32_t k, uint32_t *lo, uint32_t *hi
 }
 
 // Fused count pass (FuseScan).  Every word is read (no touched marks).  The
-// tile is taken in two halves of eight rounds, so that a half's mask words,
-// prev words and cache slots are in registers together; within a half all
-// loads of a kind are requested before any is used.  Per-batch counts, a
-// chunk of MC_CROUNDS rounds at a time: the chunk's words with new bits are
-// staged in one LDS area and its non-cached words in another, and lane b
-// counts bit b of each.
-constexpr int FC_HALF = MC_ROUNDS / 4;
+// tile is taken in four parts of four rounds, so that a part's mask words,
+// prev words and cache slots are in registers together without spilling; the
+// next part's mask words are requested together with this part's prev words
+// and cache slots, so a part costs one round trip.  Per-batch counts, a part
+// at a time: the part's words with new bits are staged in one LDS area and its
+// non-cached words in another, and lane b counts bit b of each.
+constexpr int FC_PART = MC_ROUNDS / 4;
 
 __global__ __launch_bounds__(MC_THREADS) __attribute__((amdgpu_waves_per_eu(8, 8)))
 void k_fuse_count(FuseScan a) {
@@ -720,39 +720,53 @@ void k_fuse_count(FuseScan a) {
   uint32_t al = 0, pl = 0, nl = 0;  // this lane's word: all, non-cached, new pairs
   uint32_t mine_s = 0, mine_p = 0;  // batch `lane`: new pairs, non-cached pairs
   uint64_t bad = 0;
+  // Mask words are loaded unconditionally (a node past N reads the last word,
+  // and its value is dropped): no branch between the loads of a part.
+  auto load_part = [&](int h0, uint64_t (&m)[FC_PART]) {
 #pragma unroll
-  for (int h0 = 0; h0 < MC_ROUNDS; h0 += FC_HALF) {
-    uint64_t m[FC_HALF];
-    if (rem >= MC_TILE) {
-#pragma unroll
-      for (int q = 0; q < FC_HALF; ++q) m[q] = mk[(h0 + q) * 64 + lane];
-    } else {
-#pragma unroll
-      for (int q = 0; q < FC_HALF; ++q)
-        m[q] = (h0 + q) * 64 + lane < rem ? mk[(h0 + q) * 64 + lane] : 0ull;
+    for (int q = 0; q < FC_PART; ++q) {
+      const int64_t r = (int64_t)(h0 + q) * 64 + lane;
+      m[q] = a.mask[r < rem ? t0 + r : a.N - 1];
     }
-    wait_vm_all();
-    uint64_t any[FC_HALF];  // lanes of round q with a word (uniform)
-    uint64_t nw[FC_HALF];
-    int32_t sl[FC_HALF];
 #pragma unroll
-    for (int q = 0; q < FC_HALF; ++q) {
+    for (int q = 0; q < FC_PART; ++q)
+      if ((int64_t)(h0 + q) * 64 + lane >= rem) m[q] = 0ull;
+  };
+  uint64_t m[FC_PART];
+  load_part(0, m);
+  wait_vm_all();
+#pragma unroll
+  for (int h0 = 0; h0 < MC_ROUNDS; h0 += FC_PART) {
+    uint64_t any[FC_PART];  // lanes of round q with a word (uniform)
+    uint64_t nw[FC_PART];
+    int32_t sl[FC_PART];
+#pragma unroll
+    for (int q = 0; q < FC_PART; ++q) {
       const bool has = (m[q] & keep) != 0ull;
       any[q] = __ballot(has);
       nw[q] = has ? pv[(h0 + q) * 64 + lane] : 0ull;
       sl[q] = has ? cs[(h0 + q) * 64 + lane] : -1;
     }
+    uint64_t mn[FC_PART];  // the next part's mask words
+    if (h0 + FC_PART < MC_ROUNDS) load_part(h0 + FC_PART, mn);
     wait_vm_all();
-    uint64_t cmask[FC_HALF];  // cached lanes of round q (uniform); the slots die here
+    // The cached lanes of each round, and each listed word's slot at its place
+    // in the compact list (so that the slots need no registers further on).
+    uint64_t cmask[FC_PART];  // cached lanes of round q (uniform)
+    {
+      uint32_t at0 = run;
 #pragma unroll
-    for (int q = 0; q < FC_HALF; ++q) {
-      cmask[q] = 0ull;
-      if (!any[q]) continue;
-      bad |= __ballot(sl[q] < -1);
-      cmask[q] = __ballot(sl[q] >= 0);
+      for (int q = 0; q < FC_PART; ++q) {
+        cmask[q] = 0ull;
+        if (!any[q]) continue;
+        bad |= __ballot(sl[q] < -1);
+        cmask[q] = __ballot(sl[q] >= 0);
+        if ((m[q] & keep) != 0ull) a.cw_slot[gw + rank_below(any[q], at0)] = sl[q];
+        at0 += (uint32_t)__popcll(any[q]);
+      }
     }
 #pragma unroll
-    for (int c = 0; c < FC_HALF; c += MC_CROUNDS) {
+    for (int c = 0; c < FC_PART; c += MC_CROUNDS) {
       uint32_t ks = 0, kp = 0;  // staged new / non-cached words of the chunk (uniform)
 #pragma unroll
       for (int q = c; q < c + MC_CROUNDS; ++q) {
@@ -772,7 +786,6 @@ void k_fuse_count(FuseScan a) {
           const size_t at = gw + rank_below(an, run);
           a.cw_mask[at] = mq;
           a.cw_new[at] = nq;
-          a.cw_slot[at] = sl[q];
           a.cw_off[at] = (uint16_t)((r * 64 + lane) | ((int)cached << 15));
           const uint32_t pc = (uint32_t)__popcll(mq);
           al += pc;
@@ -798,6 +811,10 @@ void k_fuse_count(FuseScan a) {
       }
       lds_count(ks, ns_lo, ns_hi, lane, mine_s);
       lds_count(kp, np_lo, np_hi, lane, mine_p);
+    }
+    if (h0 + FC_PART < MC_ROUNDS) {
+#pragma unroll
+      for (int q = 0; q < FC_PART; ++q) m[q] = mn[q];
     }
   }
   if (bad && lane == 0) atomicOr(a.err, ERR_CACHE_SLOT);

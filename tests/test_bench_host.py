@@ -28,7 +28,7 @@ def test_popcount64_matches_python():
     assert got == [bin(v & (2**64 - 1)).count("1") for v in vals]
 
 
-@pytest.mark.parametrize("kernel,main", [("fanout_gather", "dg_pack.hip"),
+@pytest.mark.parametrize("kernel,main", [("fanout_gather", "dg_gather.hip"),
                                          ("assemble", "dg_assemble.hip")])
 def test_traffic_digest_covers_the_kernel_translation_unit(tmp_path, monkeypatch, kernel, main):
     d = bench.kernel_source_digest(kernel)
