@@ -67,6 +67,11 @@ struct MaskScan {
                                      // the new bits to prev
   bool keep_prev;                    // false: leave prev as it is (nothing reads it later)
   bool clear_prev;                   // (without keep_prev) zero each non-zero prev word read
+  uint8_t *plines;                   // nullable (with prev): a byte per 2^MC_TOUCH_SHIFT
+                                     // nodes, non-zero iff one of them holds a prev bit;
+                                     // prev is read only in marked lines.  With keep_prev
+                                     // the pass marks the lines of the new words, with
+                                     // clear_prev it zeroes the marks of its tiles
   bool clear_mask;                   // zero each non-zero mask word read (packing mode)
   uint8_t *lines_out;                // sampling, whole sweeps only (nullable): a byte per
                                      // 2^MC_TOUCH_SHIFT nodes, non-zero iff one of them
@@ -119,6 +124,7 @@ int mask_scan_rows(MaskScan &m, hipStream_t s);
 struct FuseScan {
   uint64_t *mask;
   uint64_t *prev;
+  uint8_t *plines;  // nullable: prev's lines, as MaskScan::plines (zeroed with clear_prev)
   const int32_t *cache_slot;
   int64_t N;
   int B;

@@ -63,9 +63,9 @@ struct Lists {
 __global__ __launch_bounds__(THREADS) void k_seed_init(const int32_t *seeds, int B, int S,
                                                        int64_t N, int64_t node_cap,
                                                        int32_t *nodes, uint64_t *visited,
-                                                       uint64_t *prev, int32_t *local,
-                                                       const int32_t *cache_slot, int32_t *loc,
-                                                       uint32_t *err) {
+                                                       uint64_t *prev, uint8_t *plines,
+                                                       int32_t *local, const int32_t *cache_slot,
+                                                       int32_t *loc, uint32_t *err) {
   int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (i >= (int64_t)B * S) return;
   int b = (int)(i / S);
@@ -85,6 +85,7 @@ __global__ __launch_bounds__(THREADS) void k_seed_init(const int32_t *seeds, int
   unsigned long long old = atomicOr((unsigned long long *)&visited[v], bit);
   if (old & bit) atomicOr(err, ERR_DUP_NODE);
   atomicOr((unsigned long long *)&prev[v], bit);  // seeds are not new at hop 1
+  plines[v >> MC_TOUCH_SHIFT] = 1;
   if (local) local[(int64_t)v * B + b] = (int32_t)j;
 }
 
@@ -482,6 +483,7 @@ constexpr uint32_t SAMPLE_FLAGS =
 struct SampleWs {
   uint32_t *err;
   uint64_t *visited, *prev;
+  uint8_t *plines;  // lines of prev that hold a bit (a byte per 8 nodes)
   int64_t *f_off, *f_deg, *f_cnt, *f_eoff, *tiles;
   LocalTable table;  // hash relabelling
   int32_t *local;    // direct relabelling: [N][B]
@@ -497,6 +499,7 @@ void carve_sample(SampleWs &w, Carve &c, int64_t N, int B, int64_t node_cap, boo
   w.err = c.take<uint32_t>(64);
   w.visited = c.take<uint64_t>((size_t)N);
   w.prev = c.take<uint64_t>((size_t)N);
+  w.plines = c.take<uint8_t>((size_t)mc_touch_bytes(N));
   w.f_off = c.take<int64_t>((size_t)fmax);
   w.f_deg = c.take<int64_t>((size_t)fmax);
   w.f_cnt = c.take<int64_t>((size_t)fmax);
@@ -668,12 +671,16 @@ int sample_impl(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S, int
   if (!entry_clear) {
     if ((rc = fill_u64(w.visited, (size_t)N, 0, s))) return rc;
     if ((rc = fill_u64(w.prev, (size_t)N, 0, s))) return rc;
+    if ((rc = fill_u64(reinterpret_cast<uint64_t *>(w.plines), (size_t)mc_touch_bytes(N) / 8, 0,
+                       s)))
+      return rc;
   }
   bool prev_cleared = false;  // the last hop's count pass zeroed prev
   bool lines_done = false;    // the last hop's count pass wrote member_lines
   bool rl_search = false;     // the last hop's edges are relabelled by search
   hipLaunchKernelGGL(k_seed_init, dim3(blocks_for((int64_t)B * S)), dim3(THREADS), 0, s, seeds,
-                     B, S, N, node_cap, nodes, w.visited, w.prev, w.local, cache_slot, loc,
+                     B, S, N, node_cap, nodes, w.visited, w.prev, w.plines, w.local, cache_slot,
+                     loc,
                      w.err);
   DG_HIP(hipGetLastError());  // bad seeds are reported at the first hop's round trip
 
@@ -766,6 +773,7 @@ int sample_impl(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S, int
       // reads this hop's counts (it stops at each list's capacity)
       w.ms.mask = w.visited;
       w.ms.prev = w.prev;
+      w.ms.plines = w.plines;
       w.ms.keep_prev = k < K;  // after the last hop nothing reads prev
       w.ms.touched = h.touched;
       // With DG_SAMPLE_EXIT_CLEAR the last hop's count pass zeroes every prev
@@ -788,6 +796,7 @@ int sample_impl(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S, int
         memset(&F, 0, sizeof(F));
         F.mask = w.visited;
         F.prev = w.prev;
+        F.plines = w.plines;
         F.cache_slot = cache_slot;
         F.N = N;
         F.B = B;
@@ -1003,7 +1012,11 @@ int sample_impl(const dg_csr *g, const int32_t *seeds, int32_t B, int32_t S, int
     DG_HIP(hipGetLastError());
   }
   mk.r1 = tm.mark();
-  if (exit_clear && !prev_cleared && (rc = fill_u64(w.prev, (size_t)N, 0, s))) return rc;
+  if (exit_clear && !prev_cleared &&
+      ((rc = fill_u64(w.prev, (size_t)N, 0, s)) ||
+       (rc = fill_u64(reinterpret_cast<uint64_t *>(w.plines), (size_t)mc_touch_bytes(N) / 8, 0,
+                      s))))
+    return rc;
   if (member_lines && !lines_done && !(pk && pk->fused) &&
       (rc = member_lines_pass(w.visited, N, B, member_lines, s)))
     return rc;

@@ -334,6 +334,24 @@ void k_mask_count(MaskScan a) {
 #pragma unroll
   for (int r = 0; r < MC_ROUNDS; ++r) cmask[r] = 0ull;
   if (SAMPLE) {
+    // prev's lines: bit r of plm says this lane's line in round r holds a prev
+    // bit; the prev word is read only then (round r's marks are the 8 bytes at
+    // 8r, and lane l's is byte l/8 of them, as for the touched marks)
+    uint32_t plm = 0xffffu;
+    if (a.plines) {
+      const uint64_t *f = reinterpret_cast<const uint64_t *>(a.plines + (t0 >> MC_TOUCH_SHIFT));
+      const uint32_t sh = 8u * ((uint32_t)lane >> 3);
+      uint32_t lm = 0;
+#pragma unroll
+      for (int r = 0; r < MC_ROUNDS; ++r)
+        lm |= (((f[r] >> sh) & 0xffull) != 0ull ? 1u : 0u) << r;
+      plm = lm;
+      if (a.clear_prev) {  // the marks go with the prev words they describe
+        uint64_t *fw = reinterpret_cast<uint64_t *>(a.plines + (t0 >> MC_TOUCH_SHIFT));
+        const uint64_t mine = lane < MC_ROUNDS ? f[lane] : 0ull;
+        if (mine != 0ull) fw[lane] = 0ull;
+      }
+    }
     // prev words in two halves of the rounds: half the registers (so more
     // waves per SIMD) for one more round trip
     uint64_t *pv = a.prev + t0;
@@ -344,7 +362,7 @@ void k_mask_count(MaskScan a) {
 #pragma unroll
       for (int q = 0; q < H; ++q) {
         const int r = h0 + q;
-        p[q] = (any[r] && m[r] != 0ull) ? pv[r * 64 + lane] : 0ull;
+        p[q] = (any[r] && m[r] != 0ull && ((plm >> r) & 1u)) ? pv[r * 64 + lane] : 0ull;
       }
       wait_vm_all();
 #pragma unroll
@@ -356,6 +374,11 @@ void k_mask_count(MaskScan a) {
         if (a.clear_prev && p[q] != 0ull) pv[r * 64 + lane] = 0ull;
         m[r] = nw;
         any[r] = __ballot(nw != 0ull);
+        if (a.keep_prev && a.plines) {  // the lines of this hop's new words
+          const uint32_t sh = 8u * (uint32_t)lane;
+          if (lane < 8 && ((any[r] >> sh) & 0xffull) != 0ull)
+            a.plines[(t0 >> MC_TOUCH_SHIFT) + r * 8 + lane] = 1;
+        }
       }
     }
   } else if (a.cache_slot) {
@@ -732,6 +755,22 @@ void k_fuse_count(FuseScan a) {
     for (int q = 0; q < FC_PART; ++q)
       if ((int64_t)(h0 + q) * 64 + lane >= rem) m[q] = 0ull;
   };
+  // prev's lines (bit r: this lane's line in round r holds a prev bit; the
+  // prev word is read only then), zeroed with the prev words
+  uint32_t plm = 0xffffu;
+  if (a.plines) {
+    const uint64_t *f = reinterpret_cast<const uint64_t *>(a.plines + (t0 >> MC_TOUCH_SHIFT));
+    const uint32_t sh = 8u * ((uint32_t)lane >> 3);
+    uint32_t lm = 0;
+#pragma unroll
+    for (int r = 0; r < MC_ROUNDS; ++r) lm |= (((f[r] >> sh) & 0xffull) != 0ull ? 1u : 0u) << r;
+    plm = lm;
+    if (a.clear_prev) {
+      uint64_t *fw = reinterpret_cast<uint64_t *>(a.plines + (t0 >> MC_TOUCH_SHIFT));
+      const uint64_t mine = lane < MC_ROUNDS ? f[lane] : 0ull;
+      if (mine != 0ull) fw[lane] = 0ull;
+    }
+  }
   uint64_t m[FC_PART];
   load_part(0, m);
   wait_vm_all();
@@ -744,7 +783,7 @@ void k_fuse_count(FuseScan a) {
     for (int q = 0; q < FC_PART; ++q) {
       const bool has = (m[q] & keep) != 0ull;
       any[q] = __ballot(has);
-      nw[q] = has ? pv[(h0 + q) * 64 + lane] : 0ull;
+      nw[q] = (has && ((plm >> (h0 + q)) & 1u)) ? pv[(h0 + q) * 64 + lane] : 0ull;
       sl[q] = has ? cs[(h0 + q) * 64 + lane] : -1;
     }
     uint64_t mn[FC_PART];  // the next part's mask words
