@@ -254,6 +254,8 @@ CASES = [
     (600, 20, 4, 8, [6, 6], 512, torch.float32, 0.1),          # 2048-byte rows (2 vectors/lane)
     (600, 20, 4, 8, [6, 6], 1024, torch.float32, 0.1),         # 4096-byte rows (4 vectors/lane)
     (300, 20, 5, 6, [4, 0], 16, torch.float32, 0.2),           # f = 0 at the last hop
+    (300, 20, 5, 6, [6], 16, torch.float32, 0.2),              # one hop (the last is the first)
+    (300, 20, 5, 6, [], 16, torch.float32, 0.2),               # no hop: the seeds alone
 ]
 
 
