@@ -34,8 +34,12 @@ def same_sample(a, b):
         assert torch.equal(a.edge_dst[bb, :e], b.edge_dst[bb, :e]), bb
 
 
-def same_pack(a, b, counts):
-    assert a.sizes == b.sizes
+def same_pack(a, b, counts, keys=None):
+    """keys: the size fields to compare (default all of them)."""
+    if keys is None:
+        assert a.sizes == b.sizes
+    else:
+        assert {k: a.sizes[k] for k in keys} == {k: b.sizes[k] for k in keys}
     rows = a.sizes["packed_rows"]
     assert np.array_equal(a.packed_ptr_host, b.packed_ptr_host)
     assert torch.equal(a.packed_ids[:rows], b.packed_ids[:rows])

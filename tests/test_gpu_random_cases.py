@@ -11,7 +11,8 @@
    that hops fall on both sides of the touched-marks limit): every group's
    outputs must equal those of independent calls without the flags, and
    packing must leave the mask all-zero.
-3. Frequency-ranked cache selection and the MinHash disk-cache order on random
+3. Both of the above through the one-call path (dg_sample_pack_group).
+4. Frequency-ranked cache selection and the MinHash disk-cache order on random
    small groups, bit-exact against the oracle.
 
 Each case is fixed by its index, so a failure names a reproducible
@@ -84,6 +85,12 @@ def test_random_valid_case(dg, orc, case):
     slot[cache_nodes] = torch.arange(ncache, dtype=torch.int32)
     check_all(dg, orc, off, idx, seeds, c["fan"], 4242 + case, feats, slot, cache_nodes,
               batch_base=3 * case, sample_kw={"layered": c["layered"], "direct": c["direct"]})
+    if c["direct"]:
+        # the same case in one dg_sample_pack_group call: with the direct table
+        # the last hop's compaction also does packing's pass
+        check_all(dg, orc, off, idx, seeds, c["fan"], 4242 + case, feats, slot, cache_nodes,
+                  batch_base=3 * case,
+                  sample_kw={"layered": c["layered"], "direct": True, "handoff": "fused"})
 
 
 def strided_graph(nrng, n, dmax):
@@ -155,6 +162,56 @@ def test_random_group_loop_with_flags(dg, case):
         assert int(mem.count_nonzero()) == 0, g
         pr_f = dg.pack_group(feats, slot, sr_f.nodes, counts, with_unique=True, membership=mem_f)
         same_pack(pr, pr_f, counts)
+
+
+@pytest.mark.parametrize("case", range(N_LOOP_CASES))
+def test_random_group_loop_in_one_call(dg, case):
+    """Three groups through dg_sample_pack_group on one sampling workspace, one
+    packing workspace and one membership buffer (garbage in both workspaces at
+    the start), clearing flags on: each group's outputs equal those of
+    sample_group + pack_group on fresh buffers, and the membership words end
+    all-zero.  One case in four relabels by hash, where packing's own passes
+    follow sampling inside the call."""
+    rnd, c = make_loop_case(case)
+    direct = case % 4 != 3
+    print(f"one-call loop case {case}: {c} direct={direct}", flush=True)
+    n, B, S = c["n"], c["B"], c["S"]
+    nrng = np.random.default_rng(500 + case)
+    off_h, idx_h = strided_graph(nrng, n, c["dmax"])
+    off, idx = off_h.to(DEV), idx_h.to(DEV)
+    gen = torch.Generator().manual_seed(500 + case)
+    feats = torch.randn((n, c["dim"]), generator=gen).to(DEV)
+    ncache = int(n * c["share"])
+    slot = torch.full((n,), -1, dtype=torch.int32)
+    slot[torch.tensor(rnd.sample(range(n), ncache), dtype=torch.int64)] = \
+        torch.arange(ncache, dtype=torch.int32)
+    slot = slot.to(DEV)
+    groups = [torch.tensor([rnd.sample(range(n), S) for _ in range(B)], dtype=torch.int32,
+                           device=DEV) for _ in range(3)]
+    fan, rng, layered = c["fan"], 991 + case, c["layered"]
+    node_cap, edge_cap = dg.sample_bounds(n, idx.numel(), S, fan, layered)
+    flags = dg.sample_flags(layered, direct, True, True)
+    ws_s = torch.full((dg._L.dg_sample_workspace_bytes(n, B, node_cap, edge_cap, flags),), 0xA5,
+                      dtype=torch.uint8, device=DEV)
+    ws_p = torch.full((dg._L.dg_sample_pack_workspace_bytes(n, B, node_cap),), 0x5A,
+                      dtype=torch.uint8, device=DEV)
+    mem = torch.full((n,), -1, dtype=torch.int64, device=DEV)
+    for g, seeds in enumerate(groups):
+        sr, pr = dg.sample_pack_group(off, idx, seeds, fan, rng, feats, slot, batch_base=g * B,
+                                      node_cap=node_cap, edge_cap=edge_cap, with_unique=True,
+                                      workspace=ws_s, pack_workspace=ws_p, membership=mem,
+                                      layered=layered, direct=direct, entry_clear=g > 0,
+                                      exit_clear=True)
+        torch.cuda.synchronize()
+        assert int(mem.count_nonzero()) == 0, g
+        sr_f = dg.sample_group(off, idx, seeds, fan, rng, batch_base=g * B, layered=layered,
+                               direct=direct, node_cap=node_cap, edge_cap=edge_cap)
+        same_sample(sr, sr_f)
+        counts = sr_f.hop_ptr[:, -1].copy()
+        pr_f = dg.pack_group(feats, slot, sr_f.nodes, counts, with_unique=True)
+        # the one call also reports sampling's sizes; compare packing's
+        same_pack(pr, pr_f, counts, keys=("packed_rows", "unique_nodes", "unique_packed"))
+        assert pr.sizes["total_nodes"] == int(counts.sum()), g
 
 
 N_NEXT_CASES = 30
