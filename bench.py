@@ -453,6 +453,7 @@ def main():
     F_main = sum(sum(feature_bytes(st)) for st in steps_p)
     ms_step = 1e3 * t_total / args.steps
     value = F_main / t_total / 1e9
+    device = device_info(dev)
     ms_serial = 1e3 * t_serial / args.steps
     # fan-out gather: one k_fanout16 launch per step, timed by the library's
     # HIP events on the call's stream (serial region)
@@ -484,9 +485,7 @@ def main():
         "vs_baseline": None,
         "dtype": "u8",
         "data": "synthetic",
-        "device": {"name": torch.cuda.get_device_name(dev),
-                   "arch": torch.cuda.get_device_properties(dev).gcnArchName,
-                   "hip": torch.version.hip},
+        "device": device,
         "config": {"workload": cfg.name, "nodes": cfg.n, "edges": w.num_edges,
                    "rmat_draws": cfg.draws, "feature": f"{cfg.dim}x{str(cfg.dtype)[6:]}",
                    "row_bytes": R, "batches": B, "seeds_per_batch": cfg.S, "fanouts": fan,
@@ -943,6 +942,34 @@ def experiment_regime(dg, w, cfg, reps, groups=16):
             "packed_rows_over_N": {"first_group": round(packed_rows[0] / N, 4),
                                    "all_groups": round(sum(packed_rows) / N, 4)},
             "cache_rows": int(w.cache_nodes.numel())}
+
+
+def device_info(dev) -> dict:
+    """The GPU, the ROCm and HIP versions, and its peak engine and memory clocks
+    (the HIP runtime's device attributes; None where unavailable)."""
+    import ctypes
+
+    import torch
+    props = torch.cuda.get_device_properties(dev)
+    info = {"name": torch.cuda.get_device_name(dev), "arch": props.gcnArchName,
+            "compute_units": props.multi_processor_count, "hip": torch.version.hip,
+            "rocm": None, "peak_sclk_mhz": None, "peak_mclk_mhz": None}
+    try:
+        with open("/opt/rocm/.info/version") as f:
+            info["rocm"] = f.read().strip()
+    except OSError:
+        pass
+    try:
+        hip = ctypes.CDLL("libamdhip64.so")
+        idx = torch.device(dev).index or 0
+        # hipDeviceAttributeClockRate = 5, hipDeviceAttributeMemoryClockRate = 60 (kHz)
+        for key, attr in (("peak_sclk_mhz", 5), ("peak_mclk_mhz", 60)):
+            v = ctypes.c_int(0)
+            if hip.hipDeviceGetAttribute(ctypes.byref(v), attr, idx) == 0:
+                info[key] = v.value // 1000
+    except OSError:
+        pass
+    return info
 
 
 def cpu_model() -> str:
