@@ -330,6 +330,7 @@ def main():
     lines = (None if args.no_member_lines else
              torch.empty(dg.member_lines_bytes(cfg.n), dtype=torch.uint8, device=dev))
     samp_phases = {False: [], True: []}  # per region, with --sample-timing
+    call_phases = []  # the library's phase times of each timed serial call
 
     def run(gs, pipelined, record):
         """One step per group index in gs; returns per-step host marks, gather
@@ -402,6 +403,7 @@ def main():
                                             ("packed_rows", "unique_nodes", "unique_packed")}})
             if record:
                 gather_ms.append(p_out.timing["gather_ms"])
+                call_phases.append(dict(p_out.timing))
         if asm_thread is not None:
             asm_thread.drain()
         torch.cuda.synchronize()
@@ -557,6 +559,14 @@ def main():
                       "assemble_all_batches": round(float(np.mean(asm_ms)), 3),
                       "host_enqueue_assembly": round(
                           1e3 * float(np.mean([m[2] for m in marks])), 3)},
+        "call_phases_ms": {
+            "what": ("the library's HIP-event phases of each timed serial call, median: draws "
+                     "(all hops), compaction (with one call, the last hop's pass also does "
+                     "packing's), relabelling, packing's own passes (two calls, or where they "
+                     "are not fused), address tables, row copy"),
+            **{k.replace("_ms", ""): round(_median([t[k] for t in call_phases]), 3)
+               for k in ("sample_ms", "dedup_ms", "relabel_ms", "mark_ms", "order_ms",
+                         "loc_ms", "gather_ms", "total_ms")}} if call_phases else None,
         "phase_gbps": {**({} if fused else
                           {"pack_call": round(F_pack_s / (np.sum(pack_ms) * 1e-3) / 1e9, 1)}),
                        "assemble_calls": round(F_asm_s / (np.sum(asm_ms) * 1e-3) / 1e9, 1)},
