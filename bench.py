@@ -400,7 +400,10 @@ def main():
                 evs.append(e0.elapsed_time(e1))
             marks.append((t1 - t0, t2 - t1, t3 - t2))
             steps.append({**s_out.sizes, **{k_: p_out.sizes[k_] for k_ in
-                                            ("packed_rows", "unique_nodes", "unique_packed")}})
+                                            ("packed_rows", "unique_nodes", "unique_packed")},
+                          # frontier entries over all hops: the nodes listed before
+                          # the last hop's segment
+                          "frontier": int(s_out.hop_ptr[:, len(fan)].sum())})
             if record:
                 gather_ms.append(p_out.timing["gather_ms"])
                 call_phases.append(dict(p_out.timing))
@@ -567,6 +570,17 @@ def main():
             **{k.replace("_ms", ""): round(_median([t[k] for t in call_phases]), 3)
                for k in ("sample_ms", "dedup_ms", "relabel_ms", "mark_ms", "order_ms",
                          "loc_ms", "gather_ms", "total_ms")}} if call_phases else None,
+        "implied_line_rate": ({
+            "what": ("64-byte lines the draw phase touches at random: one CSR index line and "
+                     "one membership-word line per sampled edge, one offsets line per frontier "
+                     "entry; over the draw phase's own time (the library's HIP events, median "
+                     "of the timed serial calls)"),
+            "lines_per_step": int(np.median([2 * st["total_edges"] + st["frontier"]
+                                             for st in steps_s])),
+            "lines_per_s": round(np.median([2 * st["total_edges"] + st["frontier"]
+                                            for st in steps_s])
+                                 / (_median([t["sample_ms"] for t in call_phases]) * 1e-3),
+                                 1)} if call_phases and fused else None),
         "phase_gbps": {**({} if fused else
                           {"pack_call": round(F_pack_s / (np.sum(pack_ms) * 1e-3) / 1e9, 1)}),
                        "assemble_calls": round(F_asm_s / (np.sum(asm_ms) * 1e-3) / 1e9, 1)},
