@@ -15,8 +15,9 @@ with the oracle's packing of those same lists.  M1 also compares feature rows
 with the oracle's own copies; at full size (L100, W120, H65 at every cache
 share) every packed and every assembled row is checked on the device against
 an independent library gather (torch.index_select) of the feature table.
-L100, H65 and M1 relabel through the direct [N][B] table (as bench.py does),
-W120 through the hash table.  L100 and M1 are also sampled with layer-wise
+L100, H65 and M1 relabel through the direct [N][B] table (as bench.py does);
+W120 runs the three through the hash table, then once more in one call with the
+direct table, as bench.py runs it.  L100 and M1 are also sampled with layer-wise
 frontiers and compared with the oracle batch by batch."""
 import numpy as np
 import pytest
@@ -190,6 +191,57 @@ def run_and_check(dg, orc, w, ref, direct=True):
     return sr3, pr3
 
 
+def one_call_check(dg, orc, w, ref):
+    """The group in one dg_sample_pack_group call with the direct table (so
+    that the last hop's compaction does packing's pass), the row copy on a
+    second stream, garbage in every output and in the membership words (the
+    call told nothing about their state): every batch's sample against the
+    oracle's (ref), the packing tables against the oracle's packing, and every
+    packed and assembled row against a library gather of the feature table."""
+    cfg = w.cfg
+    fan = list(cfg.fanouts)
+    R = cfg.row_bytes
+    node_cap, edge_cap = dg.sample_bounds(cfg.n, w.num_edges, cfg.S, fan)
+    mem = torch.full((cfg.n,), -1, dtype=torch.int64, device=DEV)
+    refp = orc.pack_group(None, w.cache_slot.cpu().numpy(), ref["nodes"], rows=False,
+                          row_bytes=R)
+    rows, nu = refp["packed_rows"], refp["unique_nodes"]
+    out = dg.PackResult(packed=torch.zeros((rows, R), dtype=torch.uint8, device=DEV),
+                        packed_ids=torch.full((rows,), -7, dtype=torch.int32, device=DEV),
+                        packed_ptr=torch.full((cfg.B + 1,), -7, dtype=torch.int64, device=DEV),
+                        packed_ptr_host=np.zeros(cfg.B + 1, dtype=np.int64),
+                        loc=torch.full((cfg.B, node_cap), -3, dtype=torch.int32, device=DEV),
+                        unique=torch.full((nu,), -7, dtype=torch.int32, device=DEV), sizes={},
+                        timing=None, row_bytes=R)
+    side = torch.cuda.Stream(device=DEV)
+    sr, pr = dg.sample_pack_group(w.offsets, w.indices, w.seeds, fan, w.rng_seed, w.feats,
+                                  w.cache_slot, node_cap=node_cap, edge_cap=edge_cap,
+                                  pack_out=out, rows_stream=side, membership=mem, direct=True,
+                                  exit_clear=True)
+    side.synchronize()
+    torch.cuda.synchronize()
+    assert int(mem.count_nonzero()) == 0
+    compare_samples(sr, ref, cfg.B)
+    assert pr.sizes["packed_rows"] == rows and pr.sizes["unique_nodes"] == nu
+    assert pr.sizes["unique_packed"] == refp["unique_packed"]
+    assert np.array_equal(pr.packed_ptr_host, refp["packed_ptr"])
+    assert np.array_equal(pr.packed_ptr.cpu().numpy(), refp["packed_ptr"])
+    assert np.array_equal(pr.packed_ids.cpu().numpy(), refp["packed_ids"])
+    assert np.array_equal(pr.unique.cpu().numpy(), refp["unique"])
+    counts = sr.node_count
+    for b in range(cfg.B):
+        assert np.array_equal(pr.loc[b, :int(counts[b])].cpu().numpy(), refp["loc"][b]), b
+    check_rows_on_device(w.feats, pr.packed_ids, pr.packed.view(w.feats.dtype).reshape(rows, -1))
+    y = torch.empty((int(counts.max()), R), dtype=torch.uint8, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    for b in range(cfg.B):
+        n = int(counts[b])
+        dg.assemble_batch(w.cache, pr.chunk(b), pr.loc[b, :n], R, out=y, status=status)
+        check_rows_on_device(w.feats, sr.nodes[b, :n], y[:n].view(w.feats.dtype).reshape(n, -1))
+    assert int(status.item()) == 0
+    print(f"[{cfg.name}] one call with the direct table equal to the oracle", flush=True)
+
+
 def test_workload_M1_full(dg, orc):
     w = synth.make_workload("M1", device=DEV)
     sr, pr = run_and_check(dg, orc, w, oracle_sample(orc, w))
@@ -236,7 +288,11 @@ def test_workload_L100(dg, orc):
 @pytest.mark.timeout(900)
 def test_workload_W120(dg, orc):
     w = big("W120")
-    run_and_check(dg, orc, w, oracle_sample(orc, w), direct=False)
+    ref = oracle_sample(orc, w)
+    run_and_check(dg, orc, w, ref, direct=False)
+    torch.cuda.empty_cache()
+    # the benchmark's configuration for W120: direct table, one call
+    one_call_check(dg, orc, w, ref)
 
 
 @pytest.mark.big
