@@ -8,7 +8,9 @@ packing set, which packing completes.
 Every step takes a different seed group, so an output read or written by the
 wrong step would show up as a wrong row.  Each step assembles into buffers of
 its own, and all are checked against a library gather (torch.index_select) at
-the end."""
+the end.  The loop runs on M1 in both call forms, and on L100 at full size in
+the benchmark's exact form (one call per step, the assembly issued from a
+host thread of its own)."""
 import numpy as np
 import pytest
 import torch
@@ -108,6 +110,113 @@ def test_pipelined_steps_are_each_correct(dg, fused):
         dg.assemble_batches(w.cache, pr, counts, kept[k], status=status, stream=s_asm)
         asm_done[slot].record(s_asm)
         results.append((nodes, counts))
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    assert int(mem.count_nonzero()) == 0
+    for k, (nodes, counts) in enumerate(results):
+        for b in range(B):
+            n = int(counts[b])
+            ref = w.feats.index_select(0, nodes[b, :n].long()).view(torch.uint8).reshape(n, R)
+            assert torch.equal(kept[k][b][:n], ref), (k, b)
+
+
+@pytest.mark.big
+@pytest.mark.timeout(900)
+def test_pipelined_steps_full_size_L100(dg):
+    """The benchmark's own loop at full size (L100): one dg_sample_pack_group
+    call per step on the main thread with the row copy queued on the assembly
+    stream, two packing output sets and workspaces, the clearing flags, and each
+    step's dg_assemble_batches issued from a host thread of its own once that
+    step's packing is recorded.  Four steps, four distinct seed groups with
+    their own global batch numbers; every assembled row of every step is checked
+    against a library gather of the feature table."""
+    import queue
+    import threading
+
+    w = synth.make_workload("L100", device=DEV)
+    cfg = w.cfg
+    fan, B, R, steps = list(cfg.fanouts), cfg.B, cfg.row_bytes, 4
+    groups = [w.seeds] + [synth.seed_batches(cfg.n, 2 * B, cfg.S, cfg.seed, DEV,
+                                             offsets=w.offsets)[B:]]
+    groups += [synth.seed_batches(cfg.n, 4 * B, cfg.S, cfg.seed, DEV,
+                                  offsets=w.offsets)[k * B:(k + 1) * B] for k in (2, 3)]
+    node_cap, edge_cap = dg.sample_bounds(cfg.n, w.num_edges, cfg.S, fan)
+    ws_s = torch.empty(dg._L.dg_sample_workspace_bytes(cfg.n, B, node_cap, edge_cap,
+                                                       dg.sample_flags(direct=True)),
+                       dtype=torch.uint8, device=DEV)
+    ws_p = [torch.empty(dg._L.dg_sample_pack_workspace_bytes(cfg.n, B, node_cap),
+                        dtype=torch.uint8, device=DEV) for _ in range(2)]
+    mem = torch.empty(cfg.n, dtype=torch.int64, device=DEV)
+    # output capacity for the largest group, sized by a tables-only pass
+    rows_max, nmax = 0, 0
+    for k, g in enumerate(groups):
+        sr = dg.sample_group(w.offsets, w.indices, g, fan, w.rng_seed, batch_base=k * B,
+                             direct=True, workspace=ws_s, membership=mem, node_cap=node_cap,
+                             edge_cap=edge_cap)
+        pr = dg.pack_group(w.feats, w.cache_slot, sr.nodes, sr.node_count, tables_only=True,
+                           membership=mem)
+        rows_max = max(rows_max, pr.sizes["packed_rows"])
+        nmax = max(nmax, int(sr.node_count.max()))
+        del pr
+    sets = [dg.PackResult(packed=torch.empty((rows_max, R), dtype=torch.uint8, device=DEV),
+                          packed_ids=torch.empty(rows_max, dtype=torch.int32, device=DEV),
+                          packed_ptr=torch.empty(B + 1, dtype=torch.int64, device=DEV),
+                          packed_ptr_host=np.zeros(B + 1, dtype=np.int64),
+                          loc=torch.empty((B, node_cap), dtype=torch.int32, device=DEV),
+                          unique=None, sizes={}, timing=None, row_bytes=R) for _ in range(2)]
+    kept = [[torch.empty((nmax, R), dtype=torch.uint8, device=DEV) for _ in range(B)]
+            for _ in range(steps)]
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    s_asm = torch.cuda.Stream(device=DEV)
+    asm_done = [torch.cuda.Event(), torch.cuda.Event()]
+    pack_done = [torch.cuda.Event(), torch.cuda.Event()]
+    for e in asm_done + pack_done:
+        e.record(s_asm)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    free = [threading.Event(), threading.Event()]
+    for f in free:
+        f.set()
+    q, errors = queue.Queue(), []
+
+    def assembler():
+        while True:
+            item = q.get()
+            if item is None:
+                return
+            k, slot, pr, counts = item
+            try:
+                s_asm.wait_event(pack_done[slot])
+                dg.assemble_batches(w.cache, pr, counts, kept[k], status=status, stream=s_asm)
+                asm_done[slot].record(s_asm)
+            except Exception as e:  # reported by the main thread
+                errors.append(e)
+            finally:
+                free[slot].set()
+
+    t = threading.Thread(target=assembler, daemon=True)
+    t.start()
+    results = []
+    for k in range(steps):
+        slot = k & 1
+        print(f"[pipeline L100] step {k}", flush=True)
+        free[slot].wait()
+        free[slot].clear()
+        stream.wait_event(asm_done[slot])
+        sr, pr = dg.sample_pack_group(w.offsets, w.indices, groups[k], fan, w.rng_seed,
+                                      w.feats, w.cache_slot, batch_base=k * B,
+                                      node_cap=node_cap, edge_cap=edge_cap, pack_out=sets[slot],
+                                      workspace=ws_s, pack_workspace=ws_p[slot], stream=stream,
+                                      rows_stream=s_asm, membership=mem, direct=True,
+                                      exit_clear=True, entry_clear=k > 0)
+        counts = sr.node_count.copy()
+        results.append((sr.nodes.clone(), counts))  # the next step overwrites sr.nodes
+        pack_done[slot].record(stream)
+        q.put((k, slot, pr, counts))
+    q.put(None)
+    t.join(timeout=300)
+    assert not t.is_alive() and not errors, errors
     torch.cuda.synchronize()
     assert int(status.item()) == 0
     assert int(mem.count_nonzero()) == 0
