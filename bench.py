@@ -619,7 +619,7 @@ def main():
             for name, v in (("serial", samp_phases[False]), ("pipelined", samp_phases[True]))
             if v}
     if not args.no_ceiling:
-        # what a plain copy of rows reaches on this box, outside the timed
+        # what a plain copy of rows reaches on this machine, outside the timed
         # regions: the row kernels' fraction of 8 TB/s is read against it
         c = experiment_ceiling(dg, w, cfg, 3)
         out["row_copy_ceiling"] = {
