@@ -6,7 +6,9 @@ import ctypes
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libdg.so")
+# DG_LIB_PATH: another build of the same library (the host-sanitizer tests
+# load one); by default the in-tree build.
+LIB_PATH = os.environ.get("DG_LIB_PATH") or os.path.join(_HERE, "libdg.so")
 
 DG_OK, DG_EINVAL, DG_ECAPACITY, DG_EHIP, DG_EWORKSPACE = 0, -1, -2, -3, -4
 DG_SAMPLE_LAYERED = 1
