@@ -213,8 +213,9 @@ const char *dg_last_error(void);
  * sample next); with it, F_k = the node bound so far (every node samples).  A
  * negative fan-out counts as E edges; node bounds are capped at N.  For the
  * default mode this gives n_b <= min(N, S*(1 + f1 + f1*f2 + ...)).  Capacities
- * this large never trigger DG_ECAPACITY.  Returns DG_EINVAL on a null pointer,
- * S < 1, K < 0, num_nodes < 1 or unknown flags. */
+ * this large never trigger DG_ECAPACITY.  `flags` may be the whole flags word
+ * of the sampling call: only DG_SAMPLE_LAYERED changes the bounds.  Returns
+ * DG_EINVAL on a null pointer, S < 1, K < 0, num_nodes < 1 or unknown flags. */
 int dg_sample_bounds(int64_t num_nodes, int64_t num_edges, int32_t S,
                      const int32_t *fanouts /*[host] K*/, int32_t K, uint32_t flags,
                      int64_t *node_cap /*[host] out*/, int64_t *edge_cap /*[host] out*/);

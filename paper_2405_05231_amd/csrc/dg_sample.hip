@@ -534,7 +534,7 @@ extern "C" int dg_sample_bounds(int64_t num_nodes, int64_t num_edges, int32_t S,
                                 const int32_t *fanouts, int32_t K, uint32_t flags,
                                 int64_t *node_cap, int64_t *edge_cap) {
   if (!node_cap || !edge_cap || (K > 0 && !fanouts) || S < 1 || K < 0 || num_nodes < 1 ||
-      num_edges < 0 || (flags & ~DG_SAMPLE_LAYERED))
+      num_edges < 0 || (flags & ~SAMPLE_FLAGS))
     return set_error(DG_EINVAL, "dg_sample_bounds: bad argument");
   const bool layered = flags & DG_SAMPLE_LAYERED;
   // Saturating arithmetic: once a count reaches its graph bound it stays there.

@@ -58,6 +58,21 @@ def test_sample_bounds(L):
     assert dg.sample_bounds(1000, 5000, 4, [-1, 2], layered=True) == (1000, 7000)
     with pytest.raises(dg.DGError):
         dg.sample_bounds(0, 10, 1, [1])
+    # the sampling call's whole flags word is accepted; only LAYERED changes
+    # the bounds, and unknown bits are rejected
+    import ctypes
+    from paper_2405_05231_amd import _lib
+    fo = (ctypes.c_int32 * 2)(2, 3)
+    nc, ec = ctypes.c_int64(), ctypes.c_int64()
+    for flags, want in ((_lib.DG_SAMPLE_DIRECT | _lib.DG_SAMPLE_EXIT_CLEAR
+                         | _lib.DG_SAMPLE_ENTRY_CLEAR, dg.sample_bounds(10**6, 10**9, 4, [2, 3])),
+                        (_lib.DG_SAMPLE_LAYERED | _lib.DG_SAMPLE_DIRECT,
+                         dg.sample_bounds(10**6, 10**9, 4, [2, 3], layered=True))):
+        assert L.dg_sample_bounds(10**6, 10**9, 4, fo, 2, flags, ctypes.byref(nc),
+                                  ctypes.byref(ec)) == 0
+        assert (nc.value, ec.value) == want
+    assert L.dg_sample_bounds(10**6, 10**9, 4, fo, 2, 1 << 20, ctypes.byref(nc),
+                              ctypes.byref(ec)) == -1
 
 
 def test_workspace_queries(L):
