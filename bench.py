@@ -562,6 +562,14 @@ def main():
                       "assemble_all_batches": round(float(np.mean(asm_ms)), 3),
                       "host_enqueue_assembly": round(
                           1e3 * float(np.mean([m[2] for m in marks])), 3)},
+        "paper_context": {
+            "what": ("the paper gives no kernel-level figure for this path (so vs_baseline is "
+                     "null); its whole pre-processing of ogbn-papers100M (cache configuration "
+                     "and batched packing, 52.9 GB of fp32 features) took about 0.03 h (Tables "
+                     "1 and 2), which puts it near 0.5 GB/s (derived), bound by an NVMe SSD of "
+                     "3 GB/s on an AMD EPYC 7R32 host with one NVIDIA A10G (the platform of "
+                     "§7, Table 4)"),
+            "preprocessing_GBps": 0.5},
         "call_phases_ms": {
             "what": ("the library's HIP-event phases of each timed serial call, median: draws "
                      "(all hops), compaction (with one call, the last hop's pass also does "
