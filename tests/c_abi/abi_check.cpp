@@ -13,7 +13,9 @@
 //    the feature row of its node; the address tables point at the right cache
 //    or packed row; each assembled row equals the feature row of its node;
 //  - the membership words are left all-zero, and a null argument is rejected
-//    with DG_EINVAL and a message.
+//    with DG_EINVAL and a message;
+//  - dg_sample_group followed by dg_pack_group (the two calls the one call
+//    stands for) gives the same outputs on new buffers.
 // Exit status 0 when every check holds.
 #include <hip/hip_runtime.h>
 
@@ -291,6 +293,62 @@ int main() {
         "|U| %lld / %zu, |U_nc| %lld / %zu", (long long)sz.unique_nodes, U.size(),
         (long long)sz.unique_packed, U_nc.size());
   CHECK(std::vector<int32_t>(U.begin(), U.end()) == uniq, "group_unique is not U, ascending");
+
+  // The same group by the two calls the one call stands for: dg_sample_group
+  // (membership words and the cached nodes' address-table entries) followed by
+  // dg_pack_group (clearing the words, completing the pending entries), on new
+  // buffers; every output must equal the one call's.
+  {
+    const size_t ws2_bytes = dg_sample_workspace_bytes(N, B, node_cap, edge_cap, DG_SAMPLE_DIRECT);
+    const size_t pws2_bytes = dg_pack_workspace_bytes(N, B, pairs);
+    int32_t *n2 = dev_alloc<int32_t>((size_t)B * node_cap);
+    int32_t *es2 = dev_alloc<int32_t>((size_t)B * edge_cap), *ed2 = dev_alloc<int32_t>((size_t)B * edge_cap);
+    int32_t *loc2 = dev_alloc<int32_t>((size_t)B * node_cap);
+    uint8_t *pk2 = dev_alloc<uint8_t>((size_t)rows * R);
+    int32_t *pid2 = dev_alloc<int32_t>(rows), *uq2 = dev_alloc<int32_t>(nu);
+    int64_t *pp2 = dev_alloc<int64_t>(B + 1);
+    void *ws2 = dev_alloc<uint8_t>(ws2_bytes), *pws2 = dev_alloc<uint8_t>(pws2_bytes);
+    if (!n2 || !es2 || !ed2 || !loc2 || !pk2 || !pid2 || !uq2 || !pp2 || !ws2 || !pws2 ||
+        ws2_bytes == 0 || pws2_bytes == 0) {
+      std::fprintf(stderr, "two-call buffers: allocation or query failed\n");
+      return 2;
+    }
+    std::vector<int64_t> hp2((size_t)B * (K + 2)), ep2((size_t)B * (K + 1)), pph2(B + 1);
+    dg_sizes s2, p2;
+    rc = dg_sample_group(&g, d_seeds, B, S, 0, fan, K, 7, DG_SAMPLE_DIRECT, node_cap, n2,
+                         hp2.data(), edge_cap, es2, ed2, ep2.data(), d_mem, nullptr, d_slot, loc2,
+                         ws2, ws2_bytes, st, &s2, nullptr);
+    CHECK(rc == DG_OK, "dg_sample_group: status %d: %s", rc, dg_last_error());
+    rc = dg_pack_group(d_X, N, R, d_slot, B, n2, node_cap, counts.data(), rows, pk2, pid2, pp2,
+                       pph2.data(), loc2, uq2, nu, d_mem, nullptr, nullptr, 0, nullptr,
+                       DG_PACK_CLEAR_MEMBERSHIP | DG_PACK_LOC_PENDING, pws2, pws2_bytes, st,
+                       nullptr, &p2, nullptr);
+    CHECK(rc == DG_OK, "dg_pack_group: status %d: %s", rc, dg_last_error());
+    HIP_OK(hipStreamSynchronize(st));
+    CHECK(hp2 == hop_ptr && ep2 == edge_ptr && pph2 == pptr_host, "two calls: bounds differ");
+    CHECK(p2.packed_rows == rows && p2.unique_nodes == nu && p2.unique_packed == sz.unique_packed,
+          "two calls: packing sizes differ");
+    auto same = [&](const void *d, const void *h, size_t bytes) {
+      std::vector<uint8_t> t(bytes);
+      if (hipMemcpy(t.data(), d, bytes, hipMemcpyDeviceToHost) != hipSuccess) return false;
+      return bytes == 0 || std::memcmp(t.data(), h, bytes) == 0;
+    };
+    for (int b = 0; b < B; ++b) {
+      const int64_t n = counts[b], e = edge_ptr[(size_t)b * (K + 1) + K];
+      const size_t o = (size_t)b * node_cap, oe = (size_t)b * edge_cap;
+      CHECK(same(n2 + o, &nodes[o], (size_t)n * 4), "two calls: batch %d nodes differ", b);
+      CHECK(same(loc2 + o, &loc[o], (size_t)n * 4), "two calls: batch %d loc differs", b);
+      CHECK(same(es2 + oe, &esrc[oe], (size_t)e * 4) && same(ed2 + oe, &edst[oe], (size_t)e * 4),
+            "two calls: batch %d edges differ", b);
+    }
+    CHECK(same(pid2, pids.data(), (size_t)rows * 4) && same(uq2, uniq.data(), (size_t)nu * 4),
+          "two calls: packed_ids or U differ");
+    CHECK(same(pk2, packed.data(), (size_t)rows * R), "two calls: packed rows differ");
+    std::vector<uint64_t> m2(N);
+    HIP_OK(hipMemcpy(m2.data(), d_mem, (size_t)N * 8, hipMemcpyDeviceToHost));
+    CHECK(std::all_of(m2.begin(), m2.end(), [](uint64_t w) { return w == 0; }),
+          "two calls: membership words not left all-zero");
+  }
 
   // a null argument is rejected before any work, with a message
   rc = dg_sample_pack_group(&g, nullptr, B, S, 0, fan, K, 7, DG_SAMPLE_DIRECT, node_cap, d_nodes,

@@ -4,7 +4,8 @@ The program samples, packs and assembles one group and checks, on the host,
 what the header's contract fixes for any input: the frontier rule hop by hop,
 each edge against the CSR graph, the fan-out counts and draw order, P_b, every
 packed and assembled row, the address tables, U, the sizes, the membership
-words left clear, and a null argument rejected.  It is built by
+words left clear, and a null argument rejected; and the two calls the one call
+stands for (dg_sample_group, then dg_pack_group) give the same outputs.  It is built by
 __graft_entry__.build() (python tests/c_abi/build.py builds it alone)."""
 import os
 import subprocess
