@@ -272,7 +272,7 @@ def main():
         """Issues each pipelined step's assembly from a host thread of its own,
         as the trainer stage of the paper's pipeline (§5.3) consumes assembled
         batches while the next group is sampled: the main thread goes on to
-        the next sampling call while the B launches are enqueued.  Steps are
+        the next sampling call while the assembly launches are enqueued.  Steps are
         handed over in order; a packing output set (slot) is packed again only
         after the assembly that reads it has been enqueued."""
 
@@ -464,11 +464,14 @@ def main():
     # HIP events on the call's stream (serial region)
     g_ms = float(np.mean(gather_ms))
     achieved = F_pack_s / (sum(gather_ms) * 1e-3) / 1e9
-    # assembly: one k_assemble16 launch per mini-batch; its average launch time
-    # is the steps' assembly time (HIP events on its stream, serial region)
-    # over the K*B launches, and its bytes the steps' assembly bytes over them
-    a_ms = float(np.sum(asm_ms)) / (args.steps * B)
-    F_asm_launch = F_asm_s / (args.steps * B)
+    # assembly: dg_assemble_batches runs two consecutive mini-batches (with
+    # output buffers of their own, ybuf[0] and ybuf[1]) per k_assemble16_group
+    # launch; its average launch time is the steps' assembly time (HIP events
+    # on its stream, serial region) over the launches, and its bytes the
+    # steps' assembly bytes over them
+    asm_launches = (B + 1) // 2
+    a_ms = float(np.sum(asm_ms)) / (args.steps * asm_launches)
+    F_asm_launch = F_asm_s / (args.steps * asm_launches)
     achieved_asm = F_asm_launch / (a_ms * 1e-3) / 1e9
     edges = sum(st["total_edges"] for st in steps_s)
     sizes_rep = steps_r[0]
@@ -508,7 +511,8 @@ def main():
                       "assembly of step k (second stream) overlaps sampling and packing of "
                       "step k+1; the serial figures below wait for each step's assembly"),
         "packing_sets": n_sets,
-        "assembly_issue": ("direct calls: one dg_assemble_batches call (B launches) per step, "
+        "assembly_issue": ("direct calls: one dg_assemble_batches call (B/2 launches of two "
+                           "mini-batches) per step, "
                            + ("issued by the main thread" if asm_thread is None else
                               "issued by a host thread of its own in the pipelined region "
                               "(the trainer side), by the main thread in the serial region")),
@@ -595,13 +599,13 @@ def main():
         "sizes": {k: span(k, steps_p) for k in
                   ("total_nodes", "total_edges", "packed_rows", "unique_nodes",
                    "unique_packed")},
-        # the dominant kernel by time: batch assembly (B launches per step)
-        "roofline": {"kernel": "k_assemble16 (batch assembly, one launch per mini-batch)",
+        # the dominant kernel by time: batch assembly (B/2 launches per step)
+        "roofline": {"kernel": "k_assemble16_group (batch assembly, two mini-batches per launch)",
                      "bound": "hbm", "achieved": round(achieved_asm, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved_asm / HBM_PEAK_GBPS, 4),
                      "traffic": load_traffic(cfg.name, "assemble"),
                      "algorithmic_bytes": int(round(F_asm_launch)),
-                     "launch_ms": round(a_ms, 4), "launches_per_step": B},
+                     "launch_ms": round(a_ms, 4), "launches_per_step": asm_launches},
         # the other row kernel: packing's fan-out gather (one launch per step)
         "roofline_fanout": {"kernel": "k_fanout16 (fan-out gather)", "bound": "hbm",
                             "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,

@@ -24,16 +24,17 @@ __device__ __forceinline__ const char *row_source(int32_t l, const char *cache, 
   return nullptr;
 }
 
+// The rows of one batch handled by virtual block `blk` of `nblk`.
 template <int LPR, int CPL>
-__global__ __launch_bounds__(THREADS) void k_assemble16(const v4u *cache, int64_t cache_rows,
-                                                        const v4u *packed, int64_t packed_rows,
-                                                        const int32_t *loc, int64_t n, int C,
-                                                        v4u *out, int32_t *status) {
+__device__ __forceinline__ void assemble16_rows(const v4u *cache, int64_t cache_rows,
+                                                const v4u *packed, int64_t packed_rows,
+                                                const int32_t *loc, int64_t n, int C, v4u *out,
+                                                int32_t *status, int64_t blk, int64_t nblk) {
   constexpr int UNROLL = rows_in_flight(CPL);
   constexpr int GPB = THREADS / LPR;  // row groups per block
   const int sub = threadIdx.x % LPR;
-  const int64_t grp = (int64_t)blockIdx.x * GPB + threadIdx.x / LPR;
-  const int64_t ngrp = (int64_t)gridDim.x * GPB;
+  const int64_t grp = blk * GPB + threadIdx.x / LPR;
+  const int64_t ngrp = nblk * GPB;
   for (int64_t j0 = grp * UNROLL; j0 < n; j0 += ngrp * UNROLL) {
     // Every load below is unconditional, at an address that is always valid,
     // and what is not needed is discarded afterwards: with no branch between
@@ -81,6 +82,42 @@ __global__ __launch_bounds__(THREADS) void k_assemble16(const v4u *cache, int64_
       }
     }
   }
+}
+
+template <int LPR, int CPL>
+__global__ __launch_bounds__(THREADS) void k_assemble16(const v4u *cache, int64_t cache_rows,
+                                                        const v4u *packed, int64_t packed_rows,
+                                                        const int32_t *loc, int64_t n, int C,
+                                                        v4u *out, int32_t *status) {
+  assemble16_rows<LPR, CPL>(cache, cache_rows, packed, packed_rows, loc, n, C, out, status,
+                            blockIdx.x, gridDim.x);
+}
+
+// Several batches in one launch (each with an output buffer of its own): the
+// blocks of batch q are block0[q] .. block0[q+1) - 1, each batch run exactly as
+// its own launch would run it.
+constexpr int ASM_GROUP = 2;
+struct AsmGroup {
+  int G;
+  int64_t block0[ASM_GROUP + 1];
+  const v4u *packed[ASM_GROUP];
+  int64_t packed_rows[ASM_GROUP];
+  const int32_t *loc[ASM_GROUP];
+  int64_t n[ASM_GROUP];
+  v4u *out[ASM_GROUP];
+};
+
+template <int LPR, int CPL>
+__global__ __launch_bounds__(THREADS) void k_assemble16_group(AsmGroup g, const v4u *cache,
+                                                              int64_t cache_rows, int C,
+                                                              int32_t *status) {
+  int q = 0;
+#pragma unroll
+  for (int k = 1; k < ASM_GROUP; ++k)
+    if (k < g.G && (int64_t)blockIdx.x >= g.block0[k]) q = k;
+  assemble16_rows<LPR, CPL>(cache, cache_rows, g.packed[q], g.packed_rows[q], g.loc[q], g.n[q],
+                            C, g.out[q], status, (int64_t)blockIdx.x - g.block0[q],
+                            g.block0[q + 1] - g.block0[q]);
 }
 
 // Any row size / alignment: one wave per row, words of sizeof(T).
@@ -134,6 +171,76 @@ bool overlaps(const void *a, int64_t an, const void *b, int64_t bn) {
   if (!a || !b || an <= 0 || bn <= 0) return false;
   uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
   return x < y + (uintptr_t)bn && y < x + (uintptr_t)an;
+}
+
+// One batch's arguments, as dg_assemble_batch takes them.
+struct AsmArgs {
+  const void *packed;
+  int64_t packed_rows;
+  const int32_t *loc;
+  int64_t n;
+  void *out;
+};
+
+// dg_assemble_batch's argument checks (n == 0 passes: nothing to do).
+int check_batch(const void *cache, int64_t cache_rows, const AsmArgs &a, int64_t row_bytes) {
+  if (a.n < 0 || row_bytes < 1 || cache_rows < 0 || a.packed_rows < 0)
+    return set_error(DG_EINVAL, "dg_assemble_batch: bad sizes");
+  if (a.n == 0) return DG_OK;
+  if (!a.loc || !a.out || (cache_rows > 0 && !cache) || (a.packed_rows > 0 && !a.packed))
+    return set_error(DG_EINVAL, "dg_assemble_batch: null pointer argument");
+  const int64_t out_bytes = a.n * row_bytes;
+  if (overlaps(a.out, out_bytes, cache, cache_rows * row_bytes) ||
+      overlaps(a.out, out_bytes, a.packed, a.packed_rows * row_bytes) ||
+      overlaps(a.out, out_bytes, a.loc, a.n * 4))
+    return set_error(DG_EINVAL, "dg_assemble_batch: output overlaps an input");
+  return DG_OK;
+}
+
+// The 16-byte row shape a batch runs with, if it takes that path.
+bool shape16(const void *cache, const AsmArgs &a, int64_t row_bytes, RowShape *sh) {
+  return word_bytes(row_bytes, {cache, a.packed, a.out}) == 16 && row_shape16(row_bytes / 16, sh);
+}
+
+template <int LPR, int CPL>
+int64_t blocks16(int64_t n) {
+  constexpr int GPB = THREADS / LPR;
+  constexpr int UNROLL = rows_in_flight(CPL);
+  const int64_t groups = (n + UNROLL - 1) / UNROLL;
+  const int64_t blocks = (groups + GPB - 1) / GPB;
+  return blocks > (1ll << 20) ? (1ll << 20) : blocks;
+}
+
+template <int LPR, int CPL>
+int launch16_group(const void *cache, int64_t cache_rows, const AsmArgs *a, int G, int C,
+                   int32_t *status, hipStream_t s) {
+  AsmGroup g{};
+  g.G = G;
+  g.block0[0] = 0;
+  for (int q = 0; q < G; ++q) {
+    g.packed[q] = (const v4u *)a[q].packed;
+    g.packed_rows[q] = a[q].packed_rows;
+    g.loc[q] = a[q].loc;
+    g.n[q] = a[q].n;
+    g.out[q] = (v4u *)a[q].out;
+    g.block0[q + 1] = g.block0[q] + blocks16<LPR, CPL>(a[q].n);
+  }
+  hipLaunchKernelGGL((k_assemble16_group<LPR, CPL>), dim3((unsigned)g.block0[G]), dim3(THREADS),
+                     0, s, g, (const v4u *)cache, cache_rows, C, status);
+  DG_HIP(hipGetLastError());
+  return DG_OK;
+}
+
+int launch_group(const void *cache, int64_t cache_rows, const AsmArgs *a, int G,
+                 int64_t row_bytes, const RowShape &sh, int32_t *status, hipStream_t s) {
+  const int C = (int)(row_bytes / 16);
+  if (sh.lpr == 4) return launch16_group<4, 1>(cache, cache_rows, a, G, C, status, s);
+  if (sh.lpr == 8) return launch16_group<8, 1>(cache, cache_rows, a, G, C, status, s);
+  if (sh.lpr == 16) return launch16_group<16, 1>(cache, cache_rows, a, G, C, status, s);
+  if (sh.lpr == 32 && sh.cpl == 1) return launch16_group<32, 1>(cache, cache_rows, a, G, C, status, s);
+  if (sh.lpr == 64 && sh.cpl == 1) return launch16_group<64, 1>(cache, cache_rows, a, G, C, status, s);
+  if (sh.lpr == 64 && sh.cpl == 2) return launch16_group<64, 2>(cache, cache_rows, a, G, C, status, s);
+  return launch16_group<64, 4>(cache, cache_rows, a, G, C, status, s);
 }
 
 }  // namespace
@@ -191,15 +298,52 @@ extern "C" int dg_assemble_batches(const void *cache, int64_t cache_rows, const 
     if (p0 < 0 || p1 < p0 || n < 0 || n > loc_stride)
       return set_error(DG_EINVAL, "dg_assemble_batches: batch %d: bad chunk bounds or n_b", b);
   }
-  for (int32_t b = 0; b < B; ++b) {
+  // Consecutive batches with output buffers of their own (outs[b % n_outs]
+  // distinct and apart) share one launch, up to ASM_GROUP of them, when they
+  // take the 16-byte path: each batch is still checked as dg_assemble_batch
+  // checks it, in batch order, before its launch.
+  auto args_of = [&](int32_t b) {
     const int64_t p0 = packed_ptr_host[b], p1 = packed_ptr_host[b + 1];
-    const int64_t n = node_count[b];
-    const char *pb = (p1 > p0 && packed) ? static_cast<const char *>(packed) + p0 * row_bytes
-                                          : nullptr;
-    const int rc = dg_assemble_batch(cache, cache_rows, pb, p1 - p0,
-                                     loc ? loc + (int64_t)b * loc_stride : nullptr, n, row_bytes,
-                                     outs[b % n_outs], status, stream);
+    AsmArgs a;
+    a.packed = (p1 > p0 && packed) ? static_cast<const char *>(packed) + p0 * row_bytes : nullptr;
+    a.packed_rows = p1 - p0;
+    a.loc = loc ? loc + (int64_t)b * loc_stride : nullptr;
+    a.n = node_count[b];
+    a.out = outs[b % n_outs];
+    return a;
+  };
+  for (int32_t b = 0; b < B;) {
+    AsmArgs a[ASM_GROUP];
+    a[0] = args_of(b);
+    int rc = check_batch(cache, cache_rows, a[0], row_bytes);
     if (rc != DG_OK) return rc;
+    RowShape sh{};
+    int G = 1;
+    if (a[0].n > 0 && shape16(cache, a[0], row_bytes, &sh)) {
+      while (G < ASM_GROUP && G < n_outs && b + G < B) {
+        const AsmArgs c = args_of(b + G);
+        RowShape sc{};
+        bool apart = c.n > 0 && shape16(cache, c, row_bytes, &sc) && sc.lpr == sh.lpr &&
+                     sc.cpl == sh.cpl;
+        for (int q = 0; apart && q < G; ++q)
+          apart = !overlaps(c.out, c.n * row_bytes, a[q].out, a[q].n * row_bytes) &&
+                  !overlaps(c.out, c.n * row_bytes, a[q].loc, a[q].n * 4) &&
+                  !overlaps(c.out, c.n * row_bytes, a[q].packed, a[q].packed_rows * row_bytes) &&
+                  !overlaps(a[q].out, a[q].n * row_bytes, c.loc, c.n * 4) &&
+                  !overlaps(a[q].out, a[q].n * row_bytes, c.packed, c.packed_rows * row_bytes);
+        if (!apart || check_batch(cache, cache_rows, c, row_bytes) != DG_OK) break;
+        a[G++] = c;
+      }
+    }
+    if (G > 1) {
+      if ((rc = launch_group(cache, cache_rows, a, G, row_bytes, sh, status, stream)))
+        return rc;
+    } else {
+      rc = dg_assemble_batch(cache, cache_rows, a[0].packed, a[0].packed_rows, a[0].loc, a[0].n,
+                             row_bytes, a[0].out, status, stream);
+      if (rc != DG_OK) return rc;
+    }
+    b += G;
   }
   return DG_OK;
 }

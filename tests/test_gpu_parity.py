@@ -365,6 +365,51 @@ def test_assemble_batches_matches_per_batch_calls(dg):
         dg.assemble_batches(cache, pr, counts, [outs[0][:1]])
 
 
+@pytest.mark.parametrize("dim", [16, 128, 384, 512, 1024])
+@pytest.mark.parametrize("outs_kind", ["one", "two", "same_twice", "all"])
+def test_assemble_batches_output_buffers(dg, dim, outs_kind):
+    """Batches whose output buffers are distinct may share a launch; the
+    result must still be that of the per-batch calls made in batch order, on
+    every 16-byte row shape (64 B to 4 KiB rows): with one buffer (each batch
+    overwrites the last), two buffers (batch b in buffer b % 2), the same
+    buffer given twice (no sharing possible), and a buffer per batch."""
+    w = synth.make_workload("T")
+    gen = torch.Generator().manual_seed(dim)
+    X = torch.randn((w.cfg.n, dim), generator=gen).to(DEV)
+    slot = w.cache_slot.to(DEV)
+    sr = dg.sample_group(w.offsets.to(DEV), w.indices.to(DEV), w.seeds.to(DEV),
+                         list(w.cfg.fanouts), w.rng_seed)
+    pr = dg.pack_group(X, slot, sr.nodes, sr.node_count)
+    cache = X.index_select(0, w.cache_nodes.to(DEV))
+    R = pr.row_bytes
+    counts = sr.node_count
+    B, nmax = len(counts), int(counts.max())
+    refs = [dg.assemble_batch(cache, pr.chunk(b), pr.loc[b, :int(counts[b])], R).clone()
+            for b in range(B)]
+    one = torch.full((nmax, R), 0xAB, dtype=torch.uint8, device=DEV)
+    if outs_kind == "one":
+        outs = [one]
+    elif outs_kind == "two":
+        outs = [one, torch.full((nmax, R), 0xAB, dtype=torch.uint8, device=DEV)]
+    elif outs_kind == "same_twice":
+        outs = [one, one]
+    else:
+        outs = [torch.full((nmax, R), 0xAB, dtype=torch.uint8, device=DEV) for _ in range(B)]
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    dg.assemble_batches(cache, pr, counts, outs, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    # each buffer holds the last batch written to it, over what earlier batches left
+    expect = [torch.full((nmax, R), 0xAB, dtype=torch.uint8, device=DEV) for _ in outs]
+    for b in range(B):
+        k = b % len(outs)
+        tgt = expect[0] if outs_kind == "same_twice" else expect[k]
+        tgt[:int(counts[b])] = refs[b]
+    for k, o in enumerate(outs):
+        want = expect[0] if outs_kind == "same_twice" else expect[k]
+        assert torch.equal(o, want), k
+
+
 @pytest.mark.parametrize("layered,direct,handoff", [(False, False, False), (True, True, False),
                                                     (False, True, True), (False, True, "fused")])
 def test_sparse_hops_on_a_large_graph(dg, orc, layered, direct, handoff):
