@@ -480,10 +480,10 @@ int dg_assemble_batch(const void *cache, int64_t cache_rows, const void *packed_
                       hipStream_t stream);
 
 /* dg_assemble_batch for batches 0..B-1 of one packing result, in batch order on
- * `stream`, issued by one call.  Two consecutive batches whose output buffers
- * are distinct and apart (and whose rows move as 16-byte vectors) share one
- * kernel launch; the outputs are those of the per-batch calls in batch order
- * either way.
+ * `stream`, issued by one call.  Up to four consecutive batches whose output
+ * buffers are distinct and apart (and whose rows move as 16-byte vectors) share
+ * one kernel launch; the outputs are those of the per-batch calls in batch
+ * order either way.
  *   packed, packed_ptr_host [host] [B+1]  the packed chunks and their bounds as
  *              dg_pack_group returned them (packed may be NULL if every chunk is
  *              empty).
