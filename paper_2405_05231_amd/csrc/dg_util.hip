@@ -580,12 +580,58 @@ int mask_scan_rows(MaskScan &m, hipStream_t s) {
   return DG_OK;
 }
 
+// 64 x 64 bit transpose across the wave: lane i holds row i (bit j is entry
+// (i, j)); on return lane j holds column j (bit i is entry (i, j)).  Each of
+// the six block-swap stages exchanges bit s of the row index with bit s of the
+// column index between lanes i and i ^ s: the stage across the wave halves by a
+// lane shuffle, the five within each half by ds_swizzle (xor mode) on the
+// 32-bit halves of the rows, which those stages never mix.
+template <int S>
+__device__ __forceinline__ uint32_t swizzle_xor(uint32_t v) {
+  static_assert(S >= 1 && S <= 16, "xor within 32 lanes");
+  return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, (S << 10) | 0x1f);
+}
+template <int S>
+__device__ __forceinline__ void transpose_stage(uint32_t &lo, uint32_t &hi, int lane) {
+  // positions whose bit S is clear, in each 32-bit half
+  constexpr uint32_t M0 = S == 16 ? 0x0000ffffu : S == 8 ? 0x00ff00ffu : S == 4 ? 0x0f0f0f0fu
+                        : S == 2 ? 0x33333333u : 0x55555555u;
+  const bool low = (lane & S) == 0;
+  const uint32_t plo = swizzle_xor<S>(lo), phi = swizzle_xor<S>(hi);
+  // low lane: keeps its M0 positions, takes the partner's M0 positions moved up
+  // by S; high lane: keeps its other positions, takes the partner's moved down
+  const uint32_t keep = low ? M0 : ~M0;
+  const uint32_t xlo = low ? plo << S : plo >> S;
+  const uint32_t xhi = low ? phi << S : phi >> S;
+  lo = (lo & keep) | (xlo & ~keep);
+  hi = (hi & keep) | (xhi & ~keep);
+}
+__device__ __forceinline__ uint64_t wave_transpose64(uint64_t r) {
+  const int lane = lane_id();
+  uint32_t lo = (uint32_t)r, hi = (uint32_t)(r >> 32);
+  {  // bit 5: the low lane of a pair takes its partner's low half as its high
+     // half, the high lane its partner's high half as its low half
+    const bool low = (lane & 32) == 0;
+    const uint32_t got = (uint32_t)__shfl_xor((int)(low ? hi : lo), 32, 64);
+    if (low) hi = got; else lo = got;
+  }
+  transpose_stage<16>(lo, hi, lane);
+  transpose_stage<8>(lo, hi, lane);
+  transpose_stage<4>(lo, hi, lane);
+  transpose_stage<2>(lo, hi, lane);
+  transpose_stage<1>(lo, hi, lane);
+  return ((uint64_t)hi << 32) | lo;
+}
+
 // Write pass, over the compact list of non-empty words the count pass left for
 // each wave (no second read of the mask).  Batch b's next rank is the block's
 // base from the row scan, plus the wave's prefix within the block, plus what
 // lane b has emitted so far.  Per-node outputs use ballot prefixes within a
-// chunk of 64 words; the (node, batch) pairs are emitted word by word in node
-// order (lane b handles bit b), so each batch's list comes out ascending.
+// chunk of 64 words.  For the (node, batch) pairs the chunk's words are
+// transposed, so that lane b holds the set of the chunk's words with bit b,
+// and lane b walks that set in node order (the words' node IDs, cache slots
+// and pair offsets staged in LDS): each batch's list comes out ascending, and
+// a lane's walk is as long as its batch's share of the chunk.
 //   PACK:  packing outputs (U, U_nc, pair offsets, pair destinations); cached
 //          nodes are left out of the per-batch lists.
 //   LOCAL: sampling, also recording each pair's local index in local_out.
@@ -595,6 +641,8 @@ int mask_scan_rows(MaskScan &m, hipStream_t s) {
 // of its own word before the pairs are emitted.
 template <bool PACK, bool LOCAL>
 __global__ __launch_bounds__(MC_THREADS) void k_mask_write(MaskScan a) {
+  __shared__ int4 s_word[MC_WAVES][64];  // node ID, cache slot, first pair (in the chunk)
+  __shared__ uint64_t s_nc[MC_WAVES][64];  // packing: the word's listed bits
   const int lane = lane_id(), w = threadIdx.x >> 6;
   const int B = a.B, rows = mc_rows(B);
   // Neighbouring blocks append to the same stretch of every batch's list: run
@@ -635,38 +683,44 @@ __global__ __launch_bounds__(MC_THREADS) void k_mask_write(MaskScan a) {
       if (sl < -1) atomicOr(a.err, ERR_CACHE_SLOT);
     }
     const uint64_t mnc = (PACK && (off >> 15)) ? 0ull : m;
-    uint64_t anc = __ballot(mnc != 0ull);
+    const uint64_t anc = __ballot(mnc != 0ull);
+    int32_t p0 = 0, incl = 0;  // packing: the word's first pair, from run_p
     if (PACK) {
       const uint64_t any = __ballot(m != 0ull);
       if (m != 0ull && a.uniq_out) a.uniq_out[run_u + __popcll(any & lt)] = u;
       run_u += __popcll(any);
       const int32_t pc = __popcll(mnc);
-      const int64_t pair0 = run_p + (wave_incl_sum_i32(pc) - pc);
+      incl = wave_incl_sum_i32(pc);
+      p0 = incl - pc;
       if (mnc != 0ull) {
         const int64_t rk = run_nc + __popcll(anc & lt);
         a.unc_ids[rk] = u;
-        a.unc_off[rk] = pair0;
-        a.nodeoff[u] = pair0;
+        a.unc_off[rk] = run_p + p0;
+        a.nodeoff[u] = run_p + p0;
       }
       run_nc += __popcll(anc);
     }
-    while (anc) {
-      const int l = __ffsll((long long)anc) - 1;
-      anc &= ~(1ull << l);
-      const uint64_t wd = (uint64_t)read_lane((int64_t)mnc, l);
-      const int32_t ul = __builtin_amdgcn_readlane(u, l);
-      const int32_t sll = PACK ? -1 : __builtin_amdgcn_readlane(sl, l);
-      if ((wd >> lane) & 1ull) {
-        if (PACK || dest_b < end_b) a.seg_out[dest_b] = ul;
-        if (!PACK && a.loc_out && dest_b < end_b)
-          a.loc_out[dest_b] = sll >= 0 ? -(sll + 1) : (int32_t)DG_LOC_PENDING;
-        if (PACK) a.pairdest[run_p + __popcll(wd & lt)] = dest_b;
-        if (LOCAL) a.local_out[(int64_t)ul * B + lane] = local_b;
-        ++dest_b;
-        ++local_b;
-      }
-      if (PACK) run_p += __popcll(wd);
+    if (!anc) continue;  // uniform
+    uint64_t todo = wave_transpose64(mnc);  // lane b: the chunk's words with bit b
+    s_word[w][lane] = int4{u, sl, p0, 0};
+    if (PACK) s_nc[w][lane] = mnc;
+    // LDS operations of one wave complete in order: the reads below see these
+    // stores, and the next chunk's stores follow this chunk's reads.
+    __builtin_amdgcn_wave_barrier();
+    while (todo) {
+      const int k = __builtin_ctzll(todo);
+      todo &= todo - 1ull;
+      const int4 e = s_word[w][k];
+      if (PACK || dest_b < end_b) a.seg_out[dest_b] = e.x;
+      if (!PACK && a.loc_out && dest_b < end_b)
+        a.loc_out[dest_b] = e.y >= 0 ? -(e.y + 1) : (int32_t)DG_LOC_PENDING;
+      if (PACK) a.pairdest[run_p + e.z + __popcll(s_nc[w][k] & lt)] = dest_b;
+      if (LOCAL) a.local_out[(int64_t)e.x * B + lane] = local_b;
+      ++dest_b;
+      ++local_b;
     }
+    __builtin_amdgcn_wave_barrier();
+    if (PACK) run_p += __builtin_amdgcn_readlane(incl, 63);
   }
 }
 
@@ -905,14 +959,21 @@ __global__ void k_fuse_ptr(const int64_t *totals, int B, int64_t *packed_ptr) {
   }
 }
 
-// Fused write pass (FuseScan), over the compact list.  Per-node outputs
-// (U, U_nc, pair offsets) by ballot prefixes within a chunk of 64 words, as in
-// packing's write pass; then the words with new or non-cached bits one by one,
-// lane b taking bit b: a new pair goes to batch b's segment (with its
-// address-table entry when the node is cached, and its local index when
-// local_out is given), a non-cached pair to P_b with its destination and list
-// slot.  Blocks run in XCD-contiguous order, as in the other write pass.
+// Fused write pass (FuseScan), over the compact list, 64 words at a time.
+// Per-node outputs (U, U_nc, pair offsets) by ballot prefixes within the
+// chunk, as in packing's write pass.  Then lane b takes batch b's pairs: the
+// chunk's new bits and non-cached bits are transposed, so that lane b holds
+// the set of the chunk's words with bit b, and walks that set in list order
+// (the words' node IDs, cache slots and pair offsets staged in LDS).  A new
+// pair goes to batch b's segment (with its address-table entry when the node
+// is cached, and its local index when local_out is given), a non-cached pair
+// to P_b with its destination and list slot.  A lane's walk is as long as its
+// batch's share of the chunk, a few words where the chunk's nodes are cold,
+// instead of one step per word for every lane.  Blocks run in XCD-contiguous
+// order, as in the other write pass.
 __global__ __launch_bounds__(MC_THREADS) void k_fuse_write(FuseScan a) {
+  __shared__ int4 s_word[MC_WAVES][64];      // node ID, cache slot, first pair (in the chunk)
+  __shared__ uint64_t s_nc[MC_WAVES][64];    // non-cached bits
   const int lane = lane_id(), w = threadIdx.x >> 6;
   const int B = a.B, rows = mc_rows(B);
   const uint32_t blk = xcd_block(blockIdx.x, gridDim.x);
@@ -950,10 +1011,6 @@ __global__ __launch_bounds__(MC_THREADS) void k_fuse_write(FuseScan a) {
       off = co[i];
       sl = csl[i];
     }
-    // Every load of the chunk has landed here: without this wait the compiler
-    // waits for them inside the pair loop below, and so (one counter covers
-    // loads and stores) for each iteration's stores before the next.
-    wait_vm_all();
     const int32_t u = (int32_t)(t0 + (off & 1023u));
     const bool cached = (off >> 15) & 1u;
     const uint64_t mnc = cached ? 0ull : m;
@@ -965,44 +1022,51 @@ __global__ __launch_bounds__(MC_THREADS) void k_fuse_write(FuseScan a) {
     run_u += __popcll(any);
     const uint64_t anc = __ballot(mnc != 0ull);
     const int32_t pc = __popcll(mnc);
-    const int64_t pair0 = run_p + (wave_incl_sum_i32(pc) - pc);
+    const int32_t incl = wave_incl_sum_i32(pc);
+    const int32_t p0 = incl - pc;  // the word's first pair, from run_p
     if (mnc != 0ull) {
       const int64_t rk = run_nc + __popcll(anc & lt);
       if (rk < a.unc_cap) {
         a.unc_ids[rk] = u;
-        a.unc_off[rk] = pair0;
+        a.unc_off[rk] = run_p + p0;
       }
-      if (a.nodeoff) a.nodeoff[u] = pair0;
+      if (a.nodeoff) a.nodeoff[u] = run_p + p0;
     }
     run_nc += __popcll(anc);
-    uint64_t act = __ballot((nw | mnc) != 0ull);
-    while (act) {
-      const int l = __ffsll((long long)act) - 1;
-      act &= act - 1ull;
-      const uint64_t wn = (uint64_t)read_lane((int64_t)nw, l);
-      const uint64_t wp = (uint64_t)read_lane((int64_t)mnc, l);
-      const int32_t ul = __builtin_amdgcn_readlane(u, l);
-      const int32_t sll = __builtin_amdgcn_readlane(sl, l);
-      const bool is_new = (wn >> lane) & 1ull;
+    const bool has_new = __ballot(nw != 0ull) != 0ull;  // uniform
+    const uint64_t tn = has_new ? wave_transpose64(nw) : 0ull;  // lane b: words with new bit b
+    const uint64_t tp = anc ? wave_transpose64(mnc) : 0ull;      // lane b: words with non-cached bit b
+    s_word[w][lane] = int4{u, sl, p0, 0};
+    s_nc[w][lane] = mnc;
+    // LDS operations of one wave complete in order: the reads below see these
+    // stores, and the next chunk's stores follow this chunk's reads.
+    __builtin_amdgcn_wave_barrier();
+    uint64_t todo = tn | tp;
+    while (todo) {
+      const int k = __builtin_ctzll(todo);
+      todo &= todo - 1ull;
+      const int4 e = s_word[w][k];
       const int64_t slot = dest_b;
+      const bool is_new = (tn >> k) & 1ull;
       if (is_new) {
         if (dest_b < end_b) {
-          a.seg_out[dest_b] = ul;
-          if (sll >= 0) a.loc_out[dest_b] = -(sll + 1);
-          if (a.local_out) a.local_out[(int64_t)ul * B + lane] = (int32_t)(dest_b - lbase);
+          a.seg_out[dest_b] = e.x;
+          if (e.y >= 0) a.loc_out[dest_b] = -(e.y + 1);
+          if (a.local_out) a.local_out[(int64_t)e.x * B + lane] = (int32_t)(dest_b - lbase);
         }
         ++dest_b;
       }
-      if ((wp >> lane) & 1ull) {
+      if ((tp >> k) & 1ull) {
         if (pd_b < a.packed_cap)
           a.pinfo[pd_b] = ((uint64_t)(uint32_t)(is_new ? (int32_t)(slot - lbase) : -1) << 32) |
-                          (uint32_t)ul;
-        const int64_t q = run_p + __popcll(wp & lt);
+                          (uint32_t)e.x;
+        const int64_t q = run_p + e.z + __popcll(s_nc[w][k] & lt);
         if (q < a.pair_cap) a.pairdest[q] = pd_b;
         ++pd_b;
       }
-      run_p += __popcll(wp);
     }
+    __builtin_amdgcn_wave_barrier();
+    run_p += __builtin_amdgcn_readlane(incl, 63);
   }
 }
 
