@@ -583,13 +583,27 @@ int mask_scan_rows(MaskScan &m, hipStream_t s) {
 // 64 x 64 bit transpose across the wave: lane i holds row i (bit j is entry
 // (i, j)); on return lane j holds column j (bit i is entry (i, j)).  Each of
 // the six block-swap stages exchanges bit s of the row index with bit s of the
-// column index between lanes i and i ^ s: the stage across the wave halves by a
-// lane shuffle, the five within each half by ds_swizzle (xor mode) on the
-// 32-bit halves of the rows, which those stages never mix.
+// column index between lanes i and i ^ s.  The stage across the wave halves
+// moves 32-bit halves by a lane shuffle; the five within each half work on
+// the 32-bit halves of the rows, which those stages never mix, and take the
+// partner's value by DPP (s = 1, 2 within quads, 4 and 8 within rows of 16
+// lanes) or by ds_swizzle (s = 16).
 template <int S>
-__device__ __forceinline__ uint32_t swizzle_xor(uint32_t v) {
-  static_assert(S >= 1 && S <= 16, "xor within 32 lanes");
-  return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, (S << 10) | 0x1f);
+__device__ __forceinline__ uint32_t xor_partner(uint32_t v, int lane) {
+  if constexpr (S == 1) {  // quad_perm [1, 0, 3, 2]
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xb1, 0xf, 0xf, false);
+  } else if constexpr (S == 2) {  // quad_perm [2, 3, 0, 1]
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4e, 0xf, 0xf, false);
+  } else if constexpr (S == 4 || S == 8) {
+    // row_shl:S (lane i reads lane i + S) for the lanes with bit S clear,
+    // row_shr:S (lane i reads lane i - S) for the others; both stay in the row
+    const uint32_t up = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x100 | S, 0xf, 0xf, false);
+    const uint32_t dn = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x110 | S, 0xf, 0xf, false);
+    return (lane & S) ? dn : up;
+  } else {
+    static_assert(S == 16, "xor within 32 lanes");
+    return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, (S << 10) | 0x1f);
+  }
 }
 template <int S>
 __device__ __forceinline__ void transpose_stage(uint32_t &lo, uint32_t &hi, int lane) {
@@ -597,7 +611,7 @@ __device__ __forceinline__ void transpose_stage(uint32_t &lo, uint32_t &hi, int 
   constexpr uint32_t M0 = S == 16 ? 0x0000ffffu : S == 8 ? 0x00ff00ffu : S == 4 ? 0x0f0f0f0fu
                         : S == 2 ? 0x33333333u : 0x55555555u;
   const bool low = (lane & S) == 0;
-  const uint32_t plo = swizzle_xor<S>(lo), phi = swizzle_xor<S>(hi);
+  const uint32_t plo = xor_partner<S>(lo, lane), phi = xor_partner<S>(hi, lane);
   // low lane: keeps its M0 positions, takes the partner's M0 positions moved up
   // by S; high lane: keeps its other positions, takes the partner's moved down
   const uint32_t keep = low ? M0 : ~M0;
@@ -641,21 +655,27 @@ __device__ __forceinline__ uint64_t wave_transpose64(uint64_t r) {
 // of its own word before the pairs are emitted.
 template <bool PACK, bool LOCAL>
 __global__ __launch_bounds__(MC_THREADS) void k_mask_write(MaskScan a) {
-  __shared__ int4 s_word[MC_WAVES][64];  // node ID, cache slot, first pair (in the chunk)
-  __shared__ uint64_t s_nc[MC_WAVES][64];  // packing: the word's listed bits
-  const int lane = lane_id(), w = threadIdx.x >> 6;
+  // per word of the chunk: first pair (packing, from run_p) << 10 | node
+  // offset in the tile, cache slot, listed bits (packing)
+  __shared__ int4 s_word[MC_WAVES][64];
+  const int lane = lane_id();
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
   const int B = a.B, rows = mc_rows(B);
   // Neighbouring blocks append to the same stretch of every batch's list: run
   // them on one XCD, so that lines shared between them merge in its L2.
   const uint32_t blk = xcd_block(blockIdx.x, gridDim.x);
   const int64_t t0 = (int64_t)blk * MC_BLOCK_NODES + (int64_t)w * MC_TILE;
   const size_t gwi = (size_t)blk * MC_WAVES + w;
-  const uint32_t n = a.wcnt[gwi];
-  if (n == 0) return;  // wave-uniform
   const uint64_t *cm = a.cw_mask + gwi * MC_TILE;
   const uint16_t *co = a.cw_off + gwi * MC_TILE;
   const int64_t *bb = a.base + (size_t)blk * rows;
   const uint32_t *pre = a.wpre + gwi * rows;
+  // The count, the bases and the first chunk are requested together: the
+  // chunk's 64 entries lie inside the wave's part of the compact list
+  // whatever the count.
+  const uint32_t n = a.wcnt[gwi];
+  uint64_t m = cm[lane];
+  uint32_t off = co[lane];
   const int64_t run0 = lane < B ? bb[lane] + pre[lane] : 0;
   int64_t dest_b = lane < B ? a.seg_base[lane] + run0 : 0;  // next list slot of batch b
   const int64_t end_b = (!PACK && lane < B) ? a.seg_end[lane] : 0;
@@ -667,14 +687,21 @@ __global__ __launch_bounds__(MC_THREADS) void k_mask_write(MaskScan a) {
     run_nc = bb[row_packed(B)] + pre[row_packed(B)];
     run_p = bb[row_pairs(B)] + pre[row_pairs(B)];
   }
+  wait_vm_all();
+  if (n == 0) return;  // wave-uniform
   const uint64_t lt = lanes_below();
   for (uint32_t c0 = 0; c0 < n; c0 += 64) {
     const uint32_t i = c0 + lane;
-    uint64_t m = 0;
-    uint32_t off = 0;
-    if (i < n) {
-      m = cm[i];
-      off = co[i];
+    if (c0 > 0) {
+      if (i < n) {
+        m = cm[i];
+        off = co[i];
+      }
+      wait_vm_all();  // as in the fused write pass
+    }
+    if (i >= n) {
+      m = 0;
+      off = 0;
     }
     const int32_t u = (int32_t)(t0 + (off & 1023u));
     int32_t sl = -1;  // sampling with loc_out: this lane's node's cache slot
@@ -702,22 +729,29 @@ __global__ __launch_bounds__(MC_THREADS) void k_mask_write(MaskScan a) {
     }
     if (!anc) continue;  // uniform
     uint64_t todo = wave_transpose64(mnc);  // lane b: the chunk's words with bit b
-    s_word[w][lane] = int4{u, sl, p0, 0};
-    if (PACK) s_nc[w][lane] = mnc;
+    s_word[w][lane] = int4{(p0 << 10) | (int32_t)(off & 1023u), sl, (int32_t)(uint32_t)mnc,
+                           (int32_t)(uint32_t)(mnc >> 32)};
     // LDS operations of one wave complete in order: the reads below see these
     // stores, and the next chunk's stores follow this chunk's reads.
     __builtin_amdgcn_wave_barrier();
+    int k = todo ? __builtin_ctzll(todo) : 0;
+    int4 e = s_word[w][k];
     while (todo) {
-      const int k = __builtin_ctzll(todo);
       todo &= todo - 1ull;
-      const int4 e = s_word[w][k];
-      if (PACK || dest_b < end_b) a.seg_out[dest_b] = e.x;
+      const int kn = todo ? __builtin_ctzll(todo) : k;
+      const int4 en = s_word[w][kn];  // the next word's entry, requested ahead
+      const int32_t uk = (int32_t)(t0 + (e.x & 1023));
+      if (PACK || dest_b < end_b) a.seg_out[dest_b] = uk;
       if (!PACK && a.loc_out && dest_b < end_b)
         a.loc_out[dest_b] = e.y >= 0 ? -(e.y + 1) : (int32_t)DG_LOC_PENDING;
-      if (PACK) a.pairdest[run_p + e.z + __popcll(s_nc[w][k] & lt)] = dest_b;
-      if (LOCAL) a.local_out[(int64_t)e.x * B + lane] = local_b;
+      if (PACK) {
+        const uint64_t mk = ((uint64_t)(uint32_t)e.w << 32) | (uint32_t)e.z;
+        a.pairdest[run_p + (e.x >> 10) + __popcll(mk & lt)] = dest_b;
+      }
+      if (LOCAL) a.local_out[(int64_t)uk * B + lane] = local_b;
       ++dest_b;
       ++local_b;
+      e = en;
     }
     __builtin_amdgcn_wave_barrier();
     if (PACK) run_p += __builtin_amdgcn_readlane(incl, 63);
@@ -971,16 +1005,17 @@ __global__ void k_fuse_ptr(const int64_t *totals, int B, int64_t *packed_ptr) {
 // batch's share of the chunk, a few words where the chunk's nodes are cold,
 // instead of one step per word for every lane.  Blocks run in XCD-contiguous
 // order, as in the other write pass.
-__global__ __launch_bounds__(MC_THREADS) void k_fuse_write(FuseScan a) {
-  __shared__ int4 s_word[MC_WAVES][64];      // node ID, cache slot, first pair (in the chunk)
-  __shared__ uint64_t s_nc[MC_WAVES][64];    // non-cached bits
-  const int lane = lane_id(), w = threadIdx.x >> 6;
+__global__ __launch_bounds__(MC_THREADS) __attribute__((amdgpu_waves_per_eu(8, 8)))
+void k_fuse_write(FuseScan a) {
+  // per word of the chunk: first pair (from run_p) << 10 | node offset in the
+  // tile, cache slot, non-cached bits
+  __shared__ int4 s_word[MC_WAVES][64];
+  const int lane = lane_id();
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
   const int B = a.B, rows = mc_rows(B);
   const uint32_t blk = xcd_block(blockIdx.x, gridDim.x);
   const int64_t t0 = (int64_t)blk * MC_BLOCK_NODES + (int64_t)w * MC_TILE;
   const size_t gwi = (size_t)blk * MC_WAVES + w;
-  const uint32_t n = a.wcnt[gwi];
-  if (n == 0) return;  // wave-uniform
   const uint64_t *cm = a.cw_mask + gwi * MC_TILE;
   const uint64_t *cn = a.cw_new + gwi * MC_TILE;
   const uint16_t *co = a.cw_off + gwi * MC_TILE;
@@ -989,27 +1024,47 @@ __global__ __launch_bounds__(MC_THREADS) void k_fuse_write(FuseScan a) {
   const int64_t *bp = a.base_p + (size_t)blk * rows;
   const uint32_t *ps = a.wpre_s + gwi * rows;
   const uint32_t *pp = a.wpre_p + gwi * rows;
-  int64_t dest_b = 0, end_b = 0, pd_b = 0, lbase = 0;  // batch `lane`
+  // The count, the bases and the first chunk are requested together: the
+  // chunk's 64 entries lie inside the wave's part of the compact list
+  // whatever the count.
+  const uint32_t n = a.wcnt[gwi];
+  uint64_t m = cm[lane], nw = cn[lane];
+  uint32_t off = co[lane];
+  int32_t sl = csl[lane];  // the node's cache slot (for a cached node's new pairs)
+  // batch `lane`: the next slot of its segment (dest_b; li within the batch's
+  // node_cap entries) and the next row of its chunk of P
+  int64_t dest_b = 0, pd_b = 0;
+  int32_t li = 0;
   if (lane < B) {
-    dest_b = a.seg_base[lane] + bs[lane] + ps[lane];  // next slot of its segment
-    end_b = a.seg_end[lane];
-    pd_b = a.packed_ptr[lane] + bp[lane] + pp[lane];  // next row of its chunk
-    lbase = (int64_t)lane * a.node_cap;
+    dest_b = a.seg_base[lane] + bs[lane] + ps[lane];
+    li = (int32_t)(dest_b - (int64_t)lane * a.node_cap);
+    pd_b = a.packed_ptr[lane] + bp[lane] + pp[lane];
   }
   int64_t run_u = bp[row_all(B)] + pp[row_all(B)];
   int64_t run_nc = bp[row_packed(B)] + pp[row_packed(B)];
   int64_t run_p = bp[row_pairs(B)] + pp[row_pairs(B)];
+  wait_vm_all();
+  if (n == 0) return;  // wave-uniform
   const uint64_t lt = lanes_below();
   for (uint32_t c0 = 0; c0 < n; c0 += 64) {
     const uint32_t i = c0 + lane;
-    uint64_t m = 0, nw = 0;
-    uint32_t off = 0;
-    int32_t sl = -1;  // the node's cache slot (for a cached node's new pairs)
-    if (i < n) {
-      m = cm[i];
-      nw = cn[i];
-      off = co[i];
-      sl = csl[i];
+    if (c0 > 0) {
+      if (i < n) {
+        m = cm[i];
+        nw = cn[i];
+        off = co[i];
+        sl = csl[i];
+      }
+      // The chunk's loads have landed before its first store: the loads and
+      // stores share one counter, so a wait placed after the stores below
+      // (the compiler's choice for values loaded in the loop) would also wait
+      // for every store.
+      wait_vm_all();
+    }
+    if (i >= n) {
+      m = nw = 0;
+      off = 0;
+      sl = -1;
     }
     const int32_t u = (int32_t)(t0 + (off & 1023u));
     const bool cached = (off >> 15) & 1u;
@@ -1036,34 +1091,40 @@ __global__ __launch_bounds__(MC_THREADS) void k_fuse_write(FuseScan a) {
     const bool has_new = __ballot(nw != 0ull) != 0ull;  // uniform
     const uint64_t tn = has_new ? wave_transpose64(nw) : 0ull;  // lane b: words with new bit b
     const uint64_t tp = anc ? wave_transpose64(mnc) : 0ull;      // lane b: words with non-cached bit b
-    s_word[w][lane] = int4{u, sl, p0, 0};
-    s_nc[w][lane] = mnc;
+    s_word[w][lane] = int4{(p0 << 10) | (int32_t)(off & 1023u), sl, (int32_t)(uint32_t)mnc,
+                           (int32_t)(uint32_t)(mnc >> 32)};
     // LDS operations of one wave complete in order: the reads below see these
     // stores, and the next chunk's stores follow this chunk's reads.
     __builtin_amdgcn_wave_barrier();
     uint64_t todo = tn | tp;
+    int k = todo ? __builtin_ctzll(todo) : 0;
+    int4 e = s_word[w][k];
     while (todo) {
-      const int k = __builtin_ctzll(todo);
       todo &= todo - 1ull;
-      const int4 e = s_word[w][k];
-      const int64_t slot = dest_b;
+      const int kn = todo ? __builtin_ctzll(todo) : k;
+      const int4 en = s_word[w][kn];  // the next word's entry, requested ahead
+      const int32_t uk = (int32_t)(t0 + (e.x & 1023));
+      const int32_t slot = li;
       const bool is_new = (tn >> k) & 1ull;
       if (is_new) {
-        if (dest_b < end_b) {
-          a.seg_out[dest_b] = e.x;
+        if (li < a.node_cap) {
+          a.seg_out[dest_b] = uk;
           if (e.y >= 0) a.loc_out[dest_b] = -(e.y + 1);
-          if (a.local_out) a.local_out[(int64_t)e.x * B + lane] = (int32_t)(dest_b - lbase);
+          if (a.local_out) a.local_out[(int64_t)uk * B + lane] = li;
         }
         ++dest_b;
+        ++li;
       }
       if ((tp >> k) & 1ull) {
         if (pd_b < a.packed_cap)
-          a.pinfo[pd_b] = ((uint64_t)(uint32_t)(is_new ? (int32_t)(slot - lbase) : -1) << 32) |
-                          (uint32_t)e.x;
-        const int64_t q = run_p + e.z + __popcll(s_nc[w][k] & lt);
+          a.pinfo[pd_b] = ((uint64_t)(uint32_t)(is_new ? slot : -1) << 32) | (uint32_t)uk;
+        const uint64_t mk = ((uint64_t)(uint32_t)e.w << 32) | (uint32_t)e.z;
+        const int64_t q = run_p + (e.x >> 10) + __popcll(mk & lt);
         if (q < a.pair_cap) a.pairdest[q] = pd_b;
         ++pd_b;
       }
+      k = kn;
+      e = en;
     }
     __builtin_amdgcn_wave_barrier();
     run_p += __builtin_amdgcn_readlane(incl, 63);
