@@ -256,6 +256,10 @@ CASES = [
     (300, 20, 5, 6, [4, 0], 16, torch.float32, 0.2),           # f = 0 at the last hop
     (300, 20, 5, 6, [6], 16, torch.float32, 0.2),              # one hop (the last is the first)
     (300, 20, 5, 6, [], 16, torch.float32, 0.2),               # no hop: the seeds alone
+    (300, 299, 64, 5, [-1, 2], 8, torch.float32, 0.3),         # every batch holds nearly every
+                                                               # node: full 64-bit membership
+                                                               # words, several 64-word chunks
+                                                               # per wave in the write passes
 ]
 
 
