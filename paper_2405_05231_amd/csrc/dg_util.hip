@@ -810,8 +810,10 @@ __device__ __forceinline__ void lds_count(uint32_t k, uint32_t *lo, uint32_t *hi
 // non-cached words in another, and lane b counts bit b of each.
 constexpr int FC_PART = MC_ROUNDS / 4;
 
-__global__ __launch_bounds__(MC_THREADS) __attribute__((amdgpu_waves_per_eu(8, 8)))
-void k_fuse_count(FuseScan a) {
+// It runs eight waves per SIMD without a hint (54 VGPRs); a hint of eight
+// waves caps its scalar registers at 80 and spills 20 of them into vector
+// lanes (about 150 more vector instructions per wave).
+__global__ __launch_bounds__(MC_THREADS) void k_fuse_count(FuseScan a) {
   __shared__ uint32_t s_cs[MC_WAVES][DG_MAX_BATCHES + 4];
   __shared__ uint32_t s_cp[MC_WAVES][DG_MAX_BATCHES + 4];
   __shared__ __align__(16) uint32_t s_w[MC_WAVES][4][MC_CWORDS];
@@ -1005,8 +1007,7 @@ __global__ void k_fuse_ptr(const int64_t *totals, int B, int64_t *packed_ptr) {
 // batch's share of the chunk, a few words where the chunk's nodes are cold,
 // instead of one step per word for every lane.  Blocks run in XCD-contiguous
 // order, as in the other write pass.
-__global__ __launch_bounds__(MC_THREADS) __attribute__((amdgpu_waves_per_eu(8, 8)))
-void k_fuse_write(FuseScan a) {
+__global__ __launch_bounds__(MC_THREADS) void k_fuse_write(FuseScan a) {
   // per word of the chunk: first pair (from run_p) << 10 | node offset in the
   // tile, cache slot, non-cached bits
   __shared__ int4 s_word[MC_WAVES][64];
