@@ -28,6 +28,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
+# mini-batches per assembly launch in dg_assemble_batches (when their output
+# buffers are distinct)
+ASM_GROUP = 8
 
 
 def log(*a):
@@ -239,9 +242,9 @@ def main():
     ws_p2 = [torch.empty(dg._L.dg_sample_pack_workspace_bytes(cfg.n, B, node_cap) if fused else
                          dg._L.dg_pack_workspace_bytes(cfg.n, B, max_total), dtype=torch.uint8,
                          device=dev) for _ in range(n_sets)]
-    # four assembly output buffers used in turn: the library assembles up to four
+    # assembly output buffers used in turn: the library assembles up to ASM_GROUP
     # consecutive mini-batches with buffers of their own in one launch
-    ybuf = [torch.empty((nmax, R), dtype=torch.uint8, device=dev) for _ in range(4)]
+    ybuf = [torch.empty((nmax, R), dtype=torch.uint8, device=dev) for _ in range(ASM_GROUP)]
     log(f"{n_groups} groups: pairs {min(p['total_nodes'] for p in pre):,}.."
         f"{max_total:,} edges {min(p['total_edges'] for p in pre):,}.."
         f"{max(p['total_edges'] for p in pre):,} packed rows up to {max_rows:,}")
@@ -466,12 +469,12 @@ def main():
     # HIP events on the call's stream (serial region)
     g_ms = float(np.mean(gather_ms))
     achieved = F_pack_s / (sum(gather_ms) * 1e-3) / 1e9
-    # assembly: dg_assemble_batches runs four consecutive mini-batches (with
-    # output buffers of their own, ybuf[0..3]) per k_assemble16_group launch;
+    # assembly: dg_assemble_batches runs ASM_GROUP consecutive mini-batches (with
+    # output buffers of their own, one per ybuf entry) per k_assemble16_group launch;
     # its average launch time is the steps' assembly time (HIP events on its
     # stream, serial region) over the launches, and its bytes the steps'
     # assembly bytes over them
-    asm_launches = (B + 3) // 4
+    asm_launches = (B + ASM_GROUP - 1) // ASM_GROUP
     a_ms = float(np.sum(asm_ms)) / (args.steps * asm_launches)
     F_asm_launch = F_asm_s / (args.steps * asm_launches)
     achieved_asm = F_asm_launch / (a_ms * 1e-3) / 1e9
@@ -513,8 +516,8 @@ def main():
                       "assembly of step k (second stream) overlaps sampling and packing of "
                       "step k+1; the serial figures below wait for each step's assembly"),
         "packing_sets": n_sets,
-        "assembly_issue": ("direct calls: one dg_assemble_batches call (B/4 launches of four "
-                           "mini-batches) per step, "
+        "assembly_issue": (f"direct calls: one dg_assemble_batches call (B/{ASM_GROUP} launches "
+                           f"of {ASM_GROUP} mini-batches) per step, "
                            + ("issued by the main thread" if asm_thread is None else
                               "issued by a host thread of its own in the pipelined region "
                               "(the trainer side), by the main thread in the serial region")),
@@ -602,7 +605,8 @@ def main():
                   ("total_nodes", "total_edges", "packed_rows", "unique_nodes",
                    "unique_packed")},
         # the dominant kernel by time: batch assembly (B/4 launches per step)
-        "roofline": {"kernel": "k_assemble16_group (batch assembly, four mini-batches per launch)",
+        "roofline": {"kernel": f"k_assemble16_group (batch assembly, {ASM_GROUP} mini-batches "
+                               "per launch)",
                      "bound": "hbm", "achieved": round(achieved_asm, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved_asm / HBM_PEAK_GBPS, 4),
                      "traffic": load_traffic(cfg.name, "assemble"),

@@ -480,7 +480,7 @@ int dg_assemble_batch(const void *cache, int64_t cache_rows, const void *packed_
                       hipStream_t stream);
 
 /* dg_assemble_batch for batches 0..B-1 of one packing result, in batch order on
- * `stream`, issued by one call.  Up to four consecutive batches whose output
+ * `stream`, issued by one call.  Up to eight consecutive batches whose output
  * buffers are distinct and apart (and whose rows move as 16-byte vectors) share
  * one kernel launch; the outputs are those of the per-batch calls in batch
  * order either way.

@@ -96,7 +96,7 @@ __global__ __launch_bounds__(THREADS) void k_assemble16(const v4u *cache, int64_
 // Several batches in one launch (each with an output buffer of its own): the
 // blocks of batch q are block0[q] .. block0[q+1) - 1, each batch run exactly as
 // its own launch would run it.
-constexpr int ASM_GROUP = 4;
+constexpr int ASM_GROUP = 8;
 struct AsmGroup {
   int G;
   int64_t block0[ASM_GROUP + 1];

@@ -369,36 +369,57 @@ def test_assemble_batches_matches_per_batch_calls(dg):
         dg.assemble_batches(cache, pr, counts, [outs[0][:1]])
 
 
-@pytest.mark.parametrize("dim", [16, 128, 384, 512, 1024])
-@pytest.mark.parametrize("outs_kind", ["one", "two", "same_twice", "all"])
-def test_assemble_batches_output_buffers(dg, dim, outs_kind):
+def buffer_test_group(dg, group, dim):
+    """(cache, packing result, counts) of one sampled and packed group: workload
+    T (4 mini-batches), or a group of 20 mini-batches on a small random graph,
+    so that launches of eight consecutive mini-batches and a shorter last one
+    occur."""
+    gen = torch.Generator().manual_seed(dim)
+    if group == "T":
+        w = synth.make_workload("T")
+        X = torch.randn((w.cfg.n, dim), generator=gen).to(DEV)
+        slot = w.cache_slot.to(DEV)
+        sr = dg.sample_group(w.offsets.to(DEV), w.indices.to(DEV), w.seeds.to(DEV),
+                             list(w.cfg.fanouts), w.rng_seed)
+        cache_nodes = w.cache_nodes.to(DEV)
+    else:
+        n, B, S = 2000, 20, 8
+        rnd = random.Random(4242)
+        off, idx = random_case(rnd, n, 20)
+        seeds = torch.tensor([rnd.sample(range(n), S) for _ in range(B)], dtype=torch.int32)
+        X = torch.randn((n, dim), generator=gen).to(DEV)
+        cache_nodes = torch.tensor(rnd.sample(range(n), n // 10), dtype=torch.int64)
+        slot = torch.full((n,), -1, dtype=torch.int32)
+        slot[cache_nodes] = torch.arange(n // 10, dtype=torch.int32)
+        slot, cache_nodes = slot.to(DEV), cache_nodes.to(DEV)
+        sr = dg.sample_group(off.to(DEV), idx.to(DEV), seeds.to(DEV), [5, 5], 99)
+    pr = dg.pack_group(X, slot, sr.nodes, sr.node_count)
+    return X.index_select(0, cache_nodes), pr, sr.node_count
+
+
+@pytest.mark.parametrize("group,dim", [("T", 16), ("T", 128), ("T", 384), ("T", 512),
+                                       ("T", 1024), ("wide", 16), ("wide", 512)])
+@pytest.mark.parametrize("outs_kind", ["one", "two", "same_twice", "eight", "nine", "all"])
+def test_assemble_batches_output_buffers(dg, group, dim, outs_kind):
     """Batches whose output buffers are distinct may share a launch; the
     result must still be that of the per-batch calls made in batch order, on
     every 16-byte row shape (64 B to 4 KiB rows): with one buffer (each batch
-    overwrites the last), two buffers (batch b in buffer b % 2), the same
-    buffer given twice (no sharing possible), and a buffer per batch."""
-    w = synth.make_workload("T")
-    gen = torch.Generator().manual_seed(dim)
-    X = torch.randn((w.cfg.n, dim), generator=gen).to(DEV)
-    slot = w.cache_slot.to(DEV)
-    sr = dg.sample_group(w.offsets.to(DEV), w.indices.to(DEV), w.seeds.to(DEV),
-                         list(w.cfg.fanouts), w.rng_seed)
-    pr = dg.pack_group(X, slot, sr.nodes, sr.node_count)
-    cache = X.index_select(0, w.cache_nodes.to(DEV))
+    overwrites the last), two, eight or nine buffers (batch b in buffer
+    b % count), the same buffer given twice (no sharing possible), and a
+    buffer per batch; with 4 mini-batches and with 20 (launches of eight and
+    a shorter last one)."""
+    cache, pr, counts = buffer_test_group(dg, group, dim)
     R = pr.row_bytes
-    counts = sr.node_count
     B, nmax = len(counts), int(counts.max())
     refs = [dg.assemble_batch(cache, pr.chunk(b), pr.loc[b, :int(counts[b])], R).clone()
             for b in range(B)]
     one = torch.full((nmax, R), 0xAB, dtype=torch.uint8, device=DEV)
-    if outs_kind == "one":
-        outs = [one]
-    elif outs_kind == "two":
-        outs = [one, torch.full((nmax, R), 0xAB, dtype=torch.uint8, device=DEV)]
-    elif outs_kind == "same_twice":
+    if outs_kind == "same_twice":
         outs = [one, one]
     else:
-        outs = [torch.full((nmax, R), 0xAB, dtype=torch.uint8, device=DEV) for _ in range(B)]
+        count = {"one": 1, "two": 2, "eight": 8, "nine": 9, "all": B}[outs_kind]
+        outs = [one] + [torch.full((nmax, R), 0xAB, dtype=torch.uint8, device=DEV)
+                        for _ in range(count - 1)]
     status = torch.zeros(1, dtype=torch.int32, device=DEV)
     dg.assemble_batches(cache, pr, counts, outs, status=status)
     torch.cuda.synchronize()

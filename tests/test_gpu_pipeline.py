@@ -106,7 +106,7 @@ def test_pipelined_steps_are_each_correct(dg, fused):
         pack_done.record(stream)
         s_asm.wait_event(pack_done)
         # one output buffer per batch and step, so that every step's rows stay
-        # for the check (the bench uses four buffers in turn instead)
+        # for the check (the bench uses eight buffers in turn instead)
         dg.assemble_batches(w.cache, pr, counts, kept[k], status=status, stream=s_asm)
         asm_done[slot].record(s_asm)
         results.append((nodes, counts))
